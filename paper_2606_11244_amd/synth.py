@@ -1,0 +1,234 @@
+"""Seeded synthetic inputs for the W4+EC linear layer.
+
+This module produces the stored tensors that the layer consumes: packed 4-bit
+weight codes with their scales and zero points, activations, the EC factors
+A and B, and the gate parameters. It is shared by the tests, the benchmark and
+the CPU oracle's callers, and it holds none of the layer's own arithmetic: no
+dequantisation, no contraction, no EC projection and no gate. What it does
+compute is the offline side that precedes the layer:
+
+* round-to-nearest (RTN) asymmetric 4-bit quantisation of a float weight
+  matrix, per output channel or per group of input channels (the "vanilla
+  linear quantization" backbone of the paper, section 3.2 and the evaluation
+  setup in section 5.1), and
+* packing of the 4-bit codes, eight to a 32-bit word, in the layout the C ABI
+  documents: word j of row n holds code q[n][8j+i] in bits 4i..4i+3.
+
+Floating-point values are returned as numpy arrays of IEEE bit patterns
+(uint16) in the activation dtype, so that both the GPU path and the oracle see
+exactly the same stored numbers. Conversion to bfloat16 uses torch's CPU cast
+(round to nearest even).
+
+Distribution readings (the workload configurations give N(0, s) without
+saying whether s is a variance): the second argument is the standard
+deviation.
+"""
+from __future__ import annotations
+
+import dataclasses
+import numpy as np
+import torch
+
+F16 = 0
+BF16 = 1
+
+GATE_ONE = 0
+GATE_SIGMOID_LINEAR = 1
+GATE_TANH_MLP = 2
+
+_DTYPES = {F16: torch.float16, BF16: torch.bfloat16}
+
+
+def to_bits(a: np.ndarray, dtype: int) -> np.ndarray:
+    """Round a float array to fp16/bf16 (nearest even) and return uint16 bits."""
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(_DTYPES[dtype]).view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def from_bits(bits: np.ndarray, dtype: int) -> np.ndarray:
+    """uint16 bit patterns of fp16/bf16 values -> float32 array (exact)."""
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.view(_DTYPES[dtype]).to(torch.float32).numpy()
+
+
+def pack_int4(q: np.ndarray) -> np.ndarray:
+    """Pack codes q[N][K] (values 0..15, K % 8 == 0) into uint32 words [N][K/8].
+
+    Word j of row n holds q[n][8j+i] in bits 4i..4i+3 (lowest nibble first).
+    """
+    q = np.asarray(q)
+    n, k = q.shape
+    if k % 8:
+        raise ValueError("K must be a multiple of 8 to pack 4-bit codes")
+    if q.min(initial=0) < 0 or q.max(initial=0) > 15:
+        raise ValueError("codes must lie in 0..15")
+    q = q.astype(np.uint32).reshape(n, k // 8, 8)
+    words = np.zeros((n, k // 8), dtype=np.uint32)
+    for i in range(8):
+        words |= q[:, :, i] << np.uint32(4 * i)
+    return words
+
+
+def rtn_quantize(w: np.ndarray, group_size: int):
+    """Asymmetric min-max round-to-nearest 4-bit quantisation of w[N][K].
+
+    For each output row n and each group of `group_size` consecutive input
+    columns (group_size == K means one group per row, "per channel"):
+      lo, hi = min, max of the group
+      s = fp16((hi - lo) / 15)            (the stored scale)
+      z = clip(rne(-lo / s), 0, 15)       (the stored zero point)
+      q = clip(rne(w / s) + z, 0, 15)     (codes, chosen against the fp16 s)
+    A constant group (hi == lo) or a scale that rounds to zero uses s = 1 and
+    z = clip(rne(-lo), 0, 15).
+    Returns (codes int64 [N][K], scales fp16 bits [N][K/G], zeros uint8 [N][K/G]).
+    """
+    w = np.asarray(w, dtype=np.float32)
+    n, k = w.shape
+    g = k if group_size in (0, k) else group_size
+    if k % g:
+        raise ValueError("K must be a multiple of the group size")
+    wg = w.reshape(n, k // g, g).astype(np.float64)
+    lo = wg.min(axis=2)
+    hi = wg.max(axis=2)
+    s = ((hi - lo) / 15.0).astype(np.float16).astype(np.float64)
+    degenerate = (hi == lo) | (s == 0)
+    s = np.where(degenerate, 1.0, s)
+    z = np.clip(np.rint(-lo / s), 0, 15)
+    q = np.clip(np.rint(wg / s[:, :, None]) + z[:, :, None], 0, 15)
+    return (q.reshape(n, k).astype(np.int64),
+            s.astype(np.float16).view(np.uint16),
+            z.astype(np.uint8))
+
+
+@dataclasses.dataclass
+class Layer:
+    """Stored tensors of one W4+EC linear layer plus its activations.
+
+    Bit-pattern arrays are uint16 in the activation dtype unless noted.
+    """
+    M: int
+    N: int
+    K: int
+    group_size: int          # G (== K for per-channel)
+    act_dtype: int           # F16 or BF16
+    rank: int
+    gate_kind: int
+    qweight: np.ndarray      # uint32 [N][K/8]
+    scales: np.ndarray       # fp16 bits [N][K/G]
+    zeros: np.ndarray        # uint8 [N][K/G]
+    x: np.ndarray            # [M][K]
+    A: np.ndarray            # [r][K]
+    B: np.ndarray            # [N][r]
+    w_g: np.ndarray          # [K]
+    b_g: float
+    alpha: float
+    W1: np.ndarray           # [h][r]
+    b1: np.ndarray           # [h]
+    W2: np.ndarray           # [r][h]
+    b2: np.ndarray           # [r]
+
+    @property
+    def gate_hidden(self) -> int:
+        return int(self.W1.shape[0])
+
+
+def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
+               act_dtype: int = F16, gate_kind: int = GATE_SIGMOID_LINEAR,
+               seed: int = 0, config_id: int = 0, module_id: int = 0,
+               w_std: float = 0.02, x_std: float = 1.0, ec_std: float = 0.01,
+               wg_std: float = 0.05, b_g: float = 0.0, alpha: float = 1.0,
+               outlier_frac: float = 0.0, outlier_scale: float = 20.0,
+               gate_hidden: int = 0) -> Layer:
+    """Draw one layer from the seed tree SeedSequence([seed, config_id, module_id]).
+
+    Draw order: W (fp32) -> RTN -> X (with outlier channels) -> A, B -> w_g ->
+    gate-MLP parameters. The gate-MLP weights are drawn N(0, 1/sqrt(r)) for W1
+    and N(0, 1/sqrt(h)) for W2 with zero biases, so that the gate differs from
+    one across tokens.
+    """
+    g = K if group_size in (0, K) else group_size
+    rng = np.random.default_rng(np.random.SeedSequence([seed, config_id, module_id]))
+    w = rng.normal(0.0, w_std, size=(N, K)).astype(np.float32)
+    q, s, z = rtn_quantize(w, g)
+    del w
+    x = rng.normal(0.0, x_std, size=(M, K)).astype(np.float32)
+    if outlier_frac > 0.0 and M > 0:
+        n_out = int(round(outlier_frac * K))
+        idx = rng.choice(K, size=n_out, replace=False)
+        x[:, idx] *= outlier_scale
+    A = rng.normal(0.0, ec_std, size=(rank, K)).astype(np.float32)
+    B = rng.normal(0.0, ec_std, size=(N, rank)).astype(np.float32)
+    w_g = rng.normal(0.0, wg_std, size=(K,)).astype(np.float32)
+    h = gate_hidden if gate_hidden > 0 else 4 * rank
+    W1 = rng.normal(0.0, 1.0 / np.sqrt(max(rank, 1)), size=(h, rank)).astype(np.float32)
+    W2 = rng.normal(0.0, 1.0 / np.sqrt(max(h, 1)), size=(rank, h)).astype(np.float32)
+    b1 = np.zeros((h,), np.float32)
+    b2 = np.zeros((rank,), np.float32)
+    return Layer(M=M, N=N, K=K, group_size=g, act_dtype=act_dtype, rank=rank,
+                 gate_kind=gate_kind, qweight=pack_int4(q), scales=s, zeros=z,
+                 x=to_bits(x, act_dtype), A=to_bits(A, act_dtype),
+                 B=to_bits(B, act_dtype), w_g=to_bits(w_g, act_dtype),
+                 b_g=float(b_g), alpha=float(alpha),
+                 W1=to_bits(W1, act_dtype), b1=to_bits(b1, act_dtype),
+                 W2=to_bits(W2, act_dtype), b2=to_bits(b2, act_dtype))
+
+
+# ---------------------------------------------------------------------------
+# Workload configurations (synthetic stand-ins for the paper's Llama layers;
+# no trained weights are used).
+# ---------------------------------------------------------------------------
+
+LLAMA_1B = {  # hidden 2048, 32 q / 8 kv heads x 64, MLP 8192
+    "q": (2048, 2048), "k": (2048, 512), "v": (2048, 512), "o": (2048, 2048),
+    "gate": (2048, 8192), "up": (2048, 8192), "down": (8192, 2048),
+}
+LLAMA_8B = {  # hidden 4096, 32 q / 8 kv heads x 128, MLP 14336
+    "q": (4096, 4096), "k": (4096, 1024), "v": (4096, 1024), "o": (4096, 4096),
+    "gate": (4096, 14336), "up": (4096, 14336), "down": (14336, 4096),
+}
+LLAMA_70B = {  # hidden 8192, 64 q / 8 kv heads x 128, MLP 28672
+    "q": (8192, 8192), "k": (8192, 1024), "v": (8192, 1024), "o": (8192, 8192),
+    "gate": (8192, 28672), "up": (8192, 28672), "down": (28672, 8192),
+}
+MODULES = ("q", "k", "v", "o", "gate", "up", "down")
+
+CONFIGS = {
+    # config id: description and per-module (K, N) shapes, token counts, quant.
+    0: dict(name="tiny", shapes={"tiny": (256, 256)}, Ms=(4,), group_size=0,
+            rank=8, act_dtype=F16, outlier_frac=0.0, layers=1),
+    1: dict(name="llama1b-decode", shapes=LLAMA_1B, Ms=(1, 4, 16), group_size=128,
+            rank=16, act_dtype=F16, outlier_frac=0.0, layers=16),
+    2: dict(name="llama1b-prefill", shapes=LLAMA_1B, Ms=(512, 2048, 4096),
+            group_size=128, rank=16, act_dtype=F16, outlier_frac=0.01, layers=16),
+    3: dict(name="llama8b", shapes=LLAMA_8B, Ms=(1, 8, 32, 128, 512, 4096),
+            group_size=0, rank=32, act_dtype=BF16, outlier_frac=0.0, layers=32),
+    4: dict(name="llama70b", shapes=LLAMA_70B,
+            Ms=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192),
+            group_size=128, rank=64, act_dtype=F16, outlier_frac=0.0, layers=80,
+            ec_fraction=0.25),
+}
+
+
+def config_layer(config_id: int, module: str, M: int, seed: int = 0,
+                 gate_kind: int = GATE_SIGMOID_LINEAR, rank: int | None = None) -> Layer:
+    """One module of a workload configuration at token count M."""
+    c = CONFIGS[config_id]
+    K, N = c["shapes"][module]
+    mod_id = list(c["shapes"]).index(module)
+    return make_layer(M=M, N=N, K=K, group_size=c["group_size"],
+                      rank=c["rank"] if rank is None else rank,
+                      act_dtype=c["act_dtype"], gate_kind=gate_kind, seed=seed,
+                      config_id=config_id, module_id=mod_id,
+                      outlier_frac=c["outlier_frac"])
+
+
+def ec_selection_70b(seed: int = 0, layers: int = 80, fraction: float = 0.25) -> np.ndarray:
+    """Seeded choice of the (layer, module) pairs of the 70B-shaped model that
+    carry an EC: `fraction` of the layers x 7 modules, without replacement.
+    Returns a bool array [layers][7]."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 4, 999]))
+    total = layers * len(MODULES)
+    pick = rng.choice(total, size=int(round(fraction * total)), replace=False)
+    sel = np.zeros(total, dtype=bool)
+    sel[pick] = True
+    return sel.reshape(layers, len(MODULES))

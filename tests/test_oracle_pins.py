@@ -1,0 +1,492 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each check_* function takes the oracle module and returns True when the pin
+holds, so that the same checks can be run against deliberately broken copies
+of the oracle (planted mistakes, bottom of this file) to show that each
+plausible mistake is caught by at least one pin.
+
+Pins used:
+  * hand-worked golden fixtures of Eq. 3 (tests/golden/ec_worked_examples.json)
+  * IEEE rounding fixtures (tests/golden/rounding_fixtures.json)
+  * fixed packed words with known nibble contents (the documented layout)
+  * the RTN round trip: exact on the 4-bit grid, within s/2 off the grid
+  * brute force in exact rational arithmetic on tiny shapes
+  * integer-grid inputs, where float64 results must be exact
+  * reductions: r = 0, gate == 0, W_hat == 0, A == 0
+  * the static low-rank case of the tanh gate (Eq. 2 with W_comp = alpha B A)
+  * the factored form (Eq. 4) token by token
+  * gate ranges: sigma(0) = 1/2 exactly, gamma in (0, 2), gamma -> 2
+"""
+from __future__ import annotations
+
+import copy
+import json
+import math
+import os
+import types
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import spear_oracle as O
+from paper_2606_11244_amd import synth as S
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------------------
+# helpers that build stored layers from plain numbers (no oracle code)
+# ---------------------------------------------------------------------------
+
+def _f16_bits(vals):
+    return np.asarray(vals, dtype=np.float64).astype(np.float16).view(np.uint16)
+
+
+def _layer_from_case(c, dtype=S.F16):
+    qw = np.array([[int(h, 16) for h in row] for row in c["qweight_hex"]], dtype=np.uint32)
+    r = c["rank"]
+    K = c["K"]
+
+    def bits(v, shape):
+        a = np.asarray(v, dtype=np.float32).reshape(shape)
+        return S.to_bits(a, dtype)
+
+    h = len(c.get("b1", [])) or 4 * r
+    return S.Layer(
+        M=c["M"], N=c["N"], K=K, group_size=c["group_size"], act_dtype=dtype,
+        rank=r, gate_kind=c["gate_kind"], qweight=qw,
+        scales=_f16_bits(c["scales"]), zeros=np.asarray(c["zeros"], np.uint8),
+        x=bits(c["x"], (c["M"], K)), A=bits(c["A"], (r, K)), B=bits(c["B"], (c["N"], r)),
+        w_g=bits(c["w_g"], (K,)), b_g=c["b_g"], alpha=c["alpha"],
+        W1=bits(c.get("W1", np.zeros((h, r))), (h, r)), b1=bits(c.get("b1", np.zeros(h)), (h,)),
+        W2=bits(c.get("W2", np.zeros((r, h))), (r, h)), b2=bits(c.get("b2", np.zeros(r)), (r,)))
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+# ---------------------------------------------------------------------------
+# pin checks (each returns True when the pin holds for oracle module o)
+# ---------------------------------------------------------------------------
+
+def check_unpack_fixed_words(o) -> bool:
+    """Layout pin: 0x76543210 holds codes 0..7 lowest nibble first, etc."""
+    w = np.array([[0x76543210, 0xFEDCBA98, 0x0000000F, 0xF0000000]], dtype=np.uint32)
+    want = list(range(8)) + list(range(8, 16)) + [15] + [0] * 7 + [0] * 7 + [15]
+    return o.unpack_int4(w).tolist() == [want]
+
+
+def check_unpack_exhaustive(o) -> bool:
+    """Every code value at every nibble position decodes to itself and leaves
+    the other seven positions zero."""
+    for v in range(16):
+        for i in range(8):
+            w = np.array([[v << (4 * i)]], dtype=np.uint32)
+            want = [0] * 8
+            want[i] = v
+            if o.unpack_int4(w).tolist() != [want]:
+                return False
+    return True
+
+
+def check_golden_examples(o) -> bool:
+    for c in _load("ec_worked_examples.json")["cases"]:
+        layer = _layer_from_case(c)
+        W_hat = o.dequant(layer.qweight, layer.scales, layer.zeros, layer.group_size)
+        if not np.array_equal(W_hat, np.asarray(c["expected_W_hat"], np.float64)):
+            return False
+        y = o.w4ec_linear(layer)
+        if not np.allclose(y, np.asarray(c["expected_y"]), rtol=1e-15, atol=1e-15):
+            return False
+    return True
+
+
+def check_rounding_fixtures(o) -> bool:
+    for c in _load("rounding_fixtures.json")["cases"]:
+        v = np.array([c["value"]])
+        if int(o.round_f64_to_bits(v, O.F16)[0]) != int(c["f16"], 16):
+            return False
+        if int(o.round_f64_to_bits(v, O.BF16)[0]) != int(c["bf16"], 16):
+            return False
+    return True
+
+
+def check_rtn_grid_roundtrip(o, seed=0) -> bool:
+    """Weights built on the 4-bit grid, with codes 0 and 15 present in every
+    group and a dyadic fp16 scale, come back exactly through RTN + dequant."""
+    rng = np.random.default_rng(seed)
+    N, K = 24, 256
+    for G in (K, 128, 64):
+        s = 2.0 ** rng.integers(-9, -3, size=(N, K // G))
+        z = rng.integers(0, 16, size=(N, K // G))
+        q = rng.integers(0, 16, size=(N, K))
+        qg = q.reshape(N, K // G, G)
+        qg[:, :, 0] = 0
+        qg[:, :, 1] = 15
+        q = qg.reshape(N, K)
+        grp = np.arange(K) // G
+        w = ((q - z[:, grp]) * s[:, grp]).astype(np.float32)
+        q2, s2, z2 = S.rtn_quantize(w, G)
+        W_hat = o.dequant(S.pack_int4(q2), s2, z2, G)
+        if not np.array_equal(W_hat, w.astype(np.float64)):
+            return False
+    return True
+
+
+def check_rtn_error_bound(o, seed=0) -> bool:
+    """Off the grid, round-to-nearest puts every dequantised weight within half
+    a step of the original: |w - W_hat| <= s/2, plus at most 16 * 2^-11 * s at
+    the top of a group, where the fp16 rounding of s = (hi - lo)/15 can push
+    the largest weight just past code 15 before clipping."""
+    rng = np.random.default_rng(seed)
+    N, K = 32, 512
+    for G in (128, K):
+        w = rng.normal(0, 0.02, size=(N, K)).astype(np.float32)
+        q, s, z = S.rtn_quantize(w, G)
+        W_hat = o.dequant(S.pack_int4(q), s, z, G)
+        s64 = s.view(np.float16).astype(np.float64)[:, np.arange(K) // G]
+        err = np.abs(W_hat - w.astype(np.float64))
+        if not np.all(err <= (0.5 + 16 * 2.0 ** -11) * s64 + 1e-15):
+            return False
+        # and the bound is attained up to a few percent (it is not vacuous)
+        if err.max() < 0.4 * s64.min():
+            return False
+    return True
+
+
+def _brute(layer):
+    """Scalar exact-rational evaluation of Eq. 3 (gate ONE or SIGMOID with the
+    sigmoid taken in float64)."""
+    dt = layer.act_dtype
+    M, N, K, r = layer.M, layer.N, layer.K, layer.rank
+    G = layer.group_size
+    xs = S.from_bits(layer.x, dt)
+    As = S.from_bits(layer.A, dt)
+    Bs = S.from_bits(layer.B, dt)
+    wg = S.from_bits(layer.w_g, dt)
+    sc = layer.scales.view(np.float16)
+    Y = [[None] * N for _ in range(M)]
+    for m in range(M):
+        u = [sum(Fraction(float(xs[m][k])) * Fraction(float(As[j][k])) for k in range(K))
+             for j in range(r)]
+        if layer.gate_kind == S.GATE_ONE:
+            g = Fraction(1)
+        else:
+            t = sum(Fraction(float(xs[m][k])) * Fraction(float(wg[k])) for k in range(K))
+            t = float(t) + layer.b_g
+            g = Fraction(1.0 / (1.0 + math.exp(-t)) if t >= 0 else math.exp(t) / (1 + math.exp(t)))
+        for n in range(N):
+            acc = Fraction(0)
+            for k in range(K):
+                word = int(layer.qweight[n][k // 8])
+                code = (word >> (4 * (k % 8))) & 15
+                zz = int(layer.zeros[n][k // G])
+                ss = Fraction(float(sc[n][k // G]))
+                acc += Fraction(code - zz) * ss * Fraction(float(xs[m][k]))
+            ec = sum(Fraction(float(Bs[n][j])) * u[j] for j in range(r))
+            Y[m][n] = acc + Fraction(layer.alpha) * g * ec
+    return Y
+
+
+def check_brute_force(o, seed=0) -> bool:
+    cases = [dict(M=2, N=5, K=16, group_size=8, rank=3, gate_kind=S.GATE_ONE, alpha=0.75),
+             dict(M=3, N=4, K=24, group_size=24, rank=2, gate_kind=S.GATE_SIGMOID_LINEAR, alpha=1.0),
+             dict(M=1, N=3, K=32, group_size=16, rank=1, gate_kind=S.GATE_SIGMOID_LINEAR, alpha=2.0),
+             dict(M=2, N=3, K=16, group_size=16, rank=0, gate_kind=S.GATE_ONE, alpha=1.0),
+             dict(M=2, N=16, K=16, group_size=8, rank=2, gate_kind=S.GATE_ONE, alpha=1.0)]
+    for i, c in enumerate(cases):
+        for dt in (S.F16, S.BF16):
+            layer = S.make_layer(seed=seed + i, act_dtype=dt, ec_std=0.3, wg_std=0.4,
+                                 b_g=0.1, **c)
+            want = _brute(layer)
+            got = o.w4ec_linear(layer)
+            for m in range(layer.M):
+                for n in range(layer.N):
+                    wv = float(want[m][n])
+                    if abs(got[m][n] - wv) > 1e-12 * max(1.0, abs(wv)):
+                        return False
+    return True
+
+
+def check_integer_grid_exact(o, seed=0) -> bool:
+    """Small-integer activations, factors and power-of-two scales: every
+    partial sum is an exactly representable float64, so the oracle must equal
+    exact rational arithmetic with no tolerance."""
+    rng = np.random.default_rng(seed)
+    M, N, K, r, G = 3, 7, 64, 4, 16
+    q = rng.integers(0, 16, size=(N, K))
+    z = rng.integers(0, 16, size=(N, K // G))
+    s = 2.0 ** rng.integers(-3, 3, size=(N, K // G))
+    x = rng.integers(-4, 5, size=(M, K)).astype(np.float32)
+    A = rng.integers(-3, 4, size=(r, K)).astype(np.float32)
+    B = rng.integers(-3, 4, size=(N, r)).astype(np.float32)
+    layer = S.Layer(M=M, N=N, K=K, group_size=G, act_dtype=S.F16, rank=r,
+                    gate_kind=S.GATE_ONE, qweight=S.pack_int4(q),
+                    scales=_f16_bits(s), zeros=z.astype(np.uint8),
+                    x=S.to_bits(x, S.F16), A=S.to_bits(A, S.F16), B=S.to_bits(B, S.F16),
+                    w_g=S.to_bits(np.zeros(K), S.F16), b_g=0.0, alpha=0.5,
+                    W1=S.to_bits(np.zeros((4 * r, r)), S.F16), b1=S.to_bits(np.zeros(4 * r), S.F16),
+                    W2=S.to_bits(np.zeros((r, 4 * r)), S.F16), b2=S.to_bits(np.zeros(r), S.F16))
+    got = o.w4ec_linear(layer)
+    grp = np.arange(K) // G
+    for m in range(M):
+        for n in range(N):
+            acc = Fraction(0)
+            for k in range(K):
+                acc += Fraction(int(q[n, k]) - int(z[n, grp[k]])) * Fraction(float(s[n, grp[k]])) * int(x[m, k])
+            for j in range(r):
+                uj = sum(int(x[m, k]) * int(A[j, k]) for k in range(K))
+                acc += Fraction(1, 2) * int(B[n, j]) * uj
+            if Fraction(float(got[m, n])) != acc:
+                return False
+    return True
+
+
+def check_reductions(o, seed=0) -> bool:
+    """r = 0, gate == 0 (b_g = -1e4), A == 0 and B == 0 all give X W_hat^T;
+    q == z (W_hat == 0) leaves exactly the EC term."""
+    base = S.make_layer(M=5, N=48, K=256, group_size=128, rank=8, seed=seed,
+                        gate_kind=S.GATE_SIGMOID_LINEAR)
+    W_hat = o.dequant(base.qweight, base.scales, base.zeros, 128)
+    y_plain = S.from_bits(base.x, S.F16).astype(np.float64) @ W_hat.T
+    ok = np.allclose(o.w4_linear_layer(base), y_plain, rtol=0, atol=1e-12)
+    off = copy.copy(base)
+    off.b_g = -1.0e4
+    ok &= np.array_equal(o.w4ec_linear(off), o.w4_linear_layer(base))
+    r0 = copy.copy(base)
+    r0.rank = 0
+    r0.A = base.A[:0]
+    r0.B = base.B[:, :0]
+    ok &= np.array_equal(o.w4ec_linear(r0), o.w4_linear_layer(base))
+    a0 = copy.copy(base)
+    a0.A = np.zeros_like(base.A)
+    ok &= np.array_equal(o.w4ec_linear(a0), o.w4_linear_layer(base))
+    # W_hat == 0: codes equal to the zero point everywhere
+    wz = copy.copy(base)
+    z = np.full_like(base.zeros, 7)
+    wz.zeros = z
+    wz.qweight = S.pack_int4(np.full((base.N, base.K), 7))
+    x = S.from_bits(base.x, S.F16).astype(np.float64)
+    A = S.from_bits(base.A, S.F16).astype(np.float64)
+    B = S.from_bits(base.B, S.F16).astype(np.float64)
+    wgv = S.from_bits(base.w_g, S.F16).astype(np.float64)
+    t = x @ wgv + base.b_g
+    g = np.where(t >= 0, 1 / (1 + np.exp(-np.abs(t))), np.exp(-np.abs(t)) / (1 + np.exp(-np.abs(t))))
+    ec = (g[:, None] * (x @ A.T)) @ B.T * base.alpha
+    ok &= np.allclose(o.w4ec_linear(wz), ec, rtol=1e-13, atol=1e-15)
+    return bool(ok)
+
+
+def check_sigmoid_half(o) -> bool:
+    """w_g = 0, b_g = 0 gives g = 1/2 exactly: Y = X W^T + (alpha/2) (X A^T) B^T."""
+    base = S.make_layer(M=3, N=32, K=128, group_size=128, rank=4, seed=3)
+    h = copy.copy(base)
+    h.w_g = np.zeros_like(base.w_g)
+    h.b_g = 0.0
+    g = o.gate_sigmoid_linear(S.from_bits(h.x, S.F16), S.from_bits(h.w_g, S.F16), 0.0)
+    if not np.all(g == 0.5):
+        return False
+    x = S.from_bits(base.x, S.F16).astype(np.float64)
+    A = S.from_bits(base.A, S.F16).astype(np.float64)
+    B = S.from_bits(base.B, S.F16).astype(np.float64)
+    want = o.w4_linear_layer(base) + 0.5 * base.alpha * (x @ A.T) @ B.T
+    return bool(np.allclose(o.w4ec_linear(h), want, rtol=1e-13, atol=1e-15))
+
+
+def check_tanh_static_lora(o, seed=0) -> bool:
+    """W2 = 0, b2 = 0 makes gamma == 1, and Eq. 3 becomes the static
+    compensator of Eq. 2, y = (W_hat + W_comp) x with W_comp = alpha B A, which
+    is checked as one dense product with the explicit matrix."""
+    base = S.make_layer(M=4, N=40, K=128, group_size=64, rank=6, seed=seed,
+                        gate_kind=S.GATE_TANH_MLP, alpha=0.75)
+    st = copy.copy(base)
+    st.W2 = np.zeros_like(base.W2)
+    st.b2 = np.zeros_like(base.b2)
+    W_hat = o.dequant(base.qweight, base.scales, base.zeros, 64)
+    A = S.from_bits(base.A, S.F16).astype(np.float64)
+    B = S.from_bits(base.B, S.F16).astype(np.float64)
+    W_eff = W_hat + 0.75 * (B @ A)
+    x = S.from_bits(base.x, S.F16).astype(np.float64)
+    return bool(np.allclose(o.w4ec_linear(st), x @ W_eff.T, rtol=1e-12, atol=1e-14))
+
+
+def check_factored_form(o, seed=0) -> bool:
+    """Eq. 4: per token, y_m = (W_hat + alpha B diag(gamma(A x_m)) A) x_m."""
+    base = S.make_layer(M=3, N=24, K=128, group_size=128, rank=5, seed=seed,
+                        gate_kind=S.GATE_TANH_MLP, alpha=1.25, ec_std=0.2)
+    y = o.w4ec_linear(base)
+    W_hat = o.dequant(base.qweight, base.scales, base.zeros, 128)
+    f = lambda a: S.from_bits(a, S.F16).astype(np.float64)  # noqa: E731
+    x, A, B = f(base.x), f(base.A), f(base.B)
+    for m in range(base.M):
+        u = A @ x[m]
+        hid = np.maximum(f(base.W1) @ u + f(base.b1), 0.0)
+        gam = 1.0 + np.tanh(f(base.W2) @ hid + f(base.b2))
+        W_eff = W_hat + 1.25 * B @ np.diag(gam) @ A
+        if not np.allclose(y[m], W_eff @ x[m], rtol=1e-12, atol=1e-14):
+            return False
+    return True
+
+
+def check_gate_ranges(o) -> bool:
+    """gamma in (0, 2); gamma -> 2 for a large positive b2, -> 0 for a large
+    negative b2; sigma is finite and symmetric at +-1e4."""
+    rng = np.random.default_rng(0)
+    u = rng.normal(0, 3, size=(50, 4))
+    W1 = rng.normal(0, 1, size=(16, 4))
+    W2 = rng.normal(0, 1, size=(4, 16))
+    gam = o.gate_tanh_mlp(u, W1, np.zeros(16), W2, np.zeros(4))
+    ok = bool(np.all((gam >= 0) & (gam <= 2)))
+    ok &= bool(np.allclose(o.gate_tanh_mlp(u, W1, np.zeros(16), W2 * 0, np.full(4, 40.0)), 2.0))
+    ok &= bool(np.allclose(o.gate_tanh_mlp(u, W1, np.zeros(16), W2 * 0, np.full(4, -40.0)), 0.0))
+    s = o.sigmoid(np.array([-1e4, 0.0, 1e4, 3.0, -3.0]))
+    ok &= bool(s[0] == 0.0 and s[1] == 0.5 and s[2] == 1.0 and abs(s[3] + s[4] - 1) <= 4e-16)
+    return ok
+
+
+def check_dequant_bits_contract(o, seed=0) -> bool:
+    """The bit-exact dequantisation reference equals a single nearest-even
+    rounding of the exact product: cross-checked against torch's float32 ->
+    fp16/bf16 cast (an independent rounding implementation) over every code
+    and zero point with random fp16 scales."""
+    import torch
+    rng = np.random.default_rng(seed)
+    N, K = 16 * 16, 128
+    z = np.repeat(np.arange(16), 16).reshape(N, 1)
+    q = np.tile(np.arange(16), (N, K // 16))
+    s = rng.uniform(1e-4, 4.0, size=(N, 1)).astype(np.float16)
+    qw = S.pack_int4(q)
+    exact = ((q - z) * s.astype(np.float64)).astype(np.float32)
+    for dt, tdt in ((O.F16, torch.float16), (O.BF16, torch.bfloat16)):
+        want = torch.from_numpy(exact).to(tdt).view(torch.int16).numpy().view(np.uint16)
+        got = o.dequant_bits(qw, s.view(np.uint16), z.astype(np.uint8), K, dt)
+        if not np.array_equal(got, want):
+            return False
+    return True
+
+
+PINS = [check_unpack_fixed_words, check_unpack_exhaustive, check_golden_examples,
+        check_rounding_fixtures, check_rtn_grid_roundtrip, check_rtn_error_bound,
+        check_brute_force, check_integer_grid_exact, check_reductions,
+        check_sigmoid_half, check_tanh_static_lora, check_factored_form,
+        check_gate_ranges, check_dequant_bits_contract]
+
+
+@pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
+def test_oracle_pin(pin):
+    assert pin(O)
+
+
+# ---------------------------------------------------------------------------
+# planted mistakes: each broken copy of the oracle must fail some pin
+# ---------------------------------------------------------------------------
+
+def _mutant(**overrides):
+    m = types.ModuleType("oracle_mutant")
+    m.__dict__.update({k: v for k, v in O.__dict__.items() if not k.startswith("__")})
+    m.__dict__.update(overrides)
+    # re-bind module-level functions so that internal calls see the overrides
+    for name, fn in list(m.__dict__.items()):
+        if isinstance(fn, types.FunctionType) and name not in overrides:
+            m.__dict__[name] = types.FunctionType(fn.__code__, m.__dict__, name,
+                                                  fn.__defaults__, fn.__closure__)
+    return m
+
+
+def _unpack_reversed(qweight):
+    w = np.asarray(qweight, dtype=np.uint32)
+    n, kw = w.shape
+    q = np.empty((n, kw, 8), dtype=np.int64)
+    for i in range(8):
+        q[:, :, 7 - i] = (w >> np.uint32(4 * i)) & np.uint32(0xF)
+    return q.reshape(n, kw * 8)
+
+
+def _dequant_plus_zero(qweight, scales_bits, zeros, group_size):
+    q = O.unpack_int4(qweight)
+    n, k = q.shape
+    g = k if group_size in (0, k) else group_size
+    s = O.bits_to_f64(scales_bits, O.F16)
+    grp = np.arange(k) // g
+    return (q + np.asarray(zeros, np.int64)[:, grp]) * s[:, grp]
+
+
+def _dequant_wrong_group(qweight, scales_bits, zeros, group_size):
+    q = O.unpack_int4(qweight)
+    n, k = q.shape
+    g = k if group_size in (0, k) else group_size
+    s = O.bits_to_f64(scales_bits, O.F16)
+    grp = (np.arange(k) % (k // g))  # interleaved instead of contiguous groups
+    return (q - np.asarray(zeros, np.int64)[:, grp]) * s[:, grp]
+
+
+def _ec_no_alpha(x, W_hat, A, B, alpha, gate_kind, w_g=None, b_g=0.0, W1=None, b1=None,
+                 W2=None, b2=None):
+    return O.w4ec_linear_f64(x, W_hat, A, B, 1.0, gate_kind, w_g, b_g, W1, b1, W2, b2)
+
+
+def _ec_minus(x, W_hat, A, B, alpha, gate_kind, w_g=None, b_g=0.0, W1=None, b1=None,
+              W2=None, b2=None):
+    y0 = O.w4_linear(x, W_hat)
+    y1 = O.w4ec_linear_f64(x, W_hat, A, B, alpha, gate_kind, w_g, b_g, W1, b1, W2, b2)
+    return y0 - (y1 - y0)
+
+
+def _gate_no_one(u, W1, b1, W2, b2):
+    return O.gate_tanh_mlp(u, W1, b1, W2, b2) - 1.0
+
+
+def _gate_no_relu(u, W1, b1, W2, b2):
+    u = np.asarray(u, np.float64)
+    hid = u @ np.asarray(W1, np.float64).T + np.asarray(b1, np.float64)
+    return 1.0 + np.tanh(hid @ np.asarray(W2, np.float64).T + np.asarray(b2, np.float64))
+
+
+def _sigmoid_of_wrong_sign(x, w_g, b_g):
+    return O.sigmoid(-(np.asarray(x, np.float64) @ np.asarray(w_g, np.float64) + b_g))
+
+
+def _round_bf16_truncate(v, dtype):
+    if dtype == O.BF16:
+        f32 = np.asarray(v, np.float64).astype(np.float32)
+        return (f32.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+    return O.round_f64_to_bits(v, dtype)
+
+
+def _w4_linear_transposed_b(x, W_hat):
+    x = np.asarray(x, np.float64)
+    W = np.asarray(W_hat, np.float64)
+    if W.shape[0] == W.shape[1]:
+        return x @ W  # forgets the transpose on square weights
+    return x @ W.T
+
+
+MUTANTS = {
+    "nibble order reversed": dict(unpack_int4=_unpack_reversed),
+    "zero point added": dict(dequant=_dequant_plus_zero),
+    "groups interleaved": dict(dequant=_dequant_wrong_group),
+    "alpha dropped": dict(w4ec_linear_f64=_ec_no_alpha),
+    "EC term sign flipped": dict(w4ec_linear_f64=_ec_minus),
+    "gate missing the 1 +": dict(gate_tanh_mlp=_gate_no_one),
+    "gate missing the ReLU": dict(gate_tanh_mlp=_gate_no_relu),
+    "sigmoid argument negated": dict(gate_sigmoid_linear=_sigmoid_of_wrong_sign),
+    "bf16 rounding truncates": dict(round_f64_to_bits=_round_bf16_truncate),
+    "weight operand not transposed": dict(w4_linear=_w4_linear_transposed_b),
+}
+
+
+@pytest.mark.parametrize("name", list(MUTANTS))
+def test_planted_mistake_is_caught(name):
+    mut = _mutant(**MUTANTS[name])
+    failed = [p.__name__ for p in PINS if not _safe(p, mut)]
+    assert failed, f"planted mistake '{name}' passed every pin"
+
+
+def _safe(pin, mod):
+    try:
+        return bool(pin(mod))
+    except Exception:
+        return False
