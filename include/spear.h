@@ -1,0 +1,186 @@
+/*
+ * spear.h -- C ABI of the MI355X (gfx950) W4+EC linear layer.
+ *
+ * The layer is the serving hot path of SPEAR (arXiv 2606.11244): a 4-bit
+ * weight-only linear layer with the input-adaptive Error Compensator (EC)
+ * folded in (section 3.1, Eq. 3):
+ *
+ *     Y = X . What^T + alpha * ( gate(X) (.) (X . A^T) ) . B^T
+ *
+ * with What[n][k] = (q[n][k] - z[n][k/G]) * s[n][k/G], the asymmetric
+ * round-to-nearest 4-bit backbone of sections 3.2 and 5.1 (per output
+ * channel, or per group of G input channels). The phase-aware dispatch of
+ * section 4.1 chooses between a single fused kernel (decode, small M) and a
+ * semi-fused EC pre-kernel + 4-bit GEMM whose epilogue adds the EC (prefill,
+ * large M); spear_dispatch_plan exposes that choice.
+ *
+ * Conventions shared by every entry point:
+ *   - Device pointers unless stated otherwise. Every device pointer must be
+ *     16-byte aligned (SPEAR_E_ALIGN otherwise).
+ *   - Row-major layouts, sizes in elements:
+ *       x        [M][K]    activations, act dtype
+ *       y        [M][N]    output, act dtype (overwritten, not accumulated)
+ *       qweight  [N][K/8]  uint32; word j of row n holds code q[n][8j+i]
+ *                          (0..15) in bits 4i..4i+3, lowest nibble first
+ *       scales   [N][K/G]  IEEE fp16 bit patterns (both act dtypes)
+ *       zeros    [N][K/G]  uint8, values 0..15
+ *       A        [r][K]    act dtype      B  [N][r]  act dtype
+ *       w_g      [K]       act dtype (sigmoid-linear gate)
+ *       W1 [h][r], b1 [h], W2 [r][h], b2 [r]  act dtype (tanh-MLP gate)
+ *   - Ownership: the caller owns every buffer; the library never allocates
+ *     or frees device memory on these calls.
+ *   - Errors: arguments are validated on the host before any launch; a
+ *     validation failure returns a negative status and launches nothing. A
+ *     failed launch returns SPEAR_E_HIP. Nothing is printed.
+ *   - Asynchrony: every call is ordered on `hip_stream` (a hipStream_t; NULL
+ *     means the default stream) and returns without synchronising.
+ *   - Workspace: calls that need scratch take a caller-owned device buffer
+ *     of at least spear_dispatch_plan()'s workspace_bytes. It must be
+ *     zero-filled once before its first use; the kernels leave it reusable
+ *     (counters carry a per-call epoch, so stale contents cannot corrupt a
+ *     later call). Two calls that overlap in time must not share one
+ *     workspace.
+ */
+#ifndef SPEAR_H
+#define SPEAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t spear_status_t;
+
+enum {
+  SPEAR_OK = 0,
+  SPEAR_E_NULL = -1,        /* a required pointer is NULL                   */
+  SPEAR_E_SHAPE = -2,       /* M, N, K, G, r or h outside the supported set */
+  SPEAR_E_DTYPE = -3,       /* unknown activation dtype                     */
+  SPEAR_E_ALIGN = -4,       /* a device pointer is not 16-byte aligned      */
+  SPEAR_E_WORKSPACE = -5,   /* workspace missing or smaller than required   */
+  SPEAR_E_UNSUPPORTED = -6, /* gate kind or forced path not available       */
+  SPEAR_E_HIP = -7,         /* a HIP launch or query failed                 */
+  SPEAR_E_ALIAS = -8        /* the output overlaps an input                 */
+};
+
+/* Activation dtype: x, y, A, B and the gate parameters. */
+enum { SPEAR_F16 = 0, SPEAR_BF16 = 1 };
+
+/* Gate of the EC (section 3.1, Eq. 3). */
+enum {
+  SPEAR_GATE_ONE = 0,            /* gamma == 1: the static compensator of Eq. 2
+                                    with W_comp = alpha B A                    */
+  SPEAR_GATE_SIGMOID_LINEAR = 1, /* scalar per token g = sigmoid(w_g.x + b_g)  */
+  SPEAR_GATE_TANH_MLP = 2        /* gamma = 1 + tanh(W2 ReLU(W1 A x + b1) + b2),
+                                    the paper's rank-space gate (Eq. 3)        */
+};
+
+/* Execution path (section 4.1). AUTO lets spear_dispatch_plan choose by M. */
+enum {
+  SPEAR_PATH_AUTO = 0,
+  SPEAR_PATH_FUSED_GEMV = 1,     /* one kernel: split-K 4-bit GEMV; the same grid
+                                    computes A x and the gate, and the epilogue
+                                    adds B (g (.) A x). Decode, M <= 64.       */
+  SPEAR_PATH_FUSED_MFMA = 2,     /* reserved: fully fused MFMA GEMM (not built;
+                                    returns SPEAR_E_UNSUPPORTED)               */
+  SPEAR_PATH_UNFUSED_CHAIN = 3,  /* naive split: 4-bit GEMM, then separate
+                                    projection, gate and reprojection+accumulate
+                                    kernels (the baseline of section 4.1)      */
+  SPEAR_PATH_UNFUSED_2K = 4      /* semi-fused: EC pre-kernel (A x, gate) then
+                                    the 4-bit GEMM/GEMV whose epilogue adds
+                                    B (g (.) A x)                              */
+};
+
+typedef struct {
+  int64_t M;            /* tokens, >= 0 (0 is a no-op)                        */
+  int64_t N;            /* output features, >= 0 (0 is a no-op)               */
+  int64_t K;            /* input features, a positive multiple of 128         */
+  int32_t group_size;   /* G: 0 or K = per output channel; otherwise a
+                           multiple of 128 that divides K                     */
+  int32_t act_dtype;    /* SPEAR_F16 or SPEAR_BF16                            */
+  int32_t rank;         /* r, 0..256 (0: the EC is absent)                    */
+  int32_t gate_kind;    /* SPEAR_GATE_*                                       */
+  int32_t gate_hidden;  /* h of the tanh-MLP gate, 0 = 4r; at most 1024       */
+  int32_t force_path;   /* SPEAR_PATH_*; AUTO = choose by M                   */
+} spear_problem_t;
+
+typedef struct {
+  const uint32_t* qweight; /* [N][K/8] packed codes                           */
+  const uint16_t* scales;  /* [N][K/G] fp16 bits                              */
+  const uint8_t* zeros;    /* [N][K/G] 0..15                                  */
+} spear_w4_t;
+
+typedef struct {
+  const void* A;     /* [r][K] act dtype                                      */
+  const void* B;     /* [N][r] act dtype                                      */
+  float alpha;       /* EC scale (section 3.1); 1.0 when folded into B        */
+  const void* w_g;   /* [K] act dtype      (SIGMOID_LINEAR only)              */
+  float b_g;         /*                    (SIGMOID_LINEAR only)              */
+  const void* W1;    /* [h][r] act dtype   (TANH_MLP only)                    */
+  const void* b1;    /* [h]                                                   */
+  const void* W2;    /* [r][h]                                                */
+  const void* b2;    /* [r]                                                   */
+} spear_ec_t;
+
+typedef struct {
+  int32_t path;          /* resolved SPEAR_PATH_* (never AUTO)                */
+  int32_t split_k;       /* K-slices of the 4-bit product (GEMV paths)        */
+  int32_t ec_splits;     /* K-slices of the EC projection A x                 */
+  int32_t tile_m;        /* tokens per workgroup tile                         */
+  int32_t tile_n;        /* output rows per workgroup tile                    */
+  int32_t num_launches;  /* kernel launches one call makes                    */
+  int32_t grid;          /* workgroups of the main kernel                     */
+  int32_t reserved;
+  size_t workspace_bytes;/* scratch the call needs (0: none)                  */
+} spear_plan_t;
+
+/* Choose the execution path and launch shape for a problem (section 4.1:
+ * fused for decode, semi-fused for prefill, switched by the token count M).
+ * Host-only, pure and thread-safe: reads *prob, writes *out, touches no
+ * device. `with_ec` = 0 plans spear_w4_linear, 1 plans spear_w4ec_linear.
+ * Returns SPEAR_OK, or the validation error the call itself would return. */
+spear_status_t spear_dispatch_plan(const spear_problem_t* prob, int32_t with_ec,
+                                   spear_plan_t* out);
+
+/* Y = X . What^T: the 4-bit weight-only linear layer with no EC (the
+ * backbone of sections 3.2 and 5.1). The rank, gate and EC fields of *prob
+ * are ignored. */
+spear_status_t spear_w4_linear(const spear_problem_t* prob, const void* x,
+                               const spear_w4_t* w, void* y, void* workspace,
+                               size_t workspace_bytes, void* hip_stream);
+
+/* Y = X . What^T + alpha * (gate (.) (X . A^T)) . B^T (section 3.1, Eq. 3),
+ * executed on the path spear_dispatch_plan picks (or prob->force_path).
+ * rank == 0 computes exactly what spear_w4_linear computes. */
+spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x,
+                                 const spear_w4_t* w, const spear_ec_t* ec,
+                                 void* y, void* workspace,
+                                 size_t workspace_bytes, void* hip_stream);
+
+/* Diagnostic of the dequantisation the kernels use: writes
+ * w_out[n][k] = RNE_act((q[n][k] - z[n][k/G]) * s[n][k/G]) as a dense [N][K]
+ * act-dtype matrix, the exact product rounded once to nearest even
+ * (sections 3.2, 5.1). Only N, K, group_size and act_dtype of *prob are
+ * read. */
+spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w,
+                                void* w_out, void* hip_stream);
+
+/* Test hook for the fused path's bounded wait: the number of polls a
+ * workgroup makes for the EC coordinates before computing them itself
+ * (default 1 << 20; 0 forces every workgroup onto that self-computing
+ * fallback). Process-wide; returns the previous value. */
+int32_t spear_set_wait_polls(int32_t polls);
+
+/* Static text for a status code. */
+const char* spear_status_string(spear_status_t status);
+
+/* Library version, e.g. "0.1.0". */
+const char* spear_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPEAR_H */

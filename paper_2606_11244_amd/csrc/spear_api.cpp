@@ -1,0 +1,448 @@
+// Host side of the C ABI (include/spear.h): argument validation, the
+// phase-aware dispatch plan (SPEAR section 4.1), workspace layout and the
+// launch sequence of each path. No device memory is allocated here.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstring>
+
+#include "../../include/spear.h"
+#include "spear_internal.h"
+
+using namespace spear;
+
+namespace {
+
+std::atomic<uint32_t> g_epoch{0};
+std::atomic<int32_t> g_wait_polls{1 << 20};
+
+// Every call gets a fresh non-zero epoch (a zero-filled workspace holds epoch 0).
+uint32_t next_epoch() {
+  uint32_t e;
+  do {
+    e = g_epoch.fetch_add(1) + 1;
+  } while (e == 0);
+  return e;
+}
+
+// Token counts at or below this run the 4-bit product as a split-K GEMV; above
+// it the LDS-tiled MFMA GEMM. The same bound separates decode (fully fused
+// EC) from prefill (semi-fused EC pre-kernel) under SPEAR_PATH_AUTO.
+constexpr int64_t kGemvMaxM = 64;
+constexpr int kTargetBlocks = 1024;  // about four resident blocks per CU
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+struct Resolved {
+  spear_plan_t plan;
+  bool ec, gemv;
+  int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
+  int MT, RT, nrb, S, ips, ntb, P, eips, n_prod;
+  size_t off_flag, off_ectr, off_rbctr, off_upart, off_v, off_vh, off_vl, off_u, off_ypart;
+  size_t lds_gemv, lds_ec;
+};
+
+bool misaligned(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+spear_status_t validate_shape(const spear_problem_t* p, bool with_ec) {
+  if (!p) return SPEAR_E_NULL;
+  if (p->M < 0 || p->N < 0 || p->K <= 0 || p->K % kIterK) return SPEAR_E_SHAPE;
+  if (p->act_dtype != SPEAR_F16 && p->act_dtype != SPEAR_BF16) return SPEAR_E_DTYPE;
+  const int64_t G = (p->group_size == 0) ? p->K : p->group_size;
+  if (G <= 0 || G % kIterK || p->K % G) return SPEAR_E_SHAPE;
+  // element counts stay below 2^31 so that row indexing inside kernels is int
+  const int64_t lim = (int64_t)1 << 31;
+  if (p->M * p->K >= lim || p->N * p->K >= lim || p->M * p->N >= lim) return SPEAR_E_SHAPE;
+  if (p->force_path < SPEAR_PATH_AUTO || p->force_path > SPEAR_PATH_UNFUSED_2K)
+    return SPEAR_E_UNSUPPORTED;
+  if (with_ec) {
+    if (p->rank < 0 || p->rank > 256) return SPEAR_E_SHAPE;
+    if (p->gate_kind < SPEAR_GATE_ONE || p->gate_kind > SPEAR_GATE_TANH_MLP) return SPEAR_E_UNSUPPORTED;
+    if (p->gate_hidden < 0 || p->gate_hidden > 1024) return SPEAR_E_SHAPE;
+  }
+  return SPEAR_OK;
+}
+
+spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
+  spear_status_t st = validate_shape(p, with_ec);
+  if (st != SPEAR_OK) return st;
+  Resolved& z = *R;
+  std::memset(&z, 0, sizeof(z));
+  const int64_t M = p->M, N = p->N, K = p->K;
+  z.dt = p->act_dtype;
+  z.G = (int)((p->group_size == 0) ? K : p->group_size);
+  z.ngroups = (int)(K / z.G);
+  z.IT = (int)(K / kIterK);
+  z.r = with_ec ? p->rank : 0;
+  z.ec = z.r > 0;
+  z.gate = z.ec ? p->gate_kind : GATE_ONE;
+  z.R1 = z.r + (z.gate == GATE_SIGMOID ? 1 : 0);
+  z.R1p = (int)cdiv(std::max(z.R1, 1), 16) * 16;
+  z.h = z.gate == GATE_TANH ? (p->gate_hidden > 0 ? p->gate_hidden : 4 * z.r) : 0;
+  z.vstride = (int)cdiv(std::max(z.r, 1), 32) * 32;
+
+  // path
+  int path = p->force_path;
+  if (path == SPEAR_PATH_FUSED_MFMA) return SPEAR_E_UNSUPPORTED;
+  if (path == SPEAR_PATH_FUSED_GEMV && M > kGemvMaxM) return SPEAR_E_UNSUPPORTED;
+  if (path == SPEAR_PATH_AUTO || !z.ec)
+    path = (M <= kGemvMaxM) ? SPEAR_PATH_FUSED_GEMV : SPEAR_PATH_UNFUSED_2K;
+  if (!with_ec) path = (M <= kGemvMaxM) ? SPEAR_PATH_FUSED_GEMV : SPEAR_PATH_UNFUSED_2K;
+  z.gemv = M <= kGemvMaxM;
+  z.plan.path = path;
+
+  if (M == 0 || N == 0) {
+    z.plan.num_launches = 0;
+    return SPEAR_OK;
+  }
+
+  // 4-bit product shape
+  if (z.gemv) {
+    z.MT = (int)cdiv(M, 16);
+    z.RT = z.MT == 1 ? 4 : (z.MT == 2 ? 2 : 1);
+    const int RB = 16 * z.RT;
+    z.nrb = (int)cdiv(N, RB);
+    int S = (int)cdiv(kTargetBlocks, z.nrb);
+    S = std::min(S, std::max(1, z.IT / 4));
+    S = std::min<int64_t>(S, std::max<int64_t>(1, K / (32 * M)));
+    S = std::max(S, 1);
+    z.ips = (int)cdiv(z.IT, S);
+    z.S = (int)cdiv(z.IT, z.ips);
+    const int ngs_max = (int)std::min<int64_t>(z.ngroups, cdiv((int64_t)z.ips * kIterK, z.G) + 1);
+    z.lds_gemv = gemv_lds_e_off(ngs_max, z.RT, z.MT);
+    z.plan.split_k = z.S;
+    z.plan.tile_m = 16 * z.MT;
+    z.plan.tile_n = RB;
+  } else {
+    z.plan.split_k = 1;
+    z.plan.tile_m = kGemmTM;
+    z.plan.tile_n = kGemmTN;
+  }
+
+  // EC projection shape
+  z.ntb = (int)cdiv(M, kTokTile);
+  if (z.ec) {
+    if (z.gemv) {
+      const double a_bytes = (double)z.R1 * K * 2;
+      const double w_per_block = (double)N * K / 2 / std::max(1, z.nrb * z.S);
+      int P = (int)std::ceil(a_bytes / std::max(1.0, w_per_block));
+      P = std::max(1, std::min(P, z.IT));
+      z.eips = (int)cdiv(z.IT, P);
+      z.P = (int)cdiv(z.IT, z.eips);
+    } else {
+      z.P = 1;
+      z.eips = z.IT;
+    }
+    z.lds_ec = ec_lds_bytes(z.R1p, z.h, z.r);
+    if (z.gemv) z.lds_gemv += z.lds_ec;
+  }
+  z.plan.ec_splits = z.ec ? z.P : 0;
+
+  // launches and grid
+  if (!z.ec) {
+    z.plan.num_launches = 1;
+    z.plan.grid = z.gemv ? z.nrb * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
+  } else if (path == SPEAR_PATH_FUSED_GEMV) {
+    z.n_prod = z.ntb * z.P;
+    z.plan.num_launches = 1;
+    z.plan.grid = z.n_prod + z.nrb * z.S;
+  } else if (path == SPEAR_PATH_UNFUSED_2K) {
+    z.plan.num_launches = 2;
+    z.plan.grid = z.gemv ? z.nrb * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
+  } else {  // chain
+    z.plan.num_launches = 4;
+    z.plan.grid = z.gemv ? z.nrb * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
+  }
+
+  // workspace layout
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  if (z.ec) {
+    z.off_flag = take((size_t)z.ntb * 4);
+    z.off_ectr = take((size_t)z.ntb * 8);
+    if (z.P > 1) z.off_upart = take((size_t)z.ntb * z.P * kTokTile * z.R1 * 4);
+    z.off_v = take((size_t)M * z.r * 4);
+    if (!z.gemv && path == SPEAR_PATH_UNFUSED_2K) {
+      z.off_vh = take((size_t)M * z.vstride * 2);
+      z.off_vl = take((size_t)M * z.vstride * 2);
+    }
+    if (path == SPEAR_PATH_UNFUSED_CHAIN) z.off_u = take((size_t)M * z.R1 * 4);
+  }
+  if (z.gemv && z.S > 1) {
+    z.off_rbctr = take((size_t)z.nrb * 8);
+    z.off_ypart = take((size_t)z.S * M * N * 4);
+  }
+  z.plan.workspace_bytes = off;
+  return SPEAR_OK;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+spear_status_t check_w4(const spear_problem_t* p, const void* x, const spear_w4_t* w, const void* y) {
+  if (!w || !x || !y || !w->qweight || !w->scales || !w->zeros) return SPEAR_E_NULL;
+  if (misaligned(x) || misaligned(y) || misaligned(w->qweight) || misaligned(w->scales) ||
+      misaligned(w->zeros))
+    return SPEAR_E_ALIGN;
+  const size_t G = p->group_size == 0 ? (size_t)p->K : (size_t)p->group_size;
+  const size_t ybytes = (size_t)p->M * p->N * 2;
+  if (overlaps(y, ybytes, x, (size_t)p->M * p->K * 2) ||
+      overlaps(y, ybytes, w->qweight, (size_t)p->N * p->K / 2) ||
+      overlaps(y, ybytes, w->scales, (size_t)p->N * (p->K / G) * 2) ||
+      overlaps(y, ybytes, w->zeros, (size_t)p->N * (p->K / G)))
+    return SPEAR_E_ALIAS;
+  return SPEAR_OK;
+}
+
+spear_status_t check_ec(const spear_problem_t* p, const Resolved& z, const spear_ec_t* ec, const void* y) {
+  if (!z.ec) return SPEAR_OK;
+  if (!ec || !ec->A || !ec->B) return SPEAR_E_NULL;
+  if (z.gate == GATE_SIGMOID && !ec->w_g) return SPEAR_E_NULL;
+  if (z.gate == GATE_TANH && (!ec->W1 || !ec->b1 || !ec->W2 || !ec->b2)) return SPEAR_E_NULL;
+  if (misaligned(ec->A) || misaligned(ec->B) || misaligned(ec->w_g) || misaligned(ec->W1) ||
+      misaligned(ec->b1) || misaligned(ec->W2) || misaligned(ec->b2))
+    return SPEAR_E_ALIGN;
+  const size_t ybytes = (size_t)p->M * p->N * 2;
+  if (overlaps(y, ybytes, ec->A, (size_t)z.r * p->K * 2) ||
+      overlaps(y, ybytes, ec->B, (size_t)p->N * z.r * 2) ||
+      (z.gate == GATE_SIGMOID && overlaps(y, ybytes, ec->w_g, (size_t)p->K * 2)))
+    return SPEAR_E_ALIAS;
+  return SPEAR_OK;
+}
+
+spear_status_t check_ws(const spear_problem_t* p, const Resolved& z, const void* y, void* ws,
+                        size_t ws_bytes) {
+  if (z.plan.workspace_bytes == 0) return SPEAR_OK;
+  if (!ws || ws_bytes < z.plan.workspace_bytes) return SPEAR_E_WORKSPACE;
+  if (misaligned(ws)) return SPEAR_E_ALIGN;
+  if (overlaps(y, (size_t)p->M * p->N * 2, ws, z.plan.workspace_bytes)) return SPEAR_E_ALIAS;
+  return SPEAR_OK;
+}
+
+EcParams make_ec(const spear_problem_t* p, const Resolved& z, const void* x, const spear_ec_t* ec,
+                 char* ws, uint32_t epoch) {
+  EcParams e;
+  std::memset(&e, 0, sizeof(e));
+  e.x = (const uint16_t*)x;
+  e.M = (int)p->M;
+  e.K = (int)p->K;
+  e.r = z.r;
+  e.R1 = z.R1;
+  e.R1p = z.R1p;
+  e.h = z.h;
+  e.gate = z.gate;
+  e.P = z.P;
+  e.ips = z.eips;
+  e.epoch = epoch;
+  e.vstride = z.vstride;
+  if (ec) {
+    e.A = (const uint16_t*)ec->A;
+    e.wg = (const uint16_t*)ec->w_g;
+    e.W1 = (const uint16_t*)ec->W1;
+    e.b1 = (const uint16_t*)ec->b1;
+    e.W2 = (const uint16_t*)ec->W2;
+    e.b2 = (const uint16_t*)ec->b2;
+    e.b_g = ec->b_g;
+    e.alpha = ec->alpha;
+  }
+  if (ws) {
+    e.ctr = (unsigned long long*)(ws + z.off_ectr);
+    if (z.P > 1) e.upart = (float*)(ws + z.off_upart);
+    e.v = (float*)(ws + z.off_v);
+  }
+  return e;
+}
+
+GemvParams make_gemv(const spear_problem_t* p, const Resolved& z, const void* x, const spear_w4_t* w,
+                     void* y, const spear_ec_t* ec, char* ws, uint32_t epoch) {
+  GemvParams g;
+  std::memset(&g, 0, sizeof(g));
+  g.qw = w->qweight;
+  g.sc = w->scales;
+  g.zr = w->zeros;
+  g.x = (const uint16_t*)x;
+  g.y = (uint16_t*)y;
+  g.M = (int)p->M;
+  g.N = (int)p->N;
+  g.K = (int)p->K;
+  g.G = z.G;
+  g.ngroups = z.ngroups;
+  g.r = z.r;
+  g.B = ec ? (const uint16_t*)ec->B : nullptr;
+  g.S = z.S;
+  g.ips = z.ips;
+  g.epoch = epoch;
+  g.wait_polls = g_wait_polls.load();
+  if (ws && z.S > 1) {
+    g.ypart = (float*)(ws + z.off_ypart);
+    g.rb_ctr = (unsigned long long*)(ws + z.off_rbctr);
+  }
+  return g;
+}
+
+GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x, const spear_w4_t* w,
+                     void* y, const spear_ec_t* ec, char* ws) {
+  GemmParams g;
+  std::memset(&g, 0, sizeof(g));
+  g.qw = w->qweight;
+  g.sc = w->scales;
+  g.zr = w->zeros;
+  g.x = (const uint16_t*)x;
+  g.y = (uint16_t*)y;
+  g.M = (int)p->M;
+  g.N = (int)p->N;
+  g.K = (int)p->K;
+  g.G = z.G;
+  g.ngroups = z.ngroups;
+  g.r = z.r;
+  g.vstride = z.vstride;
+  if (ec && ws && z.off_vh) {
+    g.B = (const uint16_t*)ec->B;
+    g.vh = (const uint16_t*)(ws + z.off_vh);
+    g.vl = (const uint16_t*)(ws + z.off_vl);
+  }
+  return g;
+}
+
+spear_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPEAR_OK : SPEAR_E_HIP; }
+
+spear_status_t run_w4(const spear_problem_t* p, const Resolved& z, const void* x, const spear_w4_t* w,
+                      void* y, char* ws, uint32_t epoch, hipStream_t st) {
+  if (z.gemv) {
+    GemvParams g = make_gemv(p, z, x, w, y, nullptr, ws, epoch);
+    return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_NONE, g, z.nrb * z.S, z.lds_gemv, st));
+  }
+  GemmParams g = make_gemm(p, z, x, w, y, nullptr, nullptr);
+  return hip_status(launch_gemm(z.dt, EPI_NONE, g, st));
+}
+
+}  // namespace
+
+extern "C" {
+
+spear_status_t spear_dispatch_plan(const spear_problem_t* prob, int32_t with_ec, spear_plan_t* out) {
+  if (!prob || !out) return SPEAR_E_NULL;
+  Resolved z;
+  spear_status_t st = resolve(prob, with_ec != 0, &z);
+  if (st != SPEAR_OK) return st;
+  *out = z.plan;
+  return SPEAR_OK;
+}
+
+spear_status_t spear_w4_linear(const spear_problem_t* prob, const void* x, const spear_w4_t* w,
+                               void* y, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  Resolved z;
+  spear_status_t st = resolve(prob, false, &z);
+  if (st != SPEAR_OK) return st;
+  if (prob->M == 0 || prob->N == 0) return SPEAR_OK;
+  if ((st = check_w4(prob, x, w, y)) != SPEAR_OK) return st;
+  if ((st = check_ws(prob, z, y, workspace, workspace_bytes)) != SPEAR_OK) return st;
+  return run_w4(prob, z, x, w, y, (char*)workspace, next_epoch(), (hipStream_t)hip_stream);
+}
+
+spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, const spear_w4_t* w,
+                                 const spear_ec_t* ec, void* y, void* workspace,
+                                 size_t workspace_bytes, void* hip_stream) {
+  Resolved z;
+  spear_status_t st = resolve(prob, true, &z);
+  if (st != SPEAR_OK) return st;
+  if (prob->M == 0 || prob->N == 0) return SPEAR_OK;
+  if ((st = check_w4(prob, x, w, y)) != SPEAR_OK) return st;
+  if ((st = check_ec(prob, z, ec, y)) != SPEAR_OK) return st;
+  if ((st = check_ws(prob, z, y, workspace, workspace_bytes)) != SPEAR_OK) return st;
+  hipStream_t s = (hipStream_t)hip_stream;
+  char* ws = (char*)workspace;
+  const uint32_t epoch = next_epoch();
+  if (!z.ec) return run_w4(prob, z, x, w, y, ws, epoch, s);
+
+  EcParams e = make_ec(prob, z, x, ec, ws, epoch);
+  const int path = z.plan.path;
+  if (path == SPEAR_PATH_FUSED_GEMV) {
+    e.flag = (uint32_t*)(ws + z.off_flag);
+    GemvParams g = make_gemv(prob, z, x, w, y, ec, ws, epoch);
+    g.ec = e;
+    g.n_prod = z.n_prod;
+    const size_t lds = std::max(z.lds_gemv, z.lds_ec);
+    return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_FUSED, g, z.n_prod + z.nrb * z.S, lds, s));
+  }
+  if (path == SPEAR_PATH_UNFUSED_2K) {
+    if (!z.gemv) {
+      e.vh = (uint16_t*)(ws + z.off_vh);
+      e.vl = (uint16_t*)(ws + z.off_vl);
+    }
+    st = hip_status(launch_ec(z.dt, e, z.ntb, z.lds_ec, s));
+    if (st != SPEAR_OK) return st;
+    if (z.gemv) {
+      GemvParams g = make_gemv(prob, z, x, w, y, ec, ws, epoch);
+      g.ec = e;
+      return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_READY, g, z.nrb * z.S, z.lds_gemv, s));
+    }
+    GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
+    return hip_status(launch_gemm(z.dt, EPI_READY, g, s));
+  }
+  // naive chain: 4-bit product, projection, gate, reprojection + accumulate
+  st = run_w4(prob, z, x, w, y, ws, epoch, s);
+  if (st != SPEAR_OK) return st;
+  e.raw = 1;
+  e.u_out = (float*)(ws + z.off_u);
+  st = hip_status(launch_ec(z.dt, e, z.ntb, z.lds_ec, s));
+  if (st != SPEAR_OK) return st;
+  e.raw = 0;
+  st = hip_status(launch_gate(z.dt, e, z.ntb, z.lds_ec, s));
+  if (st != SPEAR_OK) return st;
+  return hip_status(launch_ec_up_acc(z.dt, e.v, (const uint16_t*)ec->B, (uint16_t*)y, (int)prob->M,
+                                     (int)prob->N, z.r, s));
+}
+
+spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w, void* w_out,
+                                void* hip_stream) {
+  if (!prob || !w) return SPEAR_E_NULL;
+  spear_problem_t q = *prob;
+  q.M = 0;
+  q.force_path = SPEAR_PATH_AUTO;
+  spear_status_t st = validate_shape(&q, false);
+  if (st != SPEAR_OK) return st;
+  if (prob->N == 0) return SPEAR_OK;
+  if (!w_out || !w->qweight || !w->scales || !w->zeros) return SPEAR_E_NULL;
+  if (misaligned(w_out) || misaligned(w->qweight) || misaligned(w->scales) || misaligned(w->zeros))
+    return SPEAR_E_ALIGN;
+  const int G = (int)(prob->group_size == 0 ? prob->K : prob->group_size);
+  const size_t outb = (size_t)prob->N * prob->K * 2;
+  if (overlaps(w_out, outb, w->qweight, (size_t)prob->N * prob->K / 2) ||
+      overlaps(w_out, outb, w->scales, (size_t)prob->N * (prob->K / G) * 2) ||
+      overlaps(w_out, outb, w->zeros, (size_t)prob->N * (prob->K / G)))
+    return SPEAR_E_ALIAS;
+  return hip_status(launch_dequant(prob->act_dtype, w->qweight, w->scales, w->zeros,
+                                   (uint16_t*)w_out, (int)prob->N, (int)prob->K, G,
+                                   (hipStream_t)hip_stream));
+}
+
+int32_t spear_set_wait_polls(int32_t polls) { return g_wait_polls.exchange(polls < 0 ? 0 : polls); }
+
+const char* spear_status_string(spear_status_t s) {
+  switch (s) {
+    case SPEAR_OK: return "ok";
+    case SPEAR_E_NULL: return "a required pointer is NULL";
+    case SPEAR_E_SHAPE: return "shape outside the supported set";
+    case SPEAR_E_DTYPE: return "unknown activation dtype";
+    case SPEAR_E_ALIGN: return "pointer not 16-byte aligned";
+    case SPEAR_E_WORKSPACE: return "workspace missing or too small";
+    case SPEAR_E_UNSUPPORTED: return "gate kind or path not supported";
+    case SPEAR_E_HIP: return "HIP launch failed";
+    case SPEAR_E_ALIAS: return "output overlaps an input";
+    default: return "unknown status";
+  }
+}
+
+const char* spear_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,224 @@
+"""Python binding of the C ABI in include/spear.h (argument marshalling only).
+
+Every step of the layer runs in libspear.so's HIP kernels; this module only
+turns torch tensors into pointers, the problem description into the C
+structs, and status codes into exceptions. If the library is not built it
+raises at import time: there is no fallback.
+
+Functions mirror the C entry points: dispatch_plan, w4_linear, w4ec_linear,
+w4_dequant, plus allocate_workspace (the caller-owned scratch buffer).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libspear.so")
+
+F16, BF16 = 0, 1
+GATE_ONE, GATE_SIGMOID_LINEAR, GATE_TANH_MLP = 0, 1, 2
+PATH_AUTO, PATH_FUSED_GEMV, PATH_FUSED_MFMA, PATH_UNFUSED_CHAIN, PATH_UNFUSED_2K = 0, 1, 2, 3, 4
+PATH_NAMES = {PATH_AUTO: "auto", PATH_FUSED_GEMV: "fused_gemv", PATH_FUSED_MFMA: "fused_mfma",
+              PATH_UNFUSED_CHAIN: "unfused_chain", PATH_UNFUSED_2K: "unfused_2k"}
+
+STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_DTYPE",
+          -4: "SPEAR_E_ALIGN", -5: "SPEAR_E_WORKSPACE", -6: "SPEAR_E_UNSUPPORTED",
+          -7: "SPEAR_E_HIP", -8: "SPEAR_E_ALIAS"}
+
+EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
+            "spear_set_wait_polls", "spear_status_string", "spear_version")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("group_size", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
+                ("rank", ctypes.c_int32), ("gate_kind", ctypes.c_int32),
+                ("gate_hidden", ctypes.c_int32), ("force_path", ctypes.c_int32)]
+
+
+class W4(ctypes.Structure):
+    _fields_ = [("qweight", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("zeros", ctypes.c_void_p)]
+
+
+class EC(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("alpha", ctypes.c_float),
+                ("w_g", ctypes.c_void_p), ("b_g", ctypes.c_float),
+                ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
+                ("W2", ctypes.c_void_p), ("b2", ctypes.c_void_p)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("split_k", ctypes.c_int32),
+                ("ec_splits", ctypes.c_int32), ("tile_m", ctypes.c_int32),
+                ("tile_n", ctypes.c_int32), ("num_launches", ctypes.c_int32),
+                ("grid", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
+
+
+class SpearError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)}")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run paper_2606_11244_amd.build.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    lib.spear_dispatch_plan.argtypes = [P(Problem), ctypes.c_int32, P(Plan)]
+    lib.spear_w4_linear.argtypes = [P(Problem), ctypes.c_void_p, P(W4), ctypes.c_void_p,
+                                    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.spear_w4ec_linear.argtypes = [P(Problem), ctypes.c_void_p, P(W4), P(EC), ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.spear_w4_dequant.argtypes = [P(Problem), P(W4), ctypes.c_void_p, ctypes.c_void_p]
+    lib.spear_set_wait_polls.argtypes = [ctypes.c_int32]
+    lib.spear_status_string.argtypes = [ctypes.c_int32]
+    lib.spear_status_string.restype = ctypes.c_char_p
+    lib.spear_version.restype = ctypes.c_char_p
+    for f in ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
+              "spear_set_wait_polls"):
+        getattr(lib, f).restype = ctypes.c_int32
+    return lib
+
+
+LIB = _load()
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float16:
+        return F16
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported activation dtype {t.dtype}")
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def problem(M, N, K, group_size=0, act_dtype=F16, rank=0, gate_kind=GATE_SIGMOID_LINEAR,
+            gate_hidden=0, force_path=PATH_AUTO) -> Problem:
+    return Problem(int(M), int(N), int(K), int(group_size), int(act_dtype), int(rank),
+                   int(gate_kind), int(gate_hidden), int(force_path))
+
+
+def dispatch_plan(prob: Problem, with_ec: bool = True) -> Plan:
+    out = Plan()
+    st = LIB.spear_dispatch_plan(ctypes.byref(prob), 1 if with_ec else 0, ctypes.byref(out))
+    if st != 0:
+        raise SpearError(st, "spear_dispatch_plan")
+    return out
+
+
+def allocate_workspace(prob: Problem, with_ec: bool = True, device="cuda") -> torch.Tensor:
+    """Zero-filled workspace of the size the plan asks for (at least 256 B)."""
+    nbytes = max(256, dispatch_plan(prob, with_ec).workspace_bytes)
+    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
+
+
+def w4_linear(prob: Problem, x, qweight, scales, zeros, y, workspace=None, stream=None):
+    w = W4(_ptr(qweight).value, _ptr(scales).value, _ptr(zeros).value)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = LIB.spear_w4_linear(ctypes.byref(prob), _ptr(x), ctypes.byref(w), _ptr(y),
+                             _ptr(workspace), ws_bytes, _stream(stream))
+    if st != 0:
+        raise SpearError(st, "spear_w4_linear")
+    return y
+
+
+def w4ec_linear(prob: Problem, x, qweight, scales, zeros, A, B, y, *, alpha=1.0, w_g=None,
+                b_g=0.0, W1=None, b1=None, W2=None, b2=None, workspace=None, stream=None):
+    w = W4(_ptr(qweight).value, _ptr(scales).value, _ptr(zeros).value)
+
+    def p(t):
+        return None if t is None else t.data_ptr()
+
+    ec = EC(p(A), p(B), float(alpha), p(w_g), float(b_g), p(W1), p(b1), p(W2), p(b2))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = LIB.spear_w4ec_linear(ctypes.byref(prob), _ptr(x), ctypes.byref(w), ctypes.byref(ec),
+                               _ptr(y), _ptr(workspace), ws_bytes, _stream(stream))
+    if st != 0:
+        raise SpearError(st, "spear_w4ec_linear")
+    return y
+
+
+def w4_dequant(prob: Problem, qweight, scales, zeros, w_out, stream=None):
+    w = W4(_ptr(qweight).value, _ptr(scales).value, _ptr(zeros).value)
+    st = LIB.spear_w4_dequant(ctypes.byref(prob), ctypes.byref(w), _ptr(w_out), _stream(stream))
+    if st != 0:
+        raise SpearError(st, "spear_w4_dequant")
+    return w_out
+
+
+def set_wait_polls(polls: int) -> int:
+    return int(LIB.spear_set_wait_polls(int(polls)))
+
+
+def version() -> str:
+    return LIB.spear_version().decode()
+
+
+# ---------------------------------------------------------------------------
+# device tensors of a generated layer (synth.Layer) and one call on them
+# ---------------------------------------------------------------------------
+
+_TORCH_DT = {F16: torch.float16, BF16: torch.bfloat16}
+
+
+class DeviceLayer:
+    """The stored tensors of one layer, resident on the GPU."""
+
+    def __init__(self, layer, device="cuda"):
+        import numpy as np
+        dt = _TORCH_DT[layer.act_dtype]
+
+        def act(a, shape=None):
+            t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(dt)
+            return t.reshape(shape).to(device) if shape else t.to(device)
+
+        self.layer = layer
+        self.M, self.N, self.K = layer.M, layer.N, layer.K
+        self.dtype = dt
+        self.qweight = torch.from_numpy(layer.qweight.view(np.int32)).to(device)
+        self.scales = torch.from_numpy(layer.scales.view(np.int16)).to(device)
+        self.zeros = torch.from_numpy(layer.zeros).to(device)
+        self.x = act(layer.x)
+        self.A = act(layer.A) if layer.rank > 0 else None
+        self.B = act(layer.B) if layer.rank > 0 else None
+        self.w_g = act(layer.w_g)
+        self.W1, self.b1 = act(layer.W1), act(layer.b1)
+        self.W2, self.b2 = act(layer.W2), act(layer.b2)
+        self.y = torch.empty((layer.M, layer.N), dtype=dt, device=device)
+
+    def problem(self, force_path=PATH_AUTO, rank=None, gate_kind=None):
+        L = self.layer
+        return problem(L.M, L.N, L.K, L.group_size, L.act_dtype,
+                       L.rank if rank is None else rank,
+                       L.gate_kind if gate_kind is None else gate_kind,
+                       L.gate_hidden if L.rank > 0 else 0, force_path)
+
+    def run_ec(self, prob, workspace, stream=None, y=None):
+        L = self.layer
+        y = self.y if y is None else y
+        return w4ec_linear(prob, self.x, self.qweight, self.scales, self.zeros, self.A, self.B, y,
+                           alpha=L.alpha, w_g=self.w_g, b_g=L.b_g, W1=self.W1, b1=self.b1,
+                           W2=self.W2, b2=self.b2, workspace=workspace, stream=stream)
+
+    def run_w4(self, prob, workspace, stream=None, y=None):
+        y = self.y if y is None else y
+        return w4_linear(prob, self.x, self.qweight, self.scales, self.zeros, y,
+                         workspace=workspace, stream=stream)

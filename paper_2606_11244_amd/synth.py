@@ -60,13 +60,13 @@ def pack_int4(q: np.ndarray) -> np.ndarray:
     n, k = q.shape
     if k % 8:
         raise ValueError("K must be a multiple of 8 to pack 4-bit codes")
-    if q.min(initial=0) < 0 or q.max(initial=0) > 15:
+    if q.size and (q.min() < 0 or q.max() > 15):
         raise ValueError("codes must lie in 0..15")
-    q = q.astype(np.uint32).reshape(n, k // 8, 8)
-    words = np.zeros((n, k // 8), dtype=np.uint32)
-    for i in range(8):
-        words |= q[:, :, i] << np.uint32(4 * i)
-    return words
+    q8 = q.astype(np.uint8, copy=False)
+    # byte j of a row holds codes 2j (low nibble) and 2j+1 (high nibble); four
+    # consecutive bytes read as a little-endian uint32 give the word layout
+    b = np.ascontiguousarray(q8[:, 0::2] | (q8[:, 1::2] << np.uint8(4)))
+    return b.view("<u4").astype(np.uint32, copy=False).reshape(n, k // 8)
 
 
 def rtn_quantize(w: np.ndarray, group_size: int):
@@ -80,24 +80,35 @@ def rtn_quantize(w: np.ndarray, group_size: int):
       q = clip(rne(w / s) + z, 0, 15)     (codes, chosen against the fp16 s)
     A constant group (hi == lo) or a scale that rounds to zero uses s = 1 and
     z = clip(rne(-lo), 0, 15).
-    Returns (codes int64 [N][K], scales fp16 bits [N][K/G], zeros uint8 [N][K/G]).
+    Returns (codes uint8 [N][K], scales fp16 bits [N][K/G], zeros uint8 [N][K/G]).
     """
     w = np.asarray(w, dtype=np.float32)
     n, k = w.shape
     g = k if group_size in (0, k) else group_size
     if k % g:
         raise ValueError("K must be a multiple of the group size")
-    wg = w.reshape(n, k // g, g).astype(np.float64)
-    lo = wg.min(axis=2)
-    hi = wg.max(axis=2)
-    s = ((hi - lo) / 15.0).astype(np.float16).astype(np.float64)
-    degenerate = (hi == lo) | (s == 0)
-    s = np.where(degenerate, 1.0, s)
-    z = np.clip(np.rint(-lo / s), 0, 15)
-    q = np.clip(np.rint(wg / s[:, :, None]) + z[:, :, None], 0, 15)
-    return (q.reshape(n, k).astype(np.int64),
-            s.astype(np.float16).view(np.uint16),
-            z.astype(np.uint8))
+    q_out = np.empty((n, k), dtype=np.uint8)
+    s_out = np.empty((n, k // g), dtype=np.uint16)
+    z_out = np.empty((n, k // g), dtype=np.uint8)
+    step = max(1, (1 << 23) // k)  # rows per chunk, bounds the temporaries
+    for r0 in range(0, n, step):
+        r1 = min(n, r0 + step)
+        wg = w[r0:r1].reshape(r1 - r0, k // g, g)
+        lo = wg.min(axis=2).astype(np.float64)
+        hi = wg.max(axis=2).astype(np.float64)
+        s = ((hi - lo) / 15.0).astype(np.float16).astype(np.float64)
+        degenerate = (hi == lo) | (s == 0)
+        s = np.where(degenerate, 1.0, s)
+        z = np.clip(np.rint(-lo / s), 0, 15)
+        # w / s in float32: s is an fp16 value (exact in float32); the quotient's
+        # rounding can only matter within 2^-24 of a rounding tie
+        qf = np.rint(wg / s.astype(np.float32)[:, :, None])
+        qf += z.astype(np.float32)[:, :, None]
+        np.clip(qf, 0, 15, out=qf)
+        q_out[r0:r1] = qf.reshape(r1 - r0, k).astype(np.uint8)
+        s_out[r0:r1] = s.astype(np.float16).view(np.uint16)
+        z_out[r0:r1] = z.astype(np.uint8)
+    return q_out, s_out, z_out
 
 
 @dataclasses.dataclass
@@ -148,10 +159,12 @@ def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
     """
     g = K if group_size in (0, K) else group_size
     rng = np.random.default_rng(np.random.SeedSequence([seed, config_id, module_id]))
-    w = rng.normal(0.0, w_std, size=(N, K)).astype(np.float32)
+    w = rng.standard_normal((N, K), dtype=np.float32)
+    w *= np.float32(w_std)
     q, s, z = rtn_quantize(w, g)
     del w
-    x = rng.normal(0.0, x_std, size=(M, K)).astype(np.float32)
+    x = rng.standard_normal((M, K), dtype=np.float32)
+    x *= np.float32(x_std)
     if outlier_frac > 0.0 and M > 0:
         n_out = int(round(outlier_frac * K))
         idx = rng.choice(K, size=n_out, replace=False)

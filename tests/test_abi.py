@@ -1,0 +1,184 @@
+"""Host-side tests of the C ABI: the library loads, exports every symbol the
+header declares, validates arguments before any launch, and plans paths.
+No call here reaches a kernel (every call is rejected on the host or is the
+pure planning function), so these run without a GPU."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_11244_amd import spear as sp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    text = open(os.path.join(ROOT, "include", "spear.h")).read()
+    return sorted(set(re.findall(r"^\S.*?\b(spear_[a-z0-9_]+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_symbols()
+    assert set(names) == set(sp.EXPORTED), names
+    for n in names:
+        assert hasattr(sp.LIB, n), n
+
+
+def test_version_and_status_strings():
+    assert sp.version() == "0.1.0"
+    for code in sp.STATUS:
+        assert sp.LIB.spear_status_string(code)
+    assert sp.LIB.spear_status_string(12345) == b"unknown status"
+
+
+def _plan(**kw):
+    args = dict(M=1, N=2048, K=2048, group_size=128, act_dtype=sp.F16, rank=16,
+                gate_kind=sp.GATE_SIGMOID_LINEAR)
+    args.update(kw)
+    with_ec = args.pop("with_ec", True)
+    return sp.dispatch_plan(sp.problem(**args), with_ec)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(K=100), -2), (dict(K=0), -2), (dict(K=192), -2), (dict(M=-1), -2), (dict(N=-3), -2),
+    (dict(group_size=64), -2), (dict(group_size=384), -2), (dict(group_size=96), -2),
+    (dict(act_dtype=2), -3), (dict(rank=257), -2), (dict(rank=-1), -2),
+    (dict(gate_kind=3), -6), (dict(gate_hidden=-1), -2), (dict(gate_hidden=2048), -2),
+    (dict(force_path=7), -6), (dict(force_path=sp.PATH_FUSED_MFMA), -6),
+    (dict(force_path=sp.PATH_FUSED_GEMV, M=65), -6),
+    (dict(M=1 << 20, K=1 << 12), -2),
+])
+def test_plan_validation(kw, code):
+    with pytest.raises(sp.SpearError) as e:
+        _plan(**kw)
+    assert e.value.status == code
+
+
+def test_plan_rejects_null():
+    out = sp.Plan()
+    assert sp.LIB.spear_dispatch_plan(None, 1, ctypes.byref(out)) == -1
+    assert sp.LIB.spear_dispatch_plan(ctypes.byref(sp.problem(1, 1, 128)), 1, None) == -1
+
+
+def test_plan_phase_aware_dispatch():
+    """Decode token counts get the single fused kernel, prefill the semi-fused
+    pre-kernel + GEMM (section 4.1)."""
+    for M in (1, 4, 16, 17, 32, 64):
+        p = _plan(M=M)
+        assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
+    for M in (65, 512, 4096):
+        p = _plan(M=M)
+        assert p.path == sp.PATH_UNFUSED_2K and p.num_launches == 2, M
+    assert _plan(M=4, force_path=sp.PATH_UNFUSED_CHAIN).num_launches == 4
+    assert _plan(M=4096, force_path=sp.PATH_UNFUSED_CHAIN).num_launches == 4
+    assert _plan(M=4, force_path=sp.PATH_UNFUSED_2K).num_launches == 2
+
+
+def test_plan_is_deterministic_and_sized():
+    a, b = _plan(M=16).as_dict(), _plan(M=16).as_dict()
+    assert a == b
+    # rank 0 or no EC -> no EC launches; the 4-bit plan matches
+    assert _plan(M=1, rank=0).num_launches == 1
+    assert _plan(M=1, with_ec=False).ec_splits == 0
+    # empty problems are legal no-ops
+    assert _plan(M=0).num_launches == 0 and _plan(N=0).num_launches == 0
+    # workspace grows with the token count at fixed shape
+    ws = [_plan(M=M).workspace_bytes for M in (1, 8, 16, 64, 128, 1024, 4096)]
+    assert all(w > 0 for w in ws)
+    # split-K never exceeds the number of 128-wide K iterations
+    for K in (128, 256, 2048, 28672):
+        p = _plan(M=1, K=K, N=512)
+        assert 1 <= p.split_k <= K // 128
+        assert 1 <= p.ec_splits <= K // 128
+
+
+def _call_ec(prob, x=None, y=None, q=None, s=None, z=None, A=None, B=None, w_g=None, ws=None,
+             ws_bytes=0):
+    w = sp.W4(q, s, z)
+    ec = sp.EC(A, B, 1.0, w_g, 0.0, None, None, None, None)
+    return sp.LIB.spear_w4ec_linear(ctypes.byref(prob), x, ctypes.byref(w), ctypes.byref(ec), y,
+                                    ws, ws_bytes, None)
+
+
+# fake but distinct, 16-byte aligned addresses: every call below is rejected on
+# the host before anything touches them
+BASE = 0x7F0000000000
+ADDR = {k: BASE + i * (1 << 32) for i, k in enumerate("xyqszABwW")}
+
+
+def test_null_pointers_rejected():
+    prob = sp.problem(4, 256, 256, 0, sp.F16, 8)
+    assert _call_ec(prob) == -1
+    full = dict(x=ADDR["x"], y=ADDR["y"], q=ADDR["q"], s=ADDR["s"], z=ADDR["z"], A=ADDR["A"],
+                B=ADDR["B"], w_g=ADDR["w"], ws=ADDR["W"], ws_bytes=1 << 30)
+    for k in ("x", "y", "q", "s", "z", "A", "B", "w_g"):
+        args = dict(full)
+        args[k] = None
+        assert _call_ec(prob, **args) == -1, k
+
+
+def test_misaligned_pointers_rejected():
+    prob = sp.problem(4, 256, 256, 0, sp.F16, 8)
+    full = dict(x=ADDR["x"], y=ADDR["y"], q=ADDR["q"], s=ADDR["s"], z=ADDR["z"], A=ADDR["A"],
+                B=ADDR["B"], w_g=ADDR["w"], ws=ADDR["W"], ws_bytes=1 << 30)
+    for k in ("x", "y", "q", "s", "z", "A", "B", "w_g", "ws"):
+        args = dict(full)
+        args[k] = args[k] + 8
+        assert _call_ec(prob, **args) == -4, k
+
+
+def test_alias_rejected():
+    prob = sp.problem(4, 256, 256, 0, sp.F16, 8)
+    full = dict(x=ADDR["x"], y=ADDR["y"], q=ADDR["q"], s=ADDR["s"], z=ADDR["z"], A=ADDR["A"],
+                B=ADDR["B"], w_g=ADDR["w"], ws=ADDR["W"], ws_bytes=1 << 30)
+    for k in ("x", "q", "s", "z", "A", "B", "w_g", "ws"):
+        args = dict(full)
+        args["y"] = args[k] + 16
+        assert _call_ec(prob, **args) == -8, k
+
+
+def test_workspace_checked():
+    prob = sp.problem(4, 256, 256, 0, sp.F16, 8)
+    need = sp.dispatch_plan(prob, True).workspace_bytes
+    assert need > 0
+    full = dict(x=ADDR["x"], y=ADDR["y"], q=ADDR["q"], s=ADDR["s"], z=ADDR["z"], A=ADDR["A"],
+                B=ADDR["B"], w_g=ADDR["w"])
+    assert _call_ec(prob, ws=None, ws_bytes=0, **full) == -5
+    assert _call_ec(prob, ws=ADDR["W"], ws_bytes=need - 1, **full) == -5
+
+
+def test_gate_parameters_required():
+    prob = sp.problem(4, 256, 256, 0, sp.F16, 8, sp.GATE_TANH_MLP)
+    w = sp.W4(ADDR["q"], ADDR["s"], ADDR["z"])
+    ec = sp.EC(ADDR["A"], ADDR["B"], 1.0, None, 0.0, None, None, None, None)
+    st = sp.LIB.spear_w4ec_linear(ctypes.byref(prob), ADDR["x"], ctypes.byref(w), ctypes.byref(ec),
+                                  ADDR["y"], ADDR["W"], 1 << 30, None)
+    assert st == -1
+
+
+def test_dequant_validation():
+    prob = sp.problem(0, 256, 100, 0, sp.F16)
+    w = sp.W4(ADDR["q"], ADDR["s"], ADDR["z"])
+    assert sp.LIB.spear_w4_dequant(ctypes.byref(prob), ctypes.byref(w), ADDR["y"], None) == -2
+    prob = sp.problem(0, 256, 256, 0, sp.F16)
+    assert sp.LIB.spear_w4_dequant(ctypes.byref(prob), ctypes.byref(w), None, None) == -1
+    assert sp.LIB.spear_w4_dequant(ctypes.byref(prob), ctypes.byref(w), ADDR["y"] + 2, None) == -4
+    assert sp.LIB.spear_w4_dequant(ctypes.byref(prob), ctypes.byref(w), ADDR["q"], None) == -8
+    # N == 0 is a no-op that succeeds without touching anything
+    prob = sp.problem(0, 0, 256, 0, sp.F16)
+    assert sp.LIB.spear_w4_dequant(ctypes.byref(prob), ctypes.byref(w), None, None) == 0
+
+
+def test_empty_problem_is_noop():
+    prob = sp.problem(0, 256, 256, 0, sp.F16, 8)
+    assert _call_ec(prob) == 0
+    prob = sp.problem(4, 0, 256, 0, sp.F16, 8)
+    assert _call_ec(prob) == 0
+
+
+def test_wait_poll_hook_roundtrip():
+    old = sp.set_wait_polls(5)
+    assert sp.set_wait_polls(old) == 5

@@ -1,0 +1,227 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+The bar: int4 unpack/dequant bit-exact; outputs within relative Frobenius
+error 5e-3 and max |d| <= 1e-2 * max |y_ref|. Inputs are seeded synthetic
+layers from paper_2606_11244_amd.synth.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import spear_oracle as O
+from paper_2606_11244_amd import synth as S
+
+from gpu_util import assert_parity, gpu_y, log, scaled_ec, with_fields, zero_weight
+
+pytestmark = pytest.mark.gpu
+
+PATHS = {"auto": 0, "fused_gemv": 1, "chain": 3, "2k": 4}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_11244_amd import spear  # noqa: F401  (fails loudly if not built)
+    yield
+
+
+def _paths_for(M):
+    return [p for name, p in PATHS.items() if not (name == "fused_gemv" and M > 64)]
+
+
+# ---------------------------------------------------------------------------
+# bit-exact dequantisation
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dt", [S.F16, S.BF16])
+@pytest.mark.parametrize("G", [128, 0])
+def test_dequant_bit_exact(dt, G):
+    from paper_2606_11244_amd import spear as sp
+    rng = np.random.default_rng(7)
+    N, K = 16 * 16, 256
+    g = K if G == 0 else G
+    # every code against every zero point, random fp16 scales (incl. subnormal-producing ones)
+    q = np.tile(np.arange(16), (N, K // 16))
+    z = np.repeat(np.arange(16), 16)[:, None].repeat(K // g, axis=1).astype(np.uint8)
+    s = rng.choice([rng.uniform(1e-5, 1e-3), rng.uniform(1e-3, 2.0)], size=(N, K // g))
+    s = np.where(rng.random((N, K // g)) < 0.2, 6e-8, s).astype(np.float16)
+    qw = S.pack_int4(q)
+    want = O.dequant_bits(qw, s.view(np.uint16), z, g, dt)
+    log(f"dequant dt={dt} G={g}")
+    dq = torch.from_numpy(qw.view(np.int32)).cuda()
+    ds = torch.from_numpy(s.view(np.int16)).cuda()
+    dz = torch.from_numpy(z).cuda()
+    out = torch.empty((N, K), dtype=torch.int16, device="cuda")
+    sp.w4_dequant(sp.problem(0, N, K, G, dt), dq, ds, dz, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, want), f"{(got != want).sum()} mismatching bits"
+
+
+# ---------------------------------------------------------------------------
+# small configurations, every path
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("path", list(PATHS))
+def test_tiny_config(seed, path):
+    """K=256, N=256, M=4, per-channel, r=8, sigmoid-linear gate, fp16."""
+    L = S.config_layer(0, "tiny", 4, seed=seed)
+    log(f"tiny seed={seed} path={path}")
+    assert_parity(gpu_y(L, PATHS[path]), O.w4ec_linear(L), f"tiny/{path}/{seed}")
+
+
+@pytest.mark.parametrize("M", [1, 2, 3, 5, 15, 16, 17, 31, 33, 48, 64, 65, 127, 129, 255])
+def test_token_counts(M):
+    """Ragged token counts across the GEMV/GEMM boundary; N not a tile multiple."""
+    L = S.make_layer(M=M, N=320, K=512, group_size=128, rank=16, seed=M)
+    ref = O.w4ec_linear(L)
+    for p in _paths_for(M):
+        log(f"M={M} path={p}")
+        assert_parity(gpu_y(L, p), ref, f"M={M} path={p}")
+
+
+@pytest.mark.parametrize("N", [1, 15, 17, 200, 1000])
+@pytest.mark.parametrize("M", [1, 16, 100])
+def test_ragged_rows(N, M):
+    L = S.make_layer(M=M, N=N, K=384, group_size=128, rank=8, seed=N + M)
+    ref = O.w4ec_linear(L)
+    for p in _paths_for(M):
+        log(f"N={N} M={M} path={p}")
+        assert_parity(gpu_y(L, p), ref, f"N={N} M={M} path={p}")
+
+
+@pytest.mark.parametrize("gate", [S.GATE_ONE, S.GATE_SIGMOID_LINEAR, S.GATE_TANH_MLP])
+@pytest.mark.parametrize("dt", [S.F16, S.BF16])
+@pytest.mark.parametrize("M", [1, 8, 40, 200])
+def test_gates_and_dtypes(gate, dt, M):
+    L = S.make_layer(M=M, N=256, K=1024, group_size=0 if dt == S.BF16 else 128, rank=16,
+                     act_dtype=dt, gate_kind=gate, seed=3, ec_std=0.05)
+    ref = O.w4ec_linear(L)
+    for p in _paths_for(M):
+        log(f"gate={gate} dt={dt} M={M} path={p}")
+        assert_parity(gpu_y(L, p), ref, f"gate={gate} dt={dt} M={M} path={p}")
+
+
+@pytest.mark.parametrize("r", [0, 1, 7, 8, 16, 32, 64, 100, 256])
+@pytest.mark.parametrize("M", [3, 130])
+def test_ranks(r, M):
+    L = S.make_layer(M=M, N=192, K=512, group_size=128, rank=r, seed=r, ec_std=0.05,
+                     gate_kind=S.GATE_TANH_MLP if r in (7, 100) else S.GATE_SIGMOID_LINEAR)
+    ref = O.w4ec_linear(L)
+    for p in _paths_for(M):
+        log(f"r={r} M={M} path={p}")
+        assert_parity(gpu_y(L, p), ref, f"r={r} M={M} path={p}")
+
+
+# ---------------------------------------------------------------------------
+# cases that isolate the EC term (it is ~1% of y at the workload scales)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dt", [S.F16, S.BF16])
+@pytest.mark.parametrize("M", [1, 16, 300])
+@pytest.mark.parametrize("gate", [S.GATE_SIGMOID_LINEAR, S.GATE_TANH_MLP])
+def test_ec_isolated_zero_weight(dt, M, gate):
+    """q == z everywhere: W_hat == 0 exactly, so y is the EC term alone."""
+    L = zero_weight(S.make_layer(M=M, N=256, K=1024, group_size=128, rank=16, act_dtype=dt,
+                                 gate_kind=gate, seed=11))
+    ref = O.w4ec_linear(L)
+    assert np.abs(O.w4_linear_layer(L)).max() == 0.0
+    for p in _paths_for(M):
+        log(f"zero-weight dt={dt} M={M} gate={gate} path={p}")
+        assert_parity(gpu_y(L, p), ref, f"zero-weight dt={dt} M={M} gate={gate} path={p}")
+
+
+@pytest.mark.parametrize("M", [2, 16, 257])
+def test_ec_scaled_x30(M):
+    L = scaled_ec(S.make_layer(M=M, N=512, K=2048, group_size=128, rank=16, seed=5), 30.0)
+    ref = O.w4ec_linear(L)
+    for p in _paths_for(M):
+        log(f"x30 M={M} path={p}")
+        assert_parity(gpu_y(L, p), ref, f"x30 M={M} path={p}")
+
+
+@pytest.mark.parametrize("M", [4, 200])
+def test_gate_pinned_values(M):
+    """b_g = -1e4 gives g = 0 (y = the plain 4-bit product); w_g = 0, b_g = 0
+    gives g = 1/2 exactly."""
+    L = S.make_layer(M=M, N=256, K=1024, group_size=128, rank=16, seed=9, ec_std=0.2)
+    off = with_fields(L, b_g=-1.0e4)
+    half = with_fields(L, w_g=np.zeros_like(L.w_g), b_g=0.0)
+    y_w4 = gpu_y(L, 0, with_ec=False)
+    for p in _paths_for(M):
+        log(f"gate-pinned M={M} path={p}")
+        assert_parity(gpu_y(off, p), O.w4_linear_layer(L), f"g=0 M={M} path={p}")
+        assert_parity(gpu_y(half, p), O.w4ec_linear(half), f"g=1/2 M={M} path={p}")
+    assert_parity(y_w4, O.w4_linear_layer(L), "w4_linear")
+
+
+@pytest.mark.parametrize("M", [1, 9, 64, 100])
+def test_rank0_equals_w4_linear(M):
+    """rank 0 runs exactly the 4-bit kernel: bit-identical to spear_w4_linear."""
+    L = S.make_layer(M=M, N=384, K=1024, group_size=128, rank=0, seed=2)
+    a = gpu_y(L, 0, with_ec=True)
+    b = gpu_y(L, 0, with_ec=False)
+    assert np.array_equal(a, b)
+    assert_parity(a, O.w4_linear_layer(L), f"r=0 M={M}")
+
+
+# ---------------------------------------------------------------------------
+# robustness of the fused path's cross-workgroup machinery
+# ---------------------------------------------------------------------------
+
+def test_fused_wait_fallback():
+    """With a zero poll budget every workgroup computes the EC itself: the
+    result must still meet the bar."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=5, N=1024, K=2048, group_size=128, rank=32, seed=4, ec_std=0.05)
+    ref = O.w4ec_linear(L)
+    old = sp.set_wait_polls(0)
+    try:
+        log("fallback fused")
+        y = gpu_y(L, PATHS["fused_gemv"])
+    finally:
+        sp.set_wait_polls(old)
+    assert_parity(y, ref, "fused fallback")
+
+
+def test_deterministic_and_stale_workspace():
+    """Repeated calls are bit-identical (fixed reduction orders), also when the
+    workspace holds garbage from elsewhere (epoch-tagged counters)."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=3, N=2048, K=4096, group_size=128, rank=16, seed=6)
+    dl = sp.DeviceLayer(L)
+    prob = dl.problem(force_path=PATHS["fused_gemv"])
+    plan = sp.dispatch_plan(prob)
+    assert plan.split_k > 1 and plan.ec_splits > 1
+    ws = sp.allocate_workspace(prob)
+    log("determinism")
+    first = gpu_y(L, PATHS["fused_gemv"], workspace=ws, dev=dl)
+    for i in range(5):
+        if i % 2:
+            ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, device="cuda"))
+        again = gpu_y(L, PATHS["fused_gemv"], workspace=ws, dev=dl)
+        assert np.array_equal(first, again), i
+    assert_parity(first, O.w4ec_linear(L), "determinism")
+
+
+def test_streams_and_reuse():
+    """Calls on a side stream, back to back with different shapes on one
+    workspace sized for the largest."""
+    from paper_2606_11244_amd import spear as sp
+    s = torch.cuda.Stream()
+    layers = [S.make_layer(M=M, N=512, K=1024, group_size=128, rank=16, seed=M) for M in (1, 7, 16)]
+    devs = [sp.DeviceLayer(L) for L in layers]
+    wsz = max(sp.dispatch_plan(d.problem()).workspace_bytes for d in devs)
+    ws = torch.zeros(wsz, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            for d in devs:
+                d.run_ec(d.problem(), ws, stream=s)
+    s.synchronize()
+    for L, d in zip(layers, devs):
+        assert_parity(d.y.float().cpu().numpy(), O.w4ec_linear(L), f"stream M={L.M}")
