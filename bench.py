@@ -1,0 +1,309 @@
+"""Benchmark of the W4+EC linear layer on one MI355X.
+
+One step = one pass of the hot path over one batch of synthetic input on a
+Llama-3.2-1B-shaped model (hidden 2048, MLP 8192; q, k, v, o, gate, up, down
+per layer; group-128 4-bit weights, EC rank 16 with the sigmoid-linear gate,
+fp16 activations):
+
+  decode   M = 1: all 16 layers x 7 modules through the automatic dispatch
+           (the fused single-kernel path). Two distinct copies of the model
+           weights alternate between steps (2 x 0.53 GB), so the weights come
+           from HBM rather than the 256 MB Infinity Cache.
+  prefill  M = 4096 tokens (1% of input channels scaled x20): the 7 modules of
+           one layer through the automatic dispatch (EC pre-kernel + 4-bit
+           GEMM with the EC in its epilogue).
+
+Both passes are captured once as HIP graphs and replayed. The printed JSON
+line reports decode HBM throughput (algorithmic bytes / time) as `value`, the
+prefill MFMA throughput under `prefill`, each with its roofline, the EC
+overhead over the same passes without EC, and the CPU oracle timed on a
+bounded sample (`cpu_baseline`).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "W4+EC linear TFLOP/s & HBM GB/s (% roofline) decode M=1 + prefill M=4096"
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 MFMA
+LAYERS_1B = 16
+RANK = 16
+GROUP = 128
+
+
+def algo_bytes(M, N, K, G, r):
+    """Algorithmic HBM bytes of one W4+EC call: codes (N K / 2), scales and
+    4-bit zeros (2.5 N K / G), A, B, w_g, X and Y in fp16."""
+    return N * K / 2 + 2.5 * N * K / G + 2 * r * K + 2 * N * r + (2 * K if r else 0) + 2 * M * K + 2 * M * N
+
+
+def algo_flops(M, N, K, r):
+    return 2 * M * N * K + (2 * M * K * (r + 1) + 2 * M * N * r if r else 0)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("spear_kernels.hip", "spear_api.cpp", "spear_internal.h"):
+        with open(os.path.join(ROOT, "paper_2606_11244_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic():
+    """HBM traffic per launch measured with rocprofv3 counters for the current
+    kernel sources, if such a measurement is stored under profiles/."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return d
+
+
+def cpu_baseline(dec_layers, pre_layer, budget_s=12.0):
+    """The float64 oracle on the host cores: the 7 decode modules of one layer
+    (repeated), and one prefill module (q, M=4096)."""
+    import numpy as np
+    from oracle import spear_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        blas = 1
+    reps, t_dec, nbytes = 0, 0.0, 0.0
+    t0 = time.perf_counter()
+    while reps < 1 or (time.perf_counter() - t0 < budget_s * 0.6 and reps < 8):
+        for L in dec_layers:
+            ts = time.perf_counter()
+            y = O.w4ec_linear(L)
+            t_dec += time.perf_counter() - ts
+            nbytes += algo_bytes(L.M, L.N, L.K, L.group_size, L.rank)
+            assert np.isfinite(y).all()
+        reps += 1
+    ts = time.perf_counter()
+    O.w4ec_linear(pre_layer)
+    t_pre = time.perf_counter() - ts
+    L = pre_layer
+    return {
+        "value": round(nbytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": int(blas),
+        "kind": "oracle",
+        "sample": (f"float64 numpy oracle: one 1B-shaped layer (7 modules, M=1) x {reps} "
+                   f"({nbytes / 1e6:.0f} MB algorithmic, {t_dec:.1f} s); prefill q module "
+                   f"M={L.M} ({t_pre:.1f} s)"),
+        "prefill_tflops": round(algo_flops(L.M, L.N, L.K, L.rank) / t_pre / 1e12, 5),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--copies", type=int, default=2, help="decode weight copies rotated per step")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-overhead", action="store_true", help="skip the W4-only reference passes")
+    ap.add_argument("--copy-calib-mb", type=int, default=0,
+                    help="also run one device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the W4+EC layer is built and timed on a single "
+              "MI355X (multi-GPU runs are out of scope); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_11244_amd import spear as sp
+    from paper_2606_11244_amd import synth as S
+
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    print("bench: generating layers", file=sys.stderr, flush=True)
+    dec_base = [S.config_layer(1, m, 1, seed=0) for m in S.MODULES]
+    pre_base = [S.config_layer(2, m, 4096, seed=0) for m in S.MODULES]
+
+    # ---- decode: copies x layers x modules, each with its own weights in HBM
+    dec_dev = []  # [copy][layer][module] DeviceLayer
+    base_dev = [sp.DeviceLayer(L, device=dev) for L in dec_base]
+    for c in range(args.copies):
+        per_copy = []
+        for _l in range(LAYERS_1B):
+            mods = []
+            for b in base_dev:
+                d = sp.DeviceLayer.__new__(sp.DeviceLayer)
+                d.__dict__.update(b.__dict__)
+                d.qweight = b.qweight.clone()
+                d.scales = b.scales.clone()
+                d.zeros = b.zeros.clone()
+                d.A, d.B, d.w_g = b.A.clone(), b.B.clone(), b.w_g.clone()
+                mods.append(d)
+            per_copy.append(mods)
+        dec_dev.append(per_copy)
+    dec_ws = max(sp.dispatch_plan(d.problem()).workspace_bytes for d in base_dev)
+    dec_ws_t = torch.zeros(max(dec_ws, 256), dtype=torch.uint8, device=dev)
+    pre_dev = [sp.DeviceLayer(L, device=dev) for L in pre_base]
+    pre_ws = max(sp.dispatch_plan(d.problem()).workspace_bytes for d in pre_dev)
+    pre_ws_t = torch.zeros(max(pre_ws, 256), dtype=torch.uint8, device=dev)
+    w4_ws = max(sp.dispatch_plan(d.problem(), with_ec=False).workspace_bytes
+                for d in base_dev + pre_dev)
+    w4_ws_t = torch.zeros(max(w4_ws, 256), dtype=torch.uint8, device=dev)
+
+    dec_bytes = LAYERS_1B * sum(algo_bytes(1, L.N, L.K, L.group_size, L.rank) for L in dec_base)
+    dec_bytes_w4 = LAYERS_1B * sum(algo_bytes(1, L.N, L.K, L.group_size, 0) for L in dec_base)
+    pre_flops = sum(algo_flops(L.M, L.N, L.K, L.rank) for L in pre_base)
+    pre_flops_w4 = sum(algo_flops(L.M, L.N, L.K, 0) for L in pre_base)
+    dec_plan = sp.dispatch_plan(base_dev[0].problem())
+    pre_plan = sp.dispatch_plan(pre_dev[0].problem())
+
+    def decode_pass(c, ec=True):
+        for mods in dec_dev[c]:
+            for d in mods:
+                if ec:
+                    d.run_ec(d.problem(), dec_ws_t)
+                else:
+                    d.run_w4(d.problem(), w4_ws_t)
+
+    def prefill_pass(ec=True):
+        for d in pre_dev:
+            if ec:
+                d.run_ec(d.problem(), pre_ws_t)
+            else:
+                d.run_w4(d.problem(), w4_ws_t)
+
+    def capture(fn):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            fn()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        torch.cuda.synchronize()
+        return g
+
+    print("bench: capturing graphs", file=sys.stderr, flush=True)
+    g_dec = [capture(lambda c=c: decode_pass(c)) for c in range(args.copies)]
+    g_pre = capture(prefill_pass)
+
+    def run_steps(n, gdec, gpre, timed):
+        ev = []
+        for i in range(n):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e2 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            gdec[i % len(gdec)].replay()
+            e1.record()
+            gpre.replay()
+            e2.record()
+            ev.append((e0, e1, e2))
+        return ev
+
+    print("bench: warmup", file=sys.stderr, flush=True)
+    run_steps(args.warmup, g_dec, g_pre, False)
+    torch.cuda.synchronize()
+    print("bench: timed steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    ev = run_steps(args.steps, g_dec, g_pre, True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    t_dec = np.array([a.elapsed_time(b) for a, b, _ in ev]) * 1e-3
+    t_pre = np.array([b.elapsed_time(c) for _, b, c in ev]) * 1e-3
+    dec_s = float(np.mean(t_dec))
+    pre_s = float(np.mean(t_pre))
+    dec_gbs = dec_bytes / dec_s / 1e9
+    pre_tfl = pre_flops / pre_s / 1e12
+
+    overhead = None
+    if not args.no_overhead:
+        print("bench: W4-only reference passes", file=sys.stderr, flush=True)
+        g_dec_w4 = [capture(lambda c=c: decode_pass(c, ec=False)) for c in range(args.copies)]
+        g_pre_w4 = capture(lambda: prefill_pass(ec=False))
+        run_steps(args.warmup, g_dec_w4, g_pre_w4, False)
+        ev4 = run_steps(args.steps, g_dec_w4, g_pre_w4, True)
+        torch.cuda.synchronize()
+        d4 = float(np.mean([a.elapsed_time(b) for a, b, _ in ev4])) * 1e-3
+        p4 = float(np.mean([b.elapsed_time(c) for _, b, c in ev4])) * 1e-3
+        overhead = {
+            "decode": round(dec_s / d4 - 1.0, 4), "prefill": round(pre_s / p4 - 1.0, 4),
+            "decode_w4_only_GBps": round(dec_bytes_w4 / d4 / 1e9, 1),
+            "prefill_w4_only_TFLOPs": round(pre_flops_w4 / p4 / 1e12, 1),
+            "decode_ec_byte_share": round(dec_bytes / dec_bytes_w4 - 1.0, 4),
+        }
+
+    if args.copy_calib_mb:
+        n = args.copy_calib_mb << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    traffic = stored_traffic()
+    n_launch_dec = LAYERS_1B * len(S.MODULES)
+    result = {
+        "metric": METRIC,
+        "value": round(dec_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": ("llama-3.2-1b-shaped W4+EC linear layers (q,k,v,o 2048->2048/512, "
+                         "gate/up 2048->8192, down 8192->2048): decode M=1 over 16 layers x 7 "
+                         "modules + prefill M=4096 over 7 modules"),
+            "group_size": GROUP, "rank": RANK, "gate": "sigmoid_linear",
+            "decode_path": sp.PATH_NAMES[dec_plan.path], "prefill_path": sp.PATH_NAMES[pre_plan.path],
+            "decode_weight_copies": args.copies,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_gemv (fused W4+EC decode), all launches of the decode pass",
+            "achieved": round(dec_bytes / n_launch_dec / (dec_s / n_launch_dec) / 1e9, 2),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+            "traffic": (traffic or {}).get("decode_bytes_per_launch"),
+            "algo_bytes_per_launch": round(dec_bytes / n_launch_dec),
+            "avg_launch_us": round(dec_s / n_launch_dec * 1e6, 3),
+        },
+        "prefill": {
+            "value": round(pre_tfl, 2), "unit": "TFLOP/s", "ms_per_pass": round(pre_s * 1e3, 4),
+            "roofline": {
+                "bound": "mfma",
+                "kernel": "k_ec pre-kernel + k_gemm (EC epilogue), 7 modules",
+                "achieved": round(pre_tfl, 2), "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(pre_tfl / MFMA_F16_PEAK_TFLOPS, 4),
+                "traffic": (traffic or {}).get("prefill_bytes_per_launch"),
+            },
+        },
+        "decode_ms_per_pass": round(dec_s * 1e3, 4),
+        "ec_overhead": overhead,
+    }
+    if not args.no_cpu_baseline:
+        print("bench: CPU oracle baseline", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(dec_base, pre_base[0])
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -36,10 +36,10 @@
  *     means the default stream) and returns without synchronising.
  *   - Workspace: calls that need scratch take a caller-owned device buffer
  *     of at least spear_dispatch_plan()'s workspace_bytes. It must be
- *     zero-filled once before its first use; the kernels leave it reusable
- *     (counters carry a per-call epoch, so stale contents cannot corrupt a
- *     later call). Two calls that overlap in time must not share one
- *     workspace.
+ *     zero-filled once before its first use; every call returns its
+ *     counters to zero, so the same workspace serves any later call (of any
+ *     shape it is large enough for) and replays of a captured graph. Two
+ *     calls that overlap in time must not share one workspace.
  */
 #ifndef SPEAR_H
 #define SPEAR_H
@@ -169,9 +169,18 @@ spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w
 
 /* Test hook for the fused path's bounded wait: the number of polls a
  * workgroup makes for the EC coordinates before computing them itself
- * (default 1 << 20; 0 forces every workgroup onto that self-computing
+ * (default 1 << 16; 0 forces every workgroup onto that self-computing
  * fallback). Process-wide; returns the previous value. */
 int32_t spear_set_wait_polls(int32_t polls);
+
+/* Tuning hook for the decode GEMV's launch shape, process-wide: 16-row
+ * tiles per workgroup, 128-wide K iterations per wave, activations staged in
+ * LDS (1), loaded per wave (0) or chosen automatically (-1), and waves per
+ * workgroup. 0 (or -1 for x_in_lds) restores the planner's choice for that
+ * field. A combination that is not compiled in makes the planner and the
+ * calls return SPEAR_E_UNSUPPORTED. For measurement sweeps only. */
+void spear_set_gemv_shape(int32_t row_tiles, int32_t iters_per_wave, int32_t x_in_lds,
+                          int32_t waves);
 
 /* Static text for a status code. */
 const char* spear_status_string(spear_status_t status);

@@ -16,7 +16,10 @@ using namespace spear;
 namespace {
 
 std::atomic<uint32_t> g_epoch{0};
-std::atomic<int32_t> g_wait_polls{1 << 20};
+std::atomic<int32_t> g_wait_polls{1 << 16};
+// tuning override of the GEMV shape (0 = automatic): row tiles, iterations
+// per wave, x staged in LDS (1) or not (0, -1 = automatic), waves per block
+std::atomic<int32_t> g_ov_rt{0}, g_ov_u{0}, g_ov_xl{-1}, g_ov_nw{0};
 
 // Every call gets a fresh non-zero epoch (a zero-filled workspace holds epoch 0).
 uint32_t next_epoch() {
@@ -39,8 +42,10 @@ struct Resolved {
   spear_plan_t plan;
   bool ec, gemv;
   int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
-  int MT, RT, nrb, S, ips, ntb, P, eips, n_prod;
-  size_t off_flag, off_ectr, off_rbctr, off_upart, off_v, off_vh, off_vl, off_u, off_ypart;
+  int MT, RT, U, NW, nrg, S, ips, ntb, P, eips, n_prod, ec_block;
+  bool XL;
+  size_t off_gen, off_vtag, off_ectr, off_done, off_rbctr, off_upart, off_v, off_vh, off_vl, off_u,
+      off_ypart;
   size_t lds_gemv, lds_ec;
 };
 
@@ -52,8 +57,9 @@ spear_status_t validate_shape(const spear_problem_t* p, bool with_ec) {
   if (p->act_dtype != SPEAR_F16 && p->act_dtype != SPEAR_BF16) return SPEAR_E_DTYPE;
   const int64_t G = (p->group_size == 0) ? p->K : p->group_size;
   if (G <= 0 || G % kIterK || p->K % G) return SPEAR_E_SHAPE;
-  // element counts stay below 2^31 so that row indexing inside kernels is int
-  const int64_t lim = (int64_t)1 << 31;
+  // every buffer stays below 2 GiB (element counts below 2^30), so that the
+  // kernels' 32-bit byte offsets and buffer-resource bounds cover it
+  const int64_t lim = (int64_t)1 << 30;
   if (p->M * p->K >= lim || p->N * p->K >= lim || p->M * p->N >= lim) return SPEAR_E_SHAPE;
   if (p->force_path < SPEAR_PATH_AUTO || p->force_path > SPEAR_PATH_UNFUSED_2K)
     return SPEAR_E_UNSUPPORTED;
@@ -100,72 +106,103 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
 
   // 4-bit product shape
   if (z.gemv) {
+    // A block owns RT 16-row tiles and a K-slice of NW * U iterations (128 K
+    // each); x goes through LDS for at most 4 tokens. Blocks are sized so
+    // that the grid covers the 256 CUs where the layer allows it.
     z.MT = (int)cdiv(M, 16);
-    z.RT = z.MT == 1 ? 4 : (z.MT == 2 ? 2 : 1);
-    const int RB = 16 * z.RT;
-    z.nrb = (int)cdiv(N, RB);
-    int S = (int)cdiv(kTargetBlocks, z.nrb);
-    S = std::min(S, std::max(1, z.IT / 4));
-    S = std::min<int64_t>(S, std::max<int64_t>(1, K / (32 * M)));
-    S = std::max(S, 1);
-    z.ips = (int)cdiv(z.IT, S);
+    z.NW = 16;
+    z.XL = M <= 4;
+    if (z.MT == 1) {
+      z.U = z.IT <= 16 ? 1 : (z.IT <= 32 ? 2 : 4);
+      if (!z.XL && z.U == 4) z.U = 2;
+    } else if (z.MT == 2) {
+      z.U = z.IT <= 16 ? 1 : 2;
+    } else {
+      z.U = 1;
+    }
+    const int S0 = (int)cdiv(z.IT, z.NW * z.U);
+    z.RT = 1;
+    for (int rt : {4, 2}) {
+      if (gemv_shape_supported(z.MT, rt, z.U, z.XL) && cdiv(N, 16 * rt) * S0 >= 256) {
+        z.RT = rt;
+        break;
+      }
+    }
+    if (g_ov_rt.load() > 0) z.RT = g_ov_rt.load();
+    if (g_ov_u.load() > 0) z.U = g_ov_u.load();
+    if (g_ov_xl.load() >= 0) z.XL = g_ov_xl.load() != 0 && M <= 4;
+    if (g_ov_nw.load() > 0) z.NW = std::min(16, g_ov_nw.load());
+    if (!gemv_shape_supported(z.MT, z.RT, z.U, z.XL)) return SPEAR_E_UNSUPPORTED;
+    z.ips = z.NW * z.U;
     z.S = (int)cdiv(z.IT, z.ips);
-    const int ngs_max = (int)std::min<int64_t>(z.ngroups, cdiv((int64_t)z.ips * kIterK, z.G) + 1);
-    z.lds_gemv = gemv_lds_e_off(ngs_max, z.RT, z.MT);
+    z.nrg = (int)cdiv(N, 16 * z.RT);
+    z.lds_gemv = gemv_lds_e_off(z.NW, z.RT, z.MT, z.XL ? (int)M : 0, z.ips);
     z.plan.split_k = z.S;
     z.plan.tile_m = 16 * z.MT;
-    z.plan.tile_n = RB;
+    z.plan.tile_n = 16 * z.RT;
   } else {
     z.plan.split_k = 1;
     z.plan.tile_m = kGemmTM;
     z.plan.tile_n = kGemmTN;
   }
 
-  // EC projection shape
+  // EC projection shape: per 16-token tile, K-slices of at most 64 iterations
+  // (16 waves x 4); decode blocks use up to 16 waves, prefill blocks 4 waves
+  // over many token tiles
   z.ntb = (int)cdiv(M, kTokTile);
   if (z.ec) {
     if (z.gemv) {
-      const double a_bytes = (double)z.R1 * K * 2;
-      const double w_per_block = (double)N * K / 2 / std::max(1, z.nrb * z.S);
-      int P = (int)std::ceil(a_bytes / std::max(1.0, w_per_block));
-      P = std::max(1, std::min(P, z.IT));
-      z.eips = (int)cdiv(z.IT, P);
+      z.ec_block = (path == SPEAR_PATH_FUSED_GEMV) ? 64 * z.NW : 1024;
+      const int per_block = 4 * (z.ec_block / 64);
+      z.P = (int)cdiv(z.IT, per_block);
+      z.eips = (int)cdiv(z.IT, z.P);
       z.P = (int)cdiv(z.IT, z.eips);
     } else {
+      z.ec_block = 256;
       z.P = 1;
       z.eips = z.IT;
     }
     z.lds_ec = ec_lds_bytes(z.R1p, z.h, z.r);
-    if (z.gemv) z.lds_gemv += z.lds_ec;
+    // EC block carve-up, then the epilogue's prefetched rows of B
+    if (z.gemv) z.lds_gemv += z.lds_ec + align_up((size_t)16 * z.RT * z.r * 2, 16);
   }
   z.plan.ec_splits = z.ec ? z.P : 0;
 
   // launches and grid
+  const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
   if (!z.ec) {
     z.plan.num_launches = 1;
-    z.plan.grid = z.gemv ? z.nrb * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
+    z.plan.grid = grid4;
   } else if (path == SPEAR_PATH_FUSED_GEMV) {
     z.n_prod = z.ntb * z.P;
     z.plan.num_launches = 1;
-    z.plan.grid = z.n_prod + z.nrb * z.S;
+    z.plan.grid = z.n_prod + grid4;
   } else if (path == SPEAR_PATH_UNFUSED_2K) {
     z.plan.num_launches = 2;
-    z.plan.grid = z.gemv ? z.nrb * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
+    z.plan.grid = grid4;
   } else {  // chain
     z.plan.num_launches = 4;
-    z.plan.grid = z.gemv ? z.nrb * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
+    z.plan.grid = grid4;
   }
 
-  // workspace layout
-  size_t off = 0;
+  // workspace layout. The first kCounterBytes hold every counter of every
+  // kind of call at fixed offsets (the generation word, the fused grid's done
+  // counter, EC-slice counters, row-group counters); each call leaves its
+  // counters at zero, and data regions start after this block, so any mix of
+  // calls can share one zero-initialised workspace.
+  size_t off = kCounterBytes;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off = align_up(off + bytes, 256);
     return o;
   };
+  z.off_gen = kCtrGen;
+  z.off_done = kCtrDone;
+  z.off_ectr = kCtrEc;
+  z.off_rbctr = kCtrRows;
   if (z.ec) {
-    z.off_flag = take((size_t)z.ntb * 4);
-    z.off_ectr = take((size_t)z.ntb * 8);
+    if (z.P > 1 && z.ntb > kMaxEcCounters) return SPEAR_E_SHAPE;
+    if (path == SPEAR_PATH_FUSED_GEMV) z.off_vtag = take((size_t)kVCopies * M * z.r * 8);
     if (z.P > 1) z.off_upart = take((size_t)z.ntb * z.P * kTokTile * z.R1 * 4);
     z.off_v = take((size_t)M * z.r * 4);
     if (!z.gemv && path == SPEAR_PATH_UNFUSED_2K) {
@@ -175,7 +212,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     if (path == SPEAR_PATH_UNFUSED_CHAIN) z.off_u = take((size_t)M * z.R1 * 4);
   }
   if (z.gemv && z.S > 1) {
-    z.off_rbctr = take((size_t)z.nrb * 8);
+    if (z.nrg > kMaxRowCounters) return SPEAR_E_SHAPE;
     z.off_ypart = take((size_t)z.S * M * N * 4);
   }
   z.plan.workspace_bytes = off;
@@ -255,7 +292,7 @@ EcParams make_ec(const spear_problem_t* p, const Resolved& z, const void* x, con
     e.alpha = ec->alpha;
   }
   if (ws) {
-    e.ctr = (unsigned long long*)(ws + z.off_ectr);
+    e.ctr = (uint32_t*)(ws + z.off_ectr);
     if (z.P > 1) e.upart = (float*)(ws + z.off_upart);
     e.v = (float*)(ws + z.off_v);
   }
@@ -284,7 +321,7 @@ GemvParams make_gemv(const spear_problem_t* p, const Resolved& z, const void* x,
   g.wait_polls = g_wait_polls.load();
   if (ws && z.S > 1) {
     g.ypart = (float*)(ws + z.off_ypart);
-    g.rb_ctr = (unsigned long long*)(ws + z.off_rbctr);
+    g.rb_ctr = (uint32_t*)(ws + z.off_rbctr);
   }
   return g;
 }
@@ -319,7 +356,8 @@ spear_status_t run_w4(const spear_problem_t* p, const Resolved& z, const void* x
                       void* y, char* ws, uint32_t epoch, hipStream_t st) {
   if (z.gemv) {
     GemvParams g = make_gemv(p, z, x, w, y, nullptr, ws, epoch);
-    return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_NONE, g, z.nrb * z.S, z.lds_gemv, st));
+    return hip_status(launch_gemv(z.dt, z.MT, z.RT, z.U, z.XL, EPI_NONE, g, z.nrg * z.S, 64 * z.NW,
+                                  z.lds_gemv, st));
   }
   GemmParams g = make_gemm(p, z, x, w, y, nullptr, nullptr);
   return hip_status(launch_gemm(z.dt, EPI_NONE, g, st));
@@ -367,24 +405,30 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   EcParams e = make_ec(prob, z, x, ec, ws, epoch);
   const int path = z.plan.path;
   if (path == SPEAR_PATH_FUSED_GEMV) {
-    e.flag = (uint32_t*)(ws + z.off_flag);
+    e.vtag = (unsigned long long*)(ws + z.off_vtag);
+    e.gen = (uint32_t*)(ws + z.off_gen);
+    e.v = nullptr;
     GemvParams g = make_gemv(prob, z, x, w, y, ec, ws, epoch);
     g.ec = e;
     g.n_prod = z.n_prod;
+    g.done_ctr = (uint32_t*)(ws + z.off_done);
+    g.grid_total = z.n_prod + z.nrg * z.S;
     const size_t lds = std::max(z.lds_gemv, z.lds_ec);
-    return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_FUSED, g, z.n_prod + z.nrb * z.S, lds, s));
+    return hip_status(launch_gemv(z.dt, z.MT, z.RT, z.U, z.XL, EPI_FUSED, g, g.grid_total,
+                                  64 * z.NW, lds, s));
   }
   if (path == SPEAR_PATH_UNFUSED_2K) {
     if (!z.gemv) {
       e.vh = (uint16_t*)(ws + z.off_vh);
       e.vl = (uint16_t*)(ws + z.off_vl);
     }
-    st = hip_status(launch_ec(z.dt, e, z.ntb, z.lds_ec, s));
+    st = hip_status(launch_ec(z.dt, e, z.ntb, z.ec_block, z.lds_ec, s));
     if (st != SPEAR_OK) return st;
     if (z.gemv) {
       GemvParams g = make_gemv(prob, z, x, w, y, ec, ws, epoch);
       g.ec = e;
-      return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_READY, g, z.nrb * z.S, z.lds_gemv, s));
+      return hip_status(launch_gemv(z.dt, z.MT, z.RT, z.U, z.XL, EPI_READY, g, z.nrg * z.S,
+                                    64 * z.NW, z.lds_gemv, s));
     }
     GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
     return hip_status(launch_gemm(z.dt, EPI_READY, g, s));
@@ -394,7 +438,7 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   if (st != SPEAR_OK) return st;
   e.raw = 1;
   e.u_out = (float*)(ws + z.off_u);
-  st = hip_status(launch_ec(z.dt, e, z.ntb, z.lds_ec, s));
+  st = hip_status(launch_ec(z.dt, e, z.ntb, z.ec_block, z.lds_ec, s));
   if (st != SPEAR_OK) return st;
   e.raw = 0;
   st = hip_status(launch_gate(z.dt, e, z.ntb, z.lds_ec, s));
@@ -427,6 +471,14 @@ spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w
 }
 
 int32_t spear_set_wait_polls(int32_t polls) { return g_wait_polls.exchange(polls < 0 ? 0 : polls); }
+
+void spear_set_gemv_shape(int32_t row_tiles, int32_t iters_per_wave, int32_t x_in_lds,
+                          int32_t waves) {
+  g_ov_rt = row_tiles > 0 ? row_tiles : 0;
+  g_ov_u = iters_per_wave > 0 ? iters_per_wave : 0;
+  g_ov_xl = x_in_lds < 0 ? -1 : (x_in_lds ? 1 : 0);
+  g_ov_nw = waves > 0 ? waves : 0;
+}
 
 const char* spear_status_string(spear_status_t s) {
   switch (s) {

@@ -22,6 +22,22 @@ constexpr int kGemmTM = 128;     // prefill tile: tokens
 constexpr int kGemmTN = 128;     // prefill tile: output rows
 constexpr int kGemmTK = 64;      // prefill tile: K per stage
 constexpr int kGemmLdsRow = kGemmTK + 8;  // padded LDS row (halves)
+constexpr int kVCopies = 8;      // tagged EC-coordinate copies (one per XCD)
+
+// Workspace: a fixed counter block at the start, shared by every kind of call
+// (each call returns its counters to zero), then the call's data regions.
+constexpr size_t kCounterBytes = 65536;
+constexpr size_t kCtrGen = 0;        // launch generation of the fused path
+constexpr size_t kCtrDone = 4;       // fused grid: blocks done
+constexpr size_t kCtrEc = 256;       // EC-slice counters, one per token tile
+constexpr int kMaxEcCounters = 64;
+constexpr size_t kCtrRows = 512;     // split-K counters, one per row group
+constexpr int kMaxRowCounters = (int)((kCounterBytes - kCtrRows) / 4);
+
+// Tag of the EC coordinates published by the fused launch of generation g:
+// a multiplicative hash, so that leftover data of another call is never
+// mistaken for a current coordinate (2^-32 chance per word).
+__host__ __device__ inline uint32_t ec_tag(uint32_t gen) { return ((gen + 1u) * 0x9E3779B1u) | 1u; }
 
 // EC projection / gate work of one token tile (16 tokens) and one K-slice.
 struct EcParams {
@@ -37,13 +53,14 @@ struct EcParams {
   int P, ips;             // K-slices and 128-wide iterations per slice
   int raw;                // 1: store u = [A; w_g] x only (no gate)
   float* upart;           // [ntb][P][16][R1] partial sums (P > 1)
-  unsigned long long* ctr;// [ntb] last-arriver counters
-  uint32_t* flag;         // [ntb] completion flags (fused path) or null
+  uint32_t* ctr;          // [ntb] last-arriver counters
   float* v;               // [M][r] gated coordinates, fp32
   uint16_t* vh;           // [M][vstride] act-dtype high part (or null)
   uint16_t* vl;           // [M][vstride] act-dtype low part  (or null)
   int vstride;
   float* u_out;           // raw mode: [M][R1]
+  unsigned long long* vtag;  // fused: [kVCopies][M][r] (tag << 32 | fp32 bits)
+  uint32_t* gen;          // fused: launch generation (tag = ec_tag(gen))
   uint32_t epoch;
 };
 
@@ -55,10 +72,12 @@ struct GemvParams {
   uint16_t* y;            // [M][N]
   const uint16_t* B;      // [N][r]
   int M, N, K, G, ngroups, r;
-  int S, ips;             // split-K slices and iterations per slice
+  int S, ips;             // K-slices per row tile and iterations per slice
   int n_prod;             // EC workgroups at the head of the grid (fused)
   float* ypart;           // [S][M][N] partial sums (S > 1)
-  unsigned long long* rb_ctr;  // [row blocks]
+  uint32_t* rb_ctr;       // [row tiles] last-arriver counters
+  uint32_t* done_ctr;     // fused: arrivals of every workgroup of the grid
+  int grid_total;              // fused: workgroups in the grid
   int wait_polls;
   uint32_t epoch;
   EcParams ec;
@@ -86,26 +105,29 @@ __host__ __device__ inline size_t ec_lds_bytes(int R1p, int h, int r) {
   return ec_lds_v_off(R1p, h) + align_up((size_t)kTokTile * (r > 0 ? r : 1) * 4, 16);
 }
 
-// LDS carve-up of a GEMV block:
-//   region A: scale/zero staging [ngs][RB] (fp16 + u8), reused after the main
-//             loop for the cross-wave reduction (3 waves x RT*MT x 1 KB)
-//   region Y: the block's sums [RB][16*MT] fp32
-//   region E: an EC block (v tile for the epilogue; u/hidden for the fallback)
-__host__ __device__ inline size_t gemv_lds_a_bytes(int ngs, int RT, int MT) {
-  size_t sz = align_up((size_t)ngs * 16 * RT * 3, 16);
-  size_t red = (size_t)3 * RT * MT * 1024;
-  return sz > red ? sz : red;
+// LDS carve-up of a GEMV block of NW waves and RT row tiles:
+//   X:    (XLDS) the block's slice of x, [M + 1][ips*128 + 8] fp16
+//   red:  per-wave partial tiles, NW x RT x MT x 1 KB (reuses X)
+//   yacc: the block's sums [16*MT tokens][16*RT rows] fp32
+//   E:    an EC block (v tile for the epilogue; u/hidden for the fallback)
+__host__ __device__ inline size_t gemv_lds_a_bytes(int NW, int RT, int MT, int xl_rows, int ips) {
+  const size_t x = xl_rows > 0 ? align_up((size_t)(xl_rows + 1) * (ips * kIterK + 8) * 2, 16) : 0;
+  const size_t red = (size_t)NW * RT * MT * 1024;
+  return x > red ? x : red;
 }
-__host__ __device__ inline size_t gemv_lds_y_off(int ngs, int RT, int MT) { return gemv_lds_a_bytes(ngs, RT, MT); }
-__host__ __device__ inline size_t gemv_lds_e_off(int ngs, int RT, int MT) {
-  return gemv_lds_y_off(ngs, RT, MT) + (size_t)RT * MT * 1024;
+__host__ __device__ inline size_t gemv_lds_y_off(int NW, int RT, int MT, int xl_rows, int ips) {
+  return gemv_lds_a_bytes(NW, RT, MT, xl_rows, ips);
+}
+__host__ __device__ inline size_t gemv_lds_e_off(int NW, int RT, int MT, int xl_rows, int ips) {
+  return gemv_lds_y_off(NW, RT, MT, xl_rows, ips) + (size_t)RT * MT * 1024;
 }
 
 hipError_t launch_dequant(int dt, const uint32_t* qw, const uint16_t* sc, const uint8_t* zr,
                           uint16_t* out, int N, int K, int G, hipStream_t st);
-hipError_t launch_ec(int dt, const EcParams& e, int ntb, size_t lds, hipStream_t st);
-hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid,
-                       size_t lds, hipStream_t st);
+hipError_t launch_ec(int dt, const EcParams& e, int ntb, int block, size_t lds, hipStream_t st);
+bool gemv_shape_supported(int MT, int RT, int U, bool XL);
+hipError_t launch_gemv(int dt, int MT, int RT, int U, bool XL, int epi, const GemvParams& p,
+                       int grid, int block, size_t lds, hipStream_t st);
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st);
 hipError_t launch_gate(int dt, const EcParams& e, int ntb, size_t lds, hipStream_t st);
 hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, uint16_t* y, int M,

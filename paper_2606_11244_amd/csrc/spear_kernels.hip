@@ -13,10 +13,11 @@
 //   k_dequant  bit-exact dequantisation diagnostic
 //   k_ec       EC projection u = [A; w_g] x over a K-slice, last-arriver
 //              reduction across slices, gate, v = alpha * gate (.) u
-//   k_gemv     decode: split-K 4-bit product with MFMA, per-128 dequant
-//              correction, cross-wave and cross-workgroup reduction, and an
-//              epilogue adding B v; in the fused variant the same grid's first
-//              workgroups run k_ec's work and publish v through a flag
+//   k_gemv     decode: 4-bit product with MFMA on one 16-row tile per block,
+//              per-128 dequant correction, cross-wave (and, for long K,
+//              cross-block) reduction, epilogue adding B v; in the fused
+//              variant the grid's first blocks run k_ec's work and publish v
+//              as tagged words that the other blocks poll
 //   k_gemm     prefill: LDS-tiled 4-bit GEMM (dequantised tiles, double
 //              buffered), MFMA epilogue adding B v from the EC pre-kernel
 //   k_gate, k_ec_up_acc   the naive split chain's separate gate and
@@ -102,20 +103,58 @@ __device__ __forceinline__ u32x4 ones8() {
 
 __device__ __forceinline__ u32x4 ldg16(const void* p) { return *(const u32x4*)p; }
 
-// Last-arriver detection with an epoch-tagged 64-bit counter: the high word
-// holds the call's epoch, the low word the arrivals of that epoch. A counter
-// left over from another call (any other epoch) restarts at 1. Returns true
-// for the arrival that completes `total`.
-__device__ __forceinline__ bool arrive_last(unsigned long long* ctr, uint32_t epoch, uint32_t total) {
-  unsigned long long old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  for (;;) {
-    const uint32_t e = (uint32_t)(old >> 32);
-    const unsigned long long nv =
-        (e == epoch) ? old + 1ull : (((unsigned long long)epoch << 32) | 1ull);
-    if (__hip_atomic_compare_exchange_strong(ctr, &old, nv, __ATOMIC_ACQ_REL, __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT))
-      return (uint32_t)nv == total;
-  }
+// Raw buffer loads through a bounds-checked resource (gfx9 descriptor word 3
+// = 0x00020000): a byte offset at or past `bytes` reads as zero. Masked
+// elements are given the offset kOOB, so every load is issued without a
+// branch and a wave's loads all stay in flight together.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 bld128(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+__device__ __forceinline__ uint32_t bld16(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+__device__ __forceinline__ uint32_t bld8(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b8(r, off, 0, 0);
+}
+
+// Cross-workgroup data (partial sums, the EC coordinates, flags, counters)
+// moves only through relaxed agent-scope atomic accesses: on gfx950 these are
+// plain loads/stores with the sc1 bit, coherent across the eight XCDs' L2s on
+// every access, so no cache-wide writeback or invalidate is ever issued.
+// Ordering comes from waiting for the stores to complete (s_waitcnt) before
+// the barrier that precedes the publishing atomic.
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_agent_u32(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// All of this thread's memory operations have completed; then the block meets.
+__device__ __forceinline__ void complete_and_sync() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
+// Last-arriver detection: one relaxed agent-scope fetch-add per arrival (no
+// compare-and-swap retries, which serialise at one memory round trip each).
+// The arrival that completes `total` resets the counter to zero, so every
+// launch (also a replayed graph) starts from zero; the workspace holding the
+// counters is zero-filled once before first use. Callers publish their data
+// with st_agent and complete_and_sync() before arriving, and the last arriver
+// reads it back with ld_agent.
+__device__ __forceinline__ bool arrive_last(uint32_t* ctr, uint32_t total) {
+  const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (old + 1u != total) return false;
+  __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -153,48 +192,56 @@ __global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ qw
 // ---------------------------------------------------------------------------
 // EC projection of one token tile over iterations [it_beg, it_end):
 // u_lds[t][j] = sum_k x[16*tb + t][k] * R[j][k], R = [A; w_g] (R1 rows), as a
-// sum over the block's four waves in a fixed order.
+// sum over the block's waves in a fixed order (wave 0 first).
 // ---------------------------------------------------------------------------
 template <int DT>
 __device__ void ec_project_tile(const EcParams& e, int tb, int it_beg, int it_end, float* u_lds) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int NW = blockDim.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int m = tb * kTokTile + lr;
-  const bool mval = m < e.M;
   const int RTe = (e.R1 + 15) >> 4;
-  const uint16_t* xrow = e.x + (size_t)(mval ? m : 0) * e.K;
+  const rsrc_t rx = make_rsrc(e.x, (uint32_t)e.M * e.K * 2);
+  const rsrc_t ra = make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
+  const rsrc_t rg = make_rsrc(e.wg, e.gate == GATE_SIGMOID ? (uint32_t)e.K * 2 : 0u);
+  const uint32_t xoff = m < e.M ? (uint32_t)m * e.K * 2 + 64 * lg : kOOB;
   for (int tg0 = 0; tg0 < RTe; tg0 += 4) {
     const int nt = min(4, RTe - tg0);
     f32x4 acc[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint16_t* rsrc[4];
+    uint32_t aoff[4], goff[4];
+    bool has_g[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int j = (tg0 + t) * 16 + lr;
-      rsrc[t] = (t < nt && j < e.r) ? e.A + (size_t)j * e.K
-                : (t < nt && j == e.r && e.gate == GATE_SIGMOID) ? e.wg
-                                                                : nullptr;
+      aoff[t] = j < e.r ? (uint32_t)j * e.K * 2 + 64 * lg : kOOB;
+      goff[t] = (j == e.r && e.gate == GATE_SIGMOID) ? 64u * lg : kOOB;
+      // uniform: does this row tile hold the gate row w_g?
+      has_g[t] = e.gate == GATE_SIGMOID && e.r >= (tg0 + t) * 16 && e.r < (tg0 + t + 1) * 16;
     }
-    for (int it = it_beg + wave; it < it_end; it += 4) {
-      const int k = it * kIterK + 32 * lg;
+    for (int it = it_beg + wave; it < it_end; it += NW) {
+      const uint32_t kb = (uint32_t)it * (kIterK * 2);
       u32x4 xv[4];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-        xv[jj] = mval ? ldg16(xrow + k + 8 * jj) : u32x4{0, 0, 0, 0};
+      for (int jj = 0; jj < 4; ++jj) xv[jj] = bld128(rx, xoff + kb + 16 * jj);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         if (t < nt) {
+          u32x4 av[4];
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            const u32x4 a = rsrc[t] ? ldg16(rsrc[t] + k + 8 * jj) : u32x4{0, 0, 0, 0};
-            acc[t] = mfma16<DT>(a, xv[jj], acc[t]);
+          for (int jj = 0; jj < 4; ++jj) av[jj] = bld128(ra, aoff[t] + kb + 16 * jj);
+          if (has_g[t]) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) av[jj] |= bld128(rg, goff[t] + kb + 16 * jj);
           }
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) acc[t] = mfma16<DT>(av[jj], xv[jj], acc[t]);
         }
       }
     }
-    // deterministic cross-wave sum: wave 0 stores, waves 1..3 add in order
-    for (int w = 0; w < 4; ++w) {
+    // deterministic cross-wave sum: wave 0 stores, waves 1.. add in order
+    for (int w = 0; w < NW; ++w) {
       __syncthreads();
       if (wave == w) {
 #pragma unroll
@@ -220,19 +267,19 @@ __device__ void ec_project_tile(const EcParams& e, int tb, int it_beg, int it_en
 template <int DT>
 __device__ void ec_gate_tile(const EcParams& e, int cnt, const float* u_lds, float* hid,
                              float* v_tile) {
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, nthr = blockDim.x;
   const int r = e.r;
   if (e.gate == GATE_TANH) {
     for (int t = 0; t < cnt; ++t) {
       const float* u = u_lds + t * e.R1p;
-      for (int i = tid; i < e.h; i += 256) {
+      for (int i = tid; i < e.h; i += nthr) {
         float a = act2f<DT>(e.b1[i]);
         const uint16_t* w1 = e.W1 + (size_t)i * r;
         for (int j = 0; j < r; ++j) a += act2f<DT>(w1[j]) * u[j];
         hid[i] = a > 0.f ? a : 0.f;
       }
       __syncthreads();
-      for (int j = tid; j < r; j += 256) {
+      for (int j = tid; j < r; j += nthr) {
         float a = act2f<DT>(e.b2[j]);
         const uint16_t* w2 = e.W2 + (size_t)j * e.h;
         for (int i = 0; i < e.h; ++i) a += act2f<DT>(w2[i]) * hid[i];
@@ -241,7 +288,7 @@ __device__ void ec_gate_tile(const EcParams& e, int cnt, const float* u_lds, flo
       __syncthreads();
     }
   } else {
-    for (int idx = tid; idx < cnt * r; idx += 256) {
+    for (int idx = tid; idx < cnt * r; idx += nthr) {
       const int t = idx / r, j = idx - t * r;
       float g = 1.f;
       if (e.gate == GATE_SIGMOID) {
@@ -255,12 +302,14 @@ __device__ void ec_gate_tile(const EcParams& e, int cnt, const float* u_lds, flo
 }
 
 // One EC block: token tile tb, K-slice p. Projects, reduces across slices
-// (last arriver), applies the gate and publishes v (fp32, and act-dtype
-// hi/lo parts when requested), then releases flag[tb] if there is one.
+// (last arriver), applies the gate and publishes v: as fp32 (consumed by a
+// later kernel), as act-dtype hi/lo parts (the GEMM epilogue), and/or as
+// tagged 64-bit words (tag << 32 | fp32 bits) in one copy per XCD, which the
+// fused kernel's workgroups poll: a word is current when its tag matches.
 template <int DT>
 __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
   __shared__ int s_last;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, nthr = blockDim.x;
   const int IT = e.K / kIterK;
   const int it_beg = p * e.ips, it_end = min(IT, it_beg + e.ips);
   float* u_lds = (float*)(smem + ec_lds_u_off());
@@ -273,20 +322,18 @@ __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
 
   if (e.P > 1) {
     float* part = e.upart + ((size_t)tb * e.P + p) * kTokTile * e.R1;
-    for (int idx = tid; idx < cnt * e.R1; idx += 256) {
+    for (int idx = tid; idx < cnt * e.R1; idx += nthr) {
       const int t = idx / e.R1, j = idx - t * e.R1;
-      part[idx] = u_lds[t * e.R1p + j];
+      st_agent(part + idx, u_lds[t * e.R1p + j]);
     }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = arrive_last(e.ctr + tb, e.epoch, (uint32_t)e.P) ? 1 : 0;
+    complete_and_sync();
+    if (tid == 0) s_last = arrive_last(e.ctr + tb, (uint32_t)e.P) ? 1 : 0;
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
     const float* base = e.upart + (size_t)tb * e.P * kTokTile * e.R1;
-    for (int idx = tid; idx < cnt * e.R1; idx += 256) {
+    for (int idx = tid; idx < cnt * e.R1; idx += nthr) {
       float a = 0.f;
-      for (int q = 0; q < e.P; ++q) a += base[(size_t)q * kTokTile * e.R1 + idx];
+      for (int q = 0; q < e.P; ++q) a += ld_agent(base + (size_t)q * kTokTile * e.R1 + idx);
       const int t = idx / e.R1, j = idx - t * e.R1;
       u_lds[t * e.R1p + j] = a;
     }
@@ -294,7 +341,7 @@ __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
   }
 
   if (e.raw) {
-    for (int idx = tid; idx < cnt * e.R1; idx += 256) {
+    for (int idx = tid; idx < cnt * e.R1; idx += nthr) {
       const int t = idx / e.R1, j = idx - t * e.R1;
       e.u_out[(size_t)(m0 + t) * e.R1 + j] = u_lds[t * e.R1p + j];
     }
@@ -302,10 +349,10 @@ __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
   }
 
   ec_gate_tile<DT>(e, cnt, u_lds, hid, v_tile);
-  for (int idx = tid; idx < cnt * e.r; idx += 256)
-    e.v[(size_t)m0 * e.r + idx] = v_tile[idx];
+  if (e.v)
+    for (int idx = tid; idx < cnt * e.r; idx += nthr) e.v[(size_t)m0 * e.r + idx] = v_tile[idx];
   if (e.vh) {
-    for (int idx = tid; idx < cnt * e.vstride; idx += 256) {
+    for (int idx = tid; idx < cnt * e.vstride; idx += nthr) {
       const int t = idx / e.vstride, j = idx - t * e.vstride;
       float val = j < e.r ? v_tile[t * e.r + j] : 0.f;
       const uint16_t hi = f2act<DT>(val);
@@ -314,15 +361,21 @@ __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
       e.vl[(size_t)(m0 + t) * e.vstride + j] = lo;
     }
   }
-  if (e.flag) {
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) __hip_atomic_store(e.flag + tb, e.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  if (e.vtag) {
+    const uint32_t tag = ec_tag(ld_agent_u32(e.gen));
+    const size_t per_copy = (size_t)e.M * e.r;
+    for (int idx = tid; idx < cnt * e.r * kVCopies; idx += nthr) {
+      const int c = idx / (cnt * e.r), o = idx - c * (cnt * e.r);
+      const unsigned long long w =
+          ((unsigned long long)tag << 32) | __float_as_uint(v_tile[o]);
+      __hip_atomic_store(e.vtag + c * per_copy + (size_t)m0 * e.r + o, w, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 
 template <int DT>
-__global__ __launch_bounds__(256) void k_ec(EcParams e) {
+__global__ __launch_bounds__(1024) void k_ec(EcParams e) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   ec_block<DT>(e, blockIdx.x / e.P, blockIdx.x % e.P, smem);
 }
@@ -336,13 +389,13 @@ __global__ __launch_bounds__(256) void k_gate(EcParams e) {
   float* v_tile = (float*)(smem + ec_lds_v_off(e.R1p, e.h));
   const int m0 = blockIdx.x * kTokTile;
   const int cnt = min(kTokTile, e.M - m0);
-  for (int idx = threadIdx.x; idx < cnt * e.R1; idx += 256) {
+  for (int idx = threadIdx.x; idx < cnt * e.R1; idx += blockDim.x) {
     const int t = idx / e.R1, j = idx - t * e.R1;
     u_lds[t * e.R1p + j] = e.u_out[(size_t)(m0 + t) * e.R1 + j];
   }
   __syncthreads();
   ec_gate_tile<DT>(e, cnt, u_lds, hid, v_tile);
-  for (int idx = threadIdx.x; idx < cnt * e.r; idx += 256) e.v[(size_t)m0 * e.r + idx] = v_tile[idx];
+  for (int idx = threadIdx.x; idx < cnt * e.r; idx += blockDim.x) e.v[(size_t)m0 * e.r + idx] = v_tile[idx];
 }
 
 // Naive chain, reprojection + accumulate: y[m][n] += sum_j v[m][j] B[n][j].
@@ -358,235 +411,307 @@ __global__ __launch_bounds__(256) void k_ec_up_acc(const float* __restrict__ v,
   y[idx] = f2act<DT>(a);
 }
 
+// Every block of the fused grid arrives here once when it is done; the last
+// one advances the generation that tags the next launch's EC coordinates, so
+// that a replayed graph (same epoch) never reads the previous replay's values.
+__device__ __forceinline__ void fused_exit(const GemvParams& a, uint32_t gen) {
+  complete_and_sync();
+  if (threadIdx.x == 0 && arrive_last(a.done_ctr, (uint32_t)a.grid_total))
+    __hip_atomic_store(a.ec.gen, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---------------------------------------------------------------------------
-// Decode GEMV. Block = 4 waves on RT row tiles (16 rows each) and one K-slice;
-// waves take the slice's 128-wide iterations round robin. Per iteration and
-// row tile a lane loads 16 B of codes (32 codes of one row), the MFMA runs on
-// biased codes (1024+q or 128+q, exact) against the matching activations,
-// and the group's scale and zero are applied in fp32:
+// Decode GEMV. A block owns RT row tiles (16 rows each) and a K-slice of
+// NW*U iterations (128 K each); each of its NW waves takes U consecutive
+// iterations of all RT tiles and issues every load before computing, so a
+// wave keeps RT*U KB of codes in flight. The MFMA multiplies activations (A
+// operand, 16 token rows) by the biased codes (B operand, 16 weight rows as
+// columns), so each lane owns one weight row per tile and needs one scale
+// and one zero point per iteration:
 //   sum_k x (q - z) s = s * ( sum_k x (bias + q) - (bias + z) * sum_k x ),
-// with sum_k x taken by an MFMA against ones.
+// with sum_k x from an MFMA against ones; the activation fragments are shared
+// by the RT tiles. With XLDS (at most 4 tokens) the block stages its slice of
+// x in LDS once instead of every wave loading mostly-empty fragments. Waves
+// are reduced in LDS in a fixed order; K-slices (only when K exceeds one
+// block's NW*U iterations) through partial sums and a last arriver.
+//
+// Fused variant: the first n_prod blocks of the grid are EC blocks (above).
+// The others, after their main loop, poll the tagged EC coordinates of their
+// XCD copy (bounded; on time-out they compute the EC themselves) and add
+// B v in the epilogue. Every block arrives at a done counter at its end; the
+// last one advances the generation that tags the next launch's coordinates.
 // ---------------------------------------------------------------------------
-template <int DT, int MT, int RT, int EPI>
-__global__ __launch_bounds__(256) void k_gemv(GemvParams a) {
+template <int DT, int MT, int RT, int U, bool XLDS, int EPI>
+__global__ __launch_bounds__(1024) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int s_flag;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int NW = blockDim.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   int bid = blockIdx.x;
+  uint32_t gen = 0;
   if constexpr (EPI == EPI_FUSED) {
+    gen = ld_agent_u32(a.ec.gen);
     if (bid < a.n_prod) {
       ec_block<DT>(a.ec, bid / a.ec.P, bid % a.ec.P, smem);
+      fused_exit(a, gen);
       return;
     }
     bid -= a.n_prod;
   }
   constexpr int RB = 16 * RT;
-  const int rb = bid / a.S, s = bid - (bid / a.S) * a.S;
-  const int n0 = rb * RB;
   const int M = a.M, N = a.N, K = a.K, G = a.G;
   const int IT = K / kIterK;
-  const int it_beg = s * a.ips, it_end = min(IT, it_beg + a.ips);
-  const int g_beg = (it_beg * kIterK) / G;
-  const int g_end = (it_end * kIterK + G - 1) / G;
-  const int ngs = max(1, g_end - g_beg);
+  const int rg = bid / a.S, s = bid - (bid / a.S) * a.S;
+  const int n0 = rg * RB;
+  const int it_blk = s * a.ips;
+  const int it_end = min(IT, it_blk + a.ips);
+  const int it_w = it_blk + wave * U;
 
-  // stage this block's scales and zero points: [group][row]
-  uint16_t* s_lds = (uint16_t*)smem;
-  uint8_t* z_lds = (uint8_t*)(smem + align_up((size_t)ngs * RB * 2, 16));
-  for (int idx = tid; idx < ngs * RB; idx += 256) {
-    const int row = idx / ngs, gg = idx - row * ngs;
-    const int n = n0 + row;
-    const bool ok = n < N && (g_beg + gg) < a.ngroups;
-    const size_t o = (size_t)n * a.ngroups + g_beg + gg;
-    s_lds[gg * RB + row] = ok ? a.sc[o] : (uint16_t)0;
-    z_lds[gg * RB + row] = ok ? a.zr[o] : (uint8_t)0;
+  // ---- issue every load of this block (masked lanes read zeros)
+  const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * (K / 2));
+  const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
+  const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
+  const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
+  u32x4 wv[RT][U];
+  uint32_t sv[RT][U], zv[RT][U];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    const int n = n0 + 16 * t + lr;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int it = it_w + u;
+      const bool ok = n < N && it < it_end;
+      const uint32_t g = (uint32_t)(it * kIterK) / G;
+      wv[t][u] = bld128(rq, ok ? (uint32_t)n * (K / 2) + (uint32_t)it * (kIterK / 2) + 16 * lg : kOOB);
+      sv[t][u] = bld16(rsc, ok ? ((uint32_t)n * a.ngroups + g) * 2 : kOOB);
+      zv[t][u] = bld8(rz, ok ? (uint32_t)n * a.ngroups + g : kOOB);
+    }
   }
-  __syncthreads();
+  // activations: either per-wave fragments, or the block's slice via LDS
+  constexpr int XM = XLDS ? 1 : MT;
+  constexpr int XU = XLDS ? 1 : U;
+  u32x4 xv[XM][XU][4];
+  // staged 16-byte chunks per thread: M <= 4 rows of ips * 16 chunks over
+  // 64 * NW threads, ips = NW * U, so at most U
+  constexpr int XCH = XLDS ? U : 1;
+  u32x4 xst[XCH];
+  const int xrow_h = a.ips * kIterK + 8;  // LDS row stride (halves) of the x slice
+  const int xchunks_row = a.ips * (kIterK / 8);
+  if constexpr (XLDS) {
+#pragma unroll
+    for (int c = 0; c < XCH; ++c) {
+      const int ci = tid + c * (int)blockDim.x;
+      const int row = ci / xchunks_row, col = ci - row * xchunks_row;
+      const int k = it_blk * kIterK + 8 * col;
+      const bool ok = row < M && k < it_end * kIterK;
+      xst[c] = bld128(rx, ok ? ((uint32_t)row * K + k) * 2 : kOOB);
+    }
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = 16 * mt + lr;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int it = it_w + u;
+        const uint32_t base = (m < M && it < it_end)
+                                  ? ((uint32_t)m * K + (uint32_t)it * kIterK + 32 * lg) * 2 : kOOB;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) xv[mt][u][jj] = bld128(rx, base + 16 * jj);
+      }
+    }
+  }
+  // the EC epilogue's rows of B ([16*RT][r], fp16/bf16) ride along with the
+  // main loads when r is a multiple of 8 and two 16-byte chunks per thread
+  // cover them; otherwise the epilogue reads B directly
+  constexpr int BCH = 2;
+  const int r = a.r;
+  const int bchunks = EPI != EPI_NONE && (r & 7) == 0 ? RB * r / 8 : 0;
+  const bool bpre = bchunks > 0 && bchunks <= BCH * (int)blockDim.x;
+  u32x4 bst[BCH];
+  if (bpre) {
+    const rsrc_t rb = make_rsrc(a.B, (uint32_t)N * r * 2);
+#pragma unroll
+    for (int c = 0; c < BCH; ++c) {
+      const int ci = tid + c * (int)blockDim.x;
+      bst[c] = bld128(rb, ci < bchunks ? (uint32_t)n0 * r * 2 + 16u * ci : kOOB);
+    }
+  }
+  // keep the scheduler from sinking these loads next to their uses: all of
+  // them must be in flight before the first wait
+  __builtin_amdgcn_sched_barrier(0);
 
+  uint16_t* xs = (uint16_t*)smem;  // XLDS: [M + 1][xrow_h], row M all zero
+  if constexpr (XLDS) {
+#pragma unroll
+    for (int c = 0; c < XCH; ++c) {
+      const int ci = tid + c * (int)blockDim.x;
+      const int row = ci / xchunks_row, col = ci - row * xchunks_row;
+      if (row < M) *(u32x4*)(xs + row * xrow_h + 8 * col) = xst[c];
+    }
+    for (int ci = tid; ci < xchunks_row; ci += blockDim.x)
+      *(u32x4*)(xs + M * xrow_h + 8 * ci) = u32x4{0, 0, 0, 0};
+    __syncthreads();
+  }
+
+  // ---- compute
+  constexpr float kBias = code_bias<DT>();
   f32x4 acc[RT][MT];
 #pragma unroll
   for (int t = 0; t < RT; ++t)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const size_t kw = (size_t)(K >> 3);
-  const uint32_t* wrow[RT];
-  bool wval[RT];
 #pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    const int n = n0 + 16 * t + lr;
-    wval[t] = n < N;
-    wrow[t] = a.qw + (size_t)(wval[t] ? n : 0) * kw + 4 * lg;
-  }
-  const uint16_t* xrow[MT];
-  bool xval[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = 16 * mt + lr;
-    xval[mt] = m < M;
-    xrow[mt] = a.x + (size_t)(xval[mt] ? m : 0) * K + 32 * lg;
-  }
-  constexpr float kBias = code_bias<DT>();
-
-  for (int it = it_beg + wave; it < it_end; it += 4) {
-    const int k0 = it * kIterK;
-    u32x4 wv[RT];
-#pragma unroll
-    for (int t = 0; t < RT; ++t) wv[t] = wval[t] ? ldg16(wrow[t] + (k0 >> 3)) : u32x4{0, 0, 0, 0};
-    u32x4 xv[MT][4];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-        xv[mt][jj] = xval[mt] ? ldg16(xrow[mt] + k0 + 8 * jj) : u32x4{0, 0, 0, 0};
+  for (int u = 0; u < U; ++u) {
     f32x4 xb[MT];
+    u32x4 xp[MT][4];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
+      u32x4 xf[4];
+      if constexpr (XLDS) {
+        const int row = lr < M ? lr : M;
+        const uint16_t* src = xs + row * xrow_h + (wave * U + u) * kIterK + 32 * lg;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) xf[jj] = *(const u32x4*)(src + 8 * jj);
+      } else {
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) xf[jj] = xv[mt][u][jj];
+      }
       xb[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) xb[mt] = mfma16<DT>(ones8<DT>(), xv[mt][jj], xb[mt]);
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) xv[mt][jj] = pair_like_codes(xv[mt][jj]);
+      for (int jj = 0; jj < 4; ++jj) {
+        xb[mt] = mfma16<DT>(xf[jj], ones8<DT>(), xb[mt]);
+        xp[mt][jj] = pair_like_codes(xf[jj]);
+      }
     }
-    const int gg = k0 / G - g_beg;
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
-      const u32x2 s4 = *(const u32x2*)(s_lds + gg * RB + 16 * t + 4 * lg);
-      const uint32_t z4 = *(const uint32_t*)(z_lds + gg * RB + 16 * t + 4 * lg);
-      float sf[4], cf[4];
-      sf[0] = h2f((uint16_t)(s4[0] & 0xFFFF));
-      sf[1] = h2f((uint16_t)(s4[0] >> 16));
-      sf[2] = h2f((uint16_t)(s4[1] & 0xFFFF));
-      sf[3] = h2f((uint16_t)(s4[1] >> 16));
-#pragma unroll
-      for (int i = 0; i < 4; ++i) cf[i] = kBias + (float)((z4 >> (8 * i)) & 0xFF);
       u32x4 wd[4];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) wd[jj] = unpack_biased<DT>(wv[t][jj]);
+      for (int jj = 0; jj < 4; ++jj) wd[jj] = unpack_biased<DT>(wv[t][u][jj]);
+      const float sf = h2f((uint16_t)sv[t][u]);
+      const float cf = kBias + (float)zv[t][u];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 pacc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) pacc = mfma16<DT>(wd[jj], xv[mt][jj], pacc);
+        for (int jj = 0; jj < 4; ++jj) pacc = mfma16<DT>(xp[mt][jj], wd[jj], pacc);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[t][mt][i] += sf[i] * (pacc[i] - cf[i] * xb[mt][i]);
+        for (int i = 0; i < 4; ++i) acc[t][mt][i] += sf * (pacc[i] - cf * xb[mt][i]);
       }
     }
   }
 
-  // cross-wave reduction (fixed order 0 + 1 + 2 + 3) into wave 0
-  __syncthreads();
+  // ---- cross-wave reduction (fixed order) into yacc[token][row]
+  if constexpr (XLDS) __syncthreads();  // the x slice is dead; reuse its LDS
   float* red = (float*)smem;
-  if (wave > 0) {
 #pragma unroll
-    for (int t = 0; t < RT; ++t)
+  for (int t = 0; t < RT; ++t)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        *(f32x4*)(red + (((wave - 1) * RT * MT + t * MT + mt) * 64 + lane) * 4) = acc[t][mt];
-  }
+    for (int mt = 0; mt < MT; ++mt)
+      *(f32x4*)(red + (((wave * RT + t) * MT + mt) * 64 + lane) * 4) = acc[t][mt];
   __syncthreads();
-  float* yacc = (float*)(smem + gemv_lds_y_off(ngs, RT, MT));
-  constexpr int YS = 16 * MT;  // row stride of yacc
-  if (wave == 0) {
-#pragma unroll
-    for (int w = 1; w < 4; ++w)
-#pragma unroll
-      for (int t = 0; t < RT; ++t)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          acc[t][mt] += *(const f32x4*)(red + (((w - 1) * RT * MT + t * MT + mt) * 64 + lane) * 4);
-#pragma unroll
-    for (int t = 0; t < RT; ++t)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) yacc[(16 * t + 4 * lg + i) * YS + 16 * mt + lr] = acc[t][mt][i];
+  float* yacc = (float*)(smem + gemv_lds_y_off(NW, RT, MT, XLDS ? M : 0, a.ips));
+  constexpr int YS = RB;  // yacc row stride: [token][RB rows]
+  for (int e = tid; e < 256 * RT * MT; e += blockDim.x) {
+    const int tm = e >> 8, rem = e & 255, ln = rem >> 2, i = rem & 3;
+    const int t = tm / MT, mt = tm - t * MT;
+    float v = 0.f;
+    for (int w = 0; w < NW; ++w) v += red[(((w * RT + t) * MT + mt) * 64 + ln) * 4 + i];
+    const int tok = 16 * mt + 4 * (ln >> 4) + i, row = 16 * t + (ln & 15);
+    yacc[tok * YS + row] = v;
   }
   __syncthreads();
 
-  // cross-workgroup split-K reduction: last arriver of the row block sums the
-  // S partials in slice order
+  // ---- cross-block split-K reduction: last arriver sums the slices in order
   if (a.S > 1) {
-    for (int idx = tid; idx < RB * M; idx += 256) {
-      const int m = idx / RB, row = idx - m * RB;
-      const int n = n0 + row;
-      if (n < N) a.ypart[((size_t)s * M + m) * N + n] = yacc[row * YS + m];
+    for (int e = tid; e < RB * M; e += blockDim.x) {
+      const int m = e / RB, row = e - m * RB;
+      if (n0 + row < N) st_agent(a.ypart + ((size_t)s * M + m) * N + n0 + row, yacc[m * YS + row]);
     }
-    __threadfence();
+    complete_and_sync();
+    if (tid == 0) s_flag = arrive_last(a.rb_ctr + rg, (uint32_t)a.S) ? 1 : 0;
     __syncthreads();
-    if (tid == 0) s_flag = arrive_last(a.rb_ctr + rb, a.epoch, (uint32_t)a.S) ? 1 : 0;
-    __syncthreads();
-    if (!s_flag) return;
-    __threadfence();
-    for (int idx = tid; idx < RB * M; idx += 256) {
-      const int m = idx / RB, row = idx - m * RB;
-      const int n = n0 + row;
-      if (n < N) {
-        float t = 0.f;
-        for (int q = 0; q < a.S; ++q) t += a.ypart[((size_t)q * M + m) * N + n];
-        yacc[row * YS + m] = t;
+    if (!s_flag) {
+      if constexpr (EPI == EPI_FUSED) fused_exit(a, gen);
+      return;
+    }
+    for (int e = tid; e < RB * M; e += blockDim.x) {
+      const int m = e / RB, row = e - m * RB;
+      if (n0 + row < N) {
+        float v = 0.f;
+        for (int q = 0; q < a.S; ++q) v += ld_agent(a.ypart + ((size_t)q * M + m) * N + n0 + row);
+        yacc[m * YS + row] = v;
       }
     }
     __syncthreads();
   }
 
   if constexpr (EPI == EPI_NONE) {
-    for (int idx = tid; idx < RB * M; idx += 256) {
-      const int m = idx / RB, row = idx - m * RB;
-      const int n = n0 + row;
-      if (n < N) a.y[(size_t)m * N + n] = f2act<DT>(yacc[row * YS + m]);
+    for (int e = tid; e < RB * M; e += blockDim.x) {
+      const int m = e / RB, row = e - m * RB;
+      if (n0 + row < N) a.y[(size_t)m * N + n0 + row] = f2act<DT>(yacc[m * YS + row]);
     }
-    return;
   } else {
     const EcParams& e = a.ec;
-    char* ec_smem = smem + gemv_lds_e_off(ngs, RT, MT);
+    char* ec_smem = smem + gemv_lds_e_off(NW, RT, MT, XLDS ? M : 0, a.ips);
     float* v_tile = (float*)(ec_smem + ec_lds_v_off(e.R1p, e.h));
-    const int ntb = (M + kTokTile - 1) / kTokTile;
-    bool have_v = true;
-    if constexpr (EPI == EPI_FUSED) {
-      // bounded wait for the EC workgroups; on time-out compute v here
-      if (tid == 0) {
-        int ok = 1;
-        for (int tb = 0; tb < ntb && ok; ++tb) {
-          int polls = 0;
-          while (__hip_atomic_load(e.flag + tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != e.epoch) {
-            if (++polls > a.wait_polls) { ok = 0; break; }
-            __builtin_amdgcn_s_sleep(8);
-          }
-        }
-        s_flag = ok;
+    uint16_t* bs = (uint16_t*)(ec_smem + ec_lds_bytes(e.R1p, e.h, r));  // [RB][r]
+    if (bpre) {
+#pragma unroll
+      for (int c = 0; c < BCH; ++c) {
+        const int ci = tid + c * (int)blockDim.x;
+        if (ci < bchunks) *(u32x4*)(bs + 8 * ci) = bst[c];
       }
       __syncthreads();
-      __threadfence();
-      have_v = s_flag != 0;
     }
-    const int r = a.r;
+    const int ntb = (M + kTokTile - 1) / kTokTile;
+    const uint32_t tag = ec_tag(gen);
+    const unsigned long long* vcopy =
+        e.vtag ? e.vtag + (size_t)(blockIdx.x % kVCopies) * ((size_t)M * r) : nullptr;
     for (int tb = 0; tb < ntb; ++tb) {
       const int m0 = tb * kTokTile, cnt = min(kTokTile, M - m0);
-      if (have_v) {
-        for (int idx = tid; idx < cnt * r; idx += 256) v_tile[idx] = e.v[(size_t)m0 * r + idx];
-        __syncthreads();
+      bool have = true;
+      if constexpr (EPI == EPI_FUSED) {
+        // bounded poll of the tagged coordinates; every thread checks its share
+        for (int poll = 0;; ++poll) {
+          int stale = 0;
+          for (int idx = tid; idx < cnt * r; idx += blockDim.x) {
+            const unsigned long long w = __hip_atomic_load(
+                const_cast<unsigned long long*>(vcopy) + (size_t)m0 * r + idx, __ATOMIC_RELAXED,
+                __HIP_MEMORY_SCOPE_AGENT);
+            if ((uint32_t)(w >> 32) != tag) stale = 1;
+            else v_tile[idx] = __uint_as_float((uint32_t)w);
+          }
+          if (!__syncthreads_or(stale)) break;
+          if (poll >= a.wait_polls) { have = false; break; }
+          __builtin_amdgcn_s_sleep(2);
+        }
+        if (!have) {
+          float* u_lds = (float*)(ec_smem + ec_lds_u_off());
+          float* hid = (float*)(ec_smem + ec_lds_hid_off(e.R1p));
+          ec_project_tile<DT>(e, tb, 0, IT, u_lds);
+          ec_gate_tile<DT>(e, cnt, u_lds, hid, v_tile);
+        }
       } else {
-        float* u_lds = (float*)(ec_smem + ec_lds_u_off());
-        float* hid = (float*)(ec_smem + ec_lds_hid_off(e.R1p));
-        ec_project_tile<DT>(e, tb, 0, IT, u_lds);
-        ec_gate_tile<DT>(e, cnt, u_lds, hid, v_tile);
+        for (int idx = tid; idx < cnt * r; idx += blockDim.x) v_tile[idx] = e.v[(size_t)m0 * r + idx];
+        __syncthreads();
       }
-      for (int idx = tid; idx < RB * cnt; idx += 256) {
+      for (int idx = tid; idx < RB * cnt; idx += blockDim.x) {
         const int t = idx / RB, row = idx - t * RB;
-        const int n = n0 + row;
-        if (n < N) {
-          float yv = yacc[row * YS + m0 + t];
-          const uint16_t* br = a.B + (size_t)n * r;
+        const int nn = n0 + row;
+        if (nn < N) {
+          float yv = yacc[(m0 + t) * YS + row];
+          const uint16_t* br = bpre ? bs + row * r : a.B + (size_t)nn * r;
           const float* vr = v_tile + t * r;
           for (int j = 0; j < r; ++j) yv += act2f<DT>(br[j]) * vr[j];
-          a.y[(size_t)(m0 + t) * N + n] = f2act<DT>(yv);
+          a.y[(size_t)(m0 + t) * N + nn] = f2act<DT>(yv);
         }
       }
       __syncthreads();
     }
   }
+  if constexpr (EPI == EPI_FUSED) fused_exit(a, gen);
 }
 
 // ---------------------------------------------------------------------------
@@ -641,35 +766,37 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams a) {
   const int n0 = (blockIdx.x % tiles_n) * kGemmTN;
   const int KT = K / kGemmTK;
 
-  // per-thread global load assignments
+  // per-thread global load assignments (bounds-checked buffer loads)
+  const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
+  const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * (K / 2));
+  const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
+  const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
   int xr[4], xc[4];
-  bool xv[4];
+  uint32_t xoff[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int c = tid + 256 * i;
     xr[i] = c >> 3;
     xc[i] = (c & 7) * 8;
-    xv[i] = m0 + xr[i] < M;
+    xoff[i] = m0 + xr[i] < M ? ((uint32_t)(m0 + xr[i]) * K + xc[i]) * 2 : kOOB;
   }
   const int wr = tid >> 1, wh = tid & 1;
   const int wn_row = n0 + wr;
   const bool wok = wn_row < N;
-  const uint32_t* wsrc = a.qw + (size_t)(wok ? wn_row : 0) * (K >> 3) + 4 * wh;
-  const size_t srow = (size_t)(wok ? wn_row : 0) * a.ngroups;
+  const uint32_t woff = wok ? (uint32_t)wn_row * (K / 2) + 16 * wh : kOOB;
 
   u32x4 xreg[4];
   u32x4 wreg;
   float sreg;
   int zreg;
   auto gload = [&](int kt) {
-    const int k0 = kt * kGemmTK;
+    const uint32_t k0 = (uint32_t)kt * kGemmTK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      xreg[i] = xv[i] ? ldg16(a.x + (size_t)(m0 + xr[i]) * K + k0 + xc[i]) : u32x4{0, 0, 0, 0};
-    wreg = wok ? ldg16(wsrc + (k0 >> 3)) : u32x4{0, 0, 0, 0};
-    const int g = k0 / a.G;
-    sreg = wok ? h2f(a.sc[srow + g]) : 0.f;
-    zreg = wok ? (int)a.zr[srow + g] : 0;
+    for (int i = 0; i < 4; ++i) xreg[i] = bld128(rx, xoff[i] + k0 * 2);
+    wreg = bld128(rq, woff + k0 / 2);
+    const uint32_t g = k0 / a.G;
+    sreg = h2f((uint16_t)bld16(rsc, wok ? ((uint32_t)wn_row * a.ngroups + g) * 2 : kOOB));
+    zreg = (int)bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
   };
   auto lstore = [&](int buf) {
     uint16_t* xs = Xs + buf * TILE;
@@ -800,13 +927,13 @@ hipError_t launch_dequant(int dt, const uint32_t* qw, const uint16_t* sc, const 
   return hipGetLastError();
 }
 
-hipError_t launch_ec(int dt, const EcParams& e, int ntb, size_t lds, hipStream_t st) {
+hipError_t launch_ec(int dt, const EcParams& e, int ntb, int block, size_t lds, hipStream_t st) {
   const unsigned grid = (unsigned)(ntb * e.P);
   if (grid == 0) return hipSuccess;
   SPEAR_DT_SWITCH(dt, {
     hipError_t err = allow_lds(k_ec<DTC>, lds);
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(k_ec<DTC>, dim3(grid), dim3(256), lds, st, e);
+    hipLaunchKernelGGL(k_ec<DTC>, dim3(grid), dim3(block), lds, st, e);
   });
   return hipGetLastError();
 }
@@ -831,31 +958,47 @@ hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, uint16_t*
   return hipGetLastError();
 }
 
-template <int DT, int MT, int RT>
-static hipError_t gemv_epi(int epi, const GemvParams& p, int grid, size_t lds, hipStream_t st) {
-  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, EPI_NONE>, lds)
-                   : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, EPI_READY>, lds)
-                                      : allow_lds(k_gemv<DT, MT, RT, EPI_FUSED>, lds);
+template <int DT, int MT, int RT, int U, bool XL>
+static hipError_t gemv_launch(int epi, const GemvParams& p, int grid, int block, size_t lds,
+                              hipStream_t st) {
+  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, U, XL, EPI_NONE>, lds)
+                   : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, U, XL, EPI_READY>, lds)
+                                      : allow_lds(k_gemv<DT, MT, RT, U, XL, EPI_FUSED>, lds);
   if (err != hipSuccess) return err;
   if (epi == EPI_NONE)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_NONE>), dim3(grid), dim3(256), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, U, XL, EPI_NONE>), dim3(grid), dim3(block), lds, st, p);
   else if (epi == EPI_READY)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_READY>), dim3(grid), dim3(256), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, U, XL, EPI_READY>), dim3(grid), dim3(block), lds, st, p);
   else
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_FUSED>), dim3(grid), dim3(256), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, U, XL, EPI_FUSED>), dim3(grid), dim3(block), lds, st, p);
   return hipGetLastError();
 }
 
-hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, size_t lds,
-                       hipStream_t st) {
+// The GEMV shapes compiled in: (MT, RT, U, XLDS). gemv_shape_supported()
+// mirrors this list for the planner.
+#define SPEAR_GEMV_SHAPES(X)                                                    \
+  X(1, 1, 1, true) X(1, 1, 2, true) X(1, 1, 4, true) X(1, 2, 1, true)           \
+  X(1, 2, 2, true) X(1, 4, 1, true) X(1, 4, 2, true)                             \
+  X(1, 1, 1, false) X(1, 1, 2, false) X(1, 2, 1, false) X(1, 2, 2, false)        \
+  X(1, 4, 1, false) X(2, 1, 1, false) X(2, 2, 1, false) X(2, 1, 2, false)        \
+  X(3, 1, 1, false) X(4, 1, 1, false)
+
+bool gemv_shape_supported(int MT, int RT, int U, bool XL) {
+#define SPEAR_GEMV_MATCH(mt, rt, u, xl) if (MT == mt && RT == rt && U == u && XL == xl) return true;
+  SPEAR_GEMV_SHAPES(SPEAR_GEMV_MATCH)
+#undef SPEAR_GEMV_MATCH
+  return false;
+}
+
+hipError_t launch_gemv(int dt, int MT, int RT, int U, bool XL, int epi, const GemvParams& p,
+                       int grid, int block, size_t lds, hipStream_t st) {
   if (grid == 0) return hipSuccess;
-  // supported (MT, RT): (1,4) (2,2) (3,1) (4,1)
-  SPEAR_DT_SWITCH(dt, {
-    if (MT == 1 && RT == 4) return gemv_epi<DTC, 1, 4>(epi, p, grid, lds, st);
-    if (MT == 2 && RT == 2) return gemv_epi<DTC, 2, 2>(epi, p, grid, lds, st);
-    if (MT == 3 && RT == 1) return gemv_epi<DTC, 3, 1>(epi, p, grid, lds, st);
-    if (MT == 4 && RT == 1) return gemv_epi<DTC, 4, 1>(epi, p, grid, lds, st);
-  });
+#define SPEAR_GEMV_CASE(mt, rt, u, xl)                                          \
+  if (MT == mt && RT == rt && U == u && XL == xl)                               \
+    return dt == DT_F16 ? gemv_launch<DT_F16, mt, rt, u, xl>(epi, p, grid, block, lds, st) \
+                        : gemv_launch<DT_BF16, mt, rt, u, xl>(epi, p, grid, block, lds, st);
+  SPEAR_GEMV_SHAPES(SPEAR_GEMV_CASE)
+#undef SPEAR_GEMV_CASE
   return hipErrorInvalidValue;
 }
 

@@ -29,7 +29,7 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
           -7: "SPEAR_E_HIP", -8: "SPEAR_E_ALIAS"}
 
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
-            "spear_set_wait_polls", "spear_status_string", "spear_version")
+            "spear_set_wait_polls", "spear_set_gemv_shape", "spear_status_string", "spear_version")
 
 
 class Problem(ctypes.Structure):
@@ -80,6 +80,8 @@ def _load():
                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
     lib.spear_w4_dequant.argtypes = [P(Problem), P(W4), ctypes.c_void_p, ctypes.c_void_p]
     lib.spear_set_wait_polls.argtypes = [ctypes.c_int32]
+    lib.spear_set_gemv_shape.argtypes = [ctypes.c_int32] * 4
+    lib.spear_set_gemv_shape.restype = None
     lib.spear_status_string.argtypes = [ctypes.c_int32]
     lib.spear_status_string.restype = ctypes.c_char_p
     lib.spear_version.restype = ctypes.c_char_p
@@ -166,6 +168,11 @@ def w4_dequant(prob: Problem, qweight, scales, zeros, w_out, stream=None):
 
 def set_wait_polls(polls: int) -> int:
     return int(LIB.spear_set_wait_polls(int(polls)))
+
+
+def set_gemv_shape(row_tiles=0, iters_per_wave=0, x_in_lds=-1, waves=0) -> None:
+    """Tuning override of the decode GEMV launch shape (0 / -1 = automatic)."""
+    LIB.spear_set_gemv_shape(int(row_tiles), int(iters_per_wave), int(x_in_lds), int(waves))
 
 
 def version() -> str:

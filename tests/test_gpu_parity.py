@@ -188,21 +188,28 @@ def test_fused_wait_fallback():
     assert_parity(y, ref, "fused fallback")
 
 
-def test_deterministic_and_stale_workspace():
-    """Repeated calls are bit-identical (fixed reduction orders), also when the
-    workspace holds garbage from elsewhere (epoch-tagged counters)."""
+def test_deterministic_and_workspace_reuse():
+    """Repeated calls are bit-identical (fixed reduction orders), also when
+    calls of other shapes use the same workspace in between: every counter is
+    back at zero after a call and every data region is rewritten before it is
+    read."""
     from paper_2606_11244_amd import spear as sp
-    L = S.make_layer(M=3, N=2048, K=4096, group_size=128, rank=16, seed=6)
-    dl = sp.DeviceLayer(L)
+    # K = 16384 spans two K-slices of the 4-bit product and two EC slices
+    L = S.make_layer(M=3, N=1024, K=16384, group_size=128, rank=16, seed=6)
+    other = S.make_layer(M=16, N=700, K=8192, group_size=128, rank=64, seed=7)
+    dl, do = sp.DeviceLayer(L), sp.DeviceLayer(other)
     prob = dl.problem(force_path=PATHS["fused_gemv"])
     plan = sp.dispatch_plan(prob)
     assert plan.split_k > 1 and plan.ec_splits > 1
-    ws = sp.allocate_workspace(prob)
+    size = max(plan.workspace_bytes, sp.dispatch_plan(do.problem()).workspace_bytes)
+    ws = torch.zeros(size, dtype=torch.uint8, device="cuda")
     log("determinism")
     first = gpu_y(L, PATHS["fused_gemv"], workspace=ws, dev=dl)
-    for i in range(5):
-        if i % 2:
-            ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, device="cuda"))
+    for i in range(4):
+        for p in (0, 3, 4):
+            gpu_y(other, p, workspace=ws, dev=do)
+        gpu_y(other, 0, with_ec=False, workspace=ws, dev=do)
+        gpu_y(L, 0, with_ec=False, workspace=ws, dev=dl)
         again = gpu_y(L, PATHS["fused_gemv"], workspace=ws, dev=dl)
         assert np.array_equal(first, again), i
     assert_parity(first, O.w4ec_linear(L), "determinism")
@@ -225,3 +232,76 @@ def test_streams_and_reuse():
     s.synchronize()
     for L, d in zip(layers, devs):
         assert_parity(d.y.float().cpu().numpy(), O.w4ec_linear(L), f"stream M={L.M}")
+
+
+@pytest.mark.parametrize("M,path", [(4, 1), (4, 4), (4, 3), (200, 0), (200, 3), (33, 1)])
+def test_graph_replay(M, path):
+    """A captured call replayed several times, with new activations written
+    between replays by eager work: every replay equals the eager call on the
+    same inputs bit for bit (counters and flags reset themselves, since a
+    graph keeps the epoch it was captured with)."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=M, N=1024, K=2048, group_size=128, rank=16, seed=M + path)
+    dl = sp.DeviceLayer(L)
+    prob = dl.problem(force_path=path)
+    ws = sp.allocate_workspace(prob)
+    y_eager = torch.empty_like(dl.y)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):  # warm-up outside capture
+        dl.run_ec(prob, ws, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dl.run_ec(prob, ws)
+    gen = torch.Generator(device="cuda").manual_seed(M)
+    for i in range(4):
+        dl.x.copy_(torch.randn(dl.x.shape, generator=gen, device="cuda").to(dl.x.dtype))
+        torch.cuda.synchronize()
+        log(f"graph M={M} path={path} replay={i}")
+        g.replay()
+        torch.cuda.synchronize()
+        y_graph = dl.y.clone()
+        dl.run_ec(prob, ws, y=y_eager)
+        torch.cuda.synchronize()
+        assert torch.equal(y_graph, y_eager), f"replay {i}"
+
+
+@pytest.mark.parametrize("M", [1, 16, 40])
+@pytest.mark.parametrize("K", [128, 8320, 16384, 28672])
+def test_long_and_short_k(M, K):
+    """K from a single 128-wide iteration to the 70B down projection's 28672:
+    one-wave blocks, partial last slices and multi-slice reductions."""
+    L = S.make_layer(M=M, N=96, K=K, group_size=128, rank=24, seed=K + M, ec_std=0.05)
+    ref = O.w4ec_linear(L)
+    for p in _paths_for(M):
+        log(f"K={K} M={M} path={p}")
+        assert_parity(gpu_y(L, p), ref, f"K={K} M={M} path={p}")
+
+
+GEMV_SHAPES = [(1, 1, 1, 1), (1, 1, 2, 1), (1, 1, 4, 1), (1, 2, 1, 1), (1, 2, 2, 1), (1, 4, 1, 1),
+               (1, 4, 2, 1), (1, 1, 1, 0), (1, 1, 2, 0), (1, 2, 1, 0), (1, 2, 2, 0), (1, 4, 1, 0),
+               (2, 1, 1, 0), (2, 2, 1, 0), (2, 1, 2, 0), (3, 1, 1, 0), (4, 1, 1, 0)]
+
+
+@pytest.mark.parametrize("shape", GEMV_SHAPES, ids=lambda t: "mt%d_rt%d_u%d_xl%d" % t)
+@pytest.mark.parametrize("waves", [4, 16])
+def test_every_gemv_launch_shape(shape, waves):
+    """Each compiled decode launch shape (row tiles, iterations per wave, x in
+    LDS or not, waves per block) meets the bar on ragged rows, with and
+    without K-slices, for the 4-bit-only and both EC paths."""
+    from paper_2606_11244_amd import spear as sp
+    mt, rt, u, xl = shape
+    M = {1: 3 if xl else 9, 2: 20, 3: 40, 4: 64}[mt]
+    sp.set_gemv_shape(rt, u, xl, waves)
+    try:
+        for K in (1024, 8192):
+            L = S.make_layer(M=M, N=200, K=K, group_size=128, rank=16, seed=K + rt, ec_std=0.05)
+            ref = O.w4ec_linear(L)
+            for p in (1, 4):
+                log(f"shape={shape} waves={waves} K={K} path={p}")
+                assert_parity(gpu_y(L, p), ref, f"shape={shape} K={K} path={p}")
+            assert_parity(gpu_y(L, 0, with_ec=False), O.w4_linear_layer(L), f"shape={shape} w4")
+    finally:
+        sp.set_gemv_shape(0, 0, -1, 0)
