@@ -174,13 +174,12 @@ spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w
 int32_t spear_set_wait_polls(int32_t polls);
 
 /* Tuning hook for the decode GEMV's launch shape, process-wide: 16-row
- * tiles per workgroup, 128-wide K iterations per wave, activations staged in
- * LDS (1), loaded per wave (0) or chosen automatically (-1), and waves per
- * workgroup. 0 (or -1 for x_in_lds) restores the planner's choice for that
- * field. A combination that is not compiled in makes the planner and the
- * calls return SPEAR_E_UNSUPPORTED. For measurement sweeps only. */
-void spear_set_gemv_shape(int32_t row_tiles, int32_t iters_per_wave, int32_t x_in_lds,
-                          int32_t waves);
+ * tiles per workgroup (1, 2 or 4 for up to 32 tokens; 1 or 2 above), K-slices
+ * per row group, and waves per workgroup (1..8). 0 restores the planner's
+ * choice for that field. A combination that is not compiled in makes the
+ * planner and the calls return SPEAR_E_UNSUPPORTED. For measurement sweeps
+ * only. */
+void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves);
 
 /* Static text for a status code. */
 const char* spear_status_string(spear_status_t status);

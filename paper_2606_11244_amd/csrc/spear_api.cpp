@@ -17,9 +17,9 @@ namespace {
 
 std::atomic<uint32_t> g_epoch{0};
 std::atomic<int32_t> g_wait_polls{1 << 16};
-// tuning override of the GEMV shape (0 = automatic): row tiles, iterations
-// per wave, x staged in LDS (1) or not (0, -1 = automatic), waves per block
-std::atomic<int32_t> g_ov_rt{0}, g_ov_u{0}, g_ov_xl{-1}, g_ov_nw{0};
+// tuning override of the GEMV shape (0 = automatic): row tiles per block,
+// K-slices per row group, waves per block
+std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0};
 
 // Every call gets a fresh non-zero epoch (a zero-filled workspace holds epoch 0).
 uint32_t next_epoch() {
@@ -42,8 +42,7 @@ struct Resolved {
   spear_plan_t plan;
   bool ec, gemv;
   int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
-  int MT, RT, U, NW, nrg, S, ips, ntb, P, eips, n_prod, ec_block;
-  bool XL;
+  int MT, RT, NW, nrg, S, ips, iw, ntb, P, eips, n_prod, ec_block;
   size_t off_gen, off_vtag, off_ectr, off_done, off_rbctr, off_upart, off_v, off_vh, off_vl, off_u,
       off_ypart;
   size_t lds_gemv, lds_ec;
@@ -106,37 +105,23 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
 
   // 4-bit product shape
   if (z.gemv) {
-    // A block owns RT 16-row tiles and a K-slice of NW * U iterations (128 K
-    // each); x goes through LDS for at most 4 tokens. Blocks are sized so
-    // that the grid covers the 256 CUs where the layer allows it.
+    // A block owns RT 16-row tiles and a K-slice; its NW waves each pipeline
+    // a contiguous chunk of iw iterations (128 K each). K-slices are added
+    // until about 4096 waves cover the 256 CUs, keeping at least two
+    // iterations per wave so that the pipeline has something to overlap.
     z.MT = (int)cdiv(M, 16);
-    z.NW = 16;
-    z.XL = M <= 4;
-    if (z.MT == 1) {
-      z.U = z.IT <= 16 ? 1 : (z.IT <= 32 ? 2 : 4);
-      if (!z.XL && z.U == 4) z.U = 2;
-    } else if (z.MT == 2) {
-      z.U = z.IT <= 16 ? 1 : 2;
-    } else {
-      z.U = 1;
-    }
-    const int S0 = (int)cdiv(z.IT, z.NW * z.U);
-    z.RT = 1;
-    for (int rt : {4, 2}) {
-      if (gemv_shape_supported(z.MT, rt, z.U, z.XL) && cdiv(N, 16 * rt) * S0 >= 256) {
-        z.RT = rt;
-        break;
-      }
-    }
+    z.NW = 8;
+    z.RT = z.MT <= 2 ? 2 : 1;
     if (g_ov_rt.load() > 0) z.RT = g_ov_rt.load();
-    if (g_ov_u.load() > 0) z.U = g_ov_u.load();
-    if (g_ov_xl.load() >= 0) z.XL = g_ov_xl.load() != 0 && M <= 4;
-    if (g_ov_nw.load() > 0) z.NW = std::min(16, g_ov_nw.load());
-    if (!gemv_shape_supported(z.MT, z.RT, z.U, z.XL)) return SPEAR_E_UNSUPPORTED;
-    z.ips = z.NW * z.U;
-    z.S = (int)cdiv(z.IT, z.ips);
+    if (g_ov_nw.load() > 0) z.NW = std::max(1, std::min(8, (int)g_ov_nw.load()));
+    if (!gemv_shape_supported(z.MT, z.RT)) return SPEAR_E_UNSUPPORTED;
     z.nrg = (int)cdiv(N, 16 * z.RT);
-    z.lds_gemv = gemv_lds_e_off(z.NW, z.RT, z.MT, z.XL ? (int)M : 0, z.ips);
+    int S = (int)std::lround(4096.0 / ((double)z.nrg * z.NW));
+    S = std::max(1, std::min(S, std::max(1, z.IT / (2 * z.NW))));
+    if (g_ov_s.load() > 0) S = std::min((int)g_ov_s.load(), z.IT);
+    z.ips = (int)cdiv(z.IT, S);
+    z.S = (int)cdiv(z.IT, z.ips);
+    z.iw = (int)cdiv(z.ips, z.NW);
     z.plan.split_k = z.S;
     z.plan.tile_m = 16 * z.MT;
     z.plan.tile_n = 16 * z.RT;
@@ -152,8 +137,9 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   z.ntb = (int)cdiv(M, kTokTile);
   if (z.ec) {
     if (z.gemv) {
-      z.ec_block = (path == SPEAR_PATH_FUSED_GEMV) ? 64 * z.NW : 1024;
-      const int per_block = 4 * (z.ec_block / 64);
+      // EC blocks: at most two 128-wide iterations per wave
+      z.ec_block = (path == SPEAR_PATH_FUSED_GEMV) ? 64 * z.NW : 512;
+      const int per_block = 2 * (z.ec_block / 64);
       z.P = (int)cdiv(z.IT, per_block);
       z.eips = (int)cdiv(z.IT, z.P);
       z.P = (int)cdiv(z.IT, z.eips);
@@ -163,8 +149,14 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
       z.eips = z.IT;
     }
     z.lds_ec = ec_lds_bytes(z.R1p, z.h, z.r);
-    // EC block carve-up, then the epilogue's prefetched rows of B
-    if (z.gemv) z.lds_gemv += z.lds_ec + align_up((size_t)16 * z.RT * z.r * 2, 16);
+  }
+  if (z.gemv) {
+    // EC block carve-up and the epilogue's rows of B, then the staged
+    // scales/zero points of one block (groups of its K-slice)
+    const int ipg = z.G / kIterK;
+    const int ngb = (int)std::min<int64_t>(z.ngroups, cdiv(z.ips, ipg) + 1);
+    z.lds_gemv = gemv_lds_sz_off(z.NW, z.RT, z.MT, z.R1p, z.h, z.r, z.ec) +
+                 (size_t)16 * z.RT * (ngb | 1) * 4;
   }
   z.plan.ec_splits = z.ec ? z.P : 0;
 
@@ -317,6 +309,7 @@ GemvParams make_gemv(const spear_problem_t* p, const Resolved& z, const void* x,
   g.B = ec ? (const uint16_t*)ec->B : nullptr;
   g.S = z.S;
   g.ips = z.ips;
+  g.iw = z.iw;
   g.epoch = epoch;
   g.wait_polls = g_wait_polls.load();
   if (ws && z.S > 1) {
@@ -356,8 +349,8 @@ spear_status_t run_w4(const spear_problem_t* p, const Resolved& z, const void* x
                       void* y, char* ws, uint32_t epoch, hipStream_t st) {
   if (z.gemv) {
     GemvParams g = make_gemv(p, z, x, w, y, nullptr, ws, epoch);
-    return hip_status(launch_gemv(z.dt, z.MT, z.RT, z.U, z.XL, EPI_NONE, g, z.nrg * z.S, 64 * z.NW,
-                                  z.lds_gemv, st));
+    return hip_status(
+        launch_gemv(z.dt, z.MT, z.RT, EPI_NONE, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, st));
   }
   GemmParams g = make_gemm(p, z, x, w, y, nullptr, nullptr);
   return hip_status(launch_gemm(z.dt, EPI_NONE, g, st));
@@ -414,8 +407,8 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
     g.done_ctr = (uint32_t*)(ws + z.off_done);
     g.grid_total = z.n_prod + z.nrg * z.S;
     const size_t lds = std::max(z.lds_gemv, z.lds_ec);
-    return hip_status(launch_gemv(z.dt, z.MT, z.RT, z.U, z.XL, EPI_FUSED, g, g.grid_total,
-                                  64 * z.NW, lds, s));
+    return hip_status(
+        launch_gemv(z.dt, z.MT, z.RT, EPI_FUSED, g, g.grid_total, 64 * z.NW, lds, s));
   }
   if (path == SPEAR_PATH_UNFUSED_2K) {
     if (!z.gemv) {
@@ -427,8 +420,8 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
     if (z.gemv) {
       GemvParams g = make_gemv(prob, z, x, w, y, ec, ws, epoch);
       g.ec = e;
-      return hip_status(launch_gemv(z.dt, z.MT, z.RT, z.U, z.XL, EPI_READY, g, z.nrg * z.S,
-                                    64 * z.NW, z.lds_gemv, s));
+      return hip_status(
+          launch_gemv(z.dt, z.MT, z.RT, EPI_READY, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, s));
     }
     GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
     return hip_status(launch_gemm(z.dt, EPI_READY, g, s));
@@ -472,11 +465,9 @@ spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w
 
 int32_t spear_set_wait_polls(int32_t polls) { return g_wait_polls.exchange(polls < 0 ? 0 : polls); }
 
-void spear_set_gemv_shape(int32_t row_tiles, int32_t iters_per_wave, int32_t x_in_lds,
-                          int32_t waves) {
+void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves) {
   g_ov_rt = row_tiles > 0 ? row_tiles : 0;
-  g_ov_u = iters_per_wave > 0 ? iters_per_wave : 0;
-  g_ov_xl = x_in_lds < 0 ? -1 : (x_in_lds ? 1 : 0);
+  g_ov_s = k_slices > 0 ? k_slices : 0;
   g_ov_nw = waves > 0 ? waves : 0;
 }
 

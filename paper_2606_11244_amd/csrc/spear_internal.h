@@ -72,7 +72,7 @@ struct GemvParams {
   uint16_t* y;            // [M][N]
   const uint16_t* B;      // [N][r]
   int M, N, K, G, ngroups, r;
-  int S, ips;             // K-slices per row tile and iterations per slice
+  int S, ips, iw;         // K-slices per row group, iterations per slice and per wave
   int n_prod;             // EC workgroups at the head of the grid (fused)
   float* ypart;           // [S][M][N] partial sums (S > 1)
   uint32_t* rb_ctr;       // [row tiles] last-arriver counters
@@ -106,28 +106,31 @@ __host__ __device__ inline size_t ec_lds_bytes(int R1p, int h, int r) {
 }
 
 // LDS carve-up of a GEMV block of NW waves and RT row tiles:
-//   X:    (XLDS) the block's slice of x, [M + 1][ips*128 + 8] fp16
-//   red:  per-wave partial tiles, NW x RT x MT x 1 KB (reuses X)
+//   red:  per-wave partial tiles, NW x RT x MT x 1 KB
 //   yacc: the block's sums [16*MT tokens][16*RT rows] fp32
-//   E:    an EC block (v tile for the epilogue; u/hidden for the fallback)
-__host__ __device__ inline size_t gemv_lds_a_bytes(int NW, int RT, int MT, int xl_rows, int ips) {
-  const size_t x = xl_rows > 0 ? align_up((size_t)(xl_rows + 1) * (ips * kIterK + 8) * 2, 16) : 0;
-  const size_t red = (size_t)NW * RT * MT * 1024;
-  return x > red ? x : red;
+//   E:    an EC block (v tile for the epilogue; u/hidden for the fallback),
+//         then the epilogue's rows of B
+__host__ __device__ inline size_t gemv_lds_y_off(int NW, int RT, int MT) {
+  return (size_t)NW * RT * MT * 1024;
 }
-__host__ __device__ inline size_t gemv_lds_y_off(int NW, int RT, int MT, int xl_rows, int ips) {
-  return gemv_lds_a_bytes(NW, RT, MT, xl_rows, ips);
+__host__ __device__ inline size_t gemv_lds_e_off(int NW, int RT, int MT) {
+  return gemv_lds_y_off(NW, RT, MT) + (size_t)RT * MT * 1024;
 }
-__host__ __device__ inline size_t gemv_lds_e_off(int NW, int RT, int MT, int xl_rows, int ips) {
-  return gemv_lds_y_off(NW, RT, MT, xl_rows, ips) + (size_t)RT * MT * 1024;
+// after E (and B, when the EC is on): the staged scales/zero points
+// [16*RT rows][groups of the block's K-slice] as u32
+__host__ __device__ inline size_t gemv_lds_sz_off(int NW, int RT, int MT, int R1p, int h, int r,
+                                                  bool ec) {
+  size_t o = gemv_lds_e_off(NW, RT, MT);
+  if (ec) o += ec_lds_bytes(R1p, h, r) + align_up((size_t)16 * RT * r * 2, 16);
+  return align_up(o, 16);
 }
 
 hipError_t launch_dequant(int dt, const uint32_t* qw, const uint16_t* sc, const uint8_t* zr,
                           uint16_t* out, int N, int K, int G, hipStream_t st);
 hipError_t launch_ec(int dt, const EcParams& e, int ntb, int block, size_t lds, hipStream_t st);
-bool gemv_shape_supported(int MT, int RT, int U, bool XL);
-hipError_t launch_gemv(int dt, int MT, int RT, int U, bool XL, int epi, const GemvParams& p,
-                       int grid, int block, size_t lds, hipStream_t st);
+bool gemv_shape_supported(int MT, int RT);
+hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, int block,
+                       size_t lds, hipStream_t st);
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st);
 hipError_t launch_gate(int dt, const EcParams& e, int ntb, size_t lds, hipStream_t st);
 hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, uint16_t* y, int M,

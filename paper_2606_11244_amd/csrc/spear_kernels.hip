@@ -82,6 +82,23 @@ __device__ __forceinline__ u32x4 unpack_biased(uint32_t w) {
   r[3] = ((w >> 12) & 0x000F000Fu) | kMag;
   return r;
 }
+// Same, with the mask and the magic number in registers (`km` = 0x000F000F,
+// `kg` = the magic pair): each code pair is then one v_and_or_b32 (plus a
+// shift), which the literal-constant form above does not compile to.
+__device__ __forceinline__ u32x4 unpack_biased_r(uint32_t w, uint32_t km, uint32_t kg) {
+  u32x4 r;
+  r[0] = (w & km) | kg;
+  r[1] = ((w >> 4) & km) | kg;
+  r[2] = ((w >> 8) & km) | kg;
+  r[3] = ((w >> 12) & km) | kg;
+  return r;
+}
+// Opaque copy of a constant in a VGPR (the compiler cannot fold it back into
+// an instruction literal).
+__device__ __forceinline__ uint32_t opaque_v(uint32_t c) {
+  asm volatile("" : "+v"(c));
+  return c;
+}
 template <int DT>
 __device__ __forceinline__ constexpr float code_bias() { return DT == DT_F16 ? 1024.f : 128.f; }
 
@@ -114,6 +131,16 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
 }
 __device__ __forceinline__ u32x4 bld128(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+// voffset (per lane, carries the mask) + soffset (wave-uniform)
+__device__ __forceinline__ u32x4 bld128s(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+__device__ __forceinline__ uint32_t bld16s(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
+__device__ __forceinline__ uint32_t bld8s(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b8(r, voff, soff, 0);
 }
 __device__ __forceinline__ uint32_t bld16(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
@@ -194,6 +221,10 @@ __global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ qw
 // u_lds[t][j] = sum_k x[16*tb + t][k] * R[j][k], R = [A; w_g] (R1 rows), as a
 // sum over the block's waves in a fixed order (wave 0 first).
 // ---------------------------------------------------------------------------
+// Row tiles of [A; w_g] projected together (bounds the registers the
+// two-iteration load batch needs).
+constexpr int kEcTiles = 2;
+
 template <int DT>
 __device__ void ec_project_tile(const EcParams& e, int tb, int it_beg, int it_end, float* u_lds) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -205,47 +236,62 @@ __device__ void ec_project_tile(const EcParams& e, int tb, int it_beg, int it_en
   const rsrc_t ra = make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
   const rsrc_t rg = make_rsrc(e.wg, e.gate == GATE_SIGMOID ? (uint32_t)e.K * 2 : 0u);
   const uint32_t xoff = m < e.M ? (uint32_t)m * e.K * 2 + 64 * lg : kOOB;
-  for (int tg0 = 0; tg0 < RTe; tg0 += 4) {
-    const int nt = min(4, RTe - tg0);
-    f32x4 acc[4];
+  for (int tg0 = 0; tg0 < RTe; tg0 += kEcTiles) {
+    const int nt = min(kEcTiles, RTe - tg0);
+    f32x4 acc[kEcTiles];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    uint32_t aoff[4], goff[4];
-    bool has_g[4];
+    for (int t = 0; t < kEcTiles; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    uint32_t aoff[kEcTiles], goff[kEcTiles];
+    bool has_g[kEcTiles];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < kEcTiles; ++t) {
       const int j = (tg0 + t) * 16 + lr;
       aoff[t] = j < e.r ? (uint32_t)j * e.K * 2 + 64 * lg : kOOB;
       goff[t] = (j == e.r && e.gate == GATE_SIGMOID) ? 64u * lg : kOOB;
       // uniform: does this row tile hold the gate row w_g?
       has_g[t] = e.gate == GATE_SIGMOID && e.r >= (tg0 + t) * 16 && e.r < (tg0 + t + 1) * 16;
     }
-    for (int it = it_beg + wave; it < it_end; it += NW) {
+    // two iterations per pass with all of their loads issued first
+    for (int it = it_beg + wave; it < it_end; it += 2 * NW) {
+      const int it2 = it + NW;
       const uint32_t kb = (uint32_t)it * (kIterK * 2);
-      u32x4 xv[4];
+      const uint32_t kb2 = (uint32_t)it2 * (kIterK * 2);
+      const bool ok2 = it2 < it_end;
+      u32x4 xv[2][4], av[2][kEcTiles][4];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) xv[jj] = bld128(rx, xoff + kb + 16 * jj);
+      for (int jj = 0; jj < 4; ++jj) {
+        xv[0][jj] = bld128(rx, xoff + kb + 16 * jj);
+        xv[1][jj] = bld128(rx, ok2 ? xoff + kb2 + 16 * jj : kOOB);
+      }
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
+      for (int t = 0; t < kEcTiles; ++t) {
         if (t < nt) {
-          u32x4 av[4];
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) av[jj] = bld128(ra, aoff[t] + kb + 16 * jj);
-          if (has_g[t]) {
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) av[jj] |= bld128(rg, goff[t] + kb + 16 * jj);
+          for (int jj = 0; jj < 4; ++jj) {
+            av[0][t][jj] = bld128(ra, aoff[t] + kb + 16 * jj);
+            av[1][t][jj] = bld128(ra, ok2 ? aoff[t] + kb2 + 16 * jj : kOOB);
+            if (has_g[t]) {
+              av[0][t][jj] |= bld128(rg, goff[t] + kb + 16 * jj);
+              av[1][t][jj] |= bld128(rg, ok2 ? goff[t] + kb2 + 16 * jj : kOOB);
+            }
           }
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) acc[t] = mfma16<DT>(av[jj], xv[jj], acc[t]);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int t = 0; t < kEcTiles; ++t)
+          if (t < nt)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) acc[t] = mfma16<DT>(av[h][t][jj], xv[h][jj], acc[t]);
     }
     // deterministic cross-wave sum: wave 0 stores, waves 1.. add in order
     for (int w = 0; w < NW; ++w) {
       __syncthreads();
       if (wave == w) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < kEcTiles; ++t) {
           if (t < nt) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -375,7 +421,7 @@ __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
 }
 
 template <int DT>
-__global__ __launch_bounds__(1024) void k_ec(EcParams e) {
+__global__ __launch_bounds__(512) void k_ec(EcParams e) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   ec_block<DT>(e, blockIdx.x / e.P, blockIdx.x % e.P, smem);
 }
@@ -422,18 +468,17 @@ __device__ __forceinline__ void fused_exit(const GemvParams& a, uint32_t gen) {
 
 // ---------------------------------------------------------------------------
 // Decode GEMV. A block owns RT row tiles (16 rows each) and a K-slice of
-// NW*U iterations (128 K each); each of its NW waves takes U consecutive
-// iterations of all RT tiles and issues every load before computing, so a
-// wave keeps RT*U KB of codes in flight. The MFMA multiplies activations (A
-// operand, 16 token rows) by the biased codes (B operand, 16 weight rows as
-// columns), so each lane owns one weight row per tile and needs one scale
-// and one zero point per iteration:
+// iterations (128 K each); each of its NW waves walks a contiguous chunk of
+// that slice as a software pipeline: the codes, scales, zero points and
+// activation fragments of iteration it+1 are in flight while iteration it is
+// computed, so memory and compute overlap within every wave. The MFMA
+// multiplies activations (A operand, 16 token rows) by the biased codes (B
+// operand, 16 weight rows as columns), so each lane owns one weight row per
+// tile and needs one scale and one zero point per iteration:
 //   sum_k x (q - z) s = s * ( sum_k x (bias + q) - (bias + z) * sum_k x ),
-// with sum_k x from an MFMA against ones; the activation fragments are shared
-// by the RT tiles. With XLDS (at most 4 tokens) the block stages its slice of
-// x in LDS once instead of every wave loading mostly-empty fragments. Waves
-// are reduced in LDS in a fixed order; K-slices (only when K exceeds one
-// block's NW*U iterations) through partial sums and a last arriver.
+// with sum_k x from an MFMA against ones, shared by the RT tiles. Waves are
+// reduced in LDS in a fixed order; K-slices through partial sums and a last
+// arriver.
 //
 // Fused variant: the first n_prod blocks of the grid are EC blocks (above).
 // The others, after their main loop, poll the tagged EC coordinates of their
@@ -441,11 +486,12 @@ __device__ __forceinline__ void fused_exit(const GemvParams& a, uint32_t gen) {
 // B v in the epilogue. Every block arrives at a done counter at its end; the
 // last one advances the generation that tags the next launch's coordinates.
 // ---------------------------------------------------------------------------
-template <int DT, int MT, int RT, int U, bool XLDS, int EPI>
-__global__ __launch_bounds__(1024) void k_gemv(GemvParams a) {
+template <int DT, int MT, int RT, int EPI>
+__global__ __launch_bounds__(512) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int s_flag;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int NW = blockDim.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   int bid = blockIdx.x;
@@ -466,64 +512,17 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvParams a) {
   const int n0 = rg * RB;
   const int it_blk = s * a.ips;
   const int it_end = min(IT, it_blk + a.ips);
-  const int it_w = it_blk + wave * U;
+  const int iw_beg = it_blk + wave * a.iw;
+  const int iw_end = min(it_end, iw_beg + a.iw);
 
-  // ---- issue every load of this block (masked lanes read zeros)
   const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * (K / 2));
   const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
   const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
   const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
-  u32x4 wv[RT][U];
-  uint32_t sv[RT][U], zv[RT][U];
-#pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    const int n = n0 + 16 * t + lr;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int it = it_w + u;
-      const bool ok = n < N && it < it_end;
-      const uint32_t g = (uint32_t)(it * kIterK) / G;
-      wv[t][u] = bld128(rq, ok ? (uint32_t)n * (K / 2) + (uint32_t)it * (kIterK / 2) + 16 * lg : kOOB);
-      sv[t][u] = bld16(rsc, ok ? ((uint32_t)n * a.ngroups + g) * 2 : kOOB);
-      zv[t][u] = bld8(rz, ok ? (uint32_t)n * a.ngroups + g : kOOB);
-    }
-  }
-  // activations: either per-wave fragments, or the block's slice via LDS
-  constexpr int XM = XLDS ? 1 : MT;
-  constexpr int XU = XLDS ? 1 : U;
-  u32x4 xv[XM][XU][4];
-  // staged 16-byte chunks per thread: M <= 4 rows of ips * 16 chunks over
-  // 64 * NW threads, ips = NW * U, so at most U
-  constexpr int XCH = XLDS ? U : 1;
-  u32x4 xst[XCH];
-  const int xrow_h = a.ips * kIterK + 8;  // LDS row stride (halves) of the x slice
-  const int xchunks_row = a.ips * (kIterK / 8);
-  if constexpr (XLDS) {
-#pragma unroll
-    for (int c = 0; c < XCH; ++c) {
-      const int ci = tid + c * (int)blockDim.x;
-      const int row = ci / xchunks_row, col = ci - row * xchunks_row;
-      const int k = it_blk * kIterK + 8 * col;
-      const bool ok = row < M && k < it_end * kIterK;
-      xst[c] = bld128(rx, ok ? ((uint32_t)row * K + k) * 2 : kOOB);
-    }
-  } else {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = 16 * mt + lr;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int it = it_w + u;
-        const uint32_t base = (m < M && it < it_end)
-                                  ? ((uint32_t)m * K + (uint32_t)it * kIterK + 32 * lg) * 2 : kOOB;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) xv[mt][u][jj] = bld128(rx, base + 16 * jj);
-      }
-    }
-  }
-  // the EC epilogue's rows of B ([16*RT][r], fp16/bf16) ride along with the
-  // main loads when r is a multiple of 8 and two 16-byte chunks per thread
-  // cover them; otherwise the epilogue reads B directly
+
+  // the EC epilogue's rows of B ([16*RT][r], fp16/bf16) are fetched up front
+  // when r is a multiple of 8 and two 16-byte chunks per thread cover them;
+  // otherwise the epilogue reads B directly
   constexpr int BCH = 2;
   const int r = a.r;
   const int bchunks = EPI != EPI_NONE && (r & 7) == 0 ? RB * r / 8 : 0;
@@ -537,60 +536,85 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvParams a) {
       bst[c] = bld128(rb, ci < bchunks ? (uint32_t)n0 * r * 2 + 16u * ci : kOOB);
     }
   }
-  // keep the scheduler from sinking these loads next to their uses: all of
-  // them must be in flight before the first wait
-  __builtin_amdgcn_sched_barrier(0);
 
-  uint16_t* xs = (uint16_t*)smem;  // XLDS: [M + 1][xrow_h], row M all zero
-  if constexpr (XLDS) {
+  // one batch = one 128-wide iteration of every row tile: codes, scales,
+  // zero points and the activation fragments. The per-lane part of every
+  // offset (row, token, lane group; kOOB for rows >= N or tokens >= M) is
+  // fixed for the whole loop; the iteration enters as a wave-uniform soffset.
+  uint32_t vw[RT], vx[MT];
 #pragma unroll
-    for (int c = 0; c < XCH; ++c) {
-      const int ci = tid + c * (int)blockDim.x;
-      const int row = ci / xchunks_row, col = ci - row * xchunks_row;
-      if (row < M) *(u32x4*)(xs + row * xrow_h + 8 * col) = xst[c];
-    }
-    for (int ci = tid; ci < xchunks_row; ci += blockDim.x)
-      *(u32x4*)(xs + M * xrow_h + 8 * ci) = u32x4{0, 0, 0, 0};
-    __syncthreads();
+  for (int t = 0; t < RT; ++t) {
+    const int n = n0 + 16 * t + lr;
+    vw[t] = n < N ? (uint32_t)n * (K / 2) + 16 * lg : kOOB;
   }
+  // lanes of tokens >= M read the last token's row: their MFMA rows only feed
+  // outputs that are never stored, and in-bounds duplicate addresses are far
+  // cheaper for the address unit than masked (out-of-range) lanes
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = min(16 * mt + lr, M - 1);
+    vx[mt] = ((uint32_t)m * K + 32 * lg) * 2;
+  }
+  auto load = [&](u32x4 (&w)[RT], u32x4 (&xv)[MT][4], int it) {
+#pragma unroll
+    for (int t = 0; t < RT; ++t) w[t] = bld128s(rq, vw[t], (uint32_t)it * (kIterK / 2));
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        xv[mt][jj] = bld128s(rx, vx[mt] + 16 * jj, (uint32_t)it * (kIterK * 2));
+  };
 
-  // ---- compute
+  // scales and zero points of the block's rows and groups, staged once in
+  // LDS with coalesced loads ([row][group] as s | z << 16): per-iteration
+  // scattered 2- and 1-byte loads would cost a cache-line request per row
+  const int ipg = G / kIterK;  // iterations per quantisation group
+  const int g_lo = it_blk / ipg;
+  const int ngb = (it_end - 1) / ipg + 1 - g_lo;
+  const int ngs = ngb | 1;  // odd LDS row stride: rows fall on distinct banks
+  uint32_t* szs = (uint32_t*)(smem + gemv_lds_sz_off(NW, RT, MT, a.ec.R1p, a.ec.h, r, EPI != EPI_NONE));
+  // the first batch goes out before the staging loads so that both overlap
+  u32x4 wA[RT], wB[RT];
+  u32x4 xA[MT][4], xB[MT][4];
+  if (iw_beg < iw_end) load(wA, xA, iw_beg);
+  for (int idx = tid; idx < RB * ngb; idx += blockDim.x) {
+    const int row = idx / ngb, gg = idx - row * ngb;
+    const int n = n0 + row;
+    const uint32_t e = (uint32_t)n * a.ngroups + g_lo + gg;
+    const uint32_t sv = bld16(rsc, n < N ? e * 2 : kOOB);
+    const uint32_t zv = bld8(rz, n < N ? e : kOOB);
+    szs[row * ngs + gg] = sv | (zv << 16);
+  }
+  __syncthreads();
   constexpr float kBias = code_bias<DT>();
   f32x4 acc[RT][MT];
 #pragma unroll
   for (int t = 0; t < RT; ++t)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
+  const uint32_t km = opaque_v(0x000F000Fu);
+  const uint32_t kg = opaque_v(DT == DT_F16 ? 0x64006400u : 0x43004300u);
+  auto compute = [&](const u32x4 (&w)[RT], const u32x4 (&xv)[MT][4], int it) {
     f32x4 xb[MT];
     u32x4 xp[MT][4];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      u32x4 xf[4];
-      if constexpr (XLDS) {
-        const int row = lr < M ? lr : M;
-        const uint16_t* src = xs + row * xrow_h + (wave * U + u) * kIterK + 32 * lg;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) xf[jj] = *(const u32x4*)(src + 8 * jj);
-      } else {
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) xf[jj] = xv[mt][u][jj];
-      }
       xb[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        xb[mt] = mfma16<DT>(xf[jj], ones8<DT>(), xb[mt]);
-        xp[mt][jj] = pair_like_codes(xf[jj]);
+        xb[mt] = mfma16<DT>(xv[mt][jj], ones8<DT>(), xb[mt]);
+        xp[mt][jj] = pair_like_codes(xv[mt][jj]);
       }
     }
+    const int gg = it / ipg - g_lo;
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
       u32x4 wd[4];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) wd[jj] = unpack_biased<DT>(wv[t][u][jj]);
-      const float sf = h2f((uint16_t)sv[t][u]);
-      const float cf = kBias + (float)zv[t][u];
+      for (int jj = 0; jj < 4; ++jj) wd[jj] = unpack_biased_r(w[t][jj], km, kg);
+      const uint32_t sz = szs[(16 * t + lr) * ngs + gg];
+      const float sf = h2f((uint16_t)(sz & 0xFFFF));
+      const float cf = kBias + (float)(sz >> 16);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         f32x4 pacc = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -600,10 +624,26 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvParams a) {
         for (int i = 0; i < 4; ++i) acc[t][mt][i] += sf * (pacc[i] - cf * xb[mt][i]);
       }
     }
+  };
+
+  // software pipeline over this wave's iterations: batch it+1 is in flight
+  // while batch it is computed (two register sets, alternating). Loads past
+  // the wave's last iteration re-read that iteration (never computed), so
+  // every load is unconditional.
+  if (iw_beg < iw_end) {
+    const int last = iw_end - 1;
+    for (int it = iw_beg; it < iw_end; it += 2) {
+      load(wB, xB, min(it + 1, last));
+      __builtin_amdgcn_sched_barrier(0);
+      compute(wA, xA, it);
+      if (it + 1 >= iw_end) break;
+      load(wA, xA, min(it + 2, last));
+      __builtin_amdgcn_sched_barrier(0);
+      compute(wB, xB, it + 1);
+    }
   }
 
   // ---- cross-wave reduction (fixed order) into yacc[token][row]
-  if constexpr (XLDS) __syncthreads();  // the x slice is dead; reuse its LDS
   float* red = (float*)smem;
 #pragma unroll
   for (int t = 0; t < RT; ++t)
@@ -611,7 +651,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvParams a) {
     for (int mt = 0; mt < MT; ++mt)
       *(f32x4*)(red + (((wave * RT + t) * MT + mt) * 64 + lane) * 4) = acc[t][mt];
   __syncthreads();
-  float* yacc = (float*)(smem + gemv_lds_y_off(NW, RT, MT, XLDS ? M : 0, a.ips));
+  float* yacc = (float*)(smem + gemv_lds_y_off(NW, RT, MT));
   constexpr int YS = RB;  // yacc row stride: [token][RB rows]
   for (int e = tid; e < 256 * RT * MT; e += blockDim.x) {
     const int tm = e >> 8, rem = e & 255, ln = rem >> 2, i = rem & 3;
@@ -654,7 +694,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvParams a) {
     }
   } else {
     const EcParams& e = a.ec;
-    char* ec_smem = smem + gemv_lds_e_off(NW, RT, MT, XLDS ? M : 0, a.ips);
+    char* ec_smem = smem + gemv_lds_e_off(NW, RT, MT);
     float* v_tile = (float*)(ec_smem + ec_lds_v_off(e.R1p, e.h));
     uint16_t* bs = (uint16_t*)(ec_smem + ec_lds_bytes(e.R1p, e.h, r));  // [RB][r]
     if (bpre) {
@@ -958,45 +998,41 @@ hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, uint16_t*
   return hipGetLastError();
 }
 
-template <int DT, int MT, int RT, int U, bool XL>
+template <int DT, int MT, int RT>
 static hipError_t gemv_launch(int epi, const GemvParams& p, int grid, int block, size_t lds,
                               hipStream_t st) {
-  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, U, XL, EPI_NONE>, lds)
-                   : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, U, XL, EPI_READY>, lds)
-                                      : allow_lds(k_gemv<DT, MT, RT, U, XL, EPI_FUSED>, lds);
+  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, EPI_NONE>, lds)
+                   : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, EPI_READY>, lds)
+                                      : allow_lds(k_gemv<DT, MT, RT, EPI_FUSED>, lds);
   if (err != hipSuccess) return err;
   if (epi == EPI_NONE)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, U, XL, EPI_NONE>), dim3(grid), dim3(block), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_NONE>), dim3(grid), dim3(block), lds, st, p);
   else if (epi == EPI_READY)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, U, XL, EPI_READY>), dim3(grid), dim3(block), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_READY>), dim3(grid), dim3(block), lds, st, p);
   else
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, U, XL, EPI_FUSED>), dim3(grid), dim3(block), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_FUSED>), dim3(grid), dim3(block), lds, st, p);
   return hipGetLastError();
 }
 
-// The GEMV shapes compiled in: (MT, RT, U, XLDS). gemv_shape_supported()
-// mirrors this list for the planner.
-#define SPEAR_GEMV_SHAPES(X)                                                    \
-  X(1, 1, 1, true) X(1, 1, 2, true) X(1, 1, 4, true) X(1, 2, 1, true)           \
-  X(1, 2, 2, true) X(1, 4, 1, true) X(1, 4, 2, true)                             \
-  X(1, 1, 1, false) X(1, 1, 2, false) X(1, 2, 1, false) X(1, 2, 2, false)        \
-  X(1, 4, 1, false) X(2, 1, 1, false) X(2, 2, 1, false) X(2, 1, 2, false)        \
-  X(3, 1, 1, false) X(4, 1, 1, false)
+// The GEMV shapes compiled in: (token tiles MT, row tiles RT).
+// gemv_shape_supported() mirrors this list for the planner.
+#define SPEAR_GEMV_SHAPES(X) \
+  X(1, 1) X(1, 2) X(1, 4) X(2, 1) X(2, 2) X(2, 4) X(3, 1) X(3, 2) X(4, 1)
 
-bool gemv_shape_supported(int MT, int RT, int U, bool XL) {
-#define SPEAR_GEMV_MATCH(mt, rt, u, xl) if (MT == mt && RT == rt && U == u && XL == xl) return true;
+bool gemv_shape_supported(int MT, int RT) {
+#define SPEAR_GEMV_MATCH(mt, rt) if (MT == mt && RT == rt) return true;
   SPEAR_GEMV_SHAPES(SPEAR_GEMV_MATCH)
 #undef SPEAR_GEMV_MATCH
   return false;
 }
 
-hipError_t launch_gemv(int dt, int MT, int RT, int U, bool XL, int epi, const GemvParams& p,
-                       int grid, int block, size_t lds, hipStream_t st) {
+hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, int block,
+                       size_t lds, hipStream_t st) {
   if (grid == 0) return hipSuccess;
-#define SPEAR_GEMV_CASE(mt, rt, u, xl)                                          \
-  if (MT == mt && RT == rt && U == u && XL == xl)                               \
-    return dt == DT_F16 ? gemv_launch<DT_F16, mt, rt, u, xl>(epi, p, grid, block, lds, st) \
-                        : gemv_launch<DT_BF16, mt, rt, u, xl>(epi, p, grid, block, lds, st);
+#define SPEAR_GEMV_CASE(mt, rt)                                                     \
+  if (MT == mt && RT == rt)                                                         \
+    return dt == DT_F16 ? gemv_launch<DT_F16, mt, rt>(epi, p, grid, block, lds, st) \
+                        : gemv_launch<DT_BF16, mt, rt>(epi, p, grid, block, lds, st);
   SPEAR_GEMV_SHAPES(SPEAR_GEMV_CASE)
 #undef SPEAR_GEMV_CASE
   return hipErrorInvalidValue;

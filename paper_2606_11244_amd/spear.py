@@ -80,7 +80,7 @@ def _load():
                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
     lib.spear_w4_dequant.argtypes = [P(Problem), P(W4), ctypes.c_void_p, ctypes.c_void_p]
     lib.spear_set_wait_polls.argtypes = [ctypes.c_int32]
-    lib.spear_set_gemv_shape.argtypes = [ctypes.c_int32] * 4
+    lib.spear_set_gemv_shape.argtypes = [ctypes.c_int32] * 3
     lib.spear_set_gemv_shape.restype = None
     lib.spear_status_string.argtypes = [ctypes.c_int32]
     lib.spear_status_string.restype = ctypes.c_char_p
@@ -170,9 +170,9 @@ def set_wait_polls(polls: int) -> int:
     return int(LIB.spear_set_wait_polls(int(polls)))
 
 
-def set_gemv_shape(row_tiles=0, iters_per_wave=0, x_in_lds=-1, waves=0) -> None:
-    """Tuning override of the decode GEMV launch shape (0 / -1 = automatic)."""
-    LIB.spear_set_gemv_shape(int(row_tiles), int(iters_per_wave), int(x_in_lds), int(waves))
+def set_gemv_shape(row_tiles=0, k_slices=0, waves=0) -> None:
+    """Tuning override of the decode GEMV launch shape (0 = automatic)."""
+    LIB.spear_set_gemv_shape(int(row_tiles), int(k_slices), int(waves))
 
 
 def version() -> str:
