@@ -15,26 +15,26 @@ using namespace spear;
 
 namespace {
 
-std::atomic<uint32_t> g_epoch{0};
 std::atomic<int32_t> g_wait_polls{1 << 16};
 // tuning override of the GEMV shape (0 = automatic): row tiles per block,
 // K-slices per row group, waves per block
 std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0};
 
-// Every call gets a fresh non-zero epoch (a zero-filled workspace holds epoch 0).
-uint32_t next_epoch() {
-  uint32_t e;
-  do {
-    e = g_epoch.fetch_add(1) + 1;
-  } while (e == 0);
-  return e;
-}
-
 // Token counts at or below this run the 4-bit product as a split-K GEMV; above
 // it the LDS-tiled MFMA GEMM. The same bound separates decode (fully fused
 // EC) from prefill (semi-fused EC pre-kernel) under SPEAR_PATH_AUTO.
 constexpr int64_t kGemvMaxM = 64;
-constexpr int kTargetBlocks = 1024;  // about four resident blocks per CU
+// Largest staged slice of x in a GEMV block's LDS (16 tokens x 2048 K fit).
+constexpr size_t kXLdsMax = 66 * 1024;
+// Fused EC: the consumers gather the K-slices' partial sums themselves when
+// there are at most this many words per launch (slices x tokens x (r + 1)).
+constexpr int64_t kGatherMaxWords = 2048;
+constexpr int kEcWaves = 8;  // waves of an EC pre-kernel block (decode)
+constexpr size_t kMaxLds = 160 * 1024;  // LDS of one CU
+// Fused EC: consumers poll the published data directly (instead of a ready
+// counter) when it is at most this many words and the grid this small.
+constexpr int64_t kDirectMaxWords = 512;
+constexpr int kDirectMaxGrid = 512;
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -42,10 +42,12 @@ struct Resolved {
   spear_plan_t plan;
   bool ec, gemv;
   int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
-  int MT, RT, NW, nrg, S, ips, iw, ntb, P, eips, n_prod, ec_block;
-  size_t off_gen, off_vtag, off_ectr, off_done, off_rbctr, off_upart, off_v, off_vh, off_vl, off_u,
-      off_ypart;
-  size_t lds_gemv, lds_ec;
+  int MT, RT, NW, nrg, S, ips, iw;            // GEMV shape
+  int ntb, P, eips, PG, tpg, ec_mode, ec_ipp, ec_block, n_prod;  // EC shape
+  int xlds, xstride, bpre, lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz;
+  size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart;
+  int npub, direct;
+  size_t lds_gemv, lds_prod, lds_gate;
 };
 
 bool misaligned(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
@@ -102,6 +104,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     z.plan.num_launches = 0;
     return SPEAR_OK;
   }
+  const bool fused = z.ec && path == SPEAR_PATH_FUSED_GEMV;
 
   // 4-bit product shape
   if (z.gemv) {
@@ -113,8 +116,14 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     z.NW = 8;
     z.RT = z.MT <= 2 ? 2 : 1;
     if (g_ov_rt.load() > 0) z.RT = g_ov_rt.load();
-    if (g_ov_nw.load() > 0) z.NW = std::max(1, std::min(8, (int)g_ov_nw.load()));
     if (!gemv_shape_supported(z.MT, z.RT)) return SPEAR_E_UNSUPPORTED;
+    // the EC variants add the EC wave to the workgroup
+    const int epi = !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN ? EPI_NONE
+                    : path == SPEAR_PATH_FUSED_GEMV           ? EPI_FUSED
+                                                              : EPI_READY;
+    const int max_nw = kGemvMaxThreads / 64 - (epi != EPI_NONE ? 1 : 0);
+    z.NW = std::min(z.NW, max_nw);
+    if (g_ov_nw.load() > 0) z.NW = std::max(1, std::min(max_nw, (int)g_ov_nw.load()));
     z.nrg = (int)cdiv(N, 16 * z.RT);
     int S = (int)std::lround(4096.0 / ((double)z.nrg * z.NW));
     S = std::max(1, std::min(S, std::max(1, z.IT / (2 * z.NW))));
@@ -131,32 +140,85 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     z.plan.tile_n = kGemmTN;
   }
 
-  // EC projection shape: per 16-token tile, K-slices of at most 64 iterations
-  // (16 waves x 4); decode blocks use up to 16 waves, prefill blocks 4 waves
-  // over many token tiles
+  // EC projection shape. Decode: one producer workgroup per (token tile,
+  // K-slice, pair of 16-row tiles of [A; w_g]), each slice one pass of the
+  // workgroup's waves, so that every producer is a single round of loads.
+  // Prefill: one workgroup per token tile over all of K and all rows.
   z.ntb = (int)cdiv(M, kTokTile);
   if (z.ec) {
+    const int RTe = (int)cdiv(z.R1, 16);
     if (z.gemv) {
-      // EC blocks: at most two 128-wide iterations per wave
-      z.ec_block = (path == SPEAR_PATH_FUSED_GEMV) ? 64 * z.NW : 512;
-      const int per_block = 2 * (z.ec_block / 64);
-      z.P = (int)cdiv(z.IT, per_block);
-      z.eips = (int)cdiv(z.IT, z.P);
+      // fused producers are workgroups of the GEMV grid: its waves plus the EC wave
+      const int nw = fused ? z.NW + 1 : kEcWaves;
+      z.ec_block = 64 * nw;
+      z.ec_ipp = 1;  // one iteration per wave: every producer is one round of loads
+      z.eips = std::max(nw * z.ec_ipp, (int)cdiv(z.IT, 512 * nw));  // <= 512 * nw slices
       z.P = (int)cdiv(z.IT, z.eips);
+      z.PG = (int)cdiv(RTe, kEcTiles);
+      z.tpg = kEcTiles;
+      z.ec_mode = path == SPEAR_PATH_UNFUSED_CHAIN ? EC_RAW : EC_LAST;
+      if (fused && z.gate != GATE_TANH) {
+        // gather mode when the slices' partials are few: with fewer, longer
+        // slices if that keeps each producer within four passes
+        const int64_t words = (int64_t)z.P * M * z.R1;
+        const int64_t pmax = kGatherMaxWords / (M * z.R1);
+        if (words <= kGatherMaxWords) {
+          z.ec_mode = EC_GATHER;
+        } else if (pmax >= 1 && cdiv(z.IT, pmax) <= 4 * nw * z.ec_ipp) {
+          z.eips = (int)cdiv(z.IT, pmax);
+          z.P = (int)cdiv(z.IT, z.eips);
+          z.ec_mode = EC_GATHER;
+        }
+      }
+      z.lds_prod = ec_block_lds(nw, z.R1p, z.h, z.r);
     } else {
       z.ec_block = 256;
-      z.P = 1;
+      z.ec_ipp = 2;
       z.eips = z.IT;
+      z.P = 1;
+      z.PG = 1;
+      z.tpg = RTe;
+      z.ec_mode = path == SPEAR_PATH_UNFUSED_CHAIN ? EC_RAW : EC_LAST;
+      z.lds_prod = ec_block_lds(4, z.R1p, z.h, z.r);
     }
-    z.lds_ec = ec_lds_bytes(z.R1p, z.h, z.r);
+    z.lds_gate = ec_lds_bytes(z.R1p, z.h, z.r);
   }
+
   if (z.gemv) {
-    // EC block carve-up and the epilogue's rows of B, then the staged
-    // scales/zero points of one block (groups of its K-slice)
-    const int ipg = z.G / kIterK;
-    const int ngb = (int)std::min<int64_t>(z.ngroups, cdiv(z.ips, ipg) + 1);
-    z.lds_gemv = gemv_lds_sz_off(z.NW, z.RT, z.MT, z.R1p, z.h, z.r, z.ec) +
-                 (size_t)16 * z.RT * (ngb | 1) * 4;
+    // LDS of a GEMV block: [x slice | wave partials | gather scratch]
+    // [yacc] [EC u/hidden/v] [rows of B] [scales and zero points]; the x
+    // slice is staged only while the whole layout fits the CU's LDS
+    const int RB = 16 * z.RT;
+    z.xstride = z.ips * kIterK * 2 + 16;
+    const size_t xbytes = (size_t)M * z.xstride;
+    auto layout = [&](bool xl) {
+      size_t U = std::max((size_t)z.NW * z.RT * z.MT * 1024, (size_t)z.S * 4);
+      if (xl) U = std::max(U, xbytes);
+      z.lds_y = (int)align_up(U, 16);
+      z.lds_e = z.lds_y + z.RT * z.MT * 1024;
+      z.lds_b = z.lds_g = z.lds_ev = z.lds_e;
+      if (z.ec) {
+        z.lds_b = (int)(z.lds_e + ec_lds_bytes(z.R1p, z.h, z.r));
+        z.bpre = (z.r % 8) == 0 && RB * z.r / 8 <= 2 * 64 * z.NW;
+        z.lds_g = (int)align_up(z.lds_b + (z.bpre ? (size_t)RB * z.r * 2 : 0), 16);
+        z.lds_ev = z.lds_g;
+        if (fused && z.ec_mode == EC_GATHER)
+          z.lds_ev = (int)(z.lds_g + (size_t)z.P * kTokTile * z.R1 * 4);
+      }
+      z.lds_sz = z.lds_ev + (z.ec ? z.RT * z.MT * 1024 : 0);
+      const int ipg = z.G / kIterK;
+      const int ngb = (int)std::min<int64_t>(z.ngroups, cdiv(z.ips, ipg) + 1);
+      z.lds_gemv = z.lds_sz + (size_t)RB * (ngb | 1) * 4;
+    };
+    z.xlds = xbytes <= kXLdsMax;
+    layout(z.xlds);
+    if (z.xlds && std::max(z.lds_gemv, z.lds_prod) > kMaxLds) {
+      z.xlds = 0;
+      layout(false);
+    }
+    if (std::max(z.lds_gemv, z.lds_prod) > kMaxLds) return SPEAR_E_SHAPE;
+  } else if (z.lds_prod > kMaxLds) {
+    return SPEAR_E_SHAPE;
   }
   z.plan.ec_splits = z.ec ? z.P : 0;
 
@@ -165,8 +227,8 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   if (!z.ec) {
     z.plan.num_launches = 1;
     z.plan.grid = grid4;
-  } else if (path == SPEAR_PATH_FUSED_GEMV) {
-    z.n_prod = z.ntb * z.P;
+  } else if (fused) {
+    z.n_prod = z.ntb * z.P * z.PG;
     z.plan.num_launches = 1;
     z.plan.grid = z.n_prod + grid4;
   } else if (path == SPEAR_PATH_UNFUSED_2K) {
@@ -178,24 +240,29 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   }
 
   // workspace layout. The first kCounterBytes hold every counter of every
-  // kind of call at fixed offsets (the generation word, the fused grid's done
-  // counter, EC-slice counters, row-group counters); each call leaves its
-  // counters at zero, and data regions start after this block, so any mix of
-  // calls can share one zero-initialised workspace.
+  // kind of call at fixed offsets (the fused path's launch counter, EC-slice
+  // counters, row-group counters); each call leaves them as it found them,
+  // and data regions start after this block, so any mix of calls can share
+  // one zero-initialised workspace.
   size_t off = kCounterBytes;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off = align_up(off + bytes, 256);
     return o;
   };
-  z.off_gen = kCtrGen;
-  z.off_done = kCtrDone;
-  z.off_ectr = kCtrEc;
-  z.off_rbctr = kCtrRows;
   if (z.ec) {
-    if (z.P > 1 && z.ntb > kMaxEcCounters) return SPEAR_E_SHAPE;
-    if (path == SPEAR_PATH_FUSED_GEMV) z.off_vtag = take((size_t)kVCopies * M * z.r * 8);
-    if (z.P > 1) z.off_upart = take((size_t)z.ntb * z.P * kTokTile * z.R1 * 4);
+    const bool partials = z.ec_mode != EC_GATHER && z.P * z.PG > 1;
+    if (partials && z.ntb > kMaxEcCounters) return SPEAR_E_SHAPE;
+    if (fused) {
+      z.off_vtag = take((size_t)kVCopies * M * 8 *
+                        (z.ec_mode == EC_GATHER ? (size_t)z.P * z.R1 : (size_t)z.r));
+      z.npub = z.ec_mode == EC_GATHER ? z.ntb * z.P * z.PG : z.ntb;
+      // small problems: the consumers poll the tagged data itself rather
+      // than the ready counter, saving the publishers' completion wait
+      const int64_t words = z.ec_mode == EC_GATHER ? (int64_t)z.P * M * z.R1 : M * z.r;
+      z.direct = words <= kDirectMaxWords && z.nrg * z.S <= kDirectMaxGrid;
+    }
+    if (partials) z.off_upart = take((size_t)z.ntb * z.P * kTokTile * z.R1 * 4);
     z.off_v = take((size_t)M * z.r * 4);
     if (!z.gemv && path == SPEAR_PATH_UNFUSED_2K) {
       z.off_vh = take((size_t)M * z.vstride * 2);
@@ -258,7 +325,7 @@ spear_status_t check_ws(const spear_problem_t* p, const Resolved& z, const void*
 }
 
 EcParams make_ec(const spear_problem_t* p, const Resolved& z, const void* x, const spear_ec_t* ec,
-                 char* ws, uint32_t epoch) {
+                 char* ws) {
   EcParams e;
   std::memset(&e, 0, sizeof(e));
   e.x = (const uint16_t*)x;
@@ -271,7 +338,9 @@ EcParams make_ec(const spear_problem_t* p, const Resolved& z, const void* x, con
   e.gate = z.gate;
   e.P = z.P;
   e.ips = z.eips;
-  e.epoch = epoch;
+  e.PG = z.PG;
+  e.tpg = z.tpg;
+  e.mode = z.ec_mode;
   e.vstride = z.vstride;
   if (ec) {
     e.A = (const uint16_t*)ec->A;
@@ -284,15 +353,15 @@ EcParams make_ec(const spear_problem_t* p, const Resolved& z, const void* x, con
     e.alpha = ec->alpha;
   }
   if (ws) {
-    e.ctr = (uint32_t*)(ws + z.off_ectr);
-    if (z.P > 1) e.upart = (float*)(ws + z.off_upart);
+    e.ctr = (uint32_t*)(ws + kCtrEc);
+    if (z.off_upart) e.upart = (float*)(ws + z.off_upart);
     e.v = (float*)(ws + z.off_v);
   }
   return e;
 }
 
 GemvParams make_gemv(const spear_problem_t* p, const Resolved& z, const void* x, const spear_w4_t* w,
-                     void* y, const spear_ec_t* ec, char* ws, uint32_t epoch) {
+                     void* y, const spear_ec_t* ec, char* ws) {
   GemvParams g;
   std::memset(&g, 0, sizeof(g));
   g.qw = w->qweight;
@@ -310,11 +379,19 @@ GemvParams make_gemv(const spear_problem_t* p, const Resolved& z, const void* x,
   g.S = z.S;
   g.ips = z.ips;
   g.iw = z.iw;
-  g.epoch = epoch;
   g.wait_polls = g_wait_polls.load();
+  g.xlds = z.xlds;
+  g.xstride = z.xstride;
+  g.bpre = ec ? z.bpre : 0;
+  g.lds_y = z.lds_y;
+  g.lds_e = z.lds_e;
+  g.lds_b = z.lds_b;
+  g.lds_g = z.lds_g;
+  g.lds_ev = z.lds_ev;
+  g.lds_sz = z.lds_sz;
   if (ws && z.S > 1) {
     g.ypart = (float*)(ws + z.off_ypart);
-    g.rb_ctr = (uint32_t*)(ws + z.off_rbctr);
+    g.rb_ctr = (uint32_t*)(ws + kCtrRows);
   }
   return g;
 }
@@ -346,9 +423,9 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
 spear_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPEAR_OK : SPEAR_E_HIP; }
 
 spear_status_t run_w4(const spear_problem_t* p, const Resolved& z, const void* x, const spear_w4_t* w,
-                      void* y, char* ws, uint32_t epoch, hipStream_t st) {
+                      void* y, char* ws, hipStream_t st) {
   if (z.gemv) {
-    GemvParams g = make_gemv(p, z, x, w, y, nullptr, ws, epoch);
+    GemvParams g = make_gemv(p, z, x, w, y, nullptr, ws);
     return hip_status(
         launch_gemv(z.dt, z.MT, z.RT, EPI_NONE, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, st));
   }
@@ -377,7 +454,7 @@ spear_status_t spear_w4_linear(const spear_problem_t* prob, const void* x, const
   if (prob->M == 0 || prob->N == 0) return SPEAR_OK;
   if ((st = check_w4(prob, x, w, y)) != SPEAR_OK) return st;
   if ((st = check_ws(prob, z, y, workspace, workspace_bytes)) != SPEAR_OK) return st;
-  return run_w4(prob, z, x, w, y, (char*)workspace, next_epoch(), (hipStream_t)hip_stream);
+  return run_w4(prob, z, x, w, y, (char*)workspace, (hipStream_t)hip_stream);
 }
 
 spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, const spear_w4_t* w,
@@ -392,49 +469,50 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   if ((st = check_ws(prob, z, y, workspace, workspace_bytes)) != SPEAR_OK) return st;
   hipStream_t s = (hipStream_t)hip_stream;
   char* ws = (char*)workspace;
-  const uint32_t epoch = next_epoch();
-  if (!z.ec) return run_w4(prob, z, x, w, y, ws, epoch, s);
+  if (!z.ec) return run_w4(prob, z, x, w, y, ws, s);
 
-  EcParams e = make_ec(prob, z, x, ec, ws, epoch);
+  EcParams e = make_ec(prob, z, x, ec, ws);
   const int path = z.plan.path;
+  const int ec_grid = z.ntb * z.P * z.PG;
   if (path == SPEAR_PATH_FUSED_GEMV) {
     e.vtag = (unsigned long long*)(ws + z.off_vtag);
-    e.gen = (uint32_t*)(ws + z.off_gen);
+    e.gen = (unsigned long long*)(ws + kCtrGen);
+    e.ready = (unsigned long long*)(ws + kCtrReady);
+    e.npub = z.npub;
+    e.direct = z.direct;
     e.v = nullptr;
-    GemvParams g = make_gemv(prob, z, x, w, y, ec, ws, epoch);
+    GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
     g.ec = e;
     g.n_prod = z.n_prod;
-    g.done_ctr = (uint32_t*)(ws + z.off_done);
     g.grid_total = z.n_prod + z.nrg * z.S;
-    const size_t lds = std::max(z.lds_gemv, z.lds_ec);
+    const size_t lds = std::max(z.lds_gemv, z.lds_prod);
     return hip_status(
-        launch_gemv(z.dt, z.MT, z.RT, EPI_FUSED, g, g.grid_total, 64 * z.NW, lds, s));
+        launch_gemv(z.dt, z.MT, z.RT, EPI_FUSED, g, g.grid_total, 64 * (z.NW + 1), lds, s));
   }
   if (path == SPEAR_PATH_UNFUSED_2K) {
     if (!z.gemv) {
       e.vh = (uint16_t*)(ws + z.off_vh);
       e.vl = (uint16_t*)(ws + z.off_vl);
+      e.v = nullptr;
     }
-    st = hip_status(launch_ec(z.dt, e, z.ntb, z.ec_block, z.lds_ec, s));
+    st = hip_status(launch_ec(z.dt, e, ec_grid, z.ec_block, z.ec_ipp, z.lds_prod, s));
     if (st != SPEAR_OK) return st;
     if (z.gemv) {
-      GemvParams g = make_gemv(prob, z, x, w, y, ec, ws, epoch);
+      GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
       g.ec = e;
-      return hip_status(
-          launch_gemv(z.dt, z.MT, z.RT, EPI_READY, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, s));
+      return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_READY, g, z.nrg * z.S, 64 * (z.NW + 1),
+                                    z.lds_gemv, s));
     }
     GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
     return hip_status(launch_gemm(z.dt, EPI_READY, g, s));
   }
   // naive chain: 4-bit product, projection, gate, reprojection + accumulate
-  st = run_w4(prob, z, x, w, y, ws, epoch, s);
+  st = run_w4(prob, z, x, w, y, ws, s);
   if (st != SPEAR_OK) return st;
-  e.raw = 1;
   e.u_out = (float*)(ws + z.off_u);
-  st = hip_status(launch_ec(z.dt, e, z.ntb, z.ec_block, z.lds_ec, s));
+  st = hip_status(launch_ec(z.dt, e, ec_grid, z.ec_block, z.ec_ipp, z.lds_prod, s));
   if (st != SPEAR_OK) return st;
-  e.raw = 0;
-  st = hip_status(launch_gate(z.dt, e, z.ntb, z.lds_ec, s));
+  st = hip_status(launch_gate(z.dt, e, z.ntb, z.lds_gate, s));
   if (st != SPEAR_OK) return st;
   return hip_status(launch_ec_up_acc(z.dt, e.v, (const uint16_t*)ec->B, (uint16_t*)y, (int)prob->M,
                                      (int)prob->N, z.r, s));

@@ -15,31 +15,64 @@ enum { EPI_NONE = 0,   // Y = X W^T
        EPI_READY = 1,  // Y = X W^T + v B^T, v already in the workspace
        EPI_FUSED = 2   // same, v produced by EC workgroups of the same grid
 };
+// How the EC projection's K-slices are combined.
+enum { EC_LAST = 0,    // the last slice to arrive sums the partials, applies
+                       // the gate and publishes v
+       EC_GATHER = 1,  // fused only: every slice publishes its tagged partial
+                       // sums; each consumer sums them and applies the gate
+       EC_RAW = 2      // like EC_LAST, but publishes u = [A; w_g] x ungated
+};
 
 constexpr int kIterK = 128;      // K consumed per GEMV/EC iteration
 constexpr int kTokTile = 16;     // tokens per MFMA token tile
+constexpr int kEcTiles = 2;      // 16-row tiles of [A; w_g] per EC pass
 constexpr int kGemmTM = 128;     // prefill tile: tokens
 constexpr int kGemmTN = 128;     // prefill tile: output rows
 constexpr int kGemmTK = 64;      // prefill tile: K per stage
 constexpr int kGemmLdsRow = kGemmTK + 8;  // padded LDS row (halves)
-constexpr int kVCopies = 8;      // tagged EC-coordinate copies (one per XCD)
+constexpr int kVCopies = 8;      // copies of the published EC data (one per XCD)
 
 // Workspace: a fixed counter block at the start, shared by every kind of call
-// (each call returns its counters to zero), then the call's data regions.
-constexpr size_t kCounterBytes = 65536;
-constexpr size_t kCtrGen = 0;        // launch generation of the fused path
-constexpr size_t kCtrDone = 4;       // fused grid: blocks done
-constexpr size_t kCtrEc = 256;       // EC-slice counters, one per token tile
+// (each call leaves its counters as it found them), then the call's data.
+constexpr size_t kCounterBytes = 131072;
+constexpr size_t kCtrGen = 0;          // fused path: kGenClasses 64-bit launch
+constexpr int kGenClasses = 64;        // counters, kGenStride apart
+constexpr size_t kGenStride = 256;
+constexpr size_t kCtrEc = 16384;       // EC-slice counters, one per token tile
 constexpr int kMaxEcCounters = 64;
-constexpr size_t kCtrRows = 512;     // split-K counters, one per row group
-constexpr int kMaxRowCounters = (int)((kCounterBytes - kCtrRows) / 4);
+constexpr size_t kCtrRows = 16896;     // split-K counters, one per row group
+constexpr size_t kCtrReady = 98304;    // fused path: kVCopies 64-bit ready
+constexpr size_t kReadyStride = 4096;  // counters, 4 KB apart (memory channels)
+constexpr int kMaxRowCounters = (int)((kCtrReady - kCtrRows) / 4);
 
-// Tag of the EC coordinates published by the fused launch of generation g:
-// a multiplicative hash, so that leftover data of another call is never
-// mistaken for a current coordinate (2^-32 chance per word).
+// Launch generation of the fused path. Workgroup b belongs to counter class
+// b % kGenClasses; every class counter advances by exactly 2^32 per launch:
+// the class's first workgroup adds 2^32 - (members - 1) when it ends, every
+// other member adds 1 (and workgroup 0 adds 2^32 to the classes no workgroup
+// of a small grid belongs to). Any workgroup of launch L therefore reads a
+// value in [L * 2^32, (L + 1) * 2^32) from its class counter when it starts,
+// and the high word is the launch generation, with no workgroup waiting for
+// another and no one address taking every workgroup's update.
+__host__ __device__ inline uint64_t gen_increment(int block, int grid) {
+  const int c = block % kGenClasses;
+  const int members = (grid - c + kGenClasses - 1) / kGenClasses;
+  return block < kGenClasses ? (1ull << 32) - (uint64_t)(members - 1) : 1ull;
+}
+// The ready counters advance by exactly 2^32 per launch too, summed over the
+// publishers of the EC data (one per producer or per token tile), each adding
+// its share (publisher_increment) once its data is complete: they read
+// (g + 1) * 2^32 when every publisher of launch g is done.
+__host__ __device__ inline uint64_t publisher_increment(int pub, int npub) {
+  return pub == 0 ? (1ull << 32) - (uint64_t)(npub - 1) : 1ull;
+}
+// Tag of data published by the fused launch of generation g: a
+// multiplicative hash, so that leftover data of another call is never
+// mistaken for current data (2^-32 chance per word).
 __host__ __device__ inline uint32_t ec_tag(uint32_t gen) { return ((gen + 1u) * 0x9E3779B1u) | 1u; }
 
-// EC projection / gate work of one token tile (16 tokens) and one K-slice.
+// EC projection / gate work. A producer workgroup owns one token tile (16
+// tokens), one K-slice (ips iterations of 128) and one group of row tiles
+// (tpg tiles of 16 rows of [A; w_g]).
 struct EcParams {
   const uint16_t* x;      // [M][K]
   const uint16_t* A;      // [r][K]
@@ -50,18 +83,24 @@ struct EcParams {
   const uint16_t* b2;     // [r]
   float b_g, alpha;
   int M, K, r, R1, R1p, h, gate;
-  int P, ips;             // K-slices and 128-wide iterations per slice
-  int raw;                // 1: store u = [A; w_g] x only (no gate)
-  float* upart;           // [ntb][P][16][R1] partial sums (P > 1)
-  uint32_t* ctr;          // [ntb] last-arriver counters
-  float* v;               // [M][r] gated coordinates, fp32
+  int P, ips;             // K-slices and iterations per slice
+  int PG, tpg;            // row-tile groups and tiles per group
+  int mode;               // EC_LAST, EC_GATHER or EC_RAW
+  float* upart;           // EC_LAST/RAW: [ntb][P][16][R1] partial sums
+  uint32_t* ctr;          // EC_LAST/RAW: [ntb] arrival counters
+  float* v;               // [M][r] gated coordinates, fp32 (or null)
   uint16_t* vh;           // [M][vstride] act-dtype high part (or null)
   uint16_t* vl;           // [M][vstride] act-dtype low part  (or null)
   int vstride;
-  float* u_out;           // raw mode: [M][R1]
-  unsigned long long* vtag;  // fused: [kVCopies][M][r] (tag << 32 | fp32 bits)
-  uint32_t* gen;          // fused: launch generation (tag = ec_tag(gen))
-  uint32_t epoch;
+  float* u_out;           // EC_RAW: [M][R1]
+  // fused: tagged words (tag << 32 | fp32 bits), kVCopies copies of
+  //   EC_LAST:   v  [M][r]
+  //   EC_GATHER: the slices' partial sums [P][M][R1]
+  unsigned long long* vtag;
+  unsigned long long* gen;  // fused: launch counters (see gen_increment)
+  unsigned long long* ready;  // fused: kVCopies ready counters, kReadyStride apart
+  int npub;                   // fused: publishers per launch
+  int direct;                 // fused: consumers poll the tagged data itself
 };
 
 struct GemvParams {
@@ -75,11 +114,15 @@ struct GemvParams {
   int S, ips, iw;         // K-slices per row group, iterations per slice and per wave
   int n_prod;             // EC workgroups at the head of the grid (fused)
   float* ypart;           // [S][M][N] partial sums (S > 1)
-  uint32_t* rb_ctr;       // [row tiles] last-arriver counters
-  uint32_t* done_ctr;     // fused: arrivals of every workgroup of the grid
-  int grid_total;              // fused: workgroups in the grid
+  uint32_t* rb_ctr;       // [row groups] last-arriver counters
+  int grid_total;         // fused: workgroups in the grid
   int wait_polls;
-  uint32_t epoch;
+  int xlds;               // 1: the block's slice of x is staged in LDS
+  int xstride;            // its LDS row stride in bytes
+  int bpre;               // 1: the epilogue's rows of B are staged in LDS
+  // LDS carve-up (byte offsets): [x | wave partials] [yacc] [EC u/hidden/v]
+  // [rows of B] [gathered partials] [EC wave's result tiles] [scales]
+  int lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz;
   EcParams ec;
 };
 
@@ -97,37 +140,29 @@ struct GemmParams {
 
 __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
-// LDS carve-up of an EC block: u [16][R1p] fp32, hidden [h] fp32, v tile [16][r] fp32.
+// GEMV workgroups have at most eight waves (a ninth would make the dispatcher
+// reserve three waves' registers on every SIMD and halve residency); the EC
+// variants give one of them to the EC wave.
+constexpr int kGemvMaxThreads = 512;
+
+// LDS of EC work: wave partials red [NW][kEcTiles][64][4] fp32, then
+// u [16][R1p] fp32, hidden [h] fp32 and the v tile [16][r] fp32.
+__host__ __device__ inline size_t ec_red_bytes(int NW) { return (size_t)NW * kEcTiles * 1024; }
 __host__ __device__ inline size_t ec_lds_u_off() { return 0; }
 __host__ __device__ inline size_t ec_lds_hid_off(int R1p) { return align_up((size_t)kTokTile * R1p * 4, 16); }
 __host__ __device__ inline size_t ec_lds_v_off(int R1p, int h) { return ec_lds_hid_off(R1p) + align_up((size_t)h * 4, 16); }
 __host__ __device__ inline size_t ec_lds_bytes(int R1p, int h, int r) {
   return ec_lds_v_off(R1p, h) + align_up((size_t)kTokTile * (r > 0 ? r : 1) * 4, 16);
 }
-
-// LDS carve-up of a GEMV block of NW waves and RT row tiles:
-//   red:  per-wave partial tiles, NW x RT x MT x 1 KB
-//   yacc: the block's sums [16*MT tokens][16*RT rows] fp32
-//   E:    an EC block (v tile for the epilogue; u/hidden for the fallback),
-//         then the epilogue's rows of B
-__host__ __device__ inline size_t gemv_lds_y_off(int NW, int RT, int MT) {
-  return (size_t)NW * RT * MT * 1024;
-}
-__host__ __device__ inline size_t gemv_lds_e_off(int NW, int RT, int MT) {
-  return gemv_lds_y_off(NW, RT, MT) + (size_t)RT * MT * 1024;
-}
-// after E (and B, when the EC is on): the staged scales/zero points
-// [16*RT rows][groups of the block's K-slice] as u32
-__host__ __device__ inline size_t gemv_lds_sz_off(int NW, int RT, int MT, int R1p, int h, int r,
-                                                  bool ec) {
-  size_t o = gemv_lds_e_off(NW, RT, MT);
-  if (ec) o += ec_lds_bytes(R1p, h, r) + align_up((size_t)16 * RT * r * 2, 16);
-  return align_up(o, 16);
+// a producer workgroup: red, then the u/hidden/v region
+__host__ __device__ inline size_t ec_block_lds(int NW, int R1p, int h, int r) {
+  return ec_red_bytes(NW) + ec_lds_bytes(R1p, h, r);
 }
 
 hipError_t launch_dequant(int dt, const uint32_t* qw, const uint16_t* sc, const uint8_t* zr,
                           uint16_t* out, int N, int K, int G, hipStream_t st);
-hipError_t launch_ec(int dt, const EcParams& e, int ntb, int block, size_t lds, hipStream_t st);
+hipError_t launch_ec(int dt, const EcParams& e, int grid, int block, int ipp, size_t lds,
+                     hipStream_t st);
 bool gemv_shape_supported(int MT, int RT);
 hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, int block,
                        size_t lds, hipStream_t st);

@@ -217,91 +217,151 @@ __global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ qw
 }
 
 // ---------------------------------------------------------------------------
-// EC projection of one token tile over iterations [it_beg, it_end):
-// u_lds[t][j] = sum_k x[16*tb + t][k] * R[j][k], R = [A; w_g] (R1 rows), as a
-// sum over the block's waves in a fixed order (wave 0 first).
+// Coherent reads of data other workgroups published in this launch: buffer
+// loads with the sc1 bit (what a relaxed agent-scope atomic load is on
+// gfx950), bounds-checked so that every load of a batch is issued without a
+// branch. A thread's loads go out four at a time, all in flight together.
 // ---------------------------------------------------------------------------
-// Row tiles of [A; w_g] projected together (bounds the registers the
-// two-iteration load batch needs).
-constexpr int kEcTiles = 2;
+__device__ __forceinline__ uint32_t bld32c(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0x10);
+}
+__device__ __forceinline__ u32x2 bld64c(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0x10);
+}
 
-template <int DT>
-__device__ void ec_project_tile(const EcParams& e, int tb, int it_beg, int it_end, float* u_lds) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// dst[i] = fp32 word at byte offset off(i) of `r`, i in [0, n). (Four named
+// registers rather than an array: the loads must stay out of scratch.)
+template <class Off>
+__device__ __forceinline__ void gather_f32(rsrc_t r, int n, Off off, float* dst) {
+  const int nthr = blockDim.x;
+  for (int i0 = threadIdx.x; i0 < n; i0 += 4 * nthr) {
+    const int i1 = i0 + nthr, i2 = i1 + nthr, i3 = i2 + nthr;
+    const uint32_t w0 = bld32c(r, off(i0));
+    const uint32_t w1 = bld32c(r, i1 < n ? off(i1) : kOOB);
+    const uint32_t w2 = bld32c(r, i2 < n ? off(i2) : kOOB);
+    const uint32_t w3 = bld32c(r, i3 < n ? off(i3) : kOOB);
+    dst[i0] = __uint_as_float(w0);
+    if (i1 < n) dst[i1] = __uint_as_float(w1);
+    if (i2 < n) dst[i2] = __uint_as_float(w2);
+    if (i3 < n) dst[i3] = __uint_as_float(w3);
+  }
+}
+
+// Same for tagged words (tag << 32 | fp32 bits); returns 1 if any word this
+// thread read carries another tag.
+template <class Off>
+__device__ __forceinline__ int gather_tagged(rsrc_t r, int n, Off off, uint32_t tag, float* dst) {
+  const int nthr = blockDim.x;
+  int stale = 0;
+  for (int i0 = threadIdx.x; i0 < n; i0 += 4 * nthr) {
+    const int i1 = i0 + nthr, i2 = i1 + nthr, i3 = i2 + nthr;
+    const u32x2 w0 = bld64c(r, off(i0));
+    const u32x2 w1 = bld64c(r, i1 < n ? off(i1) : kOOB);
+    const u32x2 w2 = bld64c(r, i2 < n ? off(i2) : kOOB);
+    const u32x2 w3 = bld64c(r, i3 < n ? off(i3) : kOOB);
+    stale |= w0[1] != tag;
+    dst[i0] = __uint_as_float(w0[0]);
+    if (i1 < n) { stale |= w1[1] != tag; dst[i1] = __uint_as_float(w1[0]); }
+    if (i2 < n) { stale |= w2[1] != tag; dst[i2] = __uint_as_float(w2[0]); }
+    if (i3 < n) { stale |= w3[1] != tag; dst[i3] = __uint_as_float(w3[0]); }
+  }
+  return stale;
+}
+
+// out(i, sum over q < P of the word at off(q, i)), i in [0, n), summed in
+// slice order; the words go through `scratch` (cap floats of LDS) in chunks.
+// Every thread of the block calls it; it ends with a barrier.
+template <class Off, class Out>
+__device__ void sum_slices(rsrc_t r, int P, int n, Off off, float* scratch, int cap, Out out) {
+  const int C = max(1, cap / P);
+  for (int e0 = 0; e0 < n; e0 += C) {
+    const int c = min(C, n - e0);
+    gather_f32(r, P * c, [&](int i) {
+      const int q = i / c;
+      return off(q, e0 + (i - q * c));
+    }, scratch);
+    __syncthreads();
+    for (int i = threadIdx.x; i < c; i += blockDim.x) {
+      float v = 0.f;
+      for (int q = 0; q < P; ++q) v += scratch[q * c + i];
+      out(e0 + i, v);
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// EC projection of one token tile over iterations [it_beg, it_end) and row
+// tiles [t_beg, t_end) of R = [A; w_g] (R1 rows; the gate row w_g is row r):
+// u_lds[t][j] = sum_k x[16*tb + t][k] * R[j][k] for the rows of those tiles.
+// Each wave takes IPP iterations per pass with all of their loads issued
+// first; the waves' partial tiles are summed in LDS in a fixed order (wave 0
+// first), so the result does not depend on timing.
+// ---------------------------------------------------------------------------
+template <int DT, int IPP>
+__device__ void ec_project(const EcParams& e, int tb, int it_beg, int it_end, int t_beg, int t_end,
+                           float* u_lds, float* red) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int NW = blockDim.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int m = tb * kTokTile + lr;
-  const int RTe = (e.R1 + 15) >> 4;
+  // token rows past M read row M-1: their results are never used
+  const int m = min(tb * kTokTile + lr, e.M - 1);
   const rsrc_t rx = make_rsrc(e.x, (uint32_t)e.M * e.K * 2);
   const rsrc_t ra = make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
   const rsrc_t rg = make_rsrc(e.wg, e.gate == GATE_SIGMOID ? (uint32_t)e.K * 2 : 0u);
-  const uint32_t xoff = m < e.M ? (uint32_t)m * e.K * 2 + 64 * lg : kOOB;
-  for (int tg0 = 0; tg0 < RTe; tg0 += kEcTiles) {
-    const int nt = min(kEcTiles, RTe - tg0);
+  const uint32_t xoff = (uint32_t)m * e.K * 2 + 64 * lg;
+  for (int tg0 = t_beg; tg0 < t_end; tg0 += kEcTiles) {
+    const int nt = min(kEcTiles, t_end - tg0);
     f32x4 acc[kEcTiles];
-#pragma unroll
-    for (int t = 0; t < kEcTiles; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     uint32_t aoff[kEcTiles], goff[kEcTiles];
     bool has_g[kEcTiles];
 #pragma unroll
     for (int t = 0; t < kEcTiles; ++t) {
+      acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       const int j = (tg0 + t) * 16 + lr;
-      aoff[t] = j < e.r ? (uint32_t)j * e.K * 2 + 64 * lg : kOOB;
-      goff[t] = (j == e.r && e.gate == GATE_SIGMOID) ? 64u * lg : kOOB;
-      // uniform: does this row tile hold the gate row w_g?
-      has_g[t] = e.gate == GATE_SIGMOID && e.r >= (tg0 + t) * 16 && e.r < (tg0 + t + 1) * 16;
+      aoff[t] = (t < nt && j < e.r) ? (uint32_t)j * e.K * 2 + 64 * lg : kOOB;
+      goff[t] = (t < nt && j == e.r && e.gate == GATE_SIGMOID) ? 64u * lg : kOOB;
+      // uniform: does this row tile hold the gate row?
+      has_g[t] = t < nt && e.gate == GATE_SIGMOID && e.r >= (tg0 + t) * 16 &&
+                 e.r < (tg0 + t + 1) * 16;
     }
-    // two iterations per pass with all of their loads issued first
-    for (int it = it_beg + wave; it < it_end; it += 2 * NW) {
-      const int it2 = it + NW;
-      const uint32_t kb = (uint32_t)it * (kIterK * 2);
-      const uint32_t kb2 = (uint32_t)it2 * (kIterK * 2);
-      const bool ok2 = it2 < it_end;
-      u32x4 xv[2][4], av[2][kEcTiles][4];
+    for (int it0 = it_beg + wave * IPP; it0 < it_end; it0 += NW * IPP) {
+      u32x4 xv[IPP][4], av[IPP][kEcTiles][4];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        xv[0][jj] = bld128(rx, xoff + kb + 16 * jj);
-        xv[1][jj] = bld128(rx, ok2 ? xoff + kb2 + 16 * jj : kOOB);
-      }
+      for (int h = 0; h < IPP; ++h) {
+        const bool ok = it0 + h < it_end;  // uniform
+        const uint32_t kb = (uint32_t)(it0 + h) * (kIterK * 2);
 #pragma unroll
-      for (int t = 0; t < kEcTiles; ++t) {
-        if (t < nt) {
+        for (int jj = 0; jj < 4; ++jj) xv[h][jj] = bld128(rx, ok ? xoff + kb + 16 * jj : kOOB);
+#pragma unroll
+        for (int t = 0; t < kEcTiles; ++t)
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
-            av[0][t][jj] = bld128(ra, aoff[t] + kb + 16 * jj);
-            av[1][t][jj] = bld128(ra, ok2 ? aoff[t] + kb2 + 16 * jj : kOOB);
-            if (has_g[t]) {
-              av[0][t][jj] |= bld128(rg, goff[t] + kb + 16 * jj);
-              av[1][t][jj] |= bld128(rg, ok2 ? goff[t] + kb2 + 16 * jj : kOOB);
-            }
+            av[h][t][jj] = bld128(ra, ok && aoff[t] != kOOB ? aoff[t] + kb + 16 * jj : kOOB);
+            if (has_g[t])
+              av[h][t][jj] |= bld128(rg, ok && goff[t] != kOOB ? goff[t] + kb + 16 * jj : kOOB);
           }
-        }
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < IPP; ++h)
 #pragma unroll
         for (int t = 0; t < kEcTiles; ++t)
-          if (t < nt)
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj) acc[t] = mfma16<DT>(av[h][t][jj], xv[h][jj], acc[t]);
+          for (int jj = 0; jj < 4; ++jj) acc[t] = mfma16<DT>(av[h][t][jj], xv[h][jj], acc[t]);
     }
-    // deterministic cross-wave sum: wave 0 stores, waves 1.. add in order
-    for (int w = 0; w < NW; ++w) {
-      __syncthreads();
-      if (wave == w) {
+    // lane l holds token l % 16 and rows 4 * (l / 16) .. + 3 of each tile
 #pragma unroll
-        for (int t = 0; t < kEcTiles; ++t) {
-          if (t < nt) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int j = (tg0 + t) * 16 + 4 * lg + i;
-              float* dst = u_lds + lr * e.R1p + j;
-              *dst = (w == 0) ? acc[t][i] : *dst + acc[t][i];
-            }
-          }
-        }
-      }
+    for (int t = 0; t < kEcTiles; ++t)
+      *(f32x4*)(red + ((wave * kEcTiles + t) * 64 + lane) * 4) = acc[t];
+    __syncthreads();
+    for (int idx = tid; idx < nt * 256; idx += blockDim.x) {
+      const int t = idx >> 8, rem = idx & 255, ln = rem >> 2, i = rem & 3;
+      float s = 0.f;
+      for (int w = 0; w < NW; ++w) s += red[((w * kEcTiles + t) * 64 + ln) * 4 + i];
+      const int j = (tg0 + t) * 16 + 4 * (ln >> 4) + i;
+      if (j < e.R1) u_lds[(ln & 15) * e.R1p + j] = s;
     }
     __syncthreads();
   }
@@ -309,7 +369,7 @@ __device__ void ec_project_tile(const EcParams& e, int tb, int it_beg, int it_en
 
 // Gate of one token tile: from u (LDS, [16][R1p]) to v_tile (LDS, [16][r]):
 // v = alpha * g * u (sigmoid-linear), alpha * (1 + tanh(W2 ReLU(W1 u + b1) + b2)) (.) u
-// (tanh-MLP), or alpha * u (gate one).
+// (tanh-MLP), or alpha * u (gate one). Ends with a barrier.
 template <int DT>
 __device__ void ec_gate_tile(const EcParams& e, int cnt, const float* u_lds, float* hid,
                              float* v_tile) {
@@ -347,46 +407,78 @@ __device__ void ec_gate_tile(const EcParams& e, int cnt, const float* u_lds, flo
   }
 }
 
-// One EC block: token tile tb, K-slice p. Projects, reduces across slices
-// (last arriver), applies the gate and publishes v: as fp32 (consumed by a
-// later kernel), as act-dtype hi/lo parts (the GEMM epilogue), and/or as
-// tagged 64-bit words (tag << 32 | fp32 bits) in one copy per XCD, which the
-// fused kernel's workgroups poll: a word is current when its tag matches.
-template <int DT>
-__device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
+// One EC producer workgroup b: token tile, K-slice and row-tile group from b.
+// It projects its share; then (EC_GATHER) publishes its tagged partial sums
+// for the consumers to add up, or joins the last-arriver reduction of its
+// token tile, whose last workgroup sums the slices in order, applies the gate
+// and publishes v: as fp32 (read by a later kernel), as act-dtype hi/lo parts
+// (the prefill GEMM epilogue) and/or as tagged words in one copy per XCD (the
+// fused kernel's consumers).
+template <int DT, int IPP>
+__device__ void ec_producer(const EcParams& e, int b, uint32_t gen, char* smem) {
   __shared__ int s_last;
   const int tid = threadIdx.x, nthr = blockDim.x;
+  const int NW = nthr >> 6;
   const int IT = e.K / kIterK;
-  const int it_beg = p * e.ips, it_end = min(IT, it_beg + e.ips);
-  float* u_lds = (float*)(smem + ec_lds_u_off());
-  float* hid = (float*)(smem + ec_lds_hid_off(e.R1p));
-  float* v_tile = (float*)(smem + ec_lds_v_off(e.R1p, e.h));
+  const int per_tb = e.P * e.PG;
+  const int tb = b / per_tb, rem = b - tb * per_tb;
+  const int pk = rem / e.PG, pg = rem - pk * e.PG;
+  const int it_beg = pk * e.ips, it_end = min(IT, it_beg + e.ips);
+  const int RTe = (e.R1 + 15) >> 4;
+  const int t_beg = pg * e.tpg, t_end = min(RTe, t_beg + e.tpg);
+  float* red = (float*)smem;
+  char* es = smem + ec_red_bytes(NW);
+  float* u_lds = (float*)(es + ec_lds_u_off());
+  float* hid = (float*)(es + ec_lds_hid_off(e.R1p));
+  float* v_tile = (float*)(es + ec_lds_v_off(e.R1p, e.h));
   const int m0 = tb * kTokTile;
   const int cnt = min(kTokTile, e.M - m0);
+  const int j_beg = 16 * t_beg, nj = min(e.R1, 16 * t_end) - j_beg;
 
-  ec_project_tile<DT>(e, tb, it_beg, it_end, u_lds);
+  ec_project<DT, IPP>(e, tb, it_beg, it_end, t_beg, t_end, u_lds, red);
 
-  if (e.P > 1) {
-    float* part = e.upart + ((size_t)tb * e.P + p) * kTokTile * e.R1;
-    for (int idx = tid; idx < cnt * e.R1; idx += nthr) {
-      const int t = idx / e.R1, j = idx - t * e.R1;
-      st_agent(part + idx, u_lds[t * e.R1p + j]);
+  if (e.mode == EC_GATHER) {
+    const uint32_t tag = ec_tag(gen);
+    const size_t per_copy = (size_t)e.P * e.M * e.R1;
+    for (int idx = tid; idx < kVCopies * cnt * nj; idx += nthr) {
+      const int c = idx / (cnt * nj), o = idx - c * (cnt * nj);
+      const int t = o / nj, j = j_beg + (o - t * nj);
+      const unsigned long long w =
+          ((unsigned long long)tag << 32) | __float_as_uint(u_lds[t * e.R1p + j]);
+      __hip_atomic_store(e.vtag + c * per_copy + ((size_t)pk * e.M + m0 + t) * e.R1 + j, w,
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    // the data is complete before the ready counters count it
     complete_and_sync();
-    if (tid == 0) s_last = arrive_last(e.ctr + tb, (uint32_t)e.P) ? 1 : 0;
-    __syncthreads();
-    if (!s_last) return;
-    const float* base = e.upart + (size_t)tb * e.P * kTokTile * e.R1;
-    for (int idx = tid; idx < cnt * e.R1; idx += nthr) {
-      float a = 0.f;
-      for (int q = 0; q < e.P; ++q) a += ld_agent(base + (size_t)q * kTokTile * e.R1 + idx);
-      const int t = idx / e.R1, j = idx - t * e.R1;
-      u_lds[t * e.R1p + j] = a;
-    }
-    __syncthreads();
+    if (tid < kVCopies)
+      __hip_atomic_fetch_add(e.ready + tid * (kReadyStride / 8), (unsigned long long)publisher_increment(b, e.npub),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
   }
 
-  if (e.raw) {
+  if (per_tb > 1) {
+    float* part = e.upart + ((size_t)tb * e.P + pk) * kTokTile * e.R1;
+    for (int idx = tid; idx < cnt * nj; idx += nthr) {
+      const int t = idx / nj, j = j_beg + (idx - t * nj);
+      st_agent(part + t * e.R1 + j, u_lds[t * e.R1p + j]);
+    }
+    complete_and_sync();
+    if (tid == 0) s_last = arrive_last(e.ctr + tb, (uint32_t)per_tb) ? 1 : 0;
+    __syncthreads();
+    if (!s_last) return;
+    // the slices' partial tiles [P][cnt][R1], summed in slice order through
+    // the wave-partials region (free now)
+    const rsrc_t rp = make_rsrc(e.upart + (size_t)tb * e.P * kTokTile * e.R1,
+                                (uint32_t)e.P * kTokTile * e.R1 * 4);
+    sum_slices(rp, e.P, cnt * e.R1,
+               [&](int q, int i) { return (uint32_t)(q * kTokTile * e.R1 + i) * 4u; }, red,
+               (int)(ec_red_bytes(NW) / 4), [&](int i, float v) {
+                 const int t = i / e.R1, j = i - t * e.R1;
+                 u_lds[t * e.R1p + j] = v;
+               });
+  }
+
+  if (e.mode == EC_RAW) {
     for (int idx = tid; idx < cnt * e.R1; idx += nthr) {
       const int t = idx / e.R1, j = idx - t * e.R1;
       e.u_out[(size_t)(m0 + t) * e.R1 + j] = u_lds[t * e.R1p + j];
@@ -400,7 +492,7 @@ __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
   if (e.vh) {
     for (int idx = tid; idx < cnt * e.vstride; idx += nthr) {
       const int t = idx / e.vstride, j = idx - t * e.vstride;
-      float val = j < e.r ? v_tile[t * e.r + j] : 0.f;
+      const float val = j < e.r ? v_tile[t * e.r + j] : 0.f;
       const uint16_t hi = f2act<DT>(val);
       const uint16_t lo = f2act<DT>(val - act2f<DT>(hi));
       e.vh[(size_t)(m0 + t) * e.vstride + j] = hi;
@@ -408,7 +500,7 @@ __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
     }
   }
   if (e.vtag) {
-    const uint32_t tag = ec_tag(ld_agent_u32(e.gen));
+    const uint32_t tag = ec_tag(gen);
     const size_t per_copy = (size_t)e.M * e.r;
     for (int idx = tid; idx < cnt * e.r * kVCopies; idx += nthr) {
       const int c = idx / (cnt * e.r), o = idx - c * (cnt * e.r);
@@ -417,13 +509,18 @@ __device__ void ec_block(const EcParams& e, int tb, int p, char* smem) {
       __hip_atomic_store(e.vtag + c * per_copy + (size_t)m0 * e.r + o, w, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     }
+    complete_and_sync();
+    if (tid < kVCopies)
+      __hip_atomic_fetch_add(e.ready + tid * (kReadyStride / 8), (unsigned long long)publisher_increment(tb, e.npub),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
-template <int DT>
+// EC pre-kernel (semi-fused and chain paths): one producer per workgroup.
+template <int DT, int IPP>
 __global__ __launch_bounds__(512) void k_ec(EcParams e) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  ec_block<DT>(e, blockIdx.x / e.P, blockIdx.x % e.P, smem);
+  ec_producer<DT, IPP>(e, blockIdx.x, 0u, smem);
 }
 
 // Naive chain, gate launch: reads u [M][R1] and writes v [M][r].
@@ -457,50 +554,318 @@ __global__ __launch_bounds__(256) void k_ec_up_acc(const float* __restrict__ v,
   y[idx] = f2act<DT>(a);
 }
 
-// Every block of the fused grid arrives here once when it is done; the last
-// one advances the generation that tags the next launch's EC coordinates, so
-// that a replayed graph (same epoch) never reads the previous replay's values.
-__device__ __forceinline__ void fused_exit(const GemvParams& a, uint32_t gen) {
-  complete_and_sync();
-  if (threadIdx.x == 0 && arrive_last(a.done_ctr, (uint32_t)a.grid_total))
-    __hip_atomic_store(a.ec.gen, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Every workgroup of the fused grid advances its class's launch counter once
+// as it ends (see gen_increment): relaxed adds that nothing waits for.
+__device__ __forceinline__ unsigned long long* gen_counter(const GemvParams& a, int block) {
+  return a.ec.gen + (size_t)(block % kGenClasses) * (kGenStride / 8);
+}
+__device__ __forceinline__ void fused_exit(const GemvParams& a) {
+  const int b = blockIdx.x;
+  if (threadIdx.x == 0)
+    __hip_atomic_fetch_add(gen_counter(a, b), (unsigned long long)gen_increment(b, a.grid_total),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // classes without a member in a small grid advance with workgroup 0
+  if (b == 0 && (int)threadIdx.x >= a.grid_total && (int)threadIdx.x < kGenClasses)
+    __hip_atomic_fetch_add(gen_counter(a, threadIdx.x), 1ull << 32, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
+// The GEMV's EC wave. In the EC variants every workgroup carries one wave
+// beyond its GEMV waves; on the first K-slice it obtains v for each token
+// tile and computes v B^T for the workgroup's rows while the GEMV waves
+// stream the codes, so its waits (for the producers, for cold caches) stay
+// off the critical path. Everything below is single-wave: lanes exchange data
+// through LDS in program order, with no workgroup barrier.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void wave_sync() { __builtin_amdgcn_wave_barrier(); }
+
+// dst[i] = fp32 part of the tagged word at off(i), i in [0, n), over the
+// wave's 64 lanes; returns 1 (in every lane) if any word carries another tag.
+// COH: coherent (sc1) loads, else loads through this XCD's L2, which are
+// cheaper but may return a line cached before the data was published (its
+// tag then tells).
+template <bool COH, class Off>
+__device__ __forceinline__ bool gather_tagged_w(rsrc_t r, int n, Off off, uint32_t tag, float* dst) {
+  const int lane = threadIdx.x & 63;
+  constexpr int aux = COH ? 0x10 : 0;
+  int stale = 0;
+  for (int i0 = lane; i0 < n; i0 += 256) {
+    const int i1 = i0 + 64, i2 = i1 + 64, i3 = i2 + 64;
+    const u32x2 w0 = __builtin_amdgcn_raw_buffer_load_b64(r, off(i0), 0, aux);
+    const u32x2 w1 = __builtin_amdgcn_raw_buffer_load_b64(r, i1 < n ? off(i1) : kOOB, 0, aux);
+    const u32x2 w2 = __builtin_amdgcn_raw_buffer_load_b64(r, i2 < n ? off(i2) : kOOB, 0, aux);
+    const u32x2 w3 = __builtin_amdgcn_raw_buffer_load_b64(r, i3 < n ? off(i3) : kOOB, 0, aux);
+    stale |= w0[1] != tag;
+    dst[i0] = __uint_as_float(w0[0]);
+    if (i1 < n) { stale |= w1[1] != tag; dst[i1] = __uint_as_float(w1[0]); }
+    if (i2 < n) { stale |= w2[1] != tag; dst[i2] = __uint_as_float(w2[0]); }
+    if (i3 < n) { stale |= w3[1] != tag; dst[i3] = __uint_as_float(w3[0]); }
+  }
+  wave_sync();
+  return __any(stale);
+}
+
+// u_lds[t][j] = sum_k x[16 tb + t][k] R[j][k] for all R1 rows and all of K,
+// by one wave (the EC wave's fallback when the producers' data never came).
+template <int DT>
+__device__ void ec_project_wave(const EcParams& e, int tb, float* u_lds) {
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int IT = e.K / kIterK, RTe = (e.R1 + 15) >> 4;
+  const int m = min(tb * kTokTile + lr, e.M - 1);
+  const rsrc_t rx = make_rsrc(e.x, (uint32_t)e.M * e.K * 2);
+  const rsrc_t ra = make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
+  const rsrc_t rg = make_rsrc(e.wg, e.gate == GATE_SIGMOID ? (uint32_t)e.K * 2 : 0u);
+  const uint32_t xoff = (uint32_t)m * e.K * 2 + 64 * lg;
+  for (int t = 0; t < RTe; ++t) {
+    const int j = t * 16 + lr;
+    const uint32_t aoff = j < e.r ? (uint32_t)j * e.K * 2 + 64 * lg : kOOB;
+    const uint32_t goff = (j == e.r && e.gate == GATE_SIGMOID) ? 64u * lg : kOOB;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int it = 0; it < IT; ++it) {
+      const uint32_t kb = (uint32_t)it * (kIterK * 2);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const u32x4 xv = bld128(rx, xoff + kb + 16 * jj);
+        u32x4 av = bld128(ra, aoff != kOOB ? aoff + kb + 16 * jj : kOOB);
+        av |= bld128(rg, goff != kOOB ? goff + kb + 16 * jj : kOOB);
+        acc = mfma16<DT>(av, xv, acc);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int jr = t * 16 + 4 * lg + i;
+      if (jr < e.R1) u_lds[lr * e.R1p + jr] = acc[i];
+    }
+  }
+  wave_sync();
+}
+
+// The gate of one token tile by one wave: u_lds [16][R1p] -> v_tile [16][r].
+template <int DT>
+__device__ void ec_gate_wave(const EcParams& e, int cnt, const float* u_lds, float* hid,
+                             float* v_tile) {
+  const int lane = threadIdx.x & 63;
+  const int r = e.r;
+  if (e.gate == GATE_TANH) {
+    for (int t = 0; t < cnt; ++t) {
+      const float* u = u_lds + t * e.R1p;
+      for (int i = lane; i < e.h; i += 64) {
+        float a = act2f<DT>(e.b1[i]);
+        const uint16_t* w1 = e.W1 + (size_t)i * r;
+        for (int j = 0; j < r; ++j) a += act2f<DT>(w1[j]) * u[j];
+        hid[i] = a > 0.f ? a : 0.f;
+      }
+      wave_sync();
+      for (int j = lane; j < r; j += 64) {
+        float a = act2f<DT>(e.b2[j]);
+        const uint16_t* w2 = e.W2 + (size_t)j * e.h;
+        for (int i = 0; i < e.h; ++i) a += act2f<DT>(w2[i]) * hid[i];
+        v_tile[t * r + j] = e.alpha * (1.f + tanhf(a)) * u[j];
+      }
+      wave_sync();
+    }
+  } else {
+    for (int idx = lane; idx < cnt * r; idx += 64) {
+      const int t = idx / r, j = idx - t * r;
+      float g = 1.f;
+      if (e.gate == GATE_SIGMOID) {
+        const float z = u_lds[t * e.R1p + r] + e.b_g;
+        g = z >= 0.f ? 1.f / (1.f + __expf(-z)) : __expf(z) / (1.f + __expf(z));
+      }
+      v_tile[idx] = e.alpha * g * u_lds[t * e.R1p + j];
+    }
+    wave_sync();
+  }
+}
+
+// The EC wave's work for the workgroup's rows n0 .. n0 + 16 RT: for every
+// token tile, v (from the previous kernel, or from this grid's producers once
+// their ready flags carry this launch's tag, or computed here on time-out),
+// then ev = v B^T as two MFMAs per 32 ranks (v split into act-dtype high and
+// low parts), stored per (row tile, token tile) in the layout of a GEMV
+// wave's accumulators.
+template <int DT, int MT, int RT, int EPI>
+__device__ void ec_wave(const GemvParams& a, uint32_t gen, char* smem, int n0, bool bpre) {
+  const EcParams& e = a.ec;
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int M = a.M, N = a.N, r = a.r;
+  char* es = smem + a.lds_e;
+  float* u_lds = (float*)(es + ec_lds_u_off());
+  float* hid = (float*)(es + ec_lds_hid_off(e.R1p));
+  float* v_tile = (float*)(es + ec_lds_v_off(e.R1p, e.h));
+  const uint16_t* bs = (const uint16_t*)(smem + a.lds_b);
+  float* gsc = (float*)(smem + a.lds_g);
+  float* evs = (float*)(smem + a.lds_ev);
+  const rsrc_t rb = make_rsrc(a.B, (uint32_t)N * r * 2);
+  const uint32_t tag = ec_tag(gen);
+  const int copy = blockIdx.x % kVCopies;
+  const int nkk = (r + 31) / 32;
+  // ev = v B^T for token tile mt from v_tile, into the result tiles
+  auto up_project = [&](int mt, int cnt) {
+    f32x4 ev[RT];
+#pragma unroll
+    for (int t = 0; t < RT; ++t) ev[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < nkk; ++kk) {
+      const int j0 = 32 * kk + 8 * lg;
+      u32x4 ah, al;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = j0 + 2 * q;
+        const float f0 = (lr < cnt && j < r) ? v_tile[lr * r + j] : 0.f;
+        const float f1 = (lr < cnt && j + 1 < r) ? v_tile[lr * r + j + 1] : 0.f;
+        const uint32_t h0 = f2act<DT>(f0), h1 = f2act<DT>(f1);
+        ah[q] = h0 | (h1 << 16);
+        al[q] = (uint32_t)f2act<DT>(f0 - act2f<DT>(h0)) |
+                ((uint32_t)f2act<DT>(f1 - act2f<DT>(h1)) << 16);
+      }
+#pragma unroll
+      for (int t = 0; t < RT; ++t) {
+        const int row = 16 * t + lr, n = n0 + row;
+        u32x4 bf;
+        if (bpre && (r & 7) == 0 && j0 < r) {
+          bf = *(const u32x4*)(bs + row * r + j0);
+        } else {
+          auto bval = [&](int j) -> uint32_t {
+            if (n >= N || j >= r) return 0u;
+            return bpre ? (uint32_t)bs[row * r + j] : bld16(rb, (uint32_t)(n * r + j) * 2);
+          };
+#pragma unroll
+          for (int q = 0; q < 4; ++q) bf[q] = bval(j0 + 2 * q) | (bval(j0 + 2 * q + 1) << 16);
+        }
+        ev[t] = mfma16<DT>(ah, bf, ev[t]);
+        ev[t] = mfma16<DT>(al, bf, ev[t]);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < RT; ++t) *(f32x4*)(evs + ((t * MT + mt) * 64 + lane) * 4) = ev[t];
+    wave_sync();
+  };
+
+  if constexpr (EPI == EPI_READY) {
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m0 = 16 * mt, cnt = min(16, M - m0);
+      for (int idx = lane; idx < cnt * r; idx += 64) v_tile[idx] = e.v[(size_t)m0 * r + idx];
+      wave_sync();
+      up_project(mt, cnt);
+    }
+    return;
+  }
+
+  // Fused: one attempt reads the published data of token tile mt (tagged
+  // words), completes v and its product, and tells whether every word was
+  // current; a stale attempt still runs the whole path, which warms this
+  // wave's caches while the producers finish. `dry` reads nothing.
+  auto attempt = [&](int mt, int cnt, bool coh, bool dry) -> bool {
+    const int m0 = 16 * mt;
+    bool stale;
+    if (e.mode == EC_GATHER) {
+      const int per = cnt * e.R1;
+      const size_t per_copy = (size_t)e.P * e.M * e.R1;
+      const rsrc_t rv = make_rsrc(e.vtag + copy * per_copy, (uint32_t)(per_copy * 8));
+      auto off = [&](int i) {
+        const int q = i / per, o = i - q * per;
+        return (uint32_t)(((size_t)q * e.M + m0) * e.R1 + o) * 8u;
+      };
+      const int n = dry ? 0 : e.P * per;
+      stale = dry || (coh ? gather_tagged_w<true>(rv, n, off, tag, gsc)
+                          : gather_tagged_w<false>(rv, n, off, tag, gsc));
+      for (int idx = lane; idx < per; idx += 64) {
+        float sum = 0.f;
+        for (int q = 0; q < e.P; ++q) sum += gsc[q * per + idx];
+        const int t = idx / e.R1, j = idx - t * e.R1;
+        u_lds[t * e.R1p + j] = sum;
+      }
+      wave_sync();
+      ec_gate_wave<DT>(e, cnt, u_lds, hid, v_tile);
+    } else {
+      const size_t per_copy = (size_t)e.M * r;
+      const rsrc_t rv = make_rsrc(e.vtag + copy * per_copy, (uint32_t)(per_copy * 8));
+      auto off = [&](int i) { return (uint32_t)((size_t)m0 * r + i) * 8u; };
+      const int n = dry ? 0 : cnt * r;
+      stale = dry || (coh ? gather_tagged_w<true>(rv, n, off, tag, v_tile)
+                          : gather_tagged_w<false>(rv, n, off, tag, v_tile));
+    }
+    up_project(mt, cnt);
+    return !stale;
+  };
+
+  // warm-up pass, then wait: small problems poll the tagged data itself;
+  // the others wait (bounded) for this copy's ready counter to show every
+  // publisher of this launch and then read the data once through the L2,
+  // re-reading it coherently if a cached line was stale
+  bool ok = true;
+  if (!e.direct) {
+    attempt(0, min(16, M), false, true);
+    const unsigned long long* rc = e.ready + copy * (kReadyStride / 8);
+    const rsrc_t rr = make_rsrc(rc, 8);
+    const unsigned long long goal = ((unsigned long long)gen + 1ull) << 32;
+    for (int poll = 0;; ++poll) {
+      const u32x2 c = bld64c(rr, 0u);
+      const unsigned long long cv = ((unsigned long long)c[1] << 32) | c[0];
+      // counts of this launch lie in [goal - 2^32, goal]; the difference is
+      // taken modulo 2^64 so that wrap-around is harmless
+      if ((long long)(cv - goal) >= 0) break;
+      if (poll >= a.wait_polls) { ok = false; break; }
+      __builtin_amdgcn_s_sleep(16);
+    }
+  }
+  for (int mt = 0; mt < MT; ++mt) {
+    const int cnt = min(16, M - 16 * mt);
+    bool have = false;
+    if (e.direct) {
+      for (int k = 0; k <= a.wait_polls && !have; ++k) {
+        have = attempt(mt, cnt, true, false);
+        if (!have) __builtin_amdgcn_s_sleep(4);
+      }
+    } else if (ok) {
+      have = attempt(mt, cnt, false, false) || attempt(mt, cnt, true, false);
+    }
+    if (!have) {
+      ec_project_wave<DT>(e, mt, u_lds);
+      ec_gate_wave<DT>(e, cnt, u_lds, hid, v_tile);
+      up_project(mt, cnt);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
 // Decode GEMV. A block owns RT row tiles (16 rows each) and a K-slice of
 // iterations (128 K each); each of its NW waves walks a contiguous chunk of
-// that slice as a software pipeline: the codes, scales, zero points and
-// activation fragments of iteration it+1 are in flight while iteration it is
-// computed, so memory and compute overlap within every wave. The MFMA
-// multiplies activations (A operand, 16 token rows) by the biased codes (B
-// operand, 16 weight rows as columns), so each lane owns one weight row per
-// tile and needs one scale and one zero point per iteration:
+// that slice as a software pipeline: the codes of iteration it+1 are in
+// flight while iteration it is computed. The block's slice of x is staged in
+// LDS once when it fits (else read through the cache per iteration), and so
+// are the scales and zero points of its rows. The MFMA multiplies
+// activations (A operand, 16 token rows) by the biased codes (B operand, 16
+// weight rows as columns), so each lane owns one weight row per tile and
+// needs one scale and one zero point per iteration:
 //   sum_k x (q - z) s = s * ( sum_k x (bias + q) - (bias + z) * sum_k x ),
-// with sum_k x from an MFMA against ones, shared by the RT tiles. Waves are
-// reduced in LDS in a fixed order; K-slices through partial sums and a last
+// with sum_k x from an MFMA against ones, shared by the RT tiles.
+// In the EC variants the block has one more wave, the EC wave (above), whose
+// v B^T tiles join the waves' partial tiles in the fixed-order reduction of
+// the first K-slice. K-slices are reduced through partial sums and a last
 // arriver.
 //
-// Fused variant: the first n_prod blocks of the grid are EC blocks (above).
-// The others, after their main loop, poll the tagged EC coordinates of their
-// XCD copy (bounded; on time-out they compute the EC themselves) and add
-// B v in the epilogue. Every block arrives at a done counter at its end; the
-// last one advances the generation that tags the next launch's coordinates.
+// Fused variant: the first n_prod blocks of the grid are EC producers; the
+// others' EC waves wait for what they publish.
 // ---------------------------------------------------------------------------
 template <int DT, int MT, int RT, int EPI>
-__global__ __launch_bounds__(512) void k_gemv(GemvParams a) {
+__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int s_flag;
+  constexpr bool kEC = EPI != EPI_NONE;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int NW = blockDim.x >> 6;
+  const int NW = (blockDim.x >> 6) - (kEC ? 1 : 0);           // GEMV waves
+  const bool gw = wave < NW;
   const int lr = lane & 15, lg = lane >> 4;
   int bid = blockIdx.x;
   uint32_t gen = 0;
   if constexpr (EPI == EPI_FUSED) {
-    gen = ld_agent_u32(a.ec.gen);
+    gen = (uint32_t)(__hip_atomic_load(gen_counter(a, bid), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> 32);
     if (bid < a.n_prod) {
-      ec_block<DT>(a.ec, bid / a.ec.P, bid % a.ec.P, smem);
-      fused_exit(a, gen);
+      ec_producer<DT, 1>(a.ec, bid, gen, smem);
+      fused_exit(a);
       return;
     }
     bid -= a.n_prod;
@@ -512,24 +877,23 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams a) {
   const int n0 = rg * RB;
   const int it_blk = s * a.ips;
   const int it_end = min(IT, it_blk + a.ips);
-  const int iw_beg = it_blk + wave * a.iw;
-  const int iw_end = min(it_end, iw_beg + a.iw);
+  const int iw_beg = gw ? it_blk + wave * a.iw : 0;
+  const int iw_end = gw ? min(it_end, iw_beg + a.iw) : 0;
+  const int r = a.r;
 
   const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * (K / 2));
   const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
   const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
   const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
+  const rsrc_t rb = make_rsrc(a.B, (uint32_t)N * r * 2);
 
-  // the EC epilogue's rows of B ([16*RT][r], fp16/bf16) are fetched up front
-  // when r is a multiple of 8 and two 16-byte chunks per thread cover them;
-  // otherwise the epilogue reads B directly
+  // the first K-slice's rows of B ([RB][r], contiguous) are fetched up front
+  // into LDS when two 16-byte chunks per thread cover them
   constexpr int BCH = 2;
-  const int r = a.r;
-  const int bchunks = EPI != EPI_NONE && (r & 7) == 0 ? RB * r / 8 : 0;
-  const bool bpre = bchunks > 0 && bchunks <= BCH * (int)blockDim.x;
+  const bool bpre = EPI != EPI_NONE && s == 0 && a.bpre;
+  const int bchunks = RB * r / 8;
   u32x4 bst[BCH];
   if (bpre) {
-    const rsrc_t rb = make_rsrc(a.B, (uint32_t)N * r * 2);
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
       const int ci = tid + c * (int)blockDim.x;
@@ -537,34 +901,70 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams a) {
     }
   }
 
-  // one batch = one 128-wide iteration of every row tile: codes, scales,
-  // zero points and the activation fragments. The per-lane part of every
-  // offset (row, token, lane group; kOOB for rows >= N or tokens >= M) is
-  // fixed for the whole loop; the iteration enters as a wave-uniform soffset.
+  // per-lane parts of the load offsets (row, token, lane group; kOOB for
+  // rows >= N); the iteration enters as a wave-uniform soffset. Token rows
+  // past M read row M-1: their MFMA rows only feed outputs that are never
+  // stored, and in-bounds duplicates cost the address unit far less than
+  // masked lanes.
   uint32_t vw[RT], vx[MT];
 #pragma unroll
   for (int t = 0; t < RT; ++t) {
     const int n = n0 + 16 * t + lr;
     vw[t] = n < N ? (uint32_t)n * (K / 2) + 16 * lg : kOOB;
   }
-  // lanes of tokens >= M read the last token's row: their MFMA rows only feed
-  // outputs that are never stored, and in-bounds duplicate addresses are far
-  // cheaper for the address unit than masked (out-of-range) lanes
+  const bool xl = a.xlds;
+  const char* xs = smem;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int m = min(16 * mt + lr, M - 1);
-    vx[mt] = ((uint32_t)m * K + 32 * lg) * 2;
+    vx[mt] = xl ? (uint32_t)m * a.xstride + 64 * lg : ((uint32_t)m * K + 32 * lg) * 2;
   }
-  auto load = [&](u32x4 (&w)[RT], u32x4 (&xv)[MT][4], int it) {
+  auto load_w = [&](u32x4 (&w)[RT], int it) {
 #pragma unroll
     for (int t = 0; t < RT; ++t) w[t] = bld128s(rq, vw[t], (uint32_t)it * (kIterK / 2));
+  };
+  auto load_x = [&](u32x4 (&xv)[MT][4], int it) {
+    if (xl) {
+      const uint32_t kb = (uint32_t)(it - it_blk) * (kIterK * 2);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-        xv[mt][jj] = bld128s(rx, vx[mt] + 16 * jj, (uint32_t)it * (kIterK * 2));
+        for (int jj = 0; jj < 4; ++jj) xv[mt][jj] = *(const u32x4*)(xs + vx[mt] + kb + 16 * jj);
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          xv[mt][jj] = bld128s(rx, vx[mt] + 16 * jj, (uint32_t)it * (kIterK * 2));
+    }
   };
 
+  u32x4 wA[RT], wB[RT];
+  u32x4 xA[MT][4], xB[MT][4];
+  if (iw_beg < iw_end) {
+    load_w(wA, iw_beg);
+    if (!xl) load_x(xA, iw_beg);
+  }
+  // the block's slice of x into LDS ([M][slice] with a padded row stride)
+  if (xl) {
+    const int cpr = (it_end - it_blk) * (kIterK / 8);  // 16-byte chunks per row
+    const int nch = M * cpr;
+    for (int base = tid; base < nch; base += 4 * (int)blockDim.x) {
+      u32x4 c4[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int ci = base + u * (int)blockDim.x;
+        const int m = ci / cpr, kc = ci - m * cpr;
+        c4[u] = bld128(rx, ci < nch ? ((uint32_t)m * K + it_blk * kIterK + 8 * kc) * 2 : kOOB);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int ci = base + u * (int)blockDim.x;
+        const int m = ci / cpr, kc = ci - m * cpr;
+        if (ci < nch) *(u32x4*)(smem + (size_t)m * a.xstride + 16 * kc) = c4[u];
+      }
+    }
+  }
   // scales and zero points of the block's rows and groups, staged once in
   // LDS with coalesced loads ([row][group] as s | z << 16): per-iteration
   // scattered 2- and 1-byte loads would cost a cache-line request per row
@@ -572,20 +972,45 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams a) {
   const int g_lo = it_blk / ipg;
   const int ngb = (it_end - 1) / ipg + 1 - g_lo;
   const int ngs = ngb | 1;  // odd LDS row stride: rows fall on distinct banks
-  uint32_t* szs = (uint32_t*)(smem + gemv_lds_sz_off(NW, RT, MT, a.ec.R1p, a.ec.h, r, EPI != EPI_NONE));
-  // the first batch goes out before the staging loads so that both overlap
-  u32x4 wA[RT], wB[RT];
-  u32x4 xA[MT][4], xB[MT][4];
-  if (iw_beg < iw_end) load(wA, xA, iw_beg);
-  for (int idx = tid; idx < RB * ngb; idx += blockDim.x) {
-    const int row = idx / ngb, gg = idx - row * ngb;
-    const int n = n0 + row;
-    const uint32_t e = (uint32_t)n * a.ngroups + g_lo + gg;
-    const uint32_t sv = bld16(rsc, n < N ? e * 2 : kOOB);
-    const uint32_t zv = bld8(rz, n < N ? e : kOOB);
-    szs[row * ngs + gg] = sv | (zv << 16);
+  uint32_t* szs = (uint32_t*)(smem + a.lds_sz);
+  {
+    // four entries per thread per round, all loads in flight together
+    const int nsz = RB * ngb, nthr = blockDim.x;
+    auto sz_off = [&](int idx, uint32_t& eo) -> bool {
+      const int row = idx / ngb, gg = idx - row * ngb;
+      eo = (uint32_t)(n0 + row) * a.ngroups + g_lo + gg;
+      return idx < nsz && n0 + row < N;
+    };
+    for (int i0 = tid; i0 < nsz; i0 += 4 * nthr) {
+      uint32_t sv[4], zv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint32_t eo;
+        const bool ok = sz_off(i0 + u * nthr, eo);
+        sv[u] = bld16(rsc, ok ? eo * 2 : kOOB);
+        zv[u] = bld8(rz, ok ? eo : kOOB);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int idx = i0 + u * nthr;
+        if (idx < nsz) {
+          const int row = idx / ngb, gg = idx - row * ngb;
+          szs[row * ngs + gg] = sv[u] | (zv[u] << 16);
+        }
+      }
+    }
+  }
+  uint16_t* bs = (uint16_t*)(smem + a.lds_b);
+  if (bpre) {
+#pragma unroll
+    for (int c = 0; c < BCH; ++c) {
+      const int ci = tid + c * (int)blockDim.x;
+      if (ci < bchunks) *(u32x4*)(bs + 8 * ci) = bst[c];
+    }
   }
   __syncthreads();
+  if (xl && iw_beg < iw_end) load_x(xA, iw_beg);
+
   constexpr float kBias = code_bias<DT>();
   f32x4 acc[RT][MT];
 #pragma unroll
@@ -633,37 +1058,49 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams a) {
   if (iw_beg < iw_end) {
     const int last = iw_end - 1;
     for (int it = iw_beg; it < iw_end; it += 2) {
-      load(wB, xB, min(it + 1, last));
+      load_w(wB, min(it + 1, last));
+      load_x(xB, min(it + 1, last));
       __builtin_amdgcn_sched_barrier(0);
       compute(wA, xA, it);
       if (it + 1 >= iw_end) break;
-      load(wA, xA, min(it + 2, last));
+      load_w(wA, min(it + 2, last));
+      load_x(xA, min(it + 2, last));
       __builtin_amdgcn_sched_barrier(0);
       compute(wB, xB, it + 1);
     }
   }
+  if constexpr (kEC) {
+    if (!gw && s == 0) ec_wave<DT, MT, RT, EPI>(a, gen, smem, n0, bpre);
+  }
+  if (xl) __syncthreads();  // the x region is reused below
 
-  // ---- cross-wave reduction (fixed order) into yacc[token][row]
+  // ---- cross-wave reduction (fixed order) into yacc[token][row]; the EC
+  // wave's tiles come last
   float* red = (float*)smem;
+  if (gw) {
 #pragma unroll
-  for (int t = 0; t < RT; ++t)
+    for (int t = 0; t < RT; ++t)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-      *(f32x4*)(red + (((wave * RT + t) * MT + mt) * 64 + lane) * 4) = acc[t][mt];
+      for (int mt = 0; mt < MT; ++mt)
+        *(f32x4*)(red + (((wave * RT + t) * MT + mt) * 64 + lane) * 4) = acc[t][mt];
+  }
   __syncthreads();
-  float* yacc = (float*)(smem + gemv_lds_y_off(NW, RT, MT));
+  float* yacc = (float*)(smem + a.lds_y);
+  const float* evs = (const float*)(smem + a.lds_ev);
+  const bool add_ev = kEC && s == 0;
   constexpr int YS = RB;  // yacc row stride: [token][RB rows]
   for (int e = tid; e < 256 * RT * MT; e += blockDim.x) {
     const int tm = e >> 8, rem = e & 255, ln = rem >> 2, i = rem & 3;
     const int t = tm / MT, mt = tm - t * MT;
     float v = 0.f;
     for (int w = 0; w < NW; ++w) v += red[(((w * RT + t) * MT + mt) * 64 + ln) * 4 + i];
+    if (add_ev) v += evs[((t * MT + mt) * 64 + ln) * 4 + i];
     const int tok = 16 * mt + 4 * (ln >> 4) + i, row = 16 * t + (ln & 15);
     yacc[tok * YS + row] = v;
   }
   __syncthreads();
 
-  // ---- cross-block split-K reduction: last arriver sums the slices in order
+  // ---- cross-block split-K reduction: the last arriver sums the slices in order
   if (a.S > 1) {
     for (int e = tid; e < RB * M; e += blockDim.x) {
       const int m = e / RB, row = e - m * RB;
@@ -673,85 +1110,26 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams a) {
     if (tid == 0) s_flag = arrive_last(a.rb_ctr + rg, (uint32_t)a.S) ? 1 : 0;
     __syncthreads();
     if (!s_flag) {
-      if constexpr (EPI == EPI_FUSED) fused_exit(a, gen);
+      if constexpr (EPI == EPI_FUSED) fused_exit(a);
       return;
     }
-    for (int e = tid; e < RB * M; e += blockDim.x) {
-      const int m = e / RB, row = e - m * RB;
-      if (n0 + row < N) {
-        float v = 0.f;
-        for (int q = 0; q < a.S; ++q) v += ld_agent(a.ypart + ((size_t)q * M + m) * N + n0 + row);
-        yacc[m * YS + row] = v;
-      }
-    }
-    __syncthreads();
+    // every slice's [M][RB] partial, summed in slice order through the
+    // wave-partials region (free now)
+    const rsrc_t rp = make_rsrc(a.ypart, (uint32_t)a.S * M * N * 4);
+    sum_slices(rp, a.S, M * RB, [&](int q, int i) {
+      const int m = i / RB, row = i - m * RB;
+      return n0 + row < N ? (uint32_t)(((size_t)q * M + m) * N + n0 + row) * 4u : kOOB;
+    }, red, a.lds_y / 4, [&](int i, float v) {
+      const int m = i / RB, row = i - m * RB;
+      yacc[m * YS + row] = v;
+    });
   }
 
-  if constexpr (EPI == EPI_NONE) {
-    for (int e = tid; e < RB * M; e += blockDim.x) {
-      const int m = e / RB, row = e - m * RB;
-      if (n0 + row < N) a.y[(size_t)m * N + n0 + row] = f2act<DT>(yacc[m * YS + row]);
-    }
-  } else {
-    const EcParams& e = a.ec;
-    char* ec_smem = smem + gemv_lds_e_off(NW, RT, MT);
-    float* v_tile = (float*)(ec_smem + ec_lds_v_off(e.R1p, e.h));
-    uint16_t* bs = (uint16_t*)(ec_smem + ec_lds_bytes(e.R1p, e.h, r));  // [RB][r]
-    if (bpre) {
-#pragma unroll
-      for (int c = 0; c < BCH; ++c) {
-        const int ci = tid + c * (int)blockDim.x;
-        if (ci < bchunks) *(u32x4*)(bs + 8 * ci) = bst[c];
-      }
-      __syncthreads();
-    }
-    const int ntb = (M + kTokTile - 1) / kTokTile;
-    const uint32_t tag = ec_tag(gen);
-    const unsigned long long* vcopy =
-        e.vtag ? e.vtag + (size_t)(blockIdx.x % kVCopies) * ((size_t)M * r) : nullptr;
-    for (int tb = 0; tb < ntb; ++tb) {
-      const int m0 = tb * kTokTile, cnt = min(kTokTile, M - m0);
-      bool have = true;
-      if constexpr (EPI == EPI_FUSED) {
-        // bounded poll of the tagged coordinates; every thread checks its share
-        for (int poll = 0;; ++poll) {
-          int stale = 0;
-          for (int idx = tid; idx < cnt * r; idx += blockDim.x) {
-            const unsigned long long w = __hip_atomic_load(
-                const_cast<unsigned long long*>(vcopy) + (size_t)m0 * r + idx, __ATOMIC_RELAXED,
-                __HIP_MEMORY_SCOPE_AGENT);
-            if ((uint32_t)(w >> 32) != tag) stale = 1;
-            else v_tile[idx] = __uint_as_float((uint32_t)w);
-          }
-          if (!__syncthreads_or(stale)) break;
-          if (poll >= a.wait_polls) { have = false; break; }
-          __builtin_amdgcn_s_sleep(2);
-        }
-        if (!have) {
-          float* u_lds = (float*)(ec_smem + ec_lds_u_off());
-          float* hid = (float*)(ec_smem + ec_lds_hid_off(e.R1p));
-          ec_project_tile<DT>(e, tb, 0, IT, u_lds);
-          ec_gate_tile<DT>(e, cnt, u_lds, hid, v_tile);
-        }
-      } else {
-        for (int idx = tid; idx < cnt * r; idx += blockDim.x) v_tile[idx] = e.v[(size_t)m0 * r + idx];
-        __syncthreads();
-      }
-      for (int idx = tid; idx < RB * cnt; idx += blockDim.x) {
-        const int t = idx / RB, row = idx - t * RB;
-        const int nn = n0 + row;
-        if (nn < N) {
-          float yv = yacc[(m0 + t) * YS + row];
-          const uint16_t* br = bpre ? bs + row * r : a.B + (size_t)nn * r;
-          const float* vr = v_tile + t * r;
-          for (int j = 0; j < r; ++j) yv += act2f<DT>(br[j]) * vr[j];
-          a.y[(size_t)(m0 + t) * N + nn] = f2act<DT>(yv);
-        }
-      }
-      __syncthreads();
-    }
+  for (int e = tid; e < RB * M; e += blockDim.x) {
+    const int m = e / RB, row = e - m * RB;
+    if (n0 + row < N) a.y[(size_t)m * N + n0 + row] = f2act<DT>(yacc[m * YS + row]);
   }
-  if constexpr (EPI == EPI_FUSED) fused_exit(a, gen);
+  if constexpr (EPI == EPI_FUSED) fused_exit(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -967,13 +1345,19 @@ hipError_t launch_dequant(int dt, const uint32_t* qw, const uint16_t* sc, const 
   return hipGetLastError();
 }
 
-hipError_t launch_ec(int dt, const EcParams& e, int ntb, int block, size_t lds, hipStream_t st) {
-  const unsigned grid = (unsigned)(ntb * e.P);
+hipError_t launch_ec(int dt, const EcParams& e, int grid, int block, int ipp, size_t lds,
+                     hipStream_t st) {
   if (grid == 0) return hipSuccess;
   SPEAR_DT_SWITCH(dt, {
-    hipError_t err = allow_lds(k_ec<DTC>, lds);
-    if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(k_ec<DTC>, dim3(grid), dim3(block), lds, st, e);
+    if (ipp == 1) {
+      hipError_t err = allow_lds(k_ec<DTC, 1>, lds);
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL((k_ec<DTC, 1>), dim3(grid), dim3(block), lds, st, e);
+    } else {
+      hipError_t err = allow_lds(k_ec<DTC, 2>, lds);
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL((k_ec<DTC, 2>), dim3(grid), dim3(block), lds, st, e);
+    }
   });
   return hipGetLastError();
 }
