@@ -18,6 +18,12 @@ line reports decode HBM throughput (algorithmic bytes / time) as `value`, the
 prefill MFMA throughput under `prefill`, each with its roofline, the EC
 overhead over the same passes without EC, and the CPU oracle timed on a
 bounded sample (`cpu_baseline`).
+
+Context line `decode_70b_layer`: one Llama-2-70B-shaped layer (7 modules,
+K/N up to 28672, EC rank 64 on every module) at M = 1, fused path, two weight
+copies alternating. Its weights are uniform random codes, scales and zero
+points drawn on the device (timing only: the kernels' work does not depend on
+the values), so that the 0.93 GB do not have to be generated on the host.
 """
 from __future__ import annotations
 
@@ -107,6 +113,73 @@ def cpu_baseline(dec_layers, pre_layer, budget_s=12.0):
     }
 
 
+def decode_70b_context(sp, torch, steps, warmup, dev):
+    """M = 1 decode of one 70B-shaped layer (fused W4+EC and W4-only)."""
+    from paper_2606_11244_amd import synth as S
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    r, G = 64, 128
+    mods = []
+    for c in range(2):
+        for m in S.MODULES:
+            K, N = S.LLAMA_70B[m]
+            q = torch.randint(-2**31, 2**31 - 1, (N, K // 8), dtype=torch.int32, device=dev, generator=g)
+            sc = (torch.rand((N, K // G), device=dev, generator=g) * 1e-3 + 1e-4).half().view(torch.int16)
+            zr = torch.randint(0, 16, (N, K // G), dtype=torch.uint8, device=dev, generator=g)
+            x = torch.randn((1, K), device=dev, generator=g).half()
+            A = (torch.randn((r, K), device=dev, generator=g) * 0.01).half()
+            B = (torch.randn((N, r), device=dev, generator=g) * 0.01).half()
+            wg = (torch.randn((K,), device=dev, generator=g) * 0.05).half()
+            y = torch.empty((1, N), dtype=torch.float16, device=dev)
+            pr = sp.problem(1, N, K, G, sp.F16, r, sp.GATE_SIGMOID_LINEAR)
+            mods.append((c, pr, q, sc, zr, x, A, B, wg, y, K, N))
+    ws = torch.zeros(max(max(sp.dispatch_plan(m[1]).workspace_bytes for m in mods), 256),
+                     dtype=torch.uint8, device=dev)
+    ws4 = torch.zeros(max(max(sp.dispatch_plan(m[1], with_ec=False).workspace_bytes for m in mods), 256),
+                      dtype=torch.uint8, device=dev)
+
+    def run(c, ec):
+        for (cc, pr, q, sc, zr, x, A, B, wg, y, K, N) in mods:
+            if cc != c:
+                continue
+            if ec:
+                sp.w4ec_linear(pr, x, q, sc, zr, A, B, y, w_g=wg, workspace=ws)
+            else:
+                sp.w4_linear(pr, x, q, sc, zr, y, workspace=ws4)
+
+    def timed(ec):
+        graphs = []
+        for c in range(2):
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                run(c, ec)
+            torch.cuda.current_stream().wait_stream(s)
+            torch.cuda.synchronize()
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                run(c, ec)
+            graphs.append(gr)
+        for i in range(warmup):
+            graphs[i % 2].replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(steps):
+            graphs[i % 2].replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / steps
+
+    t_ec, t_w4 = timed(True), timed(False)
+    nb = sum(algo_bytes(1, N, K, G, r) for (c, pr, q, sc, zr, x, A, B, wg, y, K, N) in mods if c == 0)
+    nb4 = sum(algo_bytes(1, N, K, G, 0) for (c, pr, q, sc, zr, x, A, B, wg, y, K, N) in mods if c == 0)
+    return {"GBps": round(nb / t_ec / 1e9, 1), "frac": round(nb / t_ec / 1e9 / HBM_PEAK_GBS, 4),
+            "us_per_layer": round(t_ec * 1e6, 2), "w4_only_GBps": round(nb4 / t_w4 / 1e9, 1),
+            "w4_only_us_per_layer": round(t_w4 * 1e6, 2), "ec_overhead": round(t_ec / t_w4 - 1, 4),
+            "rank": r, "path": "fused_gemv", "weights": "device-random (timing only)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +188,7 @@ def main():
     ap.add_argument("--copies", type=int, default=2, help="decode weight copies rotated per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overhead", action="store_true", help="skip the W4-only reference passes")
+    ap.add_argument("--no-70b", action="store_true", help="skip the 70B-layer context line")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -246,11 +320,19 @@ def main():
             "decode_ec_byte_share": round(dec_bytes / dec_bytes_w4 - 1.0, 4),
         }
 
+    ctx70 = None
+    if not args.no_70b:
+        print("bench: 70B-layer decode context", file=sys.stderr, flush=True)
+        ctx70 = decode_70b_context(sp, torch, args.steps, args.warmup, dev)
+
     if args.copy_calib_mb:
-        n = args.copy_calib_mb << 20
-        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        # counter calibration: one elementwise kernel that reads and writes
+        # exactly copy_calib_mb MiB each (fp32 negation)
+        n = (args.copy_calib_mb << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
-        b.copy_(a)
+        torch.cuda.synchronize()
+        torch.neg(a, out=b)
         torch.cuda.synchronize()
 
     traffic = stored_traffic()
@@ -297,6 +379,7 @@ def main():
             },
         },
         "decode_ms_per_pass": round(dec_s * 1e3, 4),
+        "decode_70b_layer": ctx70,
         "ec_overhead": overhead,
     }
     if not args.no_cpu_baseline:
