@@ -1169,7 +1169,7 @@ __device__ __forceinline__ void dequant_word_pairs(uint32_t w, float s, int z, u
 }
 
 template <int DT, int EPI>
-__global__ __launch_bounds__(256) void k_gemm(GemmParams a) {
+__global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int LR = kGemmLdsRow;
   constexpr int TILE = kGemmTM * LR;  // halves per LDS tile
@@ -1179,9 +1179,29 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams a) {
   const int lr = lane & 15, lg = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;
   const int M = a.M, N = a.N, K = a.K;
-  const int tiles_n = (N + kGemmTN - 1) / kGemmTN;
-  const int m0 = (blockIdx.x / tiles_n) * kGemmTM;
-  const int n0 = (blockIdx.x % tiles_n) * kGemmTN;
+  const int tiles_m = (M + kGemmTM - 1) / kGemmTM, tiles_n = (N + kGemmTN - 1) / kGemmTN;
+  // Workgroups are dealt to the eight XCDs in turn (b % 8), and each XCD has
+  // its own L2: give XCD x a contiguous band of token tiles (or, failing
+  // that, of row tiles) so that the tiles its workgroups share are fetched
+  // into its L2 once, instead of every activation tile once per XCD.
+  int mt_i, nt_i;
+  {
+    const int b = blockIdx.x, x = b & 7, j = b >> 3;
+    if ((tiles_m & 7) == 0) {
+      const int pm = tiles_m >> 3;
+      mt_i = x * pm + j % pm;
+      nt_i = j / pm;
+    } else if ((tiles_n & 7) == 0) {
+      const int pn = tiles_n >> 3;
+      nt_i = x * pn + j % pn;
+      mt_i = j / pn;
+    } else {
+      mt_i = b / tiles_n;
+      nt_i = b - mt_i * tiles_n;
+    }
+  }
+  const int m0 = mt_i * kGemmTM;
+  const int n0 = nt_i * kGemmTN;
   const int KT = K / kGemmTK;
 
   // per-thread global load assignments (bounds-checked buffer loads)
@@ -1203,20 +1223,31 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams a) {
   const bool wok = wn_row < N;
   const uint32_t woff = wok ? (uint32_t)wn_row * (K / 2) + 16 * wh : kOOB;
 
-  u32x4 xreg[4];
-  u32x4 wreg;
-  float sreg;
-  int zreg;
-  auto gload = [&](int kt) {
+  // two register sets of global loads, so that the loads of step kt+2 are
+  // in flight while step kt is computed. The scale and zero point stay raw
+  // until the stage is stored: converting them at load time would make the
+  // wave wait for every load issued before them (the vector-memory counter
+  // retires in order).
+  struct Stage {
+    u32x4 x[4];
+    u32x4 w;
+    uint32_t s, z;
+  };
+  Stage g0, g1;
+  auto gload = [&](Stage& st, int kt) {
     const uint32_t k0 = (uint32_t)kt * kGemmTK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) xreg[i] = bld128(rx, xoff[i] + k0 * 2);
-    wreg = bld128(rq, woff + k0 / 2);
+    for (int i = 0; i < 4; ++i) st.x[i] = bld128(rx, xoff[i] + k0 * 2);
+    st.w = bld128(rq, woff + k0 / 2);
     const uint32_t g = k0 / a.G;
-    sreg = h2f((uint16_t)bld16(rsc, wok ? ((uint32_t)wn_row * a.ngroups + g) * 2 : kOOB));
-    zreg = (int)bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
+    st.s = bld16(rsc, wok ? ((uint32_t)wn_row * a.ngroups + g) * 2 : kOOB);
+    st.z = bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
   };
-  auto lstore = [&](int buf) {
+  auto lstore = [&](const Stage& st, int buf) {
+    const u32x4 (&xreg)[4] = st.x;
+    const u32x4 wreg = st.w;
+    const float sreg = h2f((uint16_t)st.s);
+    const int zreg = (int)st.z;
     uint16_t* xs = Xs + buf * TILE;
     uint16_t* ws = Ws + buf * TILE;
 #pragma unroll
@@ -1235,12 +1266,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
+  auto compute = [&](int buf) {
     const uint16_t* xs = Xs + buf * TILE;
     const uint16_t* ws = Ws + buf * TILE;
 #pragma unroll
@@ -1255,8 +1281,35 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = mfma16<DT>(af[i], bf[j], acc[i][j]);
     }
-    if (kt + 1 < KT) lstore(buf ^ 1);
+  };
+
+  // Step kt computes LDS buffer kt & 1. Its loads were issued two steps
+  // earlier into register set kt & 1, and it is stored at the start of its
+  // step while the next step's loads are still in flight. K is a multiple of
+  // 128, so the steps come in pairs and the loop has a single exit; loads
+  // past the last step re-read it (never stored), so that every load is
+  // unconditional. Both ways into the loop head thus leave the same loads in
+  // flight, and the wait before a store covers only the stage being stored.
+  // One barrier per step: a buffer is rewritten only after every wave has
+  // passed the barrier that follows its last read.
+  const int kl = KT - 1;
+  gload(g0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  gload(g1, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int kt = 0; kt < KT; kt += 2) {
+    lstore(g0, 0);
     __syncthreads();
+    gload(g0, min(kt + 2, kl));
+    __builtin_amdgcn_sched_barrier(0);
+    compute(0);
+    __builtin_amdgcn_sched_barrier(0);
+    lstore(g1, 1);
+    __syncthreads();
+    gload(g1, min(kt + 3, kl));
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   if constexpr (EPI == EPI_READY) {
