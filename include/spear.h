@@ -88,9 +88,16 @@ enum {
   SPEAR_PATH_UNFUSED_CHAIN = 3,  /* naive split: 4-bit GEMM, then separate
                                     projection, gate and reprojection+accumulate
                                     kernels (the baseline of section 4.1)      */
-  SPEAR_PATH_UNFUSED_2K = 4      /* semi-fused: EC pre-kernel (A x, gate) then
+  SPEAR_PATH_UNFUSED_2K = 4,     /* semi-fused: EC pre-kernel (A x, gate) then
                                     the 4-bit GEMM/GEMV whose epilogue adds
                                     B (g (.) A x)                              */
+  SPEAR_PATH_FUSED_LOCAL = 5     /* one kernel: split-K 4-bit GEMV whose waves
+                                    also project x on [A; w_g] over their own K
+                                    chunks (no EC workgroups, no wait on other
+                                    workgroups beyond the split-K reduction);
+                                    rank <= 16, sigmoid-linear or identity
+                                    gate, M <= 32. AUTO picks it where it
+                                    applies, otherwise SPEAR_PATH_FUSED_GEMV   */
 };
 
 typedef struct {

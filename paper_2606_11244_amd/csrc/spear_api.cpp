@@ -24,6 +24,7 @@ std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0};
 // it the LDS-tiled MFMA GEMM. The same bound separates decode (fully fused
 // EC) from prefill (semi-fused EC pre-kernel) under SPEAR_PATH_AUTO.
 constexpr int64_t kGemvMaxM = 64;
+constexpr int64_t kLocalMaxM = 32;   // local EC variant: at most two token tiles
 // Largest staged slice of x in a GEMV block's LDS (16 tokens x 2048 K fit).
 constexpr size_t kXLdsMax = 66 * 1024;
 // Fused EC: the consumers gather the K-slices' partial sums themselves when
@@ -44,8 +45,8 @@ struct Resolved {
   int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
   int MT, RT, NW, nrg, S, ips, iw;            // GEMV shape
   int ntb, P, eips, PG, tpg, ec_mode, ec_ipp, ec_block, n_prod;  // EC shape
-  int xlds, xstride, bpre, lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz;
-  size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart;
+  int xlds, xstride, bpre, lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz, lds_a;
+  size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart, off_eupart;
   int npub, direct;
   size_t lds_gemv, lds_prod, lds_gate;
 };
@@ -62,7 +63,7 @@ spear_status_t validate_shape(const spear_problem_t* p, bool with_ec) {
   // kernels' 32-bit byte offsets and buffer-resource bounds cover it
   const int64_t lim = (int64_t)1 << 30;
   if (p->M * p->K >= lim || p->N * p->K >= lim || p->M * p->N >= lim) return SPEAR_E_SHAPE;
-  if (p->force_path < SPEAR_PATH_AUTO || p->force_path > SPEAR_PATH_UNFUSED_2K)
+  if (p->force_path < SPEAR_PATH_AUTO || p->force_path > SPEAR_PATH_FUSED_LOCAL)
     return SPEAR_E_UNSUPPORTED;
   if (with_ec) {
     if (p->rank < 0 || p->rank > 256) return SPEAR_E_SHAPE;
@@ -70,6 +71,25 @@ spear_status_t validate_shape(const spear_problem_t* p, bool with_ec) {
     if (p->gate_hidden < 0 || p->gate_hidden > 1024) return SPEAR_E_SHAPE;
   }
   return SPEAR_OK;
+}
+
+// Split-K of the decode GEMV: K-slices are added until about 4096 waves
+// cover the 256 CUs, keeping at least two iterations per wave so that the
+// pipeline has something to overlap. Returns the slice length in iterations.
+int gemv_ips(int IT, int nrg, int NW) {
+  int S = (int)std::lround(4096.0 / ((double)nrg * NW));
+  S = std::max(1, std::min(S, std::max(1, IT / (2 * NW))));
+  if (g_ov_s.load() > 0) S = std::min((int)g_ov_s.load(), IT);
+  return (int)cdiv(IT, S);
+}
+
+// Row tiles per GEMV block for MT token tiles (the local EC variant keeps one
+// row tile for two token tiles: registers).
+int gemv_rt(int MT, bool local) {
+  int RT = MT <= 2 ? 2 : 1;
+  if (local && MT == 2) RT = 1;
+  if (g_ov_rt.load() > 0) RT = g_ov_rt.load();
+  return RT;
 }
 
 spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
@@ -90,12 +110,28 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   z.h = z.gate == GATE_TANH ? (p->gate_hidden > 0 ? p->gate_hidden : 4 * z.r) : 0;
   z.vstride = (int)cdiv(std::max(z.r, 1), 32) * 32;
 
-  // path
+  // path. The local variant of the fused kernel (the GEMV waves project x on
+  // A and w_g themselves) applies to ranks up to 16 with an elementwise gate:
+  // each workgroup then reads A once more from L2, which stays cheap while A
+  // is one 16-row tile, and no workgroup waits for another.
   int path = p->force_path;
+  bool local_ok = z.ec && z.gate != GATE_TANH && z.r <= 16 && M <= kLocalMaxM;
+  if (local_ok) {
+    // the block's K-slice of A and w_g is staged in LDS
+    const int MT = (int)cdiv(M, 16), RT = gemv_rt(MT, true);
+    const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load())) : 8;
+    const int ips = gemv_ips(z.IT, (int)cdiv(N, 16 * RT), nw);
+    const size_t abytes = (size_t)17 * (ips * kIterK + 8) * 2;
+    const size_t partials = (size_t)nw * (RT + kLocalTiles) * MT * 1024;
+    local_ok = abytes <= kLocalALds && abytes + partials + 32768 <= kMaxLds;
+  }
   if (path == SPEAR_PATH_FUSED_MFMA) return SPEAR_E_UNSUPPORTED;
   if (path == SPEAR_PATH_FUSED_GEMV && M > kGemvMaxM) return SPEAR_E_UNSUPPORTED;
+  if (z.ec && path == SPEAR_PATH_FUSED_LOCAL && !local_ok) return SPEAR_E_UNSUPPORTED;
   if (path == SPEAR_PATH_AUTO || !z.ec)
-    path = (M <= kGemvMaxM) ? SPEAR_PATH_FUSED_GEMV : SPEAR_PATH_UNFUSED_2K;
+    path = M > kGemvMaxM ? SPEAR_PATH_UNFUSED_2K
+           : local_ok    ? SPEAR_PATH_FUSED_LOCAL
+                         : SPEAR_PATH_FUSED_GEMV;
   if (!with_ec) path = (M <= kGemvMaxM) ? SPEAR_PATH_FUSED_GEMV : SPEAR_PATH_UNFUSED_2K;
   z.gemv = M <= kGemvMaxM;
   z.plan.path = path;
@@ -105,6 +141,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     return SPEAR_OK;
   }
   const bool fused = z.ec && path == SPEAR_PATH_FUSED_GEMV;
+  const bool local = z.ec && path == SPEAR_PATH_FUSED_LOCAL;
 
   // 4-bit product shape
   if (z.gemv) {
@@ -114,21 +151,18 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     // iterations per wave so that the pipeline has something to overlap.
     z.MT = (int)cdiv(M, 16);
     z.NW = 8;
-    z.RT = z.MT <= 2 ? 2 : 1;
-    if (g_ov_rt.load() > 0) z.RT = g_ov_rt.load();
+    z.RT = gemv_rt(z.MT, local);
     if (!gemv_shape_supported(z.MT, z.RT)) return SPEAR_E_UNSUPPORTED;
     // the EC variants add the EC wave to the workgroup
     const int epi = !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN ? EPI_NONE
                     : path == SPEAR_PATH_FUSED_GEMV           ? EPI_FUSED
+                    : local                                   ? EPI_LOCAL
                                                               : EPI_READY;
-    const int max_nw = kGemvMaxThreads / 64 - (epi != EPI_NONE ? 1 : 0);
+    const int max_nw = kGemvMaxThreads / 64 - (epi == EPI_READY || epi == EPI_FUSED ? 1 : 0);
     z.NW = std::min(z.NW, max_nw);
     if (g_ov_nw.load() > 0) z.NW = std::max(1, std::min(max_nw, (int)g_ov_nw.load()));
     z.nrg = (int)cdiv(N, 16 * z.RT);
-    int S = (int)std::lround(4096.0 / ((double)z.nrg * z.NW));
-    S = std::max(1, std::min(S, std::max(1, z.IT / (2 * z.NW))));
-    if (g_ov_s.load() > 0) S = std::min((int)g_ov_s.load(), z.IT);
-    z.ips = (int)cdiv(z.IT, S);
+    z.ips = gemv_ips(z.IT, z.nrg, z.NW);
     z.S = (int)cdiv(z.IT, z.ips);
     z.iw = (int)cdiv(z.ips, z.NW);
     z.plan.split_k = z.S;
@@ -145,7 +179,11 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   // workgroup's waves, so that every producer is a single round of loads.
   // Prefill: one workgroup per token tile over all of K and all rows.
   z.ntb = (int)cdiv(M, kTokTile);
-  if (z.ec) {
+  if (local) {
+    // the projection is split like the 4-bit product: one slice per K-slice
+    z.P = z.S;
+    z.PG = 1;
+  } else if (z.ec) {
     const int RTe = (int)cdiv(z.R1, 16);
     if (z.gemv) {
       // fused producers are workgroups of the GEMV grid: its waves plus the EC wave
@@ -192,12 +230,19 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     z.xstride = z.ips * kIterK * 2 + 16;
     const size_t xbytes = (size_t)M * z.xstride;
     auto layout = [&](bool xl) {
-      size_t U = std::max((size_t)z.NW * z.RT * z.MT * 1024, (size_t)z.S * 4);
+      const int rtw = z.RT + (local ? kLocalTiles : 0);  // wave partial tiles
+      size_t U = std::max((size_t)z.NW * rtw * z.MT * 1024, (size_t)z.S * 4);
       if (xl) U = std::max(U, xbytes);
       z.lds_y = (int)align_up(U, 16);
       z.lds_e = z.lds_y + z.RT * z.MT * 1024;
       z.lds_b = z.lds_g = z.lds_ev = z.lds_e;
-      if (z.ec) {
+      if (local) {
+        // u [16 MT][R1p] and v [16 MT][r], the rows of B, the staged A, w_g
+        z.lds_b = (int)align_up(z.lds_e + (size_t)16 * z.MT * (z.R1p + z.r) * 4, 16);
+        z.bpre = (z.r % 8) == 0 && RB * z.r / 8 <= 2 * 64 * z.NW;
+        z.lds_a = (int)align_up(z.lds_b + (z.bpre ? (size_t)RB * z.r * 2 : 0), 16);
+        z.lds_g = z.lds_ev = (int)(z.lds_a + (size_t)17 * (z.ips * kIterK + 8) * 2);
+      } else if (z.ec) {
         z.lds_b = (int)(z.lds_e + ec_lds_bytes(z.R1p, z.h, z.r));
         z.bpre = (z.r % 8) == 0 && RB * z.r / 8 <= 2 * 64 * z.NW;
         z.lds_g = (int)align_up(z.lds_b + (z.bpre ? (size_t)RB * z.r * 2 : 0), 16);
@@ -205,7 +250,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
         if (fused && z.ec_mode == EC_GATHER)
           z.lds_ev = (int)(z.lds_g + (size_t)z.P * kTokTile * z.R1 * 4);
       }
-      z.lds_sz = z.lds_ev + (z.ec ? z.RT * z.MT * 1024 : 0);
+      z.lds_sz = z.lds_ev + (z.ec && !local ? z.RT * z.MT * 1024 : 0);
       const int ipg = z.G / kIterK;
       const int ngb = (int)std::min<int64_t>(z.ngroups, cdiv(z.ips, ipg) + 1);
       z.lds_gemv = z.lds_sz + (size_t)RB * (ngb | 1) * 4;
@@ -216,7 +261,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
       z.xlds = 0;
       layout(false);
     }
-    if (std::max(z.lds_gemv, z.lds_prod) > kMaxLds) return SPEAR_E_SHAPE;
+    if (std::max(z.lds_gemv, z.lds_prod) > kMaxLds) return local ? SPEAR_E_UNSUPPORTED : SPEAR_E_SHAPE;
   } else if (z.lds_prod > kMaxLds) {
     return SPEAR_E_SHAPE;
   }
@@ -224,7 +269,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
 
   // launches and grid
   const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
-  if (!z.ec) {
+  if (!z.ec || local) {
     z.plan.num_launches = 1;
     z.plan.grid = grid4;
   } else if (fused) {
@@ -250,7 +295,9 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     off = align_up(off + bytes, 256);
     return o;
   };
-  if (z.ec) {
+  if (local) {
+    if (z.S > 1) z.off_eupart = take((size_t)z.nrg * z.S * M * z.R1 * 4);
+  } else if (z.ec) {
     const bool partials = z.ec_mode != EC_GATHER && z.P * z.PG > 1;
     if (partials && z.ntb > kMaxEcCounters) return SPEAR_E_SHAPE;
     if (fused) {
@@ -389,6 +436,7 @@ GemvParams make_gemv(const spear_problem_t* p, const Resolved& z, const void* x,
   g.lds_g = z.lds_g;
   g.lds_ev = z.lds_ev;
   g.lds_sz = z.lds_sz;
+  g.lds_a = z.lds_a;
   if (ws && z.S > 1) {
     g.ypart = (float*)(ws + z.off_ypart);
     g.rb_ctr = (uint32_t*)(ws + kCtrRows);
@@ -474,6 +522,13 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   EcParams e = make_ec(prob, z, x, ec, ws);
   const int path = z.plan.path;
   const int ec_grid = z.ntb * z.P * z.PG;
+  if (path == SPEAR_PATH_FUSED_LOCAL) {
+    GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
+    g.ec = e;
+    if (z.S > 1) g.eupart = (float*)(ws + z.off_eupart);
+    return hip_status(
+        launch_gemv(z.dt, z.MT, z.RT, EPI_LOCAL, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, s));
+  }
   if (path == SPEAR_PATH_FUSED_GEMV) {
     e.vtag = (unsigned long long*)(ws + z.off_vtag);
     e.gen = (unsigned long long*)(ws + kCtrGen);

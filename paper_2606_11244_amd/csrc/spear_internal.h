@@ -13,7 +13,9 @@ enum { GATE_ONE = 0, GATE_SIGMOID = 1, GATE_TANH = 2 };
 // Epilogue variants of the 4-bit product kernels.
 enum { EPI_NONE = 0,   // Y = X W^T
        EPI_READY = 1,  // Y = X W^T + v B^T, v already in the workspace
-       EPI_FUSED = 2   // same, v produced by EC workgroups of the same grid
+       EPI_FUSED = 2,  // same, v produced by EC workgroups of the same grid
+       EPI_LOCAL = 3   // same, [A; w_g] x computed by the GEMV waves themselves
+                       // over their K chunks (small rank), v from it per block
 };
 // How the EC projection's K-slices are combined.
 enum { EC_LAST = 0,    // the last slice to arrive sums the partials, applies
@@ -31,6 +33,8 @@ constexpr int kGemmTN = 128;     // prefill tile: output rows
 constexpr int kGemmTK = 64;      // prefill tile: K per stage
 constexpr int kGemmLdsRow = kGemmTK + 8;  // padded LDS row (halves)
 constexpr int kVCopies = 8;      // copies of the published EC data (one per XCD)
+constexpr int kLocalTiles = 2;   // EPI_LOCAL: B operands per iteration: A (r <= 16), w_g
+constexpr size_t kLocalALds = 81920;  // EPI_LOCAL: LDS for the staged K-slice of A, w_g
 
 // Workspace: a fixed counter block at the start, shared by every kind of call
 // (each call leaves its counters as it found them), then the call's data.
@@ -114,6 +118,7 @@ struct GemvParams {
   int S, ips, iw;         // K-slices per row group, iterations per slice and per wave
   int n_prod;             // EC workgroups at the head of the grid (fused)
   float* ypart;           // [S][M][N] partial sums (S > 1)
+  float* eupart;          // EPI_LOCAL: [S][M][R1] partial sums of [A; w_g] x (S > 1)
   uint32_t* rb_ctr;       // [row groups] last-arriver counters
   int grid_total;         // fused: workgroups in the grid
   int wait_polls;
@@ -121,8 +126,10 @@ struct GemvParams {
   int xstride;            // its LDS row stride in bytes
   int bpre;               // 1: the epilogue's rows of B are staged in LDS
   // LDS carve-up (byte offsets): [x | wave partials] [yacc] [EC u/hidden/v]
-  // [rows of B] [gathered partials] [EC wave's result tiles] [scales]
+  // [rows of B] [gathered partials] [EC wave's result tiles] [scales];
+  // EPI_LOCAL: the EC region holds u [16 MT][R1p] and v [16 MT][r]
   int lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz;
+  int lds_a;              // EPI_LOCAL: [17][ips * 128 + 8] halves: A's 16 rows, w_g
   EcParams ec;
 };
 

@@ -853,7 +853,8 @@ template <int DT, int MT, int RT, int EPI>
 __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int s_flag;
-  constexpr bool kEC = EPI != EPI_NONE;
+  constexpr bool kEC = EPI == EPI_READY || EPI == EPI_FUSED;  // with an EC wave
+  constexpr bool kLoc = EPI == EPI_LOCAL;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int NW = (blockDim.x >> 6) - (kEC ? 1 : 0);           // GEMV waves
@@ -887,10 +888,12 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
   const rsrc_t rb = make_rsrc(a.B, (uint32_t)N * r * 2);
 
-  // the first K-slice's rows of B ([RB][r], contiguous) are fetched up front
-  // into LDS when two 16-byte chunks per thread cover them
+  // the rows of B ([RB][r], contiguous) of the block that adds v B^T (the
+  // first K-slice's with an EC wave; any slice's in EPI_LOCAL, whose last
+  // arriver adds it) are fetched up front into LDS when two 16-byte chunks
+  // per thread cover them
   constexpr int BCH = 2;
-  const bool bpre = EPI != EPI_NONE && s == 0 && a.bpre;
+  const bool bpre = ((kEC && s == 0) || kLoc) && a.bpre;
   const int bchunks = RB * r / 8;
   u32x4 bst[BCH];
   if (bpre) {
@@ -923,6 +926,34 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
 #pragma unroll
     for (int t = 0; t < RT; ++t) w[t] = bld128s(rq, vw[t], (uint32_t)it * (kIterK / 2));
   };
+  // EPI_LOCAL: the block's K-slice of A (16 rows, rows >= r zero) and of
+  // w_g (row 16) is staged in LDS with coalesced 16-byte chunks: read in the
+  // MFMA lane layout straight from memory, every load would touch 32 cache
+  // lines. The MFMAs then take A's rows (lane lr: row lr) and w_g in every
+  // column as two further B operands.
+  const rsrc_t ra = make_rsrc(kLoc ? a.ec.A : nullptr, kLoc ? (uint32_t)r * K * 2 : 0u);
+  const rsrc_t rgw = make_rsrc(kLoc ? a.ec.wg : nullptr,
+                               kLoc && a.ec.gate == GATE_SIGMOID ? (uint32_t)K * 2 : 0u);
+  const int acpr = (it_end - it_blk) * (kIterK / 8);  // 16-byte chunks per row
+  const int astride = acpr * 8 + 8;                   // LDS row stride (halves)
+  uint16_t* als = (uint16_t*)(smem + a.lds_a);        // [17][astride]
+  auto a_issue = [&](int base, u32x4 (&c4)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int ci = base + u * (int)blockDim.x;
+      const int row = ci / acpr, kc = ci - row * acpr;
+      c4[u] = bld128(ra, ci < 16 * acpr && row < r
+                             ? ((uint32_t)row * K + it_blk * kIterK + 8 * kc) * 2 : kOOB);
+    }
+  };
+  auto a_store = [&](int base, const u32x4 (&c4)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int ci = base + u * (int)blockDim.x;
+      const int row = ci / acpr, kc = ci - row * acpr;
+      if (ci < 16 * acpr) *(u32x4*)(als + row * astride + 8 * kc) = c4[u];
+    }
+  };
   auto load_x = [&](u32x4 (&xv)[MT][4], int it) {
     if (xl) {
       const uint32_t kb = (uint32_t)(it - it_blk) * (kIterK * 2);
@@ -939,32 +970,41 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
     }
   };
 
+  // Every global load of the prologue is issued before the first wait: the
+  // first two pipeline stages of codes, the block's slice of x, the scales
+  // and zero points, the rows of B. Small layers give a wave one or two
+  // iterations, so the prologue's round trips are most of the kernel.
   u32x4 wA[RT], wB[RT];
   u32x4 xA[MT][4], xB[MT][4];
+  const int last = iw_end - 1;
   if (iw_beg < iw_end) {
     load_w(wA, iw_beg);
-    if (!xl) load_x(xA, iw_beg);
-  }
-  // the block's slice of x into LDS ([M][slice] with a padded row stride)
-  if (xl) {
-    const int cpr = (it_end - it_blk) * (kIterK / 8);  // 16-byte chunks per row
-    const int nch = M * cpr;
-    for (int base = tid; base < nch; base += 4 * (int)blockDim.x) {
-      u32x4 c4[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int ci = base + u * (int)blockDim.x;
-        const int m = ci / cpr, kc = ci - m * cpr;
-        c4[u] = bld128(rx, ci < nch ? ((uint32_t)m * K + it_blk * kIterK + 8 * kc) * 2 : kOOB);
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int ci = base + u * (int)blockDim.x;
-        const int m = ci / cpr, kc = ci - m * cpr;
-        if (ci < nch) *(u32x4*)(smem + (size_t)m * a.xstride + 16 * kc) = c4[u];
-      }
+    load_w(wB, min(iw_beg + 1, last));
+    if (!xl) {
+      load_x(xA, iw_beg);
+      load_x(xB, min(iw_beg + 1, last));
     }
   }
+  // the block's slice of x into LDS ([M][slice] with a padded row stride),
+  // four 16-byte chunks per thread per round
+  const int cpr = (it_end - it_blk) * (kIterK / 8);  // 16-byte chunks per row
+  const int nch = xl ? M * cpr : 0;
+  auto x_issue = [&](int base, u32x4 (&c4)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int ci = base + u * (int)blockDim.x;
+      const int m = ci / cpr, kc = ci - m * cpr;
+      c4[u] = bld128(rx, ci < nch ? ((uint32_t)m * K + it_blk * kIterK + 8 * kc) * 2 : kOOB);
+    }
+  };
+  auto x_store = [&](int base, const u32x4 (&c4)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int ci = base + u * (int)blockDim.x;
+      const int m = ci / cpr, kc = ci - m * cpr;
+      if (ci < nch) *(u32x4*)(smem + (size_t)m * a.xstride + 16 * kc) = c4[u];
+    }
+  };
   // scales and zero points of the block's rows and groups, staged once in
   // LDS with coalesced loads ([row][group] as s | z << 16): per-iteration
   // scattered 2- and 1-byte loads would cost a cache-line request per row
@@ -973,30 +1013,56 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   const int ngb = (it_end - 1) / ipg + 1 - g_lo;
   const int ngs = ngb | 1;  // odd LDS row stride: rows fall on distinct banks
   uint32_t* szs = (uint32_t*)(smem + a.lds_sz);
-  {
-    // four entries per thread per round, all loads in flight together
-    const int nsz = RB * ngb, nthr = blockDim.x;
-    auto sz_off = [&](int idx, uint32_t& eo) -> bool {
+  const int nsz = RB * ngb;
+  auto sz_issue = [&](int i0, uint32_t (&sv)[4], uint32_t (&zv)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = i0 + u * (int)blockDim.x;
       const int row = idx / ngb, gg = idx - row * ngb;
-      eo = (uint32_t)(n0 + row) * a.ngroups + g_lo + gg;
-      return idx < nsz && n0 + row < N;
-    };
-    for (int i0 = tid; i0 < nsz; i0 += 4 * nthr) {
-      uint32_t sv[4], zv[4];
+      const uint32_t eo = (uint32_t)(n0 + row) * a.ngroups + g_lo + gg;
+      const bool ok = idx < nsz && n0 + row < N;
+      sv[u] = bld16(rsc, ok ? eo * 2 : kOOB);
+      zv[u] = bld8(rz, ok ? eo : kOOB);
+    }
+  };
+  auto sz_store = [&](int i0, const uint32_t (&sv)[4], const uint32_t (&zv)[4]) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        uint32_t eo;
-        const bool ok = sz_off(i0 + u * nthr, eo);
-        sv[u] = bld16(rsc, ok ? eo * 2 : kOOB);
-        zv[u] = bld8(rz, ok ? eo : kOOB);
+    for (int u = 0; u < 4; ++u) {
+      const int idx = i0 + u * (int)blockDim.x;
+      if (idx < nsz) {
+        const int row = idx / ngb, gg = idx - row * ngb;
+        szs[row * ngs + gg] = sv[u] | (zv[u] << 16);
       }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int idx = i0 + u * nthr;
-        if (idx < nsz) {
-          const int row = idx / ngb, gg = idx - row * ngb;
-          szs[row * ngs + gg] = sv[u] | (zv[u] << 16);
-        }
+    }
+  };
+  {
+    const int step = 4 * (int)blockDim.x;
+    u32x4 c4[4];
+    uint32_t sv[4], zv[4];
+    x_issue(tid, c4);
+    sz_issue(tid, sv, zv);
+    x_store(tid, c4);
+    sz_store(tid, sv, zv);
+    for (int base = tid + step; base < nch; base += step) {
+      x_issue(base, c4);
+      x_store(base, c4);
+    }
+    for (int i0 = tid + step; i0 < nsz; i0 += step) {
+      sz_issue(i0, sv, zv);
+      sz_store(i0, sv, zv);
+    }
+    if constexpr (kLoc) {
+      // A: two rounds of four chunks per thread in flight; w_g: one chunk
+      for (int base = tid; base < 16 * acpr; base += 2 * step) {
+        u32x4 a0[4], a1[4];
+        a_issue(base, a0);
+        a_issue(base + step, a1);
+        a_store(base, a0);
+        a_store(base + step, a1);
+      }
+      for (int kc = tid; kc < acpr; kc += blockDim.x) {
+        const u32x4 gv = bld128(rgw, ((uint32_t)it_blk * kIterK + 8 * kc) * 2);
+        *(u32x4*)(als + 16 * astride + 8 * kc) = gv;
       }
     }
   }
@@ -1009,7 +1075,10 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
     }
   }
   __syncthreads();
-  if (xl && iw_beg < iw_end) load_x(xA, iw_beg);
+  if (xl && iw_beg < iw_end) {
+    load_x(xA, iw_beg);
+    load_x(xB, min(iw_beg + 1, last));
+  }
 
   constexpr float kBias = code_bias<DT>();
   f32x4 acc[RT][MT];
@@ -1019,7 +1088,28 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
     for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   const uint32_t km = opaque_v(0x000F000Fu);
   const uint32_t kg = opaque_v(DT == DT_F16 ? 0x64006400u : 0x43004300u);
+  f32x4 eacc[kLocalTiles][MT];
+#pragma unroll
+  for (int t = 0; t < kLocalTiles; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) eacc[t][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto compute = [&](const u32x4 (&w)[RT], const u32x4 (&xv)[MT][4], int it) {
+    if constexpr (kLoc) {
+      // A x and w_g x: activations (A operand, token rows) times the rows of
+      // A / copies of w_g (B operand, one per column) from LDS, accumulated
+      // over the wave's chunk
+      const int kb = (it - it_blk) * kIterK + 32 * lg;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const u32x4 af = *(const u32x4*)(als + lr * astride + kb + 8 * jj);
+        const u32x4 gf = *(const u32x4*)(als + 16 * astride + kb + 8 * jj);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          eacc[0][mt] = mfma16<DT>(xv[mt][jj], af, eacc[0][mt]);
+          eacc[1][mt] = mfma16<DT>(xv[mt][jj], gf, eacc[1][mt]);
+        }
+      }
+    }
     f32x4 xb[MT];
     u32x4 xp[MT][4];
 #pragma unroll
@@ -1052,21 +1142,20 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   };
 
   // software pipeline over this wave's iterations: batch it+1 is in flight
-  // while batch it is computed (two register sets, alternating). Loads past
-  // the wave's last iteration re-read that iteration (never computed), so
-  // every load is unconditional.
+  // while batch it is computed (two register sets, alternating, both filled
+  // by the prologue). Loads past the wave's last iteration re-read that
+  // iteration (never computed), so every load is unconditional.
   if (iw_beg < iw_end) {
-    const int last = iw_end - 1;
     for (int it = iw_beg; it < iw_end; it += 2) {
-      load_w(wB, min(it + 1, last));
-      load_x(xB, min(it + 1, last));
-      __builtin_amdgcn_sched_barrier(0);
       compute(wA, xA, it);
       if (it + 1 >= iw_end) break;
       load_w(wA, min(it + 2, last));
       load_x(xA, min(it + 2, last));
       __builtin_amdgcn_sched_barrier(0);
       compute(wB, xB, it + 1);
+      load_w(wB, min(it + 3, last));
+      load_x(xB, min(it + 3, last));
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   if constexpr (kEC) {
@@ -1077,14 +1166,38 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   // ---- cross-wave reduction (fixed order) into yacc[token][row]; the EC
   // wave's tiles come last
   float* red = (float*)smem;
+  float* ered = red + NW * RT * MT * 256;  // EPI_LOCAL: [NW][kLocalTiles][MT] tiles
   if (gw) {
 #pragma unroll
     for (int t = 0; t < RT; ++t)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
         *(f32x4*)(red + (((wave * RT + t) * MT + mt) * 64 + lane) * 4) = acc[t][mt];
+    if constexpr (kLoc) {
+#pragma unroll
+      for (int t = 0; t < kLocalTiles; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          *(f32x4*)(ered + (((wave * kLocalTiles + t) * MT + mt) * 64 + lane) * 4) = eacc[t][mt];
+    }
   }
   __syncthreads();
+  // EPI_LOCAL: this block's [A; w_g] x (its K-slice), u [token][R1p] in LDS
+  float* u_loc = (float*)(smem + a.lds_e);
+  const int R1 = a.ec.R1, R1p = a.ec.R1p;
+  if constexpr (kLoc) {
+    // tile 0: column j < r is u_j; tile 1: column 0 is the gate logit w_g x
+    for (int e = tid; e < 256 * kLocalTiles * MT; e += blockDim.x) {
+      const int tm = e >> 8, rem = e & 255, ln = rem >> 2, i = rem & 3;
+      const int t = tm / MT, mt = tm - t * MT;
+      const int tok = 16 * mt + 4 * (ln >> 4) + i, c = ln & 15;
+      const int j = t == 0 ? (c < r ? c : -1) : (c == 0 && R1 > r ? r : -1);
+      if (j < 0) continue;
+      float v = 0.f;
+      for (int w = 0; w < NW; ++w) v += ered[(((w * kLocalTiles + t) * MT + mt) * 64 + ln) * 4 + i];
+      u_loc[tok * R1p + j] = v;
+    }
+  }
   float* yacc = (float*)(smem + a.lds_y);
   const float* evs = (const float*)(smem + a.lds_ev);
   const bool add_ev = kEC && s == 0;
@@ -1106,6 +1219,14 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
       const int m = e / RB, row = e - m * RB;
       if (n0 + row < N) st_agent(a.ypart + ((size_t)s * M + m) * N + n0 + row, yacc[m * YS + row]);
     }
+    if constexpr (kLoc) {
+      // the slice's partial [A; w_g] x, for the last arriver of this row
+      // group (which waits for this row group's slices only)
+      for (int e = tid; e < M * R1; e += blockDim.x) {
+        const int m = e / R1, j = e - m * R1;
+        st_agent(a.eupart + ((size_t)(rg * a.S + s) * M + m) * R1 + j, u_loc[m * R1p + j]);
+      }
+    }
     complete_and_sync();
     if (tid == 0) s_flag = arrive_last(a.rb_ctr + rg, (uint32_t)a.S) ? 1 : 0;
     __syncthreads();
@@ -1123,11 +1244,63 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
       const int m = i / RB, row = i - m * RB;
       yacc[m * YS + row] = v;
     });
+    if constexpr (kLoc) {
+      // this row group's slices' [A; w_g] x, summed in slice order
+      const rsrc_t re = make_rsrc(a.eupart, (uint32_t)((size_t)a.N / RB + 1) * a.S * M * R1 * 4);
+      sum_slices(re, a.S, M * R1, [&](int q, int i) {
+        return (uint32_t)(((size_t)(rg * a.S + q) * M) * R1 + i) * 4u;
+      }, red, a.lds_y / 4, [&](int i, float v) {
+        const int m = i / R1, j = i - m * R1;
+        u_loc[m * R1p + j] = v;
+      });
+    }
   }
+
+  // EPI_LOCAL: v = alpha g(x) (.) A x for every token (g the sigmoid of the
+  // gate row's sum plus b_g, or one), then y += v B^T in fp32 below
+  float* v_loc = u_loc + 16 * MT * R1p;
+  if constexpr (kLoc) {
+    for (int idx = tid; idx < M * r; idx += blockDim.x) {
+      const int m = idx / r, j = idx - m * r;
+      float g = 1.f;
+      if (a.ec.gate == GATE_SIGMOID) {
+        const float z = u_loc[m * R1p + r] + a.ec.b_g;
+        g = z >= 0.f ? 1.f / (1.f + __expf(-z)) : __expf(z) / (1.f + __expf(z));
+      }
+      v_loc[idx] = a.ec.alpha * g * u_loc[m * R1p + j];
+    }
+    __syncthreads();
+  }
+  const uint16_t* bsl = (const uint16_t*)(smem + a.lds_b);
 
   for (int e = tid; e < RB * M; e += blockDim.x) {
     const int m = e / RB, row = e - m * RB;
-    if (n0 + row < N) a.y[(size_t)m * N + n0 + row] = f2act<DT>(yacc[m * YS + row]);
+    if (n0 + row < N) {
+      float v = yacc[m * YS + row];
+      if constexpr (kLoc) {
+        // v B^T for this row: eight ranks per 16-byte chunk of the staged row
+        // of B (r is a multiple of 8 when B is staged), independent loads
+        const float* vm = v_loc + m * r;
+        float ev = 0.f;
+        if (bpre) {
+          for (int j0 = 0; j0 < r; j0 += 8) {
+            const u32x4 b8 = *(const u32x4*)(bsl + row * r + j0);
+            const f32x4 v0 = *(const f32x4*)(vm + j0), v1 = *(const f32x4*)(vm + j0 + 4);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float vlo = q < 2 ? v0[2 * q] : v1[2 * q - 4];
+              const float vhi = q < 2 ? v0[2 * q + 1] : v1[2 * q - 3];
+              ev += vlo * act2f<DT>((uint16_t)(b8[q] & 0xFFFFu)) + vhi * act2f<DT>((uint16_t)(b8[q] >> 16));
+            }
+          }
+        } else {
+          const uint16_t* br = a.B + (size_t)(n0 + row) * r;
+          for (int j = 0; j < r; ++j) ev += vm[j] * act2f<DT>(br[j]);
+        }
+        v += ev;
+      }
+      a.y[(size_t)m * N + n0 + row] = f2act<DT>(v);
+    }
   }
   if constexpr (EPI == EPI_FUSED) fused_exit(a);
 }
@@ -1440,14 +1613,17 @@ static hipError_t gemv_launch(int epi, const GemvParams& p, int grid, int block,
                               hipStream_t st) {
   hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, EPI_NONE>, lds)
                    : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, EPI_READY>, lds)
-                                      : allow_lds(k_gemv<DT, MT, RT, EPI_FUSED>, lds);
+                   : epi == EPI_FUSED ? allow_lds(k_gemv<DT, MT, RT, EPI_FUSED>, lds)
+                                      : allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL>, lds);
   if (err != hipSuccess) return err;
   if (epi == EPI_NONE)
     hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_NONE>), dim3(grid), dim3(block), lds, st, p);
   else if (epi == EPI_READY)
     hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_READY>), dim3(grid), dim3(block), lds, st, p);
-  else
+  else if (epi == EPI_FUSED)
     hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_FUSED>), dim3(grid), dim3(block), lds, st, p);
+  else
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL>), dim3(grid), dim3(block), lds, st, p);
   return hipGetLastError();
 }
 

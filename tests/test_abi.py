@@ -49,6 +49,9 @@ def _plan(**kw):
     (dict(gate_kind=3), -6), (dict(gate_hidden=-1), -2), (dict(gate_hidden=2048), -2),
     (dict(force_path=7), -6), (dict(force_path=sp.PATH_FUSED_MFMA), -6),
     (dict(force_path=sp.PATH_FUSED_GEMV, M=65), -6),
+    (dict(force_path=sp.PATH_FUSED_LOCAL, M=33), -6),
+    (dict(force_path=sp.PATH_FUSED_LOCAL, rank=17), -6),
+    (dict(force_path=sp.PATH_FUSED_LOCAL, gate_kind=sp.GATE_TANH_MLP), -6),
     (dict(M=1 << 20, K=1 << 12), -2),
 ])
 def test_plan_validation(kw, code):
@@ -66,9 +69,19 @@ def test_plan_rejects_null():
 def test_plan_phase_aware_dispatch():
     """Decode token counts get the single fused kernel, prefill the semi-fused
     pre-kernel + GEMM (section 4.1)."""
-    for M in (1, 4, 16, 17, 32, 64):
+    for M in (1, 4, 16, 17, 32):
+        # rank 16 + the gate row fit two 16-row tiles: the local fused variant
+        p = _plan(M=M)
+        assert p.path == sp.PATH_FUSED_LOCAL and p.num_launches == 1, M
+        p = _plan(M=M, rank=32)
+        assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
+        p = _plan(M=M, gate_kind=sp.GATE_TANH_MLP)
+        assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
+    for M in (33, 64):
         p = _plan(M=M)
         assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
+    assert _plan(M=4, force_path=sp.PATH_FUSED_GEMV).path == sp.PATH_FUSED_GEMV
+    assert _plan(M=4, force_path=sp.PATH_FUSED_LOCAL).grid == _plan(M=4, with_ec=False).grid
     for M in (65, 512, 4096):
         p = _plan(M=M)
         assert p.path == sp.PATH_UNFUSED_2K and p.num_launches == 2, M
