@@ -360,7 +360,8 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_gemv (fused W4+EC decode), all launches of the decode pass",
+            "kernel": ("k_gemv (one-kernel W4+EC decode GEMV, %s), all launches of the decode pass"
+                       % sp.PATH_NAMES[dec_plan.path]),
             "achieved": round(dec_bytes / n_launch_dec / (dec_s / n_launch_dec) / 1e9, 2),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),

@@ -29,7 +29,7 @@ constexpr int64_t kLocalMaxM = 32;   // local EC variant: at most two token tile
 constexpr size_t kXLdsMax = 66 * 1024;
 // Fused EC: the consumers gather the K-slices' partial sums themselves when
 // there are at most this many words per launch (slices x tokens x (r + 1)).
-constexpr int64_t kGatherMaxWords = 2048;
+constexpr int64_t kGatherMaxWords = 1024;
 constexpr int kEcWaves = 8;  // waves of an EC pre-kernel block (decode)
 constexpr size_t kMaxLds = 160 * 1024;  // LDS of one CU
 // Fused EC: consumers poll the published data directly (instead of a ready
