@@ -210,14 +210,15 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
       }
       z.lds_prod = ec_block_lds(nw, z.R1p, z.h, z.r);
     } else {
-      z.ec_block = 256;
+      // eight waves of two iterations per pass: K = 2048 is one pass
+      z.ec_block = 512;
       z.ec_ipp = 2;
       z.eips = z.IT;
       z.P = 1;
       z.PG = 1;
       z.tpg = RTe;
       z.ec_mode = path == SPEAR_PATH_UNFUSED_CHAIN ? EC_RAW : EC_LAST;
-      z.lds_prod = ec_block_lds(4, z.R1p, z.h, z.r);
+      z.lds_prod = ec_block_lds(8, z.R1p, z.h, z.r);
     }
     z.lds_gate = ec_lds_bytes(z.R1p, z.h, z.r);
   }

@@ -310,7 +310,11 @@ __device__ void ec_project(const EcParams& e, int tb, int it_beg, int it_end, in
   const rsrc_t rx = make_rsrc(e.x, (uint32_t)e.M * e.K * 2);
   const rsrc_t ra = make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
   const rsrc_t rg = make_rsrc(e.wg, e.gate == GATE_SIGMOID ? (uint32_t)e.K * 2 : 0u);
-  const uint32_t xoff = (uint32_t)m * e.K * 2 + 64 * lg;
+  // K order within an iteration: MFMA jj, lane group lg takes K
+  // [8 lg + 32 jj, +8) for both operands, so that each load reads 64
+  // contiguous bytes per row (the MFMA lane layout would otherwise spread a
+  // load over twice as many cache lines)
+  const uint32_t xoff = (uint32_t)m * e.K * 2 + 16 * lg;
   for (int tg0 = t_beg; tg0 < t_end; tg0 += kEcTiles) {
     const int nt = min(kEcTiles, t_end - tg0);
     f32x4 acc[kEcTiles];
@@ -320,28 +324,39 @@ __device__ void ec_project(const EcParams& e, int tb, int it_beg, int it_end, in
     for (int t = 0; t < kEcTiles; ++t) {
       acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       const int j = (tg0 + t) * 16 + lr;
-      aoff[t] = (t < nt && j < e.r) ? (uint32_t)j * e.K * 2 + 64 * lg : kOOB;
-      goff[t] = (t < nt && j == e.r && e.gate == GATE_SIGMOID) ? 64u * lg : kOOB;
+      aoff[t] = (t < nt && j < e.r) ? (uint32_t)j * e.K * 2 + 16 * lg : kOOB;
+      goff[t] = (t < nt && j == e.r && e.gate == GATE_SIGMOID) ? 16u * lg : kOOB;
       // uniform: does this row tile hold the gate row?
       has_g[t] = t < nt && e.gate == GATE_SIGMOID && e.r >= (tg0 + t) * 16 &&
                  e.r < (tg0 + t + 1) * 16;
     }
+    // the gate row's tile (uniform), or -1; w_g goes to registers of its own
+    // and joins that tile's operand only at the MFMA (a value combined right
+    // after its load would make the wave wait for every earlier load)
+    int gt = -1;
+#pragma unroll
+    for (int t = 0; t < kEcTiles; ++t)
+      if (has_g[t]) gt = t;
+    uint32_t goff_g = kOOB;
+#pragma unroll
+    for (int t = 0; t < kEcTiles; ++t)
+      if (t == gt) goff_g = goff[t];
     for (int it0 = it_beg + wave * IPP; it0 < it_end; it0 += NW * IPP) {
-      u32x4 xv[IPP][4], av[IPP][kEcTiles][4];
+      u32x4 xv[IPP][4], av[IPP][kEcTiles][4], gv[IPP][4];
 #pragma unroll
       for (int h = 0; h < IPP; ++h) {
         const bool ok = it0 + h < it_end;  // uniform
         const uint32_t kb = (uint32_t)(it0 + h) * (kIterK * 2);
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) xv[h][jj] = bld128(rx, ok ? xoff + kb + 16 * jj : kOOB);
+        for (int jj = 0; jj < 4; ++jj) xv[h][jj] = bld128(rx, ok ? xoff + kb + 64 * jj : kOOB);
 #pragma unroll
         for (int t = 0; t < kEcTiles; ++t)
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            av[h][t][jj] = bld128(ra, ok && aoff[t] != kOOB ? aoff[t] + kb + 16 * jj : kOOB);
-            if (has_g[t])
-              av[h][t][jj] |= bld128(rg, ok && goff[t] != kOOB ? goff[t] + kb + 16 * jj : kOOB);
-          }
+          for (int jj = 0; jj < 4; ++jj)
+            av[h][t][jj] = bld128(ra, ok && aoff[t] != kOOB ? aoff[t] + kb + 64 * jj : kOOB);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          gv[h][jj] = bld128(rg, ok && goff_g != kOOB ? goff_g + kb + 64 * jj : kOOB);
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -349,7 +364,8 @@ __device__ void ec_project(const EcParams& e, int tb, int it_beg, int it_end, in
 #pragma unroll
         for (int t = 0; t < kEcTiles; ++t)
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) acc[t] = mfma16<DT>(av[h][t][jj], xv[h][jj], acc[t]);
+          for (int jj = 0; jj < 4; ++jj)
+            acc[t] = mfma16<DT>(t == gt ? (av[h][t][jj] | gv[h][jj]) : av[h][t][jj], xv[h][jj], acc[t]);
     }
     // lane l holds token l % 16 and rows 4 * (l / 16) .. + 3 of each tile
 #pragma unroll
@@ -616,19 +632,21 @@ __device__ void ec_project_wave(const EcParams& e, int tb, float* u_lds) {
   const rsrc_t rx = make_rsrc(e.x, (uint32_t)e.M * e.K * 2);
   const rsrc_t ra = make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
   const rsrc_t rg = make_rsrc(e.wg, e.gate == GATE_SIGMOID ? (uint32_t)e.K * 2 : 0u);
-  const uint32_t xoff = (uint32_t)m * e.K * 2 + 64 * lg;
+  // K order within an iteration: MFMA jj, lane group lg takes K
+  // [8 lg + 32 jj, +8), so that each load reads 64 contiguous bytes per row
+  const uint32_t xoff = (uint32_t)m * e.K * 2 + 16 * lg;
   for (int t = 0; t < RTe; ++t) {
     const int j = t * 16 + lr;
-    const uint32_t aoff = j < e.r ? (uint32_t)j * e.K * 2 + 64 * lg : kOOB;
-    const uint32_t goff = (j == e.r && e.gate == GATE_SIGMOID) ? 64u * lg : kOOB;
+    const uint32_t aoff = j < e.r ? (uint32_t)j * e.K * 2 + 16 * lg : kOOB;
+    const uint32_t goff = (j == e.r && e.gate == GATE_SIGMOID) ? 16u * lg : kOOB;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int it = 0; it < IT; ++it) {
       const uint32_t kb = (uint32_t)it * (kIterK * 2);
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const u32x4 xv = bld128(rx, xoff + kb + 16 * jj);
-        u32x4 av = bld128(ra, aoff != kOOB ? aoff + kb + 16 * jj : kOOB);
-        av |= bld128(rg, goff != kOOB ? goff + kb + 16 * jj : kOOB);
+        const u32x4 xv = bld128(rx, xoff + kb + 64 * jj);
+        u32x4 av = bld128(ra, aoff != kOOB ? aoff + kb + 64 * jj : kOOB);
+        av |= bld128(rg, goff != kOOB ? goff + kb + 64 * jj : kOOB);
         acc = mfma16<DT>(av, xv, acc);
       }
     }
