@@ -83,8 +83,11 @@ enum {
   SPEAR_PATH_FUSED_GEMV = 1,     /* one kernel: split-K 4-bit GEMV; the same grid
                                     computes A x and the gate, and the epilogue
                                     adds B (g (.) A x). Decode, M <= 64.       */
-  SPEAR_PATH_FUSED_MFMA = 2,     /* reserved: fully fused MFMA GEMM (not built;
-                                    returns SPEAR_E_UNSUPPORTED)               */
+  SPEAR_PATH_FUSED_MFMA = 2,     /* one kernel: the 4-bit MFMA GEMM also projects
+                                    its activation tiles on A and w_g, and its
+                                    epilogue applies the gate and adds
+                                    B (g (.) A x); rank <= 16, sigmoid-linear or
+                                    identity gate (else SPEAR_E_UNSUPPORTED)   */
   SPEAR_PATH_UNFUSED_CHAIN = 3,  /* naive split: 4-bit GEMM, then separate
                                     projection, gate and reprojection+accumulate
                                     kernels (the baseline of section 4.1)      */

@@ -125,7 +125,10 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     const size_t partials = (size_t)nw * (RT + kLocalTiles) * MT * 1024;
     local_ok = abytes <= kLocalALds && abytes + partials + 32768 <= kMaxLds;
   }
-  if (path == SPEAR_PATH_FUSED_MFMA) return SPEAR_E_UNSUPPORTED;
+  // the fully fused GEMM: the projection rides on the GEMM's activation
+  // tiles (one 16-row tile of A plus w_g), the gate and v B^T in its epilogue
+  const bool mfma_ok = z.ec && z.gate != GATE_TANH && z.r <= 16;
+  if (z.ec && path == SPEAR_PATH_FUSED_MFMA && !mfma_ok) return SPEAR_E_UNSUPPORTED;
   if (path == SPEAR_PATH_FUSED_GEMV && M > kGemvMaxM) return SPEAR_E_UNSUPPORTED;
   if (z.ec && path == SPEAR_PATH_FUSED_LOCAL && !local_ok) return SPEAR_E_UNSUPPORTED;
   if (path == SPEAR_PATH_AUTO || !z.ec)
@@ -133,7 +136,8 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
            : local_ok    ? SPEAR_PATH_FUSED_LOCAL
                          : SPEAR_PATH_FUSED_GEMV;
   if (!with_ec) path = (M <= kGemvMaxM) ? SPEAR_PATH_FUSED_GEMV : SPEAR_PATH_UNFUSED_2K;
-  z.gemv = M <= kGemvMaxM;
+  const bool fmfma = z.ec && path == SPEAR_PATH_FUSED_MFMA;
+  z.gemv = M <= kGemvMaxM && !fmfma;
   z.plan.path = path;
 
   if (M == 0 || N == 0) {
@@ -179,7 +183,10 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   // workgroup's waves, so that every producer is a single round of loads.
   // Prefill: one workgroup per token tile over all of K and all rows.
   z.ntb = (int)cdiv(M, kTokTile);
-  if (local) {
+  if (fmfma) {
+    z.P = 1;  // each GEMM workgroup projects its token tile over all of K
+    z.PG = 1;
+  } else if (local) {
     // the projection is split like the 4-bit product: one slice per K-slice
     z.P = z.S;
     z.PG = 1;
@@ -270,7 +277,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
 
   // launches and grid
   const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
-  if (!z.ec || local) {
+  if (!z.ec || local || fmfma) {
     z.plan.num_launches = 1;
     z.plan.grid = grid4;
   } else if (fused) {
@@ -298,6 +305,8 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   };
   if (local) {
     if (z.S > 1) z.off_eupart = take((size_t)z.nrg * z.S * M * z.R1 * 4);
+  } else if (fmfma) {
+    // no workspace data
   } else if (z.ec) {
     const bool partials = z.ec_mode != EC_GATHER && z.P * z.PG > 1;
     if (partials && z.ntb > kMaxEcCounters) return SPEAR_E_SHAPE;
@@ -466,6 +475,14 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
     g.vh = (const uint16_t*)(ws + z.off_vh);
     g.vl = (const uint16_t*)(ws + z.off_vl);
   }
+  if (ec && z.plan.path == SPEAR_PATH_FUSED_MFMA) {
+    g.B = (const uint16_t*)ec->B;
+    g.A = (const uint16_t*)ec->A;
+    g.wg = (const uint16_t*)ec->w_g;
+    g.alpha = ec->alpha;
+    g.b_g = ec->b_g;
+    g.gate = z.gate;
+  }
   return g;
 }
 
@@ -523,6 +540,10 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   EcParams e = make_ec(prob, z, x, ec, ws);
   const int path = z.plan.path;
   const int ec_grid = z.ntb * z.P * z.PG;
+  if (path == SPEAR_PATH_FUSED_MFMA) {
+    GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
+    return hip_status(launch_gemm(z.dt, EPI_LOCAL, g, s));
+  }
   if (path == SPEAR_PATH_FUSED_LOCAL) {
     GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
     g.ec = e;

@@ -143,7 +143,14 @@ struct GemmParams {
   const uint16_t* vh;     // [M][vstride]
   const uint16_t* vl;
   int M, N, K, G, ngroups, r, vstride;
+  // EPI_LOCAL (fully fused prefill): the projection's inputs
+  const uint16_t* A;      // [r][K], r <= 16
+  const uint16_t* wg;     // [K] (sigmoid gate) or null
+  float alpha, b_g;
+  int gate;
 };
+// EPI_LOCAL GEMM: the EC stage tile holds A's 16 rows and w_g (row 16)
+constexpr int kGemmEcRows = 17;
 
 __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 

@@ -1362,10 +1362,13 @@ __device__ __forceinline__ void dequant_word_pairs(uint32_t w, float s, int z, u
 template <int DT, int EPI>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr bool kLoc = EPI == EPI_LOCAL;
   constexpr int LR = kGemmLdsRow;
   constexpr int TILE = kGemmTM * LR;  // halves per LDS tile
+  constexpr int ETILE = kGemmEcRows * LR;
   uint16_t* Xs = (uint16_t*)smem;             // [2][128][LR]
   uint16_t* Ws = Xs + 2 * TILE;               // [2][128][LR]
+  uint16_t* Es = Ws + 2 * TILE;               // EPI_LOCAL: [2][17][LR] A rows, w_g
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;
@@ -1413,6 +1416,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   const int wn_row = n0 + wr;
   const bool wok = wn_row < N;
   const uint32_t woff = wok ? (uint32_t)wn_row * (K / 2) + 16 * wh : kOOB;
+  // EPI_LOCAL: thread t < 136 stages 16 bytes of the EC tile per step: row
+  // t / 8 (A's row while below r, zero up to 15; w_g as row 16), chunk t % 8
+  const int er = tid >> 3, ec8 = tid & 7;
+  const rsrc_t ra = make_rsrc(kLoc ? a.A : nullptr, kLoc ? (uint32_t)a.r * K * 2 : 0u);
+  const rsrc_t rgw = make_rsrc(kLoc ? a.wg : nullptr,
+                               kLoc && a.gate == GATE_SIGMOID ? (uint32_t)K * 2 : 0u);
+  const uint32_t eoff = er < 16 && er < a.r ? ((uint32_t)er * K + 8 * ec8) * 2 : kOOB;
+  const uint32_t goff = er == 16 ? 16u * ec8 : kOOB;
 
   // two register sets of global loads, so that the loads of step kt+2 are
   // in flight while step kt is computed. The scale and zero point stay raw
@@ -1423,6 +1434,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     u32x4 x[4];
     u32x4 w;
     uint32_t s, z;
+    u32x4 e, g;  // EPI_LOCAL: A / w_g chunk, combined when stored
   };
   Stage g0, g1;
   auto gload = [&](Stage& st, int kt) {
@@ -1433,6 +1445,10 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     const uint32_t g = k0 / a.G;
     st.s = bld16(rsc, wok ? ((uint32_t)wn_row * a.ngroups + g) * 2 : kOOB);
     st.z = bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
+    if constexpr (kLoc) {
+      st.e = bld128(ra, eoff == kOOB ? kOOB : eoff + k0 * 2);
+      st.g = bld128(rgw, goff == kOOB ? kOOB : goff + k0 * 2);
+    }
   };
   auto lstore = [&](const Stage& st, int buf) {
     const u32x4 (&xreg)[4] = st.x;
@@ -1449,6 +1465,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
       dequant_word_pairs<DT>(wreg[c], sreg, zreg, o);
       *(u32x4*)(ws + wr * LR + 32 * wh + 8 * c) = u32x4{o[0], o[1], o[2], o[3]};
     }
+    if constexpr (kLoc) {
+      if (tid < kGemmEcRows * 8) *(u32x4*)(Es + buf * ETILE + er * LR + 8 * ec8) = st.e | st.g;
+    }
   };
 
   f32x4 acc[4][4];
@@ -1456,6 +1475,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // EPI_LOCAL: u = x A^T (waves of row half 0) and the gate logit x w_g
+  // (row half 1, w_g in every column) for the wave's 64 tokens
+  f32x4 eacc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) eacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   auto compute = [&](int buf) {
     const uint16_t* xs = Xs + buf * TILE;
@@ -1471,6 +1495,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = mfma16<DT>(af[i], bf[j], acc[i][j]);
+      if constexpr (kLoc) {
+        const u32x4 ef = *(const u32x4*)(Es + buf * ETILE + (wn == 0 ? lr : 16) * LR + kk + 8 * lg);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) eacc[i] = mfma16<DT>(af[i], ef, eacc[i]);
+      }
     }
   };
 
@@ -1503,19 +1532,61 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  if constexpr (EPI == EPI_READY) {
+  // EPI_LOCAL: v = alpha g(x) (.) u for the block's 128 tokens, as act-dtype
+  // high and low parts [128][32] in LDS (the stage buffers are free once
+  // every wave is past its last step)
+  constexpr int kVS = 32;
+  float* u_sh = (float*)smem;                                  // [128][17]
+  uint16_t* vh_sh = (uint16_t*)(smem + kGemmTM * 17 * 4);      // [128][kVS]
+  uint16_t* vl_sh = vh_sh + kGemmTM * kVS;
+  if constexpr (kLoc) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        const int t = wm * 64 + 16 * i + 4 * lg + e2;
+        if (wn == 0 && lr < a.r) u_sh[t * 17 + lr] = eacc[i][e2];
+        if (wn == 1 && lr == 0) u_sh[t * 17 + 16] = eacc[i][e2];
+      }
+    __syncthreads();
+    for (int idx = tid; idx < kGemmTM * kVS; idx += 256) {
+      const int t = idx / kVS, j = idx - t * kVS;
+      float val = 0.f;
+      if (j < a.r) {
+        float g = 1.f;
+        if (a.gate == GATE_SIGMOID) {
+          const float z = u_sh[t * 17 + 16] + a.b_g;
+          g = z >= 0.f ? 1.f / (1.f + __expf(-z)) : __expf(z) / (1.f + __expf(z));
+        }
+        val = a.alpha * g * u_sh[t * 17 + j];
+      }
+      const uint16_t hi = f2act<DT>(val);
+      vh_sh[idx] = hi;
+      vl_sh[idx] = f2act<DT>(val - act2f<DT>(hi));
+    }
+    __syncthreads();
+  }
+
+  if constexpr (EPI == EPI_READY || EPI == EPI_LOCAL) {
     // y += v_hi B^T + v_lo B^T over the rank (zero-padded to vstride)
     const int r = a.r;
     const bool bvec = (r & 7) == 0;
-    for (int kr = 0; kr < a.vstride; kr += 32) {
+    const int vstride = kLoc ? kVS : a.vstride;
+    for (int kr = 0; kr < vstride; kr += 32) {
       const int kk = kr + 8 * lg;
       u32x4 vhf[4], vlf[4], bfr[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int m = m0 + wm * 64 + 16 * i + lr;
+        const int t = wm * 64 + 16 * i + lr, m = m0 + t;
         const bool ok = m < M;
-        vhf[i] = ok ? ldg16(a.vh + (size_t)m * a.vstride + kk) : u32x4{0, 0, 0, 0};
-        vlf[i] = ok ? ldg16(a.vl + (size_t)m * a.vstride + kk) : u32x4{0, 0, 0, 0};
+        if constexpr (kLoc) {
+          vhf[i] = *(const u32x4*)(vh_sh + t * kVS + kk);
+          vlf[i] = *(const u32x4*)(vl_sh + t * kVS + kk);
+        } else {
+          vhf[i] = ok ? ldg16(a.vh + (size_t)m * a.vstride + kk) : u32x4{0, 0, 0, 0};
+          vlf[i] = ok ? ldg16(a.vl + (size_t)m * a.vstride + kk) : u32x4{0, 0, 0, 0};
+        }
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -1673,12 +1744,17 @@ hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st) {
   const int tm = (p.M + kGemmTM - 1) / kGemmTM, tn = (p.N + kGemmTN - 1) / kGemmTN;
   const unsigned grid = (unsigned)(tm * tn);
   if (grid == 0) return hipSuccess;
-  const size_t lds = (size_t)4 * kGemmTM * kGemmLdsRow * 2;
+  size_t lds = (size_t)4 * kGemmTM * kGemmLdsRow * 2;
+  if (epi == EPI_LOCAL) lds += (size_t)2 * kGemmEcRows * kGemmLdsRow * 2;
   SPEAR_DT_SWITCH(dt, {
     if (epi == EPI_NONE) {
       hipError_t err = allow_lds(k_gemm<DTC, EPI_NONE>, lds);
       if (err != hipSuccess) return err;
       hipLaunchKernelGGL((k_gemm<DTC, EPI_NONE>), dim3(grid), dim3(256), lds, st, p);
+    } else if (epi == EPI_LOCAL) {
+      hipError_t err = allow_lds(k_gemm<DTC, EPI_LOCAL>, lds);
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL((k_gemm<DTC, EPI_LOCAL>), dim3(grid), dim3(256), lds, st, p);
     } else {
       hipError_t err = allow_lds(k_gemm<DTC, EPI_READY>, lds);
       if (err != hipSuccess) return err;

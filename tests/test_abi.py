@@ -47,7 +47,9 @@ def _plan(**kw):
     (dict(group_size=64), -2), (dict(group_size=384), -2), (dict(group_size=96), -2),
     (dict(act_dtype=2), -3), (dict(rank=257), -2), (dict(rank=-1), -2),
     (dict(gate_kind=3), -6), (dict(gate_hidden=-1), -2), (dict(gate_hidden=2048), -2),
-    (dict(force_path=7), -6), (dict(force_path=sp.PATH_FUSED_MFMA), -6),
+    (dict(force_path=7), -6),
+    (dict(force_path=sp.PATH_FUSED_MFMA, rank=17), -6),
+    (dict(force_path=sp.PATH_FUSED_MFMA, gate_kind=sp.GATE_TANH_MLP), -6),
     (dict(force_path=sp.PATH_FUSED_GEMV, M=65), -6),
     (dict(force_path=sp.PATH_FUSED_LOCAL, M=33), -6),
     (dict(force_path=sp.PATH_FUSED_LOCAL, rank=17), -6),
@@ -81,6 +83,10 @@ def test_plan_phase_aware_dispatch():
         p = _plan(M=M)
         assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
     assert _plan(M=4, force_path=sp.PATH_FUSED_GEMV).path == sp.PATH_FUSED_GEMV
+    for M in (1, 64, 4096):
+        p = _plan(M=M, force_path=sp.PATH_FUSED_MFMA)
+        assert p.path == sp.PATH_FUSED_MFMA and p.num_launches == 1, M
+        assert p.grid == -(-M // 128) * (2048 // 128), M
     assert _plan(M=4, force_path=sp.PATH_FUSED_LOCAL).grid == _plan(M=4, with_ec=False).grid
     for M in (65, 512, 4096):
         p = _plan(M=M)

@@ -17,7 +17,7 @@ from gpu_util import assert_parity, gpu_y, log, scaled_ec, with_fields, zero_wei
 
 pytestmark = pytest.mark.gpu
 
-PATHS = {"auto": 0, "fused_gemv": 1, "chain": 3, "2k": 4, "fused_local": 5}
+PATHS = {"auto": 0, "fused_gemv": 1, "fused_mfma": 2, "chain": 3, "2k": 4, "fused_local": 5}
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -34,12 +34,19 @@ def _local_ok(L):
     return L.M <= 32 and L.gate_kind != S.GATE_TANH_MLP and L.rank <= 16
 
 
+def _mfma_ok(L):
+    """The fully fused GEMM: rank <= 16, sigmoid-linear or identity gate."""
+    return L.gate_kind != S.GATE_TANH_MLP and L.rank <= 16
+
+
 def _paths_for(M, L):
     out = []
     for name, p in PATHS.items():
         if name == "fused_gemv" and M > 64:
             continue
         if name == "fused_local" and not _local_ok(L):
+            continue
+        if name == "fused_mfma" and not _mfma_ok(L):
             continue
         out.append(p)
     return out
@@ -252,7 +259,7 @@ def test_streams_and_reuse():
 
 
 @pytest.mark.parametrize("M,path", [(4, 1), (4, 4), (4, 3), (200, 0), (200, 3), (33, 1), (4, 5),
-                                    (17, 5)])
+                                    (17, 5), (200, 2), (4, 2)])
 def test_graph_replay(M, path):
     """A captured call replayed several times, with new activations written
     between replays by eager work: every replay equals the eager call on the
