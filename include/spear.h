@@ -191,6 +191,13 @@ int32_t spear_set_wait_polls(int32_t polls);
  * only. */
 void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves);
 
+/* Tuning hook for the prefill GEMM's K-slices (1, 2, 4 or 8; each slice an
+ * even number of 64-wide K steps, else the planner and the calls return
+ * SPEAR_E_UNSUPPORTED), process-wide; 0 restores the planner's choice (more
+ * slices only while the tile grid alone leaves CUs idle). Not used by the
+ * fully fused GEMM. For measurement sweeps and tests only. */
+void spear_set_gemm_slices(int32_t k_slices);
+
 /* Static text for a status code. */
 const char* spear_status_string(spear_status_t status);
 

@@ -18,7 +18,7 @@ namespace {
 std::atomic<int32_t> g_wait_polls{1 << 16};
 // tuning override of the GEMV shape (0 = automatic): row tiles per block,
 // K-slices per row group, waves per block
-std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0};
+std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0};
 
 // Token counts at or below this run the 4-bit product as a split-K GEMV; above
 // it the LDS-tiled MFMA GEMM. The same bound separates decode (fully fused
@@ -44,9 +44,10 @@ struct Resolved {
   bool ec, gemv;
   int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
   int MT, RT, NW, nrg, S, ips, iw;            // GEMV shape
+  int Sg;                                     // GEMM K-slices
   int ntb, P, eips, PG, tpg, ec_mode, ec_ipp, ec_block, n_prod;  // EC shape
   int xlds, xstride, bpre, lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz, lds_a;
-  size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart, off_eupart;
+  size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart, off_eupart, off_gpart;
   int npub, direct;
   size_t lds_gemv, lds_prod, lds_gate;
 };
@@ -173,7 +174,21 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     z.plan.tile_m = 16 * z.MT;
     z.plan.tile_n = 16 * z.RT;
   } else {
-    z.plan.split_k = 1;
+    // prefill GEMM: K-slices (2, 4 or 8, each an even number of 64-wide
+    // steps, at least four) while the tile grid alone fills less than the
+    // 256 CUs; not for the fully fused variant, whose epilogue needs all of K
+    const int64_t tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN);
+    const int steps = (int)(K / kGemmTK);
+    z.Sg = 1;
+    if (!fmfma)
+      for (int S = 2; S <= 8; S *= 2)
+        if (tiles * z.Sg < 256 && steps % (2 * S) == 0 && steps / S >= 4) z.Sg = S;
+    if (g_ov_gs.load() > 0 && !fmfma) {
+      const int S = g_ov_gs.load();
+      if (steps % (2 * S) != 0) return SPEAR_E_UNSUPPORTED;
+      z.Sg = S;
+    }
+    z.plan.split_k = z.Sg;
     z.plan.tile_m = kGemmTM;
     z.plan.tile_n = kGemmTN;
   }
@@ -276,7 +291,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   z.plan.ec_splits = z.ec ? z.P : 0;
 
   // launches and grid
-  const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN));
+  const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN)) * z.Sg;
   if (!z.ec || local || fmfma) {
     z.plan.num_launches = 1;
     z.plan.grid = grid4;
@@ -330,6 +345,11 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   if (z.gemv && z.S > 1) {
     if (z.nrg > kMaxRowCounters) return SPEAR_E_SHAPE;
     z.off_ypart = take((size_t)z.S * M * N * 4);
+  }
+  if (!z.gemv && z.Sg > 1) {
+    const int64_t tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN);
+    if (tiles > kMaxRowCounters) return SPEAR_E_SHAPE;
+    z.off_gpart = take((size_t)z.Sg * tiles * kGemmTM * kGemmTN * 4);
   }
   z.plan.workspace_bytes = off;
   return SPEAR_OK;
@@ -458,6 +478,11 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
                      void* y, const spear_ec_t* ec, char* ws) {
   GemmParams g;
   std::memset(&g, 0, sizeof(g));
+  g.S = std::max(1, z.Sg);
+  if (ws && z.Sg > 1) {
+    g.ypart = (float*)(ws + z.off_gpart);
+    g.ctr = (uint32_t*)(ws + kCtrRows);
+  }
   g.qw = w->qweight;
   g.sc = w->scales;
   g.zr = w->zeros;
@@ -495,7 +520,7 @@ spear_status_t run_w4(const spear_problem_t* p, const Resolved& z, const void* x
     return hip_status(
         launch_gemv(z.dt, z.MT, z.RT, EPI_NONE, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, st));
   }
-  GemmParams g = make_gemm(p, z, x, w, y, nullptr, nullptr);
+  GemmParams g = make_gemm(p, z, x, w, y, nullptr, ws);
   return hip_status(launch_gemm(z.dt, EPI_NONE, g, st));
 }
 
@@ -625,6 +650,8 @@ void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves) {
   g_ov_s = k_slices > 0 ? k_slices : 0;
   g_ov_nw = waves > 0 ? waves : 0;
 }
+
+void spear_set_gemm_slices(int32_t k_slices) { g_ov_gs = k_slices > 0 ? k_slices : 0; }
 
 const char* spear_status_string(spear_status_t s) {
   switch (s) {

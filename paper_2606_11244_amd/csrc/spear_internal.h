@@ -143,6 +143,11 @@ struct GemmParams {
   const uint16_t* vh;     // [M][vstride]
   const uint16_t* vl;
   int M, N, K, G, ngroups, r, vstride;
+  // split-K over S K-slices (small tile grids; not with EPI_LOCAL): the
+  // slices' fp32 tiles [S][tiles][128 x 128] (lane-major), tile counters
+  int S;
+  float* ypart;
+  uint32_t* ctr;
   // EPI_LOCAL (fully fused prefill): the projection's inputs
   const uint16_t* A;      // [r][K], r <= 16
   const uint16_t* wg;     // [K] (sigmoid gate) or null

@@ -165,6 +165,13 @@ __device__ __forceinline__ uint32_t ld_agent_u32(const uint32_t* p) {
   return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // All of this thread's memory operations have completed; then the block meets.
+// 16-byte agent-scope (sc1) buffer store and load
+__device__ __forceinline__ void bst128c(rsrc_t r, uint32_t off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, 0x10);
+}
+__device__ __forceinline__ f32x4 bld128cf(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0x10));
+}
 __device__ __forceinline__ void complete_and_sync() {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -1378,9 +1385,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   // its own L2: give XCD x a contiguous band of token tiles (or, failing
   // that, of row tiles) so that the tiles its workgroups share are fetched
   // into its L2 once, instead of every activation tile once per XCD.
+  // split-K: workgroup b of slice s is blockIdx.x = s * tiles + b
+  const int T = tiles_m * tiles_n;
+  const int ks = (int)blockIdx.x / T, tb = (int)blockIdx.x - ks * T;
   int mt_i, nt_i;
   {
-    const int b = blockIdx.x, x = b & 7, j = b >> 3;
+    const int b = tb, x = b & 7, j = b >> 3;
     if ((tiles_m & 7) == 0) {
       const int pm = tiles_m >> 3;
       mt_i = x * pm + j % pm;
@@ -1396,7 +1406,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   }
   const int m0 = mt_i * kGemmTM;
   const int n0 = nt_i * kGemmTN;
-  const int KT = K / kGemmTK;
+  const int KT = K / kGemmTK / a.S;  // steps of this slice (an even count)
+  const int kbase = ks * KT;
 
   // per-thread global load assignments (bounds-checked buffer loads)
   const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
@@ -1438,7 +1449,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   };
   Stage g0, g1;
   auto gload = [&](Stage& st, int kt) {
-    const uint32_t k0 = (uint32_t)kt * kGemmTK;
+    const uint32_t k0 = (uint32_t)(kbase + kt) * kGemmTK;
 #pragma unroll
     for (int i = 0; i < 4; ++i) st.x[i] = bld128(rx, xoff[i] + k0 * 2);
     st.w = bld128(rq, woff + k0 / 2);
@@ -1530,6 +1541,53 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     __builtin_amdgcn_sched_barrier(0);
     compute(1);
     __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // split-K: every slice publishes its tile (lane-major f32x4); the last
+  // to arrive sums the slices in slice order (its own from registers) and
+  // runs the epilogue
+  if (a.S > 1) {
+    __shared__ int s_last;
+    const rsrc_t rp = make_rsrc(a.ypart, (uint32_t)((size_t)a.S * T * kGemmTM * kGemmTN * 4));
+    auto off = [&](int q, int i, int j) {
+      return (uint32_t)((((size_t)q * T + tb) * kGemmTM * kGemmTN) * 4 +
+                        ((size_t)((wave * 4 + i) * 4 + j) * 64 + lane) * 16);
+    };
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bst128c(rp, off(ks, i, j), acc[i][j]);
+    complete_and_sync();
+    if (tid == 0) s_last = arrive_last(a.ctr + tb, (uint32_t)a.S) ? 1 : 0;
+    __syncthreads();
+    if (!s_last) return;
+    f32x4 tot[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < a.S; ++q) {
+      if (q == ks) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) tot[i][j] += acc[i][j];
+      } else {
+        f32x4 pv[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) pv[i][j] = bld128cf(rp, off(q, i, j));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) tot[i][j] += pv[i][j];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = tot[i][j];
   }
 
   // EPI_LOCAL: v = alpha g(x) (.) u for the block's 128 tokens, as act-dtype
@@ -1730,6 +1788,9 @@ bool gemv_shape_supported(int MT, int RT) {
 
 hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, int block,
                        size_t lds, hipStream_t st) {
+  // split-K needs its partial sums and row-group counters (workspace)
+  if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.rb_ctr || (epi == EPI_LOCAL && !p.eupart))))
+    return hipErrorInvalidValue;
   if (grid == 0) return hipSuccess;
 #define SPEAR_GEMV_CASE(mt, rt)                                                     \
   if (MT == mt && RT == rt)                                                         \
@@ -1741,8 +1802,10 @@ hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int
 }
 
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st) {
+  // split-K needs its partial tiles and tile counters (workspace)
+  if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.ctr || epi == EPI_LOCAL))) return hipErrorInvalidValue;
   const int tm = (p.M + kGemmTM - 1) / kGemmTM, tn = (p.N + kGemmTN - 1) / kGemmTN;
-  const unsigned grid = (unsigned)(tm * tn);
+  const unsigned grid = (unsigned)(tm * tn * p.S);
   if (grid == 0) return hipSuccess;
   size_t lds = (size_t)4 * kGemmTM * kGemmLdsRow * 2;
   if (epi == EPI_LOCAL) lds += (size_t)2 * kGemmEcRows * kGemmLdsRow * 2;

@@ -31,7 +31,8 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
           -7: "SPEAR_E_HIP", -8: "SPEAR_E_ALIAS"}
 
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
-            "spear_set_wait_polls", "spear_set_gemv_shape", "spear_status_string", "spear_version")
+            "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
+            "spear_status_string", "spear_version")
 
 
 class Problem(ctypes.Structure):
@@ -84,6 +85,8 @@ def _load():
     lib.spear_set_wait_polls.argtypes = [ctypes.c_int32]
     lib.spear_set_gemv_shape.argtypes = [ctypes.c_int32] * 3
     lib.spear_set_gemv_shape.restype = None
+    lib.spear_set_gemm_slices.argtypes = [ctypes.c_int32]
+    lib.spear_set_gemm_slices.restype = None
     lib.spear_status_string.argtypes = [ctypes.c_int32]
     lib.spear_status_string.restype = ctypes.c_char_p
     lib.spear_version.restype = ctypes.c_char_p
@@ -175,6 +178,11 @@ def set_wait_polls(polls: int) -> int:
 def set_gemv_shape(row_tiles=0, k_slices=0, waves=0) -> None:
     """Tuning override of the decode GEMV launch shape (0 = automatic)."""
     LIB.spear_set_gemv_shape(int(row_tiles), int(k_slices), int(waves))
+
+
+def set_gemm_slices(k_slices=0) -> None:
+    """Tuning override of the prefill GEMM's K-slices (0 = automatic)."""
+    LIB.spear_set_gemm_slices(int(k_slices))
 
 
 def version() -> str:

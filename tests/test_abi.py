@@ -96,6 +96,22 @@ def test_plan_phase_aware_dispatch():
     assert _plan(M=4, force_path=sp.PATH_UNFUSED_2K).num_launches == 2
 
 
+def test_gemm_split_k_plan_and_workspace():
+    """Small tile grids split K; the workspace holds every slice's fp32 tile
+    (the 4-bit-only call included), and a missing workspace is rejected on
+    the host."""
+    for ec in (True, False):
+        p = _plan(M=512, N=1024, K=8192, rank=16, with_ec=ec)
+        tiles = 4 * 8
+        assert p.split_k == 8 and p.grid == tiles * 8
+        assert p.workspace_bytes >= 8 * tiles * 128 * 128 * 4
+    assert _plan(M=4096, N=2048, K=2048).split_k == 1   # 512 tiles: no split
+    prob = sp.problem(512, 1024, 8192, 128, sp.F16, 0)
+    w = sp.W4(ADDR["q"], ADDR["s"], ADDR["z"])
+    assert sp.LIB.spear_w4_linear(ctypes.byref(prob), ADDR["x"], ctypes.byref(w), ADDR["y"],
+                                  None, 0, None) == -5
+
+
 def test_plan_is_deterministic_and_sized():
     a, b = _plan(M=16).as_dict(), _plan(M=16).as_dict()
     assert a == b
