@@ -1,0 +1,137 @@
+"""Dispatch crossover measurement: every execution path of the W4+EC layer,
+timed per module shape and token count, next to the path the planner picks.
+
+For each (configuration, module, M) the layer's weights are copied enough
+times to exceed the last-level caches (up to 16 copies), each path's calls
+over the copies are captured once as a HIP graph and replayed, and the mean
+time per call is reported. The markdown written to --out lists, per row, the
+4-bit-only time, each EC path's time, the fastest EC path and the planner's
+AUTO choice.
+
+Usage (on a GPU):
+  python -m paper_2606_11244_amd.crossover --out profiles/dispatch_crossover.md
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import sys
+
+PATHS = [("fused_local", 5), ("fused_gemv", 1), ("fused_mfma", 2), ("unfused_2k", 4),
+         ("unfused_chain", 3)]
+
+# (configuration id, module, token counts)
+DEFAULT_CASES = [
+    (1, "q", [1, 4, 16, 32, 64]), (1, "k", [1, 16, 64]), (1, "gate", [1, 16, 32, 64]),
+    (1, "down", [1, 16, 64]),
+    (2, "q", [128, 256, 512, 1024, 2048, 4096]), (2, "k", [128, 512, 4096]),
+    (2, "gate", [128, 512, 2048, 4096]), (2, "down", [512, 4096]),
+    (3, "q", [1, 8, 32, 128, 512]), (3, "down", [1, 8, 32, 512]),
+    (4, "k", [1, 16, 64, 512]), (4, "gate", [1, 16, 64]), (4, "down", [1, 16, 64]),
+]
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", default="profiles/dispatch_crossover.md")
+    ap.add_argument("--reps", type=int, default=10)
+    args = ap.parse_args(argv)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_11244_amd import spear as sp
+    from paper_2606_11244_amd import synth as S
+
+    torch.cuda.set_device(0)
+
+    def timed(fn, copies, reps):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for c in range(copies):
+                fn(c)
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for c in range(copies):
+                fn(c)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps / copies  # us per call
+
+    rows = []
+    for cid, mod, Ms in DEFAULT_CASES:
+        for M in Ms:
+            L = S.config_layer(cid, mod, M, seed=0)
+            base = sp.DeviceLayer(L)
+            wbytes = L.N * L.K // 2
+            copies = int(min(16, max(2, math.ceil(600e6 / wbytes))))
+            devs = []
+            for _ in range(copies):
+                d = sp.DeviceLayer.__new__(sp.DeviceLayer)
+                d.__dict__.update(base.__dict__)
+                d.qweight, d.scales, d.zeros = (base.qweight.clone(), base.scales.clone(),
+                                                base.zeros.clone())
+                devs.append(d)
+            row = {"config": cid, "module": mod, "M": M, "N": L.N, "K": L.K, "rank": L.rank}
+            p4 = base.problem()
+            ws_size = sp.dispatch_plan(p4, with_ec=False).workspace_bytes
+            plans = {}
+            for name, code in PATHS:
+                try:
+                    plans[name] = sp.dispatch_plan(base.problem(force_path=code))
+                    ws_size = max(ws_size, plans[name].workspace_bytes)
+                except sp.SpearError:
+                    pass
+            auto = sp.dispatch_plan(base.problem())
+            ws = torch.zeros(max(ws_size, auto.workspace_bytes, 256), dtype=torch.uint8,
+                             device="cuda")
+            row["w4_us"] = round(timed(lambda c: devs[c].run_w4(p4, ws), copies, args.reps), 2)
+            for name, code in PATHS:
+                if name not in plans:
+                    continue
+                pr = base.problem(force_path=code)
+                row[name + "_us"] = round(timed(lambda c: devs[c].run_ec(pr, ws), copies,
+                                                args.reps), 2)
+            row["auto"] = sp.PATH_NAMES[auto.path]
+            ec_times = {n: row[n + "_us"] for n, _ in PATHS if n + "_us" in row}
+            row["best"] = min(ec_times, key=ec_times.get)
+            print(json.dumps(row), flush=True)
+            rows.append(row)
+            del devs, base
+            torch.cuda.empty_cache()
+
+    names = [n for n, _ in PATHS]
+    lines = ["# Dispatch crossover: W4+EC paths by token count", "",
+             "Command (from the repository root): `python -m paper_2606_11244_amd.crossover "
+             f"--out {args.out}`", "",
+             "Mean time per call in microseconds (graph-replayed over rotated weight copies; "
+             "synthetic layers of the named configurations, seed 0). `-` = path not available "
+             "for the shape. EC overhead = fastest EC path / 4-bit-only - 1.", "",
+             "| config | module | N | K | r | M | W4 only | " + " | ".join(names) +
+             " | fastest | AUTO | EC overhead |",
+             "|---" * (9 + len(names) + 1) + "|"]
+    for r in rows:
+        cells = [str(r.get(n + "_us", "-")) for n in names]
+        best_t = r[r["best"] + "_us"]
+        auto_mark = r["auto"] if r["auto"] == r["best"] else r["auto"] + " (*)"
+        lines.append(f"| {r['config']} | {r['module']} | {r['N']} | {r['K']} | {r['rank']} | "
+                     f"{r['M']} | {r['w4_us']} | " + " | ".join(cells) +
+                     f" | {r['best']} | {auto_mark} | {best_t / r['w4_us'] - 1:.1%} |")
+    lines += ["", "(*) AUTO differs from the fastest measured path.", ""]
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines))
+    print(f"wrote {args.out}", file=sys.stderr)
+
+
+if __name__ == "__main__":
+    main()

@@ -25,6 +25,7 @@ std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0};
 // EC) from prefill (semi-fused EC pre-kernel) under SPEAR_PATH_AUTO.
 constexpr int64_t kGemvMaxM = 64;
 constexpr int64_t kLocalMaxM = 32;   // local EC variant: at most two token tiles
+constexpr size_t kLocalRestageMax = 24u << 20;  // local EC: A and w_g staged per call
 // Largest staged slice of x in a GEMV block's LDS (16 tokens x 2048 K fit).
 constexpr size_t kXLdsMax = 66 * 1024;
 // Fused EC: the consumers gather the K-slices' partial sums themselves when
@@ -124,7 +125,11 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     const int ips = gemv_ips(z.IT, (int)cdiv(N, 16 * RT), nw);
     const size_t abytes = (size_t)17 * (ips * kIterK + 8) * 2;
     const size_t partials = (size_t)nw * (RT + kLocalTiles) * MT * 1024;
-    local_ok = abytes <= kLocalALds && abytes + partials + 32768 <= kMaxLds;
+    // every row group stages all of A and w_g once: keep that L2 traffic
+    // bounded (wide layers at two token tiles have many row groups)
+    const size_t restaged = (size_t)cdiv(N, 16 * RT) * 17 * K * 2;
+    local_ok = abytes <= kLocalALds && abytes + partials + 32768 <= kMaxLds &&
+               restaged <= kLocalRestageMax;
   }
   // the fully fused GEMM: the projection rides on the GEMM's activation
   // tiles (one 16-row tile of A plus w_g), the gate and v B^T in its epilogue
@@ -232,13 +237,26 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
       }
       z.lds_prod = ec_block_lds(nw, z.R1p, z.h, z.r);
     } else {
-      // eight waves of two iterations per pass: K = 2048 is one pass
+      // eight-wave producers; while the token tiles alone leave CUs idle
+      // (fewer than 256 workgroups), the rows of [A; w_g] are split into
+      // groups of two 16-row tiles and K into slices (at least one pass of
+      // one iteration per wave each), combined by the token tile's last
+      // producer
       z.ec_block = 512;
       z.ec_ipp = 2;
       z.eips = z.IT;
       z.P = 1;
       z.PG = 1;
       z.tpg = RTe;
+      if (z.ntb < 256 && z.ntb <= kMaxEcCounters) {
+        z.PG = (int)cdiv(RTe, kEcTiles);
+        z.tpg = kEcTiles;
+        int P = 1;
+        while ((int64_t)z.ntb * P * z.PG < 256 && cdiv(z.IT, 2 * P) >= 8) P *= 2;
+        z.eips = (int)cdiv(z.IT, P);
+        z.P = (int)cdiv(z.IT, z.eips);
+        if (z.P > 1) z.ec_ipp = 1;
+      }
       z.ec_mode = path == SPEAR_PATH_UNFUSED_CHAIN ? EC_RAW : EC_LAST;
       z.lds_prod = ec_block_lds(8, z.R1p, z.h, z.r);
     }

@@ -43,8 +43,8 @@ constexpr size_t kCtrGen = 0;          // fused path: kGenClasses 64-bit launch
 constexpr int kGenClasses = 64;        // counters, kGenStride apart
 constexpr size_t kGenStride = 256;
 constexpr size_t kCtrEc = 16384;       // EC-slice counters, one per token tile
-constexpr int kMaxEcCounters = 64;
-constexpr size_t kCtrRows = 16896;     // split-K counters, one per row group
+constexpr int kMaxEcCounters = 4096;
+constexpr size_t kCtrRows = 32768;     // split-K counters, one per row group / tile
 constexpr size_t kCtrReady = 98304;    // fused path: kVCopies 64-bit ready
 constexpr size_t kReadyStride = 4096;  // counters, 4 KB apart (memory channels)
 constexpr int kMaxRowCounters = (int)((kCtrReady - kCtrRows) / 4);
