@@ -232,6 +232,9 @@ __global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ qw
 __device__ __forceinline__ uint32_t bld32c(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0x10);
 }
+__device__ __forceinline__ u32x2 bld64(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+}
 __device__ __forceinline__ u32x2 bld64c(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0x10);
 }
@@ -1060,21 +1063,55 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
       }
     }
   };
+  // eight groups per 16-byte scale load and 8-byte zero load when the
+  // block's group range is 8-aligned (2- and 1-byte loads per entry would be
+  // a third of the block's load instructions for a few percent of its bytes)
+  const bool sz8 = (a.ngroups & 7) == 0 && (g_lo & 7) == 0 && (ngb & 7) == 0;
+  const int c8 = ngb >> 3, nsz8 = RB * c8;
+  auto sz8_issue = [&](int i, u32x4& s8, u32x2& z8) {
+    const int row = i / c8, q = i - row * c8;
+    const bool ok = i < nsz8 && n0 + row < N;
+    const uint32_t eo = (uint32_t)(n0 + row) * a.ngroups + g_lo + 8 * q;
+    s8 = bld128(rsc, ok ? eo * 2 : kOOB);
+    z8 = bld64(rz, ok ? eo : kOOB);
+  };
+  auto sz8_store = [&](int i, const u32x4& s8, const u32x2& z8) {
+    if (i < nsz8) {
+      const int row = i / c8, q = i - row * c8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t sv = (s8[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+        const uint32_t zv = (z8[e >> 2] >> (8 * (e & 3))) & 0xFFu;
+        szs[row * ngs + 8 * q + e] = sv | (zv << 16);
+      }
+    }
+  };
   {
     const int step = 4 * (int)blockDim.x;
     u32x4 c4[4];
     uint32_t sv[4], zv[4];
+    u32x4 s8;
+    u32x2 z8;
     x_issue(tid, c4);
-    sz_issue(tid, sv, zv);
+    if (sz8) sz8_issue(tid, s8, z8);
+    else sz_issue(tid, sv, zv);
     x_store(tid, c4);
-    sz_store(tid, sv, zv);
+    if (sz8) sz8_store(tid, s8, z8);
+    else sz_store(tid, sv, zv);
     for (int base = tid + step; base < nch; base += step) {
       x_issue(base, c4);
       x_store(base, c4);
     }
-    for (int i0 = tid + step; i0 < nsz; i0 += step) {
-      sz_issue(i0, sv, zv);
-      sz_store(i0, sv, zv);
+    if (sz8) {
+      for (int i = tid + (int)blockDim.x; i < nsz8; i += blockDim.x) {
+        sz8_issue(i, s8, z8);
+        sz8_store(i, s8, z8);
+      }
+    } else {
+      for (int i0 = tid + step; i0 < nsz; i0 += step) {
+        sz_issue(i0, sv, zv);
+        sz_store(i0, sv, zv);
+      }
     }
     if constexpr (kLoc) {
       // A: two rounds of four chunks per thread in flight; w_g: one chunk
