@@ -10,6 +10,12 @@ AUTO choice.
 
 Usage (on a GPU):
   python -m paper_2606_11244_amd.crossover --out profiles/dispatch_crossover.md
+  python -m paper_2606_11244_amd.crossover --lut profiles/latency_lut_llama1b.json
+
+With --lut it instead measures, for each module of the Llama-3.2-1B-shaped
+configuration, the 4-bit-only call and the W4+EC call on the path AUTO picks
+over a grid of token counts: the latency tables l_W4(M), l_EC(M) of the
+SLO-constrained chunk scheduler (section 4.3, include/spear_sched.h).
 """
 from __future__ import annotations
 
@@ -32,9 +38,13 @@ DEFAULT_CASES = [
 ]
 
 
+LUT_M = [1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096]
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default="profiles/dispatch_crossover.md")
+    ap.add_argument("--lut", default=None, help="write latency tables (JSON) instead")
     ap.add_argument("--reps", type=int, default=10)
     args = ap.parse_args(argv)
 
@@ -67,6 +77,51 @@ def main(argv=None):
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / reps / copies  # us per call
+
+    def weights_copies(base, L):
+        copies = int(min(16, max(2, math.ceil(600e6 / (L.N * L.K // 2)))))
+        devs = []
+        for _ in range(copies):
+            d = sp.DeviceLayer.__new__(sp.DeviceLayer)
+            d.__dict__.update(base.__dict__)
+            d.qweight, d.scales, d.zeros = (base.qweight.clone(), base.scales.clone(),
+                                            base.zeros.clone())
+            devs.append(d)
+        return devs
+
+    if args.lut:
+        # one table per module shape of the 1B configuration: prefill shapes
+        # (config 2, outlier activations) above 64 tokens, decode shapes below
+        tables = {}
+        for mod in S.MODULES:
+            Ms, w4, ec, paths = [], [], [], []
+            for M in LUT_M:
+                L = S.config_layer(2 if M > 64 else 1, mod, M, seed=0)
+                base = sp.DeviceLayer(L)
+                devs = weights_copies(base, L)
+                p4, pe = base.problem(), base.problem()
+                ws = torch.zeros(max(sp.dispatch_plan(p4, with_ec=False).workspace_bytes,
+                                     sp.dispatch_plan(pe).workspace_bytes, 256),
+                                 dtype=torch.uint8, device="cuda")
+                Ms.append(M)
+                w4.append(round(timed(lambda c: devs[c].run_w4(p4, ws), len(devs), args.reps), 3))
+                ec.append(round(timed(lambda c: devs[c].run_ec(pe, ws), len(devs), args.reps), 3))
+                paths.append(sp.PATH_NAMES[sp.dispatch_plan(pe).path])
+                print(json.dumps({"module": mod, "M": M, "w4_us": w4[-1], "ec_us": ec[-1],
+                                  "path": paths[-1]}), flush=True)
+                del devs, base
+                torch.cuda.empty_cache()
+            tables[mod] = {"N": L.N, "K": L.K, "rank": L.rank, "M": Ms, "w4_us": w4,
+                           "ec_us": ec, "ec_path": paths}
+        out = {"workload": "Llama-3.2-1B-shaped W4+EC linear modules (group 128, rank 16, "
+                           "sigmoid-linear gate, fp16); synthetic layers, seed 0",
+               "command": f"python -m paper_2606_11244_amd.crossover --lut {args.lut}",
+               "unit": "us per call, graph-replayed over rotated weight copies",
+               "modules": tables}
+        with open(args.lut, "w") as f:
+            json.dump(out, f, indent=1)
+        print(f"wrote {args.lut}", file=sys.stderr)
+        return
 
     rows = []
     for cid, mod, Ms in DEFAULT_CASES:

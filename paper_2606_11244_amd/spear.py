@@ -32,7 +32,7 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
 
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
             "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
-            "spear_status_string", "spear_version")
+            "spear_status_string", "spear_version", "spear_sched_latency", "spear_sched_chunk")
 
 
 class Problem(ctypes.Structure):
@@ -65,6 +65,18 @@ class Plan(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
 
 
+class Lut(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("M", ctypes.POINTER(ctypes.c_int64)),
+                ("lat_w4", ctypes.POINTER(ctypes.c_double)),
+                ("lat_ec", ctypes.POINTER(ctypes.c_double))]
+
+
+class ModelLat(ctypes.Structure):
+    _fields_ = [("layers", ctypes.c_int32), ("modules", ctypes.c_int32),
+                ("luts", ctypes.POINTER(Lut)), ("selection", ctypes.POINTER(ctypes.c_uint8)),
+                ("extra", ctypes.POINTER(Lut))]
+
+
 class SpearError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -87,6 +99,11 @@ def _load():
     lib.spear_set_gemv_shape.restype = None
     lib.spear_set_gemm_slices.argtypes = [ctypes.c_int32]
     lib.spear_set_gemm_slices.restype = None
+    lib.spear_sched_latency.argtypes = [P(ModelLat), ctypes.c_int64, P(ctypes.c_double)]
+    lib.spear_sched_chunk.argtypes = [P(ModelLat), ctypes.c_int64, ctypes.c_double,
+                                      ctypes.c_int64, ctypes.c_int64, P(ctypes.c_int64)]
+    lib.spear_sched_latency.restype = ctypes.c_int32
+    lib.spear_sched_chunk.restype = ctypes.c_int32
     lib.spear_status_string.argtypes = [ctypes.c_int32]
     lib.spear_status_string.restype = ctypes.c_char_p
     lib.spear_version.restype = ctypes.c_char_p
@@ -183,6 +200,55 @@ def set_gemv_shape(row_tiles=0, k_slices=0, waves=0) -> None:
 def set_gemm_slices(k_slices=0) -> None:
     """Tuning override of the prefill GEMM's K-slices (0 = automatic)."""
     LIB.spear_set_gemm_slices(int(k_slices))
+
+
+class LatencyModel:
+    """Latency tables and an EC selection for the scheduler of
+    include/spear_sched.h. `luts` is a list (one per module type) of
+    (M list, 4-bit latency list, W4+EC latency list) in microseconds;
+    `selection` a layers x modules list of 0/1; `extra` an optional
+    (M list, latency list) of the other per-layer work."""
+
+    def __init__(self, luts, selection, extra=None):
+        self._keep = []
+        arr = (Lut * len(luts))()
+        for j, (M, lw, le) in enumerate(luts):
+            arr[j] = self._lut(M, lw, le)
+        layers, modules = len(selection), len(luts)
+        flat = (ctypes.c_uint8 * (layers * modules))(*[int(bool(v)) for row in selection for v in row])
+        self._keep += [arr, flat]
+        ex = None
+        if extra is not None:
+            ex = ctypes.pointer(self._lut(extra[0], extra[1], extra[1]))
+            self._keep.append(ex)
+        self.c = ModelLat(layers, modules, arr, flat, ex)
+
+    def _lut(self, M, lw, le):
+        n = len(M)
+        a = (ctypes.c_int64 * n)(*[int(v) for v in M])
+        b = (ctypes.c_double * n)(*[float(v) for v in lw])
+        c = (ctypes.c_double * n)(*[float(v) for v in le])
+        self._keep += [a, b, c]
+        return Lut(n, a, b, c)
+
+
+def sched_latency(model: LatencyModel, m: int) -> float:
+    """Estimated iteration latency (us) at m tokens (SPEAR section 4.3)."""
+    out = ctypes.c_double()
+    st = LIB.spear_sched_latency(ctypes.byref(model.c), int(m), ctypes.byref(out))
+    if st != 0:
+        raise SpearError(st, "spear_sched_latency")
+    return out.value
+
+
+def sched_chunk(model: LatencyModel, d: int, t_slo_us: float, c_min: int, c_max: int) -> int:
+    """Largest prefill chunk c in [c_min, c_max] with T(d) + T(c) <= t_slo_us (0: none)."""
+    out = ctypes.c_int64()
+    st = LIB.spear_sched_chunk(ctypes.byref(model.c), int(d), float(t_slo_us), int(c_min),
+                               int(c_max), ctypes.byref(out))
+    if st != 0:
+        raise SpearError(st, "spear_sched_chunk")
+    return out.value
 
 
 def version() -> str:
