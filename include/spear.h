@@ -84,16 +84,21 @@ enum {
                                     computes A x and the gate, and the epilogue
                                     adds B (g (.) A x). Decode, M <= 64.       */
   SPEAR_PATH_FUSED_MFMA = 2,     /* one kernel: the 4-bit MFMA GEMM also projects
-                                    its activation tiles on A and w_g, and its
-                                    epilogue applies the gate and adds
-                                    B (g (.) A x); rank <= 16, sigmoid-linear or
-                                    identity gate (else SPEAR_E_UNSUPPORTED)   */
+                                    its activation tiles on A and w_g (split
+                                    over K with the product when the tile grid
+                                    is small), and its epilogue applies the
+                                    gate and adds B (g (.) A x); rank <= 16,
+                                    sigmoid-linear or identity gate (else
+                                    SPEAR_E_UNSUPPORTED). AUTO picks it for
+                                    M > 64 while the grid has at most 256
+                                    128 x 128 tiles                            */
   SPEAR_PATH_UNFUSED_CHAIN = 3,  /* naive split: 4-bit GEMM, then separate
                                     projection, gate and reprojection+accumulate
                                     kernels (the baseline of section 4.1)      */
   SPEAR_PATH_UNFUSED_2K = 4,     /* semi-fused: EC pre-kernel (A x, gate) then
                                     the 4-bit GEMM/GEMV whose epilogue adds
-                                    B (g (.) A x)                              */
+                                    B (g (.) A x). AUTO's choice for M > 64
+                                    otherwise                                  */
   SPEAR_PATH_FUSED_LOCAL = 5     /* one kernel: split-K 4-bit GEMV whose waves
                                     also project x on [A; w_g] over their own K
                                     chunks (no EC workgroups, no wait on other
@@ -194,8 +199,8 @@ void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves);
 /* Tuning hook for the prefill GEMM's K-slices (1, 2, 4 or 8; each slice an
  * even number of 64-wide K steps, else the planner and the calls return
  * SPEAR_E_UNSUPPORTED), process-wide; 0 restores the planner's choice (more
- * slices only while the tile grid alone leaves CUs idle). Not used by the
- * fully fused GEMM. For measurement sweeps and tests only. */
+ * slices only while the tile grid alone leaves CUs idle). For measurement
+ * sweeps and tests only. */
 void spear_set_gemm_slices(int32_t k_slices);
 
 /* Static text for a status code. */

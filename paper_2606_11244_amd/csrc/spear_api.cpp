@@ -48,7 +48,8 @@ struct Resolved {
   int Sg;                                     // GEMM K-slices
   int ntb, P, eips, PG, tpg, ec_mode, ec_ipp, ec_block, n_prod;  // EC shape
   int xlds, xstride, bpre, lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz, lds_a;
-  size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart, off_eupart, off_gpart;
+  size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart, off_eupart, off_gpart,
+      off_epart;
   int npub, direct;
   size_t lds_gemv, lds_prod, lds_gate;
 };
@@ -137,8 +138,12 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   if (z.ec && path == SPEAR_PATH_FUSED_MFMA && !mfma_ok) return SPEAR_E_UNSUPPORTED;
   if (path == SPEAR_PATH_FUSED_GEMV && M > kGemvMaxM) return SPEAR_E_UNSUPPORTED;
   if (z.ec && path == SPEAR_PATH_FUSED_LOCAL && !local_ok) return SPEAR_E_UNSUPPORTED;
+  // prefill: the fully fused GEMM while its tile grid is small (at most
+  // one 128 x 128 tile per CU, split over K): the separate projection
+  // kernel's fixed cost then outweighs the projection the N-tiles repeat
+  const bool few_tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN) <= 256;
   if (path == SPEAR_PATH_AUTO || !z.ec)
-    path = M > kGemvMaxM ? SPEAR_PATH_UNFUSED_2K
+    path = M > kGemvMaxM ? (mfma_ok && few_tiles ? SPEAR_PATH_FUSED_MFMA : SPEAR_PATH_UNFUSED_2K)
            : local_ok    ? SPEAR_PATH_FUSED_LOCAL
                          : SPEAR_PATH_FUSED_GEMV;
   if (!with_ec) path = (M <= kGemvMaxM) ? SPEAR_PATH_FUSED_GEMV : SPEAR_PATH_UNFUSED_2K;
@@ -181,14 +186,13 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   } else {
     // prefill GEMM: K-slices (2, 4 or 8, each an even number of 64-wide
     // steps, at least four) while the tile grid alone fills less than the
-    // 256 CUs; not for the fully fused variant, whose epilogue needs all of K
+    // 256 CUs; the fully fused variant splits its EC projection the same way
     const int64_t tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN);
     const int steps = (int)(K / kGemmTK);
     z.Sg = 1;
-    if (!fmfma)
-      for (int S = 2; S <= 8; S *= 2)
-        if (tiles * z.Sg < 256 && steps % (2 * S) == 0 && steps / S >= 4) z.Sg = S;
-    if (g_ov_gs.load() > 0 && !fmfma) {
+    for (int S = 2; S <= 8; S *= 2)
+      if (tiles * z.Sg < 256 && steps % (2 * S) == 0 && steps / S >= 4) z.Sg = S;
+    if (g_ov_gs.load() > 0) {
       const int S = g_ov_gs.load();
       if (steps % (2 * S) != 0) return SPEAR_E_UNSUPPORTED;
       z.Sg = S;
@@ -339,7 +343,8 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   if (local) {
     if (z.S > 1) z.off_eupart = take((size_t)z.nrg * z.S * M * z.R1 * 4);
   } else if (fmfma) {
-    // no workspace data
+    // the slices' EC accumulators (split-K only)
+    if (z.Sg > 1) z.off_epart = take((size_t)z.Sg * cdiv(M, kGemmTM) * cdiv(N, kGemmTN) * 16384);
   } else if (z.ec) {
     const bool partials = z.ec_mode != EC_GATHER && z.P * z.PG > 1;
     if (partials && z.ntb > kMaxEcCounters) return SPEAR_E_SHAPE;
@@ -366,8 +371,10 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   }
   if (!z.gemv && z.Sg > 1) {
     const int64_t tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN);
-    if (tiles > kMaxRowCounters) return SPEAR_E_SHAPE;
-    z.off_gpart = take((size_t)z.Sg * tiles * kGemmTM * kGemmTN * 4);
+    const size_t part = (size_t)z.Sg * tiles * kGemmTM * kGemmTN * 4;
+    // the kernel addresses the partial tiles with 32-bit offsets
+    if (tiles > kMaxRowCounters || part >= ((size_t)1 << 31)) return SPEAR_E_SHAPE;
+    z.off_gpart = take(part);
   }
   z.plan.workspace_bytes = off;
   return SPEAR_OK;
@@ -500,6 +507,7 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
   if (ws && z.Sg > 1) {
     g.ypart = (float*)(ws + z.off_gpart);
     g.ctr = (uint32_t*)(ws + kCtrRows);
+    if (z.off_epart) g.epart = (float*)(ws + z.off_epart);
   }
   g.qw = w->qweight;
   g.sc = w->scales;

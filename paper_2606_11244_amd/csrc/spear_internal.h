@@ -143,11 +143,13 @@ struct GemmParams {
   const uint16_t* vh;     // [M][vstride]
   const uint16_t* vl;
   int M, N, K, G, ngroups, r, vstride;
-  // split-K over S K-slices (small tile grids; not with EPI_LOCAL): the
-  // slices' fp32 tiles [S][tiles][128 x 128] (lane-major), tile counters
+  // split-K over S in {1, 2, 4, 8} K-slices (small tile grids): the slices'
+  // fp32 tiles [S][tiles][128 x 128] (lane-major), tile counters, and with
+  // EPI_LOCAL the slices' EC accumulators [S][tiles][4096] (lane-major)
   int S;
   float* ypart;
   uint32_t* ctr;
+  float* epart;
   // EPI_LOCAL (fully fused prefill): the projection's inputs
   const uint16_t* A;      // [r][K], r <= 16
   const uint16_t* wg;     // [K] (sigmoid gate) or null

@@ -1403,6 +1403,54 @@ __device__ __forceinline__ void dequant_word_pairs(uint32_t w, float s, int z, u
   }
 }
 
+// Split-K tile reduction of the GEMM: a thread's 16 f32x4 of the tile from
+// each of the S slices, summed in slice order (slice 0 first, so the result
+// does not depend on which slice arrives last). The slices' loads are issued
+// in rounds of 32 (S/2 rounds), each round's loads all in flight together:
+// the partials sit at the device coherence point, a memory round trip away,
+// and one round per slice would pay that latency S times.
+// base: byte offset of the thread's first f32x4 in slice 0; slice: bytes
+// between slices; entry (i, j) is 1024 * (4i + j) bytes further.
+template <int S>
+__device__ __forceinline__ void gemm_sum_slices(rsrc_t rp, uint32_t base, uint32_t slice,
+                                                f32x4 (&acc)[4][4]) {
+  constexpr int E = 32 / S;  // entries per round
+#pragma unroll
+  for (int rd = 0; rd < S / 2; ++rd) {
+    f32x4 pv[S][E];
+#pragma unroll
+    for (int q = 0; q < S; ++q)
+#pragma unroll
+      for (int e = 0; e < E; ++e) pv[q][e] = bld128cf(rp, base + q * slice + (rd * E + e) * 1024);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      f32x4 t = pv[0][e];
+#pragma unroll
+      for (int q = 1; q < S; ++q) t += pv[q][e];
+      acc[(rd * E + e) >> 2][(rd * E + e) & 3] = t;
+    }
+  }
+}
+
+// The same for the fully fused variant's EC accumulators: 4 f32x4 per
+// thread per slice, all slices' loads in one round (S <= 8: 32 loads).
+template <int S>
+__device__ __forceinline__ void gemm_sum_ec_slices(rsrc_t rp, uint32_t base, uint32_t slice,
+                                                   f32x4 (&eacc)[4]) {
+  f32x4 pv[S][4];
+#pragma unroll
+  for (int q = 0; q < S; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pv[q][i] = bld128cf(rp, base + q * slice + i * 1024);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f32x4 t = pv[0][i];
+#pragma unroll
+    for (int q = 1; q < S; ++q) t += pv[q][i];
+    eacc[i] = t;
+  }
+}
+
 template <int DT, int EPI>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -1580,51 +1628,41 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  // split-K: every slice publishes its tile (lane-major f32x4); the last
-  // to arrive sums the slices in slice order (its own from registers) and
-  // runs the epilogue
+  // split-K: every slice publishes its tile (lane-major f32x4), and with
+  // EPI_LOCAL its EC accumulators; the last to arrive sums the slices in
+  // slice order (reading its own back like the others) and runs the epilogue
   if (a.S > 1) {
     __shared__ int s_last;
-    const rsrc_t rp = make_rsrc(a.ypart, (uint32_t)((size_t)a.S * T * kGemmTM * kGemmTN * 4));
-    auto off = [&](int q, int i, int j) {
-      return (uint32_t)((((size_t)q * T + tb) * kGemmTM * kGemmTN) * 4 +
-                        ((size_t)((wave * 4 + i) * 4 + j) * 64 + lane) * 16);
-    };
+    const uint32_t tbytes = kGemmTM * kGemmTN * 4;
+    const rsrc_t rp = make_rsrc(a.ypart, (uint32_t)a.S * T * tbytes);
+    const uint32_t ybase = (uint32_t)tb * tbytes + (uint32_t)(wave * 16 * 64 + lane) * 16;
+    const uint32_t yslice = (uint32_t)T * tbytes;
+    constexpr uint32_t ebytes = 4 * 4 * 64 * 16;  // EC accumulators of a tile
+    const rsrc_t rep = make_rsrc(kLoc ? a.epart : nullptr, kLoc ? (uint32_t)a.S * T * ebytes : 0u);
+    const uint32_t ebase = (uint32_t)tb * ebytes + (uint32_t)(wave * 4 * 64 + lane) * 16;
+    const uint32_t eslice = (uint32_t)T * ebytes;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) bst128c(rp, off(ks, i, j), acc[i][j]);
+      for (int j = 0; j < 4; ++j) bst128c(rp, ybase + ks * yslice + (i * 4 + j) * 1024, acc[i][j]);
+    if constexpr (kLoc) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) bst128c(rep, ebase + ks * eslice + i * 1024, eacc[i]);
+    }
     complete_and_sync();
     if (tid == 0) s_last = arrive_last(a.ctr + tb, (uint32_t)a.S) ? 1 : 0;
     __syncthreads();
     if (!s_last) return;
-    f32x4 tot[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int q = 0; q < a.S; ++q) {
-      if (q == ks) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) tot[i][j] += acc[i][j];
-      } else {
-        f32x4 pv[4][4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) pv[i][j] = bld128cf(rp, off(q, i, j));
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) tot[i][j] += pv[i][j];
-      }
+    if (a.S == 2) {
+      gemm_sum_slices<2>(rp, ybase, yslice, acc);
+      if constexpr (kLoc) gemm_sum_ec_slices<2>(rep, ebase, eslice, eacc);
+    } else if (a.S == 4) {
+      gemm_sum_slices<4>(rp, ybase, yslice, acc);
+      if constexpr (kLoc) gemm_sum_ec_slices<4>(rep, ebase, eslice, eacc);
+    } else {
+      gemm_sum_slices<8>(rp, ybase, yslice, acc);
+      if constexpr (kLoc) gemm_sum_ec_slices<8>(rep, ebase, eslice, eacc);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = tot[i][j];
   }
 
   // EPI_LOCAL: v = alpha g(x) (.) u for the block's 128 tokens, as act-dtype
@@ -1840,7 +1878,9 @@ hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int
 
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st) {
   // split-K needs its partial tiles and tile counters (workspace)
-  if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.ctr || epi == EPI_LOCAL))) return hipErrorInvalidValue;
+  if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.ctr || (epi == EPI_LOCAL && !p.epart))) ||
+      (p.S != 1 && p.S != 2 && p.S != 4 && p.S != 8))
+    return hipErrorInvalidValue;
   const int tm = (p.M + kGemmTM - 1) / kGemmTM, tn = (p.N + kGemmTN - 1) / kGemmTN;
   const unsigned grid = (unsigned)(tm * tn * p.S);
   if (grid == 0) return hipSuccess;

@@ -87,11 +87,21 @@ def test_plan_phase_aware_dispatch():
     for M in (1, 64, 4096):
         p = _plan(M=M, force_path=sp.PATH_FUSED_MFMA)
         assert p.path == sp.PATH_FUSED_MFMA and p.num_launches == 1, M
-        assert p.grid == -(-M // 128) * (2048 // 128), M
+        assert p.grid == -(-M // 128) * (2048 // 128) * p.split_k, M
+        assert p.split_k == (1 if M == 4096 else 8), M
     assert _plan(M=4, force_path=sp.PATH_FUSED_LOCAL).grid == _plan(M=4, with_ec=False).grid
-    for M in (65, 512, 4096):
+    # prefill: the fully fused GEMM while the grid has at most 256 128 x 128
+    # tiles (N = 2048: up to M = 2048), the semi-fused pair above that and
+    # for ranks or gates the fused GEMM does not take
+    for M in (65, 512, 2048):
+        p = _plan(M=M)
+        assert p.path == sp.PATH_FUSED_MFMA and p.num_launches == 1, M
+    for M in (2049, 4096):
         p = _plan(M=M)
         assert p.path == sp.PATH_UNFUSED_2K and p.num_launches == 2, M
+    for kw in (dict(rank=32), dict(gate_kind=sp.GATE_TANH_MLP)):
+        p = _plan(M=512, **kw)
+        assert p.path == sp.PATH_UNFUSED_2K and p.num_launches == 2, kw
     assert _plan(M=4, force_path=sp.PATH_UNFUSED_CHAIN).num_launches == 4
     assert _plan(M=4096, force_path=sp.PATH_UNFUSED_CHAIN).num_launches == 4
     assert _plan(M=4, force_path=sp.PATH_UNFUSED_2K).num_launches == 2
@@ -107,6 +117,10 @@ def test_gemm_split_k_plan_and_workspace():
         assert p.split_k == 8 and p.grid == tiles * 8
         assert p.workspace_bytes >= 8 * tiles * 128 * 128 * 4
     assert _plan(M=4096, N=2048, K=2048).split_k == 1   # 512 tiles: no split
+    # the fully fused GEMM splits alike and adds the slices' EC accumulators
+    f = _plan(M=512, N=1024, K=8192, rank=16, force_path=2)
+    assert f.path == 2 and f.split_k == 8
+    assert f.workspace_bytes >= 8 * tiles * (128 * 128 + 4096) * 4
     prob = sp.problem(512, 1024, 8192, 128, sp.F16, 0)
     w = sp.W4(ADDR["q"], ADDR["s"], ADDR["z"])
     assert sp.LIB.spear_w4_linear(ctypes.byref(prob), ADDR["x"], ctypes.byref(w), ADDR["y"],

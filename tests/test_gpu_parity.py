@@ -342,14 +342,15 @@ def test_every_gemv_launch_shape(shape, slices, waves):
 @pytest.mark.parametrize("M", [65, 130, 300])
 def test_gemm_split_k(slices, M):
     """The prefill GEMM with its K split into 1..8 slices (each summed in
-    slice order by the tile's last workgroup) meets the bar on every GEMM
-    path and on the 4-bit product alone; ragged tokens and rows."""
+    slice order by the tile's last workgroup; the fully fused variant sums
+    its EC projection the same way) meets the bar on every GEMM path and on
+    the 4-bit product alone; ragged tokens and rows."""
     from paper_2606_11244_amd import spear as sp
     L = S.make_layer(M=M, N=200, K=1024, group_size=128, rank=16, seed=M + slices, ec_std=0.05)
     ref = O.w4ec_linear(L)
     sp.set_gemm_slices(slices)
     try:
-        for p in (PATHS["2k"], PATHS["chain"]):
+        for p in (PATHS["2k"], PATHS["chain"], PATHS["fused_mfma"]):
             log(f"gemm slices={slices} M={M} path={p}")
             assert_parity(gpu_y(L, p), ref, f"slices={slices} M={M} path={p}")
         assert_parity(gpu_y(L, 0, with_ec=False), O.w4_linear_layer(L), f"slices={slices} w4")
