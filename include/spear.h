@@ -127,9 +127,24 @@ typedef struct {
   const uint8_t* zeros;    /* [N][K/G] 0..15                                  */
 } spear_w4_t;
 
+/* Storage of the EC factors A and B (section 6 and the appendix: the
+ * deployed compensators keep A and B in INT8, per output channel and
+ * symmetric, and the gate in fp16). */
+enum {
+  SPEAR_AB_ACT = 0,  /* A, B in the activation dtype                          */
+  SPEAR_AB_INT8 = 1  /* A, B int8 codes q in [-127, 127]: A[i][k] =
+                        a_scale[i] * qA[i][k] (a_scale one fp32 per rank
+                        channel), B[n][j] = b_scale[n] * qB[n][j] (one fp32
+                        per output feature). Where a code feeds an MFMA it is
+                        dequantised to the activation dtype, one rounding of
+                        the fp32 product; where the kernel sums in fp32 (the
+                        fused decode epilogue, the naive chain) the codes and
+                        scale are used exactly                              */
+};
+
 typedef struct {
-  const void* A;     /* [r][K] act dtype                                      */
-  const void* B;     /* [N][r] act dtype                                      */
+  const void* A;     /* [r][K] act dtype, or int8 (SPEAR_AB_INT8)             */
+  const void* B;     /* [N][r] act dtype, or int8 (SPEAR_AB_INT8)             */
   float alpha;       /* EC scale (section 3.1); 1.0 when folded into B        */
   const void* w_g;   /* [K] act dtype      (SIGMOID_LINEAR only)              */
   float b_g;         /*                    (SIGMOID_LINEAR only)              */
@@ -137,6 +152,9 @@ typedef struct {
   const void* b1;    /* [h]                                                   */
   const void* W2;    /* [r][h]                                                */
   const void* b2;    /* [r]                                                   */
+  int32_t ab_format;       /* SPEAR_AB_*; other values: SPEAR_E_DTYPE       */
+  const float* a_scale;    /* [r] fp32 (SPEAR_AB_INT8 only; 16-byte aligned) */
+  const float* b_scale;    /* [N] fp32 (SPEAR_AB_INT8 only; 16-byte aligned) */
 } spear_ec_t;
 
 typedef struct {

@@ -29,6 +29,10 @@ tiny shapes, integer-grid exactness, the RTN round trip, reductions to the
 plain 4-bit product (r = 0, gate == 0, W_hat == 0), the static-LoRA special
 case of the tanh gate, the factored form (Eq. 4), hand-worked golden
 fixtures, and planted-mistake checks that each pin catches.
+
+INT8 EC factors (the deployed format: A and B stored as int8 codes with one
+symmetric scale per output channel) enter as their exact dequantised values
+scale[c] * q[c][.]; the rest of the evaluation is unchanged.
 """
 from __future__ import annotations
 
@@ -181,6 +185,28 @@ def w4ec_linear_f64(x, W_hat, A, B, alpha: float, gate_kind: int, w_g=None,
     return y + v @ np.asarray(B, np.float64).T
 
 
+def dequant_int8(q, scale) -> np.ndarray:
+    """INT8 per-channel symmetric factor (the deployed EC format of section 6
+    and the appendix: INT8 A and B, one scale per output channel): row c of
+    the factor is scale[c] * q[c], evaluated exactly in float64."""
+    return np.asarray(scale, np.float64)[:, None] * np.asarray(q, np.float64)
+
+
+def ec_factors(layer, rows=None):
+    """(A, B) of a stored layer as float64: the INT8 codes times their
+    per-channel scales when the layer carries them (layer.ab_int8), else the
+    activation-dtype bit patterns decoded exactly. `rows` selects rows of B."""
+    if getattr(layer, "ab_int8", False):
+        A = dequant_int8(layer.A_q, layer.a_scale)
+        Bq, bs = layer.B_q, layer.b_scale
+        if rows is not None:
+            Bq, bs = Bq[rows], bs[rows]
+        return A, dequant_int8(Bq, bs)
+    dt = layer.act_dtype
+    B = layer.B if rows is None else layer.B[rows]
+    return bits_to_f64(layer.A, dt), bits_to_f64(B, dt)
+
+
 def w4ec_linear(layer) -> np.ndarray:
     """Eq. 3 on a stored layer (any object with the generator's fields):
     decodes every stored tensor exactly, then evaluates in float64."""
@@ -189,8 +215,9 @@ def w4ec_linear(layer) -> np.ndarray:
     x = bits_to_f64(layer.x, dt)
     if layer.rank == 0:
         return w4_linear(x, W_hat)
+    A, B = ec_factors(layer)
     return w4ec_linear_f64(
-        x, W_hat, bits_to_f64(layer.A, dt), bits_to_f64(layer.B, dt), layer.alpha,
+        x, W_hat, A, B, layer.alpha,
         layer.gate_kind, w_g=bits_to_f64(layer.w_g, dt), b_g=layer.b_g,
         W1=bits_to_f64(layer.W1, dt), b1=bits_to_f64(layer.b1, dt),
         W2=bits_to_f64(layer.W2, dt), b2=bits_to_f64(layer.b2, dt))
@@ -212,8 +239,9 @@ def w4ec_linear_rows(layer, rows) -> np.ndarray:
     x = bits_to_f64(layer.x, dt)
     if layer.rank == 0:
         return w4_linear(x, W_hat)
+    A, B = ec_factors(layer, rows)
     return w4ec_linear_f64(
-        x, W_hat, bits_to_f64(layer.A, dt), bits_to_f64(layer.B, dt)[rows],
+        x, W_hat, A, B,
         layer.alpha, layer.gate_kind, w_g=bits_to_f64(layer.w_g, dt), b_g=layer.b_g,
         W1=bits_to_f64(layer.W1, dt), b1=bits_to_f64(layer.b1, dt),
         W2=bits_to_f64(layer.W2, dt), b2=bits_to_f64(layer.b2, dt))

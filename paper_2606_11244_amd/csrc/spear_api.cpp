@@ -404,18 +404,26 @@ spear_status_t check_w4(const spear_problem_t* p, const void* x, const spear_w4_
 spear_status_t check_ec(const spear_problem_t* p, const Resolved& z, const spear_ec_t* ec, const void* y) {
   if (!z.ec) return SPEAR_OK;
   if (!ec || !ec->A || !ec->B) return SPEAR_E_NULL;
+  if (ec->ab_format != SPEAR_AB_ACT && ec->ab_format != SPEAR_AB_INT8) return SPEAR_E_DTYPE;
+  const bool i8 = ec->ab_format == SPEAR_AB_INT8;
+  if (i8 && (!ec->a_scale || !ec->b_scale)) return SPEAR_E_NULL;
   if (z.gate == GATE_SIGMOID && !ec->w_g) return SPEAR_E_NULL;
   if (z.gate == GATE_TANH && (!ec->W1 || !ec->b1 || !ec->W2 || !ec->b2)) return SPEAR_E_NULL;
   if (misaligned(ec->A) || misaligned(ec->B) || misaligned(ec->w_g) || misaligned(ec->W1) ||
-      misaligned(ec->b1) || misaligned(ec->W2) || misaligned(ec->b2))
+      misaligned(ec->b1) || misaligned(ec->W2) || misaligned(ec->b2) ||
+      (i8 && (misaligned(ec->a_scale) || misaligned(ec->b_scale))))
     return SPEAR_E_ALIGN;
-  const size_t ybytes = (size_t)p->M * p->N * 2;
-  if (overlaps(y, ybytes, ec->A, (size_t)z.r * p->K * 2) ||
-      overlaps(y, ybytes, ec->B, (size_t)p->N * z.r * 2) ||
+  const size_t ybytes = (size_t)p->M * p->N * 2, eb = i8 ? 1 : 2;
+  if (overlaps(y, ybytes, ec->A, (size_t)z.r * p->K * eb) ||
+      overlaps(y, ybytes, ec->B, (size_t)p->N * z.r * eb) ||
+      (i8 && (overlaps(y, ybytes, ec->a_scale, (size_t)z.r * 4) ||
+              overlaps(y, ybytes, ec->b_scale, (size_t)p->N * 4))) ||
       (z.gate == GATE_SIGMOID && overlaps(y, ybytes, ec->w_g, (size_t)p->K * 2)))
     return SPEAR_E_ALIAS;
   return SPEAR_OK;
 }
+
+bool ab_int8(const spear_ec_t* ec) { return ec && ec->ab_format == SPEAR_AB_INT8; }
 
 spear_status_t check_ws(const spear_problem_t* p, const Resolved& z, const void* y, void* ws,
                         size_t ws_bytes) {
@@ -445,7 +453,12 @@ EcParams make_ec(const spear_problem_t* p, const Resolved& z, const void* x, con
   e.mode = z.ec_mode;
   e.vstride = z.vstride;
   if (ec) {
-    e.A = (const uint16_t*)ec->A;
+    if (ab_int8(ec)) {
+      e.A8 = (const int8_t*)ec->A;
+      e.sa = ec->a_scale;
+    } else {
+      e.A = (const uint16_t*)ec->A;
+    }
     e.wg = (const uint16_t*)ec->w_g;
     e.W1 = (const uint16_t*)ec->W1;
     e.b1 = (const uint16_t*)ec->b1;
@@ -477,14 +490,19 @@ GemvParams make_gemv(const spear_problem_t* p, const Resolved& z, const void* x,
   g.G = z.G;
   g.ngroups = z.ngroups;
   g.r = z.r;
-  g.B = ec ? (const uint16_t*)ec->B : nullptr;
+  if (ab_int8(ec)) {
+    g.B8 = (const int8_t*)ec->B;
+    g.sb = ec->b_scale;
+  } else {
+    g.B = ec ? (const uint16_t*)ec->B : nullptr;
+  }
   g.S = z.S;
   g.ips = z.ips;
   g.iw = z.iw;
   g.wait_polls = g_wait_polls.load();
   g.xlds = z.xlds;
   g.xstride = z.xstride;
-  g.bpre = ec ? z.bpre : 0;
+  g.bpre = ec && !ab_int8(ec) ? z.bpre : 0;  // B rows are staged in LDS as act dtype only
   g.lds_y = z.lds_y;
   g.lds_e = z.lds_e;
   g.lds_b = z.lds_b;
@@ -521,14 +539,27 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
   g.ngroups = z.ngroups;
   g.r = z.r;
   g.vstride = z.vstride;
+  const bool i8 = ab_int8(ec);
   if (ec && ws && z.off_vh) {
-    g.B = (const uint16_t*)ec->B;
+    if (i8) {
+      g.B8 = (const int8_t*)ec->B;
+      g.sb = ec->b_scale;
+    } else {
+      g.B = (const uint16_t*)ec->B;
+    }
     g.vh = (const uint16_t*)(ws + z.off_vh);
     g.vl = (const uint16_t*)(ws + z.off_vl);
   }
   if (ec && z.plan.path == SPEAR_PATH_FUSED_MFMA) {
-    g.B = (const uint16_t*)ec->B;
-    g.A = (const uint16_t*)ec->A;
+    if (i8) {
+      g.A8 = (const int8_t*)ec->A;
+      g.B8 = (const int8_t*)ec->B;
+      g.sa = ec->a_scale;
+      g.sb = ec->b_scale;
+    } else {
+      g.B = (const uint16_t*)ec->B;
+      g.A = (const uint16_t*)ec->A;
+    }
     g.wg = (const uint16_t*)ec->w_g;
     g.alpha = ec->alpha;
     g.b_g = ec->b_g;
@@ -593,14 +624,14 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   const int ec_grid = z.ntb * z.P * z.PG;
   if (path == SPEAR_PATH_FUSED_MFMA) {
     GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
-    return hip_status(launch_gemm(z.dt, EPI_LOCAL, g, s));
+    return hip_status(launch_gemm(z.dt, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g, s));
   }
   if (path == SPEAR_PATH_FUSED_LOCAL) {
     GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
     g.ec = e;
     if (z.S > 1) g.eupart = (float*)(ws + z.off_eupart);
-    return hip_status(
-        launch_gemv(z.dt, z.MT, z.RT, EPI_LOCAL, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, s));
+    return hip_status(launch_gemv(z.dt, z.MT, z.RT, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g,
+                                  z.nrg * z.S, 64 * z.NW, z.lds_gemv, s));
   }
   if (path == SPEAR_PATH_FUSED_GEMV) {
     e.vtag = (unsigned long long*)(ws + z.off_vtag);
@@ -642,8 +673,10 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   if (st != SPEAR_OK) return st;
   st = hip_status(launch_gate(z.dt, e, z.ntb, z.lds_gate, s));
   if (st != SPEAR_OK) return st;
-  return hip_status(launch_ec_up_acc(z.dt, e.v, (const uint16_t*)ec->B, (uint16_t*)y, (int)prob->M,
-                                     (int)prob->N, z.r, s));
+  const bool i8 = ab_int8(ec);
+  return hip_status(launch_ec_up_acc(z.dt, e.v, i8 ? nullptr : (const uint16_t*)ec->B,
+                                     i8 ? (const int8_t*)ec->B : nullptr, i8 ? ec->b_scale : nullptr,
+                                     (uint16_t*)y, (int)prob->M, (int)prob->N, z.r, s));
 }
 
 spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w, void* w_out,

@@ -14,7 +14,8 @@ enum { GATE_ONE = 0, GATE_SIGMOID = 1, GATE_TANH = 2 };
 enum { EPI_NONE = 0,   // Y = X W^T
        EPI_READY = 1,  // Y = X W^T + v B^T, v already in the workspace
        EPI_FUSED = 2,  // same, v produced by EC workgroups of the same grid
-       EPI_LOCAL = 3   // same, [A; w_g] x computed by the GEMV waves themselves
+       EPI_LOCAL = 3,  // same, [A; w_g] x computed by the GEMV waves themselves
+       EPI_LOCAL_I8 = 4  // EPI_LOCAL with INT8 A and B (per-channel fp32 scales)
                        // over their K chunks (small rank), v from it per block
 };
 // How the EC projection's K-slices are combined.
@@ -79,7 +80,9 @@ __host__ __device__ inline uint32_t ec_tag(uint32_t gen) { return ((gen + 1u) * 
 // (tpg tiles of 16 rows of [A; w_g]).
 struct EcParams {
   const uint16_t* x;      // [M][K]
-  const uint16_t* A;      // [r][K]
+  const uint16_t* A;      // [r][K] act dtype (null with INT8 A)
+  const int8_t* A8;       // [r][K] INT8 codes, or null
+  const float* sa;        // [r] INT8 per-channel scales
   const uint16_t* wg;     // [K] or null
   const uint16_t* W1;     // [h][r]
   const uint16_t* b1;     // [h]
@@ -113,7 +116,9 @@ struct GemvParams {
   const uint8_t* zr;      // [N][K/G]
   const uint16_t* x;      // [M][K]
   uint16_t* y;            // [M][N]
-  const uint16_t* B;      // [N][r]
+  const uint16_t* B;      // [N][r] act dtype (null with INT8 B)
+  const int8_t* B8;       // [N][r] INT8 codes, or null
+  const float* sb;        // [N] INT8 per-channel scales
   int M, N, K, G, ngroups, r;
   int S, ips, iw;         // K-slices per row group, iterations per slice and per wave
   int n_prod;             // EC workgroups at the head of the grid (fused)
@@ -150,6 +155,12 @@ struct GemmParams {
   float* ypart;
   uint32_t* ctr;
   float* epart;
+  // INT8 A and B (per-channel fp32 scales), or null: B8 for the
+  // up-projection of EPI_READY / EPI_LOCAL_I8, A8 for EPI_LOCAL_I8
+  const int8_t* A8;       // [r][K]
+  const int8_t* B8;       // [N][r]
+  const float* sa;        // [r]
+  const float* sb;        // [N]
   // EPI_LOCAL (fully fused prefill): the projection's inputs
   const uint16_t* A;      // [r][K], r <= 16
   const uint16_t* wg;     // [K] (sigmoid gate) or null
@@ -189,7 +200,7 @@ hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int
                        size_t lds, hipStream_t st);
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st);
 hipError_t launch_gate(int dt, const EcParams& e, int ntb, size_t lds, hipStream_t st);
-hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, uint16_t* y, int M,
-                            int N, int r, hipStream_t st);
+hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, const int8_t* B8,
+                            const float* sb, uint16_t* y, int M, int N, int r, hipStream_t st);
 
 }  // namespace spear

@@ -23,6 +23,8 @@
 //   k_gate, k_ec_up_acc   the naive split chain's separate gate and
 //              reprojection+accumulate launches
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 #include <stdint.h>
 
 #include "spear_internal.h"
@@ -119,6 +121,27 @@ __device__ __forceinline__ u32x4 ones8() {
 }
 
 __device__ __forceinline__ u32x4 ldg16(const void* p) { return *(const u32x4*)p; }
+
+// INT8 per-channel symmetric codes (the EC factors' deployment format):
+// code q of channel c stands for sa[c] * q. Where a code feeds an MFMA it is
+// dequantised to the activation dtype like the 4-bit weights, one rounding
+// of the fp32 product s * q (exact for |q| <= 127). Bytes 2p and 2p + 1 of w.
+template <int DT>
+__device__ __forceinline__ uint32_t i8pair_to_act(uint32_t w, int p, float s) {
+  const int b0 = (int)(w << (24 - 16 * p)) >> 24;
+  const int b1 = (int)(w << (16 - 16 * p)) >> 24;
+  return (uint32_t)f2act<DT>((float)b0 * s) | ((uint32_t)f2act<DT>((float)b1 * s) << 16);
+}
+// eight codes (two dwords, K order) -> an 8-element MFMA operand
+template <int DT>
+__device__ __forceinline__ u32x4 i8x8_to_act(uint32_t w0, uint32_t w1, float s) {
+  return u32x4{i8pair_to_act<DT>(w0, 0, s), i8pair_to_act<DT>(w0, 1, s),
+               i8pair_to_act<DT>(w1, 0, s), i8pair_to_act<DT>(w1, 1, s)};
+}
+template <int DT>
+__device__ __forceinline__ uint16_t i8_to_act(int8_t q, float s) {
+  return f2act<DT>((float)q * s);
+}
 
 // Raw buffer loads through a bounds-checked resource (gfx9 descriptor word 3
 // = 0x00020000): a byte offset at or past `bytes` reads as zero. Masked
@@ -318,7 +341,8 @@ __device__ void ec_project(const EcParams& e, int tb, int it_beg, int it_end, in
   // token rows past M read row M-1: their results are never used
   const int m = min(tb * kTokTile + lr, e.M - 1);
   const rsrc_t rx = make_rsrc(e.x, (uint32_t)e.M * e.K * 2);
-  const rsrc_t ra = make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
+  const bool i8 = e.A8 != nullptr;  // uniform
+  const rsrc_t ra = i8 ? make_rsrc(e.A8, (uint32_t)e.r * e.K) : make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
   const rsrc_t rg = make_rsrc(e.wg, e.gate == GATE_SIGMOID ? (uint32_t)e.K * 2 : 0u);
   // K order within an iteration: MFMA jj, lane group lg takes K
   // [8 lg + 32 jj, +8) for both operands, so that each load reads 64
@@ -351,32 +375,55 @@ __device__ void ec_project(const EcParams& e, int tb, int it_beg, int it_end, in
 #pragma unroll
     for (int t = 0; t < kEcTiles; ++t)
       if (t == gt) goff_g = goff[t];
-    for (int it0 = it_beg + wave * IPP; it0 < it_end; it0 += NW * IPP) {
-      u32x4 xv[IPP][4], av[IPP][kEcTiles][4], gv[IPP][4];
+    // the iterations, for act-dtype A (16-byte loads) or INT8 A (8-byte
+    // loads of the same eight K, dequantised with the row's scale at the MFMA)
+    auto iterate = [&](auto i8c) {
+      constexpr bool kI8 = decltype(i8c)::value;
+      float sa[kEcTiles];
 #pragma unroll
-      for (int h = 0; h < IPP; ++h) {
-        const bool ok = it0 + h < it_end;  // uniform
-        const uint32_t kb = (uint32_t)(it0 + h) * (kIterK * 2);
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) xv[h][jj] = bld128(rx, ok ? xoff + kb + 64 * jj : kOOB);
-#pragma unroll
-        for (int t = 0; t < kEcTiles; ++t)
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj)
-            av[h][t][jj] = bld128(ra, ok && aoff[t] != kOOB ? aoff[t] + kb + 64 * jj : kOOB);
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj)
-          gv[h][jj] = bld128(rg, ok && goff_g != kOOB ? goff_g + kb + 64 * jj : kOOB);
+      for (int t = 0; t < kEcTiles; ++t) {
+        const int j = (tg0 + t) * 16 + lr;
+        sa[t] = kI8 && t < nt && j < e.r ? e.sa[j] : 0.f;
       }
-      __builtin_amdgcn_sched_barrier(0);
+      for (int it0 = it_beg + wave * IPP; it0 < it_end; it0 += NW * IPP) {
+        u32x4 xv[IPP][4], av[IPP][kEcTiles][4], gv[IPP][4];
 #pragma unroll
-      for (int h = 0; h < IPP; ++h)
+        for (int h = 0; h < IPP; ++h) {
+          const bool ok = it0 + h < it_end;  // uniform
+          const uint32_t kb = (uint32_t)(it0 + h) * (kIterK * 2);
 #pragma unroll
-        for (int t = 0; t < kEcTiles; ++t)
+          for (int jj = 0; jj < 4; ++jj) xv[h][jj] = bld128(rx, ok ? xoff + kb + 64 * jj : kOOB);
+#pragma unroll
+          for (int t = 0; t < kEcTiles; ++t)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              if constexpr (kI8) {
+                // aoff[t] and kb count 2-byte elements twice: halve them
+                const u32x2 q = bld64(ra, ok && aoff[t] != kOOB ? (aoff[t] + kb) / 2 + 32 * jj : kOOB);
+                av[h][t][jj] = u32x4{q[0], q[1], 0u, 0u};
+              } else {
+                av[h][t][jj] = bld128(ra, ok && aoff[t] != kOOB ? aoff[t] + kb + 64 * jj : kOOB);
+              }
+            }
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj)
-            acc[t] = mfma16<DT>(t == gt ? (av[h][t][jj] | gv[h][jj]) : av[h][t][jj], xv[h][jj], acc[t]);
-    }
+            gv[h][jj] = bld128(rg, ok && goff_g != kOOB ? goff_g + kb + 64 * jj : kOOB);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int h = 0; h < IPP; ++h)
+#pragma unroll
+          for (int t = 0; t < kEcTiles; ++t)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              u32x4 af = av[h][t][jj];
+              if constexpr (kI8) af = i8x8_to_act<DT>(af[0], af[1], sa[t]);
+              acc[t] = mfma16<DT>(t == gt ? (af | gv[h][jj]) : af, xv[h][jj], acc[t]);
+            }
+      }
+    };
+    if (i8) iterate(std::true_type{});
+    else iterate(std::false_type{});
     // lane l holds token l % 16 and rows 4 * (l / 16) .. + 3 of each tile
 #pragma unroll
     for (int t = 0; t < kEcTiles; ++t)
@@ -567,16 +614,25 @@ __global__ __launch_bounds__(256) void k_gate(EcParams e) {
   for (int idx = threadIdx.x; idx < cnt * e.r; idx += blockDim.x) e.v[(size_t)m0 * e.r + idx] = v_tile[idx];
 }
 
-// Naive chain, reprojection + accumulate: y[m][n] += sum_j v[m][j] B[n][j].
+// Naive chain, reprojection + accumulate: y[m][n] += sum_j v[m][j] B[n][j]
+// (INT8 B: sb[n] * sum_j v[m][j] q[n][j], in fp32).
 template <int DT>
 __global__ __launch_bounds__(256) void k_ec_up_acc(const float* __restrict__ v,
                                                    const uint16_t* __restrict__ B,
+                                                   const int8_t* __restrict__ B8,
+                                                   const float* __restrict__ sb,
                                                    uint16_t* __restrict__ y, int M, int N, int r) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long long)M * N) return;
   const int m = (int)(idx / N), n = (int)(idx % N);
   float a = act2f<DT>(y[idx]);
-  for (int j = 0; j < r; ++j) a += v[(size_t)m * r + j] * act2f<DT>(B[(size_t)n * r + j]);
+  if (B8) {
+    float t = 0.f;
+    for (int j = 0; j < r; ++j) t += v[(size_t)m * r + j] * (float)B8[(size_t)n * r + j];
+    a += sb[n] * t;
+  } else {
+    for (int j = 0; j < r; ++j) a += v[(size_t)m * r + j] * act2f<DT>(B[(size_t)n * r + j]);
+  }
   y[idx] = f2act<DT>(a);
 }
 
@@ -640,7 +696,8 @@ __device__ void ec_project_wave(const EcParams& e, int tb, float* u_lds) {
   const int IT = e.K / kIterK, RTe = (e.R1 + 15) >> 4;
   const int m = min(tb * kTokTile + lr, e.M - 1);
   const rsrc_t rx = make_rsrc(e.x, (uint32_t)e.M * e.K * 2);
-  const rsrc_t ra = make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
+  const bool i8 = e.A8 != nullptr;  // uniform
+  const rsrc_t ra = i8 ? make_rsrc(e.A8, (uint32_t)e.r * e.K) : make_rsrc(e.A, (uint32_t)e.r * e.K * 2);
   const rsrc_t rg = make_rsrc(e.wg, e.gate == GATE_SIGMOID ? (uint32_t)e.K * 2 : 0u);
   // K order within an iteration: MFMA jj, lane group lg takes K
   // [8 lg + 32 jj, +8), so that each load reads 64 contiguous bytes per row
@@ -649,13 +706,20 @@ __device__ void ec_project_wave(const EcParams& e, int tb, float* u_lds) {
     const int j = t * 16 + lr;
     const uint32_t aoff = j < e.r ? (uint32_t)j * e.K * 2 + 16 * lg : kOOB;
     const uint32_t goff = (j == e.r && e.gate == GATE_SIGMOID) ? 16u * lg : kOOB;
+    const float saj = i8 && j < e.r ? e.sa[j] : 0.f;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int it = 0; it < IT; ++it) {
       const uint32_t kb = (uint32_t)it * (kIterK * 2);
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
         const u32x4 xv = bld128(rx, xoff + kb + 64 * jj);
-        u32x4 av = bld128(ra, aoff != kOOB ? aoff + kb + 64 * jj : kOOB);
+        u32x4 av;
+        if (i8) {
+          const u32x2 q = bld64(ra, aoff != kOOB ? (aoff + kb) / 2 + 32 * jj : kOOB);
+          av = i8x8_to_act<DT>(q[0], q[1], saj);
+        } else {
+          av = bld128(ra, aoff != kOOB ? aoff + kb + 64 * jj : kOOB);
+        }
         av |= bld128(rg, goff != kOOB ? goff + kb + 64 * jj : kOOB);
         acc = mfma16<DT>(av, xv, acc);
       }
@@ -756,6 +820,7 @@ __device__ void ec_wave(const GemvParams& a, uint32_t gen, char* smem, int n0, b
         } else {
           auto bval = [&](int j) -> uint32_t {
             if (n >= N || j >= r) return 0u;
+            if (a.B8) return i8_to_act<DT>(a.B8[(size_t)n * r + j], a.sb[n]);
             return bpre ? (uint32_t)bs[row * r + j] : bld16(rb, (uint32_t)(n * r + j) * 2);
           };
 #pragma unroll
@@ -882,7 +947,8 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int s_flag;
   constexpr bool kEC = EPI == EPI_READY || EPI == EPI_FUSED;  // with an EC wave
-  constexpr bool kLoc = EPI == EPI_LOCAL;
+  constexpr bool kLoc = EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8;
+  constexpr bool kI8 = EPI == EPI_LOCAL_I8;  // INT8 A and B
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int NW = (blockDim.x >> 6) - (kEC ? 1 : 0);           // GEMV waves
@@ -959,9 +1025,14 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   // MFMA lane layout straight from memory, every load would touch 32 cache
   // lines. The MFMAs then take A's rows (lane lr: row lr) and w_g in every
   // column as two further B operands.
-  const rsrc_t ra = make_rsrc(kLoc ? a.ec.A : nullptr, kLoc ? (uint32_t)r * K * 2 : 0u);
+  // INT8 A: eight codes (8 bytes) per chunk, dequantised with the row's
+  // scale when stored; the scales of A's rows sit in lanes 0..15
+  const rsrc_t ra = kI8 ? make_rsrc(a.ec.A8, (uint32_t)r * K)
+                        : make_rsrc(kLoc ? a.ec.A : nullptr, kLoc ? (uint32_t)r * K * 2 : 0u);
   const rsrc_t rgw = make_rsrc(kLoc ? a.ec.wg : nullptr,
                                kLoc && a.ec.gate == GATE_SIGMOID ? (uint32_t)K * 2 : 0u);
+  float sa_lane = 0.f;
+  if constexpr (kI8) sa_lane = (lane & 15) < r ? a.ec.sa[lane & 15] : 0.f;
   const int acpr = (it_end - it_blk) * (kIterK / 8);  // 16-byte chunks per row
   const int astride = acpr * 8 + 8;                   // LDS row stride (halves)
   uint16_t* als = (uint16_t*)(smem + a.lds_a);        // [17][astride]
@@ -970,8 +1041,13 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
     for (int u = 0; u < 4; ++u) {
       const int ci = base + u * (int)blockDim.x;
       const int row = ci / acpr, kc = ci - row * acpr;
-      c4[u] = bld128(ra, ci < 16 * acpr && row < r
-                             ? ((uint32_t)row * K + it_blk * kIterK + 8 * kc) * 2 : kOOB);
+      const bool ok = ci < 16 * acpr && row < r;
+      if constexpr (kI8) {
+        const u32x2 q = bld64(ra, ok ? (uint32_t)row * K + it_blk * kIterK + 8 * kc : kOOB);
+        c4[u] = u32x4{q[0], q[1], 0u, 0u};
+      } else {
+        c4[u] = bld128(ra, ok ? ((uint32_t)row * K + it_blk * kIterK + 8 * kc) * 2 : kOOB);
+      }
     }
   };
   auto a_store = [&](int base, const u32x4 (&c4)[4]) {
@@ -979,7 +1055,9 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
     for (int u = 0; u < 4; ++u) {
       const int ci = base + u * (int)blockDim.x;
       const int row = ci / acpr, kc = ci - row * acpr;
-      if (ci < 16 * acpr) *(u32x4*)(als + row * astride + 8 * kc) = c4[u];
+      u32x4 v = c4[u];
+      if constexpr (kI8) v = i8x8_to_act<DT>(v[0], v[1], __shfl(sa_lane, row & 15));
+      if (ci < 16 * acpr) *(u32x4*)(als + row * astride + 8 * kc) = v;
     }
   };
   auto load_x = [&](u32x4 (&xv)[MT][4], int it) {
@@ -1355,6 +1433,11 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
               ev += vlo * act2f<DT>((uint16_t)(b8[q] & 0xFFFFu)) + vhi * act2f<DT>((uint16_t)(b8[q] >> 16));
             }
           }
+        } else if constexpr (kI8) {
+          // INT8 B: the codes and the row's scale exactly, in fp32
+          const int8_t* br = a.B8 + (size_t)(n0 + row) * r;
+          for (int j = 0; j < r; ++j) ev += vm[j] * (float)br[j];
+          ev *= a.sb[n0 + row];
         } else {
           const uint16_t* br = a.B + (size_t)(n0 + row) * r;
           for (int j = 0; j < r; ++j) ev += vm[j] * act2f<DT>(br[j]);
@@ -1454,7 +1537,8 @@ __device__ __forceinline__ void gemm_sum_ec_slices(rsrc_t rp, uint32_t base, uin
 template <int DT, int EPI>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  constexpr bool kLoc = EPI == EPI_LOCAL;
+  constexpr bool kLoc = EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8;
+  constexpr bool kI8 = EPI == EPI_LOCAL_I8;  // INT8 A and B
   constexpr int LR = kGemmLdsRow;
   constexpr int TILE = kGemmTM * LR;  // halves per LDS tile
   constexpr int ETILE = kGemmEcRows * LR;
@@ -1515,10 +1599,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   // EPI_LOCAL: thread t < 136 stages 16 bytes of the EC tile per step: row
   // t / 8 (A's row while below r, zero up to 15; w_g as row 16), chunk t % 8
   const int er = tid >> 3, ec8 = tid & 7;
-  const rsrc_t ra = make_rsrc(kLoc ? a.A : nullptr, kLoc ? (uint32_t)a.r * K * 2 : 0u);
+  // INT8 A: the chunk's eight codes (8 bytes), dequantised with row er's
+  // scale when stored
+  const rsrc_t ra = kI8 ? make_rsrc(a.A8, (uint32_t)a.r * K)
+                        : make_rsrc(kLoc ? a.A : nullptr, kLoc ? (uint32_t)a.r * K * 2 : 0u);
   const rsrc_t rgw = make_rsrc(kLoc ? a.wg : nullptr,
                                kLoc && a.gate == GATE_SIGMOID ? (uint32_t)K * 2 : 0u);
   const uint32_t eoff = er < 16 && er < a.r ? ((uint32_t)er * K + 8 * ec8) * 2 : kOOB;
+  const float sa_er = kI8 && er < 16 && er < a.r ? a.sa[er] : 0.f;
   const uint32_t goff = er == 16 ? 16u * ec8 : kOOB;
 
   // two register sets of global loads, so that the loads of step kt+2 are
@@ -1541,7 +1629,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     const uint32_t g = k0 / a.G;
     st.s = bld16(rsc, wok ? ((uint32_t)wn_row * a.ngroups + g) * 2 : kOOB);
     st.z = bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
-    if constexpr (kLoc) {
+    if constexpr (kI8) {
+      const u32x2 q = bld64(ra, eoff == kOOB ? kOOB : eoff / 2 + k0);
+      st.e = u32x4{q[0], q[1], 0u, 0u};
+      st.g = bld128(rgw, goff == kOOB ? kOOB : goff + k0 * 2);
+    } else if constexpr (kLoc) {
       st.e = bld128(ra, eoff == kOOB ? kOOB : eoff + k0 * 2);
       st.g = bld128(rgw, goff == kOOB ? kOOB : goff + k0 * 2);
     }
@@ -1562,7 +1654,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
       *(u32x4*)(ws + wr * LR + 32 * wh + 8 * c) = u32x4{o[0], o[1], o[2], o[3]};
     }
     if constexpr (kLoc) {
-      if (tid < kGemmEcRows * 8) *(u32x4*)(Es + buf * ETILE + er * LR + 8 * ec8) = st.e | st.g;
+      u32x4 ev = st.e;
+      if constexpr (kI8) ev = i8x8_to_act<DT>(ev[0], ev[1], sa_er);
+      if (tid < kGemmEcRows * 8) *(u32x4*)(Es + buf * ETILE + er * LR + 8 * ec8) = ev | st.g;
     }
   };
 
@@ -1701,10 +1795,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     __syncthreads();
   }
 
-  if constexpr (EPI == EPI_READY || EPI == EPI_LOCAL) {
-    // y += v_hi B^T + v_lo B^T over the rank (zero-padded to vstride)
+  if constexpr (EPI == EPI_READY || kLoc) {
+    // y += v_hi B^T + v_lo B^T over the rank (zero-padded to vstride); INT8
+    // B rows are dequantised with their scale
     const int r = a.r;
     const bool bvec = (r & 7) == 0;
+    const bool b8 = kI8 || (EPI == EPI_READY && a.B8 != nullptr);  // uniform
     const int vstride = kLoc ? kVS : a.vstride;
     for (int kr = 0; kr < vstride; kr += 32) {
       const int kk = kr + 8 * lg;
@@ -1725,7 +1821,21 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
       for (int j = 0; j < 4; ++j) {
         const int n = n0 + wn * 64 + 16 * j + lr;
         u32x4 f = u32x4{0, 0, 0, 0};
-        if (n < N) {
+        if (n < N && b8) {
+          const int8_t* br = a.B8 + (size_t)n * r;
+          const float sb = a.sb[n];
+          if (bvec) {
+            if (kk < r) {
+              const u32x2 q = *(const u32x2*)(br + kk);
+              f = i8x8_to_act<DT>(q[0], q[1], sb);
+            }
+          } else {
+            uint32_t h[8];
+#pragma unroll
+            for (int e2 = 0; e2 < 8; ++e2) h[e2] = (kk + e2 < r) ? i8_to_act<DT>(br[kk + e2], sb) : 0u;
+            f = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+          }
+        } else if (n < N) {
           const uint16_t* br = a.B + (size_t)n * r;
           if (bvec) {
             if (kk < r) f = ldg16(br + kk);
@@ -1820,13 +1930,13 @@ hipError_t launch_gate(int dt, const EcParams& e, int ntb, size_t lds, hipStream
   return hipGetLastError();
 }
 
-hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, uint16_t* y, int M, int N,
-                            int r, hipStream_t st) {
+hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, const int8_t* B8,
+                            const float* sb, uint16_t* y, int M, int N, int r, hipStream_t st) {
   const long long total = (long long)M * N;
   const unsigned grid = (unsigned)((total + 255) / 256);
   if (grid == 0) return hipSuccess;
-  SPEAR_DT_SWITCH(dt, hipLaunchKernelGGL(k_ec_up_acc<DTC>, dim3(grid), dim3(256), 0, st, v, B, y,
-                                         M, N, r));
+  SPEAR_DT_SWITCH(dt, hipLaunchKernelGGL(k_ec_up_acc<DTC>, dim3(grid), dim3(256), 0, st, v, B, B8,
+                                         sb, y, M, N, r));
   return hipGetLastError();
 }
 
@@ -1836,7 +1946,8 @@ static hipError_t gemv_launch(int epi, const GemvParams& p, int grid, int block,
   hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, EPI_NONE>, lds)
                    : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, EPI_READY>, lds)
                    : epi == EPI_FUSED ? allow_lds(k_gemv<DT, MT, RT, EPI_FUSED>, lds)
-                                      : allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL>, lds);
+                   : epi == EPI_LOCAL ? allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL>, lds)
+                                      : allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL_I8>, lds);
   if (err != hipSuccess) return err;
   if (epi == EPI_NONE)
     hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_NONE>), dim3(grid), dim3(block), lds, st, p);
@@ -1844,8 +1955,10 @@ static hipError_t gemv_launch(int epi, const GemvParams& p, int grid, int block,
     hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_READY>), dim3(grid), dim3(block), lds, st, p);
   else if (epi == EPI_FUSED)
     hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_FUSED>), dim3(grid), dim3(block), lds, st, p);
-  else
+  else if (epi == EPI_LOCAL)
     hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL>), dim3(grid), dim3(block), lds, st, p);
+  else
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL_I8>), dim3(grid), dim3(block), lds, st, p);
   return hipGetLastError();
 }
 
@@ -1864,7 +1977,9 @@ bool gemv_shape_supported(int MT, int RT) {
 hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, int block,
                        size_t lds, hipStream_t st) {
   // split-K needs its partial sums and row-group counters (workspace)
-  if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.rb_ctr || (epi == EPI_LOCAL && !p.eupart))))
+  const bool loc = epi == EPI_LOCAL || epi == EPI_LOCAL_I8;
+  if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.rb_ctr || (loc && !p.eupart))) ||
+      (epi == EPI_LOCAL_I8 && (!p.ec.A8 || !p.ec.sa || !p.B8 || !p.sb)))
     return hipErrorInvalidValue;
   if (grid == 0) return hipSuccess;
 #define SPEAR_GEMV_CASE(mt, rt)                                                     \
@@ -1878,14 +1993,16 @@ hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int
 
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st) {
   // split-K needs its partial tiles and tile counters (workspace)
-  if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.ctr || (epi == EPI_LOCAL && !p.epart))) ||
-      (p.S != 1 && p.S != 2 && p.S != 4 && p.S != 8))
+  const bool loc = epi == EPI_LOCAL || epi == EPI_LOCAL_I8;
+  if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.ctr || (loc && !p.epart))) ||
+      (p.S != 1 && p.S != 2 && p.S != 4 && p.S != 8) ||
+      (epi == EPI_LOCAL_I8 && (!p.A8 || !p.sa || !p.B8 || !p.sb)))
     return hipErrorInvalidValue;
   const int tm = (p.M + kGemmTM - 1) / kGemmTM, tn = (p.N + kGemmTN - 1) / kGemmTN;
   const unsigned grid = (unsigned)(tm * tn * p.S);
   if (grid == 0) return hipSuccess;
   size_t lds = (size_t)4 * kGemmTM * kGemmLdsRow * 2;
-  if (epi == EPI_LOCAL) lds += (size_t)2 * kGemmEcRows * kGemmLdsRow * 2;
+  if (loc) lds += (size_t)2 * kGemmEcRows * kGemmLdsRow * 2;
   SPEAR_DT_SWITCH(dt, {
     if (epi == EPI_NONE) {
       hipError_t err = allow_lds(k_gemm<DTC, EPI_NONE>, lds);
@@ -1895,6 +2012,10 @@ hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st) {
       hipError_t err = allow_lds(k_gemm<DTC, EPI_LOCAL>, lds);
       if (err != hipSuccess) return err;
       hipLaunchKernelGGL((k_gemm<DTC, EPI_LOCAL>), dim3(grid), dim3(256), lds, st, p);
+    } else if (epi == EPI_LOCAL_I8) {
+      hipError_t err = allow_lds(k_gemm<DTC, EPI_LOCAL_I8>, lds);
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL((k_gemm<DTC, EPI_LOCAL_I8>), dim3(grid), dim3(256), lds, st, p);
     } else {
       hipError_t err = allow_lds(k_gemm<DTC, EPI_READY>, lds);
       if (err != hipSuccess) return err;

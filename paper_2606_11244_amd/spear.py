@@ -47,11 +47,16 @@ class W4(ctypes.Structure):
                 ("zeros", ctypes.c_void_p)]
 
 
+AB_ACT, AB_INT8 = 0, 1
+
+
 class EC(ctypes.Structure):
     _fields_ = [("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("alpha", ctypes.c_float),
                 ("w_g", ctypes.c_void_p), ("b_g", ctypes.c_float),
                 ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
-                ("W2", ctypes.c_void_p), ("b2", ctypes.c_void_p)]
+                ("W2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
+                ("ab_format", ctypes.c_int32), ("a_scale", ctypes.c_void_p),
+                ("b_scale", ctypes.c_void_p)]
 
 
 class Plan(ctypes.Structure):
@@ -165,13 +170,19 @@ def w4_linear(prob: Problem, x, qweight, scales, zeros, y, workspace=None, strea
 
 
 def w4ec_linear(prob: Problem, x, qweight, scales, zeros, A, B, y, *, alpha=1.0, w_g=None,
-                b_g=0.0, W1=None, b1=None, W2=None, b2=None, workspace=None, stream=None):
+                b_g=0.0, W1=None, b1=None, W2=None, b2=None, a_scale=None, b_scale=None,
+                ab_format=None, workspace=None, stream=None):
+    """A and B in the activation dtype, or int8 codes with fp32 per-channel
+    a_scale [r] and b_scale [N] (format SPEAR_AB_INT8, taken when the scales
+    are given unless ab_format says otherwise)."""
     w = W4(_ptr(qweight).value, _ptr(scales).value, _ptr(zeros).value)
 
     def p(t):
         return None if t is None else t.data_ptr()
 
-    ec = EC(p(A), p(B), float(alpha), p(w_g), float(b_g), p(W1), p(b1), p(W2), p(b2))
+    fmt = (AB_INT8 if a_scale is not None else AB_ACT) if ab_format is None else int(ab_format)
+    ec = EC(p(A), p(B), float(alpha), p(w_g), float(b_g), p(W1), p(b1), p(W2), p(b2),
+            fmt, p(a_scale), p(b_scale))
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = LIB.spear_w4ec_linear(ctypes.byref(prob), _ptr(x), ctypes.byref(w), ctypes.byref(ec),
                                _ptr(y), _ptr(workspace), ws_bytes, _stream(stream))
@@ -280,8 +291,16 @@ class DeviceLayer:
         self.scales = torch.from_numpy(layer.scales.view(np.int16)).to(device)
         self.zeros = torch.from_numpy(layer.zeros).to(device)
         self.x = act(layer.x)
-        self.A = act(layer.A) if layer.rank > 0 else None
-        self.B = act(layer.B) if layer.rank > 0 else None
+        self.ab_int8 = bool(getattr(layer, "ab_int8", False)) and layer.rank > 0
+        if self.ab_int8:
+            self.A = torch.from_numpy(np.ascontiguousarray(layer.A_q)).to(device)
+            self.B = torch.from_numpy(np.ascontiguousarray(layer.B_q)).to(device)
+            self.a_scale = torch.from_numpy(np.ascontiguousarray(layer.a_scale)).to(device)
+            self.b_scale = torch.from_numpy(np.ascontiguousarray(layer.b_scale)).to(device)
+        else:
+            self.A = act(layer.A) if layer.rank > 0 else None
+            self.B = act(layer.B) if layer.rank > 0 else None
+            self.a_scale = self.b_scale = None
         self.w_g = act(layer.w_g)
         self.W1, self.b1 = act(layer.W1), act(layer.b1)
         self.W2, self.b2 = act(layer.W2), act(layer.b2)
@@ -299,7 +318,8 @@ class DeviceLayer:
         y = self.y if y is None else y
         return w4ec_linear(prob, self.x, self.qweight, self.scales, self.zeros, self.A, self.B, y,
                            alpha=L.alpha, w_g=self.w_g, b_g=L.b_g, W1=self.W1, b1=self.b1,
-                           W2=self.W2, b2=self.b2, workspace=workspace, stream=stream)
+                           W2=self.W2, b2=self.b2, a_scale=self.a_scale, b_scale=self.b_scale,
+                           workspace=workspace, stream=stream)
 
     def run_w4(self, prob, workspace, stream=None, y=None):
         y = self.y if y is None else y

@@ -137,10 +137,29 @@ class Layer:
     b1: np.ndarray           # [h]
     W2: np.ndarray           # [r][h]
     b2: np.ndarray           # [r]
+    # INT8 per-channel symmetric copies of A and B (make_layer(ab_int8=True))
+    ab_int8: bool = False
+    A_q: np.ndarray = None   # int8 [r][K]
+    a_scale: np.ndarray = None  # fp32 [r]
+    B_q: np.ndarray = None   # int8 [N][r]
+    b_scale: np.ndarray = None  # fp32 [N]
 
     @property
     def gate_hidden(self) -> int:
         return int(self.W1.shape[0])
+
+
+def quantize_int8_rows(w: np.ndarray):
+    """Symmetric per-row INT8 quantisation of w[R][C] (the stand-in for the
+    post-calibration step that stores the EC factors in INT8):
+      s = fp32(max |row| / 127)   (1 for an all-zero row)
+      q = clip(rne(row / s), -127, 127)
+    Returns (q int8 [R][C], s fp32 [R])."""
+    w = np.asarray(w, dtype=np.float32)
+    amax = np.abs(w).max(axis=1) if w.shape[1] else np.zeros(w.shape[0], np.float32)
+    s = np.where(amax > 0, amax / np.float32(127.0), np.float32(1.0)).astype(np.float32)
+    q = np.clip(np.rint(w / s[:, None]), -127, 127).astype(np.int8)
+    return q, s
 
 
 def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
@@ -149,7 +168,7 @@ def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
                w_std: float = 0.02, x_std: float = 1.0, ec_std: float = 0.01,
                wg_std: float = 0.05, b_g: float = 0.0, alpha: float = 1.0,
                outlier_frac: float = 0.0, outlier_scale: float = 20.0,
-               gate_hidden: int = 0) -> Layer:
+               gate_hidden: int = 0, ab_int8: bool = False) -> Layer:
     """Draw one layer from the seed tree SeedSequence([seed, config_id, module_id]).
 
     Draw order: W (fp32) -> RTN -> X (with outlier channels) -> A, B -> w_g ->
@@ -177,13 +196,18 @@ def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
     W2 = rng.normal(0.0, 1.0 / np.sqrt(max(h, 1)), size=(rank, h)).astype(np.float32)
     b1 = np.zeros((h,), np.float32)
     b2 = np.zeros((rank,), np.float32)
+    i8 = {}
+    if ab_int8:
+        A_q, a_scale = quantize_int8_rows(A)
+        B_q, b_scale = quantize_int8_rows(B)
+        i8 = dict(ab_int8=True, A_q=A_q, a_scale=a_scale, B_q=B_q, b_scale=b_scale)
     return Layer(M=M, N=N, K=K, group_size=g, act_dtype=act_dtype, rank=rank,
                  gate_kind=gate_kind, qweight=pack_int4(q), scales=s, zeros=z,
                  x=to_bits(x, act_dtype), A=to_bits(A, act_dtype),
                  B=to_bits(B, act_dtype), w_g=to_bits(w_g, act_dtype),
                  b_g=float(b_g), alpha=float(alpha),
                  W1=to_bits(W1, act_dtype), b1=to_bits(b1, act_dtype),
-                 W2=to_bits(W2, act_dtype), b2=to_bits(b2, act_dtype))
+                 W2=to_bits(W2, act_dtype), b2=to_bits(b2, act_dtype), **i8)
 
 
 # ---------------------------------------------------------------------------
@@ -223,8 +247,10 @@ CONFIGS = {
 
 
 def config_layer(config_id: int, module: str, M: int, seed: int = 0,
-                 gate_kind: int = GATE_SIGMOID_LINEAR, rank: int | None = None) -> Layer:
-    """One module of a workload configuration at token count M."""
+                 gate_kind: int = GATE_SIGMOID_LINEAR, rank: int | None = None,
+                 ab_int8: bool = False) -> Layer:
+    """One module of a workload configuration at token count M (ab_int8:
+    with INT8 per-channel copies of the EC factors)."""
     c = CONFIGS[config_id]
     K, N = c["shapes"][module]
     mod_id = list(c["shapes"]).index(module)
@@ -232,7 +258,7 @@ def config_layer(config_id: int, module: str, M: int, seed: int = 0,
                       rank=c["rank"] if rank is None else rank,
                       act_dtype=c["act_dtype"], gate_kind=gate_kind, seed=seed,
                       config_id=config_id, module_id=mod_id,
-                      outlier_frac=c["outlier_frac"])
+                      outlier_frac=c["outlier_frac"], ab_int8=ab_int8)
 
 
 def ec_selection_70b(seed: int = 0, layers: int = 80, fraction: float = 0.25) -> np.ndarray:

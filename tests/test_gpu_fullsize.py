@@ -28,14 +28,16 @@ def _rows(N, k=48, seed=0):
     return np.unique(np.concatenate([[0, N - 1], rng.choice(N, size=min(k, N), replace=False)]))
 
 
-def _check(cid, module, Ms, seed=0, rank=None, paths=(0,)):
-    base = S.config_layer(cid, module, max(Ms), seed=seed, rank=rank)
+def _check(cid, module, Ms, seed=0, rank=None, paths=(0,), ab_int8=False):
+    base = S.config_layer(cid, module, max(Ms), seed=seed, rank=rank, ab_int8=ab_int8)
     rows = _rows(base.N, seed=seed)
     for M in Ms:
-        L = S.config_layer(cid, module, M, seed=seed, rank=rank) if M != max(Ms) else base
+        L = (S.config_layer(cid, module, M, seed=seed, rank=rank, ab_int8=ab_int8)
+             if M != max(Ms) else base)
         ref = O.w4ec_linear_rows(L, rows)
         for p in paths:
-            log(f"full-size config={cid} module={module} M={M} rank={L.rank} path={p}")
+            log(f"full-size config={cid} module={module} M={M} rank={L.rank} path={p} "
+                f"int8={ab_int8}")
             y = gpu_y(L, p)
             assert np.all(np.isfinite(y))
             assert_parity(y[:, rows], ref, f"c{cid}/{module}/M={M}/path={p}")
@@ -68,3 +70,11 @@ def test_llama70b_modules(module, Ms):
 def test_llama1b_more_seeds(seed):
     _check(1, "o", (1, 16), seed=seed, paths=(0, 3, 4))
     _check(2, "up", (2048,), seed=seed)
+
+
+@pytest.mark.parametrize("cid,module,Ms", [(1, "q", (1, 16)), (1, "down", (1,)),
+                                           (2, "gate", (512, 4096)), (3, "q", (1, 128)),
+                                           (4, "down", (1, 64))])
+def test_int8_factors_full_size(cid, module, Ms):
+    """INT8 per-channel EC factors at the workload sizes, automatic dispatch."""
+    _check(cid, module, Ms, ab_int8=True)

@@ -356,3 +356,50 @@ def test_gemm_split_k(slices, M):
         assert_parity(gpu_y(L, 0, with_ec=False), O.w4_linear_layer(L), f"slices={slices} w4")
     finally:
         sp.set_gemm_slices(0)
+
+
+# ---------------------------------------------------------------------------
+# INT8 per-channel symmetric EC factors (the deployed format)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("M,N,K,G,rank,dt,gate", [
+    (1, 520, 1024, 128, 16, S.F16, S.GATE_SIGMOID_LINEAR),
+    (4, 256, 2048, 0, 8, S.BF16, S.GATE_SIGMOID_LINEAR),
+    (17, 200, 1024, 128, 16, S.F16, S.GATE_ONE),
+    (3, 256, 1024, 128, 32, S.F16, S.GATE_TANH_MLP),
+    (40, 136, 512, 128, 24, S.BF16, S.GATE_SIGMOID_LINEAR),
+    (65, 200, 1024, 128, 16, S.F16, S.GATE_SIGMOID_LINEAR),
+    (300, 520, 2048, 0, 16, S.BF16, S.GATE_SIGMOID_LINEAR),
+    (130, 256, 1024, 128, 24, S.F16, S.GATE_TANH_MLP),
+])
+def test_int8_factors_all_paths(M, N, K, G, rank, dt, gate):
+    """INT8 A and B with fp32 per-channel scales on every path that takes
+    the shape: the codes are dequantised in the kernels (to the activation
+    dtype where they feed an MFMA, exactly where the sum is fp32) and the
+    result meets the bar against the oracle's exact s * q factors. The EC
+    term is made large (ec_std 0.05) so that a wrong scale cannot hide."""
+    L = S.make_layer(M=M, N=N, K=K, group_size=G, rank=rank, act_dtype=dt, gate_kind=gate,
+                     seed=M + N + rank, ec_std=0.05, ab_int8=True)
+    ref = O.w4ec_linear(L)
+    base = O.w4_linear_layer(L)
+    # the EC term is a sizeable part of the output
+    assert np.linalg.norm(ref - base) > 0.1 * np.linalg.norm(ref)
+    for p in _paths_for(M, L):
+        log(f"int8 M={M} N={N} K={K} G={G} r={rank} dt={dt} gate={gate} path={p}")
+        assert_parity(gpu_y(L, p), ref, f"int8 path={p}")
+
+
+def test_int8_factors_split_fused_gemm():
+    """The fully fused prefill GEMM with INT8 factors and K split into 2, 4
+    and 8 slices."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=130, N=200, K=2048, group_size=128, rank=16, seed=5, ec_std=0.05,
+                     ab_int8=True)
+    ref = O.w4ec_linear(L)
+    try:
+        for slices in (1, 2, 4, 8):
+            sp.set_gemm_slices(slices)
+            log(f"int8 fused gemm slices={slices}")
+            assert_parity(gpu_y(L, PATHS["fused_mfma"]), ref, f"int8 slices={slices}")
+    finally:
+        sp.set_gemm_slices(0)

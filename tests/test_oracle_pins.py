@@ -368,11 +368,87 @@ def check_dequant_bits_contract(o, seed=0) -> bool:
     return True
 
 
+def _brute_int8(layer):
+    """Scalar exact-rational evaluation of Eq. 3 with INT8 factors taken from
+    the raw codes: A[j][k] = a_scale[j] q_A[j][k], B[n][j] = b_scale[n] q_B[n][j]
+    (gate ONE or SIGMOID, the sigmoid in float64)."""
+    dt = layer.act_dtype
+    M, N, K, r = layer.M, layer.N, layer.K, layer.rank
+    G = layer.group_size
+    xs = S.from_bits(layer.x, dt)
+    wg = S.from_bits(layer.w_g, dt)
+    sc = layer.scales.view(np.float16)
+    A = [[Fraction(float(layer.a_scale[j])) * int(layer.A_q[j][k]) for k in range(K)]
+         for j in range(r)]
+    B = [[Fraction(float(layer.b_scale[n])) * int(layer.B_q[n][j]) for j in range(r)]
+         for n in range(N)]
+    Y = [[None] * N for _ in range(M)]
+    for m in range(M):
+        u = [sum(Fraction(float(xs[m][k])) * A[j][k] for k in range(K)) for j in range(r)]
+        if layer.gate_kind == S.GATE_ONE:
+            g = Fraction(1)
+        else:
+            t = sum(Fraction(float(xs[m][k])) * Fraction(float(wg[k])) for k in range(K))
+            t = float(t) + layer.b_g
+            g = Fraction(1.0 / (1.0 + math.exp(-t)) if t >= 0 else math.exp(t) / (1 + math.exp(t)))
+        for n in range(N):
+            acc = Fraction(0)
+            for k in range(K):
+                word = int(layer.qweight[n][k // 8])
+                code = (word >> (4 * (k % 8))) & 15
+                acc += (Fraction(code - int(layer.zeros[n][k // G])) *
+                        Fraction(float(sc[n][k // G])) * Fraction(float(xs[m][k])))
+            Y[m][n] = acc + Fraction(layer.alpha) * g * sum(B[n][j] * u[j] for j in range(r))
+    return Y
+
+
+def check_int8_brute_force(o, seed=0) -> bool:
+    """INT8 per-channel factors: the oracle against exact rationals built
+    from the codes and scales, on tiny layers of both dtypes."""
+    cases = [dict(M=2, N=5, K=16, group_size=8, rank=3, gate_kind=S.GATE_ONE, alpha=0.75),
+             dict(M=3, N=4, K=24, group_size=24, rank=2, gate_kind=S.GATE_SIGMOID_LINEAR, alpha=1.0),
+             dict(M=1, N=6, K=16, group_size=16, rank=4, gate_kind=S.GATE_SIGMOID_LINEAR, alpha=2.0)]
+    for i, c in enumerate(cases):
+        for dt in (S.F16, S.BF16):
+            layer = S.make_layer(seed=seed + 40 + i, act_dtype=dt, ec_std=0.3, wg_std=0.4,
+                                 b_g=0.1, ab_int8=True, **c)
+            want = _brute_int8(layer)
+            got = o.w4ec_linear(layer)
+            rows = np.arange(layer.N)[::2]
+            got_rows = o.w4ec_linear_rows(layer, rows)
+            for m in range(layer.M):
+                for n in range(layer.N):
+                    wv = float(want[m][n])
+                    if abs(got[m][n] - wv) > 1e-12 * max(1.0, abs(wv)):
+                        return False
+                for i2, n in enumerate(rows):
+                    wv = float(want[m][n])
+                    if abs(got_rows[m][i2] - wv) > 1e-12 * max(1.0, abs(wv)):
+                        return False
+    return True
+
+
+def check_int8_golden(o) -> bool:
+    """Hand-worked INT8 factors (tests/golden/int8_factors.json)."""
+    g = _load("int8_factors.json")
+    d = g["dequant"]
+    if not np.array_equal(o.dequant_int8(np.array(d["q"], np.int8), np.array(d["scale"], np.float32)),
+                          np.array(d["want"])):
+        return False
+    e = g["ec"]
+    A = o.dequant_int8(np.array(e["A_q"], np.int8), np.array(e["a_scale"], np.float32))
+    B = o.dequant_int8(np.array(e["B_q"], np.int8), np.array(e["b_scale"], np.float32))
+    x = np.array(e["x"])
+    y = o.w4ec_linear_f64(x, np.zeros((B.shape[0], x.shape[1])), A, B, 1.0, o.GATE_ONE)
+    return np.array_equal(y, np.array(e["want"]))
+
+
 PINS = [check_unpack_fixed_words, check_unpack_exhaustive, check_golden_examples,
         check_rounding_fixtures, check_rtn_grid_roundtrip, check_rtn_error_bound,
         check_brute_force, check_integer_grid_exact, check_reductions,
         check_sigmoid_half, check_tanh_static_lora, check_factored_form,
-        check_gate_ranges, check_dequant_bits_contract]
+        check_gate_ranges, check_dequant_bits_contract, check_int8_brute_force,
+        check_int8_golden]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -464,6 +540,15 @@ def _w4_linear_transposed_b(x, W_hat):
     return x @ W.T
 
 
+def _int8_scale_dropped(q, scale):
+    return np.asarray(q, np.float64)
+
+
+def _int8_scale_fp16(q, scale):
+    s16 = np.asarray(scale, np.float32).astype(np.float16).astype(np.float64)
+    return s16[:, None] * np.asarray(q, np.float64)
+
+
 MUTANTS = {
     "nibble order reversed": dict(unpack_int4=_unpack_reversed),
     "zero point added": dict(dequant=_dequant_plus_zero),
@@ -475,6 +560,8 @@ MUTANTS = {
     "sigmoid argument negated": dict(gate_sigmoid_linear=_sigmoid_of_wrong_sign),
     "bf16 rounding truncates": dict(round_f64_to_bits=_round_bf16_truncate),
     "weight operand not transposed": dict(w4_linear=_w4_linear_transposed_b),
+    "INT8 scale dropped": dict(dequant_int8=_int8_scale_dropped),
+    "INT8 scale rounded to fp16": dict(dequant_int8=_int8_scale_fp16),
 }
 
 
