@@ -46,10 +46,12 @@ RANK = 16
 GROUP = 128
 
 
-def algo_bytes(M, N, K, G, r):
+def algo_bytes(M, N, K, G, r, ab_int8=False):
     """Algorithmic HBM bytes of one W4+EC call: codes (N K / 2), scales and
-    4-bit zeros (2.5 N K / G), A, B, w_g, X and Y in fp16."""
-    return N * K / 2 + 2.5 * N * K / G + 2 * r * K + 2 * N * r + (2 * K if r else 0) + 2 * M * K + 2 * M * N
+    4-bit zeros (2.5 N K / G), A, B, w_g, X and Y in fp16 (A and B as int8
+    codes plus fp32 per-channel scales with ab_int8)."""
+    ab = (r * K + N * r + 4 * (r + N)) if ab_int8 else (2 * r * K + 2 * N * r)
+    return N * K / 2 + 2.5 * N * K / G + (ab if r else 0) + (2 * K if r else 0) + 2 * M * K + 2 * M * N
 
 
 def algo_flops(M, N, K, r):
@@ -189,6 +191,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overhead", action="store_true", help="skip the W4-only reference passes")
     ap.add_argument("--no-70b", action="store_true", help="skip the 70B-layer context line")
+    ap.add_argument("--no-int8", action="store_true",
+                    help="skip the passes with INT8 per-channel EC factors")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -320,6 +324,58 @@ def main():
             "decode_ec_byte_share": round(dec_bytes / dec_bytes_w4 - 1.0, 4),
         }
 
+    # ---- the same passes with the EC factors in INT8 (per-channel symmetric,
+    # fp32 scales): same 4-bit weights, activations and gate; A and B swapped
+    int8 = None
+    if not args.no_int8:
+        print("bench: INT8-factor passes", file=sys.stderr, flush=True)
+        dec_i8 = [sp.DeviceLayer(S.config_layer(1, m, 1, seed=0, ab_int8=True), device=dev)
+                  for m in S.MODULES]
+        pre_i8 = [sp.DeviceLayer(S.config_layer(2, m, 4096, seed=0, ab_int8=True), device=dev)
+                  for m in S.MODULES]
+
+        def swap(d, src):
+            e = sp.DeviceLayer.__new__(sp.DeviceLayer)
+            e.__dict__.update(d.__dict__)
+            e.layer, e.ab_int8 = src.layer, True
+            e.A, e.B = src.A.clone(), src.B.clone()
+            e.a_scale, e.b_scale = src.a_scale.clone(), src.b_scale.clone()
+            return e
+
+        dec_dev_i8 = [[[swap(d, dec_i8[j]) for j, d in enumerate(mods)] for mods in per_copy]
+                      for per_copy in dec_dev]
+        pre_dev_i8 = [swap(d, pre_i8[j]) for j, d in enumerate(pre_dev)]
+
+        def decode_pass_i8(c):
+            for mods in dec_dev_i8[c]:
+                for d in mods:
+                    d.run_ec(d.problem(), dec_ws_t)
+
+        def prefill_pass_i8():
+            for d in pre_dev_i8:
+                d.run_ec(d.problem(), pre_ws_t)
+
+        g_dec_i8 = [capture(lambda c=c: decode_pass_i8(c)) for c in range(args.copies)]
+        g_pre_i8 = capture(prefill_pass_i8)
+        run_steps(args.warmup, g_dec_i8, g_pre_i8, False)
+        ev8 = run_steps(args.steps, g_dec_i8, g_pre_i8, True)
+        torch.cuda.synchronize()
+        d8 = float(np.mean([a.elapsed_time(b) for a, b, _ in ev8])) * 1e-3
+        p8 = float(np.mean([b.elapsed_time(c) for _, b, c in ev8])) * 1e-3
+        dec_bytes_i8 = LAYERS_1B * sum(algo_bytes(1, L.N, L.K, L.group_size, L.rank, True)
+                                       for L in dec_base)
+        int8 = {
+            "format": "A, B int8 per-channel symmetric, fp32 scales; gate fp16",
+            "decode_ms_per_pass": round(d8 * 1e3, 4),
+            "decode_GBps": round(dec_bytes_i8 / d8 / 1e9, 2),
+            "prefill_ms_per_pass": round(p8 * 1e3, 4),
+            "prefill_TFLOPs": round(pre_flops / p8 / 1e12, 2),
+        }
+        if overhead is not None:
+            int8["decode_overhead"] = round(d8 / d4 - 1.0, 4)
+            int8["prefill_overhead"] = round(p8 / p4 - 1.0, 4)
+            int8["decode_ec_byte_share"] = round(dec_bytes_i8 / dec_bytes_w4 - 1.0, 4)
+
     ctx70 = None
     if not args.no_70b:
         print("bench: 70B-layer decode context", file=sys.stderr, flush=True)
@@ -382,6 +438,7 @@ def main():
         "decode_ms_per_pass": round(dec_s * 1e3, 4),
         "decode_70b_layer": ctx70,
         "ec_overhead": overhead,
+        "ec_int8": int8,
     }
     if not args.no_cpu_baseline:
         print("bench: CPU oracle baseline", file=sys.stderr, flush=True)

@@ -502,7 +502,9 @@ GemvParams make_gemv(const spear_problem_t* p, const Resolved& z, const void* x,
   g.wait_polls = g_wait_polls.load();
   g.xlds = z.xlds;
   g.xstride = z.xstride;
-  g.bpre = ec && !ab_int8(ec) ? z.bpre : 0;  // B rows are staged in LDS as act dtype only
+  // B rows are staged in LDS as act dtype, or as INT8 codes and scales by
+  // the local variant (the EC wave reads INT8 B from memory)
+  g.bpre = ec && (!ab_int8(ec) || z.plan.path == SPEAR_PATH_FUSED_LOCAL) ? z.bpre : 0;
   g.lds_y = z.lds_y;
   g.lds_e = z.lds_e;
   g.lds_b = z.lds_b;

@@ -142,6 +142,29 @@ template <int DT>
 __device__ __forceinline__ uint16_t i8_to_act(int8_t q, float s) {
   return f2act<DT>((float)q * s);
 }
+// Eight INT8 codes as exact activation-dtype integers (|q| <= 127 is exact
+// in both), for kernels that apply the scale to the fp32 result instead.
+// fp16: the byte q + 128 is placed under the exponent of 1024 (0x64 high
+// byte gives 1024 + b exactly) and 1152 is subtracted; bf16: through fp32.
+template <int DT>
+__device__ __forceinline__ u32x4 i8x8_exact(uint32_t w0, uint32_t w1) {
+  if constexpr (DT == DT_F16) {
+    const uint32_t b0 = w0 ^ 0x80808080u, b1 = w1 ^ 0x80808080u;
+    const f16x2 off = f16x2{(_Float16)-1152.f, (_Float16)-1152.f};
+    auto pr = [&](uint32_t b, uint32_t sel) {
+      return __builtin_bit_cast(uint32_t,
+                                __builtin_bit_cast(f16x2, __builtin_amdgcn_perm(0x64646464u, b, sel)) + off);
+    };
+    return u32x4{pr(b0, 0x04010400u), pr(b0, 0x04030402u), pr(b1, 0x04010400u), pr(b1, 0x04030402u)};
+  } else {
+    auto pr = [&](uint32_t w, int p) {
+      const float a0 = (float)((int)(w << (24 - 16 * p)) >> 24);
+      const float a1 = (float)((int)(w << (16 - 16 * p)) >> 24);
+      return (__float_as_uint(a0) >> 16) | (__float_as_uint(a1) & 0xFFFF0000u);
+    };
+    return u32x4{pr(w0, 0), pr(w0, 1), pr(w1, 0), pr(w1, 1)};
+  }
+}
 
 // Raw buffer loads through a bounds-checked resource (gfx9 descriptor word 3
 // = 0x00020000): a byte offset at or past `bytes` reads as zero. Masked
@@ -980,21 +1003,27 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
   const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
   const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
-  const rsrc_t rb = make_rsrc(a.B, (uint32_t)N * r * 2);
+  const rsrc_t rb = kI8 ? make_rsrc(a.B8, (uint32_t)N * r) : make_rsrc(a.B, (uint32_t)N * r * 2);
 
   // the rows of B ([RB][r], contiguous) of the block that adds v B^T (the
   // first K-slice's with an EC wave; any slice's in EPI_LOCAL, whose last
   // arriver adds it) are fetched up front into LDS when two 16-byte chunks
   // per thread cover them
+  // (INT8 B: the codes, 16 per chunk, and then the rows' fp32 scales)
   constexpr int BCH = 2;
   const bool bpre = ((kEC && s == 0) || kLoc) && a.bpre;
-  const int bchunks = RB * r / 8;
+  const int bchunks = kI8 ? RB * r / 16 : RB * r / 8;
   u32x4 bst[BCH];
+  uint32_t sbst = 0;
   if (bpre) {
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
       const int ci = tid + c * (int)blockDim.x;
-      bst[c] = bld128(rb, ci < bchunks ? (uint32_t)n0 * r * 2 + 16u * ci : kOOB);
+      bst[c] = bld128(rb, ci < bchunks ? (uint32_t)n0 * r * (kI8 ? 1 : 2) + 16u * ci : kOOB);
+    }
+    if constexpr (kI8) {
+      const rsrc_t rsb = make_rsrc(a.sb, (uint32_t)N * 4);
+      sbst = __builtin_amdgcn_raw_buffer_load_b32(rsb, tid < RB ? (uint32_t)(n0 + tid) * 4 : kOOB, 0, 0);
     }
   }
 
@@ -1025,14 +1054,22 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   // MFMA lane layout straight from memory, every load would touch 32 cache
   // lines. The MFMAs then take A's rows (lane lr: row lr) and w_g in every
   // column as two further B operands.
-  // INT8 A: eight codes (8 bytes) per chunk, dequantised with the row's
-  // scale when stored; the scales of A's rows sit in lanes 0..15
+  // INT8 A: eight codes (8 bytes) per chunk, staged as exact integers; the
+  // rows' scales multiply the fp32 projection sums instead. The thread that
+  // reduces column c of the projection tiles always has c = (lane / 4) % 16
+  // (the block is a whole number of waves), so it holds that row's scale.
   const rsrc_t ra = kI8 ? make_rsrc(a.ec.A8, (uint32_t)r * K)
                         : make_rsrc(kLoc ? a.ec.A : nullptr, kLoc ? (uint32_t)r * K * 2 : 0u);
   const rsrc_t rgw = make_rsrc(kLoc ? a.ec.wg : nullptr,
                                kLoc && a.ec.gate == GATE_SIGMOID ? (uint32_t)K * 2 : 0u);
-  float sa_lane = 0.f;
-  if constexpr (kI8) sa_lane = (lane & 15) < r ? a.ec.sa[lane & 15] : 0.f;
+  // (a buffer load: a flat load would also hold the LDS counter the
+  // prologue's barriers wait on)
+  float sa_c = 1.f;
+  if constexpr (kI8) {
+    const rsrc_t rsa = make_rsrc(a.ec.sa, (uint32_t)r * 4);
+    sa_c = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+        rsa, ((lane >> 2) & 15) < r ? (uint32_t)((lane >> 2) & 15) * 4 : kOOB, 0, 0));
+  }
   const int acpr = (it_end - it_blk) * (kIterK / 8);  // 16-byte chunks per row
   const int astride = acpr * 8 + 8;                   // LDS row stride (halves)
   uint16_t* als = (uint16_t*)(smem + a.lds_a);        // [17][astride]
@@ -1056,7 +1093,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
       const int ci = base + u * (int)blockDim.x;
       const int row = ci / acpr, kc = ci - row * acpr;
       u32x4 v = c4[u];
-      if constexpr (kI8) v = i8x8_to_act<DT>(v[0], v[1], __shfl(sa_lane, row & 15));
+      if constexpr (kI8) v = i8x8_exact<DT>(v[0], v[1]);
       if (ci < 16 * acpr) *(u32x4*)(als + row * astride + 8 * kc) = v;
     }
   };
@@ -1213,6 +1250,9 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
       const int ci = tid + c * (int)blockDim.x;
       if (ci < bchunks) *(u32x4*)(bs + 8 * ci) = bst[c];
     }
+    if constexpr (kI8) {
+      if (tid < RB) ((uint32_t*)((char*)bs + RB * r))[tid] = sbst;
+    }
   }
   __syncthreads();
   if (xl && iw_beg < iw_end) {
@@ -1335,6 +1375,9 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
       if (j < 0) continue;
       float v = 0.f;
       for (int w = 0; w < NW; ++w) v += ered[(((w * kLocalTiles + t) * MT + mt) * 64 + ln) * 4 + i];
+      if constexpr (kI8) {
+        if (t == 0) v *= sa_c;  // c == (lane / 4) % 16 here
+      }
       u_loc[tok * R1p + j] = v;
     }
   }
@@ -1422,7 +1465,20 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
         // of B (r is a multiple of 8 when B is staged), independent loads
         const float* vm = v_loc + m * r;
         float ev = 0.f;
-        if (bpre) {
+        if (bpre && kI8) {
+          // INT8 B staged: the codes and the row's scale exactly, in fp32
+          const int8_t* b8row = (const int8_t*)bsl + row * r;
+          for (int j0 = 0; j0 < r; j0 += 8) {
+            const u32x2 q = *(const u32x2*)(b8row + j0);
+            const f32x4 v0 = *(const f32x4*)(vm + j0), v1 = *(const f32x4*)(vm + j0 + 4);
+#pragma unroll
+            for (int e2 = 0; e2 < 4; ++e2) {
+              ev += v0[e2] * (float)((int)(q[0] << (24 - 8 * e2)) >> 24);
+              ev += v1[e2] * (float)((int)(q[1] << (24 - 8 * e2)) >> 24);
+            }
+          }
+          ev *= ((const float*)((const char*)bsl + RB * r))[row];
+        } else if (bpre) {
           for (int j0 = 0; j0 < r; j0 += 8) {
             const u32x4 b8 = *(const u32x4*)(bsl + row * r + j0);
             const f32x4 v0 = *(const f32x4*)(vm + j0), v1 = *(const f32x4*)(vm + j0 + 4);
@@ -1606,7 +1662,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   const rsrc_t rgw = make_rsrc(kLoc ? a.wg : nullptr,
                                kLoc && a.gate == GATE_SIGMOID ? (uint32_t)K * 2 : 0u);
   const uint32_t eoff = er < 16 && er < a.r ? ((uint32_t)er * K + 8 * ec8) * 2 : kOOB;
-  const float sa_er = kI8 && er < 16 && er < a.r ? a.sa[er] : 0.f;
+  float sa_er = 0.f;
+  if constexpr (kI8) {
+    const rsrc_t rsa = make_rsrc(a.sa, (uint32_t)a.r * 4);
+    sa_er = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+        rsa, er < 16 && er < a.r ? (uint32_t)er * 4 : kOOB, 0, 0));
+  }
   const uint32_t goff = er == 16 ? 16u * ec8 : kOOB;
 
   // two register sets of global loads, so that the loads of step kt+2 are
