@@ -29,8 +29,8 @@ PATHS = [("fused_local", 5), ("fused_gemv", 1), ("fused_mfma", 2), ("unfused_2k"
 
 # (configuration id, module, token counts)
 DEFAULT_CASES = [
-    (1, "q", [1, 4, 16, 32, 64]), (1, "k", [1, 16, 64]), (1, "gate", [1, 16, 32, 64]),
-    (1, "down", [1, 16, 64]),
+    (1, "q", [1, 4, 16, 32, 48, 64]), (1, "k", [1, 16, 32, 64]), (1, "gate", [1, 16, 32, 48, 64]),
+    (1, "down", [1, 16, 32, 64]),
     (2, "q", [128, 256, 512, 1024, 2048, 4096]), (2, "k", [128, 512, 4096]),
     (2, "gate", [128, 512, 2048, 4096]), (2, "down", [512, 4096]),
     (3, "q", [1, 8, 32, 128, 512]), (3, "down", [1, 8, 32, 512]),
@@ -151,6 +151,15 @@ def main(argv=None):
             ws = torch.zeros(max(ws_size, auto.workspace_bytes, 256), dtype=torch.uint8,
                              device="cuda")
             row["w4_us"] = round(timed(lambda c: devs[c].run_w4(p4, ws), copies, args.reps), 2)
+            # the 4-bit product on the other kernel where both apply
+            if M <= 64:
+                pg, pv = base.problem(force_path=4), base.problem(force_path=1)
+                ws_g = max(sp.dispatch_plan(pg, with_ec=False).workspace_bytes,
+                           sp.dispatch_plan(pv, with_ec=False).workspace_bytes)
+                if ws_g > ws.numel():
+                    ws = torch.zeros(ws_g, dtype=torch.uint8, device="cuda")
+                row["w4_gemv_us"] = round(timed(lambda c: devs[c].run_w4(pv, ws), copies, args.reps), 2)
+                row["w4_gemm_us"] = round(timed(lambda c: devs[c].run_w4(pg, ws), copies, args.reps), 2)
             for name, code in PATHS:
                 if name not in plans:
                     continue
@@ -166,6 +175,12 @@ def main(argv=None):
             torch.cuda.empty_cache()
 
     names = [n for n, _ in PATHS]
+    w4k = [r for r in rows if "w4_gemm_us" in r]
+    lines_w4 = ["", "## The 4-bit product alone at up to 64 tokens: GEMV vs GEMM", "",
+                "| config | module | M | GEMV | GEMM | AUTO |", "|---|---|---|---|---|---|"]
+    for r in w4k:
+        lines_w4.append(f"| {r['config']} | {r['module']} | {r['M']} | {r['w4_gemv_us']} | "
+                        f"{r['w4_gemm_us']} | {r['w4_us']} |")
     lines = ["# Dispatch crossover: W4+EC paths by token count", "",
              "Command (from the repository root): `python -m paper_2606_11244_amd.crossover "
              f"--out {args.out}`", "",
@@ -182,7 +197,7 @@ def main(argv=None):
         lines.append(f"| {r['config']} | {r['module']} | {r['N']} | {r['K']} | {r['rank']} | "
                      f"{r['M']} | {r['w4_us']} | " + " | ".join(cells) +
                      f" | {r['best']} | {auto_mark} | {best_t / r['w4_us'] - 1:.1%} |")
-    lines += ["", "(*) AUTO differs from the fastest measured path.", ""]
+    lines += ["", "(*) AUTO differs from the fastest measured path."] + lines_w4 + [""]
     with open(args.out, "w") as f:
         f.write("\n".join(lines))
     print(f"wrote {args.out}", file=sys.stderr)

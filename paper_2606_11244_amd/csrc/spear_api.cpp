@@ -23,7 +23,8 @@ std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0};
 // Token counts at or below this run the 4-bit product as a split-K GEMV; above
 // it the LDS-tiled MFMA GEMM. The same bound separates decode (fully fused
 // EC) from prefill (semi-fused EC pre-kernel) under SPEAR_PATH_AUTO.
-constexpr int64_t kGemvMaxM = 64;
+constexpr int64_t kGemvMaxM = 64;      // the GEMV kernels take up to this many tokens
+constexpr int64_t kAutoGemvMaxM = 32;  // AUTO: GEMV kernels up to here, GEMM kernels above
 constexpr int64_t kLocalMaxM = 32;   // local EC variant: at most two token tiles
 constexpr size_t kLocalRestageMax = 24u << 20;  // local EC: A and w_g staged per call
 // Largest staged slice of x in a GEMV block's LDS (16 tokens x 2048 K fit).
@@ -143,12 +144,28 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   // kernel's fixed cost then outweighs the projection the N-tiles repeat
   const bool few_tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN) <= 256;
   if (path == SPEAR_PATH_AUTO || !z.ec)
-    path = M > kGemvMaxM ? (mfma_ok && few_tiles ? SPEAR_PATH_FUSED_MFMA : SPEAR_PATH_UNFUSED_2K)
-           : local_ok    ? SPEAR_PATH_FUSED_LOCAL
-                         : SPEAR_PATH_FUSED_GEMV;
-  if (!with_ec) path = (M <= kGemvMaxM) ? SPEAR_PATH_FUSED_GEMV : SPEAR_PATH_UNFUSED_2K;
+    path = M > kAutoGemvMaxM ? (mfma_ok && few_tiles ? SPEAR_PATH_FUSED_MFMA : SPEAR_PATH_UNFUSED_2K)
+           : local_ok        ? SPEAR_PATH_FUSED_LOCAL
+                             : SPEAR_PATH_FUSED_GEMV;
+  if (!with_ec) {
+    // the 4-bit product alone: the GEMV up to kAutoGemvMaxM tokens, the
+    // GEMM above; force_path picks the kernel (GEMV paths: the GEMV, up to
+    // kGemvMaxM tokens; GEMM paths: the GEMM)
+    const int fp = p->force_path;
+    const bool want_gemv = fp == SPEAR_PATH_FUSED_GEMV || fp == SPEAR_PATH_FUSED_LOCAL;
+    const bool want_gemm = fp == SPEAR_PATH_FUSED_MFMA || fp == SPEAR_PATH_UNFUSED_2K ||
+                           fp == SPEAR_PATH_UNFUSED_CHAIN;
+    if (want_gemv && M > kGemvMaxM) return SPEAR_E_UNSUPPORTED;
+    path = want_gemv ? SPEAR_PATH_FUSED_GEMV
+           : want_gemm ? SPEAR_PATH_UNFUSED_2K
+           : M <= kAutoGemvMaxM ? SPEAR_PATH_FUSED_GEMV : SPEAR_PATH_UNFUSED_2K;
+  }
   const bool fmfma = z.ec && path == SPEAR_PATH_FUSED_MFMA;
-  z.gemv = M <= kGemvMaxM && !fmfma;
+  // the GEMV for the GEMV paths, and under the 4-bit product of the
+  // two-kernel and chain paths up to kAutoGemvMaxM tokens (the GEMM above)
+  z.gemv = !with_ec ? path == SPEAR_PATH_FUSED_GEMV
+           : path == SPEAR_PATH_FUSED_GEMV || path == SPEAR_PATH_FUSED_LOCAL ||
+                 (!fmfma && M <= kAutoGemvMaxM);
   z.plan.path = path;
 
   if (M == 0 || N == 0) {

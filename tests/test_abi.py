@@ -80,9 +80,21 @@ def test_plan_phase_aware_dispatch():
         assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
         p = _plan(M=M, gate_kind=sp.GATE_TANH_MLP)
         assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
+    # above 32 tokens the GEMM kernels: the fully fused one where it applies,
+    # the two-kernel path on the GEMM otherwise
     for M in (33, 64):
         p = _plan(M=M)
-        assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
+        assert p.path == sp.PATH_FUSED_MFMA and p.num_launches == 1, M
+        p = _plan(M=M, rank=32)
+        assert p.path == sp.PATH_UNFUSED_2K and p.tile_n == 128, M
+    # the 4-bit product alone: GEMV up to 32 tokens, GEMM above; force_path
+    # picks either kernel
+    assert _plan(M=32, with_ec=False).path == sp.PATH_FUSED_GEMV
+    assert _plan(M=33, with_ec=False).path == sp.PATH_UNFUSED_2K
+    assert _plan(M=4, with_ec=False, force_path=sp.PATH_UNFUSED_2K).tile_n == 128
+    assert _plan(M=64, with_ec=False, force_path=sp.PATH_FUSED_GEMV).path == sp.PATH_FUSED_GEMV
+    with pytest.raises(sp.SpearError):
+        _plan(M=65, with_ec=False, force_path=sp.PATH_FUSED_GEMV)
     assert _plan(M=4, force_path=sp.PATH_FUSED_GEMV).path == sp.PATH_FUSED_GEMV
     for M in (1, 64, 4096):
         p = _plan(M=M, force_path=sp.PATH_FUSED_MFMA)
