@@ -244,7 +244,6 @@ def main():
     pre_flops = sum(algo_flops(L.M, L.N, L.K, L.rank) for L in pre_base)
     pre_flops_w4 = sum(algo_flops(L.M, L.N, L.K, 0) for L in pre_base)
     dec_plan = sp.dispatch_plan(base_dev[0].problem())
-    pre_plan = sp.dispatch_plan(pre_dev[0].problem())
 
     def decode_pass(c, ec=True):
         for mods in dec_dev[c]:
@@ -411,7 +410,9 @@ def main():
                          "gate/up 2048->8192, down 8192->2048): decode M=1 over 16 layers x 7 "
                          "modules + prefill M=4096 over 7 modules"),
             "group_size": GROUP, "rank": RANK, "gate": "sigmoid_linear",
-            "decode_path": sp.PATH_NAMES[dec_plan.path], "prefill_path": sp.PATH_NAMES[pre_plan.path],
+            "decode_path": sp.PATH_NAMES[dec_plan.path],
+            "prefill_paths": {m: sp.PATH_NAMES[sp.dispatch_plan(d.problem()).path]
+                              for m, d in zip(S.MODULES, pre_dev)},
             "decode_weight_copies": args.copies,
         },
         "roofline": {
@@ -429,7 +430,8 @@ def main():
             "value": round(pre_tfl, 2), "unit": "TFLOP/s", "ms_per_pass": round(pre_s * 1e3, 4),
             "roofline": {
                 "bound": "mfma",
-                "kernel": "k_ec pre-kernel + k_gemm (EC epilogue), 7 modules",
+                "kernel": ("the 7 modules on their AUTO paths: k_ec pre-kernel + k_gemm with "
+                           "the EC epilogue (unfused_2k), or the fully fused k_gemm (fused_mfma)"),
                 "achieved": round(pre_tfl, 2), "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(pre_tfl / MFMA_F16_PEAK_TFLOPS, 4),
                 "traffic": (traffic or {}).get("prefill_bytes_per_launch"),
