@@ -82,7 +82,9 @@ enum {
   SPEAR_PATH_AUTO = 0,
   SPEAR_PATH_FUSED_GEMV = 1,     /* one kernel: split-K 4-bit GEMV; the same grid
                                     computes A x and the gate, and the epilogue
-                                    adds B (g (.) A x). Decode, M <= 64.       */
+                                    adds B (g (.) A x). Decode: up to 64
+                                    tokens; AUTO's choice up to 32 where the
+                                    local variant does not apply              */
   SPEAR_PATH_FUSED_MFMA = 2,     /* one kernel: the 4-bit MFMA GEMM also projects
                                     its activation tiles on A and w_g (split
                                     over K with the product when the tile grid
@@ -90,14 +92,15 @@ enum {
                                     gate and adds B (g (.) A x); rank <= 16,
                                     sigmoid-linear or identity gate (else
                                     SPEAR_E_UNSUPPORTED). AUTO picks it for
-                                    M > 64 while the grid has at most 256
-                                    128 x 128 tiles                            */
+                                    M > 32 while the grid has at most 256
+                                    128 x 128 tiles and the GEMM would not
+                                    take 256-token tiles                       */
   SPEAR_PATH_UNFUSED_CHAIN = 3,  /* naive split: 4-bit GEMM, then separate
                                     projection, gate and reprojection+accumulate
                                     kernels (the baseline of section 4.1)      */
   SPEAR_PATH_UNFUSED_2K = 4,     /* semi-fused: EC pre-kernel (A x, gate) then
                                     the 4-bit GEMM/GEMV whose epilogue adds
-                                    B (g (.) A x). AUTO's choice for M > 64
+                                    B (g (.) A x). AUTO's choice for M > 32
                                     otherwise                                  */
   SPEAR_PATH_FUSED_LOCAL = 5     /* one kernel: split-K 4-bit GEMV whose waves
                                     also project x on [A; w_g] over their own K
@@ -220,6 +223,14 @@ void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves);
  * slices only while the tile grid alone leaves CUs idle). For measurement
  * sweeps and tests only. */
 void spear_set_gemm_slices(int32_t k_slices);
+
+/* Tuning hook for the prefill GEMM's token tile, process-wide: 128 (four
+ * waves, two workgroups per CU) or 256 (eight waves, one workgroup per CU;
+ * not the fully fused path: SPEAR_E_UNSUPPORTED there); any other value
+ * restores the planner's choice (256 while those tiles fill the 256 CUs,
+ * each 4096 of K beyond the first counting as another round of tiles). For
+ * measurement sweeps and tests only. */
+void spear_set_gemm_tile(int32_t tokens);
 
 /* Static text for a status code. */
 const char* spear_status_string(spear_status_t status);

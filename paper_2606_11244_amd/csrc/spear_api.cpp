@@ -18,7 +18,7 @@ namespace {
 std::atomic<int32_t> g_wait_polls{1 << 16};
 // tuning override of the GEMV shape (0 = automatic): row tiles per block,
 // K-slices per row group, waves per block
-std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0};
+std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0}, g_ov_gt{0};
 
 // Token counts at or below this run the 4-bit product as a split-K GEMV; above
 // it the LDS-tiled MFMA GEMM. The same bound separates decode (fully fused
@@ -47,6 +47,7 @@ struct Resolved {
   int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
   int MT, RT, NW, nrg, S, ips, iw;            // GEMV shape
   int Sg;                                     // GEMM K-slices
+  int gtmw;                                   // GEMM token waves (2: 128-token tiles, 4: 256)
   int ntb, P, eips, PG, tpg, ec_mode, ec_ipp, ec_block, n_prod;  // EC shape
   int xlds, xstride, bpre, lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz, lds_a;
   size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart, off_eupart, off_gpart,
@@ -143,8 +144,12 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   // one 128 x 128 tile per CU, split over K): the separate projection
   // kernel's fixed cost then outweighs the projection the N-tiles repeat
   const bool few_tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN) <= 256;
+  // the 256-token GEMM tile applies (see the tile choice below): the
+  // semi-fused pair on it beats the fully fused GEMM on 128-token tiles
+  const bool big_tiles = cdiv(M, 256) * cdiv(N, kGemmTN) * std::max<int64_t>(1, K / 4096) >= 256;
   if (path == SPEAR_PATH_AUTO || !z.ec)
-    path = M > kAutoGemvMaxM ? (mfma_ok && few_tiles ? SPEAR_PATH_FUSED_MFMA : SPEAR_PATH_UNFUSED_2K)
+    path = M > kAutoGemvMaxM ? (mfma_ok && few_tiles && !big_tiles ? SPEAR_PATH_FUSED_MFMA
+                                                                   : SPEAR_PATH_UNFUSED_2K)
            : local_ok        ? SPEAR_PATH_FUSED_LOCAL
                              : SPEAR_PATH_FUSED_GEMV;
   if (!with_ec) {
@@ -201,10 +206,21 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     z.plan.tile_m = 16 * z.MT;
     z.plan.tile_n = 16 * z.RT;
   } else {
-    // prefill GEMM: K-slices (2, 4 or 8, each an even number of 64-wide
-    // steps, at least four) while the tile grid alone fills less than the
-    // 256 CUs; the fully fused variant splits its EC projection the same way
-    const int64_t tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN);
+    // prefill GEMM tile: 256 tokens (eight waves, one workgroup per CU)
+    // while those tiles fill the 256 CUs, counting each 4096 of K beyond the
+    // first as another round of them (measured: 1B down at M = 2048), else
+    // 128 (four waves, two workgroups per CU); the fully fused variant
+    // takes 128
+    z.gtmw = !fmfma && big_tiles ? 4 : 2;
+    if (g_ov_gt.load() > 0) {
+      z.gtmw = g_ov_gt.load() == 256 ? 4 : 2;
+      if (fmfma && z.gtmw == 4) return SPEAR_E_UNSUPPORTED;
+    }
+    const int tm = 64 * z.gtmw;
+    // K-slices (2, 4 or 8, each an even number of 64-wide steps, at least
+    // four) while the tile grid alone fills less than the 256 CUs; the fully
+    // fused variant splits its EC projection the same way
+    const int64_t tiles = cdiv(M, tm) * cdiv(N, kGemmTN);
     const int steps = (int)(K / kGemmTK);
     z.Sg = 1;
     for (int S = 2; S <= 8; S *= 2)
@@ -215,7 +231,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
       z.Sg = S;
     }
     z.plan.split_k = z.Sg;
-    z.plan.tile_m = kGemmTM;
+    z.plan.tile_m = tm;
     z.plan.tile_n = kGemmTN;
   }
 
@@ -330,7 +346,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   z.plan.ec_splits = z.ec ? z.P : 0;
 
   // launches and grid
-  const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, kGemmTM) * cdiv(N, kGemmTN)) * z.Sg;
+  const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, z.plan.tile_m) * cdiv(N, kGemmTN)) * z.Sg;
   if (!z.ec || local || fmfma) {
     z.plan.num_launches = 1;
     z.plan.grid = grid4;
@@ -387,8 +403,8 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     z.off_ypart = take((size_t)z.S * M * N * 4);
   }
   if (!z.gemv && z.Sg > 1) {
-    const int64_t tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN);
-    const size_t part = (size_t)z.Sg * tiles * kGemmTM * kGemmTN * 4;
+    const int64_t tiles = cdiv(M, z.plan.tile_m) * cdiv(N, kGemmTN);
+    const size_t part = (size_t)z.Sg * tiles * z.plan.tile_m * kGemmTN * 4;
     // the kernel addresses the partial tiles with 32-bit offsets
     if (tiles > kMaxRowCounters || part >= ((size_t)1 << 31)) return SPEAR_E_SHAPE;
     z.off_gpart = take(part);
@@ -541,6 +557,7 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
   GemmParams g;
   std::memset(&g, 0, sizeof(g));
   g.S = std::max(1, z.Sg);
+  g.tmw = z.gtmw ? z.gtmw : 2;
   if (ws && z.Sg > 1) {
     g.ypart = (float*)(ws + z.off_gpart);
     g.ctr = (uint32_t*)(ws + kCtrRows);
@@ -730,6 +747,8 @@ void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves) {
 }
 
 void spear_set_gemm_slices(int32_t k_slices) { g_ov_gs = k_slices > 0 ? k_slices : 0; }
+
+void spear_set_gemm_tile(int32_t tokens) { g_ov_gt = tokens == 128 || tokens == 256 ? tokens : 0; }
 
 const char* spear_status_string(spear_status_t s) {
   switch (s) {

@@ -155,6 +155,7 @@ struct GemmParams {
   float* ypart;
   uint32_t* ctr;
   float* epart;
+  int tmw;                // token waves: 2 (128-token tiles) or 4 (256, EPI_NONE / EPI_READY)
   // INT8 A and B (per-channel fp32 scales), or null: B8 for the
   // up-projection of EPI_READY / EPI_LOCAL_I8, A8 for EPI_LOCAL_I8
   const int8_t* A8;       // [r][K]

@@ -1590,22 +1590,32 @@ __device__ __forceinline__ void gemm_sum_ec_slices(rsrc_t rp, uint32_t base, uin
   }
 }
 
-template <int DT, int EPI>
-__global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
+// TMW: waves along the tokens. TMW = 2: 128-token tiles, 4 waves, two
+// workgroups per CU; TMW = 4: 256-token tiles, 8 waves, one workgroup per
+// CU. Both keep 64 x 64 per wave and two waves per SIMD; the 256-token tile
+// reuses each dequantised weight tile for twice the MFMAs, halving the
+// dequantisation's VALU work per MFMA.
+template <int DT, int EPI, int TMW>
+__global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr bool kLoc = EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8;
   constexpr bool kI8 = EPI == EPI_LOCAL_I8;  // INT8 A and B
+  constexpr int TM = 64 * TMW;         // tokens per tile
+  constexpr int NT = 128 * TMW;        // threads
+  constexpr int WPT = TMW == 2 ? 4 : 2;  // packed words of codes per thread and step
+  constexpr int WPR = 8 / WPT;         // threads per row of codes
   constexpr int LR = kGemmLdsRow;
-  constexpr int TILE = kGemmTM * LR;  // halves per LDS tile
+  constexpr int TILEX = TM * LR;       // halves per LDS activation tile
+  constexpr int TILEW = kGemmTN * LR;  // halves per LDS weight tile
   constexpr int ETILE = kGemmEcRows * LR;
-  uint16_t* Xs = (uint16_t*)smem;             // [2][128][LR]
-  uint16_t* Ws = Xs + 2 * TILE;               // [2][128][LR]
-  uint16_t* Es = Ws + 2 * TILE;               // EPI_LOCAL: [2][17][LR] A rows, w_g
+  uint16_t* Xs = (uint16_t*)smem;             // [2][TM][LR]
+  uint16_t* Ws = Xs + 2 * TILEX;              // [2][128][LR]
+  uint16_t* Es = Ws + 2 * TILEW;              // EPI_LOCAL: [2][17][LR] A rows, w_g
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;
   const int M = a.M, N = a.N, K = a.K;
-  const int tiles_m = (M + kGemmTM - 1) / kGemmTM, tiles_n = (N + kGemmTN - 1) / kGemmTN;
+  const int tiles_m = (M + TM - 1) / TM, tiles_n = (N + kGemmTN - 1) / kGemmTN;
   // Workgroups are dealt to the eight XCDs in turn (b % 8), and each XCD has
   // its own L2: give XCD x a contiguous band of token tiles (or, failing
   // that, of row tiles) so that the tiles its workgroups share are fetched
@@ -1629,7 +1639,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
       nt_i = b - mt_i * tiles_n;
     }
   }
-  const int m0 = mt_i * kGemmTM;
+  const int m0 = mt_i * TM;
   const int n0 = nt_i * kGemmTN;
   const int KT = K / kGemmTK / a.S;  // steps of this slice (an even count)
   const int kbase = ks * KT;
@@ -1643,15 +1653,16 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   uint32_t xoff[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i;
+    const int c = tid + NT * i;
     xr[i] = c >> 3;
     xc[i] = (c & 7) * 8;
     xoff[i] = m0 + xr[i] < M ? ((uint32_t)(m0 + xr[i]) * K + xc[i]) * 2 : kOOB;
   }
-  const int wr = tid >> 1, wh = tid & 1;
+  // codes: row wr, words [wp WPT, +WPT) of the row's 64-wide step
+  const int wr = tid / WPR, wp = tid % WPR;
   const int wn_row = n0 + wr;
   const bool wok = wn_row < N;
-  const uint32_t woff = wok ? (uint32_t)wn_row * (K / 2) + 16 * wh : kOOB;
+  const uint32_t woff = wok ? (uint32_t)wn_row * (K / 2) + 4 * WPT * wp : kOOB;
   // EPI_LOCAL: thread t < 136 stages 16 bytes of the EC tile per step: row
   // t / 8 (A's row while below r, zero up to 15; w_g as row 16), chunk t % 8
   const int er = tid >> 3, ec8 = tid & 7;
@@ -1686,7 +1697,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     const uint32_t k0 = (uint32_t)(kbase + kt) * kGemmTK;
 #pragma unroll
     for (int i = 0; i < 4; ++i) st.x[i] = bld128(rx, xoff[i] + k0 * 2);
-    st.w = bld128(rq, woff + k0 / 2);
+    if constexpr (WPT == 4) {
+      st.w = bld128(rq, woff + k0 / 2);
+    } else {
+      const u32x2 q = bld64(rq, woff + k0 / 2);
+      st.w = u32x4{q[0], q[1], 0u, 0u};
+    }
     const uint32_t g = k0 / a.G;
     st.s = bld16(rsc, wok ? ((uint32_t)wn_row * a.ngroups + g) * 2 : kOOB);
     st.z = bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
@@ -1704,15 +1720,15 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     const u32x4 wreg = st.w;
     const float sreg = h2f((uint16_t)st.s);
     const int zreg = (int)st.z;
-    uint16_t* xs = Xs + buf * TILE;
-    uint16_t* ws = Ws + buf * TILE;
+    uint16_t* xs = Xs + buf * TILEX;
+    uint16_t* ws = Ws + buf * TILEW;
 #pragma unroll
     for (int i = 0; i < 4; ++i) *(u32x4*)(xs + xr[i] * LR + xc[i]) = xreg[i];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
+    for (int c = 0; c < WPT; ++c) {
       uint32_t o[4];
       dequant_word_pairs<DT>(wreg[c], sreg, zreg, o);
-      *(u32x4*)(ws + wr * LR + 32 * wh + 8 * c) = u32x4{o[0], o[1], o[2], o[3]};
+      *(u32x4*)(ws + wr * LR + 8 * (WPT * wp + c)) = u32x4{o[0], o[1], o[2], o[3]};
     }
     if constexpr (kLoc) {
       u32x4 ev = st.e;
@@ -1733,8 +1749,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   for (int i = 0; i < 4; ++i) eacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   auto compute = [&](int buf) {
-    const uint16_t* xs = Xs + buf * TILE;
-    const uint16_t* ws = Ws + buf * TILE;
+    const uint16_t* xs = Xs + buf * TILEX;
+    const uint16_t* ws = Ws + buf * TILEW;
 #pragma unroll
     for (int kk = 0; kk < kGemmTK; kk += 32) {
       u32x4 af[4], bf[4];
@@ -1788,11 +1804,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
   // slice order (reading its own back like the others) and runs the epilogue
   if (a.S > 1) {
     __shared__ int s_last;
-    const uint32_t tbytes = kGemmTM * kGemmTN * 4;
+    const uint32_t tbytes = TM * kGemmTN * 4;
     const rsrc_t rp = make_rsrc(a.ypart, (uint32_t)a.S * T * tbytes);
     const uint32_t ybase = (uint32_t)tb * tbytes + (uint32_t)(wave * 16 * 64 + lane) * 16;
     const uint32_t yslice = (uint32_t)T * tbytes;
-    constexpr uint32_t ebytes = 4 * 4 * 64 * 16;  // EC accumulators of a tile
+    constexpr uint32_t ebytes = 2 * TMW * 4 * 64 * 16;  // EC accumulators of a tile
     const rsrc_t rep = make_rsrc(kLoc ? a.epart : nullptr, kLoc ? (uint32_t)a.S * T * ebytes : 0u);
     const uint32_t ebase = (uint32_t)tb * ebytes + (uint32_t)(wave * 4 * 64 + lane) * 16;
     const uint32_t eslice = (uint32_t)T * ebytes;
@@ -1820,13 +1836,13 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
     }
   }
 
-  // EPI_LOCAL: v = alpha g(x) (.) u for the block's 128 tokens, as act-dtype
-  // high and low parts [128][32] in LDS (the stage buffers are free once
+  // EPI_LOCAL: v = alpha g(x) (.) u for the block's TM tokens, as act-dtype
+  // high and low parts [TM][32] in LDS (the stage buffers are free once
   // every wave is past its last step)
   constexpr int kVS = 32;
-  float* u_sh = (float*)smem;                                  // [128][17]
-  uint16_t* vh_sh = (uint16_t*)(smem + kGemmTM * 17 * 4);      // [128][kVS]
-  uint16_t* vl_sh = vh_sh + kGemmTM * kVS;
+  float* u_sh = (float*)smem;                                  // [TM][17]
+  uint16_t* vh_sh = (uint16_t*)(smem + TM * 17 * 4);           // [TM][kVS]
+  uint16_t* vl_sh = vh_sh + TM * kVS;
   if constexpr (kLoc) {
     __syncthreads();
 #pragma unroll
@@ -1838,7 +1854,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmParams a) {
         if (wn == 1 && lr == 0) u_sh[t * 17 + 16] = eacc[i][e2];
       }
     __syncthreads();
-    for (int idx = tid; idx < kGemmTM * kVS; idx += 256) {
+    for (int idx = tid; idx < TM * kVS; idx += NT) {
       const int t = idx / kVS, j = idx - t * kVS;
       float val = 0.f;
       if (j < a.r) {
@@ -2053,36 +2069,41 @@ hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int
 }
 
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st) {
-  // split-K needs its partial tiles and tile counters (workspace)
+  // split-K needs its partial tiles and tile counters (workspace); the
+  // 256-token tile takes the plain and the semi-fused epilogue only
   const bool loc = epi == EPI_LOCAL || epi == EPI_LOCAL_I8;
   if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.ctr || (loc && !p.epart))) ||
       (p.S != 1 && p.S != 2 && p.S != 4 && p.S != 8) ||
-      (epi == EPI_LOCAL_I8 && (!p.A8 || !p.sa || !p.B8 || !p.sb)))
+      (epi == EPI_LOCAL_I8 && (!p.A8 || !p.sa || !p.B8 || !p.sb)) ||
+      (p.tmw != 2 && p.tmw != 4) || (p.tmw == 4 && loc))
     return hipErrorInvalidValue;
-  const int tm = (p.M + kGemmTM - 1) / kGemmTM, tn = (p.N + kGemmTN - 1) / kGemmTN;
+  const int TM = 64 * p.tmw;
+  const int tm = (p.M + TM - 1) / TM, tn = (p.N + kGemmTN - 1) / kGemmTN;
   const unsigned grid = (unsigned)(tm * tn * p.S);
   if (grid == 0) return hipSuccess;
-  size_t lds = (size_t)4 * kGemmTM * kGemmLdsRow * 2;
+  size_t lds = (size_t)2 * (TM + kGemmTN) * kGemmLdsRow * 2;
   if (loc) lds += (size_t)2 * kGemmEcRows * kGemmLdsRow * 2;
+#define SPEAR_GEMM_GO(E, W)                                                            \
+  do {                                                                                 \
+    hipError_t err = allow_lds(k_gemm<DTC, E, W>, lds);                                \
+    if (err != hipSuccess) return err;                                                 \
+    hipLaunchKernelGGL((k_gemm<DTC, E, W>), dim3(grid), dim3(128 * W), lds, st, p);    \
+  } while (0)
   SPEAR_DT_SWITCH(dt, {
-    if (epi == EPI_NONE) {
-      hipError_t err = allow_lds(k_gemm<DTC, EPI_NONE>, lds);
-      if (err != hipSuccess) return err;
-      hipLaunchKernelGGL((k_gemm<DTC, EPI_NONE>), dim3(grid), dim3(256), lds, st, p);
+    if (p.tmw == 4) {
+      if (epi == EPI_NONE) SPEAR_GEMM_GO(EPI_NONE, 4);
+      else SPEAR_GEMM_GO(EPI_READY, 4);
+    } else if (epi == EPI_NONE) {
+      SPEAR_GEMM_GO(EPI_NONE, 2);
     } else if (epi == EPI_LOCAL) {
-      hipError_t err = allow_lds(k_gemm<DTC, EPI_LOCAL>, lds);
-      if (err != hipSuccess) return err;
-      hipLaunchKernelGGL((k_gemm<DTC, EPI_LOCAL>), dim3(grid), dim3(256), lds, st, p);
+      SPEAR_GEMM_GO(EPI_LOCAL, 2);
     } else if (epi == EPI_LOCAL_I8) {
-      hipError_t err = allow_lds(k_gemm<DTC, EPI_LOCAL_I8>, lds);
-      if (err != hipSuccess) return err;
-      hipLaunchKernelGGL((k_gemm<DTC, EPI_LOCAL_I8>), dim3(grid), dim3(256), lds, st, p);
+      SPEAR_GEMM_GO(EPI_LOCAL_I8, 2);
     } else {
-      hipError_t err = allow_lds(k_gemm<DTC, EPI_READY>, lds);
-      if (err != hipSuccess) return err;
-      hipLaunchKernelGGL((k_gemm<DTC, EPI_READY>), dim3(grid), dim3(256), lds, st, p);
+      SPEAR_GEMM_GO(EPI_READY, 2);
     }
   });
+#undef SPEAR_GEMM_GO
   return hipGetLastError();
 }
 

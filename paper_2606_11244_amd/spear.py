@@ -32,6 +32,7 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
 
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
             "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
+            "spear_set_gemm_tile",
             "spear_status_string", "spear_version", "spear_sched_latency", "spear_sched_chunk")
 
 
@@ -104,6 +105,8 @@ def _load():
     lib.spear_set_gemv_shape.restype = None
     lib.spear_set_gemm_slices.argtypes = [ctypes.c_int32]
     lib.spear_set_gemm_slices.restype = None
+    lib.spear_set_gemm_tile.argtypes = [ctypes.c_int32]
+    lib.spear_set_gemm_tile.restype = None
     lib.spear_sched_latency.argtypes = [P(ModelLat), ctypes.c_int64, P(ctypes.c_double)]
     lib.spear_sched_chunk.argtypes = [P(ModelLat), ctypes.c_int64, ctypes.c_double,
                                       ctypes.c_int64, ctypes.c_int64, P(ctypes.c_int64)]
@@ -211,6 +214,11 @@ def set_gemv_shape(row_tiles=0, k_slices=0, waves=0) -> None:
 def set_gemm_slices(k_slices=0) -> None:
     """Tuning override of the prefill GEMM's K-slices (0 = automatic)."""
     LIB.spear_set_gemm_slices(int(k_slices))
+
+
+def set_gemm_tile(tokens=0) -> None:
+    """Tuning override of the prefill GEMM's token tile (128, 256; 0 = automatic)."""
+    LIB.spear_set_gemm_tile(int(tokens))
 
 
 class LatencyModel:

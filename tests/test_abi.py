@@ -128,7 +128,24 @@ def test_gemm_split_k_plan_and_workspace():
         tiles = 4 * 8
         assert p.split_k == 8 and p.grid == tiles * 8
         assert p.workspace_bytes >= 8 * tiles * 128 * 128 * 4
-    assert _plan(M=4096, N=2048, K=2048).split_k == 1   # 512 tiles: no split
+    assert _plan(M=4096, N=2048, K=2048).split_k == 1   # 256 tiles of 256 tokens: no split
+    # 256-token tiles while they alone fill the CUs, else 128
+    assert _plan(M=4096, N=2048, K=2048).tile_m == 256
+    assert _plan(M=2048, N=2048, K=2048).tile_m == 128
+    # deep K counts: 128 tiles of 256 tokens at K = 8192 take the big tile
+    assert _plan(M=2048, N=2048, K=8192, with_ec=False).tile_m == 256
+    # ... and the EC call then takes the semi-fused pair on that tile
+    p = _plan(M=2048, N=2048, K=8192)
+    assert p.path == sp.PATH_UNFUSED_2K and p.tile_m == 256
+    sp.set_gemm_tile(256)
+    try:
+        for kw in (dict(with_ec=False), dict(force_path=4)):
+            p = _plan(M=512, N=1024, K=8192, rank=16, **kw)
+            assert p.tile_m == 256 and p.grid == 2 * 8 * p.split_k, kw
+        with pytest.raises(sp.SpearError):
+            _plan(M=512, N=1024, K=8192, rank=16, force_path=2)  # fused: 128 only
+    finally:
+        sp.set_gemm_tile(0)
     # the fully fused GEMM splits alike and adds the slices' EC accumulators
     f = _plan(M=512, N=1024, K=8192, rank=16, force_path=2)
     assert f.path == 2 and f.split_k == 8

@@ -403,3 +403,27 @@ def test_int8_factors_split_fused_gemm():
             assert_parity(gpu_y(L, PATHS["fused_mfma"]), ref, f"int8 slices={slices}")
     finally:
         sp.set_gemm_slices(0)
+
+
+@pytest.mark.parametrize("tile", [128, 256])
+@pytest.mark.parametrize("M,N,K,dt,G", [(300, 200, 1024, S.F16, 128), (513, 384, 2048, S.BF16, 0),
+                                         (257, 136, 512, S.F16, 128)])
+def test_gemm_token_tiles(tile, M, N, K, dt, G):
+    """The prefill GEMM with 128-token (four waves) and 256-token (eight
+    waves) tiles, whole and split over K, on ragged token and row counts:
+    the 4-bit product, the semi-fused EC path and the chain meet the bar."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=M, N=N, K=K, group_size=G, rank=16, act_dtype=dt, seed=M + tile,
+                     ec_std=0.05)
+    ref, ref4 = O.w4ec_linear(L), O.w4_linear_layer(L)
+    sp.set_gemm_tile(tile)
+    try:
+        for slices in (1, 2, 4):
+            sp.set_gemm_slices(slices)
+            log(f"gemm tile={tile} slices={slices} M={M} N={N} K={K} dt={dt}")
+            assert_parity(gpu_y(L, 0, with_ec=False), ref4, f"tile={tile} S={slices} w4")
+            for p in (PATHS["2k"], PATHS["chain"]):
+                assert_parity(gpu_y(L, p), ref, f"tile={tile} S={slices} path={p}")
+    finally:
+        sp.set_gemm_slices(0)
+        sp.set_gemm_tile(0)
