@@ -182,6 +182,102 @@ def decode_70b_context(sp, torch, steps, warmup, dev):
             "rank": r, "path": "fused_gemv", "weights": "device-random (timing only)"}
 
 
+def model_70b_pass(sp, torch, dev, Ms=(1, 16, 64, 512, 4096, 8192), reps=3):
+    """The 70B-shaped model's linear layers as one pass per token count: all
+    80 layers x 7 modules resident in HBM (device-random 4-bit weights,
+    group 128, about 36 GB), the EC (rank 64, sigmoid-linear gate) on the
+    seeded 25% of the (layer, module) pairs and the 4-bit product alone on
+    the rest, every call on its AUTO path; the same pass with no EC at all
+    gives the model's EC overhead. Each pass is one captured graph."""
+    from paper_2606_11244_amd import synth as S
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    r, G = 64, 128
+    sel = S.ec_selection_70b(seed=0)
+    layers = []
+    for l in range(sel.shape[0]):
+        mods = []
+        for j, m in enumerate(S.MODULES):
+            K, N = S.LLAMA_70B[m]
+            q = torch.randint(-2**31, 2**31 - 1, (N, K // 8), dtype=torch.int32, device=dev, generator=g)
+            sc = (torch.rand((N, K // G), device=dev, generator=g) * 1e-3 + 1e-4).half().view(torch.int16)
+            zr = torch.randint(0, 16, (N, K // G), dtype=torch.uint8, device=dev, generator=g)
+            ec = None
+            if sel[l, j]:
+                ec = ((torch.randn((r, K), device=dev, generator=g) * 0.01).half(),
+                      (torch.randn((N, r), device=dev, generator=g) * 0.01).half(),
+                      (torch.randn((K,), device=dev, generator=g) * 0.05).half())
+            mods.append((m, K, N, q, sc, zr, ec))
+        layers.append(mods)
+    Kmax, Nmax, Mmax = max(k for k, _ in S.LLAMA_70B.values()), max(n for _, n in S.LLAMA_70B.values()), max(Ms)
+    xbuf = torch.randn((Mmax * Kmax,), device=dev, generator=g).half()
+    ybuf = torch.empty((Mmax * Nmax,), dtype=torch.float16, device=dev)
+    out = {"weights": "device-random (timing only)",
+           "ec": f"rank 64 on a seeded 25% of the (layer, module) pairs ({int(sel.sum())} of {sel.size})",
+           "passes": []}
+    for M in Ms:
+        plans = {}
+        ws_need = 256
+        for m in S.MODULES:
+            K, N = S.LLAMA_70B[m]
+            pe = sp.problem(M, N, K, G, sp.F16, r, sp.GATE_SIGMOID_LINEAR)
+            p4 = sp.problem(M, N, K, G, sp.F16, 0, sp.GATE_SIGMOID_LINEAR)
+            plans[m] = (pe, p4)
+            ws_need = max(ws_need, sp.dispatch_plan(pe).workspace_bytes,
+                          sp.dispatch_plan(p4, with_ec=False).workspace_bytes)
+        ws = torch.zeros(ws_need, dtype=torch.uint8, device=dev)
+
+        def run(with_ec):
+            for mods in layers:
+                for (m, K, N, q, sc, zr, ec) in mods:
+                    x = xbuf[:M * K].view(M, K)
+                    y = ybuf[:M * N].view(M, N)
+                    pe, p4 = plans[m]
+                    if with_ec and ec is not None:
+                        sp.w4ec_linear(pe, x, q, sc, zr, ec[0], ec[1], y, w_g=ec[2], workspace=ws)
+                    else:
+                        sp.w4_linear(p4, x, q, sc, zr, y, workspace=ws)
+
+        def timed(with_ec):
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                run(with_ec)
+            torch.cuda.current_stream().wait_stream(s)
+            torch.cuda.synchronize()
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                run(with_ec)
+            gr.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                gr.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            del gr
+            return e0.elapsed_time(e1) * 1e-3 / reps
+
+        t_ec, t_w4 = timed(True), timed(False)
+        nbytes = sum(algo_bytes(M, N, K, G, r if ec is not None else 0)
+                     for mods in layers for (m, K, N, q, sc, zr, ec) in mods)
+        flops = sum(algo_flops(M, N, K, r if ec is not None else 0)
+                    for mods in layers for (m, K, N, q, sc, zr, ec) in mods)
+        out["passes"].append({
+            "M": M, "ms_per_pass": round(t_ec * 1e3, 3), "w4_only_ms": round(t_w4 * 1e3, 3),
+            "ec_overhead": round(t_ec / t_w4 - 1, 4), "GBps": round(nbytes / t_ec / 1e9, 1),
+            "hbm_frac": round(nbytes / t_ec / 1e9 / HBM_PEAK_GBS, 4),
+            "TFLOPs": round(flops / t_ec / 1e12, 1),
+            "mfma_frac": round(flops / t_ec / 1e12 / MFMA_F16_PEAK_TFLOPS, 4)})
+        print("bench: 70B model pass M=%d: %.3f ms (W4-only %.3f ms)" % (M, t_ec * 1e3, t_w4 * 1e3),
+              file=sys.stderr, flush=True)
+        del ws
+    del layers, xbuf, ybuf
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -193,6 +289,9 @@ def main():
     ap.add_argument("--no-70b", action="store_true", help="skip the 70B-layer context line")
     ap.add_argument("--no-int8", action="store_true",
                     help="skip the passes with INT8 per-channel EC factors")
+    ap.add_argument("--model70b", action="store_true",
+                    help="also time the 70B-shaped model's linear layers (80 layers resident, "
+                         "about 36 GB) at M = 1 .. 8192")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -375,6 +474,11 @@ def main():
             int8["prefill_overhead"] = round(p8 / p4 - 1.0, 4)
             int8["decode_ec_byte_share"] = round(dec_bytes_i8 / dec_bytes_w4 - 1.0, 4)
 
+    model70 = None
+    if args.model70b:
+        print("bench: 70B-shaped model pass", file=sys.stderr, flush=True)
+        model70 = model_70b_pass(sp, torch, dev)
+
     ctx70 = None
     if not args.no_70b:
         print("bench: 70B-layer decode context", file=sys.stderr, flush=True)
@@ -439,6 +543,7 @@ def main():
         },
         "decode_ms_per_pass": round(dec_s * 1e3, 4),
         "decode_70b_layer": ctx70,
+        "model_70b": model70,
         "ec_overhead": overhead,
         "ec_int8": int8,
     }

@@ -29,7 +29,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CALIB_BYTES = 1 << 30  # the calibration kernel reads and writes 1 GiB
 
 DECODE_KERNEL = "k_gemv<0, 1, 2, 3>"   # fp16, one token tile, two row tiles, local-EC epilogue
-PREFILL_KERNEL = "k_gemm<0, 1>"        # fp16, EC epilogue
+PREFILL_KERNEL = "k_gemm<0, 1, 4>"     # fp16, EC epilogue, 256-token tiles
 
 
 def kernel_source_hash() -> str:
