@@ -57,7 +57,7 @@ enum {
   SPEAR_OK = 0,
   SPEAR_E_NULL = -1,        /* a required pointer is NULL                   */
   SPEAR_E_SHAPE = -2,       /* M, N, K, G, r or h outside the supported set */
-  SPEAR_E_DTYPE = -3,       /* unknown activation dtype                     */
+  SPEAR_E_DTYPE = -3,       /* unknown activation dtype or EC factor format */
   SPEAR_E_ALIGN = -4,       /* a device pointer is not 16-byte aligned      */
   SPEAR_E_WORKSPACE = -5,   /* workspace missing or smaller than required   */
   SPEAR_E_UNSUPPORTED = -6, /* gate kind or forced path not available       */
@@ -194,6 +194,37 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x,
                                  const spear_w4_t* w, const spear_ec_t* ec,
                                  void* y, void* workspace,
                                  size_t workspace_bytes, void* hip_stream);
+
+/* Post-EC tail (section 4.2: after the compensated product, the residual
+ * addition and the next layer's RMSNorm). */
+typedef struct {
+  const void* residual;  /* [M][N] act dtype, added to Y before Y's single
+                            rounding (Y becomes the new hidden state); may
+                            be Y itself (in place); NULL: no residual        */
+  const void* norm_w;    /* [N] act dtype: the next layer's RMSNorm weight;
+                            NULL: no norm                                    */
+  float eps;             /* RMSNorm epsilon, finite and >= 0                 */
+  void* y_norm;          /* [M][N] act dtype: Y[m][n] * w[n] /
+                            sqrt(mean_n Y[m][n]^2 + eps) over the stored Y,
+                            computed in fp32 and rounded once; required with
+                            norm_w; overlaps nothing else                    */
+} spear_tail_t;
+
+/* spear_w4ec_linear (or, with ec == NULL, spear_w4_linear) followed by the
+ * post-EC tail. The residual is added inside the layer's own final store on
+ * every path (the naive chain: in its 4-bit kernel); the RMSNorm, which needs
+ * each token's whole row of Y while the layer's workgroups each hold a
+ * slice of it, runs as one more kernel (one workgroup per token) in the same
+ * call. The workspace is the one spear_dispatch_plan gives for the call
+ * (with_ec = ec != NULL). Errors as for the layer call, plus SPEAR_E_NULL for
+ * a missing tail or y_norm, SPEAR_E_ALIGN for a misaligned tail pointer,
+ * SPEAR_E_ALIAS for y_norm overlapping another buffer or a residual that
+ * overlaps Y without being Y, SPEAR_E_SHAPE for a negative or non-finite
+ * eps. */
+spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x,
+                                      const spear_w4_t* w, const spear_ec_t* ec,
+                                      const spear_tail_t* tail, void* y, void* workspace,
+                                      size_t workspace_bytes, void* hip_stream);
 
 /* Diagnostic of the dequantisation the kernels use: writes
  * w_out[n][k] = RNE_act((q[n][k] - z[n][k/G]) * s[n][k/G]) as a dense [N][K]

@@ -223,6 +223,19 @@ def w4ec_linear(layer) -> np.ndarray:
         W2=bits_to_f64(layer.W2, dt), b2=bits_to_f64(layer.b2, dt))
 
 
+def post_ec_tail(y, residual, norm_w, eps: float):
+    """The post-EC tail (section 4.2: residual addition and the next layer's
+    RMSNorm after the compensated product), in float64:
+        h = y + residual
+        y_norm[m][n] = h[m][n] * norm_w[n] / sqrt(mean_n h[m][n]^2 + eps)
+    Returns (h, y_norm); residual None adds nothing."""
+    h = np.asarray(y, np.float64)
+    if residual is not None:
+        h = h + np.asarray(residual, np.float64)
+    ms = np.mean(h * h, axis=1, keepdims=True)
+    return h, h / np.sqrt(ms + float(eps)) * np.asarray(norm_w, np.float64)[None, :]
+
+
 def w4_linear_layer(layer) -> np.ndarray:
     """The plain 4-bit product X . W_hat^T of a stored layer (EC ignored)."""
     W_hat = dequant(layer.qweight, layer.scales, layer.zeros, layer.group_size)

@@ -606,15 +606,91 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
 
 spear_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPEAR_OK : SPEAR_E_HIP; }
 
+// res: [M][N] act-dtype residual added before the output's single rounding, or null
 spear_status_t run_w4(const spear_problem_t* p, const Resolved& z, const void* x, const spear_w4_t* w,
-                      void* y, char* ws, hipStream_t st) {
+                      void* y, char* ws, hipStream_t st, const uint16_t* res = nullptr) {
   if (z.gemv) {
     GemvParams g = make_gemv(p, z, x, w, y, nullptr, ws);
+    g.res = res;
     return hip_status(
         launch_gemv(z.dt, z.MT, z.RT, EPI_NONE, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, st));
   }
   GemmParams g = make_gemm(p, z, x, w, y, nullptr, ws);
+  g.res = res;
   return hip_status(launch_gemm(z.dt, EPI_NONE, g, st));
+}
+
+// The layer on its planned path, after validation; res as in run_w4 (the
+// chain adds it in its 4-bit kernel, every other path in its final store).
+spear_status_t run_layer(const spear_problem_t* prob, const Resolved& z, const void* x,
+                         const spear_w4_t* w, const spear_ec_t* ec, void* y, const uint16_t* res,
+                         char* ws, hipStream_t s) {
+  spear_status_t st = SPEAR_OK;
+  if (!z.ec) return run_w4(prob, z, x, w, y, ws, s, res);
+
+  EcParams e = make_ec(prob, z, x, ec, ws);
+  const int path = z.plan.path;
+  const int ec_grid = z.ntb * z.P * z.PG;
+  if (path == SPEAR_PATH_FUSED_MFMA) {
+    GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
+    g.res = res;
+    return hip_status(launch_gemm(z.dt, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g, s));
+  }
+  if (path == SPEAR_PATH_FUSED_LOCAL) {
+    GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
+    g.res = res;
+    g.ec = e;
+    if (z.S > 1) g.eupart = (float*)(ws + z.off_eupart);
+    return hip_status(launch_gemv(z.dt, z.MT, z.RT, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g,
+                                  z.nrg * z.S, 64 * z.NW, z.lds_gemv, s));
+  }
+  if (path == SPEAR_PATH_FUSED_GEMV) {
+    e.vtag = (unsigned long long*)(ws + z.off_vtag);
+    e.gen = (unsigned long long*)(ws + kCtrGen);
+    e.ready = (unsigned long long*)(ws + kCtrReady);
+    e.npub = z.npub;
+    e.direct = z.direct;
+    e.v = nullptr;
+    GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
+    g.res = res;
+    g.ec = e;
+    g.n_prod = z.n_prod;
+    g.grid_total = z.n_prod + z.nrg * z.S;
+    const size_t lds = std::max(z.lds_gemv, z.lds_prod);
+    return hip_status(
+        launch_gemv(z.dt, z.MT, z.RT, EPI_FUSED, g, g.grid_total, 64 * (z.NW + 1), lds, s));
+  }
+  if (path == SPEAR_PATH_UNFUSED_2K) {
+    if (!z.gemv) {
+      e.vh = (uint16_t*)(ws + z.off_vh);
+      e.vl = (uint16_t*)(ws + z.off_vl);
+      e.v = nullptr;
+    }
+    st = hip_status(launch_ec(z.dt, e, ec_grid, z.ec_block, z.ec_ipp, z.lds_prod, s));
+    if (st != SPEAR_OK) return st;
+    if (z.gemv) {
+      GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
+      g.res = res;
+      g.ec = e;
+      return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_READY, g, z.nrg * z.S, 64 * (z.NW + 1),
+                                    z.lds_gemv, s));
+    }
+    GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
+    g.res = res;
+    return hip_status(launch_gemm(z.dt, EPI_READY, g, s));
+  }
+  // naive chain: 4-bit product, projection, gate, reprojection + accumulate
+  st = run_w4(prob, z, x, w, y, ws, s, res);
+  if (st != SPEAR_OK) return st;
+  e.u_out = (float*)(ws + z.off_u);
+  st = hip_status(launch_ec(z.dt, e, ec_grid, z.ec_block, z.ec_ipp, z.lds_prod, s));
+  if (st != SPEAR_OK) return st;
+  st = hip_status(launch_gate(z.dt, e, z.ntb, z.lds_gate, s));
+  if (st != SPEAR_OK) return st;
+  const bool i8 = ab_int8(ec);
+  return hip_status(launch_ec_up_acc(z.dt, e.v, i8 ? nullptr : (const uint16_t*)ec->B,
+                                     i8 ? (const int8_t*)ec->B : nullptr, i8 ? ec->b_scale : nullptr,
+                                     (uint16_t*)y, (int)prob->M, (int)prob->N, z.r, s));
 }
 
 }  // namespace
@@ -651,68 +727,41 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   if ((st = check_w4(prob, x, w, y)) != SPEAR_OK) return st;
   if ((st = check_ec(prob, z, ec, y)) != SPEAR_OK) return st;
   if ((st = check_ws(prob, z, y, workspace, workspace_bytes)) != SPEAR_OK) return st;
-  hipStream_t s = (hipStream_t)hip_stream;
-  char* ws = (char*)workspace;
-  if (!z.ec) return run_w4(prob, z, x, w, y, ws, s);
+  return run_layer(prob, z, x, w, ec, y, nullptr, (char*)workspace, (hipStream_t)hip_stream);
+}
 
-  EcParams e = make_ec(prob, z, x, ec, ws);
-  const int path = z.plan.path;
-  const int ec_grid = z.ntb * z.P * z.PG;
-  if (path == SPEAR_PATH_FUSED_MFMA) {
-    GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
-    return hip_status(launch_gemm(z.dt, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g, s));
-  }
-  if (path == SPEAR_PATH_FUSED_LOCAL) {
-    GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
-    g.ec = e;
-    if (z.S > 1) g.eupart = (float*)(ws + z.off_eupart);
-    return hip_status(launch_gemv(z.dt, z.MT, z.RT, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g,
-                                  z.nrg * z.S, 64 * z.NW, z.lds_gemv, s));
-  }
-  if (path == SPEAR_PATH_FUSED_GEMV) {
-    e.vtag = (unsigned long long*)(ws + z.off_vtag);
-    e.gen = (unsigned long long*)(ws + kCtrGen);
-    e.ready = (unsigned long long*)(ws + kCtrReady);
-    e.npub = z.npub;
-    e.direct = z.direct;
-    e.v = nullptr;
-    GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
-    g.ec = e;
-    g.n_prod = z.n_prod;
-    g.grid_total = z.n_prod + z.nrg * z.S;
-    const size_t lds = std::max(z.lds_gemv, z.lds_prod);
-    return hip_status(
-        launch_gemv(z.dt, z.MT, z.RT, EPI_FUSED, g, g.grid_total, 64 * (z.NW + 1), lds, s));
-  }
-  if (path == SPEAR_PATH_UNFUSED_2K) {
-    if (!z.gemv) {
-      e.vh = (uint16_t*)(ws + z.off_vh);
-      e.vl = (uint16_t*)(ws + z.off_vl);
-      e.v = nullptr;
-    }
-    st = hip_status(launch_ec(z.dt, e, ec_grid, z.ec_block, z.ec_ipp, z.lds_prod, s));
-    if (st != SPEAR_OK) return st;
-    if (z.gemv) {
-      GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
-      g.ec = e;
-      return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_READY, g, z.nrg * z.S, 64 * (z.NW + 1),
-                                    z.lds_gemv, s));
-    }
-    GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
-    return hip_status(launch_gemm(z.dt, EPI_READY, g, s));
-  }
-  // naive chain: 4-bit product, projection, gate, reprojection + accumulate
-  st = run_w4(prob, z, x, w, y, ws, s);
+spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x,
+                                      const spear_w4_t* w, const spear_ec_t* ec,
+                                      const spear_tail_t* tail, void* y, void* workspace,
+                                      size_t workspace_bytes, void* hip_stream) {
+  Resolved z;
+  spear_status_t st = resolve(prob, ec != nullptr, &z);
   if (st != SPEAR_OK) return st;
-  e.u_out = (float*)(ws + z.off_u);
-  st = hip_status(launch_ec(z.dt, e, ec_grid, z.ec_block, z.ec_ipp, z.lds_prod, s));
-  if (st != SPEAR_OK) return st;
-  st = hip_status(launch_gate(z.dt, e, z.ntb, z.lds_gate, s));
-  if (st != SPEAR_OK) return st;
-  const bool i8 = ab_int8(ec);
-  return hip_status(launch_ec_up_acc(z.dt, e.v, i8 ? nullptr : (const uint16_t*)ec->B,
-                                     i8 ? (const int8_t*)ec->B : nullptr, i8 ? ec->b_scale : nullptr,
-                                     (uint16_t*)y, (int)prob->M, (int)prob->N, z.r, s));
+  if (!tail) return SPEAR_E_NULL;
+  if (!std::isfinite(tail->eps) || tail->eps < 0.f) return SPEAR_E_SHAPE;
+  if (prob->M == 0 || prob->N == 0) return SPEAR_OK;
+  if ((st = check_w4(prob, x, w, y)) != SPEAR_OK) return st;
+  if (ec && (st = check_ec(prob, z, ec, y)) != SPEAR_OK) return st;
+  if (tail->norm_w && !tail->y_norm) return SPEAR_E_NULL;
+  if (misaligned(tail->residual) || misaligned(tail->norm_w) || misaligned(tail->y_norm))
+    return SPEAR_E_ALIGN;
+  const size_t yb = (size_t)prob->M * prob->N * 2;
+  const size_t xb = (size_t)prob->M * prob->K * 2;
+  if (tail->residual && tail->residual != y && overlaps(tail->residual, yb, y, yb))
+    return SPEAR_E_ALIAS;
+  if (tail->norm_w &&
+      (overlaps(tail->y_norm, yb, y, yb) || overlaps(tail->y_norm, yb, x, xb) ||
+       overlaps(tail->y_norm, yb, tail->residual, yb) ||
+       overlaps(tail->y_norm, yb, tail->norm_w, (size_t)prob->N * 2) ||
+       overlaps(tail->y_norm, yb, workspace, z.plan.workspace_bytes)))
+    return SPEAR_E_ALIAS;
+  if ((st = check_ws(prob, z, y, workspace, workspace_bytes)) != SPEAR_OK) return st;
+  hipStream_t s = (hipStream_t)hip_stream;
+  st = run_layer(prob, z, x, w, ec, y, (const uint16_t*)tail->residual, (char*)workspace, s);
+  if (st != SPEAR_OK || !tail->norm_w) return st;
+  return hip_status(launch_rmsnorm(z.dt, (const uint16_t*)y, (const uint16_t*)tail->norm_w,
+                                   tail->eps, (uint16_t*)tail->y_norm, (int)prob->M,
+                                   (int)prob->N, s));
 }
 
 spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w, void* w_out,

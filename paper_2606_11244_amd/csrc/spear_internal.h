@@ -119,6 +119,7 @@ struct GemvParams {
   const uint16_t* B;      // [N][r] act dtype (null with INT8 B)
   const int8_t* B8;       // [N][r] INT8 codes, or null
   const float* sb;        // [N] INT8 per-channel scales
+  const uint16_t* res;    // [M][N] residual added before the output's rounding, or null
   int M, N, K, G, ngroups, r;
   int S, ips, iw;         // K-slices per row group, iterations per slice and per wave
   int n_prod;             // EC workgroups at the head of the grid (fused)
@@ -156,6 +157,7 @@ struct GemmParams {
   uint32_t* ctr;
   float* epart;
   int tmw;                // token waves: 2 (128-token tiles) or 4 (256, EPI_NONE / EPI_READY)
+  const uint16_t* res;    // [M][N] residual added before the output's rounding, or null
   // INT8 A and B (per-channel fp32 scales), or null: B8 for the
   // up-projection of EPI_READY / EPI_LOCAL_I8, A8 for EPI_LOCAL_I8
   const int8_t* A8;       // [r][K]
@@ -201,6 +203,9 @@ hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int
                        size_t lds, hipStream_t st);
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st);
 hipError_t launch_gate(int dt, const EcParams& e, int ntb, size_t lds, hipStream_t st);
+// y_norm[m] = RMSNorm(y[m]) * w (one workgroup per token row)
+hipError_t launch_rmsnorm(int dt, const uint16_t* y, const uint16_t* w, float eps, uint16_t* y_norm,
+                          int M, int N, hipStream_t st);
 hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, const int8_t* B8,
                             const float* sb, uint16_t* y, int M, int N, int r, hipStream_t st);
 

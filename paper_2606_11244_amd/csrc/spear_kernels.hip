@@ -659,6 +659,33 @@ __global__ __launch_bounds__(256) void k_ec_up_acc(const float* __restrict__ v,
   y[idx] = f2act<DT>(a);
 }
 
+// Post-EC tail, next-layer RMSNorm: y_norm[m][n] = y[m][n] * rsqrt(mean_n y[m][n]^2
+// + eps) * w[n] over the stored (rounded) row, in fp32, one rounding. One
+// workgroup of 256 threads per token row; the sum of squares is reduced in a
+// fixed order (per-thread strided sums, then a tree in LDS).
+template <int DT>
+__global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t* __restrict__ y,
+                                                 const uint16_t* __restrict__ w, float eps,
+                                                 uint16_t* __restrict__ y_norm, int N) {
+  __shared__ float red[256];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  const uint16_t* yr = y + (size_t)m * N;
+  float ss = 0.f;
+  for (int n = tid; n < N; n += 256) {
+    const float v = act2f<DT>(yr[n]);
+    ss += v * v;
+  }
+  red[tid] = ss;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (tid < h) red[tid] += red[tid + h];
+    __syncthreads();
+  }
+  const float scale = 1.f / sqrtf(red[0] / (float)N + eps);
+  uint16_t* out = y_norm + (size_t)m * N;
+  for (int n = tid; n < N; n += 256) out[n] = f2act<DT>(act2f<DT>(yr[n]) * scale * act2f<DT>(w[n]));
+}
+
 // Every workgroup of the fused grid advances its class's launch counter once
 // as it ends (see gen_increment): relaxed adds that nothing waits for.
 __device__ __forceinline__ unsigned long long* gen_counter(const GemvParams& a, int block) {
@@ -1500,6 +1527,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
         }
         v += ev;
       }
+      if (a.res) v += act2f<DT>(a.res[(size_t)m * N + n0 + row]);
       a.y[(size_t)m * N + n0 + row] = f2act<DT>(v);
     }
   }
@@ -1944,7 +1972,11 @@ __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams
 #pragma unroll
       for (int e2 = 0; e2 < 4; ++e2) {
         const int m = m0 + wm * 64 + 16 * i + 4 * lg + e2;
-        if (m < M) a.y[(size_t)m * N + n] = f2act<DT>(acc[i][j][e2]);
+        if (m < M) {
+          float v = acc[i][j][e2];
+          if (a.res) v += act2f<DT>(a.res[(size_t)m * N + n]);
+          a.y[(size_t)m * N + n] = f2act<DT>(v);
+        }
       }
     }
 }
@@ -2004,6 +2036,14 @@ hipError_t launch_gate(int dt, const EcParams& e, int ntb, size_t lds, hipStream
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(k_gate<DTC>, dim3(ntb), dim3(256), lds, st, e);
   });
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int dt, const uint16_t* y, const uint16_t* w, float eps, uint16_t* y_norm,
+                          int M, int N, hipStream_t st) {
+  if (M == 0 || N == 0) return hipSuccess;
+  SPEAR_DT_SWITCH(dt, hipLaunchKernelGGL(k_rmsnorm<DTC>, dim3(M), dim3(256), 0, st, y, w, eps,
+                                         y_norm, N));
   return hipGetLastError();
 }
 

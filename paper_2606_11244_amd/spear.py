@@ -31,6 +31,7 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
           -7: "SPEAR_E_HIP", -8: "SPEAR_E_ALIAS"}
 
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
+            "spear_w4ec_linear_tail",
             "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
             "spear_set_gemm_tile",
             "spear_status_string", "spear_version", "spear_sched_latency", "spear_sched_chunk")
@@ -58,6 +59,11 @@ class EC(ctypes.Structure):
                 ("W2", ctypes.c_void_p), ("b2", ctypes.c_void_p),
                 ("ab_format", ctypes.c_int32), ("a_scale", ctypes.c_void_p),
                 ("b_scale", ctypes.c_void_p)]
+
+
+class Tail(ctypes.Structure):
+    _fields_ = [("residual", ctypes.c_void_p), ("norm_w", ctypes.c_void_p),
+                ("eps", ctypes.c_float), ("y_norm", ctypes.c_void_p)]
 
 
 class Plan(ctypes.Structure):
@@ -100,6 +106,9 @@ def _load():
     lib.spear_w4ec_linear.argtypes = [P(Problem), ctypes.c_void_p, P(W4), P(EC), ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
     lib.spear_w4_dequant.argtypes = [P(Problem), P(W4), ctypes.c_void_p, ctypes.c_void_p]
+    lib.spear_w4ec_linear_tail.argtypes = [P(Problem), ctypes.c_void_p, P(W4), P(EC), P(Tail),
+                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                           ctypes.c_void_p]
     lib.spear_set_wait_polls.argtypes = [ctypes.c_int32]
     lib.spear_set_gemv_shape.argtypes = [ctypes.c_int32] * 3
     lib.spear_set_gemv_shape.restype = None
@@ -116,7 +125,7 @@ def _load():
     lib.spear_status_string.restype = ctypes.c_char_p
     lib.spear_version.restype = ctypes.c_char_p
     for f in ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
-              "spear_set_wait_polls"):
+              "spear_w4ec_linear_tail", "spear_set_wait_polls"):
         getattr(lib, f).restype = ctypes.c_int32
     return lib
 
@@ -191,6 +200,35 @@ def w4ec_linear(prob: Problem, x, qweight, scales, zeros, A, B, y, *, alpha=1.0,
                                _ptr(y), _ptr(workspace), ws_bytes, _stream(stream))
     if st != 0:
         raise SpearError(st, "spear_w4ec_linear")
+    return y
+
+
+def w4ec_linear_tail(prob: Problem, x, qweight, scales, zeros, y, *, ec_args=None, residual=None,
+                     norm_w=None, eps=1e-5, y_norm=None, workspace=None, stream=None):
+    """The layer plus the post-EC tail (include/spear.h): y gets the residual
+    added before its rounding, y_norm = RMSNorm(y) * norm_w. ec_args: the
+    keyword arguments of w4ec_linear for A, B and the gate (with "A" and
+    "B"), or None for the 4-bit layer alone."""
+    w = W4(_ptr(qweight).value, _ptr(scales).value, _ptr(zeros).value)
+
+    def p(t):
+        return None if t is None else t.data_ptr()
+
+    ec = None
+    if ec_args is not None:
+        a = dict(ec_args)
+        fmt = AB_INT8 if a.get("a_scale") is not None else AB_ACT
+        ec = EC(p(a["A"]), p(a["B"]), float(a.get("alpha", 1.0)), p(a.get("w_g")),
+                float(a.get("b_g", 0.0)), p(a.get("W1")), p(a.get("b1")), p(a.get("W2")),
+                p(a.get("b2")), fmt, p(a.get("a_scale")), p(a.get("b_scale")))
+    tail = Tail(p(residual), p(norm_w), float(eps), p(y_norm))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = LIB.spear_w4ec_linear_tail(ctypes.byref(prob), _ptr(x), ctypes.byref(w),
+                                    ctypes.byref(ec) if ec is not None else None,
+                                    ctypes.byref(tail), _ptr(y), _ptr(workspace), ws_bytes,
+                                    _stream(stream))
+    if st != 0:
+        raise SpearError(st, "spear_w4ec_linear_tail")
     return y
 
 
@@ -328,6 +366,19 @@ class DeviceLayer:
                            alpha=L.alpha, w_g=self.w_g, b_g=L.b_g, W1=self.W1, b1=self.b1,
                            W2=self.W2, b2=self.b2, a_scale=self.a_scale, b_scale=self.b_scale,
                            workspace=workspace, stream=stream)
+
+    def run_tail(self, prob, workspace, residual=None, norm_w=None, eps=1e-5, y_norm=None,
+                 with_ec=True, stream=None, y=None):
+        L = self.layer
+        y = self.y if y is None else y
+        ec_args = None
+        if with_ec:
+            ec_args = dict(A=self.A, B=self.B, alpha=L.alpha, w_g=self.w_g, b_g=L.b_g,
+                           W1=self.W1, b1=self.b1, W2=self.W2, b2=self.b2,
+                           a_scale=self.a_scale, b_scale=self.b_scale)
+        return w4ec_linear_tail(prob, self.x, self.qweight, self.scales, self.zeros, y,
+                                ec_args=ec_args, residual=residual, norm_w=norm_w, eps=eps,
+                                y_norm=y_norm, workspace=workspace, stream=stream)
 
     def run_w4(self, prob, workspace, stream=None, y=None):
         y = self.y if y is None else y

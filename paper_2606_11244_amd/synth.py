@@ -210,6 +210,17 @@ def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
                  W2=to_bits(W2, act_dtype), b2=to_bits(b2, act_dtype), **i8)
 
 
+def make_tail(layer: Layer, seed: int = 0, eps: float = 1e-5):
+    """Inputs of the post-EC tail for a layer, from a seed stream of their
+    own (the layer's draws are unchanged): a residual ~ N(0, 1) [M][N] and
+    an RMSNorm weight ~ N(1, 0.1) [N], both as activation-dtype bits."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 77, layer.M, layer.N]))
+    res = rng.standard_normal((layer.M, layer.N), dtype=np.float32)
+    w = (1.0 + 0.1 * rng.standard_normal(layer.N)).astype(np.float32)
+    return dict(residual=to_bits(res, layer.act_dtype), norm_w=to_bits(w, layer.act_dtype),
+                eps=float(eps))
+
+
 # ---------------------------------------------------------------------------
 # Workload configurations (synthetic stand-ins for the paper's Llama layers;
 # no trained weights are used).

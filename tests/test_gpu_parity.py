@@ -427,3 +427,61 @@ def test_gemm_token_tiles(tile, M, N, K, dt, G):
     finally:
         sp.set_gemm_slices(0)
         sp.set_gemm_tile(0)
+
+
+# ---------------------------------------------------------------------------
+# post-EC tail: residual addition + next-layer RMSNorm
+# ---------------------------------------------------------------------------
+
+def _tail_check(L, path, with_ec=True, in_place=False, tile=0):
+    from paper_2606_11244_amd import spear as sp
+    t = S.make_tail(L, seed=3)
+    dt = sp._TORCH_DT[L.act_dtype]
+    res = torch.from_numpy(t["residual"].view(np.int16)).view(dt).cuda()
+    nw = torch.from_numpy(t["norm_w"].view(np.int16)).view(dt).cuda()
+    dl = sp.DeviceLayer(L)
+    prob = dl.problem(force_path=path)
+    y_norm = torch.empty_like(dl.y)
+    if in_place:
+        dl.y.copy_(res)
+        res = dl.y
+    sp.set_gemm_tile(tile)  # before sizing the workspace: the plan depends on it
+    try:
+        ws = sp.allocate_workspace(prob, with_ec)
+        dl.run_tail(prob, ws, residual=res, norm_w=nw, eps=t["eps"], y_norm=y_norm,
+                    with_ec=with_ec)
+    finally:
+        sp.set_gemm_tile(0)
+    torch.cuda.synchronize()
+    y_ref = O.w4ec_linear(L) if with_ec else O.w4_linear_layer(L)
+    h_ref, n_ref = O.post_ec_tail(y_ref, S.from_bits(t["residual"], L.act_dtype),
+                                  S.from_bits(t["norm_w"], L.act_dtype), t["eps"])
+    assert_parity(dl.y.float().cpu().numpy().astype(np.float64), h_ref, f"tail h path={path}")
+    assert_parity(y_norm.float().cpu().numpy().astype(np.float64), n_ref, f"tail norm path={path}")
+
+
+@pytest.mark.parametrize("M,N,K,G,dt,rank", [
+    (1, 520, 1024, 128, S.F16, 16), (4, 256, 2048, 0, S.BF16, 8), (17, 300, 1024, 128, S.F16, 16),
+    (3, 256, 1024, 128, S.F16, 32), (65, 200, 1024, 128, S.F16, 16), (300, 520, 2048, 0, S.BF16, 16),
+])
+def test_post_ec_tail_all_paths(M, N, K, G, dt, rank):
+    """The residual is added in every path's final store and the RMSNorm
+    follows in the same call: both outputs meet the bar against the oracle's
+    float64 tail on the exact layer output; also for the 4-bit layer alone."""
+    L = S.make_layer(M=M, N=N, K=K, group_size=G, rank=rank, act_dtype=dt, seed=M + N,
+                     ec_std=0.05)
+    for p in _paths_for(M, L):
+        log(f"tail M={M} N={N} K={K} dt={dt} r={rank} path={p}")
+        _tail_check(L, p)
+    _tail_check(L, 0, with_ec=False)
+
+
+@pytest.mark.parametrize("tile", [128, 256])
+def test_post_ec_tail_in_place_and_tiles(tile):
+    """An in-place residual stream (the residual is y itself) on the prefill
+    GEMM with either token tile, and on decode."""
+    L = S.make_layer(M=300, N=256, K=1024, group_size=128, rank=16, seed=9, ec_std=0.05)
+    _tail_check(L, 4, in_place=True, tile=tile)
+    _tail_check(L, 0, with_ec=False, in_place=True, tile=tile)
+    Ld = S.make_layer(M=2, N=256, K=1024, group_size=128, rank=16, seed=10, ec_std=0.05)
+    _tail_check(Ld, 0, in_place=True)

@@ -443,12 +443,46 @@ def check_int8_golden(o) -> bool:
     return np.array_equal(y, np.array(e["want"]))
 
 
+def check_tail_golden(o) -> bool:
+    """Hand-worked residual + RMSNorm (tests/golden/post_ec_tail.json)."""
+    g = _load("post_ec_tail.json")
+    h, yn = o.post_ec_tail(np.array(g["y"]), np.array(g["residual"]), np.array(g["norm_w"]),
+                           g["eps"])
+    return np.array_equal(h, np.array(g["h"])) and np.array_equal(yn, np.array(g["y_norm"]))
+
+
+def check_tail_properties(o, seed=0) -> bool:
+    """RMSNorm facts: a constant row c gives c w / sqrt(c^2 + eps); at eps = 0
+    the normalised row (before the weight) has mean square 1 and the result
+    does not change when the row is scaled; residual None equals a zero
+    residual; the residual enters once."""
+    rng = np.random.default_rng(seed)
+    w = rng.normal(1.0, 0.2, size=6)
+    for c in (3.0, -0.25):
+        _, yn = o.post_ec_tail(np.full((1, 6), c), None, w, 0.5)
+        if not np.allclose(yn[0], c * w / math.sqrt(c * c + 0.5), rtol=1e-15, atol=0):
+            return False
+    y = rng.normal(size=(5, 6))
+    r = rng.normal(size=(5, 6))
+    _, a = o.post_ec_tail(y, r, np.ones(6), 0.0)
+    if not np.allclose(np.mean(a * a, axis=1), 1.0, rtol=1e-14):
+        return False
+    _, b = o.post_ec_tail(7.5 * y, 7.5 * r, np.ones(6), 0.0)
+    if not np.allclose(a, b, rtol=1e-14):
+        return False
+    h0, n0 = o.post_ec_tail(y, None, w, 1e-3)
+    h1, n1 = o.post_ec_tail(y, np.zeros_like(y), w, 1e-3)
+    h2, _ = o.post_ec_tail(y, r, w, 1e-3)
+    return (np.array_equal(h0, h1) and np.array_equal(n0, n1)
+            and np.allclose(h2, y + r, rtol=0, atol=1e-15))
+
+
 PINS = [check_unpack_fixed_words, check_unpack_exhaustive, check_golden_examples,
         check_rounding_fixtures, check_rtn_grid_roundtrip, check_rtn_error_bound,
         check_brute_force, check_integer_grid_exact, check_reductions,
         check_sigmoid_half, check_tanh_static_lora, check_factored_form,
         check_gate_ranges, check_dequant_bits_contract, check_int8_brute_force,
-        check_int8_golden]
+        check_int8_golden, check_tail_golden, check_tail_properties]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -549,6 +583,20 @@ def _int8_scale_fp16(q, scale):
     return s16[:, None] * np.asarray(q, np.float64)
 
 
+def _tail_no_residual(y, residual, norm_w, eps):
+    return O.post_ec_tail(y, None, norm_w, eps)
+
+
+def _tail_sum_not_mean(y, residual, norm_w, eps):
+    h = np.asarray(y, np.float64) + (0 if residual is None else np.asarray(residual, np.float64))
+    return h, h / np.sqrt(np.sum(h * h, axis=1, keepdims=True) + eps) * np.asarray(norm_w)[None, :]
+
+
+def _tail_eps_outside(y, residual, norm_w, eps):
+    h = np.asarray(y, np.float64) + (0 if residual is None else np.asarray(residual, np.float64))
+    return h, h / (np.sqrt(np.mean(h * h, axis=1, keepdims=True)) + eps) * np.asarray(norm_w)[None, :]
+
+
 MUTANTS = {
     "nibble order reversed": dict(unpack_int4=_unpack_reversed),
     "zero point added": dict(dequant=_dequant_plus_zero),
@@ -562,6 +610,9 @@ MUTANTS = {
     "weight operand not transposed": dict(w4_linear=_w4_linear_transposed_b),
     "INT8 scale dropped": dict(dequant_int8=_int8_scale_dropped),
     "INT8 scale rounded to fp16": dict(dequant_int8=_int8_scale_fp16),
+    "tail drops the residual": dict(post_ec_tail=_tail_no_residual),
+    "RMSNorm divides by the sum": dict(post_ec_tail=_tail_sum_not_mean),
+    "RMSNorm epsilon outside the root": dict(post_ec_tail=_tail_eps_outside),
 }
 
 
