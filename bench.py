@@ -289,6 +289,8 @@ def main():
     ap.add_argument("--no-70b", action="store_true", help="skip the 70B-layer context line")
     ap.add_argument("--no-int8", action="store_true",
                     help="skip the passes with INT8 per-channel EC factors")
+    ap.add_argument("--no-tail", action="store_true",
+                    help="skip the passes with the post-EC tail on o and down")
     ap.add_argument("--model70b", action="store_true",
                     help="also time the 70B-shaped model's linear layers (80 layers resident, "
                          "about 36 GB) at M = 1 .. 8192")
@@ -474,6 +476,43 @@ def main():
             int8["prefill_overhead"] = round(p8 / p4 - 1.0, 4)
             int8["decode_ec_byte_share"] = round(dec_bytes_i8 / dec_bytes_w4 - 1.0, 4)
 
+    # ---- the same EC passes with the post-EC tail where a decoder layer has
+    # it: after o and down, the residual added in place and the next
+    # RMSNorm (the other modules unchanged)
+    tail = None
+    if not args.no_tail:
+        print("bench: post-EC tail passes", file=sys.stderr, flush=True)
+        hid = torch.randn((4096 * 2048,), device=dev).half()
+        nrm_w = torch.ones((2048,), device=dev).half()
+        nrm_out = torch.empty((4096 * 2048,), dtype=torch.float16, device=dev)
+        tail_mods = {"o", "down"}
+
+        def call(d, ws_t, M):
+            if d.layer_name in tail_mods:
+                res = hid[:M * d.N].view(M, d.N)
+                d.run_tail(d.problem(), ws_t, residual=res, norm_w=nrm_w, eps=1e-5,
+                           y_norm=nrm_out[:M * d.N].view(M, d.N), y=res)
+            else:
+                d.run_ec(d.problem(), ws_t)
+
+        for c in range(args.copies):
+            for mods in dec_dev[c]:
+                for j, d in enumerate(mods):
+                    d.layer_name = S.MODULES[j]
+        for j, d in enumerate(pre_dev):
+            d.layer_name = S.MODULES[j]
+        g_dec_t = [capture(lambda c=c: [call(d, dec_ws_t, 1) for mods in dec_dev[c] for d in mods])
+                   for c in range(args.copies)]
+        g_pre_t = capture(lambda: [call(d, pre_ws_t, 4096) for d in pre_dev])
+        run_steps(args.warmup, g_dec_t, g_pre_t, False)
+        evt = run_steps(args.steps, g_dec_t, g_pre_t, True)
+        torch.cuda.synchronize()
+        dt_ = float(np.mean([a.elapsed_time(b) for a, b, _ in evt])) * 1e-3
+        pt_ = float(np.mean([b.elapsed_time(c) for _, b, c in evt])) * 1e-3
+        tail = {"modules": "o, down (residual in place + RMSNorm of the 2048-wide hidden state)",
+                "decode_ms_per_pass": round(dt_ * 1e3, 4), "prefill_ms_per_pass": round(pt_ * 1e3, 4),
+                "decode_added": round(dt_ / dec_s - 1.0, 4), "prefill_added": round(pt_ / pre_s - 1.0, 4)}
+
     model70 = None
     if args.model70b:
         print("bench: 70B-shaped model pass", file=sys.stderr, flush=True)
@@ -546,6 +585,7 @@ def main():
         "model_70b": model70,
         "ec_overhead": overhead,
         "ec_int8": int8,
+        "post_ec_tail": tail,
     }
     if not args.no_cpu_baseline:
         print("bench: CPU oracle baseline", file=sys.stderr, flush=True)

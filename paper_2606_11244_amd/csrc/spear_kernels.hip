@@ -1032,6 +1032,19 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
   const rsrc_t rb = kI8 ? make_rsrc(a.B8, (uint32_t)N * r) : make_rsrc(a.B, (uint32_t)N * r * 2);
 
+  // The residual of the post-EC tail: when the block's outputs are at most
+  // one per thread (decode), each thread's element is fetched here with the
+  // other prologue loads instead of right before its store. The load is
+  // issued unconditionally (out of range, it reads nothing): a branch around
+  // it would make the wait before the first compute cover every prologue load.
+  const bool res_pre = a.res != nullptr && RB * M <= (int)blockDim.x;
+  uint32_t resv;
+  {
+    const int m = tid / RB, row = tid - (tid / RB) * RB;
+    const rsrc_t rres = make_rsrc(a.res, a.res ? (uint32_t)M * N * 2 : 0u);
+    resv = bld16(rres, res_pre && tid < RB * M && n0 + row < N
+                           ? ((uint32_t)m * N + n0 + row) * 2 : kOOB);
+  }
   // the rows of B ([RB][r], contiguous) of the block that adds v B^T (the
   // first K-slice's with an EC wave; any slice's in EPI_LOCAL, whose last
   // arriver adds it) are fetched up front into LDS when two 16-byte chunks
@@ -1527,7 +1540,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
         }
         v += ev;
       }
-      if (a.res) v += act2f<DT>(a.res[(size_t)m * N + n0 + row]);
+      if (a.res) v += act2f<DT>(res_pre ? resv : a.res[(size_t)m * N + n0 + row]);
       a.y[(size_t)m * N + n0 + row] = f2act<DT>(v);
     }
   }
