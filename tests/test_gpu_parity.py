@@ -485,3 +485,69 @@ def test_post_ec_tail_in_place_and_tiles(tile):
     _tail_check(L, 0, with_ec=False, in_place=True, tile=tile)
     Ld = S.make_layer(M=2, N=256, K=1024, group_size=128, rank=16, seed=10, ec_std=0.05)
     _tail_check(Ld, 0, in_place=True)
+
+
+@pytest.mark.parametrize("M,path,int8,tail", [(1, 5, True, False), (4, 1, True, True),
+                                              (200, 2, True, False), (300, 4, False, True),
+                                              (2, 5, False, True)])
+def test_graph_replay_int8_and_tail(M, path, int8, tail):
+    """Graph replays of the INT8-factor paths and of the tail call: every
+    replay, with new activations written by eager work between replays,
+    equals the eager call bit for bit (the tail's residual is its own
+    buffer here, rewritten with the activations)."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=M, N=1024, K=2048, group_size=128, rank=16, seed=M + path + 50,
+                     ab_int8=int8)
+    dl = sp.DeviceLayer(L)
+    prob = dl.problem(force_path=path)
+    ws = sp.allocate_workspace(prob)
+    res = torch.randn(dl.y.shape, device="cuda").to(dl.y.dtype)
+    nw = torch.ones((L.N,), device="cuda").to(dl.y.dtype)
+    yn = torch.empty_like(dl.y)
+    yn_eager = torch.empty_like(dl.y)
+    y_eager = torch.empty_like(dl.y)
+
+    def call(y, y_norm, stream=None):
+        if tail:
+            dl.run_tail(prob, ws, residual=res, norm_w=nw, eps=1e-5, y_norm=y_norm, y=y,
+                        stream=stream)
+        else:
+            dl.run_ec(prob, ws, y=y, stream=stream)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        call(dl.y, yn, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(dl.y, yn)
+    gen = torch.Generator(device="cuda").manual_seed(M + 1)
+    for i in range(4):
+        dl.x.copy_(torch.randn(dl.x.shape, generator=gen, device="cuda").to(dl.x.dtype))
+        res.copy_(torch.randn(res.shape, generator=gen, device="cuda").to(res.dtype))
+        torch.cuda.synchronize()
+        log(f"graph int8={int8} tail={tail} M={M} path={path} replay={i}")
+        g.replay()
+        torch.cuda.synchronize()
+        y_graph, yn_graph = dl.y.clone(), yn.clone()
+        call(y_eager, yn_eager)
+        torch.cuda.synchronize()
+        assert torch.equal(y_graph, y_eager), f"replay {i}"
+        if tail:
+            assert torch.equal(yn_graph, yn_eager), f"replay {i} norm"
+
+
+@pytest.mark.parametrize("path", [5, 1, 2, 4])
+def test_int8_deterministic(path):
+    """INT8-factor calls are bit-identical from call to call."""
+    from paper_2606_11244_amd import spear as sp
+    M = 130 if path in (2, 4) else 3
+    L = S.make_layer(M=M, N=1024, K=8192, group_size=128, rank=16, seed=61, ab_int8=True)
+    dl = sp.DeviceLayer(L)
+    ws = sp.allocate_workspace(dl.problem(force_path=path))
+    first = gpu_y(L, path, workspace=ws, dev=dl)
+    for _ in range(3):
+        assert np.array_equal(first, gpu_y(L, path, workspace=ws, dev=dl))
+    assert_parity(first, O.w4ec_linear(L), f"int8 determinism {path}")
