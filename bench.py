@@ -103,6 +103,25 @@ def cpu_baseline(dec_layers, pre_layer, budget_s=12.0):
     ts = time.perf_counter()
     O.w4ec_linear(pre_layer)
     t_pre = time.perf_counter() - ts
+    # single-threaded: the tiny workload and the 1B q module at M = 1
+    single = None
+    try:
+        from threadpoolctl import threadpool_limits
+        from paper_2606_11244_amd import synth as S
+        tiny = S.config_layer(0, "tiny", 4, seed=0)
+        with threadpool_limits(limits=1):
+            out = {}
+            for name, LL, n in (("tiny", tiny, 20), ("1b_q_m1", dec_layers[0], 2)):
+                ts = time.perf_counter()
+                for _ in range(n):
+                    O.w4ec_linear(LL)
+                dt = (time.perf_counter() - ts) / n
+                out[name] = {"ms_per_call": round(dt * 1e3, 3),
+                             "GBps": round(algo_bytes(LL.M, LL.N, LL.K, LL.group_size, LL.rank)
+                                           / dt / 1e9, 4)}
+        single = out
+    except Exception as exc:  # noqa: BLE001
+        single = {"error": str(exc)[:80]}
     L = pre_layer
     return {
         "value": round(nbytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": int(blas),
@@ -112,6 +131,7 @@ def cpu_baseline(dec_layers, pre_layer, budget_s=12.0):
                    f"M={L.M} ({t_pre:.1f} s)"),
         "prefill_tflops": round(algo_flops(L.M, L.N, L.K, L.rank) / t_pre / 1e12, 5),
         "host_cpus": os.cpu_count(),
+        "single_thread": single,
     }
 
 
@@ -189,27 +209,13 @@ def model_70b_pass(sp, torch, dev, Ms=(1, 16, 64, 512, 4096, 8192), reps=3):
     seeded 25% of the (layer, module) pairs and the 4-bit product alone on
     the rest, every call on its AUTO path; the same pass with no EC at all
     gives the model's EC overhead. Each pass is one captured graph."""
+    from paper_2606_11244_amd import model70b
     from paper_2606_11244_amd import synth as S
-    g = torch.Generator(device=dev)
-    g.manual_seed(0)
-    r, G = 64, 128
-    sel = S.ec_selection_70b(seed=0)
-    layers = []
-    for l in range(sel.shape[0]):
-        mods = []
-        for j, m in enumerate(S.MODULES):
-            K, N = S.LLAMA_70B[m]
-            q = torch.randint(-2**31, 2**31 - 1, (N, K // 8), dtype=torch.int32, device=dev, generator=g)
-            sc = (torch.rand((N, K // G), device=dev, generator=g) * 1e-3 + 1e-4).half().view(torch.int16)
-            zr = torch.randint(0, 16, (N, K // G), dtype=torch.uint8, device=dev, generator=g)
-            ec = None
-            if sel[l, j]:
-                ec = ((torch.randn((r, K), device=dev, generator=g) * 0.01).half(),
-                      (torch.randn((N, r), device=dev, generator=g) * 0.01).half(),
-                      (torch.randn((K,), device=dev, generator=g) * 0.05).half())
-            mods.append((m, K, N, q, sc, zr, ec))
-        layers.append(mods)
+    r, G = model70b.RANK, model70b.GROUP
+    layers, sel = model70b.build(dev)
     Kmax, Nmax, Mmax = max(k for k, _ in S.LLAMA_70B.values()), max(n for _, n in S.LLAMA_70B.values()), max(Ms)
+    g = torch.Generator(device=dev)
+    g.manual_seed(1)
     xbuf = torch.randn((Mmax * Kmax,), device=dev, generator=g).half()
     ybuf = torch.empty((Mmax * Nmax,), dtype=torch.float16, device=dev)
     out = {"weights": "device-random (timing only)",
