@@ -226,6 +226,47 @@ spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x
                                       const spear_tail_t* tail, void* y, void* workspace,
                                       size_t workspace_bytes, void* hip_stream);
 
+/* ---- Grouped calls ---------------------------------------------------------
+ * At decode a layer call is a few microseconds of latency around a few MB of
+ * weights (section 4.2: kernel launches dominate at small M), and the modules
+ * of a transformer block that read the same hidden state (q, k, v; gate, up)
+ * are independent calls. A group runs up to SPEAR_GROUP_MAX such calls as one
+ * launch when all of them take the same single-launch GEMV variant: the 4-bit
+ * product alone (ec NULL) or the fused local path (every member M <= 32 with
+ * an elementwise gate and rank <= 16, or forced to it; same act dtype, token
+ * tiles and row tiles). Otherwise the members run one after another in array
+ * order, each on its own planned path. Either way each member's Y is exactly
+ * (bit for bit) what its own spear_w4ec_linear or spear_w4_linear call
+ * writes. */
+#define SPEAR_GROUP_MAX 4
+
+/* One member: a problem and its operands as in spear_w4ec_linear; ec NULL
+ * runs the 4-bit product alone (spear_w4_linear). Host struct; the pointers
+ * inside follow the single calls' conventions. */
+typedef struct {
+  const spear_problem_t* prob;
+  const void* x;
+  const spear_w4_t* w;
+  const spear_ec_t* ec; /* or NULL */
+  void* y;
+} spear_layer_call_t;
+
+/* Workspace bytes of a group: each member's plan's workspace_bytes rounded
+ * up to 256, summed in array order (member i uses the slice at the sum of
+ * the earlier members' sizes). Host-only. SPEAR_E_SHAPE for n outside
+ * [1, SPEAR_GROUP_MAX], and every code spear_dispatch_plan returns for a
+ * member. */
+spear_status_t spear_group_workspace(int32_t n, const spear_layer_call_t* calls, size_t* out_bytes);
+
+/* Runs the n members (see above) on hip_stream. Validation of every member
+ * (the single calls' checks) happens before any launch; in addition each
+ * member's Y may not overlap any buffer of another member (SPEAR_E_ALIAS);
+ * members may share X. Members with M == 0 or N == 0 are skipped. The
+ * workspace follows spear_group_workspace; concurrent groups need separate
+ * workspaces. */
+spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* calls, void* workspace,
+                                       size_t workspace_bytes, void* hip_stream);
+
 /* Diagnostic of the dequantisation the kernels use: writes
  * w_out[n][k] = RNE_act((q[n][k] - z[n][k/G]) * s[n][k/G]) as a dense [N][K]
  * act-dtype matrix, the exact product rounded once to nearest even

@@ -693,6 +693,57 @@ spear_status_t run_layer(const spear_problem_t* prob, const Resolved& z, const v
                                      (uint16_t*)y, (int)prob->M, (int)prob->N, z.r, s));
 }
 
+// ---- grouped calls --------------------------------------------------------
+
+size_t round256(size_t b) { return (b + 255) / 256 * 256; }
+
+// y of one member against every buffer another member reads or writes
+bool hits_member(const void* y, size_t yb, const spear_layer_call_t& c) {
+  const spear_problem_t* p = c.prob;
+  const size_t G = p->group_size == 0 ? (size_t)p->K : (size_t)p->group_size;
+  if (overlaps(y, yb, c.x, (size_t)p->M * p->K * 2) || overlaps(y, yb, c.y, (size_t)p->M * p->N * 2) ||
+      overlaps(y, yb, c.w->qweight, (size_t)p->N * p->K / 2) ||
+      overlaps(y, yb, c.w->scales, (size_t)p->N * (p->K / G) * 2) ||
+      overlaps(y, yb, c.w->zeros, (size_t)p->N * (p->K / G)))
+    return true;
+  const spear_ec_t* ec = c.ec;
+  if (!ec || p->rank == 0) return false;
+  const size_t eb = ec->ab_format == SPEAR_AB_INT8 ? 1 : 2;
+  const size_t r = (size_t)p->rank;
+  const size_t h = p->gate_hidden > 0 ? (size_t)p->gate_hidden : 4 * r;
+  return overlaps(y, yb, ec->A, r * p->K * eb) || overlaps(y, yb, ec->B, (size_t)p->N * r * eb) ||
+         overlaps(y, yb, ec->a_scale, r * 4) || overlaps(y, yb, ec->b_scale, (size_t)p->N * 4) ||
+         overlaps(y, yb, ec->w_g, (size_t)p->K * 2) || overlaps(y, yb, ec->W1, h * r * 2) ||
+         overlaps(y, yb, ec->b1, h * 2) || overlaps(y, yb, ec->W2, r * h * 2) ||
+         overlaps(y, yb, ec->b2, r * 2);
+}
+
+// The kernel variant a resolved member runs when it is a single GEMV launch
+// without cross-launch state (the 4-bit product alone or the local EC
+// variant); -1 otherwise.
+int group_epi(const Resolved& z, const spear_ec_t* ec) {
+  if (!z.gemv) return -1;
+  if (!z.ec) return EPI_NONE;
+  if (z.plan.path == SPEAR_PATH_FUSED_LOCAL) return ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL;
+  return -1;
+}
+
+spear_status_t group_resolve(int32_t n, const spear_layer_call_t* calls, Resolved* z,
+                             size_t* off, size_t* total) {
+  if (!calls || (n > 0 && !total)) return SPEAR_E_NULL;
+  if (n < 1 || n > SPEAR_GROUP_MAX) return SPEAR_E_SHAPE;
+  size_t sum = 0;
+  for (int i = 0; i < n; ++i) {
+    if (!calls[i].prob) return SPEAR_E_NULL;
+    const spear_status_t st = resolve(calls[i].prob, calls[i].ec != nullptr, &z[i]);
+    if (st != SPEAR_OK) return st;
+    off[i] = sum;
+    sum += round256(z[i].plan.workspace_bytes);
+  }
+  *total = sum;
+  return SPEAR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -762,6 +813,76 @@ spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x
   return hip_status(launch_rmsnorm(z.dt, (const uint16_t*)y, (const uint16_t*)tail->norm_w,
                                    tail->eps, (uint16_t*)tail->y_norm, (int)prob->M,
                                    (int)prob->N, s));
+}
+
+spear_status_t spear_group_workspace(int32_t n, const spear_layer_call_t* calls, size_t* out_bytes) {
+  if (!out_bytes) return SPEAR_E_NULL;
+  Resolved z[SPEAR_GROUP_MAX];
+  size_t off[SPEAR_GROUP_MAX];
+  return group_resolve(n, calls, z, off, out_bytes);
+}
+
+spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* calls, void* workspace,
+                                       size_t workspace_bytes, void* hip_stream) {
+  Resolved z[SPEAR_GROUP_MAX];
+  size_t off[SPEAR_GROUP_MAX], total = 0;
+  spear_status_t st = group_resolve(n, calls, z, off, &total);
+  if (st != SPEAR_OK) return st;
+  if (total > 0) {
+    if (!workspace || workspace_bytes < total) return SPEAR_E_WORKSPACE;
+    if (misaligned(workspace)) return SPEAR_E_ALIGN;
+  }
+  char* ws = (char*)workspace;
+  for (int i = 0; i < n; ++i) {
+    const spear_layer_call_t& c = calls[i];
+    const spear_problem_t* p = c.prob;
+    if (p->M == 0 || p->N == 0) continue;
+    if ((st = check_w4(p, c.x, c.w, c.y)) != SPEAR_OK) return st;
+    if (c.ec && (st = check_ec(p, z[i], c.ec, c.y)) != SPEAR_OK) return st;
+    const size_t yb = (size_t)p->M * p->N * 2;
+    if (overlaps(c.y, yb, workspace, total)) return SPEAR_E_ALIAS;
+    for (int j = 0; j < n; ++j)
+      if (j != i && calls[j].prob->M > 0 && calls[j].prob->N > 0 && hits_member(c.y, yb, calls[j]))
+        return SPEAR_E_ALIAS;
+  }
+  hipStream_t s = (hipStream_t)hip_stream;
+  // one launch when every member runs the same single-launch GEMV variant
+  int epi = group_epi(z[0], calls[0].ec);
+  bool one = n > 1 && epi >= 0;
+  for (int i = 1; i < n && one; ++i)
+    one = group_epi(z[i], calls[i].ec) == epi && z[i].dt == z[0].dt && z[i].MT == z[0].MT &&
+          z[i].RT == z[0].RT && z[i].NW == z[0].NW;
+  if (!one) {
+    for (int i = 0; i < n; ++i) {
+      const spear_layer_call_t& c = calls[i];
+      if (c.prob->M == 0 || c.prob->N == 0) continue;
+      st = run_layer(c.prob, z[i], c.x, c.w, c.ec, c.y, nullptr, ws ? ws + off[i] : nullptr, s);
+      if (st != SPEAR_OK) return st;
+    }
+    return SPEAR_OK;
+  }
+  GemvGroup g;
+  std::memset(&g, 0, sizeof(g));
+  g.n = n;
+  size_t lds = 0;
+  for (int i = 0; i < n; ++i) {
+    const spear_layer_call_t& c = calls[i];
+    char* wsi = ws ? ws + off[i] : nullptr;
+    const bool live = c.prob->M > 0 && c.prob->N > 0;
+    g.start[i + 1] = g.start[i] + (live ? z[i].nrg * z[i].S : 0);
+    if (!live) {
+      g.p[i].S = 1;
+      continue;
+    }
+    GemvParams& q = g.p[i];
+    q = make_gemv(c.prob, z[i], c.x, c.w, c.y, z[i].ec ? c.ec : nullptr, wsi);
+    if (z[i].ec) {
+      q.ec = make_ec(c.prob, z[i], c.x, c.ec, wsi);
+      if (z[i].S > 1) q.eupart = (float*)(wsi + z[i].off_eupart);
+    }
+    lds = std::max(lds, z[i].lds_gemv);
+  }
+  return hip_status(launch_gemv_group(z[0].dt, z[0].MT, z[0].RT, epi, g, 64 * z[0].NW, lds, s));
 }
 
 spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w, void* w_out,

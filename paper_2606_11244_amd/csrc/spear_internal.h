@@ -139,6 +139,15 @@ struct GemvParams {
   EcParams ec;
 };
 
+// Independent GEMV layer calls launched as one grid (up to kGroupMax of them,
+// one kernel variant): member i owns workgroups [start[i], start[i+1]).
+constexpr int kGroupMax = 4;
+struct GemvGroup {
+  GemvParams p[kGroupMax];
+  int start[kGroupMax + 1];
+  int n;
+};
+
 struct GemmParams {
   const uint32_t* qw;
   const uint16_t* sc;
@@ -201,6 +210,8 @@ hipError_t launch_ec(int dt, const EcParams& e, int grid, int block, int ipp, si
 bool gemv_shape_supported(int MT, int RT);
 hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, int block,
                        size_t lds, hipStream_t st);
+hipError_t launch_gemv_group(int dt, int MT, int RT, int epi, const GemvGroup& g, int block,
+                             size_t lds, hipStream_t st);
 hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st);
 hipError_t launch_gate(int dt, const EcParams& e, int ntb, size_t lds, hipStream_t st);
 // y_norm[m] = RMSNorm(y[m]) * w (one workgroup per token row)

@@ -511,7 +511,7 @@ __device__ void ec_gate_tile(const EcParams& e, int cnt, const float* u_lds, flo
 // (the prefill GEMM epilogue) and/or as tagged words in one copy per XCD (the
 // fused kernel's consumers).
 template <int DT, int IPP>
-__device__ void ec_producer(const EcParams& e, int b, uint32_t gen, char* smem) {
+__device__ __forceinline__ void ec_producer(const EcParams& e, int b, uint32_t gen, char* smem) {
   __shared__ int s_last;
   const int tid = threadIdx.x, nthr = blockDim.x;
   const int NW = nthr >> 6;
@@ -993,8 +993,7 @@ __device__ void ec_wave(const GemvParams& a, uint32_t gen, char* smem, int n0, b
 // others' EC waves wait for what they publish.
 // ---------------------------------------------------------------------------
 template <int DT, int MT, int RT, int EPI>
-__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+__device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* smem) {
   __shared__ int s_flag;
   constexpr bool kEC = EPI == EPI_READY || EPI == EPI_FUSED;  // with an EC wave
   constexpr bool kLoc = EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8;
@@ -1004,7 +1003,6 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   const int NW = (blockDim.x >> 6) - (kEC ? 1 : 0);           // GEMV waves
   const bool gw = wave < NW;
   const int lr = lane & 15, lg = lane >> 4;
-  int bid = blockIdx.x;
   uint32_t gen = 0;
   if constexpr (EPI == EPI_FUSED) {
     gen = (uint32_t)(__hip_atomic_load(gen_counter(a, bid), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> 32);
@@ -1545,6 +1543,29 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
     }
   }
   if constexpr (EPI == EPI_FUSED) fused_exit(a);
+}
+
+template <int DT, int MT, int RT, int EPI>
+__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  gemv_body<DT, MT, RT, EPI>(a, blockIdx.x, smem);
+}
+
+// Several independent layer calls of one GEMV variant in one launch: member i
+// owns the workgroups [start[i], start[i+1]) and runs exactly the blocks its
+// own launch would run, so each member's output is the one its single call
+// writes. The member index is uniform over the workgroup.
+template <int DT, int MT, int RT, int EPI>
+__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv_group(GemvGroup g) {
+  static_assert(EPI == EPI_NONE || EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8,
+                "grouped launches take the variants without cross-launch state");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int b = blockIdx.x;
+  int i = 0;
+#pragma unroll
+  for (int j = 1; j < kGroupMax; ++j)
+    if (j < g.n && b >= g.start[j]) i = j;
+  gemv_body<DT, MT, RT, EPI>(g.p[i], b - g.start[i], smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -2118,6 +2139,47 @@ hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int
                         : gemv_launch<DT_BF16, mt, rt>(epi, p, grid, block, lds, st);
   SPEAR_GEMV_SHAPES(SPEAR_GEMV_CASE)
 #undef SPEAR_GEMV_CASE
+  return hipErrorInvalidValue;
+}
+
+template <int DT, int MT, int RT>
+static hipError_t gemv_group_launch(int epi, const GemvGroup& g, int block, size_t lds,
+                                    hipStream_t st) {
+  const int grid = g.start[g.n];
+  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv_group<DT, MT, RT, EPI_NONE>, lds)
+                   : epi == EPI_LOCAL ? allow_lds(k_gemv_group<DT, MT, RT, EPI_LOCAL>, lds)
+                                      : allow_lds(k_gemv_group<DT, MT, RT, EPI_LOCAL_I8>, lds);
+  if (err != hipSuccess) return err;
+  if (epi == EPI_NONE)
+    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_NONE>), dim3(grid), dim3(block), lds, st, g);
+  else if (epi == EPI_LOCAL)
+    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_LOCAL>), dim3(grid), dim3(block), lds, st, g);
+  else
+    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_LOCAL_I8>), dim3(grid), dim3(block), lds, st,
+                       g);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_group(int dt, int MT, int RT, int epi, const GemvGroup& g, int block,
+                             size_t lds, hipStream_t st) {
+  if (g.n < 1 || g.n > kGroupMax || g.start[0] != 0 ||
+      (epi != EPI_NONE && epi != EPI_LOCAL && epi != EPI_LOCAL_I8))
+    return hipErrorInvalidValue;
+  const bool loc = epi == EPI_LOCAL || epi == EPI_LOCAL_I8;
+  for (int i = 0; i < g.n; ++i) {
+    const GemvParams& p = g.p[i];
+    if (g.start[i + 1] < g.start[i] || p.S < 1 ||
+        (p.S > 1 && (!p.ypart || !p.rb_ctr || (loc && !p.eupart))) ||
+        (epi == EPI_LOCAL_I8 && (!p.ec.A8 || !p.ec.sa || !p.B8 || !p.sb)))
+      return hipErrorInvalidValue;
+  }
+  if (g.start[g.n] == 0) return hipSuccess;
+#define SPEAR_GEMV_GROUP_CASE(mt, rt)                                                  \
+  if (MT == mt && RT == rt)                                                            \
+    return dt == DT_F16 ? gemv_group_launch<DT_F16, mt, rt>(epi, g, block, lds, st)    \
+                        : gemv_group_launch<DT_BF16, mt, rt>(epi, g, block, lds, st);
+  SPEAR_GEMV_SHAPES(SPEAR_GEMV_GROUP_CASE)
+#undef SPEAR_GEMV_GROUP_CASE
   return hipErrorInvalidValue;
 }
 

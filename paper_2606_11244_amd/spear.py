@@ -31,7 +31,7 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
           -7: "SPEAR_E_HIP", -8: "SPEAR_E_ALIAS"}
 
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
-            "spear_w4ec_linear_tail",
+            "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
             "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
             "spear_set_gemm_tile",
             "spear_status_string", "spear_version", "spear_sched_latency", "spear_sched_chunk")
@@ -64,6 +64,14 @@ class EC(ctypes.Structure):
 class Tail(ctypes.Structure):
     _fields_ = [("residual", ctypes.c_void_p), ("norm_w", ctypes.c_void_p),
                 ("eps", ctypes.c_float), ("y_norm", ctypes.c_void_p)]
+
+
+class LayerCall(ctypes.Structure):
+    _fields_ = [("prob", ctypes.POINTER(Problem)), ("x", ctypes.c_void_p),
+                ("w", ctypes.POINTER(W4)), ("ec", ctypes.POINTER(EC)), ("y", ctypes.c_void_p)]
+
+
+GROUP_MAX = 4
 
 
 class Plan(ctypes.Structure):
@@ -109,6 +117,9 @@ def _load():
     lib.spear_w4ec_linear_tail.argtypes = [P(Problem), ctypes.c_void_p, P(W4), P(EC), P(Tail),
                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                            ctypes.c_void_p]
+    lib.spear_group_workspace.argtypes = [ctypes.c_int32, P(LayerCall), P(ctypes.c_size_t)]
+    lib.spear_w4ec_linear_group.argtypes = [ctypes.c_int32, P(LayerCall), ctypes.c_void_p,
+                                            ctypes.c_size_t, ctypes.c_void_p]
     lib.spear_set_wait_polls.argtypes = [ctypes.c_int32]
     lib.spear_set_gemv_shape.argtypes = [ctypes.c_int32] * 3
     lib.spear_set_gemv_shape.restype = None
@@ -125,7 +136,8 @@ def _load():
     lib.spear_status_string.restype = ctypes.c_char_p
     lib.spear_version.restype = ctypes.c_char_p
     for f in ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
-              "spear_w4ec_linear_tail", "spear_set_wait_polls"):
+              "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
+              "spear_set_wait_polls"):
         getattr(lib, f).restype = ctypes.c_int32
     return lib
 
@@ -230,6 +242,55 @@ def w4ec_linear_tail(prob: Problem, x, qweight, scales, zeros, y, *, ec_args=Non
     if st != 0:
         raise SpearError(st, "spear_w4ec_linear_tail")
     return y
+
+
+def _ec_from_args(a):
+    def p(t):
+        return None if t is None else t.data_ptr()
+    fmt = AB_INT8 if a.get("a_scale") is not None else AB_ACT
+    return EC(p(a["A"]), p(a["B"]), float(a.get("alpha", 1.0)), p(a.get("w_g")),
+              float(a.get("b_g", 0.0)), p(a.get("W1")), p(a.get("b1")), p(a.get("W2")),
+              p(a.get("b2")), fmt, p(a.get("a_scale")), p(a.get("b_scale")))
+
+
+def _group_array(members):
+    """ctypes array of spear_layer_call_t for members = [dict(prob, x,
+    qweight, scales, zeros, y, ec_args or None)], plus the structs it points
+    to (kept alive by the caller)."""
+    n = len(members)
+    arr = (LayerCall * max(n, 1))()
+    keep = []
+    for i, m in enumerate(members):
+        w = W4(_ptr(m["qweight"]).value, _ptr(m["scales"]).value, _ptr(m["zeros"]).value)
+        ec = _ec_from_args(m["ec_args"]) if m.get("ec_args") is not None else None
+        keep += [m["prob"], w, ec]
+        arr[i].prob = ctypes.pointer(m["prob"])
+        arr[i].x = m["x"].data_ptr()
+        arr[i].w = ctypes.pointer(w)
+        arr[i].ec = ctypes.pointer(ec) if ec is not None else None
+        arr[i].y = m["y"].data_ptr()
+    return arr, keep
+
+
+def group_workspace(members) -> int:
+    """Workspace bytes of a grouped call (include/spear.h)."""
+    arr, keep = _group_array(members)
+    out = ctypes.c_size_t(0)
+    st = LIB.spear_group_workspace(len(members), arr, ctypes.byref(out))
+    if st != 0:
+        raise SpearError(st, "spear_group_workspace")
+    return out.value
+
+
+def w4ec_linear_group(members, workspace=None, stream=None):
+    """Up to GROUP_MAX independent layer calls in one launch where they share
+    a kernel variant (include/spear.h); members as in group_workspace."""
+    arr, keep = _group_array(members)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = LIB.spear_w4ec_linear_group(len(members), arr, _ptr(workspace), ws_bytes,
+                                     _stream(stream))
+    if st != 0:
+        raise SpearError(st, "spear_w4ec_linear_group")
 
 
 def w4_dequant(prob: Problem, qweight, scales, zeros, w_out, stream=None):
@@ -379,6 +440,17 @@ class DeviceLayer:
         return w4ec_linear_tail(prob, self.x, self.qweight, self.scales, self.zeros, y,
                                 ec_args=ec_args, residual=residual, norm_w=norm_w, eps=eps,
                                 y_norm=y_norm, workspace=workspace, stream=stream)
+
+    def member(self, prob, with_ec=True, y=None):
+        """This layer as a member of a grouped call."""
+        L = self.layer
+        ec_args = None
+        if with_ec and prob.rank > 0:
+            ec_args = dict(A=self.A, B=self.B, alpha=L.alpha, w_g=self.w_g, b_g=L.b_g,
+                           W1=self.W1, b1=self.b1, W2=self.W2, b2=self.b2,
+                           a_scale=self.a_scale, b_scale=self.b_scale)
+        return dict(prob=prob, x=self.x, qweight=self.qweight, scales=self.scales,
+                    zeros=self.zeros, y=self.y if y is None else y, ec_args=ec_args)
 
     def run_w4(self, prob, workspace, stream=None, y=None):
         y = self.y if y is None else y
