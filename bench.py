@@ -6,9 +6,12 @@ per layer; group-128 4-bit weights, EC rank 16 with the sigmoid-linear gate,
 fp16 activations):
 
   decode   M = 1: all 16 layers x 7 modules through the automatic dispatch
-           (the fused single-kernel path). Two distinct copies of the model
-           weights alternate between steps (2 x 0.53 GB), so the weights come
-           from HBM rather than the 256 MB Infinity Cache.
+           (the fused single-kernel path), the modules that read one hidden
+           state launched together (per layer: q, k, v in one grouped call;
+           o; gate, up in one grouped call; down). Two distinct copies of the
+           model weights alternate between steps (2 x 0.53 GB), so the
+           weights come from HBM rather than the 256 MB Infinity Cache. The
+           same pass with one call per module is reported beside it.
   prefill  M = 4096 tokens (1% of input channels scaled x20): the 7 modules of
            one layer through the automatic dispatch (EC pre-kernel + 4-bit
            GEMM with the EC in its epilogue).
@@ -44,6 +47,9 @@ MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 MFMA
 LAYERS_1B = 16
 RANK = 16
 GROUP = 128
+# per decoder layer, the modules that read one hidden state (q, k, v; gate,
+# up) go out as one grouped call; o and down alone
+DEC_GROUPS = ((0, 1, 2), (3,), (4, 5), (6,))
 
 
 def algo_bytes(M, N, K, G, r, ab_int8=False):
@@ -295,6 +301,8 @@ def main():
     ap.add_argument("--no-70b", action="store_true", help="skip the 70B-layer context line")
     ap.add_argument("--no-int8", action="store_true",
                     help="skip the passes with INT8 per-channel EC factors")
+    ap.add_argument("--no-ungrouped", action="store_true",
+                    help="skip the decode pass with one call per module")
     ap.add_argument("--no-tail", action="store_true",
                     help="skip the passes with the post-EC tail on o and down")
     ap.add_argument("--model70b", action="store_true",
@@ -335,9 +343,15 @@ def main():
                 d.zeros = b.zeros.clone()
                 d.A, d.B, d.w_g = b.A.clone(), b.B.clone(), b.w_g.clone()
                 mods.append(d)
+            # q, k, v read one hidden state, gate and up another
+            for grp in DEC_GROUPS:
+                for j in grp[1:]:
+                    mods[j].x = mods[grp[0]].x
             per_copy.append(mods)
         dec_dev.append(per_copy)
-    dec_ws = max(sp.dispatch_plan(d.problem()).workspace_bytes for d in base_dev)
+    dec_ws = max([sp.dispatch_plan(d.problem()).workspace_bytes for d in base_dev] +
+                 [sp.group_workspace([base_dev[j].member(base_dev[j].problem(rank=r), with_ec=r != 0)
+                                      for j in grp]) for grp in DEC_GROUPS for r in (None, 0)])
     dec_ws_t = torch.zeros(max(dec_ws, 256), dtype=torch.uint8, device=dev)
     pre_dev = [sp.DeviceLayer(L, device=dev) for L in pre_base]
     pre_ws = max(sp.dispatch_plan(d.problem()).workspace_bytes for d in pre_dev)
@@ -352,13 +366,16 @@ def main():
     pre_flops_w4 = sum(algo_flops(L.M, L.N, L.K, 0) for L in pre_base)
     dec_plan = sp.dispatch_plan(base_dev[0].problem())
 
-    def decode_pass(c, ec=True):
-        for mods in dec_dev[c]:
-            for d in mods:
-                if ec:
-                    d.run_ec(d.problem(), dec_ws_t)
+    def decode_pass(c, ec=True, grouped=True, devs=None):
+        for mods in (dec_dev if devs is None else devs)[c]:
+            for grp in (DEC_GROUPS if grouped else [(j,) for j in range(len(mods))]):
+                if len(grp) > 1:
+                    sp.w4ec_linear_group([mods[j].member(mods[j].problem(rank=None if ec else 0),
+                                                         with_ec=ec) for j in grp], dec_ws_t)
+                elif ec:
+                    mods[grp[0]].run_ec(mods[grp[0]].problem(), dec_ws_t)
                 else:
-                    d.run_w4(d.problem(), w4_ws_t)
+                    mods[grp[0]].run_w4(mods[grp[0]].problem(), w4_ws_t)
 
     def prefill_pass(ec=True):
         for d in pre_dev:
@@ -413,6 +430,19 @@ def main():
     dec_gbs = dec_bytes / dec_s / 1e9
     pre_tfl = pre_flops / pre_s / 1e12
 
+    # the same decode pass with one call per module
+    ungrouped = None
+    if not args.no_ungrouped:
+        print("bench: decode with one call per module", file=sys.stderr, flush=True)
+        g_dec_u = [capture(lambda c=c: decode_pass(c, grouped=False)) for c in range(args.copies)]
+        run_steps(args.warmup, g_dec_u, g_pre, False)
+        evu = run_steps(args.steps, g_dec_u, g_pre, True)
+        torch.cuda.synchronize()
+        du = float(np.mean([a.elapsed_time(b) for a, b, _ in evu])) * 1e-3
+        del g_dec_u
+        ungrouped = {"ms_per_pass": round(du * 1e3, 4), "GBps": round(dec_bytes / du / 1e9, 2),
+                     "launches": LAYERS_1B * len(S.MODULES)}
+
     overhead = None
     if not args.no_overhead:
         print("bench: W4-only reference passes", file=sys.stderr, flush=True)
@@ -452,10 +482,14 @@ def main():
                       for per_copy in dec_dev]
         pre_dev_i8 = [swap(d, pre_i8[j]) for j, d in enumerate(pre_dev)]
 
+        for per_copy in dec_dev_i8:
+            for mods in per_copy:
+                for grp in DEC_GROUPS:
+                    for j in grp[1:]:
+                        mods[j].x = mods[grp[0]].x
+
         def decode_pass_i8(c):
-            for mods in dec_dev_i8[c]:
-                for d in mods:
-                    d.run_ec(d.problem(), dec_ws_t)
+            decode_pass(c, devs=dec_dev_i8)
 
         def prefill_pass_i8():
             for d in pre_dev_i8:
@@ -507,8 +541,17 @@ def main():
                     d.layer_name = S.MODULES[j]
         for j, d in enumerate(pre_dev):
             d.layer_name = S.MODULES[j]
-        g_dec_t = [capture(lambda c=c: [call(d, dec_ws_t, 1) for mods in dec_dev[c] for d in mods])
-                   for c in range(args.copies)]
+        def decode_tail(c):
+            # the grouped calls as in the decode pass, o and down with the tail
+            for mods in dec_dev[c]:
+                for grp in DEC_GROUPS:
+                    if len(grp) > 1:
+                        sp.w4ec_linear_group([mods[j].member(mods[j].problem()) for j in grp],
+                                             dec_ws_t)
+                    else:
+                        call(mods[grp[0]], dec_ws_t, 1)
+
+        g_dec_t = [capture(lambda c=c: decode_tail(c)) for c in range(args.copies)]
         g_pre_t = capture(lambda: [call(d, pre_ws_t, 4096) for d in pre_dev])
         run_steps(args.warmup, g_dec_t, g_pre_t, False)
         evt = run_steps(args.steps, g_dec_t, g_pre_t, True)
@@ -540,7 +583,7 @@ def main():
         torch.cuda.synchronize()
 
     traffic = stored_traffic()
-    n_launch_dec = LAYERS_1B * len(S.MODULES)
+    n_launch_dec = LAYERS_1B * len(DEC_GROUPS)
     result = {
         "metric": METRIC,
         "value": round(dec_gbs, 2),
@@ -563,11 +606,13 @@ def main():
             "prefill_paths": {m: sp.PATH_NAMES[sp.dispatch_plan(d.problem()).path]
                               for m, d in zip(S.MODULES, pre_dev)},
             "decode_weight_copies": args.copies,
+            "decode_launches": ("per layer: q,k,v grouped (one launch), o, gate,up grouped "
+                                "(one launch), down: %d per pass" % n_launch_dec),
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": ("k_gemv (one-kernel W4+EC decode GEMV, %s), all launches of the decode pass"
-                       % sp.PATH_NAMES[dec_plan.path]),
+            "kernel": ("k_gemv_group / k_gemv (one-kernel W4+EC decode GEMV, %s), all "
+                       "launches of the decode pass" % sp.PATH_NAMES[dec_plan.path]),
             "achieved": round(dec_bytes / n_launch_dec / (dec_s / n_launch_dec) / 1e9, 2),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
@@ -587,6 +632,7 @@ def main():
             },
         },
         "decode_ms_per_pass": round(dec_s * 1e3, 4),
+        "decode_one_call_per_module": ungrouped,
         "decode_70b_layer": ctx70,
         "model_70b": model70,
         "ec_overhead": overhead,

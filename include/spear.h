@@ -233,8 +233,8 @@ spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x
  * are independent calls. A group runs up to SPEAR_GROUP_MAX such calls as one
  * launch when all of them take the same single-launch GEMV variant: the 4-bit
  * product alone (ec NULL) or the fused local path (every member M <= 32 with
- * an elementwise gate and rank <= 16, or forced to it; same act dtype, token
- * tiles and row tiles). Otherwise the members run one after another in array
+ * an elementwise gate and rank <= 16, where the planner takes that path;
+ * same act dtype, token tiles and row tiles). Otherwise the members run one after another in array
  * order, each on its own planned path. Either way each member's Y is exactly
  * (bit for bit) what its own spear_w4ec_linear or spear_w4_linear call
  * writes. */
@@ -251,19 +251,24 @@ typedef struct {
   void* y;
 } spear_layer_call_t;
 
-/* Workspace bytes of a group: each member's plan's workspace_bytes rounded
- * up to 256, summed in array order (member i uses the slice at the sum of
- * the earlier members' sizes). Host-only. SPEAR_E_SHAPE for n outside
- * [1, SPEAR_GROUP_MAX], and every code spear_dispatch_plan returns for a
- * member. */
+/* Workspace bytes of a group. Every nonempty workspace layout starts with
+ * the same counter block (the first 128 KiB); a group's workspace is that
+ * block followed by each member's data region (its plan's bytes past the
+ * block, rounded up to 256) in array order, so it is at least every
+ * member's own size and, like a single call's, may be shared in stream order
+ * with single calls and other groups. 0 when no member needs scratch.
+ * Host-only. SPEAR_E_NULL for a NULL array, member problem or out pointer,
+ * SPEAR_E_SHAPE for n outside [1, SPEAR_GROUP_MAX], and every code
+ * spear_dispatch_plan returns for a member. */
 spear_status_t spear_group_workspace(int32_t n, const spear_layer_call_t* calls, size_t* out_bytes);
 
 /* Runs the n members (see above) on hip_stream. Validation of every member
  * (the single calls' checks) happens before any launch; in addition each
  * member's Y may not overlap any buffer of another member (SPEAR_E_ALIAS);
  * members may share X. Members with M == 0 or N == 0 are skipped. The
- * workspace follows spear_group_workspace; concurrent groups need separate
- * workspaces. */
+ * workspace (at least spear_group_workspace's bytes, zero-filled once before
+ * first use) follows the single calls' rules: calls that overlap in time
+ * need separate workspaces. */
 spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* calls, void* workspace,
                                        size_t workspace_bytes, void* hip_stream);
 

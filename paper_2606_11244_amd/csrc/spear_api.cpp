@@ -88,16 +88,33 @@ int gemv_ips(int IT, int nrg, int NW) {
   return (int)cdiv(IT, S);
 }
 
-// Row tiles per GEMV block for MT token tiles (the local EC variant keeps one
-// row tile for two token tiles: registers).
-int gemv_rt(int MT, bool local) {
-  int RT = MT <= 2 ? 2 : 1;
-  if (local && MT == 2) RT = 1;
-  if (g_ov_rt.load() > 0) RT = g_ov_rt.load();
-  return RT;
+// Row tiles per GEMV block for MT token tiles. With one token tile (decode)
+// the 4-bit product alone and the local EC variant take the fewest rows per
+// block that keep the launch within one round of co-resident blocks (256
+// blocks of 512 threads, one per CU): a decode block's time is mostly load
+// latency, so more blocks with fewer rows each finish sooner, until a second
+// round would wait for the first (measured on the 1B- and 70B-shaped
+// modules); when no choice fits one round, two row tiles. The other EC
+// variants take two row tiles, and every variant with more token tiles two
+// or one (the local variant keeps one for two token tiles: registers).
+// rt_force > 0 imposes a row-tile count (grouped calls).
+enum { kRtW4 = 0, kRtLocal = 1, kRtOther = 2 };
+constexpr int64_t kGemvRound = 256;
+int gemv_rt(int MT, int kind, int64_t N, int IT, int NW, int rt_force) {
+  if (g_ov_rt.load() > 0) return g_ov_rt.load();
+  if (rt_force > 0) return rt_force;
+  if (MT == 1 && kind != kRtOther) {
+    for (int RT = 1; RT <= 4; RT *= 2) {
+      const int nrg = (int)cdiv(N, 16 * RT);
+      const int S = (int)cdiv(IT, gemv_ips(IT, nrg, NW));
+      if ((int64_t)nrg * S <= kGemvRound) return RT;
+    }
+    return 2;
+  }
+  return MT <= 2 && !(kind == kRtLocal && MT == 2) ? 2 : 1;
 }
 
-spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
+spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int rt_force = 0) {
   spear_status_t st = validate_shape(p, with_ec);
   if (st != SPEAR_OK) return st;
   Resolved& z = *R;
@@ -123,8 +140,9 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
   bool local_ok = z.ec && z.gate != GATE_TANH && z.r <= 16 && M <= kLocalMaxM;
   if (local_ok) {
     // the block's K-slice of A and w_g is staged in LDS
-    const int MT = (int)cdiv(M, 16), RT = gemv_rt(MT, true);
+    const int MT = (int)cdiv(M, 16);
     const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load())) : 8;
+    const int RT = gemv_rt(MT, kRtLocal, N, z.IT, nw, rt_force);
     const int ips = gemv_ips(z.IT, (int)cdiv(N, 16 * RT), nw);
     const size_t abytes = (size_t)17 * (ips * kIterK + 8) * 2;
     const size_t partials = (size_t)nw * (RT + kLocalTiles) * MT * 1024;
@@ -188,7 +206,11 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R) {
     // iterations per wave so that the pipeline has something to overlap.
     z.MT = (int)cdiv(M, 16);
     z.NW = 8;
-    z.RT = gemv_rt(z.MT, local);
+    {
+      const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load())) : 8;
+      z.RT = gemv_rt(z.MT, local ? kRtLocal : !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN ? kRtW4 : kRtOther,
+                     N, z.IT, nw, rt_force);
+    }
     if (!gemv_shape_supported(z.MT, z.RT)) return SPEAR_E_UNSUPPORTED;
     // the EC variants add the EC wave to the workgroup
     const int epi = !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN ? EPI_NONE
@@ -728,19 +750,30 @@ int group_epi(const Resolved& z, const spear_ec_t* ec) {
   return -1;
 }
 
+// Group workspace: the one counter block of every workspace, then each
+// member's data region (its plan's bytes past the counter block) in array
+// order. A member run on its own takes the workspace as it is (its data
+// regions start past the counter block); in the one-launch case member i's
+// data start after the earlier members' and its split-K counters follow
+// theirs in the counter block. Either way the counter block stays the first
+// kCounterBytes, so the workspace may be shared with single calls.
 spear_status_t group_resolve(int32_t n, const spear_layer_call_t* calls, Resolved* z,
-                             size_t* off, size_t* total) {
-  if (!calls || (n > 0 && !total)) return SPEAR_E_NULL;
+                             size_t* data_off, size_t* total) {
+  if (!calls || !total) return SPEAR_E_NULL;
   if (n < 1 || n > SPEAR_GROUP_MAX) return SPEAR_E_SHAPE;
   size_t sum = 0;
+  bool any = false;
   for (int i = 0; i < n; ++i) {
     if (!calls[i].prob) return SPEAR_E_NULL;
     const spear_status_t st = resolve(calls[i].prob, calls[i].ec != nullptr, &z[i]);
     if (st != SPEAR_OK) return st;
-    off[i] = sum;
-    sum += round256(z[i].plan.workspace_bytes);
+    const size_t b = z[i].plan.workspace_bytes;
+    if (b > 0 && b < kCounterBytes) return SPEAR_E_SHAPE;  // every layout starts with the counters
+    any = any || b > 0;
+    data_off[i] = sum;
+    sum += round256(b > 0 ? b - kCounterBytes : 0);
   }
-  *total = sum;
+  *total = any ? kCounterBytes + sum : 0;
   return SPEAR_OK;
 }
 
@@ -816,7 +849,6 @@ spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x
 }
 
 spear_status_t spear_group_workspace(int32_t n, const spear_layer_call_t* calls, size_t* out_bytes) {
-  if (!out_bytes) return SPEAR_E_NULL;
   Resolved z[SPEAR_GROUP_MAX];
   size_t off[SPEAR_GROUP_MAX];
   return group_resolve(n, calls, z, off, out_bytes);
@@ -847,26 +879,55 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
   }
   hipStream_t s = (hipStream_t)hip_stream;
   // one launch when every member runs the same single-launch GEMV variant
+  // and their split-K counters fit the counter block together
   int epi = group_epi(z[0], calls[0].ec);
   bool one = n > 1 && epi >= 0;
-  for (int i = 1; i < n && one; ++i)
+  int ctrs = 0;
+  for (int i = 0; i < n && one; ++i) {
     one = group_epi(z[i], calls[i].ec) == epi && z[i].dt == z[0].dt && z[i].MT == z[0].MT &&
           z[i].RT == z[0].RT && z[i].NW == z[0].NW;
-  if (!one) {
+    if (z[i].S > 1) ctrs += z[i].nrg;
+  }
+  if (!one || ctrs > kMaxRowCounters) {
     for (int i = 0; i < n; ++i) {
       const spear_layer_call_t& c = calls[i];
       if (c.prob->M == 0 || c.prob->N == 0) continue;
-      st = run_layer(c.prob, z[i], c.x, c.w, c.ec, c.y, nullptr, ws ? ws + off[i] : nullptr, s);
+      st = run_layer(c.prob, z[i], c.x, c.w, c.ec, c.y, nullptr, ws, s);
       if (st != SPEAR_OK) return st;
     }
     return SPEAR_OK;
+  }
+  // local EC members whose blocks exceed one round together take four row
+  // tiles each when that changes nothing but the row tiling (same K-slices,
+  // iterations per wave and waves, so the same sums in the same order): the
+  // staged A limits the local variant to one block per CU
+  if ((epi == EPI_LOCAL || epi == EPI_LOCAL_I8) && z[0].MT == 1) {
+    int64_t blocks = 0;
+    for (int i = 0; i < n; ++i) blocks += (int64_t)z[i].nrg * z[i].S;
+    if (blocks > kGemvRound) {
+      Resolved zz[SPEAR_GROUP_MAX];
+      bool same = true;
+      int64_t blocks4 = 0;
+      for (int i = 0; i < n && same; ++i) {
+        same = resolve(calls[i].prob, true, &zz[i], 4) == SPEAR_OK &&
+               group_epi(zz[i], calls[i].ec) == epi && zz[i].RT == 4 && zz[i].S == z[i].S &&
+               zz[i].ips == z[i].ips && zz[i].iw == z[i].iw && zz[i].NW == z[i].NW &&
+               zz[i].plan.workspace_bytes <= z[i].plan.workspace_bytes;
+        blocks4 += (int64_t)zz[i].nrg * zz[i].S;
+      }
+      if (same && blocks4 < blocks)
+        for (int i = 0; i < n; ++i) z[i] = zz[i];
+    }
   }
   GemvGroup g;
   std::memset(&g, 0, sizeof(g));
   g.n = n;
   size_t lds = 0;
+  int ctr = 0;
   for (int i = 0; i < n; ++i) {
     const spear_layer_call_t& c = calls[i];
+    // member i's data regions (offsets past the counter block) land in its
+    // own slice; its row counters are placed explicitly
     char* wsi = ws ? ws + off[i] : nullptr;
     const bool live = c.prob->M > 0 && c.prob->N > 0;
     g.start[i + 1] = g.start[i] + (live ? z[i].nrg * z[i].S : 0);
@@ -879,6 +940,10 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
     if (z[i].ec) {
       q.ec = make_ec(c.prob, z[i], c.x, c.ec, wsi);
       if (z[i].S > 1) q.eupart = (float*)(wsi + z[i].off_eupart);
+    }
+    if (z[i].S > 1) {
+      q.rb_ctr = (uint32_t*)(ws + kCtrRows) + ctr;
+      ctr += z[i].nrg;
     }
     lds = std::max(lds, z[i].lds_gemv);
   }

@@ -1245,12 +1245,25 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* sm
     uint32_t sv[4], zv[4];
     u32x4 s8;
     u32x2 z8;
+    // EPI_LOCAL: the first round of A and w_g goes out with the first round
+    // of x, scales and zero points, so that the staging costs one round trip
+    u32x4 a0[4], a1[4], gv0;
     x_issue(tid, c4);
     if (sz8) sz8_issue(tid, s8, z8);
     else sz_issue(tid, sv, zv);
+    if constexpr (kLoc) {
+      a_issue(tid, a0);
+      a_issue(tid + step, a1);
+      gv0 = bld128(rgw, tid < acpr ? ((uint32_t)it_blk * kIterK + 8 * tid) * 2 : kOOB);
+    }
     x_store(tid, c4);
     if (sz8) sz8_store(tid, s8, z8);
     else sz_store(tid, sv, zv);
+    if constexpr (kLoc) {
+      a_store(tid, a0);
+      a_store(tid + step, a1);
+      if (tid < acpr) *(u32x4*)(als + 16 * astride + 8 * tid) = gv0;
+    }
     for (int base = tid + step; base < nch; base += step) {
       x_issue(base, c4);
       x_store(base, c4);
@@ -1267,15 +1280,15 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* sm
       }
     }
     if constexpr (kLoc) {
-      // A: two rounds of four chunks per thread in flight; w_g: one chunk
-      for (int base = tid; base < 16 * acpr; base += 2 * step) {
-        u32x4 a0[4], a1[4];
+      // the rest of A: two rounds of four chunks per thread in flight; of
+      // w_g: one chunk
+      for (int base = tid + 2 * step; base < 16 * acpr; base += 2 * step) {
         a_issue(base, a0);
         a_issue(base + step, a1);
         a_store(base, a0);
         a_store(base + step, a1);
       }
-      for (int kc = tid; kc < acpr; kc += blockDim.x) {
+      for (int kc = tid + (int)blockDim.x; kc < acpr; kc += blockDim.x) {
         const u32x4 gv = bld128(rgw, ((uint32_t)it_blk * kIterK + 8 * kc) * 2);
         *(u32x4*)(als + 16 * astride + 8 * kc) = gv;
       }
@@ -1403,6 +1416,11 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* sm
   // EPI_LOCAL: this block's [A; w_g] x (its K-slice), u [token][R1p] in LDS
   float* u_loc = (float*)(smem + a.lds_e);
   const int R1 = a.ec.R1, R1p = a.ec.R1p;
+  // Without split-K the sums are complete here: each thread that owns u_j of
+  // a token also sums that token's gate logit and writes v_j directly
+  // (EPI_LOCAL, below), saving a pass and a barrier.
+  float* v_loc = u_loc + 16 * MT * R1p;
+  const bool v_direct = a.S == 1;
   if constexpr (kLoc) {
     // tile 0: column j < r is u_j; tile 1: column 0 is the gate logit w_g x
     for (int e = tid; e < 256 * kLocalTiles * MT; e += blockDim.x) {
@@ -1410,13 +1428,25 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* sm
       const int t = tm / MT, mt = tm - t * MT;
       const int tok = 16 * mt + 4 * (ln >> 4) + i, c = ln & 15;
       const int j = t == 0 ? (c < r ? c : -1) : (c == 0 && R1 > r ? r : -1);
-      if (j < 0) continue;
+      if (j < 0 || (v_direct && t != 0)) continue;
       float v = 0.f;
       for (int w = 0; w < NW; ++w) v += ered[(((w * kLocalTiles + t) * MT + mt) * 64 + ln) * 4 + i];
       if constexpr (kI8) {
         if (t == 0) v *= sa_c;  // c == (lane / 4) % 16 here
       }
-      u_loc[tok * R1p + j] = v;
+      if (v_direct) {
+        float g = 1.f;
+        if (a.ec.gate == GATE_SIGMOID) {
+          float zl = 0.f;  // the logit: tile 1, column 0, same token
+          for (int w = 0; w < NW; ++w)
+            zl += ered[(((w * kLocalTiles + 1) * MT + mt) * 64 + (ln & 48)) * 4 + i];
+          const float z = zl + a.ec.b_g;
+          g = z >= 0.f ? 1.f / (1.f + __expf(-z)) : __expf(z) / (1.f + __expf(z));
+        }
+        v_loc[tok * r + j] = a.ec.alpha * g * v;
+      } else {
+        u_loc[tok * R1p + j] = v;
+      }
     }
   }
   float* yacc = (float*)(smem + a.lds_y);
@@ -1479,8 +1509,7 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* sm
 
   // EPI_LOCAL: v = alpha g(x) (.) A x for every token (g the sigmoid of the
   // gate row's sum plus b_g, or one), then y += v B^T in fp32 below
-  float* v_loc = u_loc + 16 * MT * R1p;
-  if constexpr (kLoc) {
+  if (kLoc && !v_direct) {
     for (int idx = tid; idx < M * r; idx += blockDim.x) {
       const int m = idx / r, j = idx - m * r;
       float g = 1.f;

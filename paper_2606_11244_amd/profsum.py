@@ -23,13 +23,16 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CALIB_BYTES = 1 << 30  # the calibration kernel reads and writes 1 GiB
 
-DECODE_KERNEL = "k_gemv<0, 1, 2, 3>"   # fp16, one token tile, two row tiles, local-EC epilogue
-PREFILL_KERNEL = "k_gemm<0, 1, 4>"     # fp16, EC epilogue, 256-token tiles
+# fp16, one token tile, any row tiles, local-EC epilogue: every launch of the
+# decode pass (grouped and single calls)
+DECODE_KERNEL = r"k_gemv(_group)?<0, 1, \d, 3>"
+PREFILL_KERNEL = r"k_gemm<0, 1, 4>"     # fp16, EC epilogue, 256-token tiles
 
 
 def kernel_source_hash() -> str:
@@ -87,18 +90,19 @@ def main(argv):
         """Mean HBM bytes per launch (reads and writes, calibrated) of a kernel."""
         tot, n = 0.0, 0
         for (nm, g), vals in fetch.items():
-            if kernel in nm:
+            if re.search(kernel, nm):
                 tot += sum(vals) * 1024 * k_f
                 n += len(vals)
         for (nm, g), vals in write.items():
-            if kernel in nm:
+            if re.search(kernel, nm):
                 tot += sum(vals) * 1024 * k_w
         return tot / n if n else None
 
     lines = [f"# rocprofv3 summary: {name}", "",
              "Workload: bench.py (Llama-3.2-1B-shaped W4+EC layers, fp16, group 128, rank 16, "
-             "sigmoid-linear gate): decode M=1 over 16 layers x 7 modules, prefill M=4096 "
-             "over 7 modules, W4-only reference passes; synthetic data.", "",
+             "sigmoid-linear gate): decode M=1 over 16 layers x 7 modules (q,k,v and gate,up "
+             "as grouped calls), prefill M=4096 over 7 modules, W4-only reference passes; "
+             "synthetic data.", "",
              "Commands (from the repository root, with TMPDIR=/tmp):", "",
              f"    {tcmd}", f"    {fcmd}", f"    {wcmd}", "",
              f"Kernel sources hash: {kernel_source_hash()}", "",

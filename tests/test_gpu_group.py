@@ -172,3 +172,45 @@ def test_graph_replay(M):
         torch.cuda.synchronize()
         for j, d in enumerate(dls):
             assert torch.equal(got[j].view(torch.int16), d.y.view(torch.int16)), (i, j)
+
+
+def test_workspace_shared_with_single_calls():
+    """One workspace serves groups and single calls in stream order: groups
+    whose members run one after another on the producer/consumer path (rank
+    32, beyond the local variant), groups of split-K members in one launch,
+    and single calls of both kinds, interleaved over three rounds; every
+    output equals the one its call writes with a fresh workspace."""
+    from paper_2606_11244_amd import spear as sp
+
+    def dev(L):
+        return sp.DeviceLayer(L)
+
+    wide = [dev(S.make_layer(M=1, N=8192, K=2048, group_size=128, rank=32, seed=40 + i))
+            for i in range(2)]
+    deep = [dev(S.config_layer(1, "down", 1, seed=42 + i)) for i in range(2)]
+    single = [dev(S.config_layer(1, "down", 1, seed=44)),
+              dev(S.make_layer(M=1, N=2048, K=2048, group_size=128, rank=32, seed=45))]
+    paths = {n: sp.PATH_NAMES[sp.dispatch_plan(d.problem()).path]
+             for n, d in (("wide", wide[0]), ("deep", deep[0]), ("s0", single[0]),
+                          ("s1", single[1]))}
+    assert paths["wide"] == "fused_gemv" and paths["deep"] == "fused_local", paths
+    ref = []
+    for d in wide + deep + single:
+        d.run_ec(d.problem(), sp.allocate_workspace(d.problem()))
+        torch.cuda.synchronize()
+        ref.append(d.y.clone())
+    gw = [[d.member(d.problem()) for d in grp] for grp in (wide, deep)]
+    need = max([sp.group_workspace(m) for m in gw] +
+               [sp.dispatch_plan(d.problem()).workspace_bytes for d in single])
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for rnd in range(3):
+        for d in wide + deep + single:
+            d.y.zero_()
+        log(f"shared workspace round {rnd} paths={paths}")
+        sp.w4ec_linear_group(gw[0], ws)
+        single[0].run_ec(single[0].problem(), ws)
+        sp.w4ec_linear_group(gw[1], ws)
+        single[1].run_ec(single[1].problem(), ws)
+        torch.cuda.synchronize()
+        for k, d in enumerate(wide + deep + single):
+            assert torch.equal(d.y.view(torch.int16), ref[k].view(torch.int16)), (rnd, k)

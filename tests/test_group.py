@@ -47,18 +47,30 @@ def _qkv(M=1):
             sp.problem(M, 512, 2048, 128, sp.F16, 16)]
 
 
-def test_workspace_is_members_rounded_and_summed():
+COUNTER_BLOCK = 131072  # the counter block at the start of every workspace
+
+
+def _want(sizes):
+    if not any(sizes):
+        return 0
+    return COUNTER_BLOCK + sum(-(-max(0, b - COUNTER_BLOCK) // 256) * 256 for b in sizes)
+
+
+def test_workspace_is_counter_block_plus_member_data():
     for probs in (_qkv(1), _qkv(16), [sp.problem(1, 2048, 8192, 128, sp.F16, 16)] * 2,
                   [sp.problem(512, 2048, 2048, 128, sp.F16, 16), sp.problem(1, 512, 2048)]):
         st, got = _ws(probs)
         assert st == 0
-        want = sum(-(-sp.dispatch_plan(p, True).workspace_bytes // 256) * 256 for p in probs)
-        assert got == want
+        sizes = [sp.dispatch_plan(p, True).workspace_bytes for p in probs]
+        assert all(b == 0 or b >= COUNTER_BLOCK for b in sizes)
+        assert got == _want(sizes)
+        # large enough for any member run on its own at the same base
+        assert got >= max(sizes)
     # without an EC each member sizes its 4-bit plan
     probs = _qkv(1)
     st, got = _ws(probs, with_ec=False)
     assert st == 0
-    assert got == sum(-(-sp.dispatch_plan(p, False).workspace_bytes // 256) * 256 for p in probs)
+    assert got == _want([sp.dispatch_plan(p, False).workspace_bytes for p in probs])
 
 
 def test_group_size_and_nulls():
