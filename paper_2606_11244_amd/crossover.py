@@ -12,6 +12,12 @@ Usage (on a GPU):
   python -m paper_2606_11244_amd.crossover --out profiles/dispatch_crossover.md
   python -m paper_2606_11244_amd.crossover --lut profiles/latency_lut_llama1b.json
 
+With --rows it measures the decode kernels of the 1B-shaped modules at each
+row-tile count (1, 2, 4 sixteen-row tiles per block, forced with
+spear_set_gemv_shape, and the planner's own choice), single calls and the
+grouped q,k,v and gate,up calls, and writes a markdown table:
+  python -m paper_2606_11244_amd.crossover --rows profiles/decode_row_tiles.md
+
 With --lut it instead measures, for each module of the Llama-3.2-1B-shaped
 configuration, the 4-bit-only call and the W4+EC call on the path AUTO picks
 over a grid of token counts: the latency tables l_W4(M), l_EC(M) of the
@@ -45,6 +51,7 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default="profiles/dispatch_crossover.md")
     ap.add_argument("--lut", default=None, help="write latency tables (JSON) instead")
+    ap.add_argument("--rows", default=None, help="write the decode row-tile table instead")
     ap.add_argument("--reps", type=int, default=10)
     args = ap.parse_args(argv)
 
@@ -88,6 +95,10 @@ def main(argv=None):
                                             base.zeros.clone())
             devs.append(d)
         return devs
+
+    if args.rows:
+        rows_table(args, sp, S, torch, timed)
+        return
 
     if args.lut:
         # one table per module shape of the 1B configuration: prefill shapes
@@ -201,6 +212,71 @@ def main(argv=None):
     with open(args.out, "w") as f:
         f.write("\n".join(lines))
     print(f"wrote {args.out}", file=sys.stderr)
+
+
+def rows_table(args, sp, S, torch, timed, copies=24):
+    """Decode (M = 1, 16) time per call at each row-tile count."""
+    def cp(b):
+        out = []
+        for _ in range(copies):
+            d = sp.DeviceLayer.__new__(sp.DeviceLayer)
+            d.__dict__.update(b.__dict__)
+            d.qweight, d.scales, d.zeros = b.qweight.clone(), b.scales.clone(), b.zeros.clone()
+            d.A, d.B = b.A.clone(), b.B.clone()
+            out.append(d)
+        return out
+
+    ws = torch.zeros(1 << 24, dtype=torch.uint8, device="cuda")
+    names = ["q", "k", "o", "gate", "down", "q,k,v", "gate,up"]
+    lines = ["# Decode row tiles: time per call by rows per block", "",
+             "Command (from the repository root): `python -m paper_2606_11244_amd.crossover "
+             f"--rows {args.rows}`", "",
+             "Llama-3.2-1B-shaped modules (group 128, rank 16, sigmoid-linear gate, fp16; "
+             "synthetic, seed 0), microseconds per call, graph-replayed over "
+             f"{copies} weight copies; `EC / 4-bit only`. Row tiles forced with "
+             "spear_set_gemv_shape; `planner` = the automatic choice. `-` = the local EC "
+             "variant does not take that shape (the planner would pick another path). "
+             "Grouped columns: one spear_w4ec_linear_group call (q,k,v share x; gate,up "
+             "share x).", ""]
+    for M in (1, 16):
+        mods = {m: cp(sp.DeviceLayer(S.config_layer(1, m, M, seed=0)))
+                for m in ("q", "k", "v", "o", "gate", "up", "down")}
+        for c in range(copies):
+            mods["k"][c].x = mods["v"][c].x = mods["q"][c].x
+            mods["up"][c].x = mods["gate"][c].x
+        lines += [f"## M = {M}", "", "| row tiles | " + " | ".join(names) + " |",
+                  "|---" * (len(names) + 1) + "|"]
+        for rt in (1, 2, 4, 0):
+            sp.set_gemv_shape(rt, 0, 0)
+            cells = []
+            for nm in names:
+                grp = nm.split(",")
+                if any(sp.dispatch_plan(mods[m][0].problem()).path != sp.PATH_FUSED_LOCAL
+                       for m in grp):
+                    cells.append("-")
+                    continue
+                if len(grp) == 1:
+                    m = grp[0]
+                    te = timed(lambda c, m=m: mods[m][c].run_ec(mods[m][c].problem(), ws),
+                               copies, args.reps)
+                    t4 = timed(lambda c, m=m: mods[m][c].run_w4(mods[m][c].problem(rank=0), ws),
+                               copies, args.reps)
+                else:
+                    te = timed(lambda c, g=grp: sp.w4ec_linear_group(
+                        [mods[m][c].member(mods[m][c].problem()) for m in g], ws), copies, args.reps)
+                    t4 = timed(lambda c, g=grp: sp.w4ec_linear_group(
+                        [mods[m][c].member(mods[m][c].problem(rank=0), with_ec=False) for m in g],
+                        ws), copies, args.reps)
+                cells.append(f"{te:.2f} / {t4:.2f}")
+            sp.set_gemv_shape(0, 0, 0)
+            lines.append(f"| {rt if rt else 'planner'} | " + " | ".join(cells) + " |")
+            print(lines[-1], flush=True)
+        lines.append("")
+        del mods
+        torch.cuda.empty_cache()
+    with open(args.rows, "w") as f:
+        f.write("\n".join(lines))
+    print(f"wrote {args.rows}", file=sys.stderr)
 
 
 if __name__ == "__main__":
