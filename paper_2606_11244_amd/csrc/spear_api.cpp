@@ -164,7 +164,16 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   const bool few_tiles = cdiv(M, kGemmTM) * cdiv(N, kGemmTN) <= 256;
   // the 256-token GEMM tile applies (see the tile choice below): the
   // semi-fused pair on it beats the fully fused GEMM on 128-token tiles
-  const bool big_tiles = cdiv(M, 256) * cdiv(N, kGemmTN) * std::max<int64_t>(1, K / 4096) >= 256;
+  // (counting each 4096 of K beyond the first as another round of tiles):
+  // when those tiles fill the 256 CUs, or, up to 512 tokens on layers of at
+  // least 32M weights, when a quarter of them do and the halved weight
+  // traffic pays for the emptier grid (70B q: 57 us against 70 us on
+  // 128-token tiles at 256 tokens; 8B down: 58 against 71). Never at 128
+  // tokens or fewer, where the 256-token tile only adds empty rows (70B gate
+  // at 64 tokens: 107 us on 128-token tiles, 168 us on 256).
+  const int64_t t256 = cdiv(M, 256) * cdiv(N, kGemmTN) * std::max<int64_t>(1, K / 4096);
+  const bool big_tiles =
+      M > 128 && (t256 >= 256 || (M <= 512 && N * K >= ((int64_t)1 << 25) && t256 >= 64));
   if (path == SPEAR_PATH_AUTO || !z.ec)
     path = M > kAutoGemvMaxM ? (mfma_ok && few_tiles && !big_tiles ? SPEAR_PATH_FUSED_MFMA
                                                                    : SPEAR_PATH_UNFUSED_2K)
