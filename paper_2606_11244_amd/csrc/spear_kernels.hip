@@ -993,7 +993,7 @@ __device__ void ec_wave(const GemvParams& a, uint32_t gen, char* smem, int n0, b
 // others' EC waves wait for what they publish.
 // ---------------------------------------------------------------------------
 template <int DT, int MT, int RT, int EPI>
-__device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* smem) {
+__device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t gen, char* smem) {
   __shared__ int s_flag;
   constexpr bool kEC = EPI == EPI_READY || EPI == EPI_FUSED;  // with an EC wave
   constexpr bool kLoc = EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8;
@@ -1003,16 +1003,6 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* sm
   const int NW = (blockDim.x >> 6) - (kEC ? 1 : 0);           // GEMV waves
   const bool gw = wave < NW;
   const int lr = lane & 15, lg = lane >> 4;
-  uint32_t gen = 0;
-  if constexpr (EPI == EPI_FUSED) {
-    gen = (uint32_t)(__hip_atomic_load(gen_counter(a, bid), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> 32);
-    if (bid < a.n_prod) {
-      ec_producer<DT, 1>(a.ec, bid, gen, smem);
-      fused_exit(a);
-      return;
-    }
-    bid -= a.n_prod;
-  }
   constexpr int RB = 16 * RT;
   const int M = a.M, N = a.N, K = a.K, G = a.G;
   const int IT = K / kIterK;
@@ -1577,7 +1567,19 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, char* sm
 template <int DT, int MT, int RT, int EPI>
 __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  gemv_body<DT, MT, RT, EPI>(a, blockIdx.x, smem);
+  int bid = blockIdx.x;
+  uint32_t gen = 0;
+  if constexpr (EPI == EPI_FUSED) {
+    // the first n_prod workgroups are the EC producers
+    gen = (uint32_t)(__hip_atomic_load(gen_counter(a, bid), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> 32);
+    if (bid < a.n_prod) {
+      ec_producer<DT, 1>(a.ec, bid, gen, smem);
+      fused_exit(a);
+      return;
+    }
+    bid -= a.n_prod;
+  }
+  gemv_body<DT, MT, RT, EPI>(a, bid, gen, smem);
 }
 
 // Several independent layer calls of one GEMV variant in one launch: member i
@@ -1594,7 +1596,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv_group(GemvGroup g) {
 #pragma unroll
   for (int j = 1; j < kGroupMax; ++j)
     if (j < g.n && b >= g.start[j]) i = j;
-  gemv_body<DT, MT, RT, EPI>(g.p[i], b - g.start[i], smem);
+  gemv_body<DT, MT, RT, EPI>(g.p[i], b - g.start[i], 0u, smem);
 }
 
 // ---------------------------------------------------------------------------
