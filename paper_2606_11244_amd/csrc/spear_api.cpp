@@ -78,11 +78,18 @@ spear_status_t validate_shape(const spear_problem_t* p, bool with_ec) {
   return SPEAR_OK;
 }
 
-// Split-K of the decode GEMV: K-slices are added until about 4096 waves
-// cover the 256 CUs, keeping at least two iterations per wave so that the
-// pipeline has something to overlap. Returns the slice length in iterations.
-int gemv_ips(int IT, int nrg, int NW) {
-  int S = (int)std::lround(4096.0 / ((double)nrg * NW));
+// Split-K of the decode GEMV: K-slices are added until about `waves` waves
+// (4096: 16 per CU) cover the 256 CUs, keeping at least two iterations per
+// wave so that the pipeline has something to overlap, and with cap_iw > 0 at
+// most cap_iw iterations per wave. Returns the slice length in iterations.
+// At a single token the 4-bit product alone and the producer-fused EC
+// variant aim at 2048 waves: on the 70B-shaped 8192-row modules a second
+// K-slice only adds the slices' reduction (4-bit q: 11.4 us unsplit against
+// 15.1 us in two slices; fused q, rank 64: 18.3 against 23.9). At 16 tokens
+// the 1B down module is faster split in four, so the rule stays at one token.
+int gemv_ips(int IT, int nrg, int NW, int waves = 4096, int cap_iw = 0) {
+  int S = (int)std::lround((double)waves / ((double)nrg * NW));
+  if (cap_iw > 0) S = std::max(S, (int)cdiv(IT, NW * cap_iw));
   S = std::max(1, std::min(S, std::max(1, IT / (2 * NW))));
   if (g_ov_s.load() > 0) S = std::min((int)g_ov_s.load(), IT);
   return (int)cdiv(IT, S);
@@ -94,19 +101,30 @@ int gemv_ips(int IT, int nrg, int NW) {
 // blocks of 512 threads, one per CU): a decode block's time is mostly load
 // latency, so more blocks with fewer rows each finish sooner, until a second
 // round would wait for the first (measured on the 1B- and 70B-shaped
-// modules); when no choice fits one round, two row tiles. The other EC
-// variants take two row tiles, and every variant with more token tiles two
-// or one (the local variant keeps one for two token tiles: registers).
-// rt_force > 0 imposes a row-tile count (grouped calls).
-enum { kRtW4 = 0, kRtLocal = 1, kRtOther = 2 };
+// modules); when no choice fits one round, two row tiles. The producer-fused
+// EC variant at a single token (kRtFused1) takes one row tile on layers of
+// 4096 rows or more when that fits one round, else two, with at most 16
+// iterations per wave (measured, rank 32 and 64: 8B q 11.6 us against 13.3,
+// 8B down 18.6 against 24.0; the 1024-row k modules are faster on two row
+// tiles, the 28672-deep 70B down split in two). The other EC variants take
+// two row tiles, and every variant with more token tiles two or one (the
+// local variant keeps one for two token tiles: registers). rt_force > 0
+// imposes a row-tile count (grouped calls).
+enum { kRtW4 = 0, kRtLocal = 1, kRtOther = 2, kRtFused1 = 3 };
 constexpr int64_t kGemvRound = 256;
-int gemv_rt(int MT, int kind, int64_t N, int IT, int NW, int rt_force) {
+constexpr int kFusedCapIw = 16;
+int gemv_rt(int MT, int kind, int64_t N, int IT, int NW, int rt_force, int waves) {
   if (g_ov_rt.load() > 0) return g_ov_rt.load();
   if (rt_force > 0) return rt_force;
+  if (MT == 1 && kind == kRtFused1) {
+    const int nrg = (int)cdiv(N, 16);
+    const int S = (int)cdiv(IT, gemv_ips(IT, nrg, NW, waves, kFusedCapIw));
+    return N >= 4096 && (int64_t)nrg * S <= kGemvRound ? 1 : 2;
+  }
   if (MT == 1 && kind != kRtOther) {
     for (int RT = 1; RT <= 4; RT *= 2) {
       const int nrg = (int)cdiv(N, 16 * RT);
-      const int S = (int)cdiv(IT, gemv_ips(IT, nrg, NW));
+      const int S = (int)cdiv(IT, gemv_ips(IT, nrg, NW, waves));
       if ((int64_t)nrg * S <= kGemvRound) return RT;
     }
     return 2;
@@ -142,7 +160,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     // the block's K-slice of A and w_g is staged in LDS
     const int MT = (int)cdiv(M, 16);
     const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load())) : 8;
-    const int RT = gemv_rt(MT, kRtLocal, N, z.IT, nw, rt_force);
+    const int RT = gemv_rt(MT, kRtLocal, N, z.IT, nw, rt_force, 4096);
     const int ips = gemv_ips(z.IT, (int)cdiv(N, 16 * RT), nw);
     const size_t abytes = (size_t)17 * (ips * kIterK + 8) * 2;
     const size_t partials = (size_t)nw * (RT + kLocalTiles) * MT * 1024;
@@ -215,10 +233,17 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     // iterations per wave so that the pipeline has something to overlap.
     z.MT = (int)cdiv(M, 16);
     z.NW = 8;
+    const bool fused1 = fused && M == 1;
+    const int rt_kind = local                                           ? kRtLocal
+                        : !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN ? kRtW4
+                        : fused1                                    ? kRtFused1
+                                                                    : kRtOther;
+    const int waves = (rt_kind == kRtW4 && M == 1) || fused1 ? 2048 : 4096;
     {
-      const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load())) : 8;
-      z.RT = gemv_rt(z.MT, local ? kRtLocal : !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN ? kRtW4 : kRtOther,
-                     N, z.IT, nw, rt_force);
+      // the fused variant's GEMV waves: one wave of the block is the EC wave
+      const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load()))
+                                        : fused1 ? kGemvMaxThreads / 64 - 1 : 8;
+      z.RT = gemv_rt(z.MT, rt_kind, N, z.IT, nw, rt_force, waves);
     }
     if (!gemv_shape_supported(z.MT, z.RT)) return SPEAR_E_UNSUPPORTED;
     // the EC variants add the EC wave to the workgroup
@@ -230,7 +255,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     z.NW = std::min(z.NW, max_nw);
     if (g_ov_nw.load() > 0) z.NW = std::max(1, std::min(max_nw, (int)g_ov_nw.load()));
     z.nrg = (int)cdiv(N, 16 * z.RT);
-    z.ips = gemv_ips(z.IT, z.nrg, z.NW);
+    z.ips = gemv_ips(z.IT, z.nrg, z.NW, waves, fused1 ? kFusedCapIw : 0);
     z.S = (int)cdiv(z.IT, z.ips);
     z.iw = (int)cdiv(z.ips, z.NW);
     z.plan.split_k = z.S;
