@@ -192,10 +192,17 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   const int64_t t256 = cdiv(M, 256) * cdiv(N, kGemmTN) * std::max<int64_t>(1, K / 4096);
   const bool big_tiles =
       M > 128 && (t256 >= 256 || (M <= 512 && N * K >= ((int64_t)1 << 25) && t256 >= 64));
+  // decode beyond the local variant: the producer-fused GEMV, except a
+  // single token on very deep layers, where its producers' share of K
+  // outlasts the separate projection kernel (70B down, K = 28672, rank 64:
+  // 40.2 us on the two-kernel path against 47.9 us fused; at 16 tokens, and
+  // at K = 14336, the fused GEMV is faster)
+  const bool deep1 = M == 1 && K >= 16384;
   if (path == SPEAR_PATH_AUTO || !z.ec)
     path = M > kAutoGemvMaxM ? (mfma_ok && few_tiles && !big_tiles ? SPEAR_PATH_FUSED_MFMA
                                                                    : SPEAR_PATH_UNFUSED_2K)
            : local_ok        ? SPEAR_PATH_FUSED_LOCAL
+           : deep1           ? SPEAR_PATH_UNFUSED_2K
                              : SPEAR_PATH_FUSED_GEMV;
   if (!with_ec) {
     // the 4-bit product alone: the GEMV up to kAutoGemvMaxM tokens, the
