@@ -196,8 +196,12 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   // single token on very deep layers, where its producers' share of K
   // outlasts the separate projection kernel (70B down, K = 28672, rank 64:
   // 40.2 us on the two-kernel path against 47.9 us fused; at 16 tokens, and
-  // at K = 14336, the fused GEMV is faster)
-  const bool deep1 = M == 1 && K >= 16384;
+  // at K = 14336, the fused GEMV is faster).
+  // Between 2 and 32 tokens on shallow layers (K <= 4096) the two-kernel
+  // path wins too: the fused GEMV's EC wave waits for producers whose work
+  // grows with the tokens (1B gate at 32 tokens: 21.3 us against 28.3 us;
+  // 8B q at 8 tokens: 17.7 against 20.9; deeper layers keep the fused GEMV).
+  const bool deep1 = (M == 1 && K >= 16384) || (M > 1 && K <= 4096);
   if (path == SPEAR_PATH_AUTO || !z.ec)
     path = M > kAutoGemvMaxM ? (mfma_ok && few_tiles && !big_tiles ? SPEAR_PATH_FUSED_MFMA
                                                                    : SPEAR_PATH_UNFUSED_2K)

@@ -76,10 +76,19 @@ def test_plan_phase_aware_dispatch():
         # rank 16 + the gate row fit two 16-row tiles: the local fused variant
         p = _plan(M=M)
         assert p.path == sp.PATH_FUSED_LOCAL and p.num_launches == 1, M
+        # beyond the local variant: the producer-fused GEMV for one token, the
+        # two-kernel path for more on shallow layers (K <= 4096), the fused
+        # GEMV again on deeper ones, and the two-kernel path for one token
+        # on very deep layers (K >= 16384)
+        want = sp.PATH_FUSED_GEMV if M == 1 else sp.PATH_UNFUSED_2K
         p = _plan(M=M, rank=32)
-        assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
+        assert p.path == want and p.num_launches == (1 if M == 1 else 2), M
         p = _plan(M=M, gate_kind=sp.GATE_TANH_MLP)
+        assert p.path == want, M
+        p = _plan(M=M, rank=32, K=8192)
         assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
+        p = _plan(M=M, rank=64, N=8192, K=28672)
+        assert p.path == (sp.PATH_UNFUSED_2K if M == 1 else sp.PATH_FUSED_GEMV), M
     # above 32 tokens the GEMM kernels: the fully fused one where it applies,
     # the two-kernel path on the GEMM otherwise
     for M in (33, 64):
