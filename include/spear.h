@@ -228,16 +228,19 @@ spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x
 
 /* ---- Grouped calls ---------------------------------------------------------
  * At decode a layer call is a few microseconds of latency around a few MB of
- * weights (section 4.2: kernel launches dominate at small M), and the modules
- * of a transformer block that read the same hidden state (q, k, v; gate, up)
- * are independent calls. A group runs up to SPEAR_GROUP_MAX such calls as one
- * launch when all of them take the same single-launch GEMV variant: the 4-bit
- * product alone (ec NULL) or the fused local path (every member M <= 32 with
- * an elementwise gate and rank <= 16, where the planner takes that path;
- * same act dtype, token tiles and row tiles). Otherwise the members run one after another in array
- * order, each on its own planned path. Either way each member's Y is exactly
- * (bit for bit) what its own spear_w4ec_linear or spear_w4_linear call
- * writes. */
+ * weights (section 4.1: launch overhead, not arithmetic, dominates the decode
+ * path), and the modules of a transformer block that read the same hidden
+ * state (q, k, v; gate, up) are independent calls. A group runs up to
+ * SPEAR_GROUP_MAX such calls as one launch when all of them take the same
+ * single-launch GEMV variant: the 4-bit product alone (ec NULL) or the fused
+ * local path (M <= 32, an elementwise gate and rank <= 16, where the planner
+ * takes that path), with the same act dtype, token tiles and row tiles.
+ * Local-EC members whose blocks together exceed one round on the GPU are
+ * then launched on four row tiles each, when that leaves their K-slices and
+ * per-wave work unchanged. Otherwise the members run one after another in
+ * array order, each on its own planned path. Either way each member's Y is
+ * exactly (bit for bit) what its own spear_w4ec_linear or spear_w4_linear
+ * call writes. */
 #define SPEAR_GROUP_MAX 4
 
 /* One member: a problem and its operands as in spear_w4ec_linear; ec NULL
