@@ -917,12 +917,19 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
     if (misaligned(workspace)) return SPEAR_E_ALIGN;
   }
   char* ws = (char*)workspace;
+  // every member's own checks first: the cross-member checks below read the
+  // other members' pointers
   for (int i = 0; i < n; ++i) {
     const spear_layer_call_t& c = calls[i];
     const spear_problem_t* p = c.prob;
     if (p->M == 0 || p->N == 0) continue;
     if ((st = check_w4(p, c.x, c.w, c.y)) != SPEAR_OK) return st;
     if (c.ec && (st = check_ec(p, z[i], c.ec, c.y)) != SPEAR_OK) return st;
+  }
+  for (int i = 0; i < n; ++i) {
+    const spear_layer_call_t& c = calls[i];
+    const spear_problem_t* p = c.prob;
+    if (p->M == 0 || p->N == 0) continue;
     const size_t yb = (size_t)p->M * p->N * 2;
     if (overlaps(c.y, yb, workspace, total)) return SPEAR_E_ALIAS;
     for (int j = 0; j < n; ++j)

@@ -102,6 +102,11 @@ def test_member_checks_before_launch():
         for key in ("q", "x", "A", "w"):
             arr, keep = _calls(probs, override={(i, key): 0})
             assert sp.LIB.spear_w4ec_linear_group(3, arr, ws, need, None) == -1, (i, key)
+    # a later member's NULL weight struct is reported before any member's
+    # output is compared with it
+    arr, keep = _calls(probs)
+    arr[2].w = None
+    assert sp.LIB.spear_w4ec_linear_group(3, arr, ws, need, None) == -1
     # workspace size and alignment
     arr, keep = _calls(probs)
     if need > 0:
