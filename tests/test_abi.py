@@ -270,3 +270,38 @@ def test_empty_problem_is_noop():
 def test_wait_poll_hook_roundtrip():
     old = sp.set_wait_polls(5)
     assert sp.set_wait_polls(old) == 5
+
+
+def test_decode_launch_shape_rules():
+    """The measured launch-shape rules at a single token: the fewest row
+    tiles whose grid fits one round of 256 blocks, no second K-slice on the
+    70B-shaped 8192-row modules, and the producer-fused variant on one row
+    tile for layers of 4096+ rows."""
+    # 1B q: one row tile (16 rows), one K-slice, 128 blocks
+    p = _plan(M=1)
+    assert (p.tile_n, p.split_k, p.grid) == (16, 1, 128)
+    # 1B gate: one row tile would need 512 blocks, so two
+    p = _plan(M=1, N=8192)
+    assert (p.tile_n, p.grid) == (32, 256)
+    # 70B q, 4-bit only: two row tiles, unsplit
+    p = _plan(M=1, N=8192, K=8192, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k, p.grid) == (32, 1, 256)
+    # 8B q, rank 32: the fused GEMV on one row tile, unsplit
+    p = _plan(M=1, N=4096, K=4096, rank=32)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (16, 1)
+    # at 16 tokens the earlier shapes stay (1B down: two row tiles, four slices)
+    p = _plan(M=16, N=2048, K=8192, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k) == (32, 4)
+
+
+def test_prefill_tile_rule():
+    """256-token GEMM tiles only above 128 tokens: when they fill the CUs
+    (deep K counting extra rounds), or up to 512 tokens on layers of 32M+
+    weights once a quarter of the CUs have one."""
+    def tm(M, N, K, rank=64):
+        return _plan(M=M, N=N, K=K, rank=rank).tile_m
+    assert tm(64, 28672, 8192) == 128 and tm(128, 28672, 8192) == 128
+    assert tm(192, 28672, 8192) == 256
+    assert tm(256, 8192, 8192) == 256          # 70B q: 64M weights
+    assert tm(256, 2048, 8192, rank=16) == 128  # 1B down: 16M weights
+    assert tm(4096, 2048, 2048, rank=32) == 256
