@@ -8,7 +8,7 @@
  *     Y = X . What^T + alpha * ( gate(X) (.) (X . A^T) ) . B^T
  *
  * with What[n][k] = (q[n][k] - z[n][k/G]) * s[n][k/G], the asymmetric
- * round-to-nearest 4-bit backbone of sections 3.2 and 5.1 (per output
+ * round-to-nearest 4-bit backbone of sections 2.1 and 5.1 (per output
  * channel, or per group of G input channels). The phase-aware dispatch of
  * section 4.1 chooses between a single fused kernel (decode, small M) and a
  * semi-fused EC pre-kernel + 4-bit GEMM whose epilogue adds the EC (prefill,
@@ -130,7 +130,7 @@ typedef struct {
   const uint8_t* zeros;    /* [N][K/G] 0..15                                  */
 } spear_w4_t;
 
-/* Storage of the EC factors A and B (section 6 and the appendix: the
+/* Storage of the EC factors A and B (section 5.1 and Appendix B.2: the
  * deployed compensators keep A and B in INT8, per output channel and
  * symmetric, and the gate in fp16). */
 enum {
@@ -181,7 +181,7 @@ spear_status_t spear_dispatch_plan(const spear_problem_t* prob, int32_t with_ec,
                                    spear_plan_t* out);
 
 /* Y = X . What^T: the 4-bit weight-only linear layer with no EC (the
- * backbone of sections 3.2 and 5.1). The rank, gate and EC fields of *prob
+ * backbone of sections 2.1 and 5.1). The rank, gate and EC fields of *prob
  * are ignored. */
 spear_status_t spear_w4_linear(const spear_problem_t* prob, const void* x,
                                const spear_w4_t* w, void* y, void* workspace,
@@ -278,7 +278,7 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
 /* Diagnostic of the dequantisation the kernels use: writes
  * w_out[n][k] = RNE_act((q[n][k] - z[n][k/G]) * s[n][k/G]) as a dense [N][K]
  * act-dtype matrix, the exact product rounded once to nearest even
- * (sections 3.2, 5.1). Only N, K, group_size and act_dtype of *prob are
+ * (sections 2.1, 5.1). Only N, K, group_size and act_dtype of *prob are
  * read. */
 spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w,
                                 void* w_out, void* hip_stream);

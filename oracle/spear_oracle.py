@@ -7,7 +7,7 @@ headers, helpers, tables or pre/post-processing); its inputs are the stored
 tensors produced by the seeded generator, passed in as numpy arrays.
 
 What it computes (SPEAR, section 3.1, Eq. 3, with the quantised backbone of
-sections 3.2 and 5.1):
+sections 2.1 and 5.1):
 
     Y = X . What^T  +  alpha * ( gate(X) (.) (X . A^T) ) . B^T
 
@@ -28,7 +28,10 @@ Pins (see tests/test_oracle_*.py): brute-force exact rational arithmetic on
 tiny shapes, integer-grid exactness, the RTN round trip, reductions to the
 plain 4-bit product (r = 0, gate == 0, W_hat == 0), the static-LoRA special
 case of the tanh gate, the factored form (Eq. 4), hand-worked golden
-fixtures, and planted-mistake checks that each pin catches.
+fixtures, and planted-mistake checks that each pin catches. The sampled-column
+evaluation (w4ec_linear_rows) is pinned column by column against exact
+rationals and against the factored form under the tanh gate; the parity bar
+itself (tolerance_check) against hand-worked cases at and around both bounds.
 
 INT8 EC factors (the deployed format: A and B stored as int8 codes with one
 symmetric scale per output channel) enter as their exact dequantised values
@@ -76,7 +79,7 @@ def dequant(qweight, scales_bits, zeros, group_size: int) -> np.ndarray:
     """What[n][k] = (q[n][k] - z[n][k // G]) * s[n][k // G], exact in float64.
 
     (q - z) is an integer of magnitude <= 15 and s an fp16 value, so the
-    product has at most 15 significant bits and is exact (sections 3.2, 5.1:
+    product has at most 15 significant bits and is exact (sections 2.1, 5.1:
     asymmetric round-to-nearest per channel or per group of 128).
     """
     q = unpack_int4(qweight)
@@ -186,8 +189,8 @@ def w4ec_linear_f64(x, W_hat, A, B, alpha: float, gate_kind: int, w_g=None,
 
 
 def dequant_int8(q, scale) -> np.ndarray:
-    """INT8 per-channel symmetric factor (the deployed EC format of section 6
-    and the appendix: INT8 A and B, one scale per output channel): row c of
+    """INT8 per-channel symmetric factor (the deployed EC format of section 5.1
+    and Appendix B.2: INT8 A and B, one scale per output channel): row c of
     the factor is scale[c] * q[c], evaluated exactly in float64."""
     return np.asarray(scale, np.float64)[:, None] * np.asarray(q, np.float64)
 

@@ -1,7 +1,7 @@
 // gfx950 (MI355X) kernels of the W4+EC linear layer.
 //
 // Y = X . What^T + alpha * (gate (.) (X . A^T)) . B^T      (SPEAR, section 3.1, Eq. 3)
-// What[n][k] = (q[n][k] - z[n][k/G]) * s[n][k/G]          (sections 3.2, 5.1)
+// What[n][k] = (q[n][k] - z[n][k/G]) * s[n][k/G]          (sections 2.1, 5.1)
 //
 // MFMA operand convention (v_mfma_f32_16x16x32_{f16,bf16}, wave64): lane l
 // supplies row (l % 16) of the A operand and column (l % 16) of the B operand,

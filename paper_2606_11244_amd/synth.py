@@ -8,9 +8,9 @@ dequantisation, no contraction, no EC projection and no gate. What it does
 compute is the offline side that precedes the layer:
 
 * round-to-nearest (RTN) asymmetric 4-bit quantisation of a float weight
-  matrix, per output channel or per group of input channels (the "vanilla
-  linear quantization" backbone of the paper, section 3.2 and the evaluation
-  setup in section 5.1), and
+  matrix, per output channel or per group of input channels (the plain
+  linear quantiser the paper compensates: the quantised model of section 2.1,
+  evaluated per channel and per group of 128 in section 5.1), and
 * packing of the 4-bit codes, eight to a 32-bit word, in the layout the C ABI
   documents: word j of row n holds code q[n][8j+i] in bits 4i..4i+3.
 

@@ -477,12 +477,112 @@ def check_tail_properties(o, seed=0) -> bool:
             and np.allclose(h2, y + r, rtol=0, atol=1e-15))
 
 
+def check_tolerance_cases(o) -> bool:
+    """The parity bar on hand-worked cases (relative Frobenius error
+    ||y - y_ref|| / ||y_ref|| and max |y - y_ref| against a fraction of
+    max |y_ref|, both inclusive; the reference is always the second
+    argument). Values below are chosen so that every quantity is exact in
+    float64, or sits well clear of the bound."""
+    tc = o.tolerance_check
+    cases = []
+    # default bar (5e-3, 1e-2): relF just inside and just outside
+    yr = np.array([[100.0, 0.0, 0.0, 0.0]])
+    cases.append((yr + [[0, 0.49, 0, 0]], yr, {}, True))
+    cases.append((yr + [[0, 0.51, 0, 0]], yr, {}, False))
+    # a wide reference keeps relF small: the max bound decides
+    wide = np.ones((1, 10000))
+    d = np.zeros((1, 10000))
+    d[0, 17] = 0.0099
+    cases.append((wide + d, wide, {}, True))
+    d[0, 17] = 0.0101
+    cases.append((wide + d, wide, {}, False))
+    # a zero reference: only an exact zero passes
+    z = np.zeros((2, 3))
+    cases.append((z.copy(), z, {}, True))
+    tiny = z.copy()
+    tiny[1, 2] = 1e-30
+    cases.append((tiny, z, {}, False))
+    # exact boundaries (dyadic values): both bounds are inclusive
+    yr2 = np.array([[4.0, 0.0]])
+    y2 = np.array([[4.0, 1.0]])
+    cases.append((y2, yr2, dict(rel_frob=0.25, max_rel=0.5), True))
+    cases.append((y2, yr2, dict(rel_frob=1.0, max_rel=0.25), True))
+    cases.append((y2, yr2, dict(rel_frob=0.2499, max_rel=0.5), False))
+    cases.append((y2, yr2, dict(rel_frob=1.0, max_rel=0.2499), False))
+    # the reference's norm and max are the denominators, not the result's:
+    # y = 2, y_ref = 1 has relF = 1 and max|d| = 1 against max|y_ref| = 1
+    one = np.array([[1.0, 0.0]])
+    two = np.array([[2.0, 0.0]])
+    cases.append((two, one, dict(rel_frob=0.6, max_rel=1.0), False))
+    cases.append((one, two, dict(rel_frob=0.6, max_rel=1.0), True))
+    cases.append((two, one, dict(rel_frob=10.0, max_rel=0.6), False))
+    cases.append((one, two, dict(rel_frob=10.0, max_rel=0.6), True))
+    # magnitudes: a negative reference bounds by its absolute value
+    cases.append((np.array([[-4.0, 1.0]]), np.array([[-4.0, 0.0]]),
+                  dict(rel_frob=1.0, max_rel=0.25), True))
+    for y, y_ref, kw, want in cases:
+        if bool(tc(y, y_ref, **kw)[0]) != want:
+            return False
+    # the reported figures themselves
+    ok, relf, mx, bound = tc(y2, yr2, rel_frob=0.25, max_rel=0.5)
+    return ok and relf == 0.25 and mx == 1.0 and bound == 2.0
+
+
+def check_rows_brute_force(o, seed=0) -> bool:
+    """Eq. 3 on a subset of output columns (activation-dtype factors, both
+    dtypes, gates ONE and SIGMOID_LINEAR) against exact rationals, column by
+    column; the rows include the first and last and come in a scrambled
+    order."""
+    cases = [dict(M=2, N=7, K=16, group_size=8, rank=3, gate_kind=S.GATE_ONE, alpha=0.75),
+             dict(M=3, N=6, K=24, group_size=24, rank=2, gate_kind=S.GATE_SIGMOID_LINEAR, alpha=1.0),
+             dict(M=2, N=5, K=16, group_size=16, rank=0, gate_kind=S.GATE_ONE, alpha=1.0)]
+    for i, c in enumerate(cases):
+        for dt in (S.F16, S.BF16):
+            layer = S.make_layer(seed=seed + 60 + i, act_dtype=dt, ec_std=0.3, wg_std=0.4,
+                                 b_g=-0.2, **c)
+            want = _brute(layer)
+            rows = np.array([layer.N - 1, 0, 3, 1])
+            got = o.w4ec_linear_rows(layer, rows)
+            if got.shape != (layer.M, len(rows)):
+                return False
+            for m in range(layer.M):
+                for i2, n in enumerate(rows):
+                    wv = float(want[m][n])
+                    if abs(got[m][i2] - wv) > 1e-12 * max(1.0, abs(wv)):
+                        return False
+    return True
+
+
+def check_rows_tanh_factored(o, seed=0) -> bool:
+    """Sampled columns under the paper's tanh gate, both dtypes, against the
+    factored form (Eq. 4) built per token: y_m[n] = (W_hat[n] + alpha
+    B[n] diag(gamma(A x_m)) A) x_m."""
+    for dt in (S.F16, S.BF16):
+        base = S.make_layer(M=3, N=40, K=128, group_size=64, rank=5, seed=seed + 7, act_dtype=dt,
+                            gate_kind=S.GATE_TANH_MLP, alpha=0.5, ec_std=0.2)
+        rows = np.array([39, 2, 17, 0])
+        got = o.w4ec_linear_rows(base, rows)
+        f = lambda a: S.from_bits(a, dt).astype(np.float64)  # noqa: E731
+        W_hat = o.dequant(base.qweight, base.scales, base.zeros, 64)
+        x, A, B = f(base.x), f(base.A), f(base.B)
+        for m in range(base.M):
+            u = A @ x[m]
+            hid = np.maximum(f(base.W1) @ u + f(base.b1), 0.0)
+            gam = 1.0 + np.tanh(f(base.W2) @ hid + f(base.b2))
+            for i2, n in enumerate(rows):
+                w_eff = W_hat[n] + 0.5 * (B[n] * gam) @ A
+                if not np.isclose(got[m, i2], w_eff @ x[m], rtol=1e-12, atol=1e-14):
+                    return False
+    return True
+
+
 PINS = [check_unpack_fixed_words, check_unpack_exhaustive, check_golden_examples,
         check_rounding_fixtures, check_rtn_grid_roundtrip, check_rtn_error_bound,
         check_brute_force, check_integer_grid_exact, check_reductions,
         check_sigmoid_half, check_tanh_static_lora, check_factored_form,
         check_gate_ranges, check_dequant_bits_contract, check_int8_brute_force,
-        check_int8_golden, check_tail_golden, check_tail_properties]
+        check_int8_golden, check_tail_golden, check_tail_properties,
+        check_tolerance_cases, check_rows_brute_force, check_rows_tanh_factored]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -597,6 +697,69 @@ def _tail_eps_outside(y, residual, norm_w, eps):
     return h, h / (np.sqrt(np.mean(h * h, axis=1, keepdims=True)) + eps) * np.asarray(norm_w)[None, :]
 
 
+def _tol_wrong_denominator(y, y_ref, rel_frob=5e-3, max_rel=1e-2):
+    y = np.asarray(y, np.float64)
+    y_ref = np.asarray(y_ref, np.float64)
+    diff = y - y_ref
+    den = np.linalg.norm(y)
+    relf = float(np.linalg.norm(diff) / den) if den > 0 else float(np.linalg.norm(diff))
+    mx = float(np.abs(diff).max(initial=0.0))
+    bound = max_rel * float(np.abs(y_ref).max(initial=0.0))
+    return (relf <= rel_frob) and (mx <= bound if bound > 0 else mx == 0.0), relf, mx, bound
+
+
+def _tol_strict(y, y_ref, rel_frob=5e-3, max_rel=1e-2):
+    ok, relf, mx, bound = O.tolerance_check(y, y_ref, rel_frob, max_rel)
+    return (relf < rel_frob) and (mx < bound if bound > 0 else mx == 0.0), relf, mx, bound
+
+
+def _tol_bound_from_result(y, y_ref, rel_frob=5e-3, max_rel=1e-2):
+    _, relf, mx, _ = O.tolerance_check(y, y_ref, rel_frob, max_rel)
+    bound = max_rel * float(np.abs(np.asarray(y, np.float64)).max(initial=0.0))
+    return (relf <= rel_frob) and (mx <= bound if bound > 0 else mx == 0.0), relf, mx, bound
+
+
+def _tol_zero_reference_passes(y, y_ref, rel_frob=5e-3, max_rel=1e-2):
+    ok, relf, mx, bound = O.tolerance_check(y, y_ref, rel_frob, max_rel)
+    return (ok or bound == 0.0), relf, mx, bound
+
+
+def _tol_signed_max(y, y_ref, rel_frob=5e-3, max_rel=1e-2):
+    _, relf, mx, _ = O.tolerance_check(y, y_ref, rel_frob, max_rel)
+    bound = max_rel * float(np.asarray(y_ref, np.float64).max(initial=0.0))
+    return (relf <= rel_frob) and (mx <= bound if bound > 0 else mx == 0.0), relf, mx, bound
+
+
+def _rows_b_unselected(layer, rows):
+    sub = copy.copy(layer)
+    sub.B = layer.B[:len(rows)]  # B's first rows instead of the selected ones
+    W_hat = O.dequant(layer.qweight[rows], layer.scales[rows], layer.zeros[rows],
+                      layer.group_size)
+    dt = layer.act_dtype
+    x = O.bits_to_f64(layer.x, dt)
+    if layer.rank == 0:
+        return O.w4_linear(x, W_hat)
+    return O.w4ec_linear_f64(x, W_hat, O.bits_to_f64(layer.A, dt), O.bits_to_f64(sub.B, dt),
+                             layer.alpha, layer.gate_kind, w_g=O.bits_to_f64(layer.w_g, dt),
+                             b_g=layer.b_g, W1=O.bits_to_f64(layer.W1, dt),
+                             b1=O.bits_to_f64(layer.b1, dt), W2=O.bits_to_f64(layer.W2, dt),
+                             b2=O.bits_to_f64(layer.b2, dt))
+
+
+def _rows_act_drops_ec(layer, rows):
+    if getattr(layer, "ab_int8", False):
+        return O.w4ec_linear_rows(layer, rows)
+    W_hat = O.dequant(layer.qweight[rows], layer.scales[rows], layer.zeros[rows],
+                      layer.group_size)
+    return O.w4_linear(O.bits_to_f64(layer.x, layer.act_dtype), W_hat)
+
+
+def _rows_gate_dropped(layer, rows):
+    flat = copy.copy(layer)
+    flat.gate_kind = O.GATE_ONE
+    return O.w4ec_linear_rows(flat, rows)
+
+
 MUTANTS = {
     "nibble order reversed": dict(unpack_int4=_unpack_reversed),
     "zero point added": dict(dequant=_dequant_plus_zero),
@@ -613,6 +776,14 @@ MUTANTS = {
     "tail drops the residual": dict(post_ec_tail=_tail_no_residual),
     "RMSNorm divides by the sum": dict(post_ec_tail=_tail_sum_not_mean),
     "RMSNorm epsilon outside the root": dict(post_ec_tail=_tail_eps_outside),
+    "parity bar relative to the result's norm": dict(tolerance_check=_tol_wrong_denominator),
+    "parity bar with strict inequalities": dict(tolerance_check=_tol_strict),
+    "parity bar's max bound from the result": dict(tolerance_check=_tol_bound_from_result),
+    "parity bar passes any zero reference": dict(tolerance_check=_tol_zero_reference_passes),
+    "parity bar's max bound from the signed max": dict(tolerance_check=_tol_signed_max),
+    "sampled columns take B's first rows": dict(w4ec_linear_rows=_rows_b_unselected),
+    "sampled columns drop the EC (act-dtype factors)": dict(w4ec_linear_rows=_rows_act_drops_ec),
+    "sampled columns ignore the gate": dict(w4ec_linear_rows=_rows_gate_dropped),
 }
 
 
