@@ -1,32 +1,29 @@
 """Benchmark of the W4+EC linear layer on one MI355X.
 
-One step = one pass of the hot path over one batch of synthetic input on a
-Llama-3.2-1B-shaped model (hidden 2048, MLP 8192; q, k, v, o, gate, up, down
-per layer; group-128 4-bit weights, EC rank 16 with the sigmoid-linear gate,
-fp16 activations):
+One step = one pass of the hot path over one batch of synthetic input on the
+Llama-2-70B-shaped model that fits one GPU: all 80 layers x 7 linear modules
+(q/o 8192->8192, k/v 8192->1024, gate/up 8192->28672, down 28672->8192) of
+group-128 4-bit weights resident in HBM (about 36 GB of device-random codes,
+scales and zero points), the EC (rank 64, sigmoid-linear gate, fp16) on the
+seeded 25% of the (layer, module) pairs and the 4-bit product alone on the
+rest, every call on its automatic-dispatch path:
 
-  decode   M = 1: all 16 layers x 7 modules through the automatic dispatch
-           (the fused single-kernel path), the modules that read one hidden
-           state launched together (per layer: q, k, v in one grouped call;
-           o; gate, up in one grouped call; down). Two distinct copies of the
-           model weights alternate between steps (2 x 0.53 GB), so the
-           weights come from HBM rather than the 256 MB Infinity Cache. The
-           same pass with one call per module is reported beside it.
-  prefill  M = 4096 tokens (1% of input channels scaled x20): the 7 modules of
-           one layer through the automatic dispatch (EC pre-kernel + 4-bit
-           GEMM with the EC in its epilogue).
+  decode   M = 1: every module once (560 calls);
+  prefill  M = 4096 tokens: every module once.
 
-Both passes are captured once as HIP graphs and replayed. The printed JSON
-line reports decode HBM throughput (algorithmic bytes / time) as `value`, the
-prefill MFMA throughput under `prefill`, each with its roofline, the EC
-overhead over the same passes without EC, and the CPU oracle timed on a
-bounded sample (`cpu_baseline`).
+Each pass is captured once as a HIP graph and replayed. The printed JSON line
+reports the decode pass's HBM throughput (algorithmic bytes / time) as
+`value` with its roofline, the prefill pass's MFMA throughput under
+`prefill`, the model's EC overhead over the same passes with no EC, the
+decode pass under the paper's timing protocol (200 warm-up and 500 timed
+replays, median), and the CPU oracle timed on a bounded sample
+(`cpu_baseline`).
 
-Context line `decode_70b_layer`: one Llama-2-70B-shaped layer (7 modules,
-K/N up to 28672, EC rank 64 on every module) at M = 1, fused path, two weight
-copies alternating. Its weights are uniform random codes, scales and zero
-points drawn on the device (timing only: the kernels' work does not depend on
-the values), so that the 0.93 GB do not have to be generated on the host.
+Extra fields on the Llama-3.2-1B-shaped layers (`llama1b`): the decode pass
+over 16 layers x 7 modules at M = 1 (grouped calls, two weight copies
+alternating so that the weights come from HBM), the 7 modules at M = 4096,
+their EC overhead, the same passes with INT8 EC factors and with the post-EC
+tail.
 """
 from __future__ import annotations
 
@@ -47,6 +44,7 @@ MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 MFMA
 LAYERS_1B = 16
 RANK = 16
 GROUP = 128
+DEC_M, PRE_M = 1, 4096  # the metric's decode and prefill token counts
 # per decoder layer, the modules that read one hidden state (q, k, v; gate,
 # up) go out as one grouped call; o and down alone
 DEC_GROUPS = ((0, 1, 2), (3,), (4, 5), (6,))
@@ -86,244 +84,197 @@ def stored_traffic():
     return d
 
 
-def cpu_baseline(dec_layers, pre_layer, budget_s=12.0):
-    """The float64 oracle on the host cores: the 7 decode modules of one layer
-    (repeated), and one prefill module (q, M=4096)."""
+def cpu_baseline(sel, budget_s=20.0):
+    """The float64 oracle on the host cores, on a bounded sample of the
+    70B-shaped model's decode pass: for each of the 7 module shapes, with the
+    EC (rank 64) and without, the oracle evaluates a seeded layer of full K
+    restricted to 128 and to 256 output rows at M = 1 (median of three runs
+    each); the time of a full-width module is the line through those two
+    points at its N, and the pass is the sum over the 80 layers' modules with
+    the model's EC selection. The prefill rate comes from the 70B q shape at
+    M = 4096 on 256 output rows (time scaled to the full rows)."""
     import numpy as np
     from oracle import spear_oracle as O
+    from paper_2606_11244_amd import synth as S
     try:
         from threadpoolctl import threadpool_info
         blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # noqa: BLE001
         blas = 1
-    reps, t_dec, nbytes = 0, 0.0, 0.0
-    t0 = time.perf_counter()
-    while reps < 1 or (time.perf_counter() - t0 < budget_s * 0.6 and reps < 8):
-        for L in dec_layers:
-            ts = time.perf_counter()
+    t_start = time.perf_counter()
+
+    def timed(L, reps=3):
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
             y = O.w4ec_linear(L)
-            t_dec += time.perf_counter() - ts
-            nbytes += algo_bytes(L.M, L.N, L.K, L.group_size, L.rank)
+            ts.append(time.perf_counter() - t0)
             assert np.isfinite(y).all()
-        reps += 1
-    ts = time.perf_counter()
-    O.w4ec_linear(pre_layer)
-    t_pre = time.perf_counter() - ts
-    # single-threaded: the tiny workload and the 1B q module at M = 1
-    single = None
-    try:
-        from threadpoolctl import threadpool_limits
-        from paper_2606_11244_amd import synth as S
-        tiny = S.config_layer(0, "tiny", 4, seed=0)
-        with threadpool_limits(limits=1):
-            out = {}
-            for name, LL, n in (("tiny", tiny, 20), ("1b_q_m1", dec_layers[0], 2)):
-                ts = time.perf_counter()
-                for _ in range(n):
-                    O.w4ec_linear(LL)
-                dt = (time.perf_counter() - ts) / n
-                out[name] = {"ms_per_call": round(dt * 1e3, 3),
-                             "GBps": round(algo_bytes(LL.M, LL.N, LL.K, LL.group_size, LL.rank)
-                                           / dt / 1e9, 4)}
-        single = out
-    except Exception as exc:  # noqa: BLE001
-        single = {"error": str(exc)[:80]}
-    L = pre_layer
+        return float(np.median(ts))
+
+    per_module = {}
+    for j, m in enumerate(S.MODULES):
+        K, N = S.LLAMA_70B[m]
+        for r in (0, 64):
+            t = {}
+            for ns in (128, 256):
+                L = S.make_layer(M=DEC_M, N=ns, K=K, group_size=GROUP, rank=r, seed=0,
+                                 config_id=4, module_id=j)
+                t[ns] = timed(L)
+            slope = max(0.0, (t[256] - t[128]) / 128.0)
+            per_module[(m, r)] = t[128] + slope * (N - 128)
+    t_pass, nbytes = 0.0, 0.0
+    for l in range(sel.shape[0]):
+        for j, m in enumerate(S.MODULES):
+            K, N = S.LLAMA_70B[m]
+            r = 64 if sel[l, j] else 0
+            t_pass += per_module[(m, r)]
+            nbytes += algo_bytes(DEC_M, N, K, GROUP, r)
+    K, N = S.LLAMA_70B["q"]
+    Lp = S.make_layer(M=PRE_M, N=256, K=K, group_size=GROUP, rank=64, seed=0, config_id=4,
+                      module_id=0)
+    t_pre = timed(Lp, reps=1) * N / 256.0
     return {
-        "value": round(nbytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": int(blas),
+        "value": round(nbytes / t_pass / 1e9, 4), "unit": "GB/s", "cores": int(blas),
         "kind": "oracle",
-        "sample": (f"float64 numpy oracle: one 1B-shaped layer (7 modules, M=1) x {reps} "
-                   f"({nbytes / 1e6:.0f} MB algorithmic, {t_dec:.1f} s); prefill q module "
-                   f"M={L.M} ({t_pre:.1f} s)"),
-        "prefill_tflops": round(algo_flops(L.M, L.N, L.K, L.rank) / t_pre / 1e12, 5),
+        "sample": ("float64 numpy oracle on the 70B-shaped decode pass (M=1), extrapolated: "
+                   "each of the 7 module shapes with and without the EC (rank 64) on 128 and "
+                   "256 output rows of full K, median of 3, the time line evaluated at the "
+                   "module's N, summed over 80 layers with the model's EC selection "
+                   f"({t_pass:.1f} s per pass, {nbytes / 1e9:.1f} GB algorithmic)"),
+        "prefill_tflops": round(algo_flops(PRE_M, N, K, 64) / t_pre / 1e12, 5),
+        "prefill_sample": "70B q shape at M=4096, 256 of 8192 output rows, time scaled x32",
         "host_cpus": os.cpu_count(),
-        "single_thread": single,
+        "cpu_seconds": round(time.perf_counter() - t_start, 1),
     }
 
 
-def decode_70b_context(sp, torch, steps, warmup, dev):
-    """M = 1 decode of one 70B-shaped layer (fused W4+EC and W4-only)."""
-    from paper_2606_11244_amd import synth as S
-    g = torch.Generator(device=dev)
-    g.manual_seed(0)
-    r, G = 64, 128
-    mods = []
-    for c in range(2):
+class Model70B:
+    """The 70B-shaped model resident in HBM and one pass of its linear layers
+    at M tokens (every module once, each call on its AUTO path)."""
+
+    def __init__(self, sp, torch, dev, Mmax):
+        from paper_2606_11244_amd import model70b
+        from paper_2606_11244_amd import synth as S
+        self.sp, self.torch, self.S = sp, torch, S
+        self.r, self.G = model70b.RANK, model70b.GROUP
+        self.layers, self.sel = model70b.build(dev)
+        Kmax = max(k for k, _ in S.LLAMA_70B.values())
+        Nmax = max(n for _, n in S.LLAMA_70B.values())
+        g = torch.Generator(device=dev)
+        g.manual_seed(1)
+        self.xbuf = torch.randn((Mmax * Kmax,), device=dev, generator=g).half()
+        self.ybuf = torch.empty((Mmax * Nmax,), dtype=torch.float16, device=dev)
+        self.dev = dev
+
+    def plans(self, M):
+        sp, S = self.sp, self.S
+        out = {}
         for m in S.MODULES:
             K, N = S.LLAMA_70B[m]
-            q = torch.randint(-2**31, 2**31 - 1, (N, K // 8), dtype=torch.int32, device=dev, generator=g)
-            sc = (torch.rand((N, K // G), device=dev, generator=g) * 1e-3 + 1e-4).half().view(torch.int16)
-            zr = torch.randint(0, 16, (N, K // G), dtype=torch.uint8, device=dev, generator=g)
-            x = torch.randn((1, K), device=dev, generator=g).half()
-            A = (torch.randn((r, K), device=dev, generator=g) * 0.01).half()
-            B = (torch.randn((N, r), device=dev, generator=g) * 0.01).half()
-            wg = (torch.randn((K,), device=dev, generator=g) * 0.05).half()
-            y = torch.empty((1, N), dtype=torch.float16, device=dev)
-            pr = sp.problem(1, N, K, G, sp.F16, r, sp.GATE_SIGMOID_LINEAR)
-            mods.append((c, pr, q, sc, zr, x, A, B, wg, y, K, N))
-    ws = torch.zeros(max(max(sp.dispatch_plan(m[1]).workspace_bytes for m in mods), 256),
-                     dtype=torch.uint8, device=dev)
-    ws4 = torch.zeros(max(max(sp.dispatch_plan(m[1], with_ec=False).workspace_bytes for m in mods), 256),
-                      dtype=torch.uint8, device=dev)
+            out[m] = (sp.problem(M, N, K, self.G, sp.F16, self.r, sp.GATE_SIGMOID_LINEAR),
+                      sp.problem(M, N, K, self.G, sp.F16, 0, sp.GATE_SIGMOID_LINEAR))
+        return out
 
-    def run(c, ec):
-        for (cc, pr, q, sc, zr, x, A, B, wg, y, K, N) in mods:
-            if cc != c:
-                continue
-            if ec:
-                sp.w4ec_linear(pr, x, q, sc, zr, A, B, y, w_g=wg, workspace=ws)
-            else:
-                sp.w4_linear(pr, x, q, sc, zr, y, workspace=ws4)
+    def workspace(self, M):
+        sp = self.sp
+        need = 256
+        for pe, p4 in self.plans(M).values():
+            need = max(need, sp.dispatch_plan(pe).workspace_bytes,
+                       sp.dispatch_plan(p4, with_ec=False).workspace_bytes)
+        return self.torch.zeros(need, dtype=self.torch.uint8, device=self.dev)
 
-    def timed(ec):
-        graphs = []
-        for c in range(2):
-            s = torch.cuda.Stream()
-            s.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(s):
-                run(c, ec)
-            torch.cuda.current_stream().wait_stream(s)
-            torch.cuda.synchronize()
-            gr = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(gr):
-                run(c, ec)
-            graphs.append(gr)
-        for i in range(warmup):
-            graphs[i % 2].replay()
+    def run(self, M, with_ec, ws):
+        sp = self.sp
+        plans = self.plans(M)
+        for mods in self.layers:
+            for (m, K, N, q, sc, zr, ec) in mods:
+                x = self.xbuf[:M * K].view(M, K)
+                y = self.ybuf[:M * N].view(M, N)
+                pe, p4 = plans[m]
+                if with_ec and ec is not None:
+                    sp.w4ec_linear(pe, x, q, sc, zr, ec[0], ec[1], y, w_g=ec[2], workspace=ws)
+                else:
+                    sp.w4_linear(p4, x, q, sc, zr, y, workspace=ws)
+
+    def capture(self, M, with_ec, ws):
+        torch = self.torch
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            self.run(M, with_ec, ws)
+        torch.cuda.current_stream().wait_stream(s)
         torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            self.run(M, with_ec, ws)
+        torch.cuda.synchronize()
+        return gr
+
+    def work(self, M, with_ec=True):
+        """(algorithmic bytes, algorithmic flops, launches) of one pass."""
+        sp = self.sp
+        plans = self.plans(M)
+        nbytes = flops = 0.0
+        launches = 0
+        for mods in self.layers:
+            for (m, K, N, q, sc, zr, ec) in mods:
+                r = self.r if (with_ec and ec is not None) else 0
+                nbytes += algo_bytes(M, N, K, self.G, r)
+                flops += algo_flops(M, N, K, r)
+                pe, p4 = plans[m]
+                launches += (sp.dispatch_plan(pe).num_launches if r
+                             else sp.dispatch_plan(p4, with_ec=False).num_launches)
+        return nbytes, flops, launches
+
+    def paths(self, M):
+        sp = self.sp
+        return {m: sp.PATH_NAMES[sp.dispatch_plan(pe).path] for m, (pe, _) in self.plans(M).items()}
+
+
+def replay_times(torch, graph, n):
+    """Event-timed replays of one graph on the current stream (seconds each)."""
+    ev = []
+    for _ in range(n):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        for i in range(steps):
-            graphs[i % 2].replay()
+        graph.replay()
         e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e-3 / steps
-
-    t_ec, t_w4 = timed(True), timed(False)
-    nb = sum(algo_bytes(1, N, K, G, r) for (c, pr, q, sc, zr, x, A, B, wg, y, K, N) in mods if c == 0)
-    nb4 = sum(algo_bytes(1, N, K, G, 0) for (c, pr, q, sc, zr, x, A, B, wg, y, K, N) in mods if c == 0)
-    return {"GBps": round(nb / t_ec / 1e9, 1), "frac": round(nb / t_ec / 1e9 / HBM_PEAK_GBS, 4),
-            "us_per_layer": round(t_ec * 1e6, 2), "w4_only_GBps": round(nb4 / t_w4 / 1e9, 1),
-            "w4_only_us_per_layer": round(t_w4 * 1e6, 2), "ec_overhead": round(t_ec / t_w4 - 1, 4),
-            "rank": r, "path": "fused_gemv", "weights": "device-random (timing only)"}
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) * 1e-3 for a, b in ev]
 
 
-def model_70b_pass(sp, torch, dev, Ms=(1, 16, 64, 512, 4096, 8192), reps=3):
-    """The 70B-shaped model's linear layers as one pass per token count: all
-    80 layers x 7 modules resident in HBM (device-random 4-bit weights,
-    group 128, about 36 GB), the EC (rank 64, sigmoid-linear gate) on the
-    seeded 25% of the (layer, module) pairs and the 4-bit product alone on
-    the rest, every call on its AUTO path; the same pass with no EC at all
-    gives the model's EC overhead. Each pass is one captured graph."""
-    from paper_2606_11244_amd import model70b
-    from paper_2606_11244_amd import synth as S
-    r, G = model70b.RANK, model70b.GROUP
-    layers, sel = model70b.build(dev)
-    Kmax, Nmax, Mmax = max(k for k, _ in S.LLAMA_70B.values()), max(n for _, n in S.LLAMA_70B.values()), max(Ms)
-    g = torch.Generator(device=dev)
-    g.manual_seed(1)
-    xbuf = torch.randn((Mmax * Kmax,), device=dev, generator=g).half()
-    ybuf = torch.empty((Mmax * Nmax,), dtype=torch.float16, device=dev)
-    out = {"weights": "device-random (timing only)",
-           "ec": f"rank 64 on a seeded 25% of the (layer, module) pairs ({int(sel.sum())} of {sel.size})",
-           "passes": []}
+def model_70b_sweep(model, Ms=(1, 16, 64, 512, 8192), reps=3):
+    """Further token counts of the 70B-shaped model's pass (the sweep of its
+    workload), each with its EC overhead."""
+    import numpy as np
+    torch = model.torch
+    out = []
     for M in Ms:
-        plans = {}
-        ws_need = 256
-        for m in S.MODULES:
-            K, N = S.LLAMA_70B[m]
-            pe = sp.problem(M, N, K, G, sp.F16, r, sp.GATE_SIGMOID_LINEAR)
-            p4 = sp.problem(M, N, K, G, sp.F16, 0, sp.GATE_SIGMOID_LINEAR)
-            plans[m] = (pe, p4)
-            ws_need = max(ws_need, sp.dispatch_plan(pe).workspace_bytes,
-                          sp.dispatch_plan(p4, with_ec=False).workspace_bytes)
-        ws = torch.zeros(ws_need, dtype=torch.uint8, device=dev)
-
-        def run(with_ec):
-            for mods in layers:
-                for (m, K, N, q, sc, zr, ec) in mods:
-                    x = xbuf[:M * K].view(M, K)
-                    y = ybuf[:M * N].view(M, N)
-                    pe, p4 = plans[m]
-                    if with_ec and ec is not None:
-                        sp.w4ec_linear(pe, x, q, sc, zr, ec[0], ec[1], y, w_g=ec[2], workspace=ws)
-                    else:
-                        sp.w4_linear(p4, x, q, sc, zr, y, workspace=ws)
-
-        def timed(with_ec):
-            s = torch.cuda.Stream()
-            s.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(s):
-                run(with_ec)
-            torch.cuda.current_stream().wait_stream(s)
-            torch.cuda.synchronize()
-            gr = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(gr):
-                run(with_ec)
-            gr.replay()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(reps):
-                gr.replay()
-            e1.record()
-            torch.cuda.synchronize()
-            del gr
-            return e0.elapsed_time(e1) * 1e-3 / reps
-
-        t_ec, t_w4 = timed(True), timed(False)
-        nbytes = sum(algo_bytes(M, N, K, G, r if ec is not None else 0)
-                     for mods in layers for (m, K, N, q, sc, zr, ec) in mods)
-        flops = sum(algo_flops(M, N, K, r if ec is not None else 0)
-                    for mods in layers for (m, K, N, q, sc, zr, ec) in mods)
-        out["passes"].append({
-            "M": M, "ms_per_pass": round(t_ec * 1e3, 3), "w4_only_ms": round(t_w4 * 1e3, 3),
-            "ec_overhead": round(t_ec / t_w4 - 1, 4), "GBps": round(nbytes / t_ec / 1e9, 1),
-            "hbm_frac": round(nbytes / t_ec / 1e9 / HBM_PEAK_GBS, 4),
-            "TFLOPs": round(flops / t_ec / 1e12, 1),
-            "mfma_frac": round(flops / t_ec / 1e12 / MFMA_F16_PEAK_TFLOPS, 4)})
-        print("bench: 70B model pass M=%d: %.3f ms (W4-only %.3f ms)" % (M, t_ec * 1e3, t_w4 * 1e3),
+        ws = model.workspace(M)
+        t = {}
+        for ec in (True, False):
+            g = model.capture(M, ec, ws)
+            g.replay()
+            t[ec] = float(np.median(replay_times(torch, g, reps)))
+            del g
+        nbytes, flops, _ = model.work(M)
+        out.append({"M": M, "ms_per_pass": round(t[True] * 1e3, 3),
+                    "w4_only_ms": round(t[False] * 1e3, 3),
+                    "ec_overhead": round(t[True] / t[False] - 1, 4),
+                    "GBps": round(nbytes / t[True] / 1e9, 1),
+                    "hbm_frac": round(nbytes / t[True] / 1e9 / HBM_PEAK_GBS, 4),
+                    "TFLOPs": round(flops / t[True] / 1e12, 1),
+                    "mfma_frac": round(flops / t[True] / 1e12 / MFMA_F16_PEAK_TFLOPS, 4)})
+        print("bench: 70B model pass M=%d: %.3f ms (W4-only %.3f ms)" % (M, t[True] * 1e3, t[False] * 1e3),
               file=sys.stderr, flush=True)
         del ws
-    del layers, xbuf, ybuf
-    torch.cuda.empty_cache()
     return out
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--copies", type=int, default=2, help="decode weight copies rotated per step")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-overhead", action="store_true", help="skip the W4-only reference passes")
-    ap.add_argument("--no-70b", action="store_true", help="skip the 70B-layer context line")
-    ap.add_argument("--no-int8", action="store_true",
-                    help="skip the passes with INT8 per-channel EC factors")
-    ap.add_argument("--no-ungrouped", action="store_true",
-                    help="skip the decode pass with one call per module")
-    ap.add_argument("--no-tail", action="store_true",
-                    help="skip the passes with the post-EC tail on o and down")
-    ap.add_argument("--model70b", action="store_true",
-                    help="also time the 70B-shaped model's linear layers (80 layers resident, "
-                         "about 36 GB) at M = 1 .. 8192")
-    ap.add_argument("--copy-calib-mb", type=int, default=0,
-                    help="also run one device copy of this many MiB (counter calibration)")
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: the W4+EC layer is built and timed on a single "
-              "MI355X (multi-GPU runs are out of scope); use --gpus 1", file=sys.stderr)
-        sys.exit(2)
-
-    import numpy as np
-    import torch
-
-    from paper_2606_11244_amd import spear as sp
-    from paper_2606_11244_amd import synth as S
-
-    torch.cuda.set_device(0)
-    dev = "cuda:0"
+def llama1b_extras(args, sp, S, np, torch, dev):
+    """The Llama-3.2-1B-shaped decode and prefill passes (extra fields)."""
     print("bench: generating layers", file=sys.stderr, flush=True)
     dec_base = [S.config_layer(1, m, 1, seed=0) for m in S.MODULES]
     pre_base = [S.config_layer(2, m, 4096, seed=0) for m in S.MODULES]
@@ -562,15 +513,135 @@ def main():
                 "decode_ms_per_pass": round(dt_ * 1e3, 4), "prefill_ms_per_pass": round(pt_ * 1e3, 4),
                 "decode_added": round(dt_ / dec_s - 1.0, 4), "prefill_added": round(pt_ / pre_s - 1.0, 4)}
 
-    model70 = None
-    if args.model70b:
-        print("bench: 70B-shaped model pass", file=sys.stderr, flush=True)
-        model70 = model_70b_pass(sp, torch, dev)
+    traffic = stored_traffic()
+    n_launch_dec = LAYERS_1B * len(DEC_GROUPS)
+    return {
+        "workload": ("llama-3.2-1b-shaped W4+EC linear layers (q,k,v,o 2048->2048/512, "
+                     "gate/up 2048->8192, down 8192->2048), group 128, rank 16, sigmoid-linear "
+                     "gate, fp16: decode M=1 over 16 layers x 7 modules (grouped calls, "
+                     "%d weight copies alternating) + prefill M=4096 over 7 modules" % args.copies),
+        "decode_GBps": round(dec_gbs, 2), "decode_ms_per_pass": round(dec_s * 1e3, 4),
+        "decode_hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+        "decode_path": sp.PATH_NAMES[dec_plan.path],
+        "decode_launches": n_launch_dec,
+        "decode_avg_launch_us": round(dec_s / n_launch_dec * 1e6, 3),
+        "decode_traffic_per_launch": (traffic or {}).get("decode_bytes_per_launch"),
+        "decode_algo_bytes_per_launch": round(dec_bytes / n_launch_dec),
+        "prefill_TFLOPs": round(pre_tfl, 2), "prefill_ms_per_pass": round(pre_s * 1e3, 4),
+        "prefill_mfma_frac": round(pre_tfl / MFMA_F16_PEAK_TFLOPS, 4),
+        "prefill_paths": {m: sp.PATH_NAMES[sp.dispatch_plan(d.problem()).path]
+                          for m, d in zip(S.MODULES, pre_dev)},
+        "prefill_traffic_per_launch": (traffic or {}).get("prefill_bytes_per_launch"),
+        "decode_one_call_per_module": ungrouped,
+        "ec_overhead": overhead,
+        "ec_int8": int8,
+        "post_ec_tail": tail,
+    }
 
-    ctx70 = None
-    if not args.no_70b:
-        print("bench: 70B-layer decode context", file=sys.stderr, flush=True)
-        ctx70 = decode_70b_context(sp, torch, args.steps, args.warmup, dev)
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--copies", type=int, default=2,
+                    help="1B decode: weight copies rotated per step")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-overhead", action="store_true", help="skip the W4-only reference passes")
+    ap.add_argument("--no-paper-protocol", action="store_true",
+                    help="skip the decode pass timed as 200 warm-up + 500 timed replays")
+    ap.add_argument("--no-1b", action="store_true", help="skip the Llama-3.2-1B-shaped passes")
+    ap.add_argument("--no-int8", action="store_true",
+                    help="1B: skip the passes with INT8 per-channel EC factors")
+    ap.add_argument("--no-ungrouped", action="store_true",
+                    help="1B: skip the decode pass with one call per module")
+    ap.add_argument("--no-tail", action="store_true",
+                    help="1B: skip the passes with the post-EC tail on o and down")
+    ap.add_argument("--model70b", action="store_true",
+                    help="also time the 70B-shaped model's pass at M = 1, 16, 64, 512, 8192")
+    ap.add_argument("--copy-calib-mb", type=int, default=0,
+                    help="also run one device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the W4+EC layer is built and timed on a single "
+              "MI355X (multi-GPU runs are out of scope); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_11244_amd import spear as sp
+    from paper_2606_11244_amd import synth as S
+
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    print("bench: building the 70B-shaped model", file=sys.stderr, flush=True)
+    model = Model70B(sp, torch, dev, PRE_M)
+    ws_dec, ws_pre = model.workspace(DEC_M), model.workspace(PRE_M)
+    print("bench: capturing graphs", file=sys.stderr, flush=True)
+    g_dec = model.capture(DEC_M, True, ws_dec)
+    g_pre = model.capture(PRE_M, True, ws_pre)
+    dec_bytes, dec_flops, dec_launches = model.work(DEC_M)
+    pre_bytes, pre_flops, pre_launches = model.work(PRE_M)
+
+    def run_steps(n, gdec, gpre):
+        ev = []
+        for _ in range(n):
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            e0.record()
+            gdec.replay()
+            e1.record()
+            gpre.replay()
+            e2.record()
+            ev.append((e0, e1, e2))
+        torch.cuda.synchronize()
+        return (np.array([a.elapsed_time(b) for a, b, _ in ev]) * 1e-3,
+                np.array([b.elapsed_time(c) for _, b, c in ev]) * 1e-3)
+
+    print("bench: warmup", file=sys.stderr, flush=True)
+    run_steps(args.warmup, g_dec, g_pre)
+    print("bench: timed steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    t_dec, t_pre = run_steps(args.steps, g_dec, g_pre)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dec_s, pre_s = float(np.median(t_dec)), float(np.median(t_pre))
+    dec_gbs = dec_bytes / dec_s / 1e9
+    pre_tfl = pre_flops / pre_s / 1e12
+    print("bench: decode %.3f ms, prefill %.3f ms per pass" % (dec_s * 1e3, pre_s * 1e3),
+          file=sys.stderr, flush=True)
+
+    overhead = None
+    if not args.no_overhead:
+        print("bench: W4-only reference passes", file=sys.stderr, flush=True)
+        g_dec4 = model.capture(DEC_M, False, ws_dec)
+        g_pre4 = model.capture(PRE_M, False, ws_pre)
+        run_steps(args.warmup, g_dec4, g_pre4)
+        d4, p4 = run_steps(args.steps, g_dec4, g_pre4)
+        d4, p4 = float(np.median(d4)), float(np.median(p4))
+        b4 = model.work(DEC_M, with_ec=False)[0]
+        f4 = model.work(PRE_M, with_ec=False)[1]
+        overhead = {"decode": round(dec_s / d4 - 1.0, 4), "prefill": round(pre_s / p4 - 1.0, 4),
+                    "decode_w4_only_ms": round(d4 * 1e3, 4), "prefill_w4_only_ms": round(p4 * 1e3, 4),
+                    "decode_w4_only_GBps": round(b4 / d4 / 1e9, 1),
+                    "prefill_w4_only_TFLOPs": round(f4 / p4 / 1e12, 1),
+                    "decode_ec_byte_share": round(dec_bytes / b4 - 1.0, 4)}
+        del g_dec4, g_pre4
+
+    paper = None
+    if not args.no_paper_protocol:
+        print("bench: decode pass, 200 warm-up + 500 timed replays", file=sys.stderr, flush=True)
+        replay_times(torch, g_dec, 200)
+        tp = float(np.median(replay_times(torch, g_dec, 500)))
+        paper = {"protocol": "200 warm-up + 500 timed replays of the decode pass, median",
+                 "ms_per_pass": round(tp * 1e3, 4), "GBps": round(dec_bytes / tp / 1e9, 1),
+                 "hbm_frac": round(dec_bytes / tp / 1e9 / HBM_PEAK_GBS, 4)}
+
+    sweep = None
+    if args.model70b:
+        del g_pre
+        sweep = model_70b_sweep(model)
 
     if args.copy_calib_mb:
         # counter calibration: one elementwise kernel that reads and writes
@@ -581,9 +652,19 @@ def main():
         torch.cuda.synchronize()
         torch.neg(a, out=b)
         torch.cuda.synchronize()
+        del a, b
+
+    sel = model.sel
+    paths_dec, paths_pre = model.paths(DEC_M), model.paths(PRE_M)
+    del model, g_dec, ws_dec, ws_pre
+    torch.cuda.empty_cache()
+
+    extras = None
+    if not args.no_1b:
+        print("bench: 1B-shaped passes", file=sys.stderr, flush=True)
+        extras = llama1b_extras(args, sp, S, np, torch, dev)
 
     traffic = stored_traffic()
-    n_launch_dec = LAYERS_1B * len(DEC_GROUPS)
     result = {
         "metric": METRIC,
         "value": round(dec_gbs, 2),
@@ -596,52 +677,58 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f16",
-        "data": "synthetic",
+        "data": "synthetic (device-random 4-bit weights, EC factors and activations)",
         "config": {
-            "workload": ("llama-3.2-1b-shaped W4+EC linear layers (q,k,v,o 2048->2048/512, "
-                         "gate/up 2048->8192, down 8192->2048): decode M=1 over 16 layers x 7 "
-                         "modules + prefill M=4096 over 7 modules"),
-            "group_size": GROUP, "rank": RANK, "gate": "sigmoid_linear",
-            "decode_path": sp.PATH_NAMES[dec_plan.path],
-            "prefill_paths": {m: sp.PATH_NAMES[sp.dispatch_plan(d.problem()).path]
-                              for m, d in zip(S.MODULES, pre_dev)},
-            "decode_weight_copies": args.copies,
-            "decode_launches": ("per layer: q,k,v grouped (one launch), o, gate,up grouped "
-                                "(one launch), down: %d per pass" % n_launch_dec),
+            "workload": ("llama-2-70b-shaped W4+EC linear layers, the whole model resident: "
+                         "80 layers x (q,o 8192->8192; k,v 8192->1024; gate,up 8192->28672; "
+                         "down 28672->8192), group-128 int4, EC rank 64 with the sigmoid-linear "
+                         "gate on a seeded 25% of the modules (%d of %d), 4-bit only on the "
+                         "rest, fp16 activations; one step = decode pass M=1 + prefill pass "
+                         "M=4096, every module once on its AUTO path" % (int(sel.sum()), sel.size)),
+            "group_size": GROUP, "rank": 64, "gate": "sigmoid_linear",
+            "decode_M": DEC_M, "prefill_M": PRE_M,
+            "decode_paths": paths_dec, "prefill_paths": paths_pre,
+            "statistic": "median over the timed steps (per-pass HIP events)",
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": ("k_gemv_group / k_gemv (one-kernel W4+EC decode GEMV, %s), all "
-                       "launches of the decode pass" % sp.PATH_NAMES[dec_plan.path]),
-            "achieved": round(dec_bytes / n_launch_dec / (dec_s / n_launch_dec) / 1e9, 2),
+            "kernel": ("every launch of the decode pass: the 4-bit GEMV (k_gemv, EPI_NONE) on "
+                       "the modules without an EC, the producer-fused W4+EC GEMV (k_gemv, "
+                       "EPI_FUSED) on those with one, and on the 28672-deep down modules the EC "
+                       "pre-kernel k_ec + k_gemv (EPI_READY)"),
+            "achieved": round(dec_bytes / dec_launches / (dec_s / dec_launches) / 1e9, 2),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
             "traffic": (traffic or {}).get("decode_bytes_per_launch"),
-            "algo_bytes_per_launch": round(dec_bytes / n_launch_dec),
-            "avg_launch_us": round(dec_s / n_launch_dec * 1e6, 3),
+            "algo_bytes_per_launch": round(dec_bytes / dec_launches),
+            "launches_per_pass": dec_launches,
+            "avg_launch_us": round(dec_s / dec_launches * 1e6, 3),
         },
         "prefill": {
             "value": round(pre_tfl, 2), "unit": "TFLOP/s", "ms_per_pass": round(pre_s * 1e3, 4),
             "roofline": {
                 "bound": "mfma",
-                "kernel": ("the 7 modules on their AUTO paths: k_ec pre-kernel + k_gemm with "
-                           "the EC epilogue (unfused_2k), or the fully fused k_gemm (fused_mfma)"),
+                "kernel": ("every launch of the prefill pass: the 4-bit GEMM k_gemm (EPI_NONE) "
+                           "without an EC; k_ec + k_gemm with the EC epilogue (EPI_READY) with "
+                           "one"),
                 "achieved": round(pre_tfl, 2), "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(pre_tfl / MFMA_F16_PEAK_TFLOPS, 4),
                 "traffic": (traffic or {}).get("prefill_bytes_per_launch"),
+                "algo_flops_per_launch": round(pre_flops / pre_launches),
+                "launches_per_pass": pre_launches,
             },
         },
         "decode_ms_per_pass": round(dec_s * 1e3, 4),
-        "decode_one_call_per_module": ungrouped,
-        "decode_70b_layer": ctx70,
-        "model_70b": model70,
+        "decode_mean_ms_per_pass": round(float(np.mean(t_dec)) * 1e3, 4),
+        "prefill_mean_ms_per_pass": round(float(np.mean(t_pre)) * 1e3, 4),
+        "decode_paper_protocol": paper,
         "ec_overhead": overhead,
-        "ec_int8": int8,
-        "post_ec_tail": tail,
+        "model_70b_sweep": sweep,
+        "llama1b": extras,
     }
     if not args.no_cpu_baseline:
         print("bench: CPU oracle baseline", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(dec_base, pre_base[0])
+        result["cpu_baseline"] = cpu_baseline(sel)
     print(json.dumps(result), flush=True)
 
 

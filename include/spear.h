@@ -36,10 +36,15 @@
  *     means the default stream) and returns without synchronising.
  *   - Workspace: calls that need scratch take a caller-owned device buffer
  *     of at least spear_dispatch_plan()'s workspace_bytes. It must be
- *     zero-filled once before its first use; every call returns its
- *     counters to zero, so the same workspace serves any later call (of any
- *     shape it is large enough for) and replays of a captured graph. Two
- *     calls that overlap in time must not share one workspace.
+ *     zero-filled once before its first use. Its first 128 KiB hold counters:
+ *     the split-K and EC-slice counters return to zero at the end of every
+ *     call, and the fused path's launch-generation and ready counters advance
+ *     by a fixed step per launch (their wrap-around is harmless). The next
+ *     1 MiB holds the fused path's generation-tagged words and is written by
+ *     no other kind of call; every call's other scratch data follows it. So
+ *     the same workspace serves any later call (of any shape it is large
+ *     enough for) and replays of a captured graph. Two calls that overlap in
+ *     time must not share one workspace.
  */
 #ifndef SPEAR_H
 #define SPEAR_H
@@ -255,9 +260,9 @@ typedef struct {
 } spear_layer_call_t;
 
 /* Workspace bytes of a group. Every nonempty workspace layout starts with
- * the same counter block (the first 128 KiB); a group's workspace is that
- * block followed by each member's data region (its plan's bytes past the
- * block, rounded up to 256) in array order, so it is at least every
+ * the same counter block and tagged region (the first 1152 KiB); a group's
+ * workspace is those followed by each member's data region (its plan's bytes
+ * past them, rounded up to 256) in array order, so it is at least every
  * member's own size and, like a single call's, may be shared in stream order
  * with single calls and other groups. 0 when no member needs scratch.
  * Host-only. SPEAR_E_NULL for a NULL array, member problem or out pointer,
@@ -282,6 +287,17 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
  * read. */
 spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w,
                                 void* w_out, void* hip_stream);
+
+/* Workspace layout of a planned call, for tests of its invariants (host
+ * only): the fused path's tagged words occupy [*tag_begin, *tag_end) (both 0
+ * on every other path), a region at a fixed place past the counter block
+ * that no other kind of call writes; the call's other data regions lie in
+ * [*data_begin, *data_end) (both 0 when it has none), which starts past the
+ * tagged region for every call. Returns spear_dispatch_plan's status;
+ * SPEAR_E_NULL for a NULL pointer. */
+spear_status_t spear_workspace_regions(const spear_problem_t* prob, int32_t with_ec,
+                                       size_t* tag_begin, size_t* tag_end, size_t* data_begin,
+                                       size_t* data_end);
 
 /* Test hook for the fused path's bounded wait: the number of polls a
  * workgroup makes for the EC coordinates before computing them itself

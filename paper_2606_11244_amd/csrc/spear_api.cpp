@@ -52,6 +52,7 @@ struct Resolved {
   int xlds, xstride, bpre, lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz, lds_a;
   size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart, off_eupart, off_gpart,
       off_epart;
+  size_t tag_bytes;  // fused path: bytes of its tagged region at off_vtag
   int npub, direct;
   size_t lds_gemv, lds_prod, lds_gate;
 };
@@ -437,11 +438,14 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   }
 
   // workspace layout. The first kCounterBytes hold every counter of every
-  // kind of call at fixed offsets (the fused path's launch counter, EC-slice
-  // counters, row-group counters); each call leaves them as it found them,
-  // and data regions start after this block, so any mix of calls can share
-  // one zero-initialised workspace.
-  size_t off = kCounterBytes;
+  // kind of call at fixed offsets (the fused path's launch counters,
+  // EC-slice counters, row-group counters); the split-K and EC-slice
+  // counters return to zero after each call and the fused path's advance by
+  // a whole launch step. Then comes the fused path's tagged region (no other
+  // kind of call writes it), and every call's data regions start after it, so
+  // any mix of calls can share one zero-initialised workspace and a tagged
+  // word that is not this launch's carries an earlier launch's tag.
+  size_t off = kDataBase;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off = align_up(off + bytes, 256);
@@ -456,8 +460,11 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     const bool partials = z.ec_mode != EC_GATHER && z.P * z.PG > 1;
     if (partials && z.ntb > kMaxEcCounters) return SPEAR_E_SHAPE;
     if (fused) {
-      z.off_vtag = take((size_t)kVCopies * M * 8 *
-                        (z.ec_mode == EC_GATHER ? (size_t)z.P * z.R1 : (size_t)z.r));
+      const size_t tag_bytes = (size_t)kVCopies * M * 8 *
+                               (z.ec_mode == EC_GATHER ? (size_t)z.P * z.R1 : (size_t)z.r);
+      if (tag_bytes > kTagBytes) return SPEAR_E_SHAPE;
+      z.off_vtag = kCounterBytes;
+      z.tag_bytes = tag_bytes;
       z.npub = z.ec_mode == EC_GATHER ? z.ntb * z.P * z.PG : z.ntb;
       // small problems: the consumers poll the tagged data itself rather
       // than the ready counter, saving the publishers' completion wait
@@ -802,13 +809,13 @@ int group_epi(const Resolved& z, const spear_ec_t* ec) {
   return -1;
 }
 
-// Group workspace: the one counter block of every workspace, then each
-// member's data region (its plan's bytes past the counter block) in array
-// order. A member run on its own takes the workspace as it is (its data
-// regions start past the counter block); in the one-launch case member i's
-// data start after the earlier members' and its split-K counters follow
-// theirs in the counter block. Either way the counter block stays the first
-// kCounterBytes, so the workspace may be shared with single calls.
+// Group workspace: the counter block and the tagged region of every
+// workspace, then each member's data region (its plan's bytes past
+// kDataBase) in array order. A member run on its own takes the workspace as
+// it is (its data regions start at kDataBase); in the one-launch case member
+// i's data start after the earlier members' and its split-K counters follow
+// theirs in the counter block. Either way the counter block and the tagged
+// region keep their places, so the workspace may be shared with single calls.
 spear_status_t group_resolve(int32_t n, const spear_layer_call_t* calls, Resolved* z,
                              size_t* data_off, size_t* total) {
   if (!calls || !total) return SPEAR_E_NULL;
@@ -820,12 +827,12 @@ spear_status_t group_resolve(int32_t n, const spear_layer_call_t* calls, Resolve
     const spear_status_t st = resolve(calls[i].prob, calls[i].ec != nullptr, &z[i]);
     if (st != SPEAR_OK) return st;
     const size_t b = z[i].plan.workspace_bytes;
-    if (b > 0 && b < kCounterBytes) return SPEAR_E_SHAPE;  // every layout starts with the counters
+    if (b > 0 && b < kDataBase) return SPEAR_E_SHAPE;  // every layout starts with the counters
     any = any || b > 0;
     data_off[i] = sum;
-    sum += round256(b > 0 ? b - kCounterBytes : 0);
+    sum += round256(b > 0 ? b - kDataBase : 0);
   }
-  *total = any ? kCounterBytes + sum : 0;
+  *total = any ? kDataBase + sum : 0;
   return SPEAR_OK;
 }
 
@@ -1030,6 +1037,21 @@ spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w
   return hip_status(launch_dequant(prob->act_dtype, w->qweight, w->scales, w->zeros,
                                    (uint16_t*)w_out, (int)prob->N, (int)prob->K, G,
                                    (hipStream_t)hip_stream));
+}
+
+spear_status_t spear_workspace_regions(const spear_problem_t* prob, int32_t with_ec,
+                                       size_t* tag_begin, size_t* tag_end, size_t* data_begin,
+                                       size_t* data_end) {
+  if (!prob || !tag_begin || !tag_end || !data_begin || !data_end) return SPEAR_E_NULL;
+  Resolved z;
+  const spear_status_t st = resolve(prob, with_ec != 0, &z);
+  if (st != SPEAR_OK) return st;
+  *tag_begin = z.tag_bytes ? z.off_vtag : 0;
+  *tag_end = z.tag_bytes ? z.off_vtag + z.tag_bytes : 0;
+  const size_t ws = z.plan.workspace_bytes;
+  *data_begin = ws > kDataBase ? kDataBase : 0;
+  *data_end = ws > kDataBase ? ws : 0;
+  return SPEAR_OK;
 }
 
 int32_t spear_set_wait_polls(int32_t polls) { return g_wait_polls.exchange(polls < 0 ? 0 : polls); }

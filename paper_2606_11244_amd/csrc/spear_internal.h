@@ -38,8 +38,13 @@ constexpr int kLocalTiles = 2;   // EPI_LOCAL: B operands per iteration: A (r <=
 constexpr size_t kLocalALds = 81920;  // EPI_LOCAL: LDS for the staged K-slice of A, w_g
 
 // Workspace: a fixed counter block at the start, shared by every kind of call
-// (each call leaves its counters as it found them), then the call's data.
+// (the split-K and EC-slice counters return to zero after each call; the
+// fused path's generation and ready counters advance by 2^32 per launch),
+// then the region of the fused path's tagged words, which no other kind of
+// call writes, then the call's data.
 constexpr size_t kCounterBytes = 131072;
+constexpr size_t kTagBytes = (size_t)1 << 20;         // fused path: tagged words
+constexpr size_t kDataBase = kCounterBytes + kTagBytes;  // every call's data regions
 constexpr size_t kCtrGen = 0;          // fused path: kGenClasses 64-bit launch
 constexpr int kGenClasses = 64;        // counters, kGenStride apart
 constexpr size_t kGenStride = 256;
@@ -70,10 +75,12 @@ __host__ __device__ inline uint64_t gen_increment(int block, int grid) {
 __host__ __device__ inline uint64_t publisher_increment(int pub, int npub) {
   return pub == 0 ? (1ull << 32) - (uint64_t)(npub - 1) : 1ull;
 }
-// Tag of data published by the fused launch of generation g: a
-// multiplicative hash, so that leftover data of another call is never
-// mistaken for current data (2^-32 chance per word).
-__host__ __device__ inline uint32_t ec_tag(uint32_t gen) { return ((gen + 1u) * 0x9E3779B1u) | 1u; }
+// Tag of data published by the fused launch of generation g. The tagged
+// words live in a workspace region that only fused launches write, so a word
+// there is zero (never written) or was written by a fused launch of some
+// generation g' <= g; its tag equals this launch's only if g' == g modulo
+// 2^32 (g + 1 is never 0 before 2^32 - 1 launches have passed).
+__host__ __device__ inline uint32_t ec_tag(uint32_t gen) { return gen + 1u; }
 
 // EC projection / gate work. A producer workgroup owns one token tile (16
 // tokens), one K-slice (ips iterations of 128) and one group of row tiles

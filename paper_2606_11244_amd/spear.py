@@ -33,7 +33,7 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
             "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
             "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
-            "spear_set_gemm_tile",
+            "spear_set_gemm_tile", "spear_workspace_regions",
             "spear_status_string", "spear_version", "spear_sched_latency", "spear_sched_chunk")
 
 
@@ -121,6 +121,7 @@ def _load():
     lib.spear_w4ec_linear_group.argtypes = [ctypes.c_int32, P(LayerCall), ctypes.c_void_p,
                                             ctypes.c_size_t, ctypes.c_void_p]
     lib.spear_set_wait_polls.argtypes = [ctypes.c_int32]
+    lib.spear_workspace_regions.argtypes = [P(Problem), ctypes.c_int32] + [P(ctypes.c_size_t)] * 4
     lib.spear_set_gemv_shape.argtypes = [ctypes.c_int32] * 3
     lib.spear_set_gemv_shape.restype = None
     lib.spear_set_gemm_slices.argtypes = [ctypes.c_int32]
@@ -137,7 +138,7 @@ def _load():
     lib.spear_version.restype = ctypes.c_char_p
     for f in ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
               "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
-              "spear_set_wait_polls"):
+              "spear_set_wait_polls", "spear_workspace_regions"):
         getattr(lib, f).restype = ctypes.c_int32
     return lib
 
@@ -175,6 +176,17 @@ def dispatch_plan(prob: Problem, with_ec: bool = True) -> Plan:
     if st != 0:
         raise SpearError(st, "spear_dispatch_plan")
     return out
+
+
+def workspace_regions(prob: Problem, with_ec: bool = True):
+    """((tag_begin, tag_end), (data_begin, data_end)) of a planned call's
+    workspace (the fused path's tagged words; every other scratch region)."""
+    v = [ctypes.c_size_t(0) for _ in range(4)]
+    st = LIB.spear_workspace_regions(ctypes.byref(prob), 1 if with_ec else 0,
+                                     *[ctypes.byref(a) for a in v])
+    if st != 0:
+        raise SpearError(st, "spear_workspace_regions")
+    return (v[0].value, v[1].value), (v[2].value, v[3].value)
 
 
 def allocate_workspace(prob: Problem, with_ec: bool = True, device="cuda") -> torch.Tensor:

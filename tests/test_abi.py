@@ -305,3 +305,44 @@ def test_prefill_tile_rule():
     assert tm(256, 8192, 8192) == 256          # 70B q: 64M weights
     assert tm(256, 2048, 8192, rank=16) == 128  # 1B down: 16M weights
     assert tm(4096, 2048, 2048, rank=32) == 256
+
+
+COUNTERS = 131072            # the counter block every workspace starts with
+TAG_END = COUNTERS + (1 << 20)  # the fused path's tagged region ends here
+
+
+def test_tagged_region_is_written_by_the_fused_path_only():
+    """Every plan (every path, dtype, gate, rank, token count the fused GEMV
+    takes, with and without the EC) keeps its scratch data past the tagged
+    region; only the fused GEMV has a tagged region, at the fixed place right
+    after the counter block. So a tagged word a consumer reads was written by
+    a fused launch (or is still zero) and a stale one carries an older tag."""
+    shapes = [(256, 256, 0), (2048, 2048, 128), (512, 2048, 128), (8192, 2048, 128),
+              (2048, 8192, 128), (4096, 14336, 0), (8192, 28672, 128), (28672, 8192, 128),
+              (1024, 8192, 128)]
+    n_fused = 0
+    for (N, K, G) in shapes:
+        for M in (1, 2, 4, 8, 16, 17, 32, 33, 64, 65, 128, 512, 4096):
+            for r in (0, 8, 16, 32, 64, 256):
+                for gate in (sp.GATE_ONE, sp.GATE_SIGMOID_LINEAR, sp.GATE_TANH_MLP):
+                    for path in range(6):
+                        for with_ec in (True, False):
+                            pr = sp.problem(M, N, K, G, sp.F16, r, gate, force_path=path)
+                            try:
+                                plan = sp.dispatch_plan(pr, with_ec)
+                            except sp.SpearError:
+                                continue
+                            (tb, te), (db, de) = sp.workspace_regions(pr, with_ec)
+                            fused = with_ec and r > 0 and plan.path == sp.PATH_FUSED_GEMV
+                            if fused:
+                                n_fused += 1
+                                assert tb == COUNTERS and COUNTERS < te <= TAG_END
+                            else:
+                                assert (tb, te) == (0, 0)
+                            ws = plan.workspace_bytes
+                            assert ws >= TAG_END
+                            if ws > TAG_END:
+                                assert (db, de) == (TAG_END, ws)
+                            else:
+                                assert (db, de) == (0, 0)
+    assert n_fused > 100

@@ -239,6 +239,51 @@ def test_deterministic_and_workspace_reuse(path):
     assert_parity(first, O.w4ec_linear(L), f"determinism {path}")
 
 
+@pytest.mark.parametrize("M", [1, 4])
+def test_workspace_shared_by_every_path(M):
+    """The fused path's tagged words live in a region no other call writes.
+    Between fused calls every other kind of call (the naive chain, the
+    semi-fused pair on the GEMV and on the GEMM, the local and fully fused
+    variants, the 4-bit product alone on both kernels, split over K) writes
+    its partial sums into the same workspace, and then every data region past
+    the tagged one is filled with words that carry the next fused launch's
+    own tag (the workspace's launch counter tells which): the fused call must
+    still return exactly what it returned on a fresh workspace."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=M, N=1024, K=4096, group_size=128, rank=32, seed=11 + M)
+    dec = S.make_layer(M=3, N=1024, K=16384, group_size=128, rank=16, seed=12)
+    pre = S.make_layer(M=96, N=256, K=4096, group_size=128, rank=16, seed=13)
+    dl, dd, dp = sp.DeviceLayer(L), sp.DeviceLayer(dec), sp.DeviceLayer(pre)
+    fused = dl.problem(force_path=PATHS["fused_gemv"])
+    others = [(dd, PATHS[p], True) for p in ("chain", "2k", "fused_local", "fused_gemv")]
+    others += [(dp, PATHS[p], True) for p in ("chain", "2k", "fused_mfma")]
+    others += [(dd, 0, False), (dp, 0, False)]
+    size = max([sp.dispatch_plan(fused).workspace_bytes] +
+               [sp.dispatch_plan(d.problem(force_path=p), e).workspace_bytes for d, p, e in others])
+    assert sp.dispatch_plan(dd.problem(), False).split_k > 1
+    assert sp.dispatch_plan(dp.problem(), False).split_k > 1
+    data_base = 131072 + (1 << 20)
+    ws = torch.zeros(size, dtype=torch.uint8, device="cuda")
+    first = gpu_y(L, PATHS["fused_gemv"], workspace=ws, dev=dl)
+    fresh = gpu_y(L, PATHS["fused_gemv"], workspace=torch.zeros_like(ws), dev=dl)
+    assert np.array_equal(first, fresh)
+    for i in range(3):
+        for d, p, e in others:
+            log(f"shared workspace M={M} round={i} path={p} ec={e} M'={d.layer.M}")
+            gpu_y(d.layer, p, with_ec=e, workspace=ws, dev=d)
+        torch.cuda.synchronize()
+        gen = int(ws[:8].view(torch.int64).item()) >> 32  # class 0: launches so far
+        tag = (gen + 1) & 0xFFFFFFFF
+        word = (tag << 32) | 0x3F800000  # fp32 1.0 under the next launch's tag
+        if word >= 1 << 63:
+            word -= 1 << 64
+        n64 = (size - data_base) // 8
+        ws[data_base:data_base + 8 * n64].view(torch.int64).fill_(word)
+        again = gpu_y(L, PATHS["fused_gemv"], workspace=ws, dev=dl)
+        assert np.array_equal(first, again), i
+    assert_parity(first, O.w4ec_linear(L), f"shared workspace M={M}")
+
+
 def test_streams_and_reuse():
     """Calls on a side stream, back to back with different shapes on one
     workspace sized for the largest."""

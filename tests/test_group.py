@@ -47,7 +47,7 @@ def _qkv(M=1):
             sp.problem(M, 512, 2048, 128, sp.F16, 16)]
 
 
-COUNTER_BLOCK = 131072  # the counter block at the start of every workspace
+COUNTER_BLOCK = 131072 + (1 << 20)  # the counter block and the tagged region of every workspace
 
 
 def _want(sizes):
