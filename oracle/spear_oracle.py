@@ -11,7 +11,7 @@ sections 2.1 and 5.1):
 
     Y = X . What^T  +  alpha * ( gate(X) (.) (X . A^T) ) . B^T
 
-where What is the dequantised 4-bit weight matrix, A [r][K] and B [N][r] are
+where What is the dequantised 4-bit (or 3-bit) weight matrix, A [r][K] and B [N][r] are
 the EC's low-rank factors and gate() is one of
   * ONE             gamma == 1: the static low-rank compensator (Eq. 2 with
                     W_comp = alpha B A),
@@ -75,14 +75,55 @@ def unpack_int4(qweight) -> np.ndarray:
     return q.reshape(n, kw * 8)
 
 
-def dequant(qweight, scales_bits, zeros, group_size: int) -> np.ndarray:
+def unpack_int3(qweight) -> np.ndarray:
+    """3-bit codes: packed words [N][3K/32] -> codes q[N][K] (int64, 0..7).
+
+    The paper's 3-bit backbone (Appendix D.1, D.3) does not fix a storage
+    layout; this one keeps two-bit fields of neighbouring codes in the two
+    16-bit halves of a word. Codes c_t = q[n][32j + t], t = 0..31, of block j
+    of row n sit in words 3j, 3j+1, 3j+2 of the row:
+      word 3j    bits 2i, 2i+1       : low two bits of c_{2i}       (i = 0..7)
+                 bits 16+2i, 17+2i   : low two bits of c_{2i+1}
+      word 3j+1  the same for c_{16+2i} and c_{17+2i}
+      word 3j+2  bit i               : high bit of c_{2i}          (i = 0..15)
+                 bit 16+i            : high bit of c_{2i+1}
+    """
+    w = np.asarray(qweight, dtype=np.uint32)
+    n, nw = w.shape
+    if nw % 3:
+        raise ValueError("3-bit rows hold a multiple of three words")
+    blk = w.reshape(n, nw // 3, 3)
+    lo0, lo1, hi = blk[:, :, 0], blk[:, :, 1], blk[:, :, 2]
+    q = np.zeros((n, nw // 3, 32), dtype=np.int64)
+    for i in range(8):
+        q[:, :, 2 * i] = (lo0 >> np.uint32(2 * i)) & np.uint32(3)
+        q[:, :, 2 * i + 1] = (lo0 >> np.uint32(16 + 2 * i)) & np.uint32(3)
+        q[:, :, 16 + 2 * i] = (lo1 >> np.uint32(2 * i)) & np.uint32(3)
+        q[:, :, 17 + 2 * i] = (lo1 >> np.uint32(16 + 2 * i)) & np.uint32(3)
+    for i in range(16):
+        q[:, :, 2 * i] |= (((hi >> np.uint32(i)) & np.uint32(1)) << np.uint32(2)).astype(np.int64)
+        q[:, :, 2 * i + 1] |= (((hi >> np.uint32(16 + i)) & np.uint32(1)) << np.uint32(2)).astype(np.int64)
+    return q.reshape(n, (nw // 3) * 32)
+
+
+def unpack_codes(qweight, bits: int = 4) -> np.ndarray:
+    """Codes of a packed weight matrix: 4-bit (unpack_int4) or 3-bit (unpack_int3)."""
+    if bits in (0, 4):
+        return unpack_int4(qweight)
+    if bits == 3:
+        return unpack_int3(qweight)
+    raise ValueError("weights are 4- or 3-bit")
+
+
+def dequant(qweight, scales_bits, zeros, group_size: int, bits: int = 4) -> np.ndarray:
     """What[n][k] = (q[n][k] - z[n][k // G]) * s[n][k // G], exact in float64.
 
     (q - z) is an integer of magnitude <= 15 and s an fp16 value, so the
     product has at most 15 significant bits and is exact (sections 2.1, 5.1:
-    asymmetric round-to-nearest per channel or per group of 128).
+    asymmetric round-to-nearest per channel or per group of 128; with 3-bit
+    codes, Appendix D.1 and D.3, |q - z| <= 7).
     """
-    q = unpack_int4(qweight)
+    q = unpack_codes(qweight, bits)
     n, k = q.shape
     g = k if group_size in (0, k) else group_size
     s = bits_to_f64(scales_bits, F16)
@@ -116,10 +157,11 @@ def round_f64_to_bits(v, dtype: int) -> np.ndarray:
     raise ValueError("unknown dtype")
 
 
-def dequant_bits(qweight, scales_bits, zeros, group_size: int, dtype: int) -> np.ndarray:
+def dequant_bits(qweight, scales_bits, zeros, group_size: int, dtype: int,
+                 bits: int = 4) -> np.ndarray:
     """The bit-exact dequantisation contract: What rounded once (nearest even)
     to the activation dtype, as uint16 bit patterns [N][K]."""
-    return round_f64_to_bits(dequant(qweight, scales_bits, zeros, group_size), dtype)
+    return round_f64_to_bits(dequant(qweight, scales_bits, zeros, group_size, bits), dtype)
 
 
 # ---------------------------------------------------------------------------
@@ -210,11 +252,16 @@ def ec_factors(layer, rows=None):
     return bits_to_f64(layer.A, dt), bits_to_f64(B, dt)
 
 
+def weight_bits(layer) -> int:
+    """Code width of a stored layer's weights (4 unless it says 3)."""
+    return int(getattr(layer, "weight_bits", 4) or 4)
+
+
 def w4ec_linear(layer) -> np.ndarray:
     """Eq. 3 on a stored layer (any object with the generator's fields):
     decodes every stored tensor exactly, then evaluates in float64."""
     dt = layer.act_dtype
-    W_hat = dequant(layer.qweight, layer.scales, layer.zeros, layer.group_size)
+    W_hat = dequant(layer.qweight, layer.scales, layer.zeros, layer.group_size, weight_bits(layer))
     x = bits_to_f64(layer.x, dt)
     if layer.rank == 0:
         return w4_linear(x, W_hat)
@@ -241,7 +288,7 @@ def post_ec_tail(y, residual, norm_w, eps: float):
 
 def w4_linear_layer(layer) -> np.ndarray:
     """The plain 4-bit product X . W_hat^T of a stored layer (EC ignored)."""
-    W_hat = dequant(layer.qweight, layer.scales, layer.zeros, layer.group_size)
+    W_hat = dequant(layer.qweight, layer.scales, layer.zeros, layer.group_size, weight_bits(layer))
     return w4_linear(bits_to_f64(layer.x, layer.act_dtype), W_hat)
 
 
@@ -251,7 +298,7 @@ def w4ec_linear_rows(layer, rows) -> np.ndarray:
     rows = np.asarray(rows)
     dt = layer.act_dtype
     W_hat = dequant(layer.qweight[rows], layer.scales[rows], layer.zeros[rows],
-                    layer.group_size)
+                    layer.group_size, weight_bits(layer))
     x = bits_to_f64(layer.x, dt)
     if layer.rank == 0:
         return w4_linear(x, W_hat)

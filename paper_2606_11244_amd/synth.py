@@ -7,12 +7,13 @@ the CPU oracle's callers, and it holds none of the layer's own arithmetic: no
 dequantisation, no contraction, no EC projection and no gate. What it does
 compute is the offline side that precedes the layer:
 
-* round-to-nearest (RTN) asymmetric 4-bit quantisation of a float weight
+* round-to-nearest (RTN) asymmetric 4-bit (or 3-bit) quantisation of a float weight
   matrix, per output channel or per group of input channels (the plain
   linear quantiser the paper compensates: the quantised model of section 2.1,
   evaluated per channel and per group of 128 in section 5.1), and
 * packing of the 4-bit codes, eight to a 32-bit word, in the layout the C ABI
-  documents: word j of row n holds code q[n][8j+i] in bits 4i..4i+3.
+  documents: word j of row n holds code q[n][8j+i] in bits 4i..4i+3; and of
+  3-bit codes, 32 to three words (pack_int3).
 
 Floating-point values are returned as numpy arrays of IEEE bit patterns
 (uint16) in the activation dtype, so that both the GPU path and the oracle see
@@ -69,19 +70,53 @@ def pack_int4(q: np.ndarray) -> np.ndarray:
     return b.view("<u4").astype(np.uint32, copy=False).reshape(n, k // 8)
 
 
-def rtn_quantize(w: np.ndarray, group_size: int):
-    """Asymmetric min-max round-to-nearest 4-bit quantisation of w[N][K].
+def pack_int3(q: np.ndarray) -> np.ndarray:
+    """Pack 3-bit codes q[N][K] (values 0..7, K % 32 == 0) into uint32 words
+    [N][3K/32]: codes c_t = q[n][32j + t] of block j go to words 3j, 3j+1,
+    3j+2 of row n. Word 3j holds the low two bits of c_{2i} in bits 2i..2i+1
+    and of c_{2i+1} in bits 16+2i..17+2i (i = 0..7); word 3j+1 the same for
+    c_{16+2i}, c_{17+2i}; word 3j+2 holds the high bit of c_{2i} in bit i and
+    of c_{2i+1} in bit 16+i (i = 0..15)."""
+    q = np.asarray(q)
+    n, k = q.shape
+    if k % 32:
+        raise ValueError("K must be a multiple of 32 to pack 3-bit codes")
+    if q.size and (q.min() < 0 or q.max() > 7):
+        raise ValueError("codes must lie in 0..7")
+    c = q.astype(np.uint32).reshape(n, k // 32, 32)
+    even, odd = c[:, :, 0::2], c[:, :, 1::2]  # c_{2i}, c_{2i+1}, i = 0..15
+    words = np.zeros((n, k // 32, 3), dtype=np.uint32)
+    for i in range(16):
+        wi, sh = (0, 2 * i) if i < 8 else (1, 2 * (i - 8))
+        words[:, :, wi] |= (even[:, :, i] & 3) << np.uint32(sh)
+        words[:, :, wi] |= (odd[:, :, i] & 3) << np.uint32(16 + sh)
+        words[:, :, 2] |= (even[:, :, i] >> 2) << np.uint32(i)
+        words[:, :, 2] |= (odd[:, :, i] >> 2) << np.uint32(16 + i)
+    return words.reshape(n, 3 * k // 32)
+
+
+def pack_codes(q: np.ndarray, bits: int = 4) -> np.ndarray:
+    """pack_int4 or pack_int3 by code width."""
+    return pack_int3(q) if bits == 3 else pack_int4(q)
+
+
+def rtn_quantize(w: np.ndarray, group_size: int, bits: int = 4):
+    """Asymmetric min-max round-to-nearest quantisation of w[N][K] to b-bit
+    codes (b = 4, or 3 for the paper's 3-bit backbone), L = 2^b - 1.
 
     For each output row n and each group of `group_size` consecutive input
     columns (group_size == K means one group per row, "per channel"):
       lo, hi = min, max of the group
-      s = fp16((hi - lo) / 15)            (the stored scale)
-      z = clip(rne(-lo / s), 0, 15)       (the stored zero point)
-      q = clip(rne(w / s) + z, 0, 15)     (codes, chosen against the fp16 s)
+      s = fp16((hi - lo) / L)             (the stored scale)
+      z = clip(rne(-lo / s), 0, L)        (the stored zero point)
+      q = clip(rne(w / s) + z, 0, L)      (codes, chosen against the fp16 s)
     A constant group (hi == lo) or a scale that rounds to zero uses s = 1 and
-    z = clip(rne(-lo), 0, 15).
+    z = clip(rne(-lo), 0, L).
     Returns (codes uint8 [N][K], scales fp16 bits [N][K/G], zeros uint8 [N][K/G]).
     """
+    if bits not in (3, 4):
+        raise ValueError("3- or 4-bit codes")
+    top = float((1 << bits) - 1)
     w = np.asarray(w, dtype=np.float32)
     n, k = w.shape
     g = k if group_size in (0, k) else group_size
@@ -96,15 +131,15 @@ def rtn_quantize(w: np.ndarray, group_size: int):
         wg = w[r0:r1].reshape(r1 - r0, k // g, g)
         lo = wg.min(axis=2).astype(np.float64)
         hi = wg.max(axis=2).astype(np.float64)
-        s = ((hi - lo) / 15.0).astype(np.float16).astype(np.float64)
+        s = ((hi - lo) / top).astype(np.float16).astype(np.float64)
         degenerate = (hi == lo) | (s == 0)
         s = np.where(degenerate, 1.0, s)
-        z = np.clip(np.rint(-lo / s), 0, 15)
+        z = np.clip(np.rint(-lo / s), 0, top)
         # w / s in float32: s is an fp16 value (exact in float32); the quotient's
         # rounding can only matter within 2^-24 of a rounding tie
         qf = np.rint(wg / s.astype(np.float32)[:, :, None])
         qf += z.astype(np.float32)[:, :, None]
-        np.clip(qf, 0, 15, out=qf)
+        np.clip(qf, 0, top, out=qf)
         q_out[r0:r1] = qf.reshape(r1 - r0, k).astype(np.uint8)
         s_out[r0:r1] = s.astype(np.float16).view(np.uint16)
         z_out[r0:r1] = z.astype(np.uint8)
@@ -124,7 +159,7 @@ class Layer:
     act_dtype: int           # F16 or BF16
     rank: int
     gate_kind: int
-    qweight: np.ndarray      # uint32 [N][K/8]
+    qweight: np.ndarray      # uint32 [N][K/8] (4-bit) or [N][3K/32] (3-bit)
     scales: np.ndarray       # fp16 bits [N][K/G]
     zeros: np.ndarray        # uint8 [N][K/G]
     x: np.ndarray            # [M][K]
@@ -143,6 +178,7 @@ class Layer:
     a_scale: np.ndarray = None  # fp32 [r]
     B_q: np.ndarray = None   # int8 [N][r]
     b_scale: np.ndarray = None  # fp32 [N]
+    weight_bits: int = 4     # code width of qweight: 4, or 3 (zeros then 0..7)
 
     @property
     def gate_hidden(self) -> int:
@@ -168,7 +204,7 @@ def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
                w_std: float = 0.02, x_std: float = 1.0, ec_std: float = 0.01,
                wg_std: float = 0.05, b_g: float = 0.0, alpha: float = 1.0,
                outlier_frac: float = 0.0, outlier_scale: float = 20.0,
-               gate_hidden: int = 0, ab_int8: bool = False) -> Layer:
+               gate_hidden: int = 0, ab_int8: bool = False, weight_bits: int = 4) -> Layer:
     """Draw one layer from the seed tree SeedSequence([seed, config_id, module_id]).
 
     Draw order: W (fp32) -> RTN -> X (with outlier channels) -> A, B -> w_g ->
@@ -180,7 +216,7 @@ def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
     rng = np.random.default_rng(np.random.SeedSequence([seed, config_id, module_id]))
     w = rng.standard_normal((N, K), dtype=np.float32)
     w *= np.float32(w_std)
-    q, s, z = rtn_quantize(w, g)
+    q, s, z = rtn_quantize(w, g, weight_bits)
     del w
     x = rng.standard_normal((M, K), dtype=np.float32)
     x *= np.float32(x_std)
@@ -202,12 +238,13 @@ def make_layer(*, M: int, N: int, K: int, group_size: int, rank: int,
         B_q, b_scale = quantize_int8_rows(B)
         i8 = dict(ab_int8=True, A_q=A_q, a_scale=a_scale, B_q=B_q, b_scale=b_scale)
     return Layer(M=M, N=N, K=K, group_size=g, act_dtype=act_dtype, rank=rank,
-                 gate_kind=gate_kind, qweight=pack_int4(q), scales=s, zeros=z,
+                 gate_kind=gate_kind, qweight=pack_codes(q, weight_bits), scales=s, zeros=z,
                  x=to_bits(x, act_dtype), A=to_bits(A, act_dtype),
                  B=to_bits(B, act_dtype), w_g=to_bits(w_g, act_dtype),
                  b_g=float(b_g), alpha=float(alpha),
                  W1=to_bits(W1, act_dtype), b1=to_bits(b1, act_dtype),
-                 W2=to_bits(W2, act_dtype), b2=to_bits(b2, act_dtype), **i8)
+                 W2=to_bits(W2, act_dtype), b2=to_bits(b2, act_dtype),
+                 weight_bits=weight_bits, **i8)
 
 
 def make_tail(layer: Layer, seed: int = 0, eps: float = 1e-5):
@@ -259,9 +296,10 @@ CONFIGS = {
 
 def config_layer(config_id: int, module: str, M: int, seed: int = 0,
                  gate_kind: int = GATE_SIGMOID_LINEAR, rank: int | None = None,
-                 ab_int8: bool = False) -> Layer:
+                 ab_int8: bool = False, weight_bits: int = 4) -> Layer:
     """One module of a workload configuration at token count M (ab_int8:
-    with INT8 per-channel copies of the EC factors)."""
+    with INT8 per-channel copies of the EC factors; weight_bits 3: the same
+    draws quantised to 3-bit codes)."""
     c = CONFIGS[config_id]
     K, N = c["shapes"][module]
     mod_id = list(c["shapes"]).index(module)
@@ -269,7 +307,8 @@ def config_layer(config_id: int, module: str, M: int, seed: int = 0,
                       rank=c["rank"] if rank is None else rank,
                       act_dtype=c["act_dtype"], gate_kind=gate_kind, seed=seed,
                       config_id=config_id, module_id=mod_id,
-                      outlier_frac=c["outlier_frac"], ab_int8=ab_int8)
+                      outlier_frac=c["outlier_frac"], ab_int8=ab_int8,
+                      weight_bits=weight_bits)
 
 
 def ec_selection_70b(seed: int = 0, layers: int = 80, fraction: float = 0.25) -> np.ndarray:

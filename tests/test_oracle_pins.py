@@ -157,6 +157,22 @@ def check_rtn_error_bound(o, seed=0) -> bool:
     return True
 
 
+def _code(layer, n, k):
+    """One weight code read from the packed words by the documented layouts,
+    scalar by scalar (4-bit: nibble k % 8 of word k // 8; 3-bit: block k // 32,
+    position t = 2i + o, low two bits from word 0 (i < 8) or word 1 at bit
+    2 (i % 8) + 16 o, high bit from word 2 at bit i + 16 o)."""
+    row = layer.qweight[n]
+    if getattr(layer, "weight_bits", 4) != 3:
+        return (int(row[k // 8]) >> (4 * (k % 8))) & 15
+    j, t = divmod(k, 32)
+    i, o = divmod(t, 2)
+    lo_word = int(row[3 * j + (0 if i < 8 else 1)])
+    lo = (lo_word >> (2 * (i % 8) + 16 * o)) & 3
+    hi = (int(row[3 * j + 2]) >> (i + 16 * o)) & 1
+    return lo | (hi << 2)
+
+
 def _brute(layer):
     """Scalar exact-rational evaluation of Eq. 3 (gate ONE or SIGMOID with the
     sigmoid taken in float64)."""
@@ -181,8 +197,7 @@ def _brute(layer):
         for n in range(N):
             acc = Fraction(0)
             for k in range(K):
-                word = int(layer.qweight[n][k // 8])
-                code = (word >> (4 * (k % 8))) & 15
+                code = _code(layer, n, k)
                 zz = int(layer.zeros[n][k // G])
                 ss = Fraction(float(sc[n][k // G]))
                 acc += Fraction(code - zz) * ss * Fraction(float(xs[m][k]))
@@ -477,6 +492,108 @@ def check_tail_properties(o, seed=0) -> bool:
             and np.allclose(h2, y + r, rtol=0, atol=1e-15))
 
 
+def check_unpack3_fixed_words(o) -> bool:
+    """3-bit layout pin: hand-decoded blocks of three words."""
+    cases = [((0xFFFFFFFF, 0, 0), [3] * 16 + [0] * 16),
+             ((0, 0, 0x0000FFFF), [4, 0] * 16),
+             ((0, 0, 0xFFFF0000), [0, 4] * 16),
+             ((0x00010000, 0, 0x00010000), [0, 5] + [0] * 30),
+             ((0, 0xC0000000, 0x80000000), [0] * 31 + [7]),
+             ((0x0000000C, 0, 0x00000002), [0, 0, 7] + [0] * 29),
+             ((0, 0x00000003, 0x00000100), [0] * 16 + [7] + [0] * 15)]
+    for words, want in cases:
+        w = np.array([list(words) * 2], dtype=np.uint32)  # two blocks, same contents
+        if o.unpack_int3(w).tolist() != [want * 2]:
+            return False
+    return True
+
+
+def check_unpack3_exhaustive(o) -> bool:
+    """Every 3-bit code at every one of the 32 positions of a block (second
+    block of a row) decodes to itself, through the generator's packer, and
+    leaves the other positions zero; the scalar reading of the layout agrees."""
+    for v in range(8):
+        for t in range(32):
+            q = np.zeros((1, 64), dtype=np.int64)
+            q[0, 32 + t] = v
+            w = S.pack_int3(q)
+            if not np.array_equal(o.unpack_int3(w), q):
+                return False
+            lay = types.SimpleNamespace(qweight=w, weight_bits=3)
+            if _code(lay, 0, 32 + t) != v:
+                return False
+    return True
+
+
+def check_rtn3_grid_roundtrip(o, seed=0) -> bool:
+    """3-bit weights built on the grid (codes 0 and 7 in every group, dyadic
+    fp16 scales) come back exactly through the 3-bit RTN and dequant."""
+    rng = np.random.default_rng(seed)
+    N, K = 24, 256
+    for G in (K, 128, 64):
+        s = 2.0 ** rng.integers(-9, -3, size=(N, K // G))
+        z = rng.integers(0, 8, size=(N, K // G))
+        q = rng.integers(0, 8, size=(N, K))
+        qg = q.reshape(N, K // G, G)
+        qg[:, :, 0] = 0
+        qg[:, :, 1] = 7
+        q = qg.reshape(N, K)
+        grp = np.arange(K) // G
+        w = ((q - z[:, grp]) * s[:, grp]).astype(np.float32)
+        q2, s2, z2 = S.rtn_quantize(w, G, bits=3)
+        if q2.max() > 7 or z2.max() > 7:
+            return False
+        W_hat = o.dequant(S.pack_int3(q2), s2, z2, G, bits=3)
+        if not np.array_equal(W_hat, w.astype(np.float64)):
+            return False
+    return True
+
+
+def check_brute_force_w3(o, seed=0) -> bool:
+    """Eq. 3 on 3-bit layers against exact rationals (codes read scalar by
+    scalar from the documented layout), both dtypes, every output."""
+    cases = [dict(M=2, N=5, K=64, group_size=32, rank=3, gate_kind=S.GATE_ONE, alpha=0.75),
+             dict(M=3, N=4, K=96, group_size=96, rank=2, gate_kind=S.GATE_SIGMOID_LINEAR, alpha=1.0),
+             dict(M=1, N=6, K=32, group_size=32, rank=0, gate_kind=S.GATE_ONE, alpha=1.0)]
+    for i, c in enumerate(cases):
+        for dt in (S.F16, S.BF16):
+            layer = S.make_layer(seed=seed + 80 + i, act_dtype=dt, ec_std=0.3, wg_std=0.4,
+                                 b_g=0.1, weight_bits=3, **c)
+            want = _brute(layer)
+            got = o.w4ec_linear(layer)
+            rows = np.array([layer.N - 1, 0])
+            got_rows = o.w4ec_linear_rows(layer, rows)
+            for m in range(layer.M):
+                for n in range(layer.N):
+                    wv = float(want[m][n])
+                    if abs(got[m][n] - wv) > 1e-12 * max(1.0, abs(wv)):
+                        return False
+                for i2, n in enumerate(rows):
+                    wv = float(want[m][n])
+                    if abs(got_rows[m][i2] - wv) > 1e-12 * max(1.0, abs(wv)):
+                        return False
+    return True
+
+
+def check_dequant3_bits_contract(o, seed=0) -> bool:
+    """3-bit bit-exact dequantisation: one nearest-even rounding of the exact
+    product, cross-checked against torch's float32 -> fp16/bf16 cast over every
+    code and zero point."""
+    import torch
+    rng = np.random.default_rng(seed)
+    N, K = 8 * 8, 128
+    z = np.repeat(np.arange(8), 8).reshape(N, 1)
+    q = np.tile(np.arange(8), (N, K // 8))
+    s = rng.uniform(1e-4, 4.0, size=(N, 1)).astype(np.float16)
+    exact = ((q - z) * s.astype(np.float64)).astype(np.float32)
+    for dt, tdt in ((O.F16, torch.float16), (O.BF16, torch.bfloat16)):
+        want = torch.from_numpy(exact).to(tdt).view(torch.int16).numpy().view(np.uint16)
+        got = o.dequant_bits(S.pack_int3(q), s.view(np.uint16), z.astype(np.uint8), K, dt, bits=3)
+        if not np.array_equal(got, want):
+            return False
+    return True
+
+
 def check_tolerance_cases(o) -> bool:
     """The parity bar on hand-worked cases (relative Frobenius error
     ||y - y_ref|| / ||y_ref|| and max |y - y_ref| against a fraction of
@@ -582,7 +699,9 @@ PINS = [check_unpack_fixed_words, check_unpack_exhaustive, check_golden_examples
         check_sigmoid_half, check_tanh_static_lora, check_factored_form,
         check_gate_ranges, check_dequant_bits_contract, check_int8_brute_force,
         check_int8_golden, check_tail_golden, check_tail_properties,
-        check_tolerance_cases, check_rows_brute_force, check_rows_tanh_factored]
+        check_tolerance_cases, check_rows_brute_force, check_rows_tanh_factored,
+        check_unpack3_fixed_words, check_unpack3_exhaustive, check_rtn3_grid_roundtrip,
+        check_brute_force_w3, check_dequant3_bits_contract]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -760,6 +879,29 @@ def _rows_gate_dropped(layer, rows):
     return O.w4ec_linear_rows(flat, rows)
 
 
+def _unpack3_odd_high_from_low_half(qweight):
+    q = O.unpack_int3(qweight)
+    w = np.asarray(qweight, np.uint32)
+    n, nw = w.shape
+    hi = w.reshape(n, nw // 3, 3)[:, :, 2]
+    qb = q.reshape(n, nw // 3, 32)
+    for i in range(16):
+        qb[:, :, 2 * i + 1] = (qb[:, :, 2 * i + 1] & 3) | (((hi >> np.uint32(i)) & np.uint32(1)) << np.uint32(2)).astype(np.int64)
+    return qb.reshape(n, -1)
+
+
+def _unpack3_low_words_swapped(qweight):
+    w = np.asarray(qweight, np.uint32).copy()
+    n, nw = w.shape
+    b = w.reshape(n, nw // 3, 3)
+    b[:, :, [0, 1]] = b[:, :, [1, 0]]
+    return O.unpack_int3(b.reshape(n, nw))
+
+
+def _dequant_bits_ignored(qweight, scales_bits, zeros, group_size, bits=4):
+    return O.dequant(qweight, scales_bits, zeros, group_size, 4)
+
+
 MUTANTS = {
     "nibble order reversed": dict(unpack_int4=_unpack_reversed),
     "zero point added": dict(dequant=_dequant_plus_zero),
@@ -784,6 +926,9 @@ MUTANTS = {
     "sampled columns take B's first rows": dict(w4ec_linear_rows=_rows_b_unselected),
     "sampled columns drop the EC (act-dtype factors)": dict(w4ec_linear_rows=_rows_act_drops_ec),
     "sampled columns ignore the gate": dict(w4ec_linear_rows=_rows_gate_dropped),
+    "3-bit: odd codes' high bit from the low half": dict(unpack_int3=_unpack3_odd_high_from_low_half),
+    "3-bit: low-bit words swapped": dict(unpack_int3=_unpack3_low_words_swapped),
+    "3-bit codes read as 4-bit": dict(dequant=_dequant_bits_ignored),
 }
 
 
