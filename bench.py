@@ -682,7 +682,7 @@ def main():
             "workload": ("llama-2-70b-shaped W4+EC linear layers, the whole model resident: "
                          "80 layers x (q,o 8192->8192; k,v 8192->1024; gate,up 8192->28672; "
                          "down 28672->8192), group-128 int4, EC rank 64 with the sigmoid-linear "
-                         "gate on a seeded 25% of the modules (%d of %d), 4-bit only on the "
+                         "gate on a seeded 25%% of the modules (%d of %d), 4-bit only on the "
                          "rest, fp16 activations; one step = decode pass M=1 + prefill pass "
                          "M=4096, every module once on its AUTO path" % (int(sel.sum()), sel.size)),
             "group_size": GROUP, "rank": 64, "gate": "sigmoid_linear",

@@ -238,38 +238,6 @@ __device__ __forceinline__ bool arrive_last(uint32_t* ctr, uint32_t total) {
 }
 
 // ---------------------------------------------------------------------------
-// Dequantisation diagnostic: one thread per packed word, eight outputs.
-// (q - z) * s is exact in fp32 (<= 4 + 11 significant bits); the single
-// rounding is the conversion to the activation dtype.
-// ---------------------------------------------------------------------------
-template <int DT>
-__global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ qw,
-                                                 const uint16_t* __restrict__ sc,
-                                                 const uint8_t* __restrict__ zr,
-                                                 uint16_t* __restrict__ out, int N, int K, int G) {
-  const int kw = K >> 3;
-  const long long nwords = (long long)N * kw;
-  const long long wi = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (wi >= nwords) return;
-  const int n = (int)(wi / kw);
-  const int k = (int)(wi % kw) * 8;
-  const int ng = K / G;
-  const int g = k / G;
-  const float s = h2f(sc[(long long)n * ng + g]);
-  const int z = zr[(long long)n * ng + g];
-  const uint32_t w = qw[wi];
-  uint32_t o[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int q0 = (w >> (8 * i)) & 15, q1 = (w >> (8 * i + 4)) & 15;
-    const uint32_t lo = f2act<DT>((float)(q0 - z) * s);
-    const uint32_t hi = f2act<DT>((float)(q1 - z) * s);
-    o[i] = lo | (hi << 16);
-  }
-  *(u32x4*)(out + (long long)n * K + k) = u32x4{o[0], o[1], o[2], o[3]};
-}
-
-// ---------------------------------------------------------------------------
 // Coherent reads of data other workgroups published in this launch: buffer
 // loads with the sc1 bit (what a relaxed agent-scope atomic load is on
 // gfx950), bounds-checked so that every load of a batch is issued without a
@@ -1633,6 +1601,29 @@ __device__ __forceinline__ void dequant_word_pairs(uint32_t w, float s, int z, u
       out[i] = (uint32_t)f2act<DT>(a0) | ((uint32_t)f2act<DT>(a1) << 16);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Dequantisation diagnostic: one thread per packed word, eight outputs, by
+// dequant_word_pairs, the code the prefill GEMM dequantises its weight tiles
+// with: (q - z) exact, then one rounding of its product with s.
+// ---------------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ qw,
+                                                 const uint16_t* __restrict__ sc,
+                                                 const uint8_t* __restrict__ zr,
+                                                 uint16_t* __restrict__ out, int N, int K, int G) {
+  const int kw = K >> 3;
+  const long long nwords = (long long)N * kw;
+  const long long wi = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (wi >= nwords) return;
+  const int n = (int)(wi / kw);
+  const int k = (int)(wi % kw) * 8;
+  const int ng = K / G;
+  const int g = k / G;
+  uint32_t o[4];
+  dequant_word_pairs<DT>(qw[wi], h2f(sc[(long long)n * ng + g]), zr[(long long)n * ng + g], o);
+  *(u32x4*)(out + (long long)n * K + k) = u32x4{o[0], o[1], o[2], o[3]};
 }
 
 // Split-K tile reduction of the GEMM: a thread's 16 f32x4 of the tile from

@@ -81,6 +81,31 @@ def test_dequant_bit_exact(dt, G):
     assert np.array_equal(got, want), f"{(got != want).sum()} mismatching bits"
 
 
+@pytest.mark.parametrize("dt", [S.F16, S.BF16])
+@pytest.mark.parametrize("path", ["auto", "fused_gemv", "2k", "chain"])
+def test_decode_cancellation_worst_case(dt, path):
+    """The decode GEMV never forms a dequantised weight: per 128-wide group it
+    sums x (bias + q) and subtracts (bias + z) sum x in fp32 (bias 1024 for
+    fp16, 128 for bf16), which cancels. The worst case for that is a long K
+    (the 70B down projection, 28672), activations of one sign with outlier
+    channels (every group's sum of x large), and codes within one step of the
+    zero point (the exact group sums small against the biased ones). The
+    result must still meet the parity bar."""
+    M, N, K, G = 4, 512, 28672, 128
+    L = S.make_layer(M=M, N=N, K=K, group_size=G, rank=16, act_dtype=dt, seed=21)
+    rng = np.random.default_rng(21)
+    x = np.abs(rng.standard_normal((M, K))).astype(np.float32) + 2.0
+    out_idx = rng.choice(K, size=round(0.01 * K), replace=False)
+    x[:, out_idx] *= 20.0
+    z = rng.integers(1, 15, size=(N, K // G))
+    q = np.clip(z[:, np.arange(K) // G] + rng.integers(-1, 2, size=(N, K)), 0, 15)
+    L = with_fields(L, x=S.to_bits(x, dt), qweight=S.pack_int4(q), zeros=z.astype(np.uint8))
+    ref = O.w4ec_linear(L)
+    log(f"cancellation worst case dt={dt} path={path}")
+    relf, mx = assert_parity(gpu_y(L, PATHS[path]), ref, f"cancellation/{dt}/{path}")
+    log(f"  relF={relf:.2e} max|d|={mx:.2e}")
+
+
 # ---------------------------------------------------------------------------
 # small configurations, every path
 # ---------------------------------------------------------------------------
@@ -222,8 +247,11 @@ def test_deterministic_and_workspace_reuse(path):
     prob = dl.problem(force_path=PATHS[path])
     plan = sp.dispatch_plan(prob)
     assert plan.split_k > 1 and plan.ec_splits > 1
-    size = max(plan.workspace_bytes, sp.dispatch_plan(do.problem()).workspace_bytes,
-               sp.dispatch_plan(dl.problem()).workspace_bytes)
+    other_path = PATHS["fused_gemv" if path == "fused_local" else "fused_local"]
+    size = max([plan.workspace_bytes, sp.dispatch_plan(dl.problem(force_path=other_path)).workspace_bytes,
+                sp.dispatch_plan(dl.problem(), False).workspace_bytes,
+                sp.dispatch_plan(do.problem(), False).workspace_bytes] +
+               [sp.dispatch_plan(do.problem(force_path=p)).workspace_bytes for p in (0, 3, 4)])
     ws = torch.zeros(size, dtype=torch.uint8, device="cuda")
     log(f"determinism {path}")
     first = gpu_y(L, PATHS[path], workspace=ws, dev=dl)
@@ -232,8 +260,7 @@ def test_deterministic_and_workspace_reuse(path):
             gpu_y(other, p, workspace=ws, dev=do)
         gpu_y(other, 0, with_ec=False, workspace=ws, dev=do)
         gpu_y(L, 0, with_ec=False, workspace=ws, dev=dl)
-        gpu_y(L, PATHS["fused_gemv" if path == "fused_local" else "fused_local"], workspace=ws,
-              dev=dl)
+        gpu_y(L, other_path, workspace=ws, dev=dl)
         again = gpu_y(L, PATHS[path], workspace=ws, dev=dl)
         assert np.array_equal(first, again), i
     assert_parity(first, O.w4ec_linear(L), f"determinism {path}")
