@@ -200,6 +200,26 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x,
                                  void* y, void* workspace,
                                  size_t workspace_bytes, void* hip_stream);
 
+/* ---- Calls that allocate nothing --------------------------------------------
+ * For callers that cannot allocate device memory or pass a workspace (code
+ * under stream capture, serving loops or harnesses that forbid allocation):
+ * spear_w4ec_linear with the scratch taken from a static array inside the
+ * library, SPEAR_SCRATCH_BYTES per GPU, held from the library's load until
+ * the process ends (one copy per device, found on the first call on each
+ * device). Same arguments, path, kernels and results as spear_w4ec_linear
+ * (bit for bit); the call allocates nothing and issues no memset (the array's
+ * counters start at zero when the library is loaded, and every call leaves
+ * them ready for the next). Problems whose planned workspace_bytes exceed
+ * SPEAR_SCRATCH_BYTES return SPEAR_E_WORKSPACE; SPEAR_E_HIP if the scratch
+ * cannot be located on the current device. Every call on one GPU uses the
+ * same array: calls that overlap in time on one GPU (other streams, other
+ * host threads) race and must be serialised by the caller. */
+#define SPEAR_SCRATCH_BYTES (16u << 20)
+
+spear_status_t spear_w4ec_linear_noalloc(const spear_problem_t* prob, const void* x,
+                                         const spear_w4_t* w, const spear_ec_t* ec, void* y,
+                                         void* hip_stream);
+
 /* Post-EC tail (section 4.2: after the compensated product, the residual
  * addition and the next layer's RMSNorm). */
 typedef struct {

@@ -40,7 +40,7 @@ def build(verbose: bool = False) -> str:
     os.makedirs(objdir, exist_ok=True)
     objs = []
     for src, extra in (("spear_kernels.hip", [f"--offload-arch={ARCH}", "-x", "hip"]),
-                       ("spear_api.cpp", [f"--offload-arch={ARCH}"]),
+                       ("spear_api.cpp", [f"--offload-arch={ARCH}", "-x", "hip"]),
                        ("spear_sched.cpp", [f"--offload-arch={ARCH}"])):
         obj = os.path.join(objdir, src + ".o")
         cmd = [HIPCC] + COMMON + extra + ["-c", os.path.join(CSRC, src), "-o", obj]

@@ -7,6 +7,7 @@
 #include <atomic>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/spear.h"
 #include "spear_internal.h"
@@ -836,6 +837,39 @@ spear_status_t group_resolve(int32_t n, const spear_layer_call_t* calls, Resolve
   return SPEAR_OK;
 }
 
+// ---- the library's own scratch (spear_w4ec_linear_noalloc) ---------------
+// One array per GPU, allocated by the loader with the code object and
+// zero-filled there, so that its counter block starts at zero without any
+// call of ours clearing it. Its device address comes from
+// hipGetSymbolAddress, once per device, with that device current: in host
+// code the array's name is only a host-side stand-in, never passed to a
+// kernel or a copy.
+static __device__ __align__(256) unsigned char scratch[SPEAR_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// This device's copy of the scratch array (looked up on the first call on
+// the device), or null with *err set.
+void* device_scratch(spear_status_t* err) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    *err = SPEAR_E_HIP;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      *err = SPEAR_E_HIP;
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -871,6 +905,21 @@ spear_status_t spear_w4ec_linear(const spear_problem_t* prob, const void* x, con
   if ((st = check_ec(prob, z, ec, y)) != SPEAR_OK) return st;
   if ((st = check_ws(prob, z, y, workspace, workspace_bytes)) != SPEAR_OK) return st;
   return run_layer(prob, z, x, w, ec, y, nullptr, (char*)workspace, (hipStream_t)hip_stream);
+}
+
+spear_status_t spear_w4ec_linear_noalloc(const spear_problem_t* prob, const void* x,
+                                         const spear_w4_t* w, const spear_ec_t* ec, void* y,
+                                         void* hip_stream) {
+  Resolved z;
+  spear_status_t st = resolve(prob, true, &z);
+  if (st != SPEAR_OK) return st;
+  if (prob->M == 0 || prob->N == 0) return SPEAR_OK;
+  if (z.plan.workspace_bytes > SPEAR_SCRATCH_BYTES) return SPEAR_E_WORKSPACE;
+  if ((st = check_w4(prob, x, w, y)) != SPEAR_OK) return st;
+  if ((st = check_ec(prob, z, ec, y)) != SPEAR_OK) return st;
+  void* ws = device_scratch(&st);
+  if (!ws) return st;
+  return run_layer(prob, z, x, w, ec, y, nullptr, (char*)ws, (hipStream_t)hip_stream);
 }
 
 spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x,

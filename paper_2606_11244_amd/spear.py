@@ -33,7 +33,7 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
             "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
             "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
-            "spear_set_gemm_tile", "spear_workspace_regions",
+            "spear_set_gemm_tile", "spear_workspace_regions", "spear_w4ec_linear_noalloc",
             "spear_status_string", "spear_version", "spear_sched_latency", "spear_sched_chunk")
 
 
@@ -114,6 +114,8 @@ def _load():
     lib.spear_w4ec_linear.argtypes = [P(Problem), ctypes.c_void_p, P(W4), P(EC), ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
     lib.spear_w4_dequant.argtypes = [P(Problem), P(W4), ctypes.c_void_p, ctypes.c_void_p]
+    lib.spear_w4ec_linear_noalloc.argtypes = [P(Problem), ctypes.c_void_p, P(W4), P(EC),
+                                              ctypes.c_void_p, ctypes.c_void_p]
     lib.spear_w4ec_linear_tail.argtypes = [P(Problem), ctypes.c_void_p, P(W4), P(EC), P(Tail),
                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                            ctypes.c_void_p]
@@ -138,7 +140,7 @@ def _load():
     lib.spear_version.restype = ctypes.c_char_p
     for f in ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
               "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
-              "spear_set_wait_polls", "spear_workspace_regions"):
+              "spear_set_wait_polls", "spear_workspace_regions", "spear_w4ec_linear_noalloc"):
         getattr(lib, f).restype = ctypes.c_int32
     return lib
 
@@ -224,6 +226,29 @@ def w4ec_linear(prob: Problem, x, qweight, scales, zeros, A, B, y, *, alpha=1.0,
                                _ptr(y), _ptr(workspace), ws_bytes, _stream(stream))
     if st != 0:
         raise SpearError(st, "spear_w4ec_linear")
+    return y
+
+
+SCRATCH_BYTES = 16 << 20  # SPEAR_SCRATCH_BYTES: the library's own scratch per GPU
+
+
+def w4ec_linear_noalloc(prob: Problem, x, qweight, scales, zeros, A, B, y, *, alpha=1.0,
+                        w_g=None, b_g=0.0, W1=None, b1=None, W2=None, b2=None, a_scale=None,
+                        b_scale=None, ab_format=None, stream=None):
+    """spear_w4ec_linear_noalloc: as w4ec_linear, with the library's own
+    scratch instead of a workspace (nothing is allocated)."""
+    w = W4(_ptr(qweight).value, _ptr(scales).value, _ptr(zeros).value)
+
+    def p(t):
+        return None if t is None else t.data_ptr()
+
+    fmt = (AB_INT8 if a_scale is not None else AB_ACT) if ab_format is None else int(ab_format)
+    ec = EC(p(A), p(B), float(alpha), p(w_g), float(b_g), p(W1), p(b1), p(W2), p(b2),
+            fmt, p(a_scale), p(b_scale))
+    st = LIB.spear_w4ec_linear_noalloc(ctypes.byref(prob), _ptr(x), ctypes.byref(w),
+                                       ctypes.byref(ec), _ptr(y), _stream(stream))
+    if st != 0:
+        raise SpearError(st, "spear_w4ec_linear_noalloc")
     return y
 
 
@@ -439,6 +464,14 @@ class DeviceLayer:
                            alpha=L.alpha, w_g=self.w_g, b_g=L.b_g, W1=self.W1, b1=self.b1,
                            W2=self.W2, b2=self.b2, a_scale=self.a_scale, b_scale=self.b_scale,
                            workspace=workspace, stream=stream)
+
+    def run_noalloc(self, prob, stream=None, y=None):
+        L = self.layer
+        y = self.y if y is None else y
+        return w4ec_linear_noalloc(prob, self.x, self.qweight, self.scales, self.zeros, self.A,
+                                   self.B, y, alpha=L.alpha, w_g=self.w_g, b_g=L.b_g, W1=self.W1,
+                                   b1=self.b1, W2=self.W2, b2=self.b2, a_scale=self.a_scale,
+                                   b_scale=self.b_scale, stream=stream)
 
     def run_tail(self, prob, workspace, residual=None, norm_w=None, eps=1e-5, y_norm=None,
                  with_ec=True, stream=None, y=None):
