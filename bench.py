@@ -50,12 +50,13 @@ DEC_M, PRE_M = 1, 4096  # the metric's decode and prefill token counts
 DEC_GROUPS = ((0, 1, 2), (3,), (4, 5), (6,))
 
 
-def algo_bytes(M, N, K, G, r, ab_int8=False):
-    """Algorithmic HBM bytes of one W4+EC call: codes (N K / 2), scales and
-    4-bit zeros (2.5 N K / G), A, B, w_g, X and Y in fp16 (A and B as int8
-    codes plus fp32 per-channel scales with ab_int8)."""
+def algo_bytes(M, N, K, G, r, ab_int8=False, wbits=4):
+    """Algorithmic HBM bytes of one W4+EC call: codes (N K / 2; 3N K / 8 for
+    3-bit codes), scales and 4-bit zeros (2.5 N K / G), A, B, w_g, X and Y in
+    fp16 (A and B as int8 codes plus fp32 per-channel scales with ab_int8)."""
     ab = (r * K + N * r + 4 * (r + N)) if ab_int8 else (2 * r * K + 2 * N * r)
-    return N * K / 2 + 2.5 * N * K / G + (ab if r else 0) + (2 * K if r else 0) + 2 * M * K + 2 * M * N
+    return (N * K * wbits / 8 + 2.5 * N * K / G + (ab if r else 0) + (2 * K if r else 0)
+            + 2 * M * K + 2 * M * N)
 
 
 def algo_flops(M, N, K, r):
@@ -117,12 +118,12 @@ def cpu_baseline(sel, budget_s=20.0):
         K, N = S.LLAMA_70B[m]
         for r in (0, 64):
             t = {}
-            for ns in (128, 256):
+            for ns in (512, 1024):
                 L = S.make_layer(M=DEC_M, N=ns, K=K, group_size=GROUP, rank=r, seed=0,
                                  config_id=4, module_id=j)
                 t[ns] = timed(L)
-            slope = max(0.0, (t[256] - t[128]) / 128.0)
-            per_module[(m, r)] = t[128] + slope * (N - 128)
+            slope = max(0.0, (t[1024] - t[512]) / 512.0)
+            per_module[(m, r)] = t[512] + slope * (N - 512)
     t_pass, nbytes = 0.0, 0.0
     for l in range(sel.shape[0]):
         for j, m in enumerate(S.MODULES):
@@ -138,8 +139,8 @@ def cpu_baseline(sel, budget_s=20.0):
         "value": round(nbytes / t_pass / 1e9, 4), "unit": "GB/s", "cores": int(blas),
         "kind": "oracle",
         "sample": ("float64 numpy oracle on the 70B-shaped decode pass (M=1), extrapolated: "
-                   "each of the 7 module shapes with and without the EC (rank 64) on 128 and "
-                   "256 output rows of full K, median of 3, the time line evaluated at the "
+                   "each of the 7 module shapes with and without the EC (rank 64) on 512 and "
+                   "1024 output rows of full K, median of 3, the time line evaluated at the "
                    "module's N, summed over 80 layers with the model's EC selection "
                    f"({t_pass:.1f} s per pass, {nbytes / 1e9:.1f} GB algorithmic)"),
         "prefill_tflops": round(algo_flops(PRE_M, N, K, 64) / t_pre / 1e12, 5),
@@ -153,12 +154,13 @@ class Model70B:
     """The 70B-shaped model resident in HBM and one pass of its linear layers
     at M tokens (every module once, each call on its AUTO path)."""
 
-    def __init__(self, sp, torch, dev, Mmax):
+    def __init__(self, sp, torch, dev, Mmax, weight_bits=4):
         from paper_2606_11244_amd import model70b
         from paper_2606_11244_amd import synth as S
         self.sp, self.torch, self.S = sp, torch, S
         self.r, self.G = model70b.RANK, model70b.GROUP
-        self.layers, self.sel = model70b.build(dev)
+        self.wb = weight_bits
+        self.layers, self.sel = model70b.build(dev, weight_bits=weight_bits)
         Kmax = max(k for k, _ in S.LLAMA_70B.values())
         Nmax = max(n for _, n in S.LLAMA_70B.values())
         g = torch.Generator(device=dev)
@@ -172,8 +174,10 @@ class Model70B:
         out = {}
         for m in S.MODULES:
             K, N = S.LLAMA_70B[m]
-            out[m] = (sp.problem(M, N, K, self.G, sp.F16, self.r, sp.GATE_SIGMOID_LINEAR),
-                      sp.problem(M, N, K, self.G, sp.F16, 0, sp.GATE_SIGMOID_LINEAR))
+            out[m] = (sp.problem(M, N, K, self.G, sp.F16, self.r, sp.GATE_SIGMOID_LINEAR,
+                                 weight_bits=self.wb),
+                      sp.problem(M, N, K, self.G, sp.F16, 0, sp.GATE_SIGMOID_LINEAR,
+                                 weight_bits=self.wb))
         return out
 
     def workspace(self, M):
@@ -220,7 +224,7 @@ class Model70B:
         for mods in self.layers:
             for (m, K, N, q, sc, zr, ec) in mods:
                 r = self.r if (with_ec and ec is not None) else 0
-                nbytes += algo_bytes(M, N, K, self.G, r)
+                nbytes += algo_bytes(M, N, K, self.G, r, wbits=self.wb)
                 flops += algo_flops(M, N, K, r)
                 pe, p4 = plans[m]
                 launches += (sp.dispatch_plan(pe).num_launches if r
@@ -551,6 +555,8 @@ def main():
     ap.add_argument("--no-paper-protocol", action="store_true",
                     help="skip the decode pass timed as 200 warm-up + 500 timed replays")
     ap.add_argument("--no-1b", action="store_true", help="skip the Llama-3.2-1B-shaped passes")
+    ap.add_argument("--no-w3", action="store_true",
+                    help="skip the 70B-shaped model with 3-bit codes")
     ap.add_argument("--no-int8", action="store_true",
                     help="1B: skip the passes with INT8 per-channel EC factors")
     ap.add_argument("--no-ungrouped", action="store_true",
@@ -642,6 +648,8 @@ def main():
     if args.model70b:
         del g_pre
         sweep = model_70b_sweep(model)
+    else:
+        del g_pre
 
     if args.copy_calib_mb:
         # counter calibration: one elementwise kernel that reads and writes
@@ -658,6 +666,33 @@ def main():
     paths_dec, paths_pre = model.paths(DEC_M), model.paths(PRE_M)
     del model, g_dec, ws_dec, ws_pre
     torch.cuda.empty_cache()
+
+    w3 = None
+    if not args.no_w3:
+        # the same model with 3-bit codes (the paper's 3-bit backbone)
+        print("bench: 70B-shaped model with 3-bit codes", file=sys.stderr, flush=True)
+        m3 = Model70B(sp, torch, dev, PRE_M, weight_bits=3)
+        wd, wp = m3.workspace(DEC_M), m3.workspace(PRE_M)
+        res = {}
+        for what, M, ws, n in (("decode", DEC_M, wd, max(5, args.steps)), ("prefill", PRE_M, wp, 3)):
+            t = {}
+            for ec in (True, False):
+                g = m3.capture(M, ec, ws)
+                replay_times(torch, g, 2)
+                t[ec] = float(np.median(replay_times(torch, g, n)))
+                del g
+            nb, fl, _ = m3.work(M)
+            res[what] = {"ms_per_pass": round(t[True] * 1e3, 4),
+                         "w3_only_ms": round(t[False] * 1e3, 4),
+                         "ec_overhead": round(t[True] / t[False] - 1.0, 4),
+                         "GBps": round(nb / t[True] / 1e9, 1),
+                         "hbm_frac": round(nb / t[True] / 1e9 / HBM_PEAK_GBS, 4),
+                         "TFLOPs": round(fl / t[True] / 1e12, 1),
+                         "mfma_frac": round(fl / t[True] / 1e12 / MFMA_F16_PEAK_TFLOPS, 4)}
+        w3 = {"weights": "3-bit codes, 32 to three words; group 128; device-random",
+              "decode_M1": res["decode"], "prefill_M4096": res["prefill"]}
+        del m3, wd, wp
+        torch.cuda.empty_cache()
 
     extras = None
     if not args.no_1b:
@@ -724,6 +759,7 @@ def main():
         "decode_paper_protocol": paper,
         "ec_overhead": overhead,
         "model_70b_sweep": sweep,
+        "w3_model_70b": w3,
         "llama1b": extras,
     }
     if not args.no_cpu_baseline:

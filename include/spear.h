@@ -22,6 +22,7 @@
  *       y        [M][N]    output, act dtype (overwritten, not accumulated)
  *       qweight  [N][K/8]  uint32; word j of row n holds code q[n][8j+i]
  *                          (0..15) in bits 4i..4i+3, lowest nibble first
+ *                          (3-bit codes: [N][3K/32], see spear_w4_t)
  *       scales   [N][K/G]  IEEE fp16 bit patterns (both act dtypes)
  *       zeros    [N][K/G]  uint8, values 0..15
  *       A        [r][K]    act dtype      B  [N][r]  act dtype
@@ -62,7 +63,8 @@ enum {
   SPEAR_OK = 0,
   SPEAR_E_NULL = -1,        /* a required pointer is NULL                   */
   SPEAR_E_SHAPE = -2,       /* M, N, K, G, r or h outside the supported set */
-  SPEAR_E_DTYPE = -3,       /* unknown activation dtype or EC factor format */
+  SPEAR_E_DTYPE = -3,       /* unknown activation dtype, EC factor format or
+                               weight code width                              */
   SPEAR_E_ALIGN = -4,       /* a device pointer is not 16-byte aligned      */
   SPEAR_E_WORKSPACE = -5,   /* workspace missing or smaller than required   */
   SPEAR_E_UNSUPPORTED = -6, /* gate kind or forced path not available       */
@@ -127,12 +129,23 @@ typedef struct {
   int32_t gate_kind;    /* SPEAR_GATE_*                                       */
   int32_t gate_hidden;  /* h of the tanh-MLP gate, 0 = 4r; at most 1024       */
   int32_t force_path;   /* SPEAR_PATH_*; AUTO = choose by M                   */
+  int32_t weight_bits;  /* code width of qweight: 0 or 4 (the default), or 3
+                           (the 3-bit backbone of Appendix D.1 and D.3; zeros
+                           then 0..7; layout at spear_w4_t); other values:
+                           SPEAR_E_DTYPE                                      */
 } spear_problem_t;
 
+/* The quantised weight. 4-bit codes: qweight [N][K/8], word j of row n
+ * holding q[n][8j+i] in bits 4i..4i+3. 3-bit codes (weight_bits = 3):
+ * qweight [N][3K/32], the codes c_t = q[n][32j+t] (t = 0..31) of block j in
+ * words 3j, 3j+1, 3j+2 of row n: word 3j holds the low two bits of c_{2i} in
+ * bits 2i..2i+1 and of c_{2i+1} in bits 16+2i..17+2i (i = 0..7), word 3j+1
+ * the same for c_{16+2i} and c_{17+2i}, word 3j+2 the high bit of c_{2i} in
+ * bit i and of c_{2i+1} in bit 16+i (i = 0..15). */
 typedef struct {
-  const uint32_t* qweight; /* [N][K/8] packed codes                           */
+  const uint32_t* qweight; /* [N][K/8] (4-bit) or [N][3K/32] (3-bit) codes    */
   const uint16_t* scales;  /* [N][K/G] fp16 bits                              */
-  const uint8_t* zeros;    /* [N][K/G] 0..15                                  */
+  const uint8_t* zeros;    /* [N][K/G] 0..15 (4-bit) or 0..7 (3-bit)          */
 } spear_w4_t;
 
 /* Storage of the EC factors A and B (section 5.1 and Appendix B.2: the

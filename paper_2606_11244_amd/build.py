@@ -6,6 +6,7 @@ tree; nothing is installed.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import os
 import shutil
 import subprocess
@@ -35,19 +36,25 @@ def _run(cmd):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every HIP/C++ source of the library and link libspear.so."""
+    """Compile every HIP/C++ source of the library (in parallel processes) and
+    link libspear.so. spear_kernels.hip is compiled twice: for 4-bit and for
+    3-bit weight codes (SPEAR_WB)."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
-    objs = []
-    for src, extra in (("spear_kernels.hip", [f"--offload-arch={ARCH}", "-x", "hip"]),
-                       ("spear_api.cpp", [f"--offload-arch={ARCH}", "-x", "hip"]),
-                       ("spear_sched.cpp", [f"--offload-arch={ARCH}"])):
-        obj = os.path.join(objdir, src + ".o")
+    units = (("spear_kernels.hip", "w4", [f"--offload-arch={ARCH}", "-x", "hip", "-DSPEAR_WB=4"]),
+             ("spear_kernels.hip", "w3", [f"--offload-arch={ARCH}", "-x", "hip", "-DSPEAR_WB=3"]),
+             ("spear_api.cpp", "", [f"--offload-arch={ARCH}", "-x", "hip"]),
+             ("spear_sched.cpp", "", [f"--offload-arch={ARCH}"]))
+    cmds, objs = [], []
+    for src, tag, extra in units:
+        obj = os.path.join(objdir, src + (("." + tag) if tag else "") + ".o")
         cmd = [HIPCC] + COMMON + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd))
-        _run(cmd)
+        cmds.append(cmd)
         objs.append(obj)
+    with cf.ThreadPoolExecutor(len(cmds)) as ex:
+        list(ex.map(_run, cmds))
     tmp = LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs)
     os.replace(tmp, LIB)

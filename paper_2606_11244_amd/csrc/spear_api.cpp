@@ -45,6 +45,7 @@ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 struct Resolved {
   spear_plan_t plan;
   bool ec, gemv;
+  int wb;  // weight code width: 4 or 3
   int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
   int MT, RT, NW, nrg, S, ips, iw;            // GEMV shape
   int Sg;                                     // GEMM K-slices
@@ -64,6 +65,7 @@ spear_status_t validate_shape(const spear_problem_t* p, bool with_ec) {
   if (!p) return SPEAR_E_NULL;
   if (p->M < 0 || p->N < 0 || p->K <= 0 || p->K % kIterK) return SPEAR_E_SHAPE;
   if (p->act_dtype != SPEAR_F16 && p->act_dtype != SPEAR_BF16) return SPEAR_E_DTYPE;
+  if (p->weight_bits != 0 && p->weight_bits != 4 && p->weight_bits != 3) return SPEAR_E_DTYPE;
   const int64_t G = (p->group_size == 0) ? p->K : p->group_size;
   if (G <= 0 || G % kIterK || p->K % G) return SPEAR_E_SHAPE;
   // every buffer stays below 2 GiB (element counts below 2^30), so that the
@@ -141,6 +143,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   std::memset(&z, 0, sizeof(z));
   const int64_t M = p->M, N = p->N, K = p->K;
   z.dt = p->act_dtype;
+  z.wb = p->weight_bits == 3 ? 3 : 4;
   z.G = (int)((p->group_size == 0) ? K : p->group_size);
   z.ngroups = (int)(K / z.G);
   z.IT = (int)(K / kIterK);
@@ -495,6 +498,11 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   return SPEAR_OK;
 }
 
+// Bytes of the packed codes of an [N][K] weight of this code width.
+size_t code_bytes(const spear_problem_t* p) {
+  return p->weight_bits == 3 ? (size_t)p->N * p->K / 8 * 3 : (size_t)p->N * p->K / 2;
+}
+
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   if (!a || !b || na == 0 || nb == 0) return false;
   const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
@@ -509,7 +517,7 @@ spear_status_t check_w4(const spear_problem_t* p, const void* x, const spear_w4_
   const size_t G = p->group_size == 0 ? (size_t)p->K : (size_t)p->group_size;
   const size_t ybytes = (size_t)p->M * p->N * 2;
   if (overlaps(y, ybytes, x, (size_t)p->M * p->K * 2) ||
-      overlaps(y, ybytes, w->qweight, (size_t)p->N * p->K / 2) ||
+      overlaps(y, ybytes, w->qweight, code_bytes(p)) ||
       overlaps(y, ybytes, w->scales, (size_t)p->N * (p->K / G) * 2) ||
       overlaps(y, ybytes, w->zeros, (size_t)p->N * (p->K / G)))
     return SPEAR_E_ALIAS;
@@ -688,18 +696,27 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
 
 spear_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPEAR_OK : SPEAR_E_HIP; }
 
+// The kernels that read the packed codes, for the problem's code width.
+hipError_t launch_gemv_wb(const Resolved& z, int epi, const GemvParams& p, int grid, int block,
+                          size_t lds, hipStream_t st) {
+  return z.wb == 3 ? launch_gemv_w3(z.dt, z.MT, z.RT, epi, p, grid, block, lds, st)
+                   : launch_gemv_w4(z.dt, z.MT, z.RT, epi, p, grid, block, lds, st);
+}
+hipError_t launch_gemm_wb(const Resolved& z, int epi, const GemmParams& p, hipStream_t st) {
+  return z.wb == 3 ? launch_gemm_w3(z.dt, epi, p, st) : launch_gemm_w4(z.dt, epi, p, st);
+}
+
 // res: [M][N] act-dtype residual added before the output's single rounding, or null
 spear_status_t run_w4(const spear_problem_t* p, const Resolved& z, const void* x, const spear_w4_t* w,
                       void* y, char* ws, hipStream_t st, const uint16_t* res = nullptr) {
   if (z.gemv) {
     GemvParams g = make_gemv(p, z, x, w, y, nullptr, ws);
     g.res = res;
-    return hip_status(
-        launch_gemv(z.dt, z.MT, z.RT, EPI_NONE, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, st));
+    return hip_status(launch_gemv_wb(z, EPI_NONE, g, z.nrg * z.S, 64 * z.NW, z.lds_gemv, st));
   }
   GemmParams g = make_gemm(p, z, x, w, y, nullptr, ws);
   g.res = res;
-  return hip_status(launch_gemm(z.dt, EPI_NONE, g, st));
+  return hip_status(launch_gemm_wb(z, EPI_NONE, g, st));
 }
 
 // The layer on its planned path, after validation; res as in run_w4 (the
@@ -716,15 +733,15 @@ spear_status_t run_layer(const spear_problem_t* prob, const Resolved& z, const v
   if (path == SPEAR_PATH_FUSED_MFMA) {
     GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
     g.res = res;
-    return hip_status(launch_gemm(z.dt, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g, s));
+    return hip_status(launch_gemm_wb(z, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g, s));
   }
   if (path == SPEAR_PATH_FUSED_LOCAL) {
     GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
     g.res = res;
     g.ec = e;
     if (z.S > 1) g.eupart = (float*)(ws + z.off_eupart);
-    return hip_status(launch_gemv(z.dt, z.MT, z.RT, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g,
-                                  z.nrg * z.S, 64 * z.NW, z.lds_gemv, s));
+    return hip_status(launch_gemv_wb(z, ab_int8(ec) ? EPI_LOCAL_I8 : EPI_LOCAL, g, z.nrg * z.S,
+                                     64 * z.NW, z.lds_gemv, s));
   }
   if (path == SPEAR_PATH_FUSED_GEMV) {
     e.vtag = (unsigned long long*)(ws + z.off_vtag);
@@ -739,8 +756,7 @@ spear_status_t run_layer(const spear_problem_t* prob, const Resolved& z, const v
     g.n_prod = z.n_prod;
     g.grid_total = z.n_prod + z.nrg * z.S;
     const size_t lds = std::max(z.lds_gemv, z.lds_prod);
-    return hip_status(
-        launch_gemv(z.dt, z.MT, z.RT, EPI_FUSED, g, g.grid_total, 64 * (z.NW + 1), lds, s));
+    return hip_status(launch_gemv_wb(z, EPI_FUSED, g, g.grid_total, 64 * (z.NW + 1), lds, s));
   }
   if (path == SPEAR_PATH_UNFUSED_2K) {
     if (!z.gemv) {
@@ -754,12 +770,12 @@ spear_status_t run_layer(const spear_problem_t* prob, const Resolved& z, const v
       GemvParams g = make_gemv(prob, z, x, w, y, ec, ws);
       g.res = res;
       g.ec = e;
-      return hip_status(launch_gemv(z.dt, z.MT, z.RT, EPI_READY, g, z.nrg * z.S, 64 * (z.NW + 1),
-                                    z.lds_gemv, s));
+      return hip_status(launch_gemv_wb(z, EPI_READY, g, z.nrg * z.S, 64 * (z.NW + 1), z.lds_gemv,
+                                       s));
     }
     GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
     g.res = res;
-    return hip_status(launch_gemm(z.dt, EPI_READY, g, s));
+    return hip_status(launch_gemm_wb(z, EPI_READY, g, s));
   }
   // naive chain: 4-bit product, projection, gate, reprojection + accumulate
   st = run_w4(prob, z, x, w, y, ws, s, res);
@@ -784,7 +800,7 @@ bool hits_member(const void* y, size_t yb, const spear_layer_call_t& c) {
   const spear_problem_t* p = c.prob;
   const size_t G = p->group_size == 0 ? (size_t)p->K : (size_t)p->group_size;
   if (overlaps(y, yb, c.x, (size_t)p->M * p->K * 2) || overlaps(y, yb, c.y, (size_t)p->M * p->N * 2) ||
-      overlaps(y, yb, c.w->qweight, (size_t)p->N * p->K / 2) ||
+      overlaps(y, yb, c.w->qweight, code_bytes(p)) ||
       overlaps(y, yb, c.w->scales, (size_t)p->N * (p->K / G) * 2) ||
       overlaps(y, yb, c.w->zeros, (size_t)p->N * (p->K / G)))
     return true;
@@ -999,7 +1015,8 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
   bool one = n > 1 && epi >= 0;
   int ctrs = 0;
   for (int i = 0; i < n && one; ++i) {
-    one = group_epi(z[i], calls[i].ec) == epi && z[i].dt == z[0].dt && z[i].MT == z[0].MT &&
+    one = group_epi(z[i], calls[i].ec) == epi && z[i].dt == z[0].dt && z[i].wb == z[0].wb &&
+          z[i].MT == z[0].MT &&
           z[i].RT == z[0].RT && z[i].NW == z[0].NW;
     if (z[i].S > 1) ctrs += z[i].nrg;
   }
@@ -1062,7 +1079,9 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
     }
     lds = std::max(lds, z[i].lds_gemv);
   }
-  return hip_status(launch_gemv_group(z[0].dt, z[0].MT, z[0].RT, epi, g, 64 * z[0].NW, lds, s));
+  return hip_status(z[0].wb == 3
+                        ? launch_gemv_group_w3(z[0].dt, z[0].MT, z[0].RT, epi, g, 64 * z[0].NW, lds, s)
+                        : launch_gemv_group_w4(z[0].dt, z[0].MT, z[0].RT, epi, g, 64 * z[0].NW, lds, s));
 }
 
 spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w, void* w_out,
@@ -1079,13 +1098,13 @@ spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w
     return SPEAR_E_ALIGN;
   const int G = (int)(prob->group_size == 0 ? prob->K : prob->group_size);
   const size_t outb = (size_t)prob->N * prob->K * 2;
-  if (overlaps(w_out, outb, w->qweight, (size_t)prob->N * prob->K / 2) ||
+  if (overlaps(w_out, outb, w->qweight, code_bytes(prob)) ||
       overlaps(w_out, outb, w->scales, (size_t)prob->N * (prob->K / G) * 2) ||
       overlaps(w_out, outb, w->zeros, (size_t)prob->N * (prob->K / G)))
     return SPEAR_E_ALIAS;
-  return hip_status(launch_dequant(prob->act_dtype, w->qweight, w->scales, w->zeros,
-                                   (uint16_t*)w_out, (int)prob->N, (int)prob->K, G,
-                                   (hipStream_t)hip_stream));
+  const auto dq = prob->weight_bits == 3 ? launch_dequant_w3 : launch_dequant_w4;
+  return hip_status(dq(prob->act_dtype, w->qweight, w->scales, w->zeros, (uint16_t*)w_out,
+                       (int)prob->N, (int)prob->K, G, (hipStream_t)hip_stream));
 }
 
 spear_status_t spear_workspace_regions(const spear_problem_t* prob, int32_t with_ec,
@@ -1130,6 +1149,6 @@ const char* spear_status_string(spear_status_t s) {
   }
 }
 
-const char* spear_version(void) { return "0.1.0"; }
+const char* spear_version(void) { return "0.2.0"; }
 
 }  // extern "C"

@@ -210,16 +210,23 @@ __host__ __device__ inline size_t ec_block_lds(int NW, int R1p, int h, int r) {
   return ec_red_bytes(NW) + ec_lds_bytes(R1p, h, r);
 }
 
-hipError_t launch_dequant(int dt, const uint32_t* qw, const uint16_t* sc, const uint8_t* zr,
-                          uint16_t* out, int N, int K, int G, hipStream_t st);
+// The kernels that read packed codes come in a 4-bit (_w4) and a 3-bit (_w3)
+// build of spear_kernels.hip; the others only in the 4-bit one.
+#define SPEAR_WEIGHT_LAUNCHERS(W)                                                                 \
+  hipError_t launch_dequant_##W(int dt, const uint32_t* qw, const uint16_t* sc,                 \
+                                const uint8_t* zr, uint16_t* out, int N, int K, int G,          \
+                                hipStream_t st);                                                \
+  hipError_t launch_gemv_##W(int dt, int MT, int RT, int epi, const GemvParams& p, int grid,    \
+                             int block, size_t lds, hipStream_t st);                            \
+  hipError_t launch_gemv_group_##W(int dt, int MT, int RT, int epi, const GemvGroup& g,         \
+                                   int block, size_t lds, hipStream_t st);                      \
+  hipError_t launch_gemm_##W(int dt, int epi, const GemmParams& p, hipStream_t st);
+SPEAR_WEIGHT_LAUNCHERS(w4)
+SPEAR_WEIGHT_LAUNCHERS(w3)
+#undef SPEAR_WEIGHT_LAUNCHERS
 hipError_t launch_ec(int dt, const EcParams& e, int grid, int block, int ipp, size_t lds,
                      hipStream_t st);
 bool gemv_shape_supported(int MT, int RT);
-hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, int block,
-                       size_t lds, hipStream_t st);
-hipError_t launch_gemv_group(int dt, int MT, int RT, int epi, const GemvGroup& g, int block,
-                             size_t lds, hipStream_t st);
-hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st);
 hipError_t launch_gate(int dt, const EcParams& e, int ntb, size_t lds, hipStream_t st);
 // y_norm[m] = RMSNorm(y[m]) * w (one workgroup per token row)
 hipError_t launch_rmsnorm(int dt, const uint16_t* y, const uint16_t* w, float eps, uint16_t* y_norm,

@@ -29,6 +29,18 @@
 
 #include "spear_internal.h"
 
+// This translation unit's weight-code width: the kernels that read the
+// packed codes are instantiated for SPEAR_WB (4 or 3) and their launchers
+// carry it in their names (launch_gemv_w4, launch_gemv_w3, ...); the build
+// compiles this file once per width. Kernels that do not read the codes are
+// compiled with the 4-bit unit only.
+#ifndef SPEAR_WB
+#define SPEAR_WB 4
+#endif
+#define SPEAR_CAT2(a, b) a##b
+#define SPEAR_CAT(a, b) SPEAR_CAT2(a, b)
+#define SPEAR_W(name) SPEAR_CAT(name, SPEAR_CAT(_w, SPEAR_WB))
+
 namespace spear {
 
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
@@ -37,6 +49,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
 
 // ---------------------------------------------------------------------------
 // small helpers
@@ -95,6 +108,30 @@ __device__ __forceinline__ u32x4 unpack_biased_r(uint32_t w, uint32_t km, uint32
   r[3] = ((w >> 12) & km) | kg;
   return r;
 }
+// 3-bit codes: a block of 32 codes c_0..c_31 in three words (w[0], w[1]:
+// two-bit low fields, c_{2i} in bits 2i..2i+1 and c_{2i+1} in bits
+// 16+2i..17+2i of w[0] for i < 8, of w[1] for i >= 8; w[2]: the high bits,
+// c_{2i} at bit i and c_{2i+1} at bit 16+i). Pair p = (c_{2p}, c_{2p+1}),
+// in natural K order, as two 16-bit lanes; `kg` = 0 gives the codes
+// themselves, the magic pair (above) the biased act-dtype values.
+__device__ __forceinline__ uint32_t w3_pair(const u32x4& w, int p, uint32_t kg) {
+  const uint32_t lo = p < 8 ? w[0] : w[1];
+  const uint32_t l = (lo >> (2 * (p & 7))) & 0x00030003u;
+  const uint32_t h = (p >= 2 ? (w[2] >> (p - 2)) : (w[2] << (2 - p))) & 0x00040004u;
+  return l | h | kg;
+}
+// MFMA operand jj (codes 8 jj .. 8 jj + 7 of the block, natural order) as
+// biased act-dtype values
+__device__ __forceinline__ u32x4 unpack3_biased(const u32x4& w, int jj, uint32_t kg) {
+  return u32x4{w3_pair(w, 4 * jj, kg), w3_pair(w, 4 * jj + 1, kg), w3_pair(w, 4 * jj + 2, kg),
+               w3_pair(w, 4 * jj + 3, kg)};
+}
+// Bytes of one row of packed codes.
+template <int WB>
+__host__ __device__ __forceinline__ uint32_t row_code_bytes(int K) {
+  return WB == 4 ? (uint32_t)K / 2 : (uint32_t)K / 8 * 3;
+}
+
 // Opaque copy of a constant in a VGPR (the compiler cannot fold it back into
 // an instruction literal).
 __device__ __forceinline__ uint32_t opaque_v(uint32_t c) {
@@ -181,6 +218,11 @@ __device__ __forceinline__ u32x4 bld128(rsrc_t r, uint32_t off) {
 // voffset (per lane, carries the mask) + soffset (wave-uniform)
 __device__ __forceinline__ u32x4 bld128s(rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+// 12 bytes (one block of 3-bit codes) into the first three lanes of a u32x4
+__device__ __forceinline__ u32x4 bld96s(rsrc_t r, uint32_t voff, uint32_t soff) {
+  const u32x3 v = __builtin_amdgcn_raw_buffer_load_b96(r, voff, soff, 0);
+  return u32x4{v[0], v[1], v[2], 0u};
 }
 __device__ __forceinline__ uint32_t bld16s(rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
@@ -960,7 +1002,7 @@ __device__ void ec_wave(const GemvParams& a, uint32_t gen, char* smem, int n0, b
 // Fused variant: the first n_prod blocks of the grid are EC producers; the
 // others' EC waves wait for what they publish.
 // ---------------------------------------------------------------------------
-template <int DT, int MT, int RT, int EPI>
+template <int DT, int MT, int RT, int EPI, int WB>
 __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t gen, char* smem) {
   __shared__ int s_flag;
   constexpr bool kEC = EPI == EPI_READY || EPI == EPI_FUSED;  // with an EC wave
@@ -982,7 +1024,7 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   const int iw_end = gw ? min(it_end, iw_beg + a.iw) : 0;
   const int r = a.r;
 
-  const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * (K / 2));
+  const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * row_code_bytes<WB>(K));
   const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
   const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
   const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
@@ -1032,7 +1074,9 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
 #pragma unroll
   for (int t = 0; t < RT; ++t) {
     const int n = n0 + 16 * t + lr;
-    vw[t] = n < N ? (uint32_t)n * (K / 2) + 16 * lg : kOOB;
+    // lane group lg: the codes of K [32 lg, 32 lg + 32) of each iteration
+    // (4-bit: 16 bytes, 3-bit: one block of 12)
+    vw[t] = n < N ? (uint32_t)n * row_code_bytes<WB>(K) + (WB == 4 ? 16 : 12) * lg : kOOB;
   }
   const bool xl = a.xlds;
   const char* xs = smem;
@@ -1043,7 +1087,9 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   }
   auto load_w = [&](u32x4 (&w)[RT], int it) {
 #pragma unroll
-    for (int t = 0; t < RT; ++t) w[t] = bld128s(rq, vw[t], (uint32_t)it * (kIterK / 2));
+    for (int t = 0; t < RT; ++t)
+      w[t] = WB == 4 ? bld128s(rq, vw[t], (uint32_t)it * (kIterK / 2))
+                     : bld96s(rq, vw[t], (uint32_t)it * (kIterK / 8 * 3));
   };
   // EPI_LOCAL: the block's K-slice of A (16 rows, rows >= r zero) and of
   // w_g (row 16) is staged in LDS with coalesced 16-byte chunks: read in the
@@ -1307,7 +1353,9 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
         xb[mt] = mfma16<DT>(xv[mt][jj], ones8<DT>(), xb[mt]);
-        xp[mt][jj] = pair_like_codes(xv[mt][jj]);
+        // 4-bit codes pair (q_i, q_{i+4}) within a word: the activations
+        // follow; 3-bit pairs are in natural order
+        xp[mt][jj] = WB == 4 ? pair_like_codes(xv[mt][jj]) : xv[mt][jj];
       }
     }
     const int gg = it / ipg - g_lo;
@@ -1315,7 +1363,8 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
     for (int t = 0; t < RT; ++t) {
       u32x4 wd[4];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) wd[jj] = unpack_biased_r(w[t][jj], km, kg);
+      for (int jj = 0; jj < 4; ++jj)
+        wd[jj] = WB == 4 ? unpack_biased_r(w[t][jj], km, kg) : unpack3_biased(w[t], jj, kg);
       const uint32_t sz = szs[(16 * t + lr) * ngs + gg];
       const float sf = h2f((uint16_t)(sz & 0xFFFF));
       const float cf = kBias + (float)(sz >> 16);
@@ -1532,7 +1581,7 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   if constexpr (EPI == EPI_FUSED) fused_exit(a);
 }
 
-template <int DT, int MT, int RT, int EPI>
+template <int DT, int MT, int RT, int EPI, int WB>
 __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int bid = blockIdx.x;
@@ -1547,14 +1596,14 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
     }
     bid -= a.n_prod;
   }
-  gemv_body<DT, MT, RT, EPI>(a, bid, gen, smem);
+  gemv_body<DT, MT, RT, EPI, WB>(a, bid, gen, smem);
 }
 
 // Several independent layer calls of one GEMV variant in one launch: member i
 // owns the workgroups [start[i], start[i+1]) and runs exactly the blocks its
 // own launch would run, so each member's output is the one its single call
 // writes. The member index is uniform over the workgroup.
-template <int DT, int MT, int RT, int EPI>
+template <int DT, int MT, int RT, int EPI, int WB>
 __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv_group(GemvGroup g) {
   static_assert(EPI == EPI_NONE || EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8,
                 "grouped launches take the variants without cross-launch state");
@@ -1564,7 +1613,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv_group(GemvGroup g) {
 #pragma unroll
   for (int j = 1; j < kGroupMax; ++j)
     if (j < g.n && b >= g.start[j]) i = j;
-  gemv_body<DT, MT, RT, EPI>(g.p[i], b - g.start[i], 0u, smem);
+  gemv_body<DT, MT, RT, EPI, WB>(g.p[i], b - g.start[i], 0u, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -1573,29 +1622,26 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv_group(GemvGroup g) {
 // per block into the LDS tile, (q - z) exact then times s with one rounding
 // (fp16) or via fp32 (bf16). Four waves, 2x2, each 64x64 = 4x4 MFMA tiles.
 // ---------------------------------------------------------------------------
-template <int DT>
-__device__ __forceinline__ void dequant_word_pairs(uint32_t w, float s, int z, uint32_t out[4]) {
-  // natural order pairs (q0,q1), (q2,q3), (q4,q5), (q6,q7)
-  const uint32_t lo = w & 0x0F0F0F0Fu;         // q0 q2 q4 q6
-  const uint32_t hi = (w >> 4) & 0x0F0F0F0Fu;  // q1 q3 q5 q7
-  uint32_t p[4];
-  p[0] = __builtin_amdgcn_perm(hi, lo, 0x0C040C00u);
-  p[1] = __builtin_amdgcn_perm(hi, lo, 0x0C050C01u);
-  p[2] = __builtin_amdgcn_perm(hi, lo, 0x0C060C02u);
-  p[3] = __builtin_amdgcn_perm(hi, lo, 0x0C070C03u);
+// NP pairs of raw codes (natural K order, one code per 16-bit lane) to
+// dequantised act-dtype pairs: (q - z) exact, then one rounding of its
+// product with s (fp16: the biased code minus 1024 + z, an exact integer, in
+// packed half math; bf16: in fp32, then rounded).
+template <int DT, int NP>
+__device__ __forceinline__ void dequant_pairs(const uint32_t (&p)[NP], float s, int z,
+                                              uint32_t (&out)[NP]) {
   if constexpr (DT == DT_F16) {
     const _Float16 zb = (_Float16)(1024 + z);
     const f16x2 nz = f16x2{-zb, -zb};
     const f16x2 s2 = f16x2{(_Float16)s, (_Float16)s};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NP; ++i) {
       const f16x2 q = __builtin_bit_cast(f16x2, p[i] | 0x64006400u);
       out[i] = __builtin_bit_cast(uint32_t, (q + nz) * s2);
     }
   } else {
     const float zf = (float)z;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NP; ++i) {
       const float a0 = ((float)(p[i] & 0xFFFF) - zf) * s;
       const float a1 = ((float)(p[i] >> 16) - zf) * s;
       out[i] = (uint32_t)f2act<DT>(a0) | ((uint32_t)f2act<DT>(a1) << 16);
@@ -1603,27 +1649,66 @@ __device__ __forceinline__ void dequant_word_pairs(uint32_t w, float s, int z, u
   }
 }
 
-// ---------------------------------------------------------------------------
-// Dequantisation diagnostic: one thread per packed word, eight outputs, by
-// dequant_word_pairs, the code the prefill GEMM dequantises its weight tiles
-// with: (q - z) exact, then one rounding of its product with s.
-// ---------------------------------------------------------------------------
+// One packed word of 4-bit codes, dequantised in natural order: pairs
+// (q0,q1), (q2,q3), (q4,q5), (q6,q7).
 template <int DT>
+__device__ __forceinline__ void dequant_word_pairs(uint32_t w, float s, int z, uint32_t (&out)[4]) {
+  const uint32_t lo = w & 0x0F0F0F0Fu;         // q0 q2 q4 q6
+  const uint32_t hi = (w >> 4) & 0x0F0F0F0Fu;  // q1 q3 q5 q7
+  uint32_t p[4];
+  p[0] = __builtin_amdgcn_perm(hi, lo, 0x0C040C00u);
+  p[1] = __builtin_amdgcn_perm(hi, lo, 0x0C050C01u);
+  p[2] = __builtin_amdgcn_perm(hi, lo, 0x0C060C02u);
+  p[3] = __builtin_amdgcn_perm(hi, lo, 0x0C070C03u);
+  dequant_pairs<DT, 4>(p, s, z, out);
+}
+
+// Pairs P0 .. P0 + NP - 1 of a block of 3-bit codes (three words in w),
+// dequantised in natural order.
+template <int DT, int P0, int NP>
+__device__ __forceinline__ void dequant_block3_pairs(const u32x4& w, float s, int z,
+                                                     uint32_t (&out)[NP]) {
+  uint32_t p[NP];
+#pragma unroll
+  for (int i = 0; i < NP; ++i) p[i] = w3_pair(w, P0 + i, 0u);
+  dequant_pairs<DT, NP>(p, s, z, out);
+}
+
+// ---------------------------------------------------------------------------
+// Dequantisation diagnostic, by the code the prefill GEMM dequantises its
+// weight tiles with ((q - z) exact, then one rounding of its product with s):
+// one thread per packed word of 4-bit codes (eight outputs), or per block of
+// 3-bit codes (three words, 32 outputs).
+// ---------------------------------------------------------------------------
+template <int DT, int WB>
 __global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ qw,
                                                  const uint16_t* __restrict__ sc,
                                                  const uint8_t* __restrict__ zr,
                                                  uint16_t* __restrict__ out, int N, int K, int G) {
-  const int kw = K >> 3;
-  const long long nwords = (long long)N * kw;
+  constexpr int CPU = WB == 4 ? 8 : 32;  // codes per unit (word or block)
+  const int kw = K / CPU;
+  const long long nunits = (long long)N * kw;
   const long long wi = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (wi >= nwords) return;
+  if (wi >= nunits) return;
   const int n = (int)(wi / kw);
-  const int k = (int)(wi % kw) * 8;
+  const int k = (int)(wi % kw) * CPU;
   const int ng = K / G;
   const int g = k / G;
-  uint32_t o[4];
-  dequant_word_pairs<DT>(qw[wi], h2f(sc[(long long)n * ng + g]), zr[(long long)n * ng + g], o);
-  *(u32x4*)(out + (long long)n * K + k) = u32x4{o[0], o[1], o[2], o[3]};
+  const float s = h2f(sc[(long long)n * ng + g]);
+  const int z = zr[(long long)n * ng + g];
+  if constexpr (WB == 4) {
+    uint32_t o[4];
+    dequant_word_pairs<DT>(qw[wi], s, z, o);
+    *(u32x4*)(out + (long long)n * K + k) = u32x4{o[0], o[1], o[2], o[3]};
+  } else {
+    const uint32_t* b = qw + 3 * wi;
+    const u32x4 w = u32x4{b[0], b[1], b[2], 0u};
+    uint32_t o[16];
+    dequant_block3_pairs<DT, 0, 16>(w, s, z, o);
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      *(u32x4*)(out + (long long)n * K + k + 8 * c) = u32x4{o[4 * c], o[4 * c + 1], o[4 * c + 2], o[4 * c + 3]};
+  }
 }
 
 // Split-K tile reduction of the GEMM: a thread's 16 f32x4 of the tile from
@@ -1679,7 +1764,7 @@ __device__ __forceinline__ void gemm_sum_ec_slices(rsrc_t rp, uint32_t base, uin
 // CU. Both keep 64 x 64 per wave and two waves per SIMD; the 256-token tile
 // reuses each dequantised weight tile for twice the MFMAs, halving the
 // dequantisation's VALU work per MFMA.
-template <int DT, int EPI, int TMW>
+template <int DT, int EPI, int TMW, int WB>
 __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr bool kLoc = EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8;
@@ -1730,7 +1815,7 @@ __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams
 
   // per-thread global load assignments (bounds-checked buffer loads)
   const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
-  const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * (K / 2));
+  const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * row_code_bytes<WB>(K));
   const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
   const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
   int xr[4], xc[4];
@@ -1742,11 +1827,15 @@ __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams
     xc[i] = (c & 7) * 8;
     xoff[i] = m0 + xr[i] < M ? ((uint32_t)(m0 + xr[i]) * K + xc[i]) * 2 : kOOB;
   }
-  // codes: row wr, words [wp WPT, +WPT) of the row's 64-wide step
+  // codes: row wr, K [8 WPT wp, +8 WPT) of the row's 64-wide step: 4-bit
+  // words [wp WPT, +WPT); 3-bit: block wp (WPT = 4) or half wp % 2 of block
+  // wp / 2 (WPT = 2), whose three words are loaded whole
   const int wr = tid / WPR, wp = tid % WPR;
   const int wn_row = n0 + wr;
   const bool wok = wn_row < N;
-  const uint32_t woff = wok ? (uint32_t)wn_row * (K / 2) + 4 * WPT * wp : kOOB;
+  const uint32_t woff = !wok      ? kOOB
+                        : WB == 4 ? (uint32_t)wn_row * (K / 2) + 4 * WPT * wp
+                                  : (uint32_t)wn_row * row_code_bytes<WB>(K) + 12 * (WPT == 4 ? wp : wp >> 1);
   // EPI_LOCAL: thread t < 136 stages 16 bytes of the EC tile per step: row
   // t / 8 (A's row while below r, zero up to 15; w_g as row 16), chunk t % 8
   const int er = tid >> 3, ec8 = tid & 7;
@@ -1781,7 +1870,9 @@ __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams
     const uint32_t k0 = (uint32_t)(kbase + kt) * kGemmTK;
 #pragma unroll
     for (int i = 0; i < 4; ++i) st.x[i] = bld128(rx, xoff[i] + k0 * 2);
-    if constexpr (WPT == 4) {
+    if constexpr (WB == 3) {
+      st.w = bld96s(rq, woff, k0 / 8 * 3);
+    } else if constexpr (WPT == 4) {
       st.w = bld128(rq, woff + k0 / 2);
     } else {
       const u32x2 q = bld64(rq, woff + k0 / 2);
@@ -1808,11 +1899,27 @@ __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams
     uint16_t* ws = Ws + buf * TILEW;
 #pragma unroll
     for (int i = 0; i < 4; ++i) *(u32x4*)(xs + xr[i] * LR + xc[i]) = xreg[i];
+    if constexpr (WB == 4) {
 #pragma unroll
-    for (int c = 0; c < WPT; ++c) {
-      uint32_t o[4];
-      dequant_word_pairs<DT>(wreg[c], sreg, zreg, o);
-      *(u32x4*)(ws + wr * LR + 8 * (WPT * wp + c)) = u32x4{o[0], o[1], o[2], o[3]};
+      for (int c = 0; c < WPT; ++c) {
+        uint32_t o[4];
+        dequant_word_pairs<DT>(wreg[c], sreg, zreg, o);
+        *(u32x4*)(ws + wr * LR + 8 * (WPT * wp + c)) = u32x4{o[0], o[1], o[2], o[3]};
+      }
+    } else {
+      uint32_t o[4 * WPT];
+      if constexpr (WPT == 4) {
+        dequant_block3_pairs<DT, 0, 16>(wreg, sreg, zreg, o);
+      } else {
+        // half 1 of the block: its low fields are word 1, its high bits the
+        // upper byte of each half of word 2 (moved down: no branch per lane)
+        const bool h1 = (wp & 1) != 0;
+        const u32x4 wh = u32x4{h1 ? wreg[1] : wreg[0], 0u, h1 ? wreg[2] >> 8 : wreg[2], 0u};
+        dequant_block3_pairs<DT, 0, 8>(wh, sreg, zreg, o);
+      }
+#pragma unroll
+      for (int c = 0; c < WPT; ++c)
+        *(u32x4*)(ws + wr * LR + 8 * (WPT * wp + c)) = u32x4{o[4 * c], o[4 * c + 1], o[4 * c + 2], o[4 * c + 3]};
     }
     if constexpr (kLoc) {
       u32x4 ev = st.e;
@@ -2058,15 +2165,17 @@ static hipError_t allow_lds(F* fn, size_t lds) {
     }                                     \
   } while (0)
 
-hipError_t launch_dequant(int dt, const uint32_t* qw, const uint16_t* sc, const uint8_t* zr,
-                          uint16_t* out, int N, int K, int G, hipStream_t st) {
-  const long long nwords = (long long)N * (K / 8);
-  const unsigned grid = (unsigned)((nwords + 255) / 256);
+hipError_t SPEAR_W(launch_dequant)(int dt, const uint32_t* qw, const uint16_t* sc, const uint8_t* zr,
+                                   uint16_t* out, int N, int K, int G, hipStream_t st) {
+  const long long nunits = (long long)N * (K / (SPEAR_WB == 4 ? 8 : 32));
+  const unsigned grid = (unsigned)((nunits + 255) / 256);
   if (grid == 0) return hipSuccess;
-  SPEAR_DT_SWITCH(dt, hipLaunchKernelGGL(k_dequant<DTC>, dim3(grid), dim3(256), 0, st, qw, sc, zr,
-                                         out, N, K, G));
+  SPEAR_DT_SWITCH(dt, hipLaunchKernelGGL((k_dequant<DTC, SPEAR_WB>), dim3(grid), dim3(256), 0, st,
+                                         qw, sc, zr, out, N, K, G));
   return hipGetLastError();
 }
+
+#if SPEAR_WB == 4
 
 hipError_t launch_ec(int dt, const EcParams& e, int grid, int block, int ipp, size_t lds,
                      hipStream_t st) {
@@ -2113,25 +2222,28 @@ hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, const int
   return hipGetLastError();
 }
 
+#endif  // SPEAR_WB == 4
+
 template <int DT, int MT, int RT>
 static hipError_t gemv_launch(int epi, const GemvParams& p, int grid, int block, size_t lds,
                               hipStream_t st) {
-  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, EPI_NONE>, lds)
-                   : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, EPI_READY>, lds)
-                   : epi == EPI_FUSED ? allow_lds(k_gemv<DT, MT, RT, EPI_FUSED>, lds)
-                   : epi == EPI_LOCAL ? allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL>, lds)
-                                      : allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL_I8>, lds);
+  constexpr int WB = SPEAR_WB;
+  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, EPI_NONE, WB>, lds)
+                   : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, EPI_READY, WB>, lds)
+                   : epi == EPI_FUSED ? allow_lds(k_gemv<DT, MT, RT, EPI_FUSED, WB>, lds)
+                   : epi == EPI_LOCAL ? allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL, WB>, lds)
+                                      : allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL_I8, WB>, lds);
   if (err != hipSuccess) return err;
   if (epi == EPI_NONE)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_NONE>), dim3(grid), dim3(block), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_NONE, WB>), dim3(grid), dim3(block), lds, st, p);
   else if (epi == EPI_READY)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_READY>), dim3(grid), dim3(block), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_READY, WB>), dim3(grid), dim3(block), lds, st, p);
   else if (epi == EPI_FUSED)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_FUSED>), dim3(grid), dim3(block), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_FUSED, WB>), dim3(grid), dim3(block), lds, st, p);
   else if (epi == EPI_LOCAL)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL>), dim3(grid), dim3(block), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL, WB>), dim3(grid), dim3(block), lds, st, p);
   else
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL_I8>), dim3(grid), dim3(block), lds, st, p);
+    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL_I8, WB>), dim3(grid), dim3(block), lds, st, p);
   return hipGetLastError();
 }
 
@@ -2140,15 +2252,17 @@ static hipError_t gemv_launch(int epi, const GemvParams& p, int grid, int block,
 #define SPEAR_GEMV_SHAPES(X) \
   X(1, 1) X(1, 2) X(1, 4) X(2, 1) X(2, 2) X(2, 4) X(3, 1) X(3, 2) X(4, 1)
 
+#if SPEAR_WB == 4
 bool gemv_shape_supported(int MT, int RT) {
 #define SPEAR_GEMV_MATCH(mt, rt) if (MT == mt && RT == rt) return true;
   SPEAR_GEMV_SHAPES(SPEAR_GEMV_MATCH)
 #undef SPEAR_GEMV_MATCH
   return false;
 }
+#endif
 
-hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int grid, int block,
-                       size_t lds, hipStream_t st) {
+hipError_t SPEAR_W(launch_gemv)(int dt, int MT, int RT, int epi, const GemvParams& p, int grid,
+                                int block, size_t lds, hipStream_t st) {
   // split-K needs its partial sums and row-group counters (workspace)
   const bool loc = epi == EPI_LOCAL || epi == EPI_LOCAL_I8;
   if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.rb_ctr || (loc && !p.eupart))) ||
@@ -2167,23 +2281,24 @@ hipError_t launch_gemv(int dt, int MT, int RT, int epi, const GemvParams& p, int
 template <int DT, int MT, int RT>
 static hipError_t gemv_group_launch(int epi, const GemvGroup& g, int block, size_t lds,
                                     hipStream_t st) {
+  constexpr int WB = SPEAR_WB;
   const int grid = g.start[g.n];
-  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv_group<DT, MT, RT, EPI_NONE>, lds)
-                   : epi == EPI_LOCAL ? allow_lds(k_gemv_group<DT, MT, RT, EPI_LOCAL>, lds)
-                                      : allow_lds(k_gemv_group<DT, MT, RT, EPI_LOCAL_I8>, lds);
+  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv_group<DT, MT, RT, EPI_NONE, WB>, lds)
+                   : epi == EPI_LOCAL ? allow_lds(k_gemv_group<DT, MT, RT, EPI_LOCAL, WB>, lds)
+                                      : allow_lds(k_gemv_group<DT, MT, RT, EPI_LOCAL_I8, WB>, lds);
   if (err != hipSuccess) return err;
   if (epi == EPI_NONE)
-    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_NONE>), dim3(grid), dim3(block), lds, st, g);
+    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_NONE, WB>), dim3(grid), dim3(block), lds, st, g);
   else if (epi == EPI_LOCAL)
-    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_LOCAL>), dim3(grid), dim3(block), lds, st, g);
+    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_LOCAL, WB>), dim3(grid), dim3(block), lds, st, g);
   else
-    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_LOCAL_I8>), dim3(grid), dim3(block), lds, st,
+    hipLaunchKernelGGL((k_gemv_group<DT, MT, RT, EPI_LOCAL_I8, WB>), dim3(grid), dim3(block), lds, st,
                        g);
   return hipGetLastError();
 }
 
-hipError_t launch_gemv_group(int dt, int MT, int RT, int epi, const GemvGroup& g, int block,
-                             size_t lds, hipStream_t st) {
+hipError_t SPEAR_W(launch_gemv_group)(int dt, int MT, int RT, int epi, const GemvGroup& g,
+                                      int block, size_t lds, hipStream_t st) {
   if (g.n < 1 || g.n > kGroupMax || g.start[0] != 0 ||
       (epi != EPI_NONE && epi != EPI_LOCAL && epi != EPI_LOCAL_I8))
     return hipErrorInvalidValue;
@@ -2205,7 +2320,7 @@ hipError_t launch_gemv_group(int dt, int MT, int RT, int epi, const GemvGroup& g
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st) {
+hipError_t SPEAR_W(launch_gemm)(int dt, int epi, const GemmParams& p, hipStream_t st) {
   // split-K needs its partial tiles and tile counters (workspace); the
   // 256-token tile takes the plain and the semi-fused epilogue only
   const bool loc = epi == EPI_LOCAL || epi == EPI_LOCAL_I8;
@@ -2222,9 +2337,9 @@ hipError_t launch_gemm(int dt, int epi, const GemmParams& p, hipStream_t st) {
   if (loc) lds += (size_t)2 * kGemmEcRows * kGemmLdsRow * 2;
 #define SPEAR_GEMM_GO(E, W)                                                            \
   do {                                                                                 \
-    hipError_t err = allow_lds(k_gemm<DTC, E, W>, lds);                                \
+    hipError_t err = allow_lds(k_gemm<DTC, E, W, SPEAR_WB>, lds);                      \
     if (err != hipSuccess) return err;                                                 \
-    hipLaunchKernelGGL((k_gemm<DTC, E, W>), dim3(grid), dim3(128 * W), lds, st, p);    \
+    hipLaunchKernelGGL((k_gemm<DTC, E, W, SPEAR_WB>), dim3(grid), dim3(128 * W), lds, st, p); \
   } while (0)
   SPEAR_DT_SWITCH(dt, {
     if (p.tmw == 4) {

@@ -9,11 +9,12 @@ from __future__ import annotations
 RANK, GROUP = 64, 128
 
 
-def build(device="cuda", seed=0, layers=None):
+def build(device="cuda", seed=0, layers=None, weight_bits=4):
     """Returns (modules, selection): modules[l][j] = (name, K, N, qweight
-    int32 [N][K/8], scales fp16 bits as int16 [N][K/128], zeros uint8
-    [N][K/128], ec) with ec = (A [64][K], B [N][64], w_g [K]) fp16 on the
-    selected pairs, else None; selection is the bool [80][7] EC choice."""
+    int32 [N][K/8] (3-bit codes: [N][3K/32]), scales fp16 bits as int16
+    [N][K/128], zeros uint8 [N][K/128], ec) with ec = (A [64][K], B [N][64],
+    w_g [K]) fp16 on the selected pairs, else None; selection is the bool
+    [80][7] EC choice."""
     import torch
 
     from paper_2606_11244_amd import synth as S
@@ -26,10 +27,11 @@ def build(device="cuda", seed=0, layers=None):
         mods = []
         for j, m in enumerate(S.MODULES):
             K, N = S.LLAMA_70B[m]
-            q = torch.randint(-2**31, 2**31 - 1, (N, K // 8), dtype=torch.int32, device=device,
-                              generator=g)
+            q = torch.randint(-2**31, 2**31 - 1, (N, K // 8 if weight_bits == 4 else K // 32 * 3),
+                              dtype=torch.int32, device=device, generator=g)
             sc = (torch.rand((N, K // GROUP), device=device, generator=g) * 1e-3 + 1e-4).half()
-            zr = torch.randint(0, 16, (N, K // GROUP), dtype=torch.uint8, device=device, generator=g)
+            zr = torch.randint(0, 1 << weight_bits, (N, K // GROUP), dtype=torch.uint8,
+                               device=device, generator=g)
             ec = None
             if sel[l, j]:
                 ec = ((torch.randn((RANK, K), device=device, generator=g) * 0.01).half(),

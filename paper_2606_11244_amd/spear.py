@@ -41,7 +41,8 @@ class Problem(ctypes.Structure):
     _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
                 ("group_size", ctypes.c_int32), ("act_dtype", ctypes.c_int32),
                 ("rank", ctypes.c_int32), ("gate_kind", ctypes.c_int32),
-                ("gate_hidden", ctypes.c_int32), ("force_path", ctypes.c_int32)]
+                ("gate_hidden", ctypes.c_int32), ("force_path", ctypes.c_int32),
+                ("weight_bits", ctypes.c_int32)]
 
 
 class W4(ctypes.Structure):
@@ -167,9 +168,9 @@ def _stream(stream):
 
 
 def problem(M, N, K, group_size=0, act_dtype=F16, rank=0, gate_kind=GATE_SIGMOID_LINEAR,
-            gate_hidden=0, force_path=PATH_AUTO) -> Problem:
+            gate_hidden=0, force_path=PATH_AUTO, weight_bits=0) -> Problem:
     return Problem(int(M), int(N), int(K), int(group_size), int(act_dtype), int(rank),
-                   int(gate_kind), int(gate_hidden), int(force_path))
+                   int(gate_kind), int(gate_hidden), int(force_path), int(weight_bits))
 
 
 def dispatch_plan(prob: Problem, with_ec: bool = True) -> Plan:
@@ -455,7 +456,8 @@ class DeviceLayer:
         return problem(L.M, L.N, L.K, L.group_size, L.act_dtype,
                        L.rank if rank is None else rank,
                        L.gate_kind if gate_kind is None else gate_kind,
-                       L.gate_hidden if L.rank > 0 else 0, force_path)
+                       L.gate_hidden if L.rank > 0 else 0, force_path,
+                       getattr(L, "weight_bits", 4))
 
     def run_ec(self, prob, workspace, stream=None, y=None):
         L = self.layer

@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_version_and_status_strings():
-    assert sp.version() == "0.1.0"
+    assert sp.version() == "0.2.0"
     for code in sp.STATUS:
         assert sp.LIB.spear_status_string(code)
     assert sp.LIB.spear_status_string(12345) == b"unknown status"
@@ -346,3 +346,30 @@ def test_tagged_region_is_written_by_the_fused_path_only():
                             else:
                                 assert (db, de) == (0, 0)
     assert n_fused > 100
+
+
+def test_weight_code_width():
+    """3-bit codes (weight_bits = 3) take the same plan as 4-bit ones; any
+    other width is rejected; the alias checks cover the 3-bit codes' own
+    extent (3K/8 bytes per row)."""
+    for M, N, K, G in ((1, 2048, 2048, 128), (16, 8192, 2048, 128), (4096, 4096, 4096, 0),
+                       (64, 28672, 8192, 128)):
+        for r in (0, 16, 64):
+            p4 = sp.dispatch_plan(sp.problem(M, N, K, G, sp.F16, r))
+            p3 = sp.dispatch_plan(sp.problem(M, N, K, G, sp.F16, r, weight_bits=3))
+            assert (p3.path, p3.split_k, p3.tile_m, p3.tile_n, p3.grid, p3.workspace_bytes) == \
+                (p4.path, p4.split_k, p4.tile_m, p4.tile_n, p4.grid, p4.workspace_bytes)
+    for bad in (1, 2, 5, 8, -1):
+        with pytest.raises(sp.SpearError) as e:
+            sp.dispatch_plan(sp.problem(4, 256, 256, 0, sp.F16, 8, weight_bits=bad))
+        assert e.value.status == -3
+    prob = sp.problem(4, 256, 256, 0, sp.F16, 8, weight_bits=3)
+    full = dict(x=ADDR["x"], y=ADDR["y"], q=ADDR["q"], s=ADDR["s"], z=ADDR["z"], A=ADDR["A"],
+                B=ADDR["B"], w_g=ADDR["w"], ws=ADDR["W"], ws_bytes=1 << 30)
+    args = dict(full)
+    args["y"] = ADDR["q"] + 256 * 256 * 3 // 8 - 16  # the last 16 bytes of the 3-bit codes
+    assert _call_ec(prob, **args) == -8
+    dq = sp.problem(0, 256, 256, 0, sp.F16, weight_bits=3)
+    w = sp.W4(ADDR["q"], ADDR["s"], ADDR["z"])
+    assert sp.LIB.spear_w4_dequant(ctypes.byref(dq), ctypes.byref(w),
+                                   ADDR["q"] + 256 * 256 * 3 // 8 - 16, None) == -8
