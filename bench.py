@@ -474,6 +474,55 @@ def llama1b_extras(args, sp, S, np, torch, dev):
     # ---- the same EC passes with the post-EC tail where a decoder layer has
     # it: after o and down, the residual added in place and the next
     # RMSNorm (the other modules unchanged)
+    # ---- the paper's own gate (tanh-MLP on u = A x, Eq. 3) on the same
+    # passes, each module on its AUTO path (one call per module at decode)
+    tanh = None
+    if not args.no_tanh:
+        print("bench: tanh-MLP gate passes", file=sys.stderr, flush=True)
+
+        need = max([sp.dispatch_plan(d.problem(gate_kind=S.GATE_TANH_MLP)).workspace_bytes
+                    for d in base_dev + pre_dev])
+        tanh_ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=dev)
+
+        def decode_tanh(c):
+            for mods in dec_dev[c]:
+                for d in mods:
+                    d.run_ec(d.problem(gate_kind=S.GATE_TANH_MLP), tanh_ws)
+
+        def prefill_tanh():
+            for d in pre_dev:
+                d.run_ec(d.problem(gate_kind=S.GATE_TANH_MLP), tanh_ws)
+
+        def decode_sig_single(c):
+            for mods in dec_dev[c]:
+                for d in mods:
+                    d.run_ec(d.problem(), dec_ws_t)
+
+        g_dt = [capture(lambda c=c: decode_tanh(c)) for c in range(args.copies)]
+        g_ds = [capture(lambda c=c: decode_sig_single(c)) for c in range(args.copies)]
+        g_pt = capture(prefill_tanh)
+        run_steps(args.warmup, g_dt, g_pt, False)
+        evt = run_steps(args.steps, g_dt, g_pt, True)
+        evs = run_steps(args.steps, g_ds, g_pre, True)
+        torch.cuda.synchronize()
+        dt_ = float(np.median([a.elapsed_time(b) for a, b, _ in evt])) * 1e-3
+        pt_ = float(np.median([b.elapsed_time(c) for _, b, c in evt])) * 1e-3
+        ds_ = float(np.median([a.elapsed_time(b) for a, b, _ in evs])) * 1e-3
+        tanh = {"gate": "tanh-MLP, h = 4r = 64 (Eq. 3), fp16 parameters",
+                "decode_paths": sorted({sp.PATH_NAMES[sp.dispatch_plan(
+                    d.problem(gate_kind=S.GATE_TANH_MLP)).path] for d in base_dev}),
+                "prefill_paths": sorted({sp.PATH_NAMES[sp.dispatch_plan(
+                    d.problem(gate_kind=S.GATE_TANH_MLP)).path] for d in pre_dev}),
+                "decode_ms_per_pass": round(dt_ * 1e3, 4),
+                "decode_sigmoid_same_calls_ms": round(ds_ * 1e3, 4),
+                "prefill_ms_per_pass": round(pt_ * 1e3, 4),
+                "decode_vs_sigmoid": round(dt_ / ds_ - 1.0, 4),
+                "prefill_vs_sigmoid": round(pt_ / pre_s - 1.0, 4)}
+        if overhead is not None:
+            tanh["decode_overhead_vs_w4"] = round(dt_ / d4 - 1.0, 4)
+            tanh["prefill_overhead_vs_w4"] = round(pt_ / p4 - 1.0, 4)
+        del g_dt, g_ds, g_pt
+
     tail = None
     if not args.no_tail:
         print("bench: post-EC tail passes", file=sys.stderr, flush=True)
@@ -540,6 +589,7 @@ def llama1b_extras(args, sp, S, np, torch, dev):
         "ec_overhead": overhead,
         "ec_int8": int8,
         "post_ec_tail": tail,
+        "tanh_gate": tanh,
     }
 
 
@@ -563,6 +613,8 @@ def main():
                     help="1B: skip the decode pass with one call per module")
     ap.add_argument("--no-tail", action="store_true",
                     help="1B: skip the passes with the post-EC tail on o and down")
+    ap.add_argument("--no-tanh", action="store_true",
+                    help="1B: skip the passes with the paper's tanh-MLP gate")
     ap.add_argument("--model70b", action="store_true",
                     help="also time the 70B-shaped model's pass at M = 1, 16, 64, 512, 8192")
     ap.add_argument("--copy-calib-mb", type=int, default=0,

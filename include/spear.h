@@ -97,8 +97,8 @@ enum {
                                     over K with the product when the tile grid
                                     is small), and its epilogue applies the
                                     gate and adds B (g (.) A x); rank <= 16,
-                                    sigmoid-linear or identity gate (else
-                                    SPEAR_E_UNSUPPORTED). AUTO picks it for
+                                    every gate (else SPEAR_E_UNSUPPORTED).
+                                    AUTO picks it for
                                     M > 32 while the grid has at most 256
                                     128 x 128 tiles and the GEMM would not
                                     take 256-token tiles                       */
@@ -113,8 +113,8 @@ enum {
                                     also project x on [A; w_g] over their own K
                                     chunks (no EC workgroups, no wait on other
                                     workgroups beyond the split-K reduction);
-                                    rank <= 16, sigmoid-linear or identity
-                                    gate, M <= 32. AUTO picks it where it
+                                    rank <= 16, every gate, M <= 32. AUTO
+                                    picks it where it
                                     applies, otherwise SPEAR_PATH_FUSED_GEMV   */
 };
 
@@ -345,6 +345,13 @@ int32_t spear_set_wait_polls(int32_t polls);
  * planner and the calls return SPEAR_E_UNSUPPORTED. For measurement sweeps
  * only. */
 void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves);
+
+/* Tuning hook for the decode GEMV's pipeline depth, process-wide: stages of
+ * packed codes in flight per wave, 2, 4 or 8 (4 and 8: one token tile, the
+ * 4-bit product alone, the producer-fused and the semi-fused variants; else
+ * the planner and the calls return SPEAR_E_UNSUPPORTED); 0 restores the
+ * planner's choice. For measurement sweeps and tests only. */
+void spear_set_gemv_stages(int32_t stages);
 
 /* Tuning hook for the prefill GEMM's K-slices (1, 2, 4 or 8; each slice an
  * even number of 64-wide K steps, else the planner and the calls return

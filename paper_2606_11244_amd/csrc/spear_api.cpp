@@ -19,7 +19,7 @@ namespace {
 std::atomic<int32_t> g_wait_polls{1 << 16};
 // tuning override of the GEMV shape (0 = automatic): row tiles per block,
 // K-slices per row group, waves per block
-std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0}, g_ov_gt{0};
+std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0}, g_ov_gt{0}, g_ov_nst{0};
 
 // Token counts at or below this run the 4-bit product as a split-K GEMV; above
 // it the LDS-tiled MFMA GEMM. The same bound separates decode (fully fused
@@ -48,6 +48,7 @@ struct Resolved {
   int wb;  // weight code width: 4 or 3
   int dt, gate, G, ngroups, IT, r, R1, R1p, h, vstride;
   int MT, RT, NW, nrg, S, ips, iw;            // GEMV shape
+  int nst;                                    // GEMV stages of codes in flight per wave
   int Sg;                                     // GEMM K-slices
   int gtmw;                                   // GEMM token waves (2: 128-token tiles, 4: 256)
   int ntb, P, eips, PG, tpg, ec_mode, ec_ipp, ec_block, n_prod;  // EC shape
@@ -160,7 +161,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   // each workgroup then reads A once more from L2, which stays cheap while A
   // is one 16-row tile, and no workgroup waits for another.
   int path = p->force_path;
-  bool local_ok = z.ec && z.gate != GATE_TANH && z.r <= 16 && M <= kLocalMaxM;
+  bool local_ok = z.ec && z.r <= 16 && M <= kLocalMaxM;
   if (local_ok) {
     // the block's K-slice of A and w_g is staged in LDS
     const int MT = (int)cdiv(M, 16);
@@ -177,7 +178,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   }
   // the fully fused GEMM: the projection rides on the GEMM's activation
   // tiles (one 16-row tile of A plus w_g), the gate and v B^T in its epilogue
-  const bool mfma_ok = z.ec && z.gate != GATE_TANH && z.r <= 16;
+  const bool mfma_ok = z.ec && z.r <= 16;
   if (z.ec && path == SPEAR_PATH_FUSED_MFMA && !mfma_ok) return SPEAR_E_UNSUPPORTED;
   if (path == SPEAR_PATH_FUSED_GEMV && M > kGemvMaxM) return SPEAR_E_UNSUPPORTED;
   if (z.ec && path == SPEAR_PATH_FUSED_LOCAL && !local_ok) return SPEAR_E_UNSUPPORTED;
@@ -281,6 +282,16 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     z.ips = gemv_ips(z.IT, z.nrg, z.NW, waves, fused1 ? kFusedCapIw : 0);
     z.S = (int)cdiv(z.IT, z.ips);
     z.iw = (int)cdiv(z.ips, z.NW);
+    z.nst = 2;
+    if (g_ov_nst.load() > 0) {
+      // deeper pipelines: one token tile, the 4-bit-only, fused and
+      // semi-fused variants
+      const int n = g_ov_nst.load();
+      if ((n != 2 && n != 4 && n != 8) ||
+          (n != 2 && (z.MT != 1 || epi == EPI_LOCAL)))
+        return SPEAR_E_UNSUPPORTED;
+      z.nst = n;
+    }
     z.plan.split_k = z.S;
     z.plan.tile_m = 16 * z.MT;
     z.plan.tile_n = 16 * z.RT;
@@ -394,8 +405,12 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
       z.lds_e = z.lds_y + z.RT * z.MT * 1024;
       z.lds_b = z.lds_g = z.lds_ev = z.lds_e;
       if (local) {
-        // u [16 MT][R1p] and v [16 MT][r], the rows of B, the staged A, w_g
-        z.lds_b = (int)align_up(z.lds_e + (size_t)16 * z.MT * (z.R1p + z.r) * 4, 16);
+        // u [16 MT][R1p] and v [16 MT][r] (and the tanh-MLP gate's hidden
+        // layer), the rows of B, the staged A, w_g
+        const size_t hid = z.gate == GATE_TANH ? (size_t)local_tanh_cap((int)M, z.h) * z.h * 4 +
+                                                     (size_t)tanh_stage_halves(z.h, z.r) * 2
+                                               : 0;
+        z.lds_b = (int)align_up(z.lds_e + (size_t)16 * z.MT * (z.R1p + z.r) * 4 + hid, 16);
         z.bpre = (z.r % 8) == 0 && RB * z.r / 8 <= 2 * 64 * z.NW;
         z.lds_a = (int)align_up(z.lds_b + (z.bpre ? (size_t)RB * z.r * 2 : 0), 16);
         z.lds_g = z.lds_ev = (int)(z.lds_a + (size_t)17 * (z.ips * kIterK + 8) * 2);
@@ -687,6 +702,11 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
       g.A = (const uint16_t*)ec->A;
     }
     g.wg = (const uint16_t*)ec->w_g;
+    g.W1 = (const uint16_t*)ec->W1;
+    g.b1 = (const uint16_t*)ec->b1;
+    g.W2 = (const uint16_t*)ec->W2;
+    g.b2 = (const uint16_t*)ec->b2;
+    g.h = z.h;
     g.alpha = ec->alpha;
     g.b_g = ec->b_g;
     g.gate = z.gate;
@@ -699,8 +719,10 @@ spear_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPEAR_OK : SP
 // The kernels that read the packed codes, for the problem's code width.
 hipError_t launch_gemv_wb(const Resolved& z, int epi, const GemvParams& p, int grid, int block,
                           size_t lds, hipStream_t st) {
-  return z.wb == 3 ? launch_gemv_w3(z.dt, z.MT, z.RT, epi, p, grid, block, lds, st)
-                   : launch_gemv_w4(z.dt, z.MT, z.RT, epi, p, grid, block, lds, st);
+  // the naive chain's 4-bit kernel and grouped launches keep two stages
+  const int nst = epi == EPI_NONE || epi == EPI_READY || epi == EPI_FUSED ? z.nst : 2;
+  return z.wb == 3 ? launch_gemv_w3(z.dt, z.MT, z.RT, epi, nst, p, grid, block, lds, st)
+                   : launch_gemv_w4(z.dt, z.MT, z.RT, epi, nst, p, grid, block, lds, st);
 }
 hipError_t launch_gemm_wb(const Resolved& z, int epi, const GemmParams& p, hipStream_t st) {
   return z.wb == 3 ? launch_gemm_w3(z.dt, epi, p, st) : launch_gemm_w4(z.dt, epi, p, st);
@@ -1131,6 +1153,8 @@ void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves) {
 }
 
 void spear_set_gemm_slices(int32_t k_slices) { g_ov_gs = k_slices > 0 ? k_slices : 0; }
+
+void spear_set_gemv_stages(int32_t stages) { g_ov_nst = stages > 0 ? stages : 0; }
 
 void spear_set_gemm_tile(int32_t tokens) { g_ov_gt = tokens == 128 || tokens == 256 ? tokens : 0; }
 

@@ -183,13 +183,30 @@ struct GemmParams {
   // EPI_LOCAL (fully fused prefill): the projection's inputs
   const uint16_t* A;      // [r][K], r <= 16
   const uint16_t* wg;     // [K] (sigmoid gate) or null
+  const uint16_t* W1;     // [h][r] (tanh-MLP gate) or null
+  const uint16_t* b1;     // [h]
+  const uint16_t* W2;     // [r][h]
+  const uint16_t* b2;     // [r]
   float alpha, b_g;
-  int gate;
+  int gate, h;
 };
 // EPI_LOCAL GEMM: the EC stage tile holds A's 16 rows and w_g (row 16)
 constexpr int kGemmEcRows = 17;
 
 __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Tokens per pass of the tanh-MLP gate in the local GEMV variant, whose LDS
+// keeps 2048 floats for the gate's hidden layer (cap x h).
+__host__ __device__ inline int local_tanh_cap(int M, int h) {
+  const int c = 2048 / (h > 0 ? h : 1);
+  return c < 1 ? 1 : (c < M ? c : M);
+}
+// Halves of the tanh-MLP gate's parameters (W1, b1, W2, b2) staged in LDS
+// for the gate, or 0 when they exceed 4096 halves (then read from memory).
+__host__ __device__ inline int tanh_stage_halves(int h, int r) {
+  const int n = 2 * h * r + h + r;
+  return n <= 4096 ? n : 0;
+}
 
 // GEMV workgroups have at most eight waves (a ninth would make the dispatcher
 // reserve three waves' registers on every SIMD and halve residency); the EC
@@ -216,8 +233,8 @@ __host__ __device__ inline size_t ec_block_lds(int NW, int R1p, int h, int r) {
   hipError_t launch_dequant_##W(int dt, const uint32_t* qw, const uint16_t* sc,                 \
                                 const uint8_t* zr, uint16_t* out, int N, int K, int G,          \
                                 hipStream_t st);                                                \
-  hipError_t launch_gemv_##W(int dt, int MT, int RT, int epi, const GemvParams& p, int grid,    \
-                             int block, size_t lds, hipStream_t st);                            \
+  hipError_t launch_gemv_##W(int dt, int MT, int RT, int epi, int nst, const GemvParams& p,     \
+                             int grid, int block, size_t lds, hipStream_t st);                  \
   hipError_t launch_gemv_group_##W(int dt, int MT, int RT, int epi, const GemvGroup& g,         \
                                    int block, size_t lds, hipStream_t st);                      \
   hipError_t launch_gemm_##W(int dt, int epi, const GemmParams& p, hipStream_t st);

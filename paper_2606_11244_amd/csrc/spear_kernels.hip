@@ -473,6 +473,52 @@ __device__ void ec_project(const EcParams& e, int tb, int it_beg, int it_end, in
   }
 }
 
+// The paper's rank-space gate for cnt tokens at once, by the whole block:
+// hid = ReLU(W1 u + b1) for every token, then v = alpha (1 + tanh(W2 hid +
+// b2)) (.) u, in fp32, cap tokens per pass (hid holds cap x h floats). u
+// rows are us floats apart, v rows vs. With wst (LDS room for
+// tanh_stage_halves(h, r) halves, or null) the gate's parameters are first
+// copied there with coalesced loads, so that the dot products read LDS
+// rather than one global load per term. Ends with a barrier.
+template <int DT>
+__device__ void tanh_gate_tokens(int cnt, int r, int h, const float* u, int us,
+                                 const uint16_t* W1, const uint16_t* b1, const uint16_t* W2,
+                                 const uint16_t* b2, float alpha, float* hid, int cap, float* v,
+                                 int vs, uint16_t* wst) {
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  if (wst) {
+    const int n1 = h * r, n2 = n1 + h, n3 = n2 + r * h, n4 = n3 + r;
+    for (int i = tid; i < n4; i += nthr)
+      wst[i] = i < n1 ? W1[i] : i < n2 ? b1[i - n1] : i < n3 ? W2[i - n2] : b2[i - n3];
+    __syncthreads();
+    W1 = wst;
+    b1 = wst + n1;
+    W2 = wst + n2;
+    b2 = wst + n3;
+  }
+  for (int t0 = 0; t0 < cnt; t0 += cap) {
+    const int c = min(cap, cnt - t0);
+    for (int idx = tid; idx < c * h; idx += nthr) {
+      const int t = idx / h, i = idx - t * h;
+      const float* ut = u + (t0 + t) * us;
+      const uint16_t* w1 = W1 + (size_t)i * r;
+      float a = act2f<DT>(b1[i]);
+      for (int j = 0; j < r; ++j) a += act2f<DT>(w1[j]) * ut[j];
+      hid[idx] = a > 0.f ? a : 0.f;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < c * r; idx += nthr) {
+      const int t = idx / r, j = idx - t * r;
+      const float* ht = hid + t * h;
+      const uint16_t* w2 = W2 + (size_t)j * h;
+      float a = act2f<DT>(b2[j]);
+      for (int i = 0; i < h; ++i) a += act2f<DT>(w2[i]) * ht[i];
+      v[(t0 + t) * vs + j] = alpha * (1.f + tanhf(a)) * u[(t0 + t) * us + j];
+    }
+    __syncthreads();
+  }
+}
+
 // Gate of one token tile: from u (LDS, [16][R1p]) to v_tile (LDS, [16][r]):
 // v = alpha * g * u (sigmoid-linear), alpha * (1 + tanh(W2 ReLU(W1 u + b1) + b2)) (.) u
 // (tanh-MLP), or alpha * u (gate one). Ends with a barrier.
@@ -1002,7 +1048,7 @@ __device__ void ec_wave(const GemvParams& a, uint32_t gen, char* smem, int n0, b
 // Fused variant: the first n_prod blocks of the grid are EC producers; the
 // others' EC waves wait for what they publish.
 // ---------------------------------------------------------------------------
-template <int DT, int MT, int RT, int EPI, int WB>
+template <int DT, int MT, int RT, int EPI, int WB, int NST = 2>
 __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t gen, char* smem) {
   __shared__ int s_flag;
   constexpr bool kEC = EPI == EPI_READY || EPI == EPI_FUSED;  // with an EC wave
@@ -1159,15 +1205,24 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   // first two pipeline stages of codes, the block's slice of x, the scales
   // and zero points, the rows of B. Small layers give a wave one or two
   // iterations, so the prologue's round trips are most of the kernel.
+  // NST stages of codes in flight per wave: two alternating register sets,
+  // or (NST > 2, for long K-slices on wide layers) a ring of NST sets with
+  // the activations read right before each iteration (from LDS when staged)
   u32x4 wA[RT], wB[RT];
   u32x4 xA[MT][4], xB[MT][4];
+  u32x4 wR[NST > 2 ? NST : 1][RT];
   const int last = iw_end - 1;
   if (iw_beg < iw_end) {
-    load_w(wA, iw_beg);
-    load_w(wB, min(iw_beg + 1, last));
-    if (!xl) {
-      load_x(xA, iw_beg);
-      load_x(xB, min(iw_beg + 1, last));
+    if constexpr (NST > 2) {
+#pragma unroll
+      for (int q = 0; q < NST; ++q) load_w(wR[q], min(iw_beg + q, last));
+    } else {
+      load_w(wA, iw_beg);
+      load_w(wB, min(iw_beg + 1, last));
+      if (!xl) {
+        load_x(xA, iw_beg);
+        load_x(xB, min(iw_beg + 1, last));
+      }
     }
   }
   // the block's slice of x into LDS ([M][slice] with a padded row stride),
@@ -1310,7 +1365,7 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
     }
   }
   __syncthreads();
-  if (xl && iw_beg < iw_end) {
+  if (NST == 2 && xl && iw_beg < iw_end) {
     load_x(xA, iw_beg);
     load_x(xB, min(iw_beg + 1, last));
   }
@@ -1383,7 +1438,20 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   // while batch it is computed (two register sets, alternating, both filled
   // by the prologue). Loads past the wave's last iteration re-read that
   // iteration (never computed), so every load is unconditional.
-  if (iw_beg < iw_end) {
+  if (NST > 2 && iw_beg < iw_end) {
+    for (int it = iw_beg; it < iw_end; it += NST) {
+#pragma unroll
+      for (int q = 0; q < NST; ++q) {
+        if (it + q < iw_end) {  // uniform
+          u32x4 xv[MT][4];
+          load_x(xv, it + q);
+          compute(wR[q], xv, it + q);
+          load_w(wR[q], min(it + q + NST, last));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  } else if (iw_beg < iw_end) {
     for (int it = iw_beg; it < iw_end; it += 2) {
       compute(wA, xA, it);
       if (it + 1 >= iw_end) break;
@@ -1427,7 +1495,7 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   // a token also sums that token's gate logit and writes v_j directly
   // (EPI_LOCAL, below), saving a pass and a barrier.
   float* v_loc = u_loc + 16 * MT * R1p;
-  const bool v_direct = a.S == 1;
+  const bool v_direct = a.S == 1 && a.ec.gate != GATE_TANH;
   if constexpr (kLoc) {
     // tile 0: column j < r is u_j; tile 1: column 0 is the gate logit w_g x
     for (int e = tid; e < 256 * kLocalTiles * MT; e += blockDim.x) {
@@ -1515,8 +1583,17 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   }
 
   // EPI_LOCAL: v = alpha g(x) (.) A x for every token (g the sigmoid of the
-  // gate row's sum plus b_g, or one), then y += v B^T in fp32 below
-  if (kLoc && !v_direct) {
+  // gate row's sum plus b_g, or one; or the tanh-MLP gate of u, whose hidden
+  // layer takes the LDS after v), then y += v B^T in fp32 below
+  if (kLoc && !v_direct && a.ec.gate == GATE_TANH) {
+    // LDS after v: the hidden layer (cap x h floats), then the staged
+    // parameters when they fit
+    float* hid = v_loc + 16 * MT * r;
+    const int cap = local_tanh_cap(M, a.ec.h);
+    uint16_t* wst = tanh_stage_halves(a.ec.h, r) > 0 ? (uint16_t*)(hid + cap * a.ec.h) : nullptr;
+    tanh_gate_tokens<DT>(M, r, a.ec.h, u_loc, R1p, a.ec.W1, a.ec.b1, a.ec.W2, a.ec.b2, a.ec.alpha,
+                         hid, cap, v_loc, r, wst);
+  } else if (kLoc && !v_direct) {
     for (int idx = tid; idx < M * r; idx += blockDim.x) {
       const int m = idx / r, j = idx - m * r;
       float g = 1.f;
@@ -1581,7 +1658,7 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   if constexpr (EPI == EPI_FUSED) fused_exit(a);
 }
 
-template <int DT, int MT, int RT, int EPI, int WB>
+template <int DT, int MT, int RT, int EPI, int WB, int NST>
 __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int bid = blockIdx.x;
@@ -1596,7 +1673,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
     }
     bid -= a.n_prod;
   }
-  gemv_body<DT, MT, RT, EPI, WB>(a, bid, gen, smem);
+  gemv_body<DT, MT, RT, EPI, WB, NST>(a, bid, gen, smem);
 }
 
 // Several independent layer calls of one GEMV variant in one launch: member i
@@ -2045,10 +2122,27 @@ __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams
         if (wn == 1 && lr == 0) u_sh[t * 17 + 16] = eacc[i][e2];
       }
     __syncthreads();
+    // the tanh-MLP gate: v [TM][16] in fp32 first, its hidden layer in the
+    // rest of the (free) stage buffers
+    float* v_sh = (float*)(smem + TM * 17 * 4 + 2 * TM * kVS * 2);
+    const bool tanh_g = a.gate == GATE_TANH;  // uniform
+    if (tanh_g) {
+      // after v: the staged parameters (when they fit), then the hidden layer
+      constexpr int kLds = 2 * (TM + kGemmTN) * LR * 2 + 2 * kGemmEcRows * LR * 2;
+      const int nst = tanh_stage_halves(a.h, a.r);
+      uint16_t* wst = nst > 0 ? (uint16_t*)(v_sh + TM * 16) : nullptr;
+      float* hid = (float*)((char*)(v_sh + TM * 16) + align_up((size_t)nst * 2, 16));
+      const int hid_floats = (kLds - (int)((char*)hid - smem)) / 4;
+      const int cap = max(1, min(TM, hid_floats / max(1, a.h)));
+      tanh_gate_tokens<DT>(TM, a.r, a.h, u_sh, 17, a.W1, a.b1, a.W2, a.b2, a.alpha, hid, cap,
+                           v_sh, 16, wst);
+    }
     for (int idx = tid; idx < TM * kVS; idx += NT) {
       const int t = idx / kVS, j = idx - t * kVS;
       float val = 0.f;
-      if (j < a.r) {
+      if (j < a.r && tanh_g) {
+        val = v_sh[t * 16 + j];
+      } else if (j < a.r) {
         float g = 1.f;
         if (a.gate == GATE_SIGMOID) {
           const float z = u_sh[t * 17 + 16] + a.b_g;
@@ -2224,27 +2318,38 @@ hipError_t launch_ec_up_acc(int dt, const float* v, const uint16_t* B, const int
 
 #endif  // SPEAR_WB == 4
 
-template <int DT, int MT, int RT>
-static hipError_t gemv_launch(int epi, const GemvParams& p, int grid, int block, size_t lds,
-                              hipStream_t st) {
-  constexpr int WB = SPEAR_WB;
-  hipError_t err = epi == EPI_NONE    ? allow_lds(k_gemv<DT, MT, RT, EPI_NONE, WB>, lds)
-                   : epi == EPI_READY ? allow_lds(k_gemv<DT, MT, RT, EPI_READY, WB>, lds)
-                   : epi == EPI_FUSED ? allow_lds(k_gemv<DT, MT, RT, EPI_FUSED, WB>, lds)
-                   : epi == EPI_LOCAL ? allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL, WB>, lds)
-                                      : allow_lds(k_gemv<DT, MT, RT, EPI_LOCAL_I8, WB>, lds);
+template <int DT, int MT, int RT, int EPI, int NST>
+static hipError_t gemv_launch_one(const GemvParams& p, int grid, int block, size_t lds,
+                                  hipStream_t st) {
+  hipError_t err = allow_lds(k_gemv<DT, MT, RT, EPI, SPEAR_WB, NST>, lds);
   if (err != hipSuccess) return err;
-  if (epi == EPI_NONE)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_NONE, WB>), dim3(grid), dim3(block), lds, st, p);
-  else if (epi == EPI_READY)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_READY, WB>), dim3(grid), dim3(block), lds, st, p);
-  else if (epi == EPI_FUSED)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_FUSED, WB>), dim3(grid), dim3(block), lds, st, p);
-  else if (epi == EPI_LOCAL)
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL, WB>), dim3(grid), dim3(block), lds, st, p);
-  else
-    hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI_LOCAL_I8, WB>), dim3(grid), dim3(block), lds, st, p);
+  hipLaunchKernelGGL((k_gemv<DT, MT, RT, EPI, SPEAR_WB, NST>), dim3(grid), dim3(block), lds, st, p);
   return hipGetLastError();
+}
+
+// Pipeline depths compiled in: 2 everywhere; 4 and 8 for one token tile on
+// the variants wide layers take at decode (4-bit only, fused, semi-fused).
+template <int DT, int MT, int RT, int EPI>
+static hipError_t gemv_launch_nst(int nst, const GemvParams& p, int grid, int block, size_t lds,
+                                  hipStream_t st) {
+  if constexpr (MT == 1 && (EPI == EPI_NONE || EPI == EPI_READY || EPI == EPI_FUSED)) {
+    if (nst == 4) return gemv_launch_one<DT, MT, RT, EPI, 4>(p, grid, block, lds, st);
+    if (nst == 8) return gemv_launch_one<DT, MT, RT, EPI, 8>(p, grid, block, lds, st);
+  }
+  if (nst != 2) return hipErrorInvalidValue;
+  return gemv_launch_one<DT, MT, RT, EPI, 2>(p, grid, block, lds, st);
+}
+
+template <int DT, int MT, int RT>
+static hipError_t gemv_launch(int epi, int nst, const GemvParams& p, int grid, int block,
+                              size_t lds, hipStream_t st) {
+  switch (epi) {
+    case EPI_NONE: return gemv_launch_nst<DT, MT, RT, EPI_NONE>(nst, p, grid, block, lds, st);
+    case EPI_READY: return gemv_launch_nst<DT, MT, RT, EPI_READY>(nst, p, grid, block, lds, st);
+    case EPI_FUSED: return gemv_launch_nst<DT, MT, RT, EPI_FUSED>(nst, p, grid, block, lds, st);
+    case EPI_LOCAL: return gemv_launch_nst<DT, MT, RT, EPI_LOCAL>(nst, p, grid, block, lds, st);
+    default: return gemv_launch_nst<DT, MT, RT, EPI_LOCAL_I8>(nst, p, grid, block, lds, st);
+  }
 }
 
 // The GEMV shapes compiled in: (token tiles MT, row tiles RT).
@@ -2261,8 +2366,8 @@ bool gemv_shape_supported(int MT, int RT) {
 }
 #endif
 
-hipError_t SPEAR_W(launch_gemv)(int dt, int MT, int RT, int epi, const GemvParams& p, int grid,
-                                int block, size_t lds, hipStream_t st) {
+hipError_t SPEAR_W(launch_gemv)(int dt, int MT, int RT, int epi, int nst, const GemvParams& p,
+                                int grid, int block, size_t lds, hipStream_t st) {
   // split-K needs its partial sums and row-group counters (workspace)
   const bool loc = epi == EPI_LOCAL || epi == EPI_LOCAL_I8;
   if (p.S < 1 || (p.S > 1 && (!p.ypart || !p.rb_ctr || (loc && !p.eupart))) ||
@@ -2271,8 +2376,8 @@ hipError_t SPEAR_W(launch_gemv)(int dt, int MT, int RT, int epi, const GemvParam
   if (grid == 0) return hipSuccess;
 #define SPEAR_GEMV_CASE(mt, rt)                                                     \
   if (MT == mt && RT == rt)                                                         \
-    return dt == DT_F16 ? gemv_launch<DT_F16, mt, rt>(epi, p, grid, block, lds, st) \
-                        : gemv_launch<DT_BF16, mt, rt>(epi, p, grid, block, lds, st);
+    return dt == DT_F16 ? gemv_launch<DT_F16, mt, rt>(epi, nst, p, grid, block, lds, st) \
+                        : gemv_launch<DT_BF16, mt, rt>(epi, nst, p, grid, block, lds, st);
   SPEAR_GEMV_SHAPES(SPEAR_GEMV_CASE)
 #undef SPEAR_GEMV_CASE
   return hipErrorInvalidValue;

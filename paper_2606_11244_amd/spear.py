@@ -34,6 +34,7 @@ EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spea
             "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
             "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
             "spear_set_gemm_tile", "spear_workspace_regions", "spear_w4ec_linear_noalloc",
+            "spear_set_gemv_stages",
             "spear_status_string", "spear_version", "spear_sched_latency", "spear_sched_chunk")
 
 
@@ -131,6 +132,8 @@ def _load():
     lib.spear_set_gemm_slices.restype = None
     lib.spear_set_gemm_tile.argtypes = [ctypes.c_int32]
     lib.spear_set_gemm_tile.restype = None
+    lib.spear_set_gemv_stages.argtypes = [ctypes.c_int32]
+    lib.spear_set_gemv_stages.restype = None
     lib.spear_sched_latency.argtypes = [P(ModelLat), ctypes.c_int64, P(ctypes.c_double)]
     lib.spear_sched_chunk.argtypes = [P(ModelLat), ctypes.c_int64, ctypes.c_double,
                                       ctypes.c_int64, ctypes.c_int64, P(ctypes.c_int64)]
@@ -351,6 +354,11 @@ def set_gemv_shape(row_tiles=0, k_slices=0, waves=0) -> None:
 def set_gemm_slices(k_slices=0) -> None:
     """Tuning override of the prefill GEMM's K-slices (0 = automatic)."""
     LIB.spear_set_gemm_slices(int(k_slices))
+
+
+def set_gemv_stages(stages=0) -> None:
+    """Decode GEMV pipeline depth (2, 4, 8; 0 = the planner's choice)."""
+    LIB.spear_set_gemv_stages(int(stages))
 
 
 def set_gemm_tile(tokens=0) -> None:

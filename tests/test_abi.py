@@ -50,11 +50,9 @@ def _plan(**kw):
     (dict(gate_kind=3), -6), (dict(gate_hidden=-1), -2), (dict(gate_hidden=2048), -2),
     (dict(force_path=7), -6),
     (dict(force_path=sp.PATH_FUSED_MFMA, rank=17), -6),
-    (dict(force_path=sp.PATH_FUSED_MFMA, gate_kind=sp.GATE_TANH_MLP), -6),
     (dict(force_path=sp.PATH_FUSED_GEMV, M=65), -6),
     (dict(force_path=sp.PATH_FUSED_LOCAL, M=33), -6),
     (dict(force_path=sp.PATH_FUSED_LOCAL, rank=17), -6),
-    (dict(force_path=sp.PATH_FUSED_LOCAL, gate_kind=sp.GATE_TANH_MLP), -6),
     (dict(M=1 << 20, K=1 << 12), -2),
 ])
 def test_plan_validation(kw, code):
@@ -83,8 +81,9 @@ def test_plan_phase_aware_dispatch():
         want = sp.PATH_FUSED_GEMV if M == 1 else sp.PATH_UNFUSED_2K
         p = _plan(M=M, rank=32)
         assert p.path == want and p.num_launches == (1 if M == 1 else 2), M
+        # the paper's tanh-MLP gate takes the local variant too (rank 16)
         p = _plan(M=M, gate_kind=sp.GATE_TANH_MLP)
-        assert p.path == want, M
+        assert p.path == sp.PATH_FUSED_LOCAL and p.num_launches == 1, M
         p = _plan(M=M, rank=32, K=8192)
         assert p.path == sp.PATH_FUSED_GEMV and p.num_launches == 1, M
         p = _plan(M=M, rank=64, N=8192, K=28672)
@@ -120,9 +119,10 @@ def test_plan_phase_aware_dispatch():
     for M in (2049, 4096):
         p = _plan(M=M)
         assert p.path == sp.PATH_UNFUSED_2K and p.num_launches == 2, M
-    for kw in (dict(rank=32), dict(gate_kind=sp.GATE_TANH_MLP)):
-        p = _plan(M=512, **kw)
-        assert p.path == sp.PATH_UNFUSED_2K and p.num_launches == 2, kw
+    p = _plan(M=512, rank=32)
+    assert p.path == sp.PATH_UNFUSED_2K and p.num_launches == 2
+    p = _plan(M=512, gate_kind=sp.GATE_TANH_MLP)
+    assert p.path == sp.PATH_FUSED_MFMA and p.num_launches == 1
     assert _plan(M=4, force_path=sp.PATH_UNFUSED_CHAIN).num_launches == 4
     assert _plan(M=4096, force_path=sp.PATH_UNFUSED_CHAIN).num_launches == 4
     assert _plan(M=4, force_path=sp.PATH_UNFUSED_2K).num_launches == 2

@@ -115,7 +115,7 @@ class _Dev:
 
 def _decode_paths(L):
     paths = [P_AUTO, P_GEMV, P_2K, P_CHAIN]
-    if L.rank <= 16 and L.gate_kind != S.GATE_TANH_MLP:
+    if L.rank <= 16:
         paths.append(P_LOCAL)
     return paths
 
@@ -172,7 +172,7 @@ def _check_prefill(cid, module, Ms, gate=S.GATE_SIGMOID_LINEAR, ec_only=False, p
         idx = _tile_tokens(M)
         ref = ref_all[np.searchsorted(every, idx)]
         ps = paths if paths is not None else (
-            [P_AUTO, P_2K] + ([P_MFMA] if L.rank <= 16 and L.gate_kind != S.GATE_TANH_MLP else []))
+            [P_AUTO, P_2K] + ([P_MFMA] if L.rank <= 16 else []))
         for p in ps:
             log(f"full-size prefill {NAME[cid]} {module} M={M} tokens={len(idx)} path={p} "
                 f"ec_only={ec_only}")
@@ -251,9 +251,12 @@ def test_prefill_full_rows(cid, module, ec_only):
 @pytest.mark.parametrize("ec_only", [False, True])
 @pytest.mark.parametrize("module", ["q", "gate"])
 def test_prefill_full_rows_tanh_gate(module, ec_only):
-    """The tanh-MLP gate on the 8B prefill shapes (semi-fused pair and chain)."""
+    """The tanh-MLP gate on the 8B prefill shapes (rank 32: semi-fused pair
+    and chain) and on the 1B ones (rank 16: the fully fused GEMM too)."""
     _check_prefill(3, module, (512, 4096), gate=S.GATE_TANH_MLP, ec_only=ec_only,
                    paths=[P_AUTO, P_2K, P_CHAIN])
+    _check_prefill(2, module, (512, 2048), gate=S.GATE_TANH_MLP, ec_only=ec_only,
+                   paths=[P_AUTO, P_MFMA, P_2K])
 
 
 @pytest.mark.parametrize("cid,module,Ms", [(1, "q", (1, 16)), (1, "down", (1,)),

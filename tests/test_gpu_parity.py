@@ -29,14 +29,13 @@ def _gpu():
 
 
 def _local_ok(L):
-    """The local fused variant: M <= 32, rank <= 16, sigmoid-linear or
-    identity gate."""
-    return L.M <= 32 and L.gate_kind != S.GATE_TANH_MLP and L.rank <= 16
+    """The local fused variant: M <= 32, rank <= 16, every gate."""
+    return L.M <= 32 and L.rank <= 16
 
 
 def _mfma_ok(L):
-    """The fully fused GEMM: rank <= 16, sigmoid-linear or identity gate."""
-    return L.gate_kind != S.GATE_TANH_MLP and L.rank <= 16
+    """The fully fused GEMM: rank <= 16, every gate."""
+    return L.rank <= 16
 
 
 def _paths_for(M, L):
@@ -623,3 +622,27 @@ def test_int8_deterministic(path):
     for _ in range(3):
         assert np.array_equal(first, gpu_y(L, path, workspace=ws, dev=dl))
     assert_parity(first, O.w4ec_linear(L), f"int8 determinism {path}")
+
+
+@pytest.mark.parametrize("stages", [4, 8])
+@pytest.mark.parametrize("M,N,K,wb", [(1, 1024, 8192, 4), (16, 768, 2048, 4), (3, 512, 28672, 4),
+                                      (1, 300, 256, 4), (5, 640, 8192, 3)])
+def test_gemv_pipeline_depths(stages, M, N, K, wb):
+    """The decode GEMV with 4 and 8 stages of codes in flight per wave (one
+    token tile: the 4-bit product alone, the producer-fused and the
+    semi-fused variants), including waves with fewer iterations than
+    stages, against the oracle and bit-identical across repeats."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=M, N=N, K=K, group_size=128, rank=32, seed=stages + M, weight_bits=wb)
+    ref, ref4 = O.w4ec_linear(L), O.w4_linear_layer(L)
+    sp.set_gemv_stages(stages)
+    try:
+        for p in (PATHS["fused_gemv"], PATHS["2k"]):
+            log(f"gemv stages={stages} M={M} N={N} K={K} wb={wb} path={p}")
+            y = gpu_y(L, p)
+            assert_parity(y, ref, f"stages={stages} path={p}")
+            assert np.array_equal(y, gpu_y(L, p))
+        log(f"gemv stages={stages} M={M} N={N} K={K} wb={wb} w4-only")
+        assert_parity(gpu_y(L, 0, with_ec=False), ref4, f"stages={stages} w4-only")
+    finally:
+        sp.set_gemv_stages(0)
