@@ -109,6 +109,18 @@ enum {
                                     the 4-bit GEMM/GEMV whose epilogue adds
                                     B (g (.) A x). AUTO's choice for M > 32
                                     otherwise                                  */
+  SPEAR_PATH_OVERLAP_2K = 6,     /* semi-fused with the EC on a second stream
+                                    (section 4.1's prefill design): the EC
+                                    pre-kernel runs on a library-owned side
+                                    stream concurrently with the 4-bit
+                                    GEMM/GEMV on hip_stream; the side stream
+                                    joins hip_stream before a final kernel adds
+                                    B (g (.) A x) to Y. Three launches. The
+                                    first call on a device creates the side
+                                    stream and two events (so make it outside
+                                    stream capture); calls from several host
+                                    threads are serialised while they enqueue.
+                                    AUTO does not pick it (measured slower)   */
   SPEAR_PATH_FUSED_LOCAL = 5     /* one kernel: split-K 4-bit GEMV whose waves
                                     also project x on [A; w_g] over their own K
                                     chunks (no EC workgroups, no wait on other
@@ -347,9 +359,9 @@ int32_t spear_set_wait_polls(int32_t polls);
 void spear_set_gemv_shape(int32_t row_tiles, int32_t k_slices, int32_t waves);
 
 /* Tuning hook for the decode GEMV's pipeline depth, process-wide: stages of
- * packed codes in flight per wave, 2, 4 or 8 (4 and 8: one token tile, the
- * 4-bit product alone, the producer-fused and the semi-fused variants; else
- * the planner and the calls return SPEAR_E_UNSUPPORTED); 0 restores the
+ * packed codes in flight per wave, 2 or 4 (4: one token tile, the 4-bit
+ * product alone, the producer-fused and the semi-fused variants; else the
+ * planner and the calls return SPEAR_E_UNSUPPORTED); 0 restores the
  * planner's choice. For measurement sweeps and tests only. */
 void spear_set_gemv_stages(int32_t stages);
 

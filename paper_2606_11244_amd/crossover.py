@@ -31,7 +31,7 @@ import math
 import sys
 
 PATHS = [("fused_local", 5), ("fused_gemv", 1), ("fused_mfma", 2), ("unfused_2k", 4),
-         ("unfused_chain", 3)]
+         ("overlap_2k", 6), ("unfused_chain", 3)]
 
 # (configuration id, module, token counts)
 DEFAULT_CASES = [

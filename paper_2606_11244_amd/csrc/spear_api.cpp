@@ -73,7 +73,7 @@ spear_status_t validate_shape(const spear_problem_t* p, bool with_ec) {
   // kernels' 32-bit byte offsets and buffer-resource bounds cover it
   const int64_t lim = (int64_t)1 << 30;
   if (p->M * p->K >= lim || p->N * p->K >= lim || p->M * p->N >= lim) return SPEAR_E_SHAPE;
-  if (p->force_path < SPEAR_PATH_AUTO || p->force_path > SPEAR_PATH_FUSED_LOCAL)
+  if (p->force_path < SPEAR_PATH_AUTO || p->force_path > SPEAR_PATH_OVERLAP_2K)
     return SPEAR_E_UNSUPPORTED;
   if (with_ec) {
     if (p->rank < 0 || p->rank > 256) return SPEAR_E_SHAPE;
@@ -221,7 +221,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     const int fp = p->force_path;
     const bool want_gemv = fp == SPEAR_PATH_FUSED_GEMV || fp == SPEAR_PATH_FUSED_LOCAL;
     const bool want_gemm = fp == SPEAR_PATH_FUSED_MFMA || fp == SPEAR_PATH_UNFUSED_2K ||
-                           fp == SPEAR_PATH_UNFUSED_CHAIN;
+                           fp == SPEAR_PATH_UNFUSED_CHAIN || fp == SPEAR_PATH_OVERLAP_2K;
     if (want_gemv && M > kGemvMaxM) return SPEAR_E_UNSUPPORTED;
     path = want_gemv ? SPEAR_PATH_FUSED_GEMV
            : want_gemm ? SPEAR_PATH_UNFUSED_2K
@@ -251,11 +251,16 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     z.MT = (int)cdiv(M, 16);
     z.NW = 8;
     const bool fused1 = fused && M == 1;
+    // (the naive chain and the overlapped pair run the 4-bit product alone)
+    const bool w4_kernel = !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN || path == SPEAR_PATH_OVERLAP_2K;
     const int rt_kind = local                                           ? kRtLocal
-                        : !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN ? kRtW4
+                        : w4_kernel                                 ? kRtW4
                         : fused1                                    ? kRtFused1
                                                                     : kRtOther;
-    const int waves = (rt_kind == kRtW4 && M == 1) || fused1 ? 2048 : 4096;
+    // one token: the 4-bit product alone, the producer-fused and the
+    // semi-fused GEMV aim at 2048 waves (70B down, semi-fused: 38.8 us in one
+    // K-slice against 40.7 us in two)
+    const int waves = M == 1 && (rt_kind == kRtW4 || rt_kind == kRtOther) || fused1 ? 2048 : 4096;
     {
       // the fused variant's GEMV waves: one wave of the block is the EC wave
       const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load()))
@@ -264,7 +269,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     }
     if (!gemv_shape_supported(z.MT, z.RT)) return SPEAR_E_UNSUPPORTED;
     // the EC variants add the EC wave to the workgroup
-    const int epi = !z.ec || path == SPEAR_PATH_UNFUSED_CHAIN ? EPI_NONE
+    const int epi = w4_kernel                                 ? EPI_NONE
                     : path == SPEAR_PATH_FUSED_GEMV           ? EPI_FUSED
                     : local                                   ? EPI_LOCAL
                                                               : EPI_READY;
@@ -284,14 +289,14 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     z.iw = (int)cdiv(z.ips, z.NW);
     z.nst = 2;
     if (g_ov_nst.load() > 0) {
-      // deeper pipelines: one token tile, the 4-bit-only, fused and
+      // a deeper pipeline: one token tile, the 4-bit-only, fused and
       // semi-fused variants
       const int n = g_ov_nst.load();
-      if ((n != 2 && n != 4 && n != 8) ||
-          (n != 2 && (z.MT != 1 || epi == EPI_LOCAL)))
+      if ((n != 2 && n != 4) || (n != 2 && (z.MT != 1 || epi == EPI_LOCAL)))
         return SPEAR_E_UNSUPPORTED;
       z.nst = n;
     }
+
     z.plan.split_k = z.S;
     z.plan.tile_m = 16 * z.MT;
     z.plan.tile_n = 16 * z.RT;
@@ -450,6 +455,9 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     z.plan.grid = z.n_prod + grid4;
   } else if (path == SPEAR_PATH_UNFUSED_2K) {
     z.plan.num_launches = 2;
+    z.plan.grid = grid4;
+  } else if (path == SPEAR_PATH_OVERLAP_2K) {
+    z.plan.num_launches = 3;
     z.plan.grid = grid4;
   } else {  // chain
     z.plan.num_launches = 4;
@@ -716,6 +724,30 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
 
 spear_status_t hip_status(hipError_t e) { return e == hipSuccess ? SPEAR_OK : SPEAR_E_HIP; }
 
+// The overlapped semi-fused path's side stream and fork/join events, one set
+// per device, created on the first such call there and kept until the
+// process ends. Default priority; non-blocking against the null stream.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mu;
+SideStream g_side[64];
+
+spear_status_t side_stream(SideStream** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return SPEAR_E_HIP;
+  SideStream& ss = g_side[dev];
+  if (!ss.s) {
+    if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess)
+      return SPEAR_E_HIP;
+  }
+  *out = &ss;
+  return SPEAR_OK;
+}
+
 // The kernels that read the packed codes, for the problem's code width.
 hipError_t launch_gemv_wb(const Resolved& z, int epi, const GemvParams& p, int grid, int block,
                           size_t lds, hipStream_t st) {
@@ -798,6 +830,27 @@ spear_status_t run_layer(const spear_problem_t* prob, const Resolved& z, const v
     GemmParams g = make_gemm(prob, z, x, w, y, ec, ws);
     g.res = res;
     return hip_status(launch_gemm_wb(z, EPI_READY, g, s));
+  }
+  if (path == SPEAR_PATH_OVERLAP_2K) {
+    // fork: the EC pre-kernel (A x, gate, v in fp32) on the side stream,
+    // after everything already on the caller's stream; the 4-bit product on
+    // the caller's stream meanwhile; join before the final accumulation
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    SideStream* ss = nullptr;
+    if ((st = side_stream(&ss)) != SPEAR_OK) return st;
+    if (hipEventRecord(ss->fork, s) != hipSuccess || hipStreamWaitEvent(ss->s, ss->fork, 0) != hipSuccess)
+      return SPEAR_E_HIP;
+    st = hip_status(launch_ec(z.dt, e, ec_grid, z.ec_block, z.ec_ipp, z.lds_prod, ss->s));
+    if (st != SPEAR_OK) return st;
+    if (hipEventRecord(ss->join, ss->s) != hipSuccess) return SPEAR_E_HIP;
+    st = run_w4(prob, z, x, w, y, ws, s, res);
+    if (st != SPEAR_OK) return st;
+    if (hipStreamWaitEvent(s, ss->join, 0) != hipSuccess) return SPEAR_E_HIP;
+    const bool i8o = ab_int8(ec);
+    return hip_status(launch_ec_up_acc(z.dt, e.v, i8o ? nullptr : (const uint16_t*)ec->B,
+                                       i8o ? (const int8_t*)ec->B : nullptr,
+                                       i8o ? ec->b_scale : nullptr, (uint16_t*)y, (int)prob->M,
+                                       (int)prob->N, z.r, s));
   }
   // naive chain: 4-bit product, projection, gate, reprojection + accumulate
   st = run_w4(prob, z, x, w, y, ws, s, res);

@@ -1218,11 +1218,9 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
       for (int q = 0; q < NST; ++q) load_w(wR[q], min(iw_beg + q, last));
     } else {
       load_w(wA, iw_beg);
+      if (!xl) load_x(xA, iw_beg);
       load_w(wB, min(iw_beg + 1, last));
-      if (!xl) {
-        load_x(xA, iw_beg);
-        load_x(xB, min(iw_beg + 1, last));
-      }
+      if (!xl) load_x(xB, min(iw_beg + 1, last));
     }
   }
   // the block's slice of x into LDS ([M][slice] with a padded row stride),
@@ -1306,29 +1304,43 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
     u32x2 z8;
     // EPI_LOCAL: the first round of A and w_g goes out with the first round
     // of x, scales and zero points, so that the staging costs one round trip
+    // the second round of x and of the 8-group scale loads goes out with the
+    // first (a deep slice, 28672 wide, needs two): one round trip, not two
     u32x4 a0[4], a1[4], gv0;
+    u32x4 c4b[4], s8b;
+    u32x2 z8b;
     x_issue(tid, c4);
-    if (sz8) sz8_issue(tid, s8, z8);
-    else sz_issue(tid, sv, zv);
+    x_issue(tid + step, c4b);
+    if (sz8) {
+      sz8_issue(tid, s8, z8);
+      sz8_issue(tid + (int)blockDim.x, s8b, z8b);
+    } else {
+      sz_issue(tid, sv, zv);
+    }
     if constexpr (kLoc) {
       a_issue(tid, a0);
       a_issue(tid + step, a1);
       gv0 = bld128(rgw, tid < acpr ? ((uint32_t)it_blk * kIterK + 8 * tid) * 2 : kOOB);
     }
     x_store(tid, c4);
-    if (sz8) sz8_store(tid, s8, z8);
-    else sz_store(tid, sv, zv);
+    x_store(tid + step, c4b);
+    if (sz8) {
+      sz8_store(tid, s8, z8);
+      sz8_store(tid + (int)blockDim.x, s8b, z8b);
+    } else {
+      sz_store(tid, sv, zv);
+    }
     if constexpr (kLoc) {
       a_store(tid, a0);
       a_store(tid + step, a1);
       if (tid < acpr) *(u32x4*)(als + 16 * astride + 8 * tid) = gv0;
     }
-    for (int base = tid + step; base < nch; base += step) {
+    for (int base = tid + 2 * step; base < nch; base += step) {
       x_issue(base, c4);
       x_store(base, c4);
     }
     if (sz8) {
-      for (int i = tid + (int)blockDim.x; i < nsz8; i += blockDim.x) {
+      for (int i = tid + 2 * (int)blockDim.x; i < nsz8; i += blockDim.x) {
         sz8_issue(i, s8, z8);
         sz8_store(i, s8, z8);
       }
@@ -2327,14 +2339,13 @@ static hipError_t gemv_launch_one(const GemvParams& p, int grid, int block, size
   return hipGetLastError();
 }
 
-// Pipeline depths compiled in: 2 everywhere; 4 and 8 for one token tile on
-// the variants wide layers take at decode (4-bit only, fused, semi-fused).
+// Pipeline depths compiled in: 2 everywhere; 4 for one token tile on the
+// variants wide layers take at decode (4-bit only, fused, semi-fused).
 template <int DT, int MT, int RT, int EPI>
 static hipError_t gemv_launch_nst(int nst, const GemvParams& p, int grid, int block, size_t lds,
                                   hipStream_t st) {
   if constexpr (MT == 1 && (EPI == EPI_NONE || EPI == EPI_READY || EPI == EPI_FUSED)) {
     if (nst == 4) return gemv_launch_one<DT, MT, RT, EPI, 4>(p, grid, block, lds, st);
-    if (nst == 8) return gemv_launch_one<DT, MT, RT, EPI, 8>(p, grid, block, lds, st);
   }
   if (nst != 2) return hipErrorInvalidValue;
   return gemv_launch_one<DT, MT, RT, EPI, 2>(p, grid, block, lds, st);

@@ -168,8 +168,9 @@ def _pass_of(name, grid):
 
 
 def main70(argv):
-    """profsum --llama70b TRACE_DIR FETCH_DIR WRITE_DIR SQ_DIR NAME TRACE_CMD FETCH_CMD
-    WRITE_CMD SQ_CMD"""
+    """profsum --llama70b TRACE_DIR FETCH_DIR WRITE_DIR SQ_DIRS NAME TRACE_CMD FETCH_CMD
+    WRITE_CMD SQ_CMDS. SQ_DIRS is a comma-separated list of counter runs (or "-"),
+    SQ_CMDS their commands joined by " | "."""
     trace_dir, fetch_dir, write_dir, sq_dir, name, tcmd, fcmd, wcmd, scmd = argv[2:11]
     stats = list(csv.DictReader(open(_one(os.path.join(trace_dir, "**", "*kernel_stats.csv")))))
     trace = list(csv.DictReader(open(_one(os.path.join(trace_dir, "**", "*kernel_trace.csv")))))
@@ -200,8 +201,8 @@ def main70(argv):
             byp[p][1] += len(vals)
         rows.append((short, g, len(vals), rd, wr, p))
     sq = {}
-    if sq_dir and sq_dir != "-":
-        srows = list(csv.DictReader(open(_one(os.path.join(sq_dir, "**", "*counter_collection.csv")))))
+    for one_dir in ([] if not sq_dir or sq_dir == "-" else sq_dir.split(",")):
+        srows = list(csv.DictReader(open(_one(os.path.join(one_dir, "**", "*counter_collection.csv")))))
         for r in srows:
             nm = r["Kernel_Name"].split("(")[0].replace("void spear::", "")
             if "spear::" not in r["Kernel_Name"]:
@@ -215,7 +216,7 @@ def main70(argv):
              "with the sigmoid-linear gate on a seeded 25% of the modules: decode pass at M = 1 "
              "and prefill pass at M = 4096, every call on its AUTO path; synthetic data.", "",
              "Commands (from the repository root, with TMPDIR=/tmp):", "",
-             f"    {tcmd}", f"    {fcmd}", f"    {wcmd}"] + ([f"    {scmd}"] if sq else []) + [
+             f"    {tcmd}", f"    {fcmd}", f"    {wcmd}"] + [f"    {c.strip()}" for c in (scmd.split(" | ") if sq else [])] + [
              "", f"Kernel sources hash: {kernel_source_hash()}", "",
              "## Kernel durations (kernel trace, --stats)", "",
              "| kernel | calls | average us | min us | max us | share |",
@@ -280,7 +281,7 @@ def main70(argv):
            "prefill_kernel": "every prefill-pass launch (k_gemm*, k_ec with >= 256 workgroups)",
            "prefill_bytes_per_launch": round(pre),
            "read_scale": round(k_f, 4), "write_scale": round(k_w, 4),
-           "commands": [tcmd, fcmd, wcmd] + ([scmd] if sq else [])}
+           "commands": [tcmd, fcmd, wcmd] + ([c.strip() for c in scmd.split(" | ")] if sq else [])}
     with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out))

@@ -22,9 +22,10 @@ F16, BF16 = 0, 1
 GATE_ONE, GATE_SIGMOID_LINEAR, GATE_TANH_MLP = 0, 1, 2
 PATH_AUTO, PATH_FUSED_GEMV, PATH_FUSED_MFMA, PATH_UNFUSED_CHAIN, PATH_UNFUSED_2K = 0, 1, 2, 3, 4
 PATH_FUSED_LOCAL = 5
+PATH_OVERLAP_2K = 6
 PATH_NAMES = {PATH_AUTO: "auto", PATH_FUSED_GEMV: "fused_gemv", PATH_FUSED_MFMA: "fused_mfma",
               PATH_UNFUSED_CHAIN: "unfused_chain", PATH_UNFUSED_2K: "unfused_2k",
-              PATH_FUSED_LOCAL: "fused_local"}
+              PATH_FUSED_LOCAL: "fused_local", PATH_OVERLAP_2K: "overlap_2k"}
 
 STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_DTYPE",
           -4: "SPEAR_E_ALIGN", -5: "SPEAR_E_WORKSPACE", -6: "SPEAR_E_UNSUPPORTED",

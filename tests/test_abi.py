@@ -325,7 +325,7 @@ def test_tagged_region_is_written_by_the_fused_path_only():
         for M in (1, 2, 4, 8, 16, 17, 32, 33, 64, 65, 128, 512, 4096):
             for r in (0, 8, 16, 32, 64, 256):
                 for gate in (sp.GATE_ONE, sp.GATE_SIGMOID_LINEAR, sp.GATE_TANH_MLP):
-                    for path in range(6):
+                    for path in range(7):
                         for with_ec in (True, False):
                             pr = sp.problem(M, N, K, G, sp.F16, r, gate, force_path=path)
                             try:

@@ -17,7 +17,8 @@ from gpu_util import assert_parity, gpu_y, log, scaled_ec, with_fields, zero_wei
 
 pytestmark = pytest.mark.gpu
 
-PATHS = {"auto": 0, "fused_gemv": 1, "fused_mfma": 2, "chain": 3, "2k": 4, "fused_local": 5}
+PATHS = {"auto": 0, "fused_gemv": 1, "fused_mfma": 2, "chain": 3, "2k": 4, "fused_local": 5,
+         "overlap": 6}
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -330,7 +331,7 @@ def test_streams_and_reuse():
 
 
 @pytest.mark.parametrize("M,path", [(4, 1), (4, 4), (4, 3), (200, 0), (200, 3), (33, 1), (4, 5),
-                                    (17, 5), (200, 2), (4, 2)])
+                                    (17, 5), (200, 2), (4, 2), (4, 6), (200, 6)])
 def test_graph_replay(M, path):
     """A captured call replayed several times, with new activations written
     between replays by eager work: every replay equals the eager call on the
@@ -624,7 +625,7 @@ def test_int8_deterministic(path):
     assert_parity(first, O.w4ec_linear(L), f"int8 determinism {path}")
 
 
-@pytest.mark.parametrize("stages", [4, 8])
+@pytest.mark.parametrize("stages", [4])
 @pytest.mark.parametrize("M,N,K,wb", [(1, 1024, 8192, 4), (16, 768, 2048, 4), (3, 512, 28672, 4),
                                       (1, 300, 256, 4), (5, 640, 8192, 3)])
 def test_gemv_pipeline_depths(stages, M, N, K, wb):
