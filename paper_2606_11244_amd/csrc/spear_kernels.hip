@@ -772,23 +772,31 @@ __device__ __forceinline__ void wave_sync() { __builtin_amdgcn_wave_barrier(); }
 // wave's 64 lanes; returns 1 (in every lane) if any word carries another tag.
 // COH: coherent (sc1) loads, else loads through this XCD's L2, which are
 // cheaper but may return a line cached before the data was published (its
-// tag then tells).
+// tag then tells). Nine loads per lane go out together (576 words), so that
+// the EC data of a token tile at rank 64 (520 words in eight partials) costs
+// one round trip, not three; more would push the fused GEMV past its
+// 128-VGPR budget into scratch.
 template <bool COH, class Off>
 __device__ __forceinline__ bool gather_tagged_w(rsrc_t r, int n, Off off, uint32_t tag, float* dst) {
   const int lane = threadIdx.x & 63;
   constexpr int aux = COH ? 0x10 : 0;
+  constexpr int U = 9;
   int stale = 0;
-  for (int i0 = lane; i0 < n; i0 += 256) {
-    const int i1 = i0 + 64, i2 = i1 + 64, i3 = i2 + 64;
-    const u32x2 w0 = __builtin_amdgcn_raw_buffer_load_b64(r, off(i0), 0, aux);
-    const u32x2 w1 = __builtin_amdgcn_raw_buffer_load_b64(r, i1 < n ? off(i1) : kOOB, 0, aux);
-    const u32x2 w2 = __builtin_amdgcn_raw_buffer_load_b64(r, i2 < n ? off(i2) : kOOB, 0, aux);
-    const u32x2 w3 = __builtin_amdgcn_raw_buffer_load_b64(r, i3 < n ? off(i3) : kOOB, 0, aux);
-    stale |= w0[1] != tag;
-    dst[i0] = __uint_as_float(w0[0]);
-    if (i1 < n) { stale |= w1[1] != tag; dst[i1] = __uint_as_float(w1[0]); }
-    if (i2 < n) { stale |= w2[1] != tag; dst[i2] = __uint_as_float(w2[0]); }
-    if (i3 < n) { stale |= w3[1] != tag; dst[i3] = __uint_as_float(w3[0]); }
+  for (int i0 = lane; i0 < n; i0 += 64 * U) {
+    u32x2 w[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + 64 * u;
+      w[u] = __builtin_amdgcn_raw_buffer_load_b64(r, i < n ? off(i) : kOOB, 0, aux);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + 64 * u;
+      if (i < n) {
+        stale |= w[u][1] != tag;
+        dst[i] = __uint_as_float(w[u][0]);
+      }
+    }
   }
   wave_sync();
   return __any(stale);
@@ -992,7 +1000,10 @@ __device__ void ec_wave(const GemvParams& a, uint32_t gen, char* smem, int n0, b
   // warm-up pass, then wait: small problems poll the tagged data itself;
   // the others wait (bounded) for this copy's ready counter to show every
   // publisher of this launch and then read the data once through the L2,
-  // re-reading it coherently if a cached line was stale
+  // re-reading it coherently if a cached line was stale. (Coherent reads
+  // from every EC wave at once were measured: hundreds of waves reading the
+  // same few lines at the memory side delay the producers' own stores, 70B
+  // q 44.7 us against 18.7 us.)
   bool ok = true;
   if (!e.direct) {
     attempt(0, min(16, M), false, true);
@@ -1303,17 +1314,20 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
     u32x4 s8;
     u32x2 z8;
     // EPI_LOCAL: the first round of A and w_g goes out with the first round
-    // of x, scales and zero points, so that the staging costs one round trip
-    // the second round of x and of the 8-group scale loads goes out with the
-    // first (a deep slice, 28672 wide, needs two): one round trip, not two
+    // of x, scales and zero points, so that the staging costs one round
+    // trip. The second round of x and of the 8-group scales goes out with
+    // the first too (a deep slice, 28672 wide, needs two), except in the
+    // producer-fused variant, whose 22 more VGPRs there would cost it the
+    // second workgroup per CU.
+    constexpr bool kTwo = EPI != EPI_FUSED;
     u32x4 a0[4], a1[4], gv0;
     u32x4 c4b[4], s8b;
     u32x2 z8b;
     x_issue(tid, c4);
-    x_issue(tid + step, c4b);
+    if constexpr (kTwo) x_issue(tid + step, c4b);
     if (sz8) {
       sz8_issue(tid, s8, z8);
-      sz8_issue(tid + (int)blockDim.x, s8b, z8b);
+      if constexpr (kTwo) sz8_issue(tid + (int)blockDim.x, s8b, z8b);
     } else {
       sz_issue(tid, sv, zv);
     }
@@ -1323,10 +1337,10 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
       gv0 = bld128(rgw, tid < acpr ? ((uint32_t)it_blk * kIterK + 8 * tid) * 2 : kOOB);
     }
     x_store(tid, c4);
-    x_store(tid + step, c4b);
+    if constexpr (kTwo) x_store(tid + step, c4b);
     if (sz8) {
       sz8_store(tid, s8, z8);
-      sz8_store(tid + (int)blockDim.x, s8b, z8b);
+      if constexpr (kTwo) sz8_store(tid + (int)blockDim.x, s8b, z8b);
     } else {
       sz_store(tid, sv, zv);
     }
@@ -1335,12 +1349,12 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
       a_store(tid + step, a1);
       if (tid < acpr) *(u32x4*)(als + 16 * astride + 8 * tid) = gv0;
     }
-    for (int base = tid + 2 * step; base < nch; base += step) {
+    for (int base = tid + (kTwo ? 2 : 1) * step; base < nch; base += step) {
       x_issue(base, c4);
       x_store(base, c4);
     }
     if (sz8) {
-      for (int i = tid + 2 * (int)blockDim.x; i < nsz8; i += blockDim.x) {
+      for (int i = tid + (kTwo ? 2 : 1) * (int)blockDim.x; i < nsz8; i += blockDim.x) {
         sz8_issue(i, s8, z8);
         sz8_store(i, s8, z8);
       }
@@ -1670,8 +1684,18 @@ __device__ __forceinline__ void gemv_body(const GemvParams& a, int bid, uint32_t
   if constexpr (EPI == EPI_FUSED) fused_exit(a);
 }
 
+// Minimum waves per SIMD the compiler must leave room for (the second
+// launch bound). One token tile on up to 32 rows without the local EC asks
+// for 4, two workgroups of eight waves per CU (at most 128 VGPRs): wide
+// layers run several rounds of blocks, and one block per CU leaves half the
+// latency hiding unused (70B gate, fused: 60.8 us at 156 VGPRs, 42.6 us at
+// 125).
+constexpr int gemv_min_waves(int MT, int RT, int EPI) {
+  return MT == 1 && RT <= 2 && EPI <= EPI_FUSED ? 4 : 1;
+}
+
 template <int DT, int MT, int RT, int EPI, int WB, int NST>
-__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
+__global__ __launch_bounds__(kGemvMaxThreads, gemv_min_waves(MT, RT, EPI)) void k_gemv(GemvParams a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int bid = blockIdx.x;
   uint32_t gen = 0;
@@ -1693,7 +1717,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemvParams a) {
 // own launch would run, so each member's output is the one its single call
 // writes. The member index is uniform over the workgroup.
 template <int DT, int MT, int RT, int EPI, int WB>
-__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv_group(GemvGroup g) {
+__global__ __launch_bounds__(kGemvMaxThreads, gemv_min_waves(MT, RT, EPI)) void k_gemv_group(GemvGroup g) {
   static_assert(EPI == EPI_NONE || EPI == EPI_LOCAL || EPI == EPI_LOCAL_I8,
                 "grouped launches take the variants without cross-launch state");
   extern __shared__ __attribute__((aligned(16))) char smem[];
