@@ -19,7 +19,7 @@ namespace {
 std::atomic<int32_t> g_wait_polls{1 << 16};
 // tuning override of the GEMV shape (0 = automatic): row tiles per block,
 // K-slices per row group, waves per block
-std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0}, g_ov_gt{0}, g_ov_nst{0};
+std::atomic<int32_t> g_ov_rt{0}, g_ov_s{0}, g_ov_nw{0}, g_ov_gs{0}, g_ov_gt{0}, g_ov_nst{0}, g_ov_gr{0};
 
 // Token counts at or below this run the 4-bit product as a split-K GEMV; above
 // it the LDS-tiled MFMA GEMM. The same bound separates decode (fully fused
@@ -51,6 +51,7 @@ struct Resolved {
   int nst;                                    // GEMV stages of codes in flight per wave
   int Sg;                                     // GEMM K-slices
   int gtmw;                                   // GEMM token waves (2: 128-token tiles, 4: 256)
+  int groles;                                 // GEMM wave roles (1: every wave both, 2, 3: split)
   int ntb, P, eips, PG, tpg, ec_mode, ec_ipp, ec_block, n_prod;  // EC shape
   int xlds, xstride, bpre, lds_y, lds_e, lds_b, lds_g, lds_ev, lds_sz, lds_a;
   size_t off_vtag, off_upart, off_v, off_vh, off_vl, off_u, off_ypart, off_eupart, off_gpart,
@@ -325,9 +326,18 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
       if (steps % (2 * S) != 0) return SPEAR_E_UNSUPPORTED;
       z.Sg = S;
     }
+    // 256-token tiles in one K-slice with 4-bit codes (the plain and the
+    // semi-fused epilogue): loading and multiplying waves (k_gemm_ws), on
+    // 256 x 256 tiles while those alone fill the 256 CUs, else 256 x 128
+    const bool split_ok = z.gtmw == 4 && z.Sg == 1 && z.wb == 4;
+    z.groles = !split_ok ? 1 : cdiv(M, tm) * cdiv(N, 2 * kGemmTN) >= 256 ? 3 : 2;
+    if (g_ov_gr.load() > 0) {
+      z.groles = g_ov_gr.load();
+      if (z.groles >= 2 && !split_ok) return SPEAR_E_UNSUPPORTED;
+    }
     z.plan.split_k = z.Sg;
     z.plan.tile_m = tm;
-    z.plan.tile_n = kGemmTN;
+    z.plan.tile_n = z.groles == 3 ? 2 * kGemmTN : kGemmTN;
   }
 
   // EC projection shape. Decode: one producer workgroup per (token tile,
@@ -445,7 +455,7 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   z.plan.ec_splits = z.ec ? z.P : 0;
 
   // launches and grid
-  const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, z.plan.tile_m) * cdiv(N, kGemmTN)) * z.Sg;
+  const int grid4 = z.gemv ? z.nrg * z.S : (int)(cdiv(M, z.plan.tile_m) * cdiv(N, z.plan.tile_n)) * z.Sg;
   if (!z.ec || local || fmfma) {
     z.plan.num_launches = 1;
     z.plan.grid = grid4;
@@ -671,6 +681,7 @@ GemmParams make_gemm(const spear_problem_t* p, const Resolved& z, const void* x,
   std::memset(&g, 0, sizeof(g));
   g.S = std::max(1, z.Sg);
   g.tmw = z.gtmw ? z.gtmw : 2;
+  g.roles = z.groles >= 2 ? z.groles : 1;
   if (ws && z.Sg > 1) {
     g.ypart = (float*)(ws + z.off_gpart);
     g.ctr = (uint32_t*)(ws + kCtrRows);
@@ -1210,6 +1221,7 @@ void spear_set_gemm_slices(int32_t k_slices) { g_ov_gs = k_slices > 0 ? k_slices
 void spear_set_gemv_stages(int32_t stages) { g_ov_nst = stages > 0 ? stages : 0; }
 
 void spear_set_gemm_tile(int32_t tokens) { g_ov_gt = tokens == 128 || tokens == 256 ? tokens : 0; }
+void spear_set_gemm_roles(int32_t roles) { g_ov_gr = roles >= 1 && roles <= 3 ? roles : 0; }
 
 const char* spear_status_string(spear_status_t s) {
   switch (s) {

@@ -2275,6 +2275,297 @@ __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams
 }
 
 // ---------------------------------------------------------------------------
+// Prefill GEMM with loading and multiplying waves (4-bit codes, 256 x 128
+// tiles, one K-slice; the plain and the semi-fused epilogue). In k_gemm every
+// wave dequantises its share of the next step and then multiplies, and the
+// step's barrier lines the waves up, so a SIMD runs the dequantisation's
+// VALU work and the MFMAs one after the other. Here waves 0-3 only multiply
+// (each owns 128 tokens x 64 rows: 8 x 4 MFMA tiles) and waves 4-7 only load:
+// they dequantise and store step kt+1's tiles into the free LDS buffer while
+// the multiplying waves read step kt's, and issue the loads of step kt+3.
+// Each SIMD holds one loading wave beside its multiplying ones, so the two
+// streams overlap; one barrier per step. A wave also reads 12 fragments per
+// 32 MFMAs here, not 16.
+// TNB = 1: 256 x 128 tiles, four multiplying waves (one per SIMD);
+// TNB = 2: 256 x 256 tiles, eight multiplying waves (two per SIMD, 144 KB
+// of LDS), twelve waves in all, at most 168 registers each.
+// ---------------------------------------------------------------------------
+template <int DT, int EPI, int TNB>
+__global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
+  static_assert(EPI == EPI_NONE || EPI == EPI_READY, "plain and semi-fused epilogues");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr int TM = 256, TN = kGemmTN * TNB, LR = kGemmLdsRow;
+  constexpr int TILEX = TM * LR, TILEW = TN * LR;
+  constexpr int FM = 8, FN = 4;  // a multiplying wave's 16 x 16 tiles
+  constexpr int NCW = 4 * TNB;   // multiplying waves: 2 along the tokens, 2 TNB along the rows
+  constexpr int WPT = 4 * TNB;   // code words per loading thread and step
+  uint16_t* Xs = (uint16_t*)smem;  // [2][TM][LR]
+  uint16_t* Ws = Xs + 2 * TILEX;   // [2][TN][LR]
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int M = a.M, N = a.N, K = a.K;
+  const int tiles_m = (M + TM - 1) / TM, tiles_n = (N + TN - 1) / TN;
+  // XCD banding as in k_gemm
+  int mt_i, nt_i;
+  {
+    const int b = (int)blockIdx.x, x = b & 7, j = b >> 3;
+    if ((tiles_m & 7) == 0) {
+      const int pm = tiles_m >> 3;
+      mt_i = x * pm + j % pm;
+      nt_i = j / pm;
+    } else if ((tiles_n & 7) == 0) {
+      const int pn = tiles_n >> 3;
+      nt_i = x * pn + j % pn;
+      mt_i = j / pn;
+    } else {
+      mt_i = b / tiles_n;
+      nt_i = b - mt_i * tiles_n;
+    }
+  }
+  const int m0 = mt_i * TM, n0 = nt_i * TN;
+  const int KT = K / kGemmTK;  // steps (K is a multiple of 128: an even count)
+
+  // EPI_READY: v_hi, v_lo [TM][64] and B [TN][64] (act dtype, zero past the
+  // rank, INT8 rows dequantised with their scale) for rank columns
+  // kr0 .. kr0 + 63, staged into LDS (free after the K loop) by all waves
+  constexpr int ER = 72;  // padded LDS row (halves)
+  uint16_t* vhs = (uint16_t*)smem;  // [TM][ER]
+  uint16_t* vls = vhs + TM * ER;    // [TM][ER]
+  uint16_t* bss = vls + TM * ER;    // [TN][ER]
+  auto ec_stage = [&](int kr0) {
+    const int r = a.r;
+    for (int c = tid; c < 2 * TM * 8; c += 256 * (1 + TNB)) {
+      const int lo = c >= TM * 8, cc = lo ? c - TM * 8 : c;
+      const int t = cc >> 3, col = kr0 + (cc & 7) * 8, m = m0 + t;
+      u32x4 v = u32x4{0, 0, 0, 0};
+      if (m < M && col < a.vstride) v = ldg16((lo ? a.vl : a.vh) + (size_t)m * a.vstride + col);
+      *(u32x4*)((lo ? vls : vhs) + t * ER + (cc & 7) * 8) = v;
+    }
+    for (int c = tid; c < TN * 8; c += 256 * (1 + TNB)) {
+      const int row = c >> 3, col = kr0 + (c & 7) * 8, n = n0 + row;
+      u32x4 f = u32x4{0, 0, 0, 0};
+      if (n < N && col < r) {
+        if (a.B8) {
+          const int8_t* br = a.B8 + (size_t)n * r;
+          const float sb = a.sb[n];
+          if ((r & 7) == 0) {
+            const u32x2 q = *(const u32x2*)(br + col);
+            f = i8x8_to_act<DT>(q[0], q[1], sb);
+          } else {
+            uint32_t h[8];
+#pragma unroll
+            for (int e2 = 0; e2 < 8; ++e2) h[e2] = col + e2 < r ? i8_to_act<DT>(br[col + e2], sb) : 0u;
+            f = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+          }
+        } else {
+          const uint16_t* br = a.B + (size_t)n * r;
+          if ((r & 7) == 0) {
+            f = ldg16(br + col);
+          } else {
+            uint32_t h[8];
+#pragma unroll
+            for (int e2 = 0; e2 < 8; ++e2) h[e2] = col + e2 < r ? br[col + e2] : 0u;
+            f = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+          }
+        }
+      }
+      *(u32x4*)(bss + row * ER + (c & 7) * 8) = f;
+    }
+  };
+
+  if (wave >= NCW) {
+    // ---- loading waves: thread pt stages activation chunks pt + 256 i
+    // (row c / 8, 8 halves at column 8 (c % 8)) and, of each 64-wide step,
+    // the four code words 4 (pt % 2) .. +4 of row pt / 2 (TNB = 1) or all
+    // eight of row pt (TNB = 2)
+    const int pt = tid - 64 * NCW;
+    const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
+    const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * (K / 2));
+    const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
+    const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
+    uint32_t xoff[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = pt + 256 * i, row = c >> 3;
+      xoff[i] = m0 + row < M ? ((uint32_t)(m0 + row) * K + (c & 7) * 8) * 2 : kOOB;
+    }
+    const int wr = TNB == 2 ? pt : pt >> 1, wp = TNB == 2 ? 0 : pt & 1;
+    const int wn_row = n0 + wr;
+    const bool wok = wn_row < N;
+    const uint32_t woff = wok ? (uint32_t)wn_row * (K / 2) + 16 * wp : kOOB;
+    struct Stage {
+      u32x4 x[8];
+      u32x4 w[TNB];
+      uint32_t s, z;
+    };
+    Stage g0, g1;
+    auto gload = [&](Stage& st, int kt) {
+      const uint32_t k0 = (uint32_t)kt * kGemmTK;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) st.x[i] = bld128(rx, xoff[i] + k0 * 2);
+#pragma unroll
+      for (int h = 0; h < TNB; ++h) st.w[h] = bld128(rq, wok ? woff + k0 / 2 + 16 * h : kOOB);
+      const uint32_t g = k0 / a.G;
+      st.s = bld16(rsc, wok ? ((uint32_t)wn_row * a.ngroups + g) * 2 : kOOB);
+      st.z = bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
+    };
+    auto lstore = [&](const Stage& st, int buf) {
+      uint16_t* xs = Xs + buf * TILEX;
+      uint16_t* ws = Ws + buf * TILEW;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int c = pt + 256 * i;
+        *(u32x4*)(xs + (c >> 3) * LR + (c & 7) * 8) = st.x[i];
+      }
+      const float sreg = h2f((uint16_t)st.s);
+      const int zreg = (int)st.z;
+#pragma unroll
+      for (int c = 0; c < WPT; ++c) {
+        uint32_t o[4];
+        dequant_word_pairs<DT>(st.w[c >> 2][c & 3], sreg, zreg, o);
+        *(u32x4*)(ws + wr * LR + 8 * (4 * wp + c)) = u32x4{o[0], o[1], o[2], o[3]};
+      }
+    };
+    // step kt stores step kt + 1 (loaded two steps earlier) and then loads
+    // step kt + 3 into the same registers; loads past the end re-read the
+    // last step (never stored), so that every load is unconditional
+    const int kl = KT - 1;
+    gload(g0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    gload(g1, min(1, kl));
+    __builtin_amdgcn_sched_barrier(0);
+    lstore(g0, 0);
+    gload(g0, min(2, kl));
+    __syncthreads();
+    for (int kt = 0; kt < KT; kt += 2) {
+      lstore(g1, 1);
+      gload(g1, min(kt + 3, kl));
+      __syncthreads();
+      if (kt + 2 < KT) {
+        lstore(g0, 0);
+        gload(g0, min(kt + 4, kl));
+      }
+      __syncthreads();
+    }
+    if constexpr (EPI == EPI_READY) {
+      for (int kr0 = 0; kr0 < a.vstride; kr0 += 64) {
+        ec_stage(kr0);
+        __syncthreads();
+        __syncthreads();
+      }
+    }
+    return;
+  }
+
+  // ---- multiplying waves: wave c owns tokens 128 (c / (2 TNB)) .., rows
+  // 64 (c % (2 TNB)) ..
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wm = wave / (2 * TNB), wn = wave % (2 * TNB);
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // one wave per SIMD multiplies, so it hides its own LDS latency: the
+  // second half-step's fragments are read while the first half's 32 MFMAs
+  // run (the scheduling barriers keep the compiler from sinking each read
+  // next to its first use)
+  auto compute = [&](int buf) {
+    const uint16_t* xs = Xs + buf * TILEX;
+    const uint16_t* ws = Ws + buf * TILEW;
+    if constexpr (TNB == 2) {
+      // two multiplying waves per SIMD cover each other's LDS waits; the
+      // token fragments come one at a time to stay within 168 registers
+#pragma unroll
+      for (int kk = 0; kk < kGemmTK; kk += 32) {
+        u32x4 bf[FN];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bf[j] = *(const u32x4*)(ws + (wn * 64 + 16 * j + lr) * LR + kk + 8 * lg);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const u32x4 af = *(const u32x4*)(xs + (wm * 128 + 16 * i + lr) * LR + kk + 8 * lg);
+#pragma unroll
+          for (int j = 0; j < FN; ++j) acc[i][j] = mfma16<DT>(af, bf[j], acc[i][j]);
+        }
+      }
+      return;
+    }
+    u32x4 bf[2][FN], af[2][FM];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        bf[h][j] = *(const u32x4*)(ws + (wn * 64 + 16 * j + lr) * LR + 32 * h + 8 * lg);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        af[h][i] = *(const u32x4*)(xs + (wm * 128 + 16 * i + lr) * LR + 32 * h + 8 * lg);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma16<DT>(af[h][i], bf[h][j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  __syncthreads();
+  // one copy of the step's MFMAs in the loop (two copies, one per buffer,
+  // make the register allocator shuffle accumulators between them)
+  for (int kt = 0; kt < KT; ++kt) {
+    compute(kt & 1);
+    __syncthreads();
+  }
+
+  if constexpr (EPI == EPI_READY) {
+    // y += v_hi B^T + v_lo B^T over the rank (zero-padded to vstride), 64
+    // rank columns at a time from LDS, the fragments streamed like the K loop
+    for (int kr0 = 0; kr0 < a.vstride; kr0 += 64) {
+      ec_stage(kr0);
+      __syncthreads();
+#pragma unroll
+      for (int kk = 0; kk < 64; kk += 32) {
+        if (kr0 + kk < a.vstride) {
+          u32x4 bf[FN];
+#pragma unroll
+          for (int j = 0; j < FN; ++j) bf[j] = *(const u32x4*)(bss + (wn * 64 + 16 * j + lr) * ER + kk + 8 * lg);
+#pragma unroll
+          for (int i = 0; i < FM; ++i) {
+            const int t = wm * 128 + 16 * i + lr;
+            const u32x4 vh = *(const u32x4*)(vhs + t * ER + kk + 8 * lg);
+            const u32x4 vl = *(const u32x4*)(vls + t * ER + kk + 8 * lg);
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+              acc[i][j] = mfma16<DT>(vh, bf[j], acc[i][j]);
+              acc[i][j] = mfma16<DT>(vl, bf[j], acc[i][j]);
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * 64 + 16 * j + lr;
+      if (n >= N) continue;
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        const int m = m0 + wm * 128 + 16 * i + 4 * lg + e2;
+        if (m < M) {
+          float v = acc[i][j][e2];
+          if (a.res) v += act2f<DT>(a.res[(size_t)m * N + n]);
+          a.y[(size_t)m * N + n] = f2act<DT>(v);
+        }
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 // Raise a kernel's dynamic-LDS limit when a launch needs more than 64 KB.
@@ -2481,6 +2772,34 @@ hipError_t SPEAR_W(launch_gemm)(int dt, int epi, const GemmParams& p, hipStream_
     if (err != hipSuccess) return err;                                                 \
     hipLaunchKernelGGL((k_gemm<DTC, E, W, SPEAR_WB>), dim3(grid), dim3(128 * W), lds, st, p); \
   } while (0)
+  if (p.roles == 2 || p.roles == 3) {
+    // loading and multiplying waves: 256 x 128 (roles 2) or 256 x 256
+    // (roles 3) tiles, one K-slice, 4-bit codes
+    if (p.tmw != 4 || p.S != 1 || SPEAR_WB != 4 || (epi != EPI_NONE && epi != EPI_READY))
+      return hipErrorInvalidValue;
+#if SPEAR_WB == 4
+    const int tnb = p.roles == 3 ? 2 : 1;
+    const unsigned gws = (unsigned)(tm * ((p.N + 128 * tnb - 1) / (128 * tnb)));
+    const size_t lws = (size_t)2 * (TM + 128 * tnb) * kGemmLdsRow * 2;
+#define SPEAR_GEMM_WS(E, B)                                                               \
+  do {                                                                                    \
+    hipError_t err = allow_lds(k_gemm_ws<DTC, E, B>, lws);                                \
+    if (err != hipSuccess) return err;                                                    \
+    hipLaunchKernelGGL((k_gemm_ws<DTC, E, B>), dim3(gws), dim3(256 * (1 + B)), lws, st, p); \
+  } while (0)
+    SPEAR_DT_SWITCH(dt, {
+      if (tnb == 2) {
+        if (epi == EPI_NONE) SPEAR_GEMM_WS(EPI_NONE, 2);
+        else SPEAR_GEMM_WS(EPI_READY, 2);
+      } else {
+        if (epi == EPI_NONE) SPEAR_GEMM_WS(EPI_NONE, 1);
+        else SPEAR_GEMM_WS(EPI_READY, 1);
+      }
+    });
+#undef SPEAR_GEMM_WS
+#endif
+    return hipGetLastError();
+  }
   SPEAR_DT_SWITCH(dt, {
     if (p.tmw == 4) {
       if (epi == EPI_NONE) SPEAR_GEMM_GO(EPI_NONE, 4);

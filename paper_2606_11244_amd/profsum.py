@@ -256,17 +256,20 @@ def main70(argv):
     if sq:
         names = sorted({c for v in sq.values() for c in v})
         lines += ["## SQ counters (one pass, mean per launch)", "",
-                  "MFMA utilisation = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x 256 CUs x "
-                  "4 SIMDs): the share of the SIMDs' cycles, while the kernel ran, in which the "
-                  "matrix unit was busy (SQ_VALU_MFMA_BUSY_CYCLES counts per SIMD). MFMA flops "
-                  "= SQ_INSTS_VALU_MFMA_MOPS_F16 x 512.", "",
+                  "MFMA utilisation = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x "
+                  "256 CUs x 4 SIMDs): the share of the SIMDs' cycles, while the kernel ran, in "
+                  "which the matrix unit was busy. GRBM_GUI_ACTIVE comes summed over the eight "
+                  "XCDs (divided by 8 it matches the kernel's duration at 2.4 GHz) and "
+                  "SQ_VALU_MFMA_BUSY_CYCLES summed over the SIMDs. MFMA flops = "
+                  "SQ_INSTS_VALU_MFMA_MOPS_F16 x 512 (= SQ_INSTS_MFMA x 16384 for the 16x16x32 "
+                  "MFMA).", "",
                   "| kernel | workgroups | " + " | ".join(names) + " | MFMA utilisation | "
                   "MFMA TFLOP per launch |",
                   "|---|---|" + "---|" * len(names) + "---|---|"]
         for (k, g), cs in sorted(sq.items()):
             means = {c: sum(v) / len(v) for c, v in cs.items()}
             gui = means.get("GRBM_GUI_ACTIVE", 0.0)
-            util = (means.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (gui * 256 * 4)) if gui else float("nan")
+            util = (means.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (gui / 8 * 256 * 4)) if gui else float("nan")
             tfl = means.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0.0) * 512 / 1e12
             lines.append(f"| `{k}` | {g} | " + " | ".join(f"{means.get(c, 0):,.0f}" for c in names)
                          + f" | {util:.3f} | {tfl:.4f} |")

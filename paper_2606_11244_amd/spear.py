@@ -34,7 +34,8 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
             "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
             "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
-            "spear_set_gemm_tile", "spear_workspace_regions", "spear_w4ec_linear_noalloc",
+            "spear_set_gemm_tile", "spear_set_gemm_roles", "spear_workspace_regions",
+            "spear_w4ec_linear_noalloc",
             "spear_set_gemv_stages",
             "spear_status_string", "spear_version", "spear_sched_latency", "spear_sched_chunk")
 
@@ -133,6 +134,8 @@ def _load():
     lib.spear_set_gemm_slices.restype = None
     lib.spear_set_gemm_tile.argtypes = [ctypes.c_int32]
     lib.spear_set_gemm_tile.restype = None
+    lib.spear_set_gemm_roles.argtypes = [ctypes.c_int32]
+    lib.spear_set_gemm_roles.restype = None
     lib.spear_set_gemv_stages.argtypes = [ctypes.c_int32]
     lib.spear_set_gemv_stages.restype = None
     lib.spear_sched_latency.argtypes = [P(ModelLat), ctypes.c_int64, P(ctypes.c_double)]
@@ -365,6 +368,12 @@ def set_gemv_stages(stages=0) -> None:
 def set_gemm_tile(tokens=0) -> None:
     """Tuning override of the prefill GEMM's token tile (128, 256; 0 = automatic)."""
     LIB.spear_set_gemm_tile(int(tokens))
+
+
+def set_gemm_roles(roles=0) -> None:
+    """Tuning override of the prefill GEMM's wave roles (1 = every wave both,
+    2 = loading and multiplying waves; 0 = automatic)."""
+    LIB.spear_set_gemm_roles(int(roles))
 
 
 class LatencyModel:

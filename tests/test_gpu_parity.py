@@ -501,6 +501,33 @@ def test_gemm_token_tiles(tile, M, N, K, dt, G):
         sp.set_gemm_tile(0)
 
 
+@pytest.mark.parametrize("roles", [1, 2, 3])
+@pytest.mark.parametrize("M,N,K,dt,G,rank", [
+    (300, 200, 1024, S.F16, 128, 16), (513, 520, 2048, S.BF16, 0, 64), (257, 136, 512, S.F16, 128, 12),
+    (256, 256, 1024, S.BF16, 128, 32), (600, 1000, 1536, S.F16, 0, 24), (1, 128, 256, S.F16, 128, 8)])
+def test_gemm_wave_roles(roles, M, N, K, dt, G, rank):
+    """The 256-token GEMM with every wave loading and multiplying (k_gemm)
+    and with four loading and four multiplying waves (k_gemm_ws), on ragged
+    token and row counts and ranks that are and are not multiples of eight:
+    the 4-bit product, the semi-fused EC path and the chain meet the bar."""
+    from paper_2606_11244_amd import spear as sp
+    L = S.make_layer(M=M, N=N, K=K, group_size=G, rank=rank, act_dtype=dt, seed=M + N,
+                     ec_std=0.05)
+    ref, ref4 = O.w4ec_linear(L), O.w4_linear_layer(L)
+    sp.set_gemm_tile(256)
+    sp.set_gemm_slices(1)
+    sp.set_gemm_roles(roles)
+    try:
+        log(f"gemm roles={roles} M={M} N={N} K={K} dt={dt} G={G} r={rank}")
+        assert_parity(gpu_y(L, 0 if M > 64 else PATHS["2k"], with_ec=False), ref4, f"roles={roles} w4")
+        for p in (PATHS["2k"], PATHS["chain"]):
+            assert_parity(gpu_y(L, p), ref, f"roles={roles} path={p}")
+    finally:
+        sp.set_gemm_roles(0)
+        sp.set_gemm_slices(0)
+        sp.set_gemm_tile(0)
+
+
 # ---------------------------------------------------------------------------
 # post-EC tail: residual addition + next-layer RMSNorm
 # ---------------------------------------------------------------------------
