@@ -383,8 +383,8 @@ void spear_set_gemm_tile(int32_t tokens);
 /* Tuning override of the prefill GEMM's wave roles: 1 = every wave loads,
  * dequantises and multiplies (k_gemm); 2 = four loading and four
  * multiplying waves on 256 x 128 tiles, 3 = four loading and eight
- * multiplying waves on 256 x 256 tiles (k_gemm_ws: 4-bit codes, 256-token
- * tiles, one K-slice, the plain and semi-fused epilogues; planning a problem
+ * multiplying waves on 256 x 256 tiles (k_gemm_ws: 256-token tiles, one
+ * K-slice, the plain and semi-fused epilogues; planning a problem
  * that does not allow them then returns SPEAR_E_UNSUPPORTED); 0 restores the
  * planner's choice (3 where 256 x 256 tiles fill the 256 CUs, else 2, where
  * allowed). For measurement sweeps and tests only. */

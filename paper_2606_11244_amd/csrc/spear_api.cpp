@@ -326,10 +326,10 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
       if (steps % (2 * S) != 0) return SPEAR_E_UNSUPPORTED;
       z.Sg = S;
     }
-    // 256-token tiles in one K-slice with 4-bit codes (the plain and the
-    // semi-fused epilogue): loading and multiplying waves (k_gemm_ws), on
-    // 256 x 256 tiles while those alone fill the 256 CUs, else 256 x 128
-    const bool split_ok = z.gtmw == 4 && z.Sg == 1 && z.wb == 4;
+    // 256-token tiles in one K-slice (the plain and the semi-fused
+    // epilogue): loading and multiplying waves (k_gemm_ws), on 256 x 256
+    // tiles while those alone fill the 256 CUs, else 256 x 128
+    const bool split_ok = z.gtmw == 4 && z.Sg == 1;
     z.groles = !split_ok ? 1 : cdiv(M, tm) * cdiv(N, 2 * kGemmTN) >= 256 ? 3 : 2;
     if (g_ov_gr.load() > 0) {
       z.groles = g_ov_gr.load();

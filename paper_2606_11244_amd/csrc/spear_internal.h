@@ -173,7 +173,7 @@ struct GemmParams {
   uint32_t* ctr;
   float* epart;
   int tmw;                // token waves: 2 (128-token tiles) or 4 (256, EPI_NONE / EPI_READY)
-  int roles;              // loading and multiplying waves (k_gemm_ws: tmw 4, S 1, 4-bit):
+  int roles;              // loading and multiplying waves (k_gemm_ws: tmw 4, S 1):
                           // 2 = 256 x 128 tiles, 3 = 256 x 256; else every wave both
   const uint16_t* res;    // [M][N] residual added before the output's rounding, or null
   // INT8 A and B (per-channel fp32 scales), or null: B8 for the

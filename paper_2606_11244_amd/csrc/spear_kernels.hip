@@ -2289,8 +2289,9 @@ __global__ __launch_bounds__(128 * TMW, TMW == 2 ? 2 : 1) void k_gemm(GemmParams
 // TNB = 1: 256 x 128 tiles, four multiplying waves (one per SIMD);
 // TNB = 2: 256 x 256 tiles, eight multiplying waves (two per SIMD, 144 KB
 // of LDS), twelve waves in all, at most 168 registers each.
+// WB: code width (4, or 3: three words per 32 codes).
 // ---------------------------------------------------------------------------
-template <int DT, int EPI, int TNB>
+template <int DT, int EPI, int TNB, int WB>
 __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
   static_assert(EPI == EPI_NONE || EPI == EPI_READY, "plain and semi-fused epilogues");
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -2376,11 +2377,11 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
   if (wave >= NCW) {
     // ---- loading waves: thread pt stages activation chunks pt + 256 i
     // (row c / 8, 8 halves at column 8 (c % 8)) and, of each 64-wide step,
-    // the four code words 4 (pt % 2) .. +4 of row pt / 2 (TNB = 1) or all
-    // eight of row pt (TNB = 2)
+    // the codes of K half pt % 2 of row pt / 2 (TNB = 1) or both halves of
+    // row pt (TNB = 2): per half four words, or one 3-bit block of three
     const int pt = tid - 64 * NCW;
     const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
-    const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * (K / 2));
+    const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * row_code_bytes<WB>(K));
     const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
     const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
     uint32_t xoff[8];
@@ -2392,7 +2393,7 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
     const int wr = TNB == 2 ? pt : pt >> 1, wp = TNB == 2 ? 0 : pt & 1;
     const int wn_row = n0 + wr;
     const bool wok = wn_row < N;
-    const uint32_t woff = wok ? (uint32_t)wn_row * (K / 2) + 16 * wp : kOOB;
+    const uint32_t woff = !wok ? kOOB : (uint32_t)wn_row * row_code_bytes<WB>(K) + (WB == 4 ? 16 : 12) * wp;
     struct Stage {
       u32x4 x[8];
       u32x4 w[TNB];
@@ -2404,7 +2405,10 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) st.x[i] = bld128(rx, xoff[i] + k0 * 2);
 #pragma unroll
-      for (int h = 0; h < TNB; ++h) st.w[h] = bld128(rq, wok ? woff + k0 / 2 + 16 * h : kOOB);
+      for (int h = 0; h < TNB; ++h) {
+        if constexpr (WB == 4) st.w[h] = bld128(rq, wok ? woff + k0 / 2 + 16 * h : kOOB);
+        else st.w[h] = bld96s(rq, woff, k0 / 8 * 3 + 12 * h);
+      }
       const uint32_t g = k0 / a.G;
       st.s = bld16(rsc, wok ? ((uint32_t)wn_row * a.ngroups + g) * 2 : kOOB);
       st.z = bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
@@ -2419,11 +2423,23 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
       }
       const float sreg = h2f((uint16_t)st.s);
       const int zreg = (int)st.z;
+      if constexpr (WB == 4) {
 #pragma unroll
-      for (int c = 0; c < WPT; ++c) {
-        uint32_t o[4];
-        dequant_word_pairs<DT>(st.w[c >> 2][c & 3], sreg, zreg, o);
-        *(u32x4*)(ws + wr * LR + 8 * (4 * wp + c)) = u32x4{o[0], o[1], o[2], o[3]};
+        for (int c = 0; c < WPT; ++c) {
+          uint32_t o[4];
+          dequant_word_pairs<DT>(st.w[c >> 2][c & 3], sreg, zreg, o);
+          *(u32x4*)(ws + wr * LR + 8 * (4 * wp + c)) = u32x4{o[0], o[1], o[2], o[3]};
+        }
+      } else {
+#pragma unroll
+        for (int h = 0; h < TNB; ++h) {
+          uint32_t o[16];
+          dequant_block3_pairs<DT, 0, 16>(st.w[h], sreg, zreg, o);
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            *(u32x4*)(ws + wr * LR + 8 * (4 * (wp + h) + c)) =
+                u32x4{o[4 * c], o[4 * c + 1], o[4 * c + 2], o[4 * c + 3]};
+        }
       }
     };
     // step kt stores step kt + 1 (loaded two steps earlier) and then loads
@@ -2458,7 +2474,10 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
   }
 
   // ---- multiplying waves: wave c owns tokens 128 (c / (2 TNB)) .., rows
-  // 64 (c % (2 TNB)) ..
+  // 64 (c % (2 TNB)) .. They issue ahead of the loading wave of their SIMD
+  // when both are ready: the loading waves have a step of slack, the MFMA
+  // pipe none.
+  __builtin_amdgcn_s_setprio(1);
   const int lr = lane & 15, lg = lane >> 4;
   const int wm = wave / (2 * TNB), wn = wave % (2 * TNB);
   f32x4 acc[FM][FN];
@@ -2774,18 +2793,16 @@ hipError_t SPEAR_W(launch_gemm)(int dt, int epi, const GemmParams& p, hipStream_
   } while (0)
   if (p.roles == 2 || p.roles == 3) {
     // loading and multiplying waves: 256 x 128 (roles 2) or 256 x 256
-    // (roles 3) tiles, one K-slice, 4-bit codes
-    if (p.tmw != 4 || p.S != 1 || SPEAR_WB != 4 || (epi != EPI_NONE && epi != EPI_READY))
-      return hipErrorInvalidValue;
-#if SPEAR_WB == 4
+    // (roles 3) tiles, one K-slice
+    if (p.tmw != 4 || p.S != 1 || (epi != EPI_NONE && epi != EPI_READY)) return hipErrorInvalidValue;
     const int tnb = p.roles == 3 ? 2 : 1;
     const unsigned gws = (unsigned)(tm * ((p.N + 128 * tnb - 1) / (128 * tnb)));
     const size_t lws = (size_t)2 * (TM + 128 * tnb) * kGemmLdsRow * 2;
 #define SPEAR_GEMM_WS(E, B)                                                               \
   do {                                                                                    \
-    hipError_t err = allow_lds(k_gemm_ws<DTC, E, B>, lws);                                \
+    hipError_t err = allow_lds(k_gemm_ws<DTC, E, B, SPEAR_WB>, lws);                      \
     if (err != hipSuccess) return err;                                                    \
-    hipLaunchKernelGGL((k_gemm_ws<DTC, E, B>), dim3(gws), dim3(256 * (1 + B)), lws, st, p); \
+    hipLaunchKernelGGL((k_gemm_ws<DTC, E, B, SPEAR_WB>), dim3(gws), dim3(256 * (1 + B)), lws, st, p); \
   } while (0)
     SPEAR_DT_SWITCH(dt, {
       if (tnb == 2) {
@@ -2797,7 +2814,6 @@ hipError_t SPEAR_W(launch_gemm)(int dt, int epi, const GemmParams& p, hipStream_
       }
     });
 #undef SPEAR_GEMM_WS
-#endif
     return hipGetLastError();
   }
   SPEAR_DT_SWITCH(dt, {

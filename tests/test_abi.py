@@ -349,19 +349,13 @@ def test_tagged_region_is_written_by_the_fused_path_only():
 
 
 def test_weight_code_width():
-    """3-bit codes (weight_bits = 3) take the same plan as 4-bit ones (except
-    the 256 x 256 tile of the prefill GEMM with loading waves, which is
-    4-bit only: compared with it switched off); any other width is rejected;
-    the alias checks cover the 3-bit codes' own extent (3K/8 bytes per
-    row)."""
+    """3-bit codes (weight_bits = 3) take the same plan as 4-bit ones; any
+    other width is rejected; the alias checks cover the 3-bit codes' own
+    extent (3K/8 bytes per row)."""
     for M, N, K, G in ((1, 2048, 2048, 128), (16, 8192, 2048, 128), (4096, 4096, 4096, 0),
                        (64, 28672, 8192, 128)):
         for r in (0, 16, 64):
-            sp.set_gemm_roles(1)
-            try:
-                p4 = sp.dispatch_plan(sp.problem(M, N, K, G, sp.F16, r))
-            finally:
-                sp.set_gemm_roles(0)
+            p4 = sp.dispatch_plan(sp.problem(M, N, K, G, sp.F16, r))
             p3 = sp.dispatch_plan(sp.problem(M, N, K, G, sp.F16, r, weight_bits=3))
             assert (p3.path, p3.split_k, p3.tile_m, p3.tile_n, p3.grid, p3.workspace_bytes) == \
                 (p4.path, p4.split_k, p4.tile_m, p4.tile_n, p4.grid, p4.workspace_bytes)
@@ -382,9 +376,9 @@ def test_weight_code_width():
 
 
 def test_gemm_wave_roles_rules():
-    """Loading and multiplying waves need 4-bit codes, 256-token tiles and one
-    K-slice; the hook refuses them elsewhere (planning returns
-    SPEAR_E_UNSUPPORTED) and planning is unchanged otherwise."""
+    """Loading and multiplying waves need 256-token tiles and one K-slice;
+    the hook refuses them elsewhere (planning returns SPEAR_E_UNSUPPORTED);
+    3-bit codes take the same plan as 4-bit ones."""
     q = sp.problem(4096, 8192, 8192, 128, sp.F16, 64, force_path=4)
     base = sp.dispatch_plan(q, True)
     assert (base.tile_m, base.tile_n, base.split_k) == (256, 256, 1)
@@ -399,9 +393,8 @@ def test_gemm_wave_roles_rules():
         with pytest.raises(sp.SpearError):
             sp.dispatch_plan(q, True)
         sp.set_gemm_tile(0)
-        with pytest.raises(sp.SpearError):
-            sp.dispatch_plan(sp.problem(4096, 8192, 8192, 128, sp.F16, 64, force_path=4,
-                                        weight_bits=3), True)
+        q3 = sp.problem(4096, 8192, 8192, 128, sp.F16, 64, force_path=4, weight_bits=3)
+        assert sp.dispatch_plan(q3, True).as_dict() == base.as_dict()
         sp.set_gemm_slices(2)
         with pytest.raises(sp.SpearError):
             sp.dispatch_plan(q, True)

@@ -73,6 +73,27 @@ def test_w3_paths(path, M, dt, G, rank):
     assert_parity(gpu_y(L, p, with_ec=False), O.w4_linear_layer(L), f"w3 w4-only/{path}/M={M}")
 
 
+@pytest.mark.parametrize("roles", [2, 3])
+@pytest.mark.parametrize("M,N,K,G", [(300, 384, 4096, 128), (513, 520, 2048, 0), (256, 256, 1024, 128)])
+def test_w3_gemm_wave_roles(roles, M, N, K, G):
+    """The prefill GEMM with loading and multiplying waves on 3-bit codes
+    (256 x 128 and 256 x 256 tiles), ragged token and row counts: the 3-bit
+    product and the semi-fused EC path meet the bar."""
+    from paper_2606_11244_amd import spear as sp
+    L = _w3(M=M, N=N, K=K, group_size=G, rank=24, seed=M + roles)
+    sp.set_gemm_tile(256)
+    sp.set_gemm_slices(1)
+    sp.set_gemm_roles(roles)
+    try:
+        log(f"w3 gemm roles={roles} M={M} N={N} K={K} G={G}")
+        assert_parity(gpu_y(L, 4, with_ec=False), O.w4_linear_layer(L), f"w3 roles={roles} w3-only")
+        assert_parity(gpu_y(L, 4), O.w4ec_linear(L), f"w3 roles={roles} 2k")
+    finally:
+        sp.set_gemm_roles(0)
+        sp.set_gemm_slices(0)
+        sp.set_gemm_tile(0)
+
+
 @pytest.mark.parametrize("tile", [128, 256])
 @pytest.mark.parametrize("slices", [1, 2, 8])
 def test_w3_gemm_tiles_split_k(tile, slices):
@@ -80,11 +101,13 @@ def test_w3_gemm_tiles_split_k(tile, slices):
     L = _w3(M=300, N=384, K=4096, group_size=128, rank=16, seed=5)
     sp.set_gemm_tile(tile)
     sp.set_gemm_slices(slices)
+    sp.set_gemm_roles(1)  # every wave loads and multiplies (k_gemm)
     try:
         for p in ((0, 4) if tile == 128 else (4,)):  # the 256-token tile: not fully fused
             log(f"w3 gemm tile={tile} slices={slices} path={p}")
             assert_parity(gpu_y(L, p), O.w4ec_linear(L), f"w3 tile={tile} S={slices} p={p}")
     finally:
+        sp.set_gemm_roles(0)
         sp.set_gemm_tile(0)
         sp.set_gemm_slices(0)
 
