@@ -795,9 +795,11 @@ def main():
             "value": round(pre_tfl, 2), "unit": "TFLOP/s", "ms_per_pass": round(pre_s * 1e3, 4),
             "roofline": {
                 "bound": "mfma",
-                "kernel": ("every launch of the prefill pass: the 4-bit GEMM k_gemm (EPI_NONE) "
-                           "without an EC; k_ec + k_gemm with the EC epilogue (EPI_READY) with "
-                           "one"),
+                "kernel": ("every launch of the prefill pass: the 4-bit GEMM with loading and "
+                           "multiplying waves k_gemm_ws (EPI_NONE; 256 x 256 tiles, 256 x 128 "
+                           "on q/o-sized layers if 256 x 256 would not fill the CUs) or, on the "
+                           "1024-row k and v modules, the split-K k_gemm, without an EC; k_ec + "
+                           "the same GEMM with the EC epilogue (EPI_READY) with one"),
                 "achieved": round(pre_tfl, 2), "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(pre_tfl / MFMA_F16_PEAK_TFLOPS, 4),
                 "traffic": (traffic or {}).get("prefill_bytes_per_launch"),
