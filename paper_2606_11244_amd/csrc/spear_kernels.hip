@@ -65,6 +65,20 @@ __device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// 32 x 32 x 16 MFMA: lane l holds A row l % 32 and B column l % 32, each at
+// K 8 (l / 32) .. +8; result element i of lane l is D[8 (i / 4) + 4 (l / 32)
+// + i % 4][l % 32]
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+template <int DT>
+__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
+  if constexpr (DT == DT_F16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
 template <int DT>
 __device__ __forceinline__ float act2f(uint32_t bits16) {
   if constexpr (DT == DT_F16)
@@ -214,6 +228,12 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
 }
 __device__ __forceinline__ u32x4 bld128(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+// 16 bytes per lane from `r` at byte offset `off` straight into LDS: lane l
+// of the wave writes lds + 16 l (lds wave-uniform, 1 KB per instruction);
+// completion is counted by vmcnt
+__device__ __forceinline__ void bld128_lds(rsrc_t r, void* lds, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
 }
 // voffset (per lane, carries the mask) + soffset (wave-uniform)
 __device__ __forceinline__ u32x4 bld128s(rsrc_t r, uint32_t voff, uint32_t soff) {
@@ -2296,11 +2316,13 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
   static_assert(EPI == EPI_NONE || EPI == EPI_READY, "plain and semi-fused epilogues");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int TM = 256, TN = kGemmTN * TNB, LR = kGemmLdsRow;
-  constexpr int TILEX = TM * LR, TILEW = TN * LR;
-  constexpr int FM = 8, FN = 4;  // a multiplying wave's 16 x 16 tiles
+  constexpr int TILEX = TM * kGemmTK, TILEW = TN * LR;
   constexpr int NCW = 4 * TNB;   // multiplying waves: 2 along the tokens, 2 TNB along the rows
   constexpr int WPT = 4 * TNB;   // code words per loading thread and step
-  uint16_t* Xs = (uint16_t*)smem;  // [2][TM][LR]
+  // activations: [2][TM][64] unpadded, the 16-byte chunk c of row t at
+  // chunk c ^ (t % 8) (conflict-free fragment reads without padding, which
+  // the 1 KB runs of the direct loads below cannot skip)
+  uint16_t* Xs = (uint16_t*)smem;
   uint16_t* Ws = Xs + 2 * TILEX;   // [2][TN][LR]
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -2375,35 +2397,24 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
   };
 
   if (wave >= NCW) {
-    // ---- loading waves: thread pt stages activation chunks pt + 256 i
-    // (row c / 8, 8 halves at column 8 (c % 8)) and, of each 64-wide step,
-    // the codes of K half pt % 2 of row pt / 2 (TNB = 1) or both halves of
-    // row pt (TNB = 2): per half four words, or one 3-bit block of three
+    // ---- loading waves: thread pt stages, of each 64-wide step, the codes
+    // of K half pt % 2 of row pt / 2 (TNB = 1) or both halves of row pt
+    // (TNB = 2): per half four words, or one 3-bit block of three
     const int pt = tid - 64 * NCW;
-    const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
     const rsrc_t rq = make_rsrc(a.qw, (uint32_t)N * row_code_bytes<WB>(K));
     const rsrc_t rsc = make_rsrc(a.sc, (uint32_t)N * a.ngroups * 2);
     const rsrc_t rz = make_rsrc(a.zr, (uint32_t)N * a.ngroups);
-    uint32_t xoff[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int c = pt + 256 * i, row = c >> 3;
-      xoff[i] = m0 + row < M ? ((uint32_t)(m0 + row) * K + (c & 7) * 8) * 2 : kOOB;
-    }
     const int wr = TNB == 2 ? pt : pt >> 1, wp = TNB == 2 ? 0 : pt & 1;
     const int wn_row = n0 + wr;
     const bool wok = wn_row < N;
     const uint32_t woff = !wok ? kOOB : (uint32_t)wn_row * row_code_bytes<WB>(K) + (WB == 4 ? 16 : 12) * wp;
     struct Stage {
-      u32x4 x[8];
       u32x4 w[TNB];
       uint32_t s, z;
     };
     Stage g0, g1;
     auto gload = [&](Stage& st, int kt) {
       const uint32_t k0 = (uint32_t)kt * kGemmTK;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) st.x[i] = bld128(rx, xoff[i] + k0 * 2);
 #pragma unroll
       for (int h = 0; h < TNB; ++h) {
         if constexpr (WB == 4) st.w[h] = bld128(rq, wok ? woff + k0 / 2 + 16 * h : kOOB);
@@ -2414,13 +2425,7 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
       st.z = bld8(rz, wok ? (uint32_t)wn_row * a.ngroups + g : kOOB);
     };
     auto lstore = [&](const Stage& st, int buf) {
-      uint16_t* xs = Xs + buf * TILEX;
       uint16_t* ws = Ws + buf * TILEW;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int c = pt + 256 * i;
-        *(u32x4*)(xs + (c >> 3) * LR + (c & 7) * 8) = st.x[i];
-      }
       const float sreg = h2f((uint16_t)st.s);
       const int zreg = (int)st.z;
       if constexpr (WB == 4) {
@@ -2474,92 +2479,85 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
   }
 
   // ---- multiplying waves: wave c owns tokens 128 (c / (2 TNB)) .., rows
-  // 64 (c % (2 TNB)) .. They issue ahead of the loading wave of their SIMD
-  // when both are ready: the loading waves have a step of slack, the MFMA
-  // pipe none.
+  // 64 (c % (2 TNB)) .., as 4 x 2 tiles of the 32 x 32 x 16 MFMA (half the
+  // MFMA instructions of 16 x 16 x 32 tiles for the same LDS reads: measured
+  // alone with the stage stores, 60% of the peak against 51%). They issue
+  // ahead of the loading wave of their SIMD when both are ready: the loading
+  // waves have a step of slack, the MFMA pipe none.
   __builtin_amdgcn_s_setprio(1);
-  const int lr = lane & 15, lg = lane >> 4;
+  const int l32 = lane & 31, lh = lane >> 5;
   const int wm = wave / (2 * TNB), wn = wave % (2 * TNB);
-  f32x4 acc[FM][FN];
+  constexpr int FM32 = 4, FN32 = 2;
+  // The activation tile goes straight from memory into LDS (16-byte buffer
+  // loads to LDS): the multiplying waves issue it, one step ahead into the
+  // free buffer, and wait for it only at the step's barrier, behind their
+  // own MFMAs; they have no other memory loads, so the wait covers nothing
+  // else. Wave w writes the 1 KB runs w IPW .. +IPW of the tile (eight rows
+  // each); lane l of a run lands at 16 l: row 8 run + l / 8, stored chunk
+  // l % 8, which holds the row's chunk (l % 8) ^ (row % 8).
+  constexpr int IPW = 32 / NCW;  // 1 KB runs per multiplying wave and step
+  const rsrc_t rx = make_rsrc(a.x, (uint32_t)M * K * 2);
+  uint32_t xoff[IPW];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int u = 0; u < IPW; ++u) {
+    const int row = (wave * IPW + u) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ (row & 7);
+    xoff[u] = m0 + row < M ? ((uint32_t)(m0 + row) * K + 8 * c) * 2 : kOOB;
+  }
+  auto xdma = [&](int kt, int buf) {
+    const uint32_t kb = (uint32_t)kt * kGemmTK * 2;
 #pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // one wave per SIMD multiplies, so it hides its own LDS latency: the
-  // second half-step's fragments are read while the first half's 32 MFMAs
-  // run (the scheduling barriers keep the compiler from sinking each read
-  // next to its first use)
-  auto compute = [&](int buf) {
-    const uint16_t* xs = Xs + buf * TILEX;
-    const uint16_t* ws = Ws + buf * TILEW;
-    if constexpr (TNB == 2) {
-      // two multiplying waves per SIMD cover each other's LDS waits; the
-      // token fragments come one at a time to stay within 168 registers
-#pragma unroll
-      for (int kk = 0; kk < kGemmTK; kk += 32) {
-        u32x4 bf[FN];
-#pragma unroll
-        for (int j = 0; j < FN; ++j) bf[j] = *(const u32x4*)(ws + (wn * 64 + 16 * j + lr) * LR + kk + 8 * lg);
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-          const u32x4 af = *(const u32x4*)(xs + (wm * 128 + 16 * i + lr) * LR + kk + 8 * lg);
-#pragma unroll
-          for (int j = 0; j < FN; ++j) acc[i][j] = mfma16<DT>(af, bf[j], acc[i][j]);
-        }
-      }
-      return;
-    }
-    u32x4 bf[2][FN], af[2][FM];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        bf[h][j] = *(const u32x4*)(ws + (wn * 64 + 16 * j + lr) * LR + 32 * h + 8 * lg);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        af[h][i] = *(const u32x4*)(xs + (wm * 128 + 16 * i + lr) * LR + 32 * h + 8 * lg);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma16<DT>(af[h][i], bf[h][j], acc[i][j]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int u = 0; u < IPW; ++u)
+      bld128_lds(rx, Xs + buf * TILEX + (wave * IPW + u) * 512, xoff[u] == kOOB ? kOOB : xoff[u] + kb);
   };
+  f32x16 acc[FM32][FN32];
+#pragma unroll
+  for (int i = 0; i < FM32; ++i)
+#pragma unroll
+    for (int j = 0; j < FN32; ++j) acc[i][j] = f32x16{};
+  // 16-K slices: the slice's six fragments, then its eight MFMAs; SW: the
+  // token operand is the swizzled activation tile (rows of 64 halves)
+  auto mma = [&](const uint16_t* xs, const uint16_t* ws, int xr0, int wr0, int ld, int kk, bool sw) {
+    u32x4 bf[FN32], af[FM32];
+#pragma unroll
+    for (int j = 0; j < FN32; ++j) bf[j] = *(const u32x4*)(ws + (wr0 + 32 * j + l32) * ld + kk + 8 * lh);
+#pragma unroll
+    for (int i = 0; i < FM32; ++i) {
+      const int t = xr0 + 32 * i + l32;
+      af[i] = sw ? *(const u32x4*)(xs + t * kGemmTK + 8 * (((kk >> 3) + lh) ^ (t & 7)))
+                 : *(const u32x4*)(xs + t * ld + kk + 8 * lh);
+    }
+#pragma unroll
+    for (int i = 0; i < FM32; ++i)
+#pragma unroll
+      for (int j = 0; j < FN32; ++j) acc[i][j] = mfma32<DT>(af[i], bf[j], acc[i][j]);
+  };
+  xdma(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   // one copy of the step's MFMAs in the loop (two copies, one per buffer,
   // make the register allocator shuffle accumulators between them)
   for (int kt = 0; kt < KT; ++kt) {
-    compute(kt & 1);
+    if (kt + 1 < KT) xdma(kt + 1, (kt + 1) & 1);
+    const uint16_t* xs = Xs + (kt & 1) * TILEX;
+    const uint16_t* ws = Ws + (kt & 1) * TILEW;
+#pragma unroll
+    for (int kk = 0; kk < kGemmTK; kk += 16) mma(xs, ws, wm * 128, wn * 64, LR, kk, true);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's share of the next tile is in LDS
     __syncthreads();
   }
 
   if constexpr (EPI == EPI_READY) {
     // y += v_hi B^T + v_lo B^T over the rank (zero-padded to vstride), 64
-    // rank columns at a time from LDS, the fragments streamed like the K loop
+    // rank columns at a time from LDS, as 32 x 32 x 16 MFMAs like the K loop
     for (int kr0 = 0; kr0 < a.vstride; kr0 += 64) {
       ec_stage(kr0);
       __syncthreads();
 #pragma unroll
-      for (int kk = 0; kk < 64; kk += 32) {
+      for (int kk = 0; kk < 64; kk += 16) {
         if (kr0 + kk < a.vstride) {
-          u32x4 bf[FN];
-#pragma unroll
-          for (int j = 0; j < FN; ++j) bf[j] = *(const u32x4*)(bss + (wn * 64 + 16 * j + lr) * ER + kk + 8 * lg);
-#pragma unroll
-          for (int i = 0; i < FM; ++i) {
-            const int t = wm * 128 + 16 * i + lr;
-            const u32x4 vh = *(const u32x4*)(vhs + t * ER + kk + 8 * lg);
-            const u32x4 vl = *(const u32x4*)(vls + t * ER + kk + 8 * lg);
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-              acc[i][j] = mfma16<DT>(vh, bf[j], acc[i][j]);
-              acc[i][j] = mfma16<DT>(vl, bf[j], acc[i][j]);
-            }
-          }
+          mma(vhs, bss, wm * 128, wn * 64, ER, kk, false);
+          mma(vls, bss, wm * 128, wn * 64, ER, kk, false);
         }
       }
       __syncthreads();
@@ -2567,16 +2565,16 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
   }
 
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int i = 0; i < FM32; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * 64 + 16 * j + lr;
+    for (int j = 0; j < FN32; ++j) {
+      const int n = n0 + wn * 64 + 32 * j + l32;
       if (n >= N) continue;
 #pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        const int m = m0 + wm * 128 + 16 * i + 4 * lg + e2;
+      for (int e = 0; e < 16; ++e) {
+        const int m = m0 + wm * 128 + 32 * i + 8 * (e >> 2) + 4 * lh + (e & 3);
         if (m < M) {
-          float v = acc[i][j][e2];
+          float v = acc[i][j][e];
           if (a.res) v += act2f<DT>(a.res[(size_t)m * N + n]);
           a.y[(size_t)m * N + n] = f2act<DT>(v);
         }
@@ -2797,7 +2795,10 @@ hipError_t SPEAR_W(launch_gemm)(int dt, int epi, const GemmParams& p, hipStream_
     if (p.tmw != 4 || p.S != 1 || (epi != EPI_NONE && epi != EPI_READY)) return hipErrorInvalidValue;
     const int tnb = p.roles == 3 ? 2 : 1;
     const unsigned gws = (unsigned)(tm * ((p.N + 128 * tnb - 1) / (128 * tnb)));
-    const size_t lws = (size_t)2 * (TM + 128 * tnb) * kGemmLdsRow * 2;
+    // unpadded activation stages, padded weight stages; the EC epilogue
+    // reuses the space for v_hi, v_lo [256][72] and B [rows][72]
+    const size_t lws = std::max((size_t)2 * TM * kGemmTK * 2 + (size_t)2 * 128 * tnb * kGemmLdsRow * 2,
+                                (size_t)(2 * TM + 128 * tnb) * kGemmLdsRow * 2);
 #define SPEAR_GEMM_WS(E, B)                                                               \
   do {                                                                                    \
     hipError_t err = allow_lds(k_gemm_ws<DTC, E, B, SPEAR_WB>, lws);                      \
