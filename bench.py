@@ -6,9 +6,11 @@ Llama-2-70B-shaped model that fits one GPU: all 80 layers x 7 linear modules
 group-128 4-bit weights resident in HBM (about 36 GB of device-random codes,
 scales and zero points), the EC (rank 64, sigmoid-linear gate, fp16) on the
 seeded 25% of the (layer, module) pairs and the 4-bit product alone on the
-rest, every call on its automatic-dispatch path:
+rest, every call on its automatic-dispatch path, the modules of a block that
+read one hidden state (q, k, v; gate, up) as grouped calls (members that take
+one GEMV variant share a launch; the others run on their own):
 
-  decode   M = 1: every module once (560 calls);
+  decode   M = 1: every module once;
   prefill  M = 4096 tokens: every module once.
 
 Each pass is captured once as a HIP graph and replayed. The printed JSON line
@@ -48,6 +50,12 @@ DEC_M, PRE_M = 1, 4096  # the metric's decode and prefill token counts
 # per decoder layer, the modules that read one hidden state (q, k, v; gate,
 # up) go out as one grouped call; o and down alone
 DEC_GROUPS = ((0, 1, 2), (3,), (4, 5), (6,))
+
+
+# the 70B-shaped model's decode and prefill passes call the modules of a
+# block that read one hidden state (q, k, v; gate, up) as grouped calls: the
+# members of one GEMV variant share a launch, the others run on their own
+GROUPS_70B = (("q", "k", "v"), ("o",), ("gate", "up"), ("down",))
 
 
 def algo_bytes(M, N, K, G, r, ab_int8=False, wbits=4):
@@ -166,7 +174,9 @@ class Model70B:
         g = torch.Generator(device=dev)
         g.manual_seed(1)
         self.xbuf = torch.randn((Mmax * Kmax,), device=dev, generator=g).half()
-        self.ybuf = torch.empty((Mmax * Nmax,), dtype=torch.float16, device=dev)
+        # each member of a grouped call writes its own slice
+        ny = max(sum(S.LLAMA_70B[m][1] for m in grp) for grp in GROUPS_70B)
+        self.ybuf = torch.empty((Mmax * max(ny, Nmax),), dtype=torch.float16, device=dev)
         self.dev = dev
 
     def plans(self, M):
@@ -180,26 +190,56 @@ class Model70B:
                                  weight_bits=self.wb))
         return out
 
+    def calls(self, M, with_ec):
+        """The pass as a list of calls: ("one", args of a single call) or
+        ("group", members of a grouped call: q, k, v and gate, up, which read
+        one hidden state)."""
+        plans = self.plans(M)
+        out = []
+        for mods in self.layers:
+            byname = {mod[0]: mod for mod in mods}
+            for grp in GROUPS_70B:
+                members, off = [], 0
+                for name in grp:
+                    (m, K, N, q, sc, zr, ec) = byname[name]
+                    pe, p4 = plans[m]
+                    use_ec = with_ec and ec is not None
+                    x = self.xbuf[:M * K].view(M, K)
+                    y = self.ybuf[off:off + M * N].view(M, N)
+                    off += M * N
+                    members.append(dict(prob=pe if use_ec else p4, x=x, qweight=q, scales=sc,
+                                        zeros=zr, y=y,
+                                        ec_args=dict(A=ec[0], B=ec[1], w_g=ec[2]) if use_ec else None))
+                if len(members) == 1:
+                    out.append(("one", members[0]))
+                else:
+                    out.append(("group", members))
+        return out
+
     def workspace(self, M):
         sp = self.sp
         need = 256
         for pe, p4 in self.plans(M).values():
             need = max(need, sp.dispatch_plan(pe).workspace_bytes,
                        sp.dispatch_plan(p4, with_ec=False).workspace_bytes)
+        for with_ec in (True, False):
+            for kind, c in self.calls(M, with_ec):
+                if kind == "group":
+                    need = max(need, sp.group_workspace(c))
         return self.torch.zeros(need, dtype=self.torch.uint8, device=self.dev)
 
     def run(self, M, with_ec, ws):
         sp = self.sp
-        plans = self.plans(M)
-        for mods in self.layers:
-            for (m, K, N, q, sc, zr, ec) in mods:
-                x = self.xbuf[:M * K].view(M, K)
-                y = self.ybuf[:M * N].view(M, N)
-                pe, p4 = plans[m]
-                if with_ec and ec is not None:
-                    sp.w4ec_linear(pe, x, q, sc, zr, ec[0], ec[1], y, w_g=ec[2], workspace=ws)
-                else:
-                    sp.w4_linear(p4, x, q, sc, zr, y, workspace=ws)
+        for kind, c in self.calls(M, with_ec):
+            if kind == "group":
+                sp.w4ec_linear_group(c, ws)
+            elif c["ec_args"] is not None:
+                e = c["ec_args"]
+                sp.w4ec_linear(c["prob"], c["x"], c["qweight"], c["scales"], c["zeros"], e["A"],
+                               e["B"], c["y"], w_g=e["w_g"], workspace=ws)
+            else:
+                sp.w4_linear(c["prob"], c["x"], c["qweight"], c["scales"], c["zeros"], c["y"],
+                             workspace=ws)
 
     def capture(self, M, with_ec, ws):
         torch = self.torch
@@ -218,17 +258,18 @@ class Model70B:
     def work(self, M, with_ec=True):
         """(algorithmic bytes, algorithmic flops, launches) of one pass."""
         sp = self.sp
-        plans = self.plans(M)
         nbytes = flops = 0.0
         launches = 0
-        for mods in self.layers:
-            for (m, K, N, q, sc, zr, ec) in mods:
-                r = self.r if (with_ec and ec is not None) else 0
-                nbytes += algo_bytes(M, N, K, self.G, r, wbits=self.wb)
-                flops += algo_flops(M, N, K, r)
-                pe, p4 = plans[m]
-                launches += (sp.dispatch_plan(pe).num_launches if r
-                             else sp.dispatch_plan(p4, with_ec=False).num_launches)
+        for kind, c in self.calls(M, with_ec):
+            for mem in (c if kind == "group" else [c]):
+                p = mem["prob"]
+                r = p.rank if mem["ec_args"] is not None else 0
+                nbytes += algo_bytes(M, p.N, p.K, self.G, r, wbits=self.wb)
+                flops += algo_flops(M, p.N, p.K, r)
+            if kind == "group":
+                launches += sp.group_launches(c)
+            else:
+                launches += sp.dispatch_plan(c["prob"], with_ec=c["ec_args"] is not None).num_launches
         return nbytes, flops, launches
 
     def paths(self, M):
@@ -771,7 +812,8 @@ def main():
                          "down 28672->8192), group-128 int4, EC rank 64 with the sigmoid-linear "
                          "gate on a seeded 25%% of the modules (%d of %d), 4-bit only on the "
                          "rest, fp16 activations; one step = decode pass M=1 + prefill pass "
-                         "M=4096, every module once on its AUTO path" % (int(sel.sum()), sel.size)),
+                         "M=4096, every module once on its AUTO path, q/k/v and gate/up as "
+                         "grouped calls" % (int(sel.sum()), sel.size)),
             "group_size": GROUP, "rank": 64, "gate": "sigmoid_linear",
             "decode_M": DEC_M, "prefill_M": PRE_M,
             "decode_paths": paths_dec, "prefill_paths": paths_pre,
@@ -779,8 +821,9 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": ("every launch of the decode pass: the 4-bit GEMV (k_gemv, EPI_NONE) on "
-                       "the modules without an EC, the producer-fused W4+EC GEMV (k_gemv, "
+            "kernel": ("every launch of the decode pass: the 4-bit GEMV (k_gemv, EPI_NONE; "
+                       "k_gemv_group where modules of a grouped call without an EC share a "
+                       "launch) on the modules without an EC, the producer-fused W4+EC GEMV (k_gemv, "
                        "EPI_FUSED) on those with one, and on the 28672-deep down modules the EC "
                        "pre-kernel k_ec + k_gemv (EPI_READY)"),
             "achieved": round(dec_bytes / dec_launches / (dec_s / dec_launches) / 1e9, 2),

@@ -281,16 +281,20 @@ spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x
  * weights (section 4.1: launch overhead, not arithmetic, dominates the decode
  * path), and the modules of a transformer block that read the same hidden
  * state (q, k, v; gate, up) are independent calls. A group runs up to
- * SPEAR_GROUP_MAX such calls as one launch when all of them take the same
- * single-launch GEMV variant: the 4-bit product alone (ec NULL) or the fused
- * local path (M <= 32, an elementwise gate and rank <= 16, where the planner
- * takes that path), with the same act dtype, token tiles and row tiles.
- * Local-EC members whose blocks together exceed one round on the GPU are
- * then launched on four row tiles each, when that leaves their K-slices and
- * per-wave work unchanged. Otherwise the members run one after another in
- * array order, each on its own planned path. Either way each member's Y is
- * exactly (bit for bit) what its own spear_w4ec_linear or spear_w4_linear
- * call writes. */
+ * SPEAR_GROUP_MAX such calls, and the members that take one single-launch
+ * GEMV variant share one launch: the 4-bit product alone (ec NULL) or the
+ * fused local path (M <= 32, an elementwise gate and rank <= 16, where the
+ * planner takes that path), with the same act dtype, code width and token
+ * tiles. Of several such sets the largest (at least two members) shares the
+ * launch. Its members are re-planned to one row-tile count where their own
+ * plans differ and the re-plan leaves every member's K-slices and per-wave
+ * work unchanged (the largest such count); local-EC members whose blocks
+ * together exceed one round on the GPU then take four row tiles each under
+ * the same condition. The other members (other variants, token counts
+ * beyond the GEMV, a tiling that cannot be shared) run first, one after
+ * another in array order on the same stream, each on its own planned path.
+ * Either way each member's Y is exactly (bit for bit) what its own
+ * spear_w4ec_linear or spear_w4_linear call writes. */
 #define SPEAR_GROUP_MAX 4
 
 /* One member: a problem and its operands as in spear_w4ec_linear; ec NULL
@@ -314,6 +318,12 @@ typedef struct {
  * SPEAR_E_SHAPE for n outside [1, SPEAR_GROUP_MAX], and every code
  * spear_dispatch_plan returns for a member. */
 spear_status_t spear_group_workspace(int32_t n, const spear_layer_call_t* calls, size_t* out_bytes);
+
+/* Kernel launches a spear_w4ec_linear_group call with these members makes:
+ * one for the members that share a launch, plus each other member's own
+ * launch count (spear_plan_t.num_launches). Host-only. Errors as in
+ * spear_group_workspace. */
+spear_status_t spear_group_launches(int32_t n, const spear_layer_call_t* calls, int32_t* out_launches);
 
 /* Runs the n members (see above) on hip_stream. Validation of every member
  * (the single calls' checks) happens before any launch; in addition each

@@ -1058,10 +1058,102 @@ spear_status_t spear_w4ec_linear_tail(const spear_problem_t* prob, const void* x
                                    (int)prob->N, s));
 }
 
+// The members of a grouped call that share one launch: those that run one
+// single-launch GEMV variant (same variant, dtype, code width and token
+// tiles), the largest such set of at least two members. in[i] marks them
+// (their plans in z re-planned to one tiling where needed); returns their
+// count (0: every member runs on its own), with the launch's variant in
+// *epi_out and its first member in *first_out.
+int group_select(int32_t n, const spear_layer_call_t* calls, Resolved* z, bool* in, int* epi_out,
+                 int* first_out) {
+  int key[SPEAR_GROUP_MAX];
+  for (int i = 0; i < n; ++i) {
+    const bool live = calls[i].prob->M > 0 && calls[i].prob->N > 0;
+    const int epi_i = live ? group_epi(z[i], calls[i].ec) : -1;
+    key[i] = epi_i < 0 ? -1 : ((epi_i * 2 + z[i].dt) * 8 + z[i].wb) * 64 + z[i].MT;
+  }
+  for (int i = 0; i < n; ++i) in[i] = false;
+  int best = -1, best_cnt = 1;
+  for (int i = 0; i < n; ++i) {
+    if (key[i] < 0) continue;
+    int cnt = 0;
+    for (int j = 0; j < n; ++j) cnt += key[j] == key[i];
+    if (cnt > best_cnt) best = key[i], best_cnt = cnt;
+  }
+  for (int i = 0; i < n; ++i) in[i] = best >= 0 && key[i] == best;
+  int first = -1;
+  for (int i = 0; i < n && first < 0; ++i)
+    if (in[i]) first = i;
+  const int epi = first >= 0 ? group_epi(z[first], calls[first].ec) : -1;
+  // One launch needs one row-tile count and one wave count. Members that
+  // differ are re-planned to a common row-tile count when that changes
+  // nothing but the row tiling (same K-slices, iterations per wave and
+  // waves, so the same sums in the same order); the largest such count
+  // (fewest workgroups) wins. Without one, the set keeps the members that
+  // share the first member's tiling.
+  if (first >= 0) {
+    bool same = true;
+    for (int i = 0; i < n; ++i)
+      if (in[i]) same = same && z[i].RT == z[first].RT && z[i].NW == z[first].NW;
+    if (!same) {
+      Resolved zz[SPEAR_GROUP_MAX];
+      bool found = false;
+      for (int rt = 4; rt >= 1 && !found; rt /= 2) {
+        bool ok = true;
+        for (int i = 0; i < n && ok; ++i) {
+          if (!in[i]) continue;
+          ok = resolve(calls[i].prob, calls[i].ec != nullptr, &zz[i], rt) == SPEAR_OK &&
+               group_epi(zz[i], calls[i].ec) == epi && zz[i].RT == rt && zz[i].S == z[i].S &&
+               zz[i].ips == z[i].ips && zz[i].iw == z[i].iw && zz[i].NW == z[i].NW &&
+               zz[i].NW == z[first].NW &&
+               zz[i].plan.workspace_bytes <= z[i].plan.workspace_bytes;
+        }
+        if (ok) {
+          found = true;
+          for (int i = 0; i < n; ++i)
+            if (in[i]) z[i] = zz[i];
+        }
+      }
+      if (!found)
+        for (int i = 0; i < n; ++i)
+          if (in[i]) in[i] = z[i].RT == z[first].RT && z[i].NW == z[first].NW;
+    }
+  }
+  int n_in = 0, ctrs = 0;
+  for (int i = 0; i < n; ++i)
+    if (in[i]) {
+      ++n_in;
+      if (z[i].S > 1) ctrs += z[i].nrg;
+    }
+  if (n_in < 2 || ctrs > kMaxRowCounters) {
+    for (int i = 0; i < n; ++i) in[i] = false;
+    n_in = 0;
+  }
+  *epi_out = epi;
+  *first_out = first;
+  return n_in;
+}
+
 spear_status_t spear_group_workspace(int32_t n, const spear_layer_call_t* calls, size_t* out_bytes) {
   Resolved z[SPEAR_GROUP_MAX];
   size_t off[SPEAR_GROUP_MAX];
   return group_resolve(n, calls, z, off, out_bytes);
+}
+
+spear_status_t spear_group_launches(int32_t n, const spear_layer_call_t* calls, int32_t* out_launches) {
+  if (!out_launches) return SPEAR_E_NULL;
+  Resolved z[SPEAR_GROUP_MAX];
+  size_t off[SPEAR_GROUP_MAX], total = 0;
+  const spear_status_t st = group_resolve(n, calls, z, off, &total);
+  if (st != SPEAR_OK) return st;
+  bool in[SPEAR_GROUP_MAX];
+  int epi = -1, first = -1;
+  const int n_in = group_select(n, calls, z, in, &epi, &first);
+  int32_t launches = n_in > 0 ? 1 : 0;
+  for (int i = 0; i < n; ++i)
+    if (!in[i] && calls[i].prob->M > 0 && calls[i].prob->N > 0) launches += z[i].plan.num_launches;
+  *out_launches = launches;
+  return SPEAR_OK;
 }
 
 spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* calls, void* workspace,
@@ -1095,38 +1187,33 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
         return SPEAR_E_ALIAS;
   }
   hipStream_t s = (hipStream_t)hip_stream;
-  // one launch when every member runs the same single-launch GEMV variant
-  // and their split-K counters fit the counter block together
-  int epi = group_epi(z[0], calls[0].ec);
-  bool one = n > 1 && epi >= 0;
-  int ctrs = 0;
-  for (int i = 0; i < n && one; ++i) {
-    one = group_epi(z[i], calls[i].ec) == epi && z[i].dt == z[0].dt && z[i].wb == z[0].wb &&
-          z[i].MT == z[0].MT &&
-          z[i].RT == z[0].RT && z[i].NW == z[0].NW;
-    if (z[i].S > 1) ctrs += z[i].nrg;
+  // Members of one single-launch GEMV variant share one launch; the other
+  // members run one after another on the same stream, as their own calls
+  // would. Every member's output is the one its own call writes.
+  bool in[SPEAR_GROUP_MAX];
+  int epi = -1, first = -1;
+  const int n_in = group_select(n, calls, z, in, &epi, &first);
+  for (int i = 0; i < n; ++i) {
+    const spear_layer_call_t& c = calls[i];
+    if (in[i] || c.prob->M == 0 || c.prob->N == 0) continue;
+    st = run_layer(c.prob, z[i], c.x, c.w, c.ec, c.y, nullptr, ws, s);
+    if (st != SPEAR_OK) return st;
   }
-  if (!one || ctrs > kMaxRowCounters) {
-    for (int i = 0; i < n; ++i) {
-      const spear_layer_call_t& c = calls[i];
-      if (c.prob->M == 0 || c.prob->N == 0) continue;
-      st = run_layer(c.prob, z[i], c.x, c.w, c.ec, c.y, nullptr, ws, s);
-      if (st != SPEAR_OK) return st;
-    }
-    return SPEAR_OK;
-  }
+  if (n_in == 0) return SPEAR_OK;
   // local EC members whose blocks exceed one round together take four row
   // tiles each when that changes nothing but the row tiling (same K-slices,
   // iterations per wave and waves, so the same sums in the same order): the
   // staged A limits the local variant to one block per CU
-  if ((epi == EPI_LOCAL || epi == EPI_LOCAL_I8) && z[0].MT == 1) {
+  if ((epi == EPI_LOCAL || epi == EPI_LOCAL_I8) && z[first].MT == 1) {
     int64_t blocks = 0;
-    for (int i = 0; i < n; ++i) blocks += (int64_t)z[i].nrg * z[i].S;
+    for (int i = 0; i < n; ++i)
+      if (in[i]) blocks += (int64_t)z[i].nrg * z[i].S;
     if (blocks > kGemvRound) {
       Resolved zz[SPEAR_GROUP_MAX];
       bool same = true;
       int64_t blocks4 = 0;
       for (int i = 0; i < n && same; ++i) {
+        if (!in[i]) continue;
         same = resolve(calls[i].prob, true, &zz[i], 4) == SPEAR_OK &&
                group_epi(zz[i], calls[i].ec) == epi && zz[i].RT == 4 && zz[i].S == z[i].S &&
                zz[i].ips == z[i].ips && zz[i].iw == z[i].iw && zz[i].NW == z[i].NW &&
@@ -1134,26 +1221,23 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
         blocks4 += (int64_t)zz[i].nrg * zz[i].S;
       }
       if (same && blocks4 < blocks)
-        for (int i = 0; i < n; ++i) z[i] = zz[i];
+        for (int i = 0; i < n; ++i)
+          if (in[i]) z[i] = zz[i];
     }
   }
+  // the launch's members, in array order, as GemvGroup slots
   GemvGroup g;
   std::memset(&g, 0, sizeof(g));
-  g.n = n;
   size_t lds = 0;
-  int ctr = 0;
+  int ctr = 0, k = 0;
   for (int i = 0; i < n; ++i) {
+    if (!in[i]) continue;
     const spear_layer_call_t& c = calls[i];
     // member i's data regions (offsets past the counter block) land in its
     // own slice; its row counters are placed explicitly
     char* wsi = ws ? ws + off[i] : nullptr;
-    const bool live = c.prob->M > 0 && c.prob->N > 0;
-    g.start[i + 1] = g.start[i] + (live ? z[i].nrg * z[i].S : 0);
-    if (!live) {
-      g.p[i].S = 1;
-      continue;
-    }
-    GemvParams& q = g.p[i];
+    g.start[k + 1] = g.start[k] + z[i].nrg * z[i].S;
+    GemvParams& q = g.p[k];
     q = make_gemv(c.prob, z[i], c.x, c.w, c.y, z[i].ec ? c.ec : nullptr, wsi);
     if (z[i].ec) {
       q.ec = make_ec(c.prob, z[i], c.x, c.ec, wsi);
@@ -1164,10 +1248,13 @@ spear_status_t spear_w4ec_linear_group(int32_t n, const spear_layer_call_t* call
       ctr += z[i].nrg;
     }
     lds = std::max(lds, z[i].lds_gemv);
+    ++k;
   }
-  return hip_status(z[0].wb == 3
-                        ? launch_gemv_group_w3(z[0].dt, z[0].MT, z[0].RT, epi, g, 64 * z[0].NW, lds, s)
-                        : launch_gemv_group_w4(z[0].dt, z[0].MT, z[0].RT, epi, g, 64 * z[0].NW, lds, s));
+  g.n = k;
+  const Resolved& z0 = z[first];
+  return hip_status(z0.wb == 3
+                        ? launch_gemv_group_w3(z0.dt, z0.MT, z0.RT, epi, g, 64 * z0.NW, lds, s)
+                        : launch_gemv_group_w4(z0.dt, z0.MT, z0.RT, epi, g, 64 * z0.NW, lds, s));
 }
 
 spear_status_t spear_w4_dequant(const spear_problem_t* prob, const spear_w4_t* w, void* w_out,

@@ -2516,7 +2516,10 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
 #pragma unroll
     for (int j = 0; j < FN32; ++j) acc[i][j] = f32x16{};
   // 16-K slices: the slice's six fragments, then its eight MFMAs; SW: the
-  // token operand is the swizzled activation tile (rows of 64 halves)
+  // token operand is the swizzled activation tile (rows of 64 halves). The
+  // scheduling groups keep the reads ahead: the weight fragments and the
+  // first two token fragments go out before the first MFMA, then each pair
+  // of MFMAs is followed by the next token fragment's read.
   auto mma = [&](const uint16_t* xs, const uint16_t* ws, int xr0, int wr0, int ld, int kk, bool sw) {
     u32x4 bf[FN32], af[FM32];
 #pragma unroll
@@ -2531,6 +2534,12 @@ __global__ __launch_bounds__(256 * (1 + TNB), 1) void k_gemm_ws(GemmParams a) {
     for (int i = 0; i < FM32; ++i)
 #pragma unroll
       for (int j = 0; j < FN32; ++j) acc[i][j] = mfma32<DT>(af[i], bf[j], acc[i][j]);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // 4 LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   };
   xdma(0, 0);
   __builtin_amdgcn_s_waitcnt(0);

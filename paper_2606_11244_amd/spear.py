@@ -33,7 +33,8 @@ STATUS = {0: "SPEAR_OK", -1: "SPEAR_E_NULL", -2: "SPEAR_E_SHAPE", -3: "SPEAR_E_D
 
 EXPORTED = ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
             "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
-            "spear_set_wait_polls", "spear_set_gemv_shape", "spear_set_gemm_slices",
+            "spear_group_launches", "spear_set_wait_polls", "spear_set_gemv_shape",
+            "spear_set_gemm_slices",
             "spear_set_gemm_tile", "spear_set_gemm_roles", "spear_workspace_regions",
             "spear_w4ec_linear_noalloc",
             "spear_set_gemv_stages",
@@ -124,6 +125,7 @@ def _load():
                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                            ctypes.c_void_p]
     lib.spear_group_workspace.argtypes = [ctypes.c_int32, P(LayerCall), P(ctypes.c_size_t)]
+    lib.spear_group_launches.argtypes = [ctypes.c_int32, P(LayerCall), P(ctypes.c_int32)]
     lib.spear_w4ec_linear_group.argtypes = [ctypes.c_int32, P(LayerCall), ctypes.c_void_p,
                                             ctypes.c_size_t, ctypes.c_void_p]
     lib.spear_set_wait_polls.argtypes = [ctypes.c_int32]
@@ -148,7 +150,8 @@ def _load():
     lib.spear_version.restype = ctypes.c_char_p
     for f in ("spear_dispatch_plan", "spear_w4_linear", "spear_w4ec_linear", "spear_w4_dequant",
               "spear_w4ec_linear_tail", "spear_group_workspace", "spear_w4ec_linear_group",
-              "spear_set_wait_polls", "spear_workspace_regions", "spear_w4ec_linear_noalloc"):
+              "spear_group_launches", "spear_set_wait_polls", "spear_workspace_regions",
+              "spear_w4ec_linear_noalloc"):
         getattr(lib, f).restype = ctypes.c_int32
     return lib
 
@@ -327,9 +330,19 @@ def group_workspace(members) -> int:
     return out.value
 
 
+def group_launches(members) -> int:
+    """Kernel launches a grouped call with these members makes (include/spear.h)."""
+    arr, keep = _group_array(members)
+    out = ctypes.c_int32(0)
+    st = LIB.spear_group_launches(len(members), arr, ctypes.byref(out))
+    if st != 0:
+        raise SpearError(st, "spear_group_launches")
+    return out.value
+
+
 def w4ec_linear_group(members, workspace=None, stream=None):
-    """Up to GROUP_MAX independent layer calls in one launch where they share
-    a kernel variant (include/spear.h); members as in group_workspace."""
+    """Up to GROUP_MAX independent layer calls; those of one kernel variant
+    share one launch (include/spear.h); members as in group_workspace."""
     arr, keep = _group_array(members)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = LIB.spear_w4ec_linear_group(len(members), arr, _ptr(workspace), ws_bytes,

@@ -4,7 +4,8 @@ oracle under the parity bar on sampled rows; covers the one-launch case
 (members of one GEMV variant: the 4-bit product alone or the fused local
 path, split-K members included), the one-after-another case (mixed
 variants, token counts beyond the GEMV), INT8 factors, bf16, shared inputs,
-empty members and graph replays."""
+empty members and graph replays, and groups where only some members share
+the launch."""
 from __future__ import annotations
 
 import numpy as np
@@ -120,6 +121,18 @@ def test_mixed_variants_run_in_order():
     _check([(1, "q", True), (1, "k", False), (1, "v", True)], 1, seed=13)
     _check(QKV, 48, seed=14)
     _check([(2, "q", True), (2, "k", True)], 256, seed=15)
+
+
+def test_70b_shaped_members_share_a_launch():
+    # 4-bit-only q, k, v at one token: k and v re-planned to q's row tiles in
+    # one launch; next to a q on the producer-fused EC path, k and v share
+    # the launch without it
+    from paper_2606_11244_amd import spear as sp
+    specs = [(4, "q", False), (4, "k", False), (4, "v", False)]
+    _, dls, probs = _build(specs, 1, 31)
+    assert sp.group_launches([d.member(p, with_ec=False) for d, p in zip(dls, probs)]) == 1
+    _check(specs, 1, seed=31)
+    _check([(4, "q", True), (4, "k", False), (4, "v", False)], 1, seed=33)
 
 
 def test_separate_inputs():

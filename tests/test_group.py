@@ -127,3 +127,69 @@ def test_cross_member_alias_rejected():
     assert need > 256
     arr, keep = _calls(probs, override={(2, "y"): ws + 256})
     assert sp.LIB.spear_w4ec_linear_group(3, arr, ws, need, None) == -8
+
+
+def _launches(probs, ecs):
+    """spear_group_launches with member i carrying an EC iff ecs[i]."""
+    arr, keep = _calls(probs)
+    for i, e in enumerate(ecs):
+        if not e:
+            arr[i].ec = None
+    out = ctypes.c_int32(-1)
+    st = sp.LIB.spear_group_launches(len(probs), arr, ctypes.byref(out))
+    return st, out.value
+
+
+def _own(p, ec):
+    return sp.dispatch_plan(p, ec).num_launches
+
+
+def test_group_launches_share_one_launch():
+    # 70B-shaped q, k, v and gate, up at one token, 4-bit only: one launch
+    # each (k and v re-planned to q's row tiles, which leaves their K-slices
+    # and per-wave work unchanged)
+    qkv = [sp.problem(1, 8192, 8192, 128, sp.F16, 0), sp.problem(1, 1024, 8192, 128, sp.F16, 0),
+           sp.problem(1, 1024, 8192, 128, sp.F16, 0)]
+    assert _launches(qkv, [False] * 3) == (0, 1)
+    gu = [sp.problem(1, 28672, 8192, 128, sp.F16, 0)] * 2
+    assert _launches(gu, [False] * 2) == (0, 1)
+    # 1B-shaped q, k, v with the local EC at one and 16 tokens
+    for M in (1, 16):
+        assert _launches(_qkv(M), [True] * 3) == (0, 1)
+
+
+def test_group_launches_mixed_members():
+    # an EC member on the producer-fused path runs on its own; the two
+    # 4-bit-only members share a launch
+    probs = [sp.problem(1, 8192, 8192, 128, sp.F16, 64), sp.problem(1, 1024, 8192, 128, sp.F16, 0),
+             sp.problem(1, 1024, 8192, 128, sp.F16, 0)]
+    assert sp.PATH_NAMES[sp.dispatch_plan(probs[0], True).path] == "fused_gemv"
+    st, n = _launches(probs, [True, False, False])
+    assert st == 0 and n == _own(probs[0], True) + 1
+    # local EC on q and v, k 4-bit only: the larger set (q, v) shares a
+    # launch, k runs on its own
+    probs = _qkv(1)
+    st, n = _launches(probs, [True, False, True])
+    assert st == 0 and n == 1 + _own(probs[1], False)
+    # every member on its own variant: each its own launches
+    probs = [sp.problem(1, 8192, 8192, 128, sp.F16, 64), sp.problem(1, 1024, 8192, 128, sp.F16, 0)]
+    st, n = _launches(probs, [True, False])
+    assert st == 0 and n == _own(probs[0], True) + _own(probs[1], False)
+
+
+def test_group_launches_beyond_the_gemv_and_empty_members():
+    # prefill token counts take the GEMM: every member on its own
+    probs = [sp.problem(4096, 8192, 8192, 128, sp.F16, 64), sp.problem(4096, 1024, 8192, 128, sp.F16, 0),
+             sp.problem(4096, 1024, 8192, 128, sp.F16, 0)]
+    st, n = _launches(probs, [True, False, False])
+    assert st == 0 and n == _own(probs[0], True) + 2 * _own(probs[1], False)
+    # an empty member makes no launch and does not join the shared one
+    probs = _qkv(1)
+    probs[1] = sp.problem(0, 512, 2048, 128, sp.F16, 16)
+    assert _launches(probs, [True] * 3) == (0, 1)
+    probs = [sp.problem(1, 2048, 2048, 128, sp.F16, 16), sp.problem(0, 512, 2048, 128, sp.F16, 16)]
+    st, n = _launches(probs, [True, True])
+    assert st == 0 and n == _own(probs[0], True)
+    # a NULL out pointer
+    arr, keep = _calls(_qkv(1))
+    assert sp.LIB.spear_group_launches(3, arr, None) == -1
