@@ -656,6 +656,8 @@ def main():
                     help="1B: skip the passes with the post-EC tail on o and down")
     ap.add_argument("--no-tanh", action="store_true",
                     help="1B: skip the passes with the paper's tanh-MLP gate")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the measured HBM-read and MFMA ceilings")
     ap.add_argument("--model70b", action="store_true",
                     help="also time the 70B-shaped model's pass at M = 1, 16, 64, 512, 8192")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
@@ -792,6 +794,21 @@ def main():
         print("bench: 1B-shaped passes", file=sys.stderr, flush=True)
         extras = llama1b_extras(args, sp, S, np, torch, dev)
 
+    ceil = None
+    if not args.no_ceiling:
+        # what the chip sustains, beside the published peaks: a streaming read
+        # of one 117 MB gate/up/down module's codes, and 32x32x16 fp16 MFMAs
+        # with full-entropy operands
+        from paper_2606_11244_amd import ceiling
+        print("bench: measured ceilings", file=sys.stderr, flush=True)
+        rd, _ = ceiling.read_ceiling(torch, 28672 * 8192 // 2)
+        mf, _ = ceiling.mfma_ceiling(torch, True)
+        ceil = {"hbm_read_GBps": round(rd, 1), "mfma_f16_TFLOPs": round(mf, 1),
+                "how": ("python -m paper_2606_11244_amd.ceiling: streaming read of 117 MB "
+                        "(rotated copies beyond the Infinity Cache); sustained 32x32x16 fp16 "
+                        "MFMAs with full-entropy operands")}
+        torch.cuda.empty_cache()
+
     traffic = stored_traffic()
     result = {
         "metric": METRIC,
@@ -833,6 +850,9 @@ def main():
             "algo_bytes_per_launch": round(dec_bytes / dec_launches),
             "launches_per_pass": dec_launches,
             "avg_launch_us": round(dec_s / dec_launches * 1e6, 3),
+            "measured_ceiling": None if ceil is None else {
+                "value": ceil["hbm_read_GBps"], "unit": "GB/s",
+                "frac": round(dec_gbs / ceil["hbm_read_GBps"], 4), "how": ceil["how"]},
         },
         "prefill": {
             "value": round(pre_tfl, 2), "unit": "TFLOP/s", "ms_per_pass": round(pre_s * 1e3, 4),
@@ -848,6 +868,9 @@ def main():
                 "traffic": (traffic or {}).get("prefill_bytes_per_launch"),
                 "algo_flops_per_launch": round(pre_flops / pre_launches),
                 "launches_per_pass": pre_launches,
+                "measured_ceiling": None if ceil is None else {
+                    "value": ceil["mfma_f16_TFLOPs"], "unit": "TFLOP/s",
+                    "frac": round(pre_tfl / ceil["mfma_f16_TFLOPs"], 4), "how": ceil["how"]},
             },
         },
         "decode_ms_per_pass": round(dec_s * 1e3, 4),

@@ -16,6 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libspear.so")
+CEIL = os.path.join(HERE, "libspear_ceiling.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -38,7 +39,8 @@ def _run(cmd):
 def build(verbose: bool = False) -> str:
     """Compile every HIP/C++ source of the library (in parallel processes) and
     link libspear.so. spear_kernels.hip is compiled twice: for 4-bit and for
-    3-bit weight codes (SPEAR_WB)."""
+    3-bit weight codes (SPEAR_WB). The measured-ceiling kernels go into
+    libspear_ceiling.so."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     units = (("spear_kernels.hip", "w4", [f"--offload-arch={ARCH}", "-x", "hip", "-DSPEAR_WB=4"]),
@@ -58,6 +60,11 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs)
     os.replace(tmp, LIB)
+    # the measured-ceiling kernels (measurement only), a library of their own
+    tmp = CEIL + ".tmp"
+    _run([HIPCC] + COMMON + [f"--offload-arch={ARCH}", "-x", "hip", "-shared",
+                             os.path.join(CSRC, "spear_ceiling.hip"), "-o", tmp])
+    os.replace(tmp, CEIL)
     shutil.rmtree(objdir, ignore_errors=True)
     return LIB
 

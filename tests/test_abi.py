@@ -402,3 +402,14 @@ def test_gemm_wave_roles_rules():
         sp.set_gemm_roles(0)
         sp.set_gemm_slices(0)
         sp.set_gemm_tile(0)
+
+
+def test_ceiling_library_exports():
+    # the measured-ceiling kernels (measurement only) ship as their own
+    # library; host-side argument checks reject bad sizes before any launch
+    from paper_2606_11244_amd import ceiling
+    lib = ceiling._lib()
+    assert hasattr(lib, "spear_ceiling_read") and hasattr(lib, "spear_ceiling_mfma")
+    assert lib.spear_ceiling_read(None, 1 << 20, None, None) != 0
+    assert lib.spear_ceiling_read(ctypes.c_void_p(1 << 40), 15, ctypes.c_void_p(1 << 40), None) != 0
+    assert lib.spear_ceiling_mfma(0, 1, 1, ctypes.c_void_p(1 << 40), None) != 0
