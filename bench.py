@@ -607,7 +607,7 @@ def llama1b_extras(args, sp, S, np, torch, dev):
                 "decode_ms_per_pass": round(dt_ * 1e3, 4), "prefill_ms_per_pass": round(pt_ * 1e3, 4),
                 "decode_added": round(dt_ / dec_s - 1.0, 4), "prefill_added": round(pt_ / pre_s - 1.0, 4)}
 
-    traffic = stored_traffic()
+    # (the stored counter runs cover the 70B-shaped headline workload only)
     n_launch_dec = LAYERS_1B * len(DEC_GROUPS)
     return {
         "workload": ("llama-3.2-1b-shaped W4+EC linear layers (q,k,v,o 2048->2048/512, "
@@ -619,13 +619,13 @@ def llama1b_extras(args, sp, S, np, torch, dev):
         "decode_path": sp.PATH_NAMES[dec_plan.path],
         "decode_launches": n_launch_dec,
         "decode_avg_launch_us": round(dec_s / n_launch_dec * 1e6, 3),
-        "decode_traffic_per_launch": (traffic or {}).get("decode_bytes_per_launch"),
+        "decode_traffic_per_launch": None,
         "decode_algo_bytes_per_launch": round(dec_bytes / n_launch_dec),
         "prefill_TFLOPs": round(pre_tfl, 2), "prefill_ms_per_pass": round(pre_s * 1e3, 4),
         "prefill_mfma_frac": round(pre_tfl / MFMA_F16_PEAK_TFLOPS, 4),
         "prefill_paths": {m: sp.PATH_NAMES[sp.dispatch_plan(d.problem()).path]
                           for m, d in zip(S.MODULES, pre_dev)},
-        "prefill_traffic_per_launch": (traffic or {}).get("prefill_bytes_per_launch"),
+        "prefill_traffic_per_launch": None,
         "decode_one_call_per_module": ungrouped,
         "ec_overhead": overhead,
         "ec_int8": int8,
@@ -677,7 +677,8 @@ def main():
     torch.cuda.set_device(0)
     dev = "cuda:0"
     print("bench: building the 70B-shaped model", file=sys.stderr, flush=True)
-    model = Model70B(sp, torch, dev, PRE_M)
+    # the --model70b sweep reaches 8192 tokens
+    model = Model70B(sp, torch, dev, max(PRE_M, 8192) if args.model70b else PRE_M)
     ws_dec, ws_pre = model.workspace(DEC_M), model.workspace(PRE_M)
     print("bench: capturing graphs", file=sys.stderr, flush=True)
     g_dec = model.capture(DEC_M, True, ws_dec)
