@@ -194,10 +194,12 @@ def main(argv=None):
                         f"{r['w4_gemm_us']} | {r['w4_us']} |")
     lines = ["# Dispatch crossover: W4+EC paths by token count", "",
              "Command (from the repository root): `python -m paper_2606_11244_amd.crossover "
-             f"--out {args.out}`", "",
+             "--out profiles/dispatch_crossover.md`", "",
              "Mean time per call in microseconds (graph-replayed over rotated weight copies; "
              "synthetic layers of the named configurations, seed 0). `-` = path not available "
-             "for the shape. EC overhead = fastest EC path / 4-bit-only - 1.", "",
+             "for the shape. EC overhead = fastest EC path / 4-bit-only - 1. config: the "
+             "synthetic workload's id, counted from 0 (0 tiny K = N = 256, 1 Llama-3.2-1B "
+             "decode, 2 the same layers at prefill, 3 Llama-3-8B, 4 Llama-2-70B).", "",
              "| config | module | N | K | r | M | W4 only | " + " | ".join(names) +
              " | fastest | AUTO | EC overhead |",
              "|---" * (9 + len(names) + 1) + "|"]
