@@ -119,10 +119,19 @@ int gemv_ips(int IT, int nrg, int NW, int waves = 4096, int cap_iw = 0) {
 enum { kRtW4 = 0, kRtLocal = 1, kRtOther = 2, kRtFused1 = 3 };
 constexpr int64_t kGemvRound = 256;
 constexpr int kFusedCapIw = 16;
+// The producer-fused variant at a single token on layers narrower than this
+// takes one row tile and one K-slice when each wave then has at most
+// kFusedCapIw iterations: no split-K reduction after the stream (70B k,
+// 1024 x 8192, rank 64: 12.2 us against 14.0 us on two row tiles in four
+// K-slices).
+constexpr int64_t kFusedNarrowN = 4096;
 int gemv_rt(int MT, int kind, int64_t N, int IT, int NW, int rt_force, int waves) {
   if (g_ov_rt.load() > 0) return g_ov_rt.load();
   if (rt_force > 0) return rt_force;
   if (MT == 1 && kind == kRtFused1) {
+    // (narrow layers: one row tile, over all of K when that keeps each wave
+    // within the iteration cap, see kFusedNarrowN)
+    if (N < kFusedNarrowN && IT <= NW * kFusedCapIw) return 1;
     const int nrg = (int)cdiv(N, 16);
     const int S = (int)cdiv(IT, gemv_ips(IT, nrg, NW, waves, kFusedCapIw));
     return N >= 4096 && (int64_t)nrg * S <= kGemvRound ? 1 : 2;
@@ -285,7 +294,10 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     }
     if (g_ov_nw.load() > 0) z.NW = std::max(1, std::min(max_nw, (int)g_ov_nw.load()));
     z.nrg = (int)cdiv(N, 16 * z.RT);
-    z.ips = gemv_ips(z.IT, z.nrg, z.NW, waves, fused1 ? kFusedCapIw : 0);
+    z.ips = fused1 && N < kFusedNarrowN && z.RT == 1 && z.IT <= z.NW * kFusedCapIw &&
+                    g_ov_s.load() == 0
+                ? z.IT
+                : gemv_ips(z.IT, z.nrg, z.NW, waves, fused1 ? kFusedCapIw : 0);
     z.S = (int)cdiv(z.IT, z.ips);
     z.iw = (int)cdiv(z.ips, z.NW);
     z.nst = 2;

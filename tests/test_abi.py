@@ -276,7 +276,8 @@ def test_decode_launch_shape_rules():
     """The measured launch-shape rules at a single token: the fewest row
     tiles whose grid fits one round of 256 blocks, no second K-slice on the
     70B-shaped 8192-row modules, and the producer-fused variant on one row
-    tile for layers of 4096+ rows."""
+    tile for layers of 4096+ rows that fit one round, and on one row tile and
+    one K-slice for narrower layers."""
     # 1B q: one row tile (16 rows), one K-slice, 128 blocks
     p = _plan(M=1)
     assert (p.tile_n, p.split_k, p.grid) == (16, 1, 128)
@@ -292,6 +293,13 @@ def test_decode_launch_shape_rules():
     # at 16 tokens the earlier shapes stay (1B down: two row tiles, four slices)
     p = _plan(M=16, N=2048, K=8192, rank=0, with_ec=False)
     assert (p.tile_n, p.split_k) == (32, 4)
+    # 70B k, rank 64: the fused GEMV on one row tile over all of K (64
+    # iterations, ten per wave), 64 consumer workgroups after the producers
+    p = _plan(M=1, N=1024, K=8192, rank=64)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (16, 1)
+    # 70B gate, rank 64: wide, so two row tiles as before
+    p = _plan(M=1, N=28672, K=8192, rank=64)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (32, 1)
 
 
 def test_prefill_tile_rule():
