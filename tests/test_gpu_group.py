@@ -187,6 +187,40 @@ def test_graph_replay(M):
             assert torch.equal(got[j].view(torch.int16), d.y.view(torch.int16)), (i, j)
 
 
+def test_graph_replay_partly_shared_launch():
+    """A group where two members share the launch and one runs on its own
+    (a 4-bit-only k between local-EC q and v), captured and replayed with new
+    activations between replays: every replay equals the eager call."""
+    from paper_2606_11244_amd import spear as sp
+    specs = [(1, "q", True), (1, "k", False), (1, "v", True)]
+    Ls, dls, probs = _build(specs, 1, 41)
+    members = [d.member(p, with_ec=p.rank > 0) for d, p in zip(dls, probs)]
+    assert sp.group_launches(members) == 2
+    ws = torch.zeros(max(256, sp.group_workspace(members)), dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        sp.w4ec_linear_group(members, ws, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sp.w4ec_linear_group(members, ws)
+    gen = torch.Generator(device="cuda").manual_seed(43)
+    x = dls[0].x
+    for i in range(3):
+        x.copy_(torch.randn(x.shape, generator=gen, device="cuda").to(x.dtype))
+        torch.cuda.synchronize()
+        log(f"partly shared group graph replay={i}")
+        g.replay()
+        torch.cuda.synchronize()
+        got = [d.y.clone() for d in dls]
+        sp.w4ec_linear_group(members, ws)
+        torch.cuda.synchronize()
+        for j, d in enumerate(dls):
+            assert torch.equal(got[j].view(torch.int16), d.y.view(torch.int16)), (i, j)
+
+
 def test_workspace_shared_with_single_calls():
     """One workspace serves groups and single calls in stream order: groups
     whose members run one after another on the producer/consumer path (rank
