@@ -269,13 +269,26 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
                                                                     : kRtOther;
     // one token: the 4-bit product alone, the producer-fused and the
     // semi-fused GEMV aim at 2048 waves (70B down, semi-fused: 38.8 us in one
-    // K-slice against 40.7 us in two)
-    const int waves = M == 1 && (rt_kind == kRtW4 || rt_kind == kRtOther) || fused1 ? 2048 : 4096;
+    // K-slice against 40.7 us in two). Two to sixteen tokens (one token
+    // tile) on layers of 4096 rows or more: the 4-bit product alone and the
+    // producer-fused GEMV aim at 2048 waves too, and from eight tokens on,
+    // layers too wide for one round of two-row-tile blocks take four row
+    // tiles, since every row group's blocks read the whole token tile of x
+    // (70B shapes at 16 tokens, 4-bit only: q 26.4 -> 19.9 us, gate 68.9 ->
+    // 46.1, down 61.1 -> 52.5; fused: q 32.9 -> 26.0, gate 70.7 -> 57.5,
+    // down 72.0 -> 61.9). The 2048-row 1B down module keeps its split in
+    // four at 16 tokens, measured faster.
+    const bool tile1 = z.MT == 1 && M > 1 && N >= 4096 &&
+                       (rt_kind == kRtW4 || (fused && rt_kind == kRtOther));
+    const bool wide1 = tile1 && M >= 8 && rt_force == 0 && g_ov_rt.load() == 0 &&
+                       cdiv(N, 32) > kGemvRound;
+    const int waves =
+        (M == 1 && (rt_kind == kRtW4 || rt_kind == kRtOther)) || fused1 || tile1 ? 2048 : 4096;
     {
       // the fused variant's GEMV waves: one wave of the block is the EC wave
       const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load()))
                                         : fused1 ? kGemvMaxThreads / 64 - 1 : 8;
-      z.RT = gemv_rt(z.MT, rt_kind, N, z.IT, nw, rt_force, waves);
+      z.RT = wide1 ? 4 : gemv_rt(z.MT, rt_kind, N, z.IT, nw, rt_force, waves);
     }
     if (!gemv_shape_supported(z.MT, z.RT)) return SPEAR_E_UNSUPPORTED;
     // the EC variants add the EC wave to the workgroup
@@ -292,6 +305,9 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
       const int nrg = (int)cdiv(N, 16 * z.RT);
       if ((int64_t)nrg * cdiv(z.IT, gemv_ips(z.IT, nrg, z.NW, waves)) > kGemvRound) z.NW = 4;
     }
+    // and on the four-row-tile blocks of eight to sixteen tokens (70B gate at
+    // 16 tokens: 46.1 us against 55.0 with eight waves)
+    if (wide1 && rt_kind == kRtW4) z.NW = 4;
     if (g_ov_nw.load() > 0) z.NW = std::max(1, std::min(max_nw, (int)g_ov_nw.load()));
     z.nrg = (int)cdiv(N, 16 * z.RT);
     z.ips = fused1 && N < kFusedNarrowN && z.RT == 1 && z.IT <= z.NW * kFusedCapIw &&

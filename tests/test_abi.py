@@ -293,6 +293,21 @@ def test_decode_launch_shape_rules():
     # at 16 tokens the earlier shapes stay (1B down: two row tiles, four slices)
     p = _plan(M=16, N=2048, K=8192, rank=0, with_ec=False)
     assert (p.tile_n, p.split_k) == (32, 4)
+    # 70B-shaped layers at 16 and 8 tokens: 2048 waves (no second K-slice on
+    # q), gate four row tiles of four-wave blocks, the fused gate four row
+    # tiles; at 4 tokens gate keeps two row tiles
+    p = _plan(M=16, N=8192, K=8192, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k, p.grid) == (32, 1, 256)
+    p = _plan(M=16, N=28672, K=8192, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k, p.grid) == (64, 1, 448)
+    p = _plan(M=8, N=28672, K=8192, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k) == (64, 1)
+    p = _plan(M=4, N=28672, K=8192, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k) == (32, 1)
+    p = _plan(M=16, N=28672, K=8192, rank=64)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (64, 1)
+    p = _plan(M=16, N=8192, K=8192, rank=64)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (32, 1)
     # 70B k, rank 64: the fused GEMV on one row tile over all of K (64
     # iterations, ten per wave), 64 consumer workgroups after the producers
     p = _plan(M=1, N=1024, K=8192, rank=64)
