@@ -269,16 +269,18 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
                                                                     : kRtOther;
     // one token: the 4-bit product alone, the producer-fused and the
     // semi-fused GEMV aim at 2048 waves (70B down, semi-fused: 38.8 us in one
-    // K-slice against 40.7 us in two). Two to sixteen tokens (one token
-    // tile) on layers of 4096 rows or more: the 4-bit product alone and the
-    // producer-fused GEMV aim at 2048 waves too, and from eight tokens on,
-    // layers too wide for one round of two-row-tile blocks take four row
-    // tiles, since every row group's blocks read the whole token tile of x
-    // (70B shapes at 16 tokens, 4-bit only: q 26.4 -> 19.9 us, gate 68.9 ->
-    // 46.1, down 61.1 -> 52.5; fused: q 32.9 -> 26.0, gate 70.7 -> 57.5,
-    // down 72.0 -> 61.9). The 2048-row 1B down module keeps its split in
-    // four at 16 tokens, measured faster.
-    const bool tile1 = z.MT == 1 && M > 1 && N >= 4096 &&
+    // K-slice against 40.7 us in two). Four to sixteen tokens (one token
+    // tile) on layers of at least 8192 rows and 8192 K: the 4-bit product
+    // alone and the producer-fused GEMV aim at 2048 waves too, and from
+    // eight tokens on, layers too wide for one round of two-row-tile blocks
+    // take four row tiles, since every row group's blocks read the whole
+    // token tile of x (70B shapes at 16 tokens, 4-bit only: q 26.4 -> 19.9
+    // us, gate 68.9 -> 46.1, down 61.1 -> 52.5; fused: q 32.9 -> 26.0, gate
+    // 70.7 -> 57.5, down 72.0 -> 61.9). Measured worse and left alone: two
+    // tokens on 70B down (one K-slice no longer stages x in LDS: 38.6 against
+    // 32.6 us) and the 8B shapes at eight tokens (gate 15.9 against 13.2,
+    // down 18.3 against 16.0).
+    const bool tile1 = z.MT == 1 && M >= 4 && N >= 8192 && K >= 8192 &&
                        (rt_kind == kRtW4 || (fused && rt_kind == kRtOther));
     const bool wide1 = tile1 && M >= 8 && rt_force == 0 && g_ov_rt.load() == 0 &&
                        cdiv(N, 32) > kGemvRound;
