@@ -218,10 +218,16 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
   // grows with the tokens (1B gate at 32 tokens: 21.3 us against 28.3 us;
   // 8B q at 8 tokens: 17.7 against 20.9; deeper layers keep the fused GEMV).
   const bool deep1 = (M == 1 && K >= 16384) || (M > 1 && K <= 4096);
+  // a single token on narrow layers at least 8192 deep: the producer-fused
+  // GEMV on one row tile over all of K beats the local variant, whose
+  // workgroups each restage A for their K-slice (1B down, 2048 x 8192,
+  // rank 16: 11.2 us against 13.3 us)
+  const bool narrow_deep1 = M == 1 && N < kFusedNarrowN && K >= 8192 &&
+                            K / kIterK <= (kGemvMaxThreads / 64 - 1) * kFusedCapIw;
   if (path == SPEAR_PATH_AUTO || !z.ec)
     path = M > kAutoGemvMaxM ? (mfma_ok && few_tiles && !big_tiles ? SPEAR_PATH_FUSED_MFMA
                                                                    : SPEAR_PATH_UNFUSED_2K)
-           : local_ok        ? SPEAR_PATH_FUSED_LOCAL
+           : local_ok && !narrow_deep1 ? SPEAR_PATH_FUSED_LOCAL
            : deep1           ? SPEAR_PATH_UNFUSED_2K
                              : SPEAR_PATH_FUSED_GEMV;
   if (!with_ec) {

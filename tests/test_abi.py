@@ -308,6 +308,12 @@ def test_decode_launch_shape_rules():
     assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (64, 1)
     p = _plan(M=16, N=8192, K=8192, rank=64)
     assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (32, 1)
+    # 1B down (2048 x 8192, rank 16) at one token: the producer-fused GEMV
+    # on one row tile over all of K, not the local variant; at two tokens
+    # the local variant
+    p = _plan(M=1, N=2048, K=8192, rank=16)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (16, 1)
+    assert _plan(M=2, N=2048, K=8192, rank=16).path == sp.PATH_FUSED_LOCAL
     # 70B k, rank 64: the fused GEMV on one row tile over all of K (64
     # iterations, ten per wave), 64 consumer workgroups after the producers
     p = _plan(M=1, N=1024, K=8192, rank=64)

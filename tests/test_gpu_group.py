@@ -97,9 +97,10 @@ def test_gate_up_one_launch(M):
 
 
 def test_split_k_members():
-    # the 8192-deep module splits K at decode: each member's partials and
-    # counters sit in its own slice of the group workspace
-    _check([(1, "down", True), (1, "down", True), (1, "down", True)], 1, seed=5)
+    # the 8192-deep module splits K at decode (the local variant at two
+    # tokens): each member's partials and counters sit in its own slice of
+    # the group workspace
+    _check([(1, "down", True), (1, "down", True), (1, "down", True)], 2, seed=5)
 
 
 def test_four_members_w4_only():
@@ -234,8 +235,10 @@ def test_workspace_shared_with_single_calls():
 
     wide = [dev(S.make_layer(M=1, N=8192, K=2048, group_size=128, rank=32, seed=40 + i))
             for i in range(2)]
-    deep = [dev(S.config_layer(1, "down", 1, seed=42 + i)) for i in range(2)]
-    single = [dev(S.config_layer(1, "down", 1, seed=44)),
+    # (the 8192-deep 1B down module at two tokens: the local variant split
+    # over K; at one token it takes the producer-fused GEMV)
+    deep = [dev(S.config_layer(1, "down", 2, seed=42 + i)) for i in range(2)]
+    single = [dev(S.config_layer(1, "down", 2, seed=44)),
               dev(S.make_layer(M=1, N=2048, K=2048, group_size=128, rank=32, seed=45))]
     paths = {n: sp.PATH_NAMES[sp.dispatch_plan(d.problem()).path]
              for n, d in (("wide", wide[0]), ("deep", deep[0]), ("s0", single[0]),
