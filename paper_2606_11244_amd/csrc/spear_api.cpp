@@ -292,11 +292,24 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
                        cdiv(N, 32) > kGemvRound;
     const int waves =
         (M == 1 && (rt_kind == kRtW4 || rt_kind == kRtOther)) || fused1 || tile1 ? 2048 : 4096;
+    // 17 to 32 tokens (two token tiles) on the same layers: four row tiles
+    // (two for the 4-bit product alone on layers that fit one round of
+    // two-row-tile blocks, K < 16384), K split in two from K = 16384 on and
+    // unsplit below, and four-wave blocks for the 4-bit product alone (70B
+    // shapes at 32 tokens, 4-bit only: q 42.3 -> 27.3 us, gate 112.2 ->
+    // 64.4, down 96.8 -> 61.1; fused: q 56.7 -> 40.1, gate 120.1 -> 79.7,
+    // down 126.7 -> 92.2)
+    const bool tile2 = z.MT == 2 && N >= 8192 && K >= 8192 && rt_force == 0 &&
+                       g_ov_rt.load() == 0 && g_ov_s.load() == 0 && g_ov_nw.load() == 0 &&
+                       (rt_kind == kRtW4 || (fused && rt_kind == kRtOther));
+    const int s_tile2 = K >= 16384 ? 2 : 1;
     {
       // the fused variant's GEMV waves: one wave of the block is the EC wave
       const int nw = g_ov_nw.load() > 0 ? std::max(1, std::min(8, (int)g_ov_nw.load()))
                                         : fused1 ? kGemvMaxThreads / 64 - 1 : 8;
-      z.RT = wide1 ? 4 : gemv_rt(z.MT, rt_kind, N, z.IT, nw, rt_force, waves);
+      z.RT = tile2 ? (fused || cdiv(N, 32) > kGemvRound || K >= 16384 ? 4 : 2)
+             : wide1 ? 4
+                     : gemv_rt(z.MT, rt_kind, N, z.IT, nw, rt_force, waves);
     }
     if (!gemv_shape_supported(z.MT, z.RT)) return SPEAR_E_UNSUPPORTED;
     // the EC variants add the EC wave to the workgroup
@@ -314,11 +327,13 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
       if ((int64_t)nrg * cdiv(z.IT, gemv_ips(z.IT, nrg, z.NW, waves)) > kGemvRound) z.NW = 4;
     }
     // and on the four-row-tile blocks of eight to sixteen tokens (70B gate at
-    // 16 tokens: 46.1 us against 55.0 with eight waves)
-    if (wide1 && rt_kind == kRtW4) z.NW = 4;
+    // 16 tokens: 46.1 us against 55.0 with eight waves), and at 17 to 32
+    // tokens on the layers above
+    if ((wide1 || tile2) && rt_kind == kRtW4) z.NW = 4;
     if (g_ov_nw.load() > 0) z.NW = std::max(1, std::min(max_nw, (int)g_ov_nw.load()));
     z.nrg = (int)cdiv(N, 16 * z.RT);
-    z.ips = fused1 && N < kFusedNarrowN && z.RT == 1 && z.IT <= z.NW * kFusedCapIw &&
+    z.ips = tile2 ? (int)cdiv(z.IT, s_tile2)
+            : fused1 && N < kFusedNarrowN && z.RT == 1 && z.IT <= z.NW * kFusedCapIw &&
                     g_ov_s.load() == 0
                 ? z.IT
                 : gemv_ips(z.IT, z.nrg, z.NW, waves, fused1 ? kFusedCapIw : 0);

@@ -314,6 +314,18 @@ def test_decode_launch_shape_rules():
     p = _plan(M=1, N=2048, K=8192, rank=16)
     assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (16, 1)
     assert _plan(M=2, N=2048, K=8192, rank=16).path == sp.PATH_FUSED_LOCAL
+    # two token tiles (32 tokens) on the 70B-shaped layers: four row tiles
+    # (two for the 4-bit product on q), K split in two from K = 16384 on
+    p = _plan(M=32, N=8192, K=8192, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k, p.grid) == (32, 1, 256)
+    p = _plan(M=32, N=28672, K=8192, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k) == (64, 1)
+    p = _plan(M=32, N=8192, K=28672, rank=0, with_ec=False)
+    assert (p.tile_n, p.split_k) == (64, 2)
+    p = _plan(M=32, N=8192, K=8192, rank=64)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (64, 1)
+    p = _plan(M=32, N=8192, K=28672, rank=64)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (64, 2)
     # 70B k, rank 64: the fused GEMV on one row tile over all of K (64
     # iterations, ten per wave), 64 consumer workgroups after the producers
     p = _plan(M=1, N=1024, K=8192, rank=64)

@@ -151,6 +151,27 @@ def _check_decode_w4(cid, module):
             assert_parity(dev.run(d, p, False), ref16[:M], f"{NAME[cid]}/{module}/M={M}/w4/{p}")
 
 
+@pytest.mark.parametrize("module", ["q", "gate", "down"])
+def test_decode_two_token_tiles_full_outputs(module):
+    """32 tokens (two token tiles) on the 70B-shaped modules, whose launch
+    shapes there (four row tiles, K split in two from K = 16384) are their
+    own: complete outputs of the 4-bit product alone and of the W4+EC call
+    (the producer-fused GEMV) against the oracle, the EC also isolated."""
+    base = _layer(4, module, 32)
+    for ec_only in (False, True):
+        B = _ec_only(base) if ec_only else base
+        dev = _Dev(B)
+        d = dev.with_x(B)
+        ref = oracle_full(B)
+        log(f"full-size decode 32 tokens llama70b {module} ec_only={ec_only}")
+        assert_parity(dev.run(d, P_AUTO, True), ref, f"llama70b/{module}/M=32/auto/ec_only={ec_only}")
+        assert_parity(dev.run(d, P_GEMV, True), ref, f"llama70b/{module}/M=32/gemv/ec_only={ec_only}")
+        if not ec_only:
+            W4 = with_fields(B, rank=0)
+            ref4 = oracle_full(W4)
+            assert_parity(dev.run(d, P_AUTO, False), ref4, f"llama70b/{module}/M=32/w4")
+
+
 def _tile_tokens(M):
     """One token of every 16-token tile, at a different offset in each."""
     t = np.arange((M + 15) // 16)
