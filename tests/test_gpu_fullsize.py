@@ -172,6 +172,19 @@ def test_decode_two_token_tiles_full_outputs(module):
             assert_parity(dev.run(d, P_AUTO, False), ref4, f"llama70b/{module}/M=32/w4")
 
 
+def test_decode_two_token_tiles_int8_factors():
+    """INT8 EC factors on the four-row-tile fused GEMV at 32 tokens (70B q),
+    complete outputs against the oracle."""
+    base = S.config_layer(4, "q", 32, seed=0, ab_int8=True)
+    for ec_only in (False, True):
+        B = _ec_only(base) if ec_only else base
+        dev = _Dev(B)
+        d = dev.with_x(B)
+        ref = oracle_full(B)
+        log(f"full-size decode 32 tokens llama70b q int8 ec_only={ec_only}")
+        assert_parity(dev.run(d, P_AUTO, True), ref, f"llama70b/q/M=32/int8/ec_only={ec_only}")
+
+
 def _tile_tokens(M):
     """One token of every 16-token tile, at a different offset in each."""
     t = np.arange((M + 15) // 16)
