@@ -290,7 +290,7 @@ def replay_times(torch, graph, n):
     return [a.elapsed_time(b) * 1e-3 for a, b in ev]
 
 
-def model_70b_sweep(model, Ms=(1, 16, 32, 64, 512, 8192), reps=3):
+def model_70b_sweep(model, Ms=(1, 4, 8, 16, 32, 64, 512, 8192), reps=3):
     """Further token counts of the 70B-shaped model's pass (the sweep of its
     workload), each with its EC overhead."""
     import numpy as np
@@ -659,7 +659,7 @@ def main():
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the measured HBM-read and MFMA ceilings")
     ap.add_argument("--model70b", action="store_true",
-                    help="also time the 70B-shaped model's pass at M = 1, 16, 32, 64, 512, 8192")
+                    help="also time the 70B-shaped model's pass at M = 1, 4, 8, 16, 32, 64, 512, 8192")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()

@@ -288,8 +288,11 @@ spear_status_t resolve(const spear_problem_t* p, bool with_ec, Resolved* R, int 
     // down 18.3 against 16.0).
     const bool tile1 = z.MT == 1 && M >= 4 && N >= 8192 && K >= 8192 &&
                        (rt_kind == kRtW4 || (fused && rt_kind == kRtOther));
-    const bool wide1 = tile1 && M >= 8 && rt_force == 0 && g_ov_rt.load() == 0 &&
-                       cdiv(N, 32) > kGemvRound;
+    // (the producer-fused GEMV from four tokens on: 70B gate at 4 tokens
+    // 70.9 -> 48.8 us; the 4-bit product alone keeps two row tiles there,
+    // 36.0 against 39.7 us)
+    const bool wide1 = tile1 && (M >= 8 || (fused && M >= 4)) && rt_force == 0 &&
+                       g_ov_rt.load() == 0 && cdiv(N, 32) > kGemvRound;
     const int waves =
         (M == 1 && (rt_kind == kRtW4 || rt_kind == kRtOther)) || fused1 || tile1 ? 2048 : 4096;
     // 17 to 32 tokens (two token tiles) on the same layers: four row tiles

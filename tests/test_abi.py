@@ -304,6 +304,9 @@ def test_decode_launch_shape_rules():
     assert (p.tile_n, p.split_k) == (64, 1)
     p = _plan(M=4, N=28672, K=8192, rank=0, with_ec=False)
     assert (p.tile_n, p.split_k) == (32, 1)
+    # the fused gate takes four row tiles from four tokens on
+    p = _plan(M=4, N=28672, K=8192, rank=64)
+    assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (64, 1)
     p = _plan(M=16, N=28672, K=8192, rank=64)
     assert p.path == sp.PATH_FUSED_GEMV and (p.tile_n, p.split_k) == (64, 1)
     p = _plan(M=16, N=8192, K=8192, rank=64)
